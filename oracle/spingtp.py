@@ -1,0 +1,170 @@
+"""The SpinGTP bilinear map as an explicit sparse real tensor.
+
+Test infrastructure only (see ``oracle/__init__.py``).
+
+For one unit (edge n, channel c) with real-basis inputs x1 (degree <= L1) and
+x2 (degree <= L2), both carrying the spins of ``spins``:
+
+1. a_i = Q x_i                                  (App. C, a_complex = Q a_real)
+2. c[s3,l3,m3] = sum_{s1+s2=s3} sum G^{(l3,m3,s3)}_{(l1,m1,s1)(l2,m2,s2)} a1[s1,l1,m1] a2[s2,l2,m2]
+   for s3 in ``spins`` and l3 <= Lout        (Sec. 3.2 eq. generalized_gaunt;
+                                              App. B proof: coefficient of the
+                                              pointwise product of the two
+                                              spin-weighted functions)
+3. y = Re(Q^dagger c)                           (App. C, a_real = Re(Q^dagger a_complex))
+
+This is y[k3] = sum_{k1,k2} T[k1,k2,k3] x1[k1] x2[k2] with
+T = Re(conj(Q3) G Q1 Q2), built once per (L1, L2, Lout, spins, basis).
+
+Readings where the paper is silent:
+* output spins: every pair (s1, s2) of ``spins`` contributes to s3 = s1 + s2,
+  pairs with equal s3 are summed with no normalisation, and s3 outside
+  ``spins`` (e.g. +-2 for spins (-1,0,1)) is dropped;
+* output degrees: l3 <= Lout only;
+* slots with l < |s| are ignored on input and zero on output;
+* unit path weights (W = 1) and the elementwise channel mode (App. E.1 "uuu"):
+  x1 and x2 of the same (edge, channel) are multiplied.
+"""
+
+import functools
+
+import numpy as np
+import scipy.sparse as sp
+
+from .gaunt import gauss_legendre_grid, gaunt_block
+from .realbasis import BASIS_PAPER, q_matrix, real_index
+
+_PRUNE = 1e-13
+
+
+def _row_lists(Q):
+    """Nonzero (column, value) pairs of each row of Q, padded to 2 per row."""
+    n = Q.shape[0]
+    cols = np.zeros((n, 2), dtype=np.int64)
+    vals = np.zeros((n, 2), dtype=np.complex128)
+    for r in range(n):
+        nz = np.nonzero(Q[r])[0]
+        if len(nz) > 2:
+            raise AssertionError("Q row with more than two entries")
+        cols[r, :len(nz)] = nz
+        vals[r, :len(nz)] = Q[r, nz]
+    return cols, vals
+
+
+class RealGauntTensor:
+    """Sparse real tensor T[k1, k2, k3] of the SpinGTP map (see module docstring)."""
+
+    def __init__(self, L1, L2, Lout, spins, basis=BASIS_PAPER, skip_triangle=True):
+        spins = tuple(int(s) for s in spins)
+        self.L1, self.L2, self.Lout, self.spins, self.basis = L1, L2, Lout, spins, basis
+        self.n1 = len(spins) * (L1 + 1) ** 2
+        self.n2 = len(spins) * (L2 + 1) ** 2
+        self.n3 = len(spins) * (Lout + 1) ** 2
+        theta, w_t, phi, w_p = gauss_legendre_grid(L1 + L2 + Lout)
+
+        # Step 2: complex Gaunt entries (a, b, e, g) over complex slot indices.
+        A, B, E, Gv = [], [], [], []
+        for s1 in spins:
+            for s2 in spins:
+                s3 = s1 + s2
+                if s3 not in spins:
+                    continue
+                for l1 in range(abs(s1), L1 + 1):
+                    for l2 in range(abs(s2), L2 + 1):
+                        for l3 in range(abs(s3), Lout + 1):
+                            if skip_triangle and not (abs(l1 - l2) <= l3 <= l1 + l2):
+                                continue
+                            G = gaunt_block(l1, s1, l2, s2, l3, s3, theta, w_t, phi, w_p)
+                            ia, ib = np.nonzero(G)
+                            if len(ia) == 0:
+                                continue
+                            m1 = ia - l1
+                            m2 = ib - l2
+                            m3 = m1 + m2
+                            A.append(real_index(spins, L1, s1, l1, 0) + m1)
+                            B.append(real_index(spins, L2, s2, l2, 0) + m2)
+                            E.append(real_index(spins, Lout, s3, l3, 0) + m3)
+                            Gv.append(G[ia, ib])
+        A = np.concatenate(A) if A else np.zeros(0, np.int64)
+        B = np.concatenate(B) if B else np.zeros(0, np.int64)
+        E = np.concatenate(E) if E else np.zeros(0, np.int64)
+        Gv = np.concatenate(Gv) if Gv else np.zeros(0, np.complex128)
+        self.n_gaunt = len(Gv)
+        self._complex = (A, B, E, Gv)
+
+        # Steps 1 and 3 folded in: T = Re(conj(Q3[e,k3]) G[a,b,e] Q1[a,k1] Q2[b,k2]).
+        c1, v1 = _row_lists(q_matrix(spins, L1, basis))
+        c2, v2 = _row_lists(q_matrix(spins, L2, basis))
+        c3, v3 = _row_lists(q_matrix(spins, Lout, basis))
+        K1, K2, K3, V = [], [], [], []
+        for i in range(2):
+            for j in range(2):
+                for l in range(2):
+                    val = (v1[A, i] * v2[B, j] * Gv * np.conj(v3[E, l])).real
+                    keep = val != 0.0
+                    K1.append(c1[A, i][keep])
+                    K2.append(c2[B, j][keep])
+                    K3.append(c3[E, l][keep])
+                    V.append(val[keep])
+        K1, K2, K3, V = map(np.concatenate, (K1, K2, K3, V))
+        rows = K1 * self.n2 + K2
+        M = sp.coo_matrix((V, (rows, K3)), shape=(self.n1 * self.n2, self.n3)).tocsr()
+        M.sum_duplicates()
+        M.data[np.abs(M.data) <= _PRUNE] = 0.0
+        M.eliminate_zeros()
+        self.matrix = M  # rows (k1, k2) flattened, columns k3
+
+    def apply_complex(self, a1, a2) -> np.ndarray:
+        """Step 2 alone on complex coefficients: c[u,e] = sum G[a,b,e] a1[u,a] a2[u,b]."""
+        A, B, E, Gv = self._complex
+        a1 = np.asarray(a1, dtype=np.complex128).reshape(-1, self.n1)
+        a2 = np.asarray(a2, dtype=np.complex128).reshape(-1, self.n2)
+        c = np.zeros((a1.shape[0], self.n3), dtype=np.complex128)
+        for u in range(a1.shape[0]):
+            np.add.at(c[u], E, Gv * a1[u, A] * a2[u, B])
+        return c
+
+    @property
+    def nnz(self) -> int:
+        return self.matrix.nnz
+
+    def dense(self) -> np.ndarray:
+        """T as a dense [n1, n2, n3] array (small L only)."""
+        return self.matrix.toarray().reshape(self.n1, self.n2, self.n3)
+
+    def apply(self, x1, x2, chunk=None) -> np.ndarray:
+        """y[u, k3] = sum T[k1,k2,k3] x1[u,k1] x2[u,k2] in float64.
+
+        x1: [..., n1] (or [..., n_spins, (L1+1)^2]); x2 likewise; returns
+        [..., n_spins, (Lout+1)^2].
+        """
+        x1 = np.asarray(x1, dtype=np.float64)
+        x2 = np.asarray(x2, dtype=np.float64)
+        ns = len(self.spins)
+        if x1.ndim >= 2 and x1.shape[-2:] == (ns, (self.L1 + 1) ** 2):
+            lead = x1.shape[:-2]
+        else:
+            lead = x1.shape[:-1]
+        X1 = x1.reshape(-1, self.n1)
+        X2 = x2.reshape(-1, self.n2)
+        if X1.shape[0] != X2.shape[0]:
+            raise ValueError("x1 and x2 hold different numbers of units")
+        U = X1.shape[0]
+        if chunk is None:
+            chunk = max(1, min(U, (1 << 24) // max(1, self.n1 * self.n2)))
+        Y = np.empty((U, self.n3))
+        for u0 in range(0, U, chunk):
+            u1 = min(U, u0 + chunk)
+            P = (X1[u0:u1, :, None] * X2[u0:u1, None, :]).reshape(u1 - u0, -1)
+            Y[u0:u1] = np.asarray(P @ self.matrix)
+        return Y.reshape(lead + (len(self.spins), (self.Lout + 1) ** 2))
+
+
+@functools.lru_cache(maxsize=16)
+def _cached_tensor(L1, L2, Lout, spins, basis):
+    return RealGauntTensor(L1, L2, Lout, spins, basis)
+
+
+def spingtp(x1, x2, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER) -> np.ndarray:
+    """Oracle value of the SpinGTP forward for a batch of units (float64)."""
+    return _cached_tensor(L1, L2, Lout, tuple(spins), basis).apply(x1, x2)
