@@ -1,0 +1,127 @@
+/*
+ * spingtp.h -- C ABI of the spin-weighted Gaunt tensor product (SpinGTP) on
+ * AMD MI355X (gfx950).
+ *
+ * The operation (paper Sec. 3.2 eq. generalized_gaunt, Sec. 3.3 eq. real_swsh,
+ * App. B proof of the runtime proposition, App. C):
+ *
+ *   For every unit (edge n, channel c) independently, with real-basis spin-weighted
+ *   spherical-harmonic (SWSH) coefficients x1 (degree <= L1) and x2 (degree <= L2),
+ *   both carrying the spins listed in `spins`:
+ *     a_i   = Q x_i                                (real -> complex, App. C)
+ *     f_i,s = sum_{l,m} a_i[s,l,m] sY_lm           (spin-weighted fields on S^2)
+ *     h_s3  = sum_{s1+s2=s3} f_1,s1 * f_2,s2       (pointwise product, s3 in spins)
+ *     c[s3,l3,m3] = int h_s3 conj(s3Y_l3m3) dOmega (l3 <= Lout)
+ *     out   = Re(Q^dagger c)                       (complex -> real, App. C)
+ *   i.e. out[k3] = sum G x1 x2 with G the spin-weighted Gaunt coefficients.
+ *   Spin pairs with the same s3 are summed with no normalisation; products with
+ *   s3 outside `spins` (e.g. s3 = +-2 for spins {-1,0,+1}) are dropped.  This is the
+ *   elementwise channel mode ("uuu", App. E.1) with unit path weights.
+ *
+ * Layout of x1, x2, out (all dense, row-major, same dtype):
+ *   x1  [N][C][n_spins][(L1+1)^2],  x2 [N][C][n_spins][(L2+1)^2],
+ *   out [N][C][n_spins][(Lout+1)^2].
+ *   The spin axis holds the real-basis sector spins[i] (spins strictly ascending,
+ *   the -|s| sector first as in App. C).  Inside a spin block the flat index is
+ *   l^2 + l + k with k = -l..l ascending.  Slots with l < |s| are ignored on input
+ *   and written as 0 on output.
+ *
+ * Real basis at m = 0 for |s| > 0 (the paper's eq. real_swsh sets sR_l0 = sY_l0):
+ *   SPINGTP_BASIS_REAL_PAPER      that definition literally (default);
+ *   SPINGTP_BASIS_REAL_M0_PAIRED  the m = 0 pair (s,0),(-s,0) mixed as
+ *                                 (1/sqrt2)(1, (-1)^s) and (i/sqrt2)(1, -(-1)^s),
+ *                                 which makes the real basis closed under rotation.
+ *
+ * Threading and ownership: a plan is immutable after creation; concurrent
+ * spingtp_forward calls with one plan on different streams or threads are safe.
+ * The caller owns x1, x2 and out.  No call keeps global error state.
+ */
+#ifndef SPINGTP_H
+#define SPINGTP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct spingtp_plan_s* spingtp_plan; /* opaque */
+
+typedef enum {
+    SPINGTP_OK = 0,
+    SPINGTP_ERR_INVALID_ARG = 1,   /* bad degree, spin list, pointer, alignment or size */
+    SPINGTP_ERR_UNSUPPORTED = 2,   /* valid by the paper but not built in this library */
+    SPINGTP_ERR_OUT_OF_MEMORY = 3, /* device allocation failed */
+    SPINGTP_ERR_HIP = 4,           /* a HIP runtime call or kernel launch failed */
+    SPINGTP_ERR_INTERNAL = 5       /* plan self-check failed (a library bug) */
+} spingtp_status;
+
+typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
+
+#define SPINGTP_BASIS_REAL_PAPER 0u
+#define SPINGTP_BASIS_REAL_M0_PAIRED 1u
+
+/*
+ * Create a plan for degrees (L1, L2, Lout) and a spin set.
+ *   0 <= L1, L2 <= 16, 0 <= Lout <= L1 + L2 (the product of degrees l1, l2 has
+ *   degree <= l1 + l2, App. B proof); otherwise SPINGTP_ERR_INVALID_ARG.
+ *   spins/n_spins: host array, strictly ascending and symmetric; {0} and
+ *   {-1, 0, +1} are supported, other valid sets give SPINGTP_ERR_UNSUPPORTED.
+ *   dtype: element type of x1, x2 and out.  bf16 plans compute in fp32 and round
+ *   the output to bf16 (round to nearest even).
+ *   flags: one SPINGTP_BASIS_* value.
+ * The plan tables (Gauss-Legendre weights and SWSH values on the quadrature
+ * nodes, trigonometric tables, real-basis mixing constants) are computed in
+ * float64 on the host, rounded to fp32 and copied synchronously to the current
+ * HIP device, which the plan is bound to.  *out_plan receives the handle; on any
+ * error it is set to NULL and nothing is leaked.
+ */
+spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                   spingtp_dtype dtype, unsigned flags, spingtp_plan* out_plan);
+
+/*
+ * out = SpinGTP(x1, x2) for N*C units, asynchronously on `stream` (a hipStream_t;
+ * NULL = the null stream of the plan's device).
+ *   x1, x2, out: device pointers of the plan's dtype in the layout above, each
+ *   16-byte aligned; out must not overlap x1 or x2 (undefined otherwise).
+ *   N, C >= 0; N*C == 0 is a no-op that returns SPINGTP_OK without touching
+ *   memory.  Null pointers (when N*C > 0), misalignment or negative sizes give
+ *   SPINGTP_ERR_INVALID_ARG before anything is launched.
+ * out is overwritten (not accumulated).  No allocation and no host
+ * synchronisation.  A launch failure gives SPINGTP_ERR_HIP.
+ */
+spingtp_status spingtp_forward(spingtp_plan plan, const void* x1, const void* x2, void* out,
+                               int64_t N, int64_t C, void* stream);
+
+/* Free the plan's device tables.  The caller must ensure that no forward using
+ * the plan is still running.  NULL is accepted (no-op). */
+spingtp_status spingtp_plan_destroy(spingtp_plan plan);
+
+/* Static English description of a status code. */
+const char* spingtp_status_string(spingtp_status s);
+
+/*
+ * Host-only inspection of the plan tables in float64, before rounding.  Needs no
+ * GPU.  Same argument rules as spingtp_plan_create.  Writes at most `capacity`
+ * doubles to `tables` (may be NULL when capacity is 0) and the full count to
+ * *n_tables; `dims` (may be NULL) receives 8 ints:
+ *   {n_theta, n_phi, L1, L2, Lout, n_spins, per_theta_block, global_block}.
+ * The table layout is the one documented in csrc/layout.h of the library source.
+ */
+spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                        unsigned flags, double* tables, size_t capacity,
+                                        size_t* n_tables, int* dims);
+
+/*
+ * Describe the kernel a plan launches: writes the waves per workgroup, units per
+ * workgroup, LDS bytes per workgroup and a kernel-family id (1 = register-tiled
+ * fixed-degree kernel) to the 4 ints of `info`.
+ */
+spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPINGTP_H */

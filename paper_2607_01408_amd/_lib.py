@@ -1,0 +1,57 @@
+"""ctypes loader for the in-tree ``libspingtp.so``.  Fails loudly when it is missing."""
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspingtp.so")
+
+SPINGTP_OK = 0
+STATUS_NAMES = {0: "OK", 1: "ERR_INVALID_ARG", 2: "ERR_UNSUPPORTED", 3: "ERR_OUT_OF_MEMORY",
+                4: "ERR_HIP", 5: "ERR_INTERNAL"}
+EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "spingtp_status_string",
+            "spingtp_plan_tables_host", "spingtp_plan_kernel_info")
+
+_lib = None
+
+
+class SpinGTPError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)} ({message(status)})")
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                               "(or python paper_2607_01408_amd/build.py)")
+        L = ctypes.CDLL(LIB_PATH)
+        c_int_p = ctypes.POINTER(ctypes.c_int)
+        L.spingtp_plan_create.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, c_int_p, ctypes.c_int,
+                                          ctypes.c_int, ctypes.c_uint, ctypes.POINTER(ctypes.c_void_p)]
+        L.spingtp_plan_create.restype = ctypes.c_int
+        L.spingtp_forward.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        L.spingtp_forward.restype = ctypes.c_int
+        L.spingtp_plan_destroy.argtypes = [ctypes.c_void_p]
+        L.spingtp_plan_destroy.restype = ctypes.c_int
+        L.spingtp_status_string.argtypes = [ctypes.c_int]
+        L.spingtp_status_string.restype = ctypes.c_char_p
+        L.spingtp_plan_tables_host.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, c_int_p, ctypes.c_int,
+                                               ctypes.c_uint, ctypes.POINTER(ctypes.c_double), ctypes.c_size_t,
+                                               ctypes.POINTER(ctypes.c_size_t), c_int_p]
+        L.spingtp_plan_tables_host.restype = ctypes.c_int
+        L.spingtp_plan_kernel_info.argtypes = [ctypes.c_void_p, c_int_p]
+        L.spingtp_plan_kernel_info.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def message(status: int) -> str:
+    return lib().spingtp_status_string(int(status)).decode()
+
+
+def check(status: int, where: str) -> None:
+    if status != SPINGTP_OK:
+        raise SpinGTPError(status, where)

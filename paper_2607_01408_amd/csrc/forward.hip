@@ -1,0 +1,467 @@
+// Fused SpinGTP forward kernel for gfx950 (CDNA4) and its launch entry point.
+//
+// Method (paper App. B proof of the runtime proposition; Sec. 3.2 eq.
+// generalized_gaunt): each output coefficient is the projection of the
+// pointwise product of the two input fields, so a unit is
+//   (A) coefficients -> theta-Fourier form of the fields at a Gauss-Legendre node
+//   (B) synthesis of the fields at the n_phi uniform phi nodes
+//   (C) spin-pair products  h_s3 = sum_{s1+s2=s3} f1_s1 f2_s2
+//   (D) analysis of the products onto cos/sin(t phi)
+//   (E) projection onto the output coefficients with the node's weight,
+// summed over the n_theta nodes.  The grid is exact (layout.h), so the result
+// equals the Gaunt contraction up to fp32 rounding.
+//
+// Work mapping.  A workgroup owns 64 units (one per lane) and one wave per
+// theta node, so every table value a wave reads is the same for its 64 lanes
+// and comes from the scalar cache; the per-unit data lives in VGPRs.  The two
+// input tiles are staged through LDS with coalesced 16-byte loads; the partial
+// outputs of the theta-node waves are summed in LDS with ds_add_f32 and written
+// back with coalesced 16-byte stores.  Fields, products and spectra never leave
+// the CU.
+//
+// Spin structure for spins {-1, 0, +1} (real basis, eq. real_swsh / App. C):
+// for t = |m| >= 1 the field of spin -1 is the complex conjugate of the field of
+// spin +1, so each input carries three real trigonometric polynomials per node:
+//   A = f_0,   B~ = sqrt2 (Re f+ + Re f-)/2,   C~ = sqrt2 (Im f+ - Im f-)/2,
+// plus two m = 0 constants delta = Re(f- - conj f+), eps = Im(f- - conj f+).
+// The only output combinations the real projection needs are
+//   R0 = Re h_0 = A a + B~ b~ + C~ c~ - (d1 d2 + e1 e2)/2,
+//   P1 = Re h+ + Re h- = sqrt2 (A b~ + a B~),   P2 = Im h+ - Im h- = sqrt2 (A c~ + a C~),
+// and, at m3 = 0 only, Re h+ - Re h- and Im h+ + Im h-, which follow from the
+// t = 0 coefficients and delta, eps in closed form.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "internal.h"
+
+namespace spingtp {
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);  // quiet NaN
+    u += 0x7fffu + ((u >> 16) & 1u);                                                     // nearest even
+    return static_cast<uint16_t>(u >> 16);
+}
+
+template <int NC, int ST>
+__device__ __forceinline__ void put(float* dst, int e, float v) {
+    const int u = e / NC;
+    dst[u * ST + (e - u * NC)] = v;
+}
+
+// Global tile (contiguous nvalid * NC elements, 256-byte aligned) -> LDS rows of stride ST.
+template <int NC, int ST>
+__device__ __forceinline__ void load_tile(const float* __restrict__ src, int nvalid, float* dst, int tid, int nthr) {
+    const int n = nvalid * NC;
+    const int n4 = n >> 2;
+    const v4f* s4 = reinterpret_cast<const v4f*>(src);
+    for (int i = tid; i < n4; i += nthr) {
+        const v4f v = __builtin_nontemporal_load(s4 + i);
+        const int e = 4 * i;
+        put<NC, ST>(dst, e, v.x);
+        put<NC, ST>(dst, e + 1, v.y);
+        put<NC, ST>(dst, e + 2, v.z);
+        put<NC, ST>(dst, e + 3, v.w);
+    }
+    for (int e = 4 * n4 + tid; e < n; e += nthr) put<NC, ST>(dst, e, src[e]);
+}
+
+template <int NC, int ST>
+__device__ __forceinline__ void load_tile(const uint16_t* __restrict__ src, int nvalid, float* dst, int tid, int nthr) {
+    const int n = nvalid * NC;
+    const int n8 = n >> 3;
+    const v4u* s8 = reinterpret_cast<const v4u*>(src);
+    for (int i = tid; i < n8; i += nthr) {
+        const v4u v = __builtin_nontemporal_load(s8 + i);
+        const int e = 8 * i;
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            put<NC, ST>(dst, e + 2 * q, __uint_as_float(w[q] << 16));
+            put<NC, ST>(dst, e + 2 * q + 1, __uint_as_float(w[q] & 0xffff0000u));
+        }
+    }
+    for (int e = 8 * n8 + tid; e < n; e += nthr) put<NC, ST>(dst, e, bf16_to_f32(src[e]));
+}
+
+template <int NC, int ST>
+__device__ __forceinline__ float get(const float* src, int e) {
+    const int u = e / NC;
+    return src[u * ST + (e - u * NC)];
+}
+
+template <int NC, int ST>
+__device__ __forceinline__ void store_tile(float* __restrict__ dst, int nvalid, const float* src, int tid, int nthr) {
+    const int n = nvalid * NC;
+    const int n4 = n >> 2;
+    v4f* d4 = reinterpret_cast<v4f*>(dst);
+    for (int i = tid; i < n4; i += nthr) {
+        const int e = 4 * i;
+        v4f v;
+        v.x = get<NC, ST>(src, e);
+        v.y = get<NC, ST>(src, e + 1);
+        v.z = get<NC, ST>(src, e + 2);
+        v.w = get<NC, ST>(src, e + 3);
+        __builtin_nontemporal_store(v, d4 + i);
+    }
+    for (int e = 4 * n4 + tid; e < n; e += nthr) dst[e] = get<NC, ST>(src, e);
+}
+
+template <int NC, int ST>
+__device__ __forceinline__ void store_tile(uint16_t* __restrict__ dst, int nvalid, const float* src, int tid, int nthr) {
+    const int n = nvalid * NC;
+    const int n8 = n >> 3;
+    v4u* d8 = reinterpret_cast<v4u*>(dst);
+    for (int i = tid; i < n8; i += nthr) {
+        const int e = 8 * i;
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            w[q] = static_cast<uint32_t>(f32_to_bf16(get<NC, ST>(src, e + 2 * q))) |
+                   (static_cast<uint32_t>(f32_to_bf16(get<NC, ST>(src, e + 2 * q + 1))) << 16);
+        const v4u v = {w[0], w[1], w[2], w[3]};
+        __builtin_nontemporal_store(v, d8 + i);
+    }
+    for (int e = 8 * n8 + tid; e < n; e += nthr) dst[e] = f32_to_bf16(get<NC, ST>(src, e));
+}
+
+// Step (A) for one input of degree L at one theta node.
+//   xr  : this lane's LDS row ([n_spins][(L+1)^2], spin order -1, 0, +1)
+//   tb  : the node's table block; n0: the global N0 mixing.
+template <int L, int LA, bool SPIN>
+__device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const float* __restrict__ tb,
+                                                      const float* __restrict__ n0, float (&Ac)[L + 1],
+                                                      float (&As)[L + 1], float (&Bc)[L + 1], float (&Bs)[L + 1],
+                                                      float (&Cc)[L + 1], float (&Cs)[L + 1], float& dl, float& ep) {
+    constexpr Layout Y = make_layout(LA, 0, 0);  // only the per-node A offsets are used
+    constexpr int B = (L + 1) * (L + 1);
+    const float* x0 = xr + (SPIN ? B : 0);
+#pragma unroll
+    for (int t = 0; t <= L; ++t) {
+        float sc = 0.f, ss = 0.f;
+#pragma unroll
+        for (int l = t; l <= L; ++l) {
+            sc = fmaf(x0[l * l + l + t], tb[Y.a0c + tri(LA, t, l)], sc);
+            if (t > 0) ss = fmaf(x0[l * l + l - t], tb[Y.a0s + tri(LA, t, l)], ss);
+        }
+        Ac[t] = sc;
+        As[t] = ss;
+    }
+    if constexpr (SPIN) {
+        const float* xm = xr;
+        const float* xp = xr + 2 * B;
+#pragma unroll
+        for (int t = 1; t <= L; ++t) {
+            float up = 0.f, vp = 0.f, um = 0.f, vm = 0.f;
+#pragma unroll
+            for (int l = t; l <= L; ++l) {
+                const float wp = tb[Y.aup + tri(LA, t, l)];
+                const float wm = tb[Y.aum + tri(LA, t, l)];
+                up = fmaf(xp[l * l + l + t], wp, up);
+                vp = fmaf(xp[l * l + l - t], wp, vp);
+                um = fmaf(xm[l * l + l + t], wm, um);
+                vm = fmaf(xm[l * l + l - t], wm, vm);
+            }
+            Bc[t] = up + um;
+            Bs[t] = -(vp + vm);
+            Cc[t] = vp - vm;
+            Cs[t] = up - um;
+        }
+        float wpl = 0.f, wmi = 0.f;
+#pragma unroll
+        for (int l = 1; l <= L; ++l) {
+            const float w = tb[Y.aw + l];
+            wpl = fmaf(xp[l * l + l], w, wpl);
+            wmi = fmaf(xm[l * l + l], w, wmi);
+        }
+        Bc[0] = fmaf(n0[0], wpl, n0[1] * wmi);
+        Cc[0] = fmaf(n0[2], wpl, n0[3] * wmi);
+        dl = fmaf(n0[4], wpl, n0[5] * wmi);
+        ep = fmaf(n0[6], wpl, n0[7] * wmi);
+        Bs[0] = 0.f;
+        Cs[0] = 0.f;
+    } else {
+        dl = ep = 0.f;
+    }
+}
+
+template <int L>
+__device__ __forceinline__ void synth(const float (&pc)[L + 1], const float (&ps)[L + 1], const float* __restrict__ cs,
+                                      const float* __restrict__ sn, float& plus, float& minus) {
+    float ev = pc[0], od = 0.f;
+#pragma unroll
+    for (int t = 1; t <= L; ++t) {
+        ev = fmaf(pc[t], cs[t], ev);
+        od = fmaf(ps[t], sn[t], od);
+    }
+    plus = ev + od;
+    minus = ev - od;
+}
+
+template <int L1, int L2, int LO, bool SPIN>
+struct Shape {
+    static constexpr Layout Y = make_layout(L1, L2, LO);
+    static constexpr int NS = SPIN ? 3 : 1;
+    static constexpr int NC1 = NS * (L1 + 1) * (L1 + 1);
+    static constexpr int NC2 = NS * (L2 + 1) * (L2 + 1);
+    static constexpr int NCO = NS * (LO + 1) * (LO + 1);
+    static constexpr int ST1 = NC1 | 1;  // odd strides: conflict-free ds_read_b32 across lanes
+    static constexpr int ST2 = NC2 | 1;
+    static constexpr int STO = NCO | 1;
+    static constexpr int NT = Y.NT;
+    static constexpr int NP = Y.NP;
+    static constexpr int KP = (NP - 1) / 2;
+    static constexpr int WAVES = NT;
+    static constexpr int THREADS = 64 * WAVES;
+    static constexpr int LDS_FLOATS = 64 * (ST1 + ST2 + STO);
+};
+
+template <int L1, int L2, int LO, bool SPIN, typename TIO>
+__global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fwd_kernel(
+    const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units,
+    const float* __restrict__ tab) {
+    using S = Shape<L1, L2, LO, SPIN>;
+    constexpr Layout Y = S::Y;
+    constexpr int LA = Y.LA;
+    constexpr int TM1 = Y.TM + 1;
+    __shared__ float lds[S::LDS_FLOATS];
+    float* X1 = lds;
+    float* X2 = X1 + 64 * S::ST1;
+    float* YT = X2 + 64 * S::ST2;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int node = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t u0 = static_cast<int64_t>(blockIdx.x) * 64;
+    const int nvalid = static_cast<int>(units - u0 < 64 ? units - u0 : 64);
+
+    for (int i = tid; i < 64 * S::STO; i += S::THREADS) YT[i] = 0.f;
+    load_tile<S::NC1, S::ST1>(x1 + u0 * S::NC1, nvalid, X1, tid, S::THREADS);
+    load_tile<S::NC2, S::ST2>(x2 + u0 * S::NC2, nvalid, X2, tid, S::THREADS);
+    __syncthreads();
+
+    const float* __restrict__ g = tab;
+    const float* __restrict__ tb = tab + Y.glob + node * Y.pb;
+
+    // (A) both inputs at this node
+    float Ac[L1 + 1], As[L1 + 1], Bc[L1 + 1], Bs[L1 + 1], Cc[L1 + 1], Cs[L1 + 1], d1, e1;
+    float ac[L2 + 1], as[L2 + 1], bc[L2 + 1], bs[L2 + 1], cc[L2 + 1], cs2[L2 + 1], d2, e2;
+    coef_to_theta_fourier<L1, LA, SPIN>(X1 + lane * S::ST1, tb, g + Y.n0, Ac, As, Bc, Bs, Cc, Cs, d1, e1);
+    coef_to_theta_fourier<L2, LA, SPIN>(X2 + lane * S::ST2, tb, g + Y.n0, ac, as, bc, bs, cc, cs2, d2, e2);
+
+    // (B)-(D) over the phi nodes, k and n_phi - k together
+    float R0c[LO + 1], R0s[LO + 1], P1c[LO + 1], P1s[LO + 1], P2c[LO + 1], P2s[LO + 1];
+#pragma unroll
+    for (int t = 0; t <= LO; ++t) R0c[t] = R0s[t] = P1c[t] = P1s[t] = P2c[t] = P2s[t] = 0.f;
+    {
+        float A = 0.f, B = 0.f, C = 0.f, a = 0.f, b = 0.f, c = 0.f;
+#pragma unroll
+        for (int t = 0; t <= L1; ++t) {
+            A += Ac[t];
+            if constexpr (SPIN) B += Bc[t], C += Cc[t];
+        }
+#pragma unroll
+        for (int t = 0; t <= L2; ++t) {
+            a += ac[t];
+            if constexpr (SPIN) b += bc[t], c += cc[t];
+        }
+        float r0 = A * a, p1 = 0.f, p2 = 0.f;
+        if constexpr (SPIN) {
+            r0 = fmaf(B, b, fmaf(C, c, r0));
+            p1 = fmaf(A, b, a * B);
+            p2 = fmaf(A, c, a * C);
+        }
+#pragma unroll
+        for (int t = 0; t <= LO; ++t) {
+            R0c[t] += r0;
+            if constexpr (SPIN) P1c[t] += p1, P2c[t] += p2;
+        }
+    }
+#pragma unroll
+    for (int k = 1; k <= S::KP; ++k) {
+        const float* __restrict__ cs = g + Y.cosT + k * TM1;
+        const float* __restrict__ sn = g + Y.sinT + k * TM1;
+        float Ap, Am, ap, am;
+        synth<L1>(Ac, As, cs, sn, Ap, Am);
+        synth<L2>(ac, as, cs, sn, ap, am);
+        float r0p = Ap * ap, r0m = Am * am, p1p = 0.f, p1m = 0.f, p2p = 0.f, p2m = 0.f;
+        if constexpr (SPIN) {
+            float Bp, Bm, Cp, Cm, bp, bm, cp, cm;
+            synth<L1>(Bc, Bs, cs, sn, Bp, Bm);
+            synth<L1>(Cc, Cs, cs, sn, Cp, Cm);
+            synth<L2>(bc, bs, cs, sn, bp, bm);
+            synth<L2>(cc, cs2, cs, sn, cp, cm);
+            r0p = fmaf(Bp, bp, fmaf(Cp, cp, r0p));
+            r0m = fmaf(Bm, bm, fmaf(Cm, cm, r0m));
+            p1p = fmaf(Ap, bp, ap * Bp);
+            p1m = fmaf(Am, bm, am * Bm);
+            p2p = fmaf(Ap, cp, ap * Cp);
+            p2m = fmaf(Am, cm, am * Cm);
+        }
+        const float sr = r0p + r0m, dr = r0p - r0m;
+        R0c[0] += sr;
+#pragma unroll
+        for (int t = 1; t <= LO; ++t) {
+            R0c[t] = fmaf(sr, cs[t], R0c[t]);
+            R0s[t] = fmaf(dr, sn[t], R0s[t]);
+        }
+        if constexpr (SPIN) {
+            const float s1 = p1p + p1m, q1 = p1p - p1m, s2 = p2p + p2m, q2 = p2p - p2m;
+            P1c[0] += s1;
+            P2c[0] += s2;
+#pragma unroll
+            for (int t = 1; t <= LO; ++t) {
+                P1c[t] = fmaf(s1, cs[t], P1c[t]);
+                P1s[t] = fmaf(q1, sn[t], P1s[t]);
+                P2c[t] = fmaf(s2, cs[t], P2c[t]);
+                P2s[t] = fmaf(q2, sn[t], P2s[t]);
+            }
+        }
+    }
+    if constexpr (S::NP % 2 == 0) {  // phi = pi: cos(t pi) = (-1)^t, sin = 0
+        float A = 0.f, B = 0.f, C = 0.f, a = 0.f, b = 0.f, c = 0.f;
+#pragma unroll
+        for (int t = 0; t <= L1; ++t) {
+            const float sg = (t & 1) ? -1.f : 1.f;
+            A = fmaf(sg, Ac[t], A);
+            if constexpr (SPIN) B = fmaf(sg, Bc[t], B), C = fmaf(sg, Cc[t], C);
+        }
+#pragma unroll
+        for (int t = 0; t <= L2; ++t) {
+            const float sg = (t & 1) ? -1.f : 1.f;
+            a = fmaf(sg, ac[t], a);
+            if constexpr (SPIN) b = fmaf(sg, bc[t], b), c = fmaf(sg, cc[t], c);
+        }
+        float r0 = A * a, p1 = 0.f, p2 = 0.f;
+        if constexpr (SPIN) {
+            r0 = fmaf(B, b, fmaf(C, c, r0));
+            p1 = fmaf(A, b, a * B);
+            p2 = fmaf(A, c, a * C);
+        }
+#pragma unroll
+        for (int t = 0; t <= LO; ++t) {
+            const float sg = (t & 1) ? -1.f : 1.f;
+            R0c[t] = fmaf(sg, r0, R0c[t]);
+            if constexpr (SPIN) P1c[t] = fmaf(sg, p1, P1c[t]), P2c[t] = fmaf(sg, p2, P2c[t]);
+        }
+    }
+
+    // (E) projection onto output coefficients; partial sums of all nodes meet in LDS
+    constexpr int BO = (LO + 1) * (LO + 1);
+    float* yr = YT + lane * S::STO;
+    float* y0 = yr + (SPIN ? BO : 0);
+    if constexpr (SPIN) R0c[0] = fmaf(-0.5f * S::NP, fmaf(d1, d2, e1 * e2), R0c[0]);
+#pragma unroll
+    for (int t = 0; t <= LO; ++t) {
+#pragma unroll
+        for (int l = t; l <= LO; ++l) {
+            atomicAdd(&y0[l * l + l + t], tb[Y.e0c + tri(LO, t, l)] * R0c[t]);
+            if (t > 0) atomicAdd(&y0[l * l + l - t], tb[Y.e0s + tri(LO, t, l)] * R0s[t]);
+        }
+    }
+    if constexpr (SPIN) {
+        float* ym = yr;
+        float* yp = yr + 2 * BO;
+#pragma unroll
+        for (int t = 1; t <= LO; ++t) {
+            const float zpc = P1c[t] + P2s[t], zmc = P1c[t] - P2s[t];
+            const float zps = P2c[t] - P1s[t], zms = -P2c[t] - P1s[t];
+#pragma unroll
+            for (int l = t; l <= LO; ++l) {
+                const float wp = tb[Y.e1p + tri(LO, t, l)];
+                const float wm = tb[Y.e1m + tri(LO, t, l)];
+                atomicAdd(&yp[l * l + l + t], wp * zpc);
+                atomicAdd(&ym[l * l + l + t], wm * zmc);
+                atomicAdd(&yp[l * l + l - t], wp * zps);
+                atomicAdd(&ym[l * l + l - t], wm * zms);
+            }
+        }
+        if constexpr (LO >= 1) {
+            // m3 = 0, |s3| = 1: sums over phi of Re/Im h+ and h-
+            const float sP1 = 1.41421356237309505f * P1c[0];
+            const float sP2 = 1.41421356237309505f * P2c[0];
+            const float sP4 = -static_cast<float>(S::NP) * fmaf(d2, Ac[0], d1 * ac[0]);
+            const float sP3 = static_cast<float>(S::NP) * fmaf(e2, Ac[0], e1 * ac[0]);
+            const float v0 = 0.5f * (sP1 + sP4), v1 = 0.5f * (sP3 + sP2);
+            const float v2 = 0.5f * (sP1 - sP4), v3 = 0.5f * (sP3 - sP2);
+            const float* m0 = g + Y.m0;
+            const float zp = fmaf(m0[0], v0, fmaf(m0[1], v1, fmaf(m0[2], v2, m0[3] * v3)));
+            const float zm = fmaf(m0[4], v0, fmaf(m0[5], v1, fmaf(m0[6], v2, m0[7] * v3)));
+#pragma unroll
+            for (int l = 1; l <= LO; ++l) {
+                const float w = tb[Y.e1z + l];
+                atomicAdd(&yp[l * l + l], w * zp);
+                atomicAdd(&ym[l * l + l], w * zm);
+            }
+        }
+    }
+    __syncthreads();
+    store_tile<S::NCO, S::STO>(out + u0 * S::NCO, nvalid, YT, tid, S::THREADS);
+}
+
+template <int L1, int L2, int LO, bool SPIN, typename TIO>
+hipError_t launch(const void* x1, const void* x2, void* out, int64_t units, const float* tab, hipStream_t stream) {
+    using S = Shape<L1, L2, LO, SPIN>;
+    const int64_t blocks = (units + 63) / 64;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((spingtp_fwd_kernel<L1, L2, LO, SPIN, TIO>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(S::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
+                       static_cast<TIO*>(out), units, tab);
+    return hipGetLastError();
+}
+
+struct Registered {
+    int L1, L2, LO, spin, dtype;
+    KernelEntry entry;
+};
+
+template <int L1, int L2, int LO, bool SPIN, typename TIO>
+constexpr Registered reg() {
+    using S = Shape<L1, L2, LO, SPIN>;
+    return Registered{L1, L2, LO, SPIN ? 1 : 0, sizeof(TIO) == 4 ? 0 : 1,
+                      KernelEntry{S::WAVES, 64, static_cast<int>(S::LDS_FLOATS * sizeof(float)), 1,
+                                  &launch<L1, L2, LO, SPIN, TIO>}};
+}
+
+#define SPINGTP_REG(L1, L2, LO, SPIN) reg<L1, L2, LO, SPIN, float>(), reg<L1, L2, LO, SPIN, uint16_t>()
+
+const Registered kRegistry[] = {
+    SPINGTP_REG(0, 0, 0, false), SPINGTP_REG(1, 1, 1, false), SPINGTP_REG(2, 2, 2, false),
+    SPINGTP_REG(3, 3, 3, false), SPINGTP_REG(4, 4, 4, false), SPINGTP_REG(6, 6, 6, false),
+    SPINGTP_REG(1, 1, 1, true),  SPINGTP_REG(2, 2, 2, true),  SPINGTP_REG(3, 3, 3, true),
+    SPINGTP_REG(4, 4, 4, true),  SPINGTP_REG(5, 5, 5, true),  SPINGTP_REG(6, 6, 6, true),
+    SPINGTP_REG(1, 3, 3, true),  SPINGTP_REG(2, 1, 3, true),
+};
+
+}  // namespace
+
+const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype) {
+    for (const Registered& r : kRegistry)
+        if (r.L1 == L1 && r.L2 == L2 && r.LO == LO && r.spin == spin_mode && r.dtype == dtype) return &r.entry;
+    return nullptr;
+}
+
+}  // namespace spingtp
+
+extern "C" spingtp_status spingtp_forward(spingtp_plan plan, const void* x1, const void* x2, void* out, int64_t N,
+                                          int64_t C, void* stream) {
+    if (plan == nullptr || N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
+    if (N == 0 || C == 0) return SPINGTP_OK;
+    if (N > (int64_t{1} << 40) / C) return SPINGTP_ERR_INVALID_ARG;
+    if (x1 == nullptr || x2 == nullptr || out == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    const auto misaligned = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; };
+    if (misaligned(x1) || misaligned(x2) || misaligned(out)) return SPINGTP_ERR_INVALID_ARG;
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
+    if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
+    const hipError_t e =
+        plan->kernel->launch(x1, x2, out, N * C, plan->d_tab, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
+}

@@ -1,0 +1,343 @@
+// Host side of the SpinGTP library: argument checks, float64 plan tables, plan
+// lifetime and the C ABI entry points other than the forward launch.
+//
+// The tables hold everything the forward kernel needs to evaluate the two input
+// fields on the exact quadrature grid (layout.h), multiply them spin pair by spin
+// pair, and project the products back (paper App. B proof: a path is two inverse
+// transforms, a pointwise product and one forward transform).  The spin-weighted
+// harmonics come from the explicit Goldberg sum (paper App. A.1), the real-basis
+// maps from eq. real_swsh and App. C.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "internal.h"
+
+namespace spingtp {
+namespace {
+
+constexpr double kPi = 3.14159265358979323846264338327950288;
+constexpr double kSqrt2 = 1.41421356237309504880168872420969808;
+
+double factorial(int n) {
+    double f = 1.0;
+    for (int i = 2; i <= n; ++i) f *= i;
+    return f;
+}
+
+double binom(int n, int k) {
+    if (k < 0 || k > n) return 0.0;
+    double b = 1.0;
+    for (int i = 1; i <= k; ++i) b = b * (n - k + i) / i;
+    return std::round(b);
+}
+
+// sY_lm(theta, 0) from the Goldberg sum (App. A.1) in half-angle form,
+// sin^{2l}(theta/2) cot^k(theta/2) = sin^{2l-k} cos^k, k = 2r + s - m, with the
+// prefactor (-1)^{m+l-s} sqrt((l+m)!(l-m)!(2l+1) / (4 pi (l+s)!(l-s)!)) that
+// reproduces the closed forms of 1Y10 and 1Y1(+-1) printed there.
+double swsh_theta(int s, int l, int m, double theta) {
+    if (std::abs(s) > l || std::abs(m) > l) return 0.0;
+    const double c = std::cos(0.5 * theta), sn = std::sin(0.5 * theta);
+    double sum = 0.0;
+    for (int r = 0; r <= l - s; ++r) {
+        const int j = r + s - m;
+        if (j < 0 || j > l + s) continue;
+        const int k = 2 * r + s - m;
+        const double coef = ((r & 1) ? -1.0 : 1.0) * binom(l - s, r) * binom(l + s, j);
+        sum += coef * std::pow(sn, 2 * l - k) * std::pow(c, k);
+    }
+    const double mag = std::sqrt((2 * l + 1) / (4.0 * kPi) * (factorial(l + m) * factorial(l - m)) /
+                                 (factorial(l + s) * factorial(l - s)));
+    const double sign = (((m + l - s) % 2) != 0) ? -1.0 : 1.0;
+    return sign * mag * sum;
+}
+
+// Gauss-Legendre rule on [-1, 1] by Newton iteration on P_n (three-term
+// recurrence), the classical method of e.g. Numerical Recipes "gauleg".
+void gauss_legendre(int n, std::vector<double>& x, std::vector<double>& w) {
+    x.assign(n, 0.0);
+    w.assign(n, 0.0);
+    for (int i = 0; i < n; ++i) {
+        double z = std::cos(kPi * (i + 0.75) / (n + 0.5));
+        double dp = 1.0;
+        for (int it = 0; it < 100; ++it) {
+            double p0 = 1.0, p1 = z;
+            for (int k = 2; k <= n; ++k) {
+                const double p2 = ((2.0 * k - 1.0) * z * p1 - (k - 1.0) * p0) / k;
+                p0 = p1;
+                p1 = p2;
+            }
+            if (n == 1) p0 = 1.0, p1 = z;
+            dp = n * (z * p1 - p0) / (z * z - 1.0);
+            const double dz = p1 / dp;
+            z -= dz;
+            if (std::fabs(dz) < 1e-16) break;
+        }
+        double p0 = 1.0, p1 = z;
+        for (int k = 2; k <= n; ++k) {
+            const double p2 = ((2.0 * k - 1.0) * z * p1 - (k - 1.0) * p0) / k;
+            p0 = p1;
+            p1 = p2;
+        }
+        dp = n * (z * p1 - p0) / (z * z - 1.0);
+        x[i] = z;
+        w[i] = 2.0 / ((1.0 - z * z) * dp * dp);
+    }
+}
+
+// Complex entry Q[(s, 0), (sigma, 0)] of the real->complex map for |s| = 1 at
+// m = 0 (App. C; eq. real_swsh sets sR_l0 = sY_l0, the paired reading mixes the
+// two m = 0 slots).
+struct Cplx {
+    double re, im;
+};
+Cplx q_m0(unsigned flags, int s, int sigma) {
+    const double h = 1.0 / kSqrt2;
+    if (flags == SPINGTP_BASIS_REAL_PAPER) return (s == sigma) ? Cplx{1.0, 0.0} : Cplx{0.0, 0.0};
+    // paired, |s| = 1: column (+1,0) -> (h, -h) on rows (+1,0), (-1,0);
+    //                   column (-1,0) -> (i h, i h)
+    if (sigma > 0) return (s > 0) ? Cplx{h, 0.0} : Cplx{-h, 0.0};
+    return Cplx{0.0, h};
+}
+
+}  // namespace
+
+bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::vector<double>& out) {
+    const Layout Y = make_layout(L1, L2, LO);
+    out.assign(Y.total, 0.0);
+    const double sq2 = kSqrt2;
+
+    if (spin_mode == 1) {
+        // Input, t = 0, |s| = 1: with W_sigma = sum_l x[sigma,l,0] Theta_{1,l,0} and
+        // Theta_{-1,l,0} = -Theta_{1,l,0}, the m = 0 part of field f_s is
+        // s * sum_sigma Q[(s,0),(sigma,0)] W_sigma.  The kernel keeps
+        // B~c0 = sqrt2 (Re f+ + Re f-)/2, C~c0 = sqrt2 (Im f+ - Im f-)/2,
+        // delta = Re f- - Re f+, eps = Im f- + Im f+.
+        for (int col = 0; col < 2; ++col) {
+            const int sigma = col == 0 ? 1 : -1;
+            const Cplx qp = q_m0(flags, 1, sigma), qm = q_m0(flags, -1, sigma);
+            const double Rp = qp.re, Ip = qp.im, Rm = -qm.re, Im_ = -qm.im;
+            out[Y.n0 + 0 * 2 + col] = sq2 * (Rp + Rm) / 2.0;
+            out[Y.n0 + 1 * 2 + col] = sq2 * (Ip - Im_) / 2.0;
+            out[Y.n0 + 2 * 2 + col] = Rm - Rp;
+            out[Y.n0 + 3 * 2 + col] = Im_ + Ip;
+        }
+        // Output, t = 0, |s| = 1: y[sigma,l,0] = Theta_{1,l,0} Re[conj(q(+,sigma)) h^+(0)
+        // - conj(q(-,sigma)) h^-(0)], written on the sums of Re/Im h+- over phi.
+        for (int row = 0; row < 2; ++row) {
+            const int sigma = row == 0 ? 1 : -1;
+            const Cplx qp = q_m0(flags, 1, sigma), qm = q_m0(flags, -1, sigma);
+            out[Y.m0 + row * 4 + 0] = qp.re;
+            out[Y.m0 + row * 4 + 1] = qp.im;
+            out[Y.m0 + row * 4 + 2] = -qm.re;
+            out[Y.m0 + row * 4 + 3] = -qm.im;
+        }
+    }
+    for (int k = 0; k < Y.NP; ++k) {
+        for (int t = 0; t <= Y.TM; ++t) {
+            const double ang = 2.0 * kPi * static_cast<double>((k * t) % Y.NP) / Y.NP;
+            out[Y.cosT + k * (Y.TM + 1) + t] = std::cos(ang);
+            out[Y.sinT + k * (Y.TM + 1) + t] = std::sin(ang);
+        }
+    }
+    std::vector<double> gx, gw;
+    gauss_legendre(Y.NT, gx, gw);
+    const double cphi = 2.0 * kPi / Y.NP;
+    double wsum = 0.0;
+    for (int j = 0; j < Y.NT; ++j) {
+        const double th = std::acos(gx[j]);
+        const double wc = gw[j] * cphi;
+        wsum += gw[j];
+        double* b = out.data() + Y.glob + static_cast<size_t>(j) * Y.pb;
+        for (int t = 0; t <= Y.LA; ++t) {
+            for (int l = t; l <= Y.LA; ++l) {
+                const double th0 = swsh_theta(0, l, t, th);
+                b[Y.a0c + tri(Y.LA, t, l)] = (t == 0 ? 1.0 : sq2) * th0;
+                if (t > 0) b[Y.a0s + tri(Y.LA, t, l)] = -sq2 * th0;
+                if (spin_mode == 1 && t > 0) {
+                    b[Y.aup + tri(Y.LA, t, l)] = swsh_theta(1, l, t, th);
+                    b[Y.aum + tri(Y.LA, t, l)] = swsh_theta(-1, l, t, th);
+                }
+            }
+        }
+        if (spin_mode == 1)
+            for (int l = 1; l <= Y.LA; ++l) b[Y.aw + l] = swsh_theta(1, l, 0, th);
+        for (int t = 0; t <= LO; ++t) {
+            for (int l = t; l <= LO; ++l) {
+                const double th0 = swsh_theta(0, l, t, th);
+                b[Y.e0c + tri(LO, t, l)] = wc * (t == 0 ? 1.0 : sq2) * th0;
+                if (t > 0) b[Y.e0s + tri(LO, t, l)] = -wc * sq2 * th0;
+                if (spin_mode == 1 && t > 0) {
+                    b[Y.e1p + tri(LO, t, l)] = wc * swsh_theta(1, l, t, th);
+                    b[Y.e1m + tri(LO, t, l)] = wc * swsh_theta(-1, l, t, th);
+                }
+            }
+        }
+        if (spin_mode == 1)
+            for (int l = 1; l <= LO; ++l) b[Y.e1z + l] = wc * swsh_theta(1, l, 0, th);
+    }
+
+    // Self-checks: the weights integrate 1 exactly, and the rule reproduces
+    // orthonormality of the highest-degree harmonics it has to integrate.
+    if (std::fabs(wsum - 2.0) > 1e-13) return false;
+    const int lmax = Y.TM;
+    for (int s = 0; s <= spin_mode; ++s) {
+        for (int m = 0; m <= lmax; m += (lmax > 0 ? lmax : 1)) {
+            for (int l = std::max(std::abs(s), m); l <= lmax; ++l) {
+                double g = 0.0;
+                for (int j = 0; j < Y.NT; ++j) {
+                    const double v = swsh_theta(s, l, m, std::acos(gx[j]));
+                    g += gw[j] * 2.0 * kPi * v * v;
+                }
+                if (std::fabs(g - 1.0) > 1e-10) return false;
+            }
+        }
+    }
+    return true;
+}
+
+}  // namespace spingtp
+
+namespace {
+
+spingtp_status check_args(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
+                          int* spin_mode) {
+    if (L1 < 0 || L2 < 0 || L1 > 16 || L2 > 16 || Lout < 0 || Lout > L1 + L2) return SPINGTP_ERR_INVALID_ARG;
+    if (spins == nullptr || n_spins <= 0 || n_spins > 64) return SPINGTP_ERR_INVALID_ARG;
+    if (flags != SPINGTP_BASIS_REAL_PAPER && flags != SPINGTP_BASIS_REAL_M0_PAIRED)
+        return SPINGTP_ERR_INVALID_ARG;
+    bool has0 = false;
+    for (int i = 0; i < n_spins; ++i) {
+        if (i > 0 && spins[i] <= spins[i - 1]) return SPINGTP_ERR_INVALID_ARG;
+        if (spins[i] == 0) has0 = true;
+        bool mirrored = false;
+        for (int j = 0; j < n_spins; ++j) mirrored |= (spins[j] == -spins[i]);
+        if (!mirrored) return SPINGTP_ERR_INVALID_ARG;
+    }
+    if (!has0) return SPINGTP_ERR_INVALID_ARG;
+    if (n_spins == 1) {
+        *spin_mode = 0;
+    } else if (n_spins == 3 && spins[0] == -1 && spins[2] == 1) {
+        *spin_mode = 1;
+    } else {
+        return SPINGTP_ERR_UNSUPPORTED;
+    }
+    return SPINGTP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* spingtp_status_string(spingtp_status s) {
+    switch (s) {
+        case SPINGTP_OK: return "ok";
+        case SPINGTP_ERR_INVALID_ARG: return "invalid argument";
+        case SPINGTP_ERR_UNSUPPORTED: return "unsupported configuration";
+        case SPINGTP_ERR_OUT_OF_MEMORY: return "out of device memory";
+        case SPINGTP_ERR_HIP: return "HIP runtime error";
+        case SPINGTP_ERR_INTERNAL: return "internal error (plan self-check failed)";
+    }
+    return "unknown status";
+}
+
+spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                        unsigned flags, double* tables, size_t capacity,
+                                        size_t* n_tables, int* dims) {
+    int spin_mode = 0;
+    spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
+    if (st != SPINGTP_OK) return st;
+    if (n_tables == nullptr || (capacity > 0 && tables == nullptr)) return SPINGTP_ERR_INVALID_ARG;
+    std::vector<double> tab;
+    try {
+        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags, tab)) return SPINGTP_ERR_INTERNAL;
+    } catch (const std::bad_alloc&) {
+        return SPINGTP_ERR_OUT_OF_MEMORY;
+    }
+    *n_tables = tab.size();
+    const size_t n = tab.size() < capacity ? tab.size() : capacity;
+    if (n) std::memcpy(tables, tab.data(), n * sizeof(double));
+    if (dims) {
+        const spingtp::Layout Y = spingtp::make_layout(L1, L2, Lout);
+        const int d[8] = {Y.NT, Y.NP, L1, L2, Lout, n_spins, Y.pb, Y.glob};
+        std::memcpy(dims, d, sizeof(d));
+    }
+    return SPINGTP_OK;
+}
+
+spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                   spingtp_dtype dtype, unsigned flags, spingtp_plan* out_plan) {
+    if (out_plan == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    *out_plan = nullptr;
+    int spin_mode = 0;
+    spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
+    if (st != SPINGTP_OK) return st;
+    if (dtype != SPINGTP_FP32 && dtype != SPINGTP_BF16) return SPINGTP_ERR_INVALID_ARG;
+    const spingtp::KernelEntry* k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
+    if (k == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+
+    std::vector<double> tab;
+    try {
+        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags, tab)) return SPINGTP_ERR_INTERNAL;
+    } catch (const std::bad_alloc&) {
+        return SPINGTP_ERR_OUT_OF_MEMORY;
+    }
+    std::vector<float> tabf(tab.size());
+    for (size_t i = 0; i < tab.size(); ++i) tabf[i] = static_cast<float>(tab[i]);  // round to nearest
+
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return SPINGTP_ERR_HIP;
+    float* d = nullptr;
+    hipError_t e = hipMalloc(&d, tabf.size() * sizeof(float));
+    if (e == hipErrorOutOfMemory) return SPINGTP_ERR_OUT_OF_MEMORY;
+    if (e != hipSuccess) return SPINGTP_ERR_HIP;
+    if (hipMemcpy(d, tabf.data(), tabf.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(d);
+        return SPINGTP_ERR_HIP;
+    }
+    spingtp_plan p = new (std::nothrow) spingtp_plan_s;
+    if (p == nullptr) {
+        (void)hipFree(d);
+        return SPINGTP_ERR_OUT_OF_MEMORY;
+    }
+    p->L1 = L1;
+    p->L2 = L2;
+    p->LO = Lout;
+    p->spin_mode = spin_mode;
+    p->n_spins = n_spins;
+    p->dtype = dtype;
+    p->flags = flags;
+    p->device = dev;
+    p->d_tab = d;
+    p->n_tab = tabf.size();
+    p->kernel = k;
+    *out_plan = p;
+    return SPINGTP_OK;
+}
+
+spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
+    if (plan == nullptr) return SPINGTP_OK;
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != plan->device) e = hipSetDevice(plan->device);
+    if (e == hipSuccess) e = hipFree(plan->d_tab);
+    if (cur != plan->device) (void)hipSetDevice(cur);
+    delete plan;
+    return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
+}
+
+spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info) {
+    if (plan == nullptr || info == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    info[0] = plan->kernel->waves;
+    info[1] = plan->kernel->units;
+    info[2] = plan->kernel->lds_bytes;
+    info[3] = plan->kernel->family;
+    return SPINGTP_OK;
+}
+
+}  // extern "C"

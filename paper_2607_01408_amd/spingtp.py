@@ -1,0 +1,111 @@
+"""Python binding of the SpinGTP C ABI (``include/spingtp.h``).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libspingtp.so``.  torch provides device memory and the stream.
+"""
+
+import ctypes
+
+import numpy as np
+
+from . import _lib
+
+BASIS_PAPER = 0
+BASIS_M0_PAIRED = 1
+FP32 = 0
+BF16 = 1
+
+
+def _spin_array(spins):
+    spins = [int(s) for s in spins]
+    return (ctypes.c_int * len(spins))(*spins), len(spins)
+
+
+def plan_tables_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Float64 plan tables and dims (host only, no GPU needed)."""
+    arr, n = _spin_array(spins)
+    count = ctypes.c_size_t(0)
+    dims = (ctypes.c_int * 8)()
+    _lib.check(_lib.lib().spingtp_plan_tables_host(L1, L2, Lout, arr, n, basis, None, 0,
+                                                   ctypes.byref(count), dims), "spingtp_plan_tables_host")
+    out = np.zeros(count.value, dtype=np.float64)
+    _lib.check(_lib.lib().spingtp_plan_tables_host(
+        L1, L2, Lout, arr, n, basis, out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), out.size,
+        ctypes.byref(count), dims), "spingtp_plan_tables_host")
+    keys = ("n_theta", "n_phi", "L1", "L2", "Lout", "n_spins", "per_theta_block", "global_block")
+    return out, dict(zip(keys, list(dims)))
+
+
+class Plan:
+    """spingtp_plan_create / spingtp_forward / spingtp_plan_destroy."""
+
+    def __init__(self, L1, L2, Lout, spins=(-1, 0, 1), dtype="fp32", basis=BASIS_PAPER):
+        import torch  # device memory and streams only
+
+        self.L1, self.L2, self.Lout = int(L1), int(L2), int(Lout)
+        self.spins = tuple(int(s) for s in spins)
+        self.dtype_name = {"fp32": "fp32", "float32": "fp32", "bf16": "bf16", "bfloat16": "bf16"}[str(dtype)]
+        self.torch_dtype = torch.float32 if self.dtype_name == "fp32" else torch.bfloat16
+        self.basis = int(basis)
+        self._handle = ctypes.c_void_p()
+        arr, n = _spin_array(self.spins)
+        code = FP32 if self.dtype_name == "fp32" else BF16
+        _lib.check(_lib.lib().spingtp_plan_create(self.L1, self.L2, self.Lout, arr, n, code, self.basis,
+                                                  ctypes.byref(self._handle)), "spingtp_plan_create")
+        self.device = torch.cuda.current_device()
+
+    @property
+    def handle(self):
+        return self._handle
+
+    def shape_in(self, which):
+        L = self.L1 if which == 1 else self.L2
+        return (len(self.spins), (L + 1) ** 2)
+
+    @property
+    def shape_out(self):
+        return (len(self.spins), (self.Lout + 1) ** 2)
+
+    def kernel_info(self):
+        info = (ctypes.c_int * 4)()
+        _lib.check(_lib.lib().spingtp_plan_kernel_info(self._handle, info), "spingtp_plan_kernel_info")
+        return {"waves": info[0], "units_per_workgroup": info[1], "lds_bytes": info[2], "family": info[3]}
+
+    def forward(self, x1, x2, out=None, stream=None):
+        """out[N, C, n_spins, (Lout+1)^2] = SpinGTP(x1, x2) on the current (or given) stream."""
+        import torch
+
+        if x1.dim() != 4 or x2.dim() != 4:
+            raise ValueError("x1 and x2 must be [N, C, n_spins, (L+1)^2]")
+        N, C = x1.shape[0], x1.shape[1]
+        if tuple(x1.shape[2:]) != self.shape_in(1) or tuple(x2.shape[2:]) != self.shape_in(2):
+            raise ValueError(f"trailing shapes {tuple(x1.shape[2:])}, {tuple(x2.shape[2:])} do not match "
+                             f"{self.shape_in(1)}, {self.shape_in(2)}")
+        if tuple(x2.shape[:2]) != (N, C):
+            raise ValueError("x1 and x2 must share [N, C]")
+        for t in (x1, x2):
+            if t.dtype != self.torch_dtype or not t.is_cuda or not t.is_contiguous():
+                raise ValueError(f"inputs must be contiguous {self.torch_dtype} device tensors")
+        if out is None:
+            out = torch.empty((N, C) + self.shape_out, dtype=self.torch_dtype, device=x1.device)
+        elif (tuple(out.shape) != (N, C) + self.shape_out or out.dtype != self.torch_dtype
+              or not out.is_contiguous()):
+            raise ValueError("out has the wrong shape, dtype or layout")
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+        _lib.check(_lib.lib().spingtp_forward(self._handle, x1.data_ptr(), x2.data_ptr(), out.data_ptr(),
+                                              N, C, ctypes.c_void_p(stream.cuda_stream)), "spingtp_forward")
+        return out
+
+    __call__ = forward
+
+    def close(self):
+        if self._handle is not None and self._handle.value:
+            _lib.check(_lib.lib().spingtp_plan_destroy(self._handle), "spingtp_plan_destroy")
+            self._handle = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

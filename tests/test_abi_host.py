@@ -1,0 +1,187 @@
+"""Host-side tests of the C-ABI library (CPU only, no GPU calls that compute).
+
+* the library loads and exports every function ``include/spingtp.h`` declares;
+* argument checking of the host-only table entry point;
+* the float64 plan tables, pushed through a numpy re-enactment of the kernel's
+  five steps, reproduce the oracle.  This checks the plan builder's mathematics
+  (grid, SWSH values, real-basis mixing, folded constants) before any GPU run.
+"""
+
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_01408_amd import _lib
+from paper_2607_01408_amd.spingtp import plan_tables_host
+from tests.oracle_helpers import valid_mask
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spingtp.h")
+
+
+@pytest.fixture(scope="session", autouse=True)
+def built_library():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2607_01408_amd import build
+        build.build()
+    return _lib.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_][a-z_0-9]*\s*\*?\s*(spingtp_[a-z_0-9]+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def test_exports_every_declared_symbol(built_library):
+    names = declared_functions()
+    assert set(names) >= set(_lib.EXPORTED)
+    for n in names:
+        assert hasattr(built_library, n), n
+
+
+def _spins(s):
+    return (ctypes.c_int * len(s))(*s), len(s)
+
+
+@pytest.mark.parametrize("args,status", [
+    ((2, 2, 5, (-1, 0, 1), 0), 1),      # Lout > L1 + L2
+    ((17, 2, 2, (-1, 0, 1), 0), 1),     # L1 > 16
+    ((-1, 2, 2, (-1, 0, 1), 0), 1),     # negative degree
+    ((2, 2, 2, (0, 1), 0), 1),          # not symmetric
+    ((2, 2, 2, (1, 0, -1), 0), 1),      # not ascending
+    ((2, 2, 2, (-1, 1), 0), 1),         # no spin 0
+    ((2, 2, 2, (-2, -1, 0, 1, 2), 0), 2),  # valid, not built
+    ((2, 2, 2, (-1, 0, 1), 7), 1),      # unknown basis flag
+    ((2, 2, 2, (-1, 0, 1), 0), 0),
+    ((3, 1, 4, (0,), 1), 0),
+])
+def test_table_entry_point_argument_checks(built_library, args, status):
+    L1, L2, Lout, spins, flags = args
+    arr, n = _spins(spins)
+    count = ctypes.c_size_t(0)
+    got = built_library.spingtp_plan_tables_host(L1, L2, Lout, arr, n, flags, None, 0, ctypes.byref(count), None)
+    assert got == status
+
+
+def test_status_strings(built_library):
+    for s in range(6):
+        assert len(_lib.message(s)) >= 2
+
+
+def emulate_kernel(x1, x2, L1, L2, LO, spin, basis):
+    """float64 re-enactment of the forward kernel from the host tables (layout.h)."""
+    tab, dims = plan_tables_host(L1, L2, LO, (-1, 0, 1) if spin else (0,), basis)
+    NT, NP, PB, GLOB = dims["n_theta"], dims["n_phi"], dims["per_theta_block"], dims["global_block"]
+    LA, TM = max(L1, L2), max(L1, L2, LO)
+    triA, triO = (LA + 1) * (LA + 2) // 2, (LO + 1) * (LO + 2) // 2
+    tri = lambda L, t, l: t * (L + 1) - t * (t - 1) // 2 + (l - t)  # noqa: E731
+    a0c, a0s, aup, aum, aw = 0, triA, 2 * triA, 3 * triA, 4 * triA
+    e0c = aw + LA + 1
+    e0s, e1p, e1m, e1z = e0c + triO, e0c + 2 * triO, e0c + 3 * triO, e0c + 4 * triO
+    N0 = tab[0:8].reshape(4, 2)
+    M0 = tab[8:16].reshape(2, 4)
+    COS = tab[16:16 + NP * (TM + 1)].reshape(NP, TM + 1)
+    SIN = tab[16 + NP * (TM + 1):16 + 2 * NP * (TM + 1)].reshape(NP, TM + 1)
+    NS = 3 if spin else 1
+    U = x1.shape[0]
+
+    def block(x, L, si):
+        return x[:, si * (L + 1) ** 2:(si + 1) * (L + 1) ** 2]
+
+    def fourier(x, L, tb):
+        x0 = block(x, L, 1 if spin else 0)
+        P = {k: np.zeros((U, L + 1)) for k in ("Ac", "As", "Bc", "Bs", "Cc", "Cs")}
+        for t in range(L + 1):
+            for l in range(t, L + 1):
+                P["Ac"][:, t] += x0[:, l * l + l + t] * tb[a0c + tri(LA, t, l)]
+                if t:
+                    P["As"][:, t] += x0[:, l * l + l - t] * tb[a0s + tri(LA, t, l)]
+        d = e = np.zeros(U)
+        if spin:
+            xm, xp = block(x, L, 0), block(x, L, 2)
+            for t in range(1, L + 1):
+                up = vp = um = vm = 0.0
+                for l in range(t, L + 1):
+                    wp, wm = tb[aup + tri(LA, t, l)], tb[aum + tri(LA, t, l)]
+                    up = up + xp[:, l * l + l + t] * wp
+                    vp = vp + xp[:, l * l + l - t] * wp
+                    um = um + xm[:, l * l + l + t] * wm
+                    vm = vm + xm[:, l * l + l - t] * wm
+                P["Bc"][:, t], P["Bs"][:, t] = up + um, -(vp + vm)
+                P["Cc"][:, t], P["Cs"][:, t] = vp - vm, up - um
+            wpl = sum(xp[:, l * l + l] * tb[aw + l] for l in range(1, L + 1)) if L else np.zeros(U)
+            wmi = sum(xm[:, l * l + l] * tb[aw + l] for l in range(1, L + 1)) if L else np.zeros(U)
+            v = N0 @ np.stack([wpl, wmi])
+            P["Bc"][:, 0], P["Cc"][:, 0], d, e = v
+        return P, d, e
+
+    y = np.zeros((U, NS * (LO + 1) ** 2))
+    for j in range(NT):
+        tb = tab[GLOB + j * PB:GLOB + (j + 1) * PB]
+        F1, d1, e1 = fourier(x1, L1, tb)
+        F2, d2, e2 = fourier(x2, L2, tb)
+
+        def val(P, key, L, k):
+            return P[key + "c"] @ COS[k, :L + 1] + P[key + "s"] @ SIN[k, :L + 1]
+
+        R0c, R0s, P1c, P1s, P2c, P2s = (np.zeros((U, LO + 1)) for _ in range(6))
+        for k in range(NP):
+            A, a = val(F1, "A", L1, k), val(F2, "A", L2, k)
+            B, b = val(F1, "B", L1, k), val(F2, "B", L2, k)
+            C, c = val(F1, "C", L1, k), val(F2, "C", L2, k)
+            r0 = A * a + (B * b + C * c if spin else 0)
+            p1, p2 = A * b + a * B, A * c + a * C
+            R0c += np.outer(r0, COS[k, :LO + 1])
+            R0s += np.outer(r0, SIN[k, :LO + 1])
+            P1c += np.outer(p1, COS[k, :LO + 1])
+            P1s += np.outer(p1, SIN[k, :LO + 1])
+            P2c += np.outer(p2, COS[k, :LO + 1])
+            P2s += np.outer(p2, SIN[k, :LO + 1])
+        if spin:
+            R0c[:, 0] += -0.5 * NP * (d1 * d2 + e1 * e2)
+        B0 = (LO + 1) ** 2
+        y0 = y[:, B0:2 * B0] if spin else y
+        for t in range(LO + 1):
+            for l in range(t, LO + 1):
+                y0[:, l * l + l + t] += tb[e0c + tri(LO, t, l)] * R0c[:, t]
+                if t:
+                    y0[:, l * l + l - t] += tb[e0s + tri(LO, t, l)] * R0s[:, t]
+        if spin:
+            ym, yp = y[:, :B0], y[:, 2 * B0:]
+            for t in range(1, LO + 1):
+                for l in range(t, LO + 1):
+                    wp, wm = tb[e1p + tri(LO, t, l)], tb[e1m + tri(LO, t, l)]
+                    yp[:, l * l + l + t] += wp * (P1c[:, t] + P2s[:, t])
+                    ym[:, l * l + l + t] += wm * (P1c[:, t] - P2s[:, t])
+                    yp[:, l * l + l - t] += wp * (P2c[:, t] - P1s[:, t])
+                    ym[:, l * l + l - t] += wm * (-P2c[:, t] - P1s[:, t])
+            sP1, sP2 = math.sqrt(2) * P1c[:, 0], math.sqrt(2) * P2c[:, 0]
+            sP4 = -NP * (d2 * F1["Ac"][:, 0] + d1 * F2["Ac"][:, 0])
+            sP3 = NP * (e2 * F1["Ac"][:, 0] + e1 * F2["Ac"][:, 0])
+            Z = M0 @ np.stack([(sP1 + sP4) / 2, (sP3 + sP2) / 2, (sP1 - sP4) / 2, (sP3 - sP2) / 2])
+            for l in range(1, LO + 1):
+                yp[:, l * l + l] += tb[e1z + l] * Z[0]
+                ym[:, l * l + l] += tb[e1z + l] * Z[1]
+    return y
+
+
+@pytest.mark.parametrize("L1,L2,LO,spin,basis", [
+    (2, 2, 2, True, 0), (2, 2, 2, True, 1), (1, 1, 1, True, 0), (3, 2, 4, True, 0), (2, 3, 1, True, 1),
+    (4, 4, 4, True, 0), (6, 6, 6, True, 0), (2, 2, 2, False, 0), (3, 1, 2, False, 0), (0, 0, 0, False, 0),
+    (1, 3, 3, True, 0), (8, 8, 8, True, 0),
+])
+def test_plan_tables_reproduce_oracle(built_library, L1, L2, LO, spin, basis):
+    S = (-1, 0, 1) if spin else (0,)
+    rng = np.random.default_rng(L1 * 100 + L2 * 10 + LO)
+    x1 = rng.standard_normal((6, len(S) * (L1 + 1) ** 2)) * valid_mask(S, L1)
+    x2 = rng.standard_normal((6, len(S) * (L2 + 1) ** 2)) * valid_mask(S, L2)
+    y = emulate_kernel(x1, x2, L1, L2, LO, spin, basis)
+    yo = oracle.RealGauntTensor(L1, L2, LO, S, basis).apply(x1, x2).reshape(6, -1)
+    assert np.abs(y - yo).max() <= 1e-12 * max(1.0, np.abs(yo).max())

@@ -1,0 +1,187 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Bar (per element set, relative L2 over the compared units): 1e-5 in fp32 and
+2e-2 in bf16.  The oracle always sees the exact dtype-rounded inputs the GPU saw
+(read back from the device).  Large workloads compare the first and last 512
+units (tile tails) and a seeded random sample, at the full size and in the
+launch configuration the benchmark times.
+"""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from tests.oracle_helpers import valid_mask
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU visible", allow_module_level=True)
+
+from paper_2607_01408_amd import Plan, SpinGTPError, workloads  # noqa: E402
+from paper_2607_01408_amd import _lib  # noqa: E402
+
+S3 = (-1, 0, 1)
+TOL = {"fp32": 1e-5, "bf16": 2e-2}
+
+
+def rel_l2(y, ref):
+    return float(np.linalg.norm(y - ref) / max(np.linalg.norm(ref), 1e-300))
+
+
+def run_and_compare(L1, L2, LO, spins, N, C, dtype="fp32", basis=0, seed=0, scale="unit", units=None):
+    print(f"[parity] L=({L1},{L2},{LO}) spins={spins} N={N} C={C} {dtype} basis={basis}", flush=True)
+    x1 = workloads.draw(L1, N, C, 7000 + seed, dtype, spins, scale, "cuda")
+    x2 = workloads.draw(L2, N, C, 8000 + seed, dtype, spins, scale, "cuda")
+    plan = Plan(L1, L2, LO, spins, dtype, basis)
+    y = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    U = N * C
+    idx = np.arange(U) if units is None else units
+    ti = torch.as_tensor(idx, device="cuda")
+    a = x1.view(U, -1)[ti].double().cpu().numpy()
+    b = x2.view(U, -1)[ti].double().cpu().numpy()
+    g = y.view(U, -1)[ti].double().cpu().numpy()
+    ref = oracle.RealGauntTensor(L1, L2, LO, spins, basis).apply(a, b).reshape(len(idx), -1)
+    err = rel_l2(g, ref)
+    print(f"[parity]   rel_l2={err:.3e}", flush=True)
+    assert err <= TOL[dtype], err
+    return err
+
+
+def sample_units(U, n_random, seed):
+    rng = np.random.default_rng(seed)
+    head = np.arange(min(512, U))
+    tail = np.arange(max(0, U - 512), U)
+    rnd = rng.choice(U, size=min(n_random, U), replace=False)
+    return np.unique(np.concatenate([head, tail, rnd]))
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("basis", [0, 1])
+def test_ragged_spin_shapes(L, basis):
+    # 37 * 3 = 111 units: one full 64-unit tile and a ragged tail of 47
+    run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=L)
+
+
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 4, 6])
+def test_ragged_scalar_shapes(L):
+    run_and_compare(L, L, L, (0,), 29, 5, "fp32", 0, seed=10 + L)
+
+
+@pytest.mark.parametrize("L1,L2,LO", [(1, 3, 3), (2, 1, 3)])
+def test_mixed_degrees(L1, L2, LO):
+    run_and_compare(L1, L2, LO, S3, 50, 7, "fp32", 0, seed=20 + L1)
+
+
+@pytest.mark.parametrize("L", [2, 4, 6])
+def test_bf16_small(L):
+    run_and_compare(L, L, L, S3, 45, 6, "bf16", 0, seed=30 + L)
+
+
+def test_small_workload_all_units():
+    x1, x2, m = workloads.make_pair("small", device="cuda")
+    plan = Plan(m["L"], m["L"], m["L"], S3, "fp32")
+    y = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    ref = oracle.spingtp(x1.double().cpu().numpy(), x2.double().cpu().numpy(), m["L"], m["L"], m["L"], S3)
+    assert rel_l2(y.double().cpu().numpy(), ref) <= 1e-5
+
+
+@pytest.mark.parametrize("name,dtype", [("molecule", "fp32"), ("organic", "fp32"), ("organic", "bf16")])
+def test_full_size_sampled(name, dtype):
+    print(f"[parity] full-size {name} {dtype}", flush=True)
+    x1, x2, m = workloads.make_pair(name, dtype=dtype, device="cuda")
+    L, U = m["L"], m["N"] * m["C"]
+    plan = Plan(L, L, L, S3, dtype)
+    y = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    idx = sample_units(U, 8192, 99)
+    ti = torch.as_tensor(idx, device="cuda")
+    a = x1.view(U, -1)[ti].double().cpu().numpy()
+    b = x2.view(U, -1)[ti].double().cpu().numpy()
+    g = y.view(U, -1)[ti].double().cpu().numpy()
+    del x1, x2, y
+    torch.cuda.empty_cache()
+    ref = oracle.spingtp(a, b, L, L, L, S3).reshape(len(idx), -1)
+    err = rel_l2(g, ref)
+    print(f"[parity]   rel_l2={err:.3e} over {len(idx)} units", flush=True)
+    assert err <= TOL[dtype]
+
+
+def test_empty_is_noop():
+    plan = Plan(2, 2, 2, S3, "fp32")
+    x = torch.zeros((0, 4, 3, 9), device="cuda")
+    out = plan.forward(x, x)
+    assert out.shape == (0, 4, 3, 9)
+    L = _lib.lib()
+    assert L.spingtp_forward(plan.handle, None, None, None, 0, 5, None) == 0
+    assert L.spingtp_forward(plan.handle, None, None, None, 7, 0, None) == 0
+
+
+def test_invalid_arguments():
+    plan = Plan(2, 2, 2, S3, "fp32")
+    L = _lib.lib()
+    x = torch.zeros((4, 2, 3, 9), device="cuda")
+    y = torch.zeros_like(x)
+    p = x.data_ptr()
+    assert L.spingtp_forward(plan.handle, None, p, y.data_ptr(), 4, 2, None) == 1
+    assert L.spingtp_forward(plan.handle, p + 4, p, y.data_ptr(), 4, 2, None) == 1  # misaligned
+    assert L.spingtp_forward(plan.handle, p, p, y.data_ptr(), -1, 2, None) == 1
+    assert L.spingtp_forward(None, p, p, y.data_ptr(), 4, 2, None) == 1
+    with pytest.raises(SpinGTPError):
+        Plan(2, 2, 2, (-2, -1, 0, 1, 2), "fp32")
+    with pytest.raises(SpinGTPError):
+        Plan(3, 3, 7, S3, "fp32")
+
+
+def test_nan_poisoned_output_and_invalid_slots():
+    L, N, C = 3, 33, 5
+    x1 = workloads.draw(L, N, C, 11, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(L, N, C, 12, "fp32", S3, "unit", "cuda")
+    plan = Plan(L, L, L, S3, "fp32")
+    ref = plan.forward(x1, x2).clone()
+    inv = torch.as_tensor(~valid_mask(S3, L), device="cuda").view(3, -1)
+    g1, g2 = x1.clone(), x2.clone()
+    g1[:, :, inv] = float("nan")
+    g2[:, :, inv] = 1e30
+    out = torch.full_like(ref, float("nan"))
+    plan.forward(g1, g2, out=out)
+    torch.cuda.synchronize()
+    assert not torch.isnan(out).any()
+    torch.testing.assert_close(out, ref, rtol=1e-6, atol=1e-6)
+    assert (out[:, :, inv] == 0).all()
+
+
+def test_gpu_invariants():
+    """Oracle-free checks on the GPU path: constant function and commutativity."""
+    L, N, C = 4, 20, 6
+    x1 = workloads.draw(L, N, C, 21, "fp32", S3, "unit", "cuda")
+    x2 = torch.zeros_like(x1)
+    x2[:, :, 1, 0] = 2.5  # s = 0, l = 0
+    plan = Plan(L, L, L, S3, "fp32")
+    y = plan.forward(x1, x2)
+    torch.testing.assert_close(y, x1 * (2.5 / np.sqrt(4 * np.pi)), rtol=2e-6, atol=2e-6)
+    x3 = workloads.draw(L, N, C, 22, "fp32", S3, "unit", "cuda")
+    torch.testing.assert_close(plan.forward(x1, x3), plan.forward(x3, x1), rtol=1e-5, atol=1e-6)
+
+
+def test_plan_reuse_across_streams():
+    L, N, C = 6, 300, 8
+    x1 = workloads.draw(L, N, C, 31, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(L, N, C, 32, "fp32", S3, "unit", "cuda")
+    plan = Plan(L, L, L, S3, "fp32")
+    ref = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s1):
+        a = plan.forward(x1, x2)
+    with torch.cuda.stream(s2):
+        b = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    torch.testing.assert_close(a, ref, rtol=1e-6, atol=1e-6)
+    torch.testing.assert_close(b, ref, rtol=1e-6, atol=1e-6)
