@@ -205,6 +205,55 @@ __device__ __forceinline__ void synth(const float (&pc)[L + 1], const float (&ps
     minus = ev - od;
 }
 
+// Per-node spectra exchanged between the theta-node waves before the final
+// projection (step E).  Slot order inside one unit's record:
+//   t = 0 : R0c[0], and with spins Z+ and Z- (the m3 = 0, |s3| = 1 sums);
+//   t >= 1: R0c[t], R0s[t], and with spins the four combinations
+//           P1c+P2s (s3=+1, m3=+t), P1c-P2s (s3=-1, m3=+t),
+//           P2c-P1s (s3=+1, m3=-t), -P2c-P1s (s3=-1, m3=-t).
+// A "group" is one slot: it feeds the output coefficients l = lmin..Lout of one
+// (spin block, m3).  Each group is owned by exactly one wave, which sums the
+// slot over all theta nodes in a fixed order, so the result is deterministic.
+template <int LO, bool SPIN>
+struct Spectra {
+    static constexpr int PER_T = SPIN ? 6 : 2;
+    static constexpr int ND = (SPIN ? 3 : 1) + PER_T * LO;  // slots per unit per node
+    static constexpr int DS = ND | 1;                        // odd LDS stride
+    static constexpr int NG = ND;                            // one group per slot
+    __host__ __device__ static constexpr int t_of(int g) { return g < (SPIN ? 3 : 1) ? 0 : 1 + (g - (SPIN ? 3 : 1)) / PER_T; }
+    __host__ __device__ static constexpr int slot_of(int g) { return g < (SPIN ? 3 : 1) ? g : (g - (SPIN ? 3 : 1)) % PER_T; }
+    __host__ __device__ static constexpr int lmin(int g) {
+        return t_of(g) == 0 ? (slot_of(g) == 0 ? 0 : 1) : t_of(g);
+    }
+    __host__ __device__ static constexpr int size(int g) { return LO + 1 - lmin(g); }
+};
+
+template <int NG>
+struct Owners {
+    int owner[NG];
+};
+
+// Longest-processing-time assignment of the groups to NW waves.
+template <int LO, bool SPIN, int NW>
+constexpr Owners<Spectra<LO, SPIN>::NG> assign_owners() {
+    using SP = Spectra<LO, SPIN>;
+    Owners<SP::NG> o{};
+    int load[NW] = {};
+    bool done[SP::NG] = {};
+    for (int n = 0; n < SP::NG; ++n) {
+        int best = -1;
+        for (int g = 0; g < SP::NG; ++g)
+            if (!done[g] && (best < 0 || SP::size(g) > SP::size(best))) best = g;
+        int w = 0;
+        for (int k = 1; k < NW; ++k)
+            if (load[k] < load[w]) w = k;
+        o.owner[best] = w;
+        load[w] += SP::size(best);
+        done[best] = true;
+    }
+    return o;
+}
+
 template <int L1, int L2, int LO, bool SPIN>
 struct Shape {
     static constexpr Layout Y = make_layout(L1, L2, LO);
@@ -220,7 +269,11 @@ struct Shape {
     static constexpr int KP = (NP - 1) / 2;
     static constexpr int WAVES = NT;
     static constexpr int THREADS = 64 * WAVES;
-    static constexpr int LDS_FLOATS = 64 * (ST1 + ST2 + STO);
+    // LDS: the input tiles, later reused for the per-node spectra, then the output tile
+    static constexpr int XF = 64 * (ST1 + ST2);
+    static constexpr int DF = NT * 64 * Spectra<LO, SPIN>::DS;
+    static constexpr int REGION = XF > DF ? XF : DF;
+    static constexpr int LDS_FLOATS = REGION + 64 * STO;
 };
 
 template <int L1, int L2, int LO, bool SPIN, typename TIO>
@@ -234,7 +287,7 @@ __global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fw
     __shared__ float lds[S::LDS_FLOATS];
     float* X1 = lds;
     float* X2 = X1 + 64 * S::ST1;
-    float* YT = X2 + 64 * S::ST2;
+    float* YT = lds + S::REGION;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -353,53 +406,73 @@ __global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fw
         }
     }
 
-    // (E) projection onto output coefficients; partial sums of all nodes meet in LDS
+    // (E) publish this node's spectra, then every owner wave projects its groups
+    //     onto the output coefficients, summing over the nodes in a fixed order.
+    using SP = Spectra<LO, SPIN>;
     constexpr int BO = (LO + 1) * (LO + 1);
-    float* yr = YT + lane * S::STO;
-    float* y0 = yr + (SPIN ? BO : 0);
-    if constexpr (SPIN) R0c[0] = fmaf(-0.5f * S::NP, fmaf(d1, d2, e1 * e2), R0c[0]);
-#pragma unroll
-    for (int t = 0; t <= LO; ++t) {
-#pragma unroll
-        for (int l = t; l <= LO; ++l) {
-            atomicAdd(&y0[l * l + l + t], tb[Y.e0c + tri(LO, t, l)] * R0c[t]);
-            if (t > 0) atomicAdd(&y0[l * l + l - t], tb[Y.e0s + tri(LO, t, l)] * R0s[t]);
-        }
-    }
+    float* D = X1 + (node * 64 + lane) * SP::DS;  // aliases the input tiles
+    __syncthreads();                               // every wave is past step (A)
     if constexpr (SPIN) {
-        float* ym = yr;
-        float* yp = yr + 2 * BO;
+        R0c[0] = fmaf(-0.5f * S::NP, fmaf(d1, d2, e1 * e2), R0c[0]);
+        // m3 = 0, |s3| = 1: sums over phi of Re/Im h+ and h-
+        const float sP1 = 1.41421356237309505f * P1c[0];
+        const float sP2 = 1.41421356237309505f * P2c[0];
+        const float sP4 = -static_cast<float>(S::NP) * fmaf(d2, Ac[0], d1 * ac[0]);
+        const float sP3 = static_cast<float>(S::NP) * fmaf(e2, Ac[0], e1 * ac[0]);
+        const float v0 = 0.5f * (sP1 + sP4), v1 = 0.5f * (sP3 + sP2);
+        const float v2 = 0.5f * (sP1 - sP4), v3 = 0.5f * (sP3 - sP2);
+        const float* m0 = g + Y.m0;
+        D[0] = R0c[0];
+        D[1] = fmaf(m0[0], v0, fmaf(m0[1], v1, fmaf(m0[2], v2, m0[3] * v3)));
+        D[2] = fmaf(m0[4], v0, fmaf(m0[5], v1, fmaf(m0[6], v2, m0[7] * v3)));
 #pragma unroll
         for (int t = 1; t <= LO; ++t) {
-            const float zpc = P1c[t] + P2s[t], zmc = P1c[t] - P2s[t];
-            const float zps = P2c[t] - P1s[t], zms = -P2c[t] - P1s[t];
-#pragma unroll
-            for (int l = t; l <= LO; ++l) {
-                const float wp = tb[Y.e1p + tri(LO, t, l)];
-                const float wm = tb[Y.e1m + tri(LO, t, l)];
-                atomicAdd(&yp[l * l + l + t], wp * zpc);
-                atomicAdd(&ym[l * l + l + t], wm * zmc);
-                atomicAdd(&yp[l * l + l - t], wp * zps);
-                atomicAdd(&ym[l * l + l - t], wm * zms);
-            }
+            float* d = D + 3 + 6 * (t - 1);
+            d[0] = R0c[t];
+            d[1] = R0s[t];
+            d[2] = P1c[t] + P2s[t];
+            d[3] = P1c[t] - P2s[t];
+            d[4] = P2c[t] - P1s[t];
+            d[5] = -P2c[t] - P1s[t];
         }
-        if constexpr (LO >= 1) {
-            // m3 = 0, |s3| = 1: sums over phi of Re/Im h+ and h-
-            const float sP1 = 1.41421356237309505f * P1c[0];
-            const float sP2 = 1.41421356237309505f * P2c[0];
-            const float sP4 = -static_cast<float>(S::NP) * fmaf(d2, Ac[0], d1 * ac[0]);
-            const float sP3 = static_cast<float>(S::NP) * fmaf(e2, Ac[0], e1 * ac[0]);
-            const float v0 = 0.5f * (sP1 + sP4), v1 = 0.5f * (sP3 + sP2);
-            const float v2 = 0.5f * (sP1 - sP4), v3 = 0.5f * (sP3 - sP2);
-            const float* m0 = g + Y.m0;
-            const float zp = fmaf(m0[0], v0, fmaf(m0[1], v1, fmaf(m0[2], v2, m0[3] * v3)));
-            const float zm = fmaf(m0[4], v0, fmaf(m0[5], v1, fmaf(m0[6], v2, m0[7] * v3)));
+    } else {
+        D[0] = R0c[0];
 #pragma unroll
-            for (int l = 1; l <= LO; ++l) {
-                const float w = tb[Y.e1z + l];
-                atomicAdd(&yp[l * l + l], w * zp);
-                atomicAdd(&ym[l * l + l], w * zm);
-            }
+        for (int t = 1; t <= LO; ++t) {
+            D[1 + 2 * (t - 1)] = R0c[t];
+            D[2 + 2 * (t - 1)] = R0s[t];
+        }
+    }
+    __syncthreads();
+
+    constexpr Owners<SP::NG> own = assign_owners<LO, SPIN, S::WAVES>();
+    float* yr = YT + lane * S::STO;
+#pragma unroll
+    for (int gi = 0; gi < SP::NG; ++gi) {
+        if (own.owner[gi] != node) continue;
+        const int t = SP::t_of(gi), slot = SP::slot_of(gi);
+        float dv[S::NT];
+#pragma unroll
+        for (int j = 0; j < S::NT; ++j) dv[j] = X1[(j * 64 + lane) * SP::DS + gi];
+        // output block and table of this group
+        int blk = 0, sgn = 1, tab_base = 0;
+        bool e1z = false;
+        if (t == 0) {
+            if (slot == 0) { blk = SPIN ? 1 : 0; tab_base = Y.e0c; }
+            else { blk = slot == 1 ? 2 : 0; e1z = true; tab_base = Y.e1z; }
+        } else if (slot == 0) { blk = SPIN ? 1 : 0; tab_base = Y.e0c; }
+        else if (slot == 1) { blk = SPIN ? 1 : 0; tab_base = Y.e0s; sgn = -1; }
+        else if (slot == 2) { blk = 2; tab_base = Y.e1p; }
+        else if (slot == 3) { blk = 0; tab_base = Y.e1m; }
+        else if (slot == 4) { blk = 2; tab_base = Y.e1p; sgn = -1; }
+        else { blk = 0; tab_base = Y.e1m; sgn = -1; }
+#pragma unroll
+        for (int l = SP::lmin(gi); l <= LO; ++l) {
+            const int toff = e1z ? tab_base + l : tab_base + tri(LO, t, l);
+            float acc = 0.f;
+#pragma unroll
+            for (int j = 0; j < S::NT; ++j) acc = fmaf(tab[Y.glob + j * Y.pb + toff], dv[j], acc);
+            yr[blk * BO + l * l + l + sgn * t] = acc;
         }
     }
     __syncthreads();
