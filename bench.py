@@ -135,6 +135,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--parity-units", type=int, default=2048)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after timing, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -181,6 +183,15 @@ def main():
     achieved_tflops = flops_unit * U / (avg_launch_ms / 1e3) / 1e12
     bytes_unit = hbm_bytes_per_unit(L, L, L, args.dtype)
     traffic = measured_traffic(meta["workload"], args.dtype, U)
+
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # sampled parity against the oracle on the timed output
     import oracle

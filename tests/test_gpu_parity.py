@@ -185,3 +185,15 @@ def test_plan_reuse_across_streams():
     torch.cuda.synchronize()
     torch.testing.assert_close(a, ref, rtol=1e-6, atol=1e-6)
     torch.testing.assert_close(b, ref, rtol=1e-6, atol=1e-6)
+
+
+def test_bitwise_deterministic():
+    """The node sums run in a fixed order (no atomics): repeated launches agree bit for bit."""
+    L, N, C = 6, 700, 16
+    x1 = workloads.draw(L, N, C, 41, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(L, N, C, 42, "fp32", S3, "unit", "cuda")
+    plan = Plan(L, L, L, S3, "fp32")
+    a = plan.forward(x1, x2)
+    b = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
