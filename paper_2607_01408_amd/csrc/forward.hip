@@ -479,6 +479,260 @@ __global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fw
     store_tile<S::NCO, S::STO>(out + u0 * S::NCO, nvalid, YT, tid, S::THREADS);
 }
 
+// ---------------------------------------------------------------------------
+// Lane-pair kernel for L1 = L2 = Lout = L with larger L (7, 8).
+//
+// Lanes 2u and 2u+1 share unit u: lane 2u keeps the three polynomials of input
+// 1, lane 2u+1 those of input 2 (halving the per-lane state), and each
+// synthesised value is handed to the partner lane with one DPP swap.  The
+// products are symmetric in the two inputs, so both lanes form them with the
+// same code.  The analysis is split by trigonometric type: the even lane
+// accumulates the cosine spectra of R0, P1, P2 and the odd lane the sine
+// spectra, reading its own row of a cos/sin table in LDS; every other table
+// value is still wave-uniform.  Step (E) pairs the output coefficient
+// m3 = +t (even lane) with m3 = -t (odd lane), which use the same table entry
+// (for R0 the sine table is the negated cosine table, folded into the sign of
+// the exchanged value).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float swap_pair(float v) {
+    // quad_perm [1,0,3,2]: exchange with the neighbouring lane
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+}
+
+template <int L, bool SPIN>
+struct PairShape {
+    static constexpr Layout Y = make_layout(L, L, L);
+    static constexpr int NS = SPIN ? 3 : 1;
+    static constexpr int NC = NS * (L + 1) * (L + 1);
+    static constexpr int ST = NC | 1;
+    static constexpr int NT = Y.NT;
+    static constexpr int NP = Y.NP;
+    static constexpr int KP = (NP - 1) / 2;
+    static constexpr int UNITS = 32;
+    static constexpr int WAVES = NT;
+    static constexpr int THREADS = 64 * WAVES;
+    // exchanged slots per unit: t = 0: (R0, unused, Z+, Z-) | t >= 1: (R0 +/-, P +/-, M +/-)
+    static constexpr int T0 = SPIN ? 4 : 2;
+    static constexpr int PER_T = SPIN ? 6 : 2;
+    static constexpr int ND = T0 + PER_T * L;
+    static constexpr int DS = ND | 1;
+    static constexpr int XF = UNITS * 2 * ST;
+    static constexpr int DF = NT * UNITS * DS;
+    static constexpr int REGION = XF > DF ? XF : DF;
+    static constexpr int TRIG = 2 * NP * (L + 1);
+    static constexpr int LDS_FLOATS = REGION + UNITS * ST + TRIG;
+    // pair groups: t = 0 -> R0 (l >= 0), Z (l >= 1, spins); t >= 1 -> R0, P, M (spins) or R0
+    static constexpr int G0 = SPIN ? 2 : 1;
+    static constexpr int GT = SPIN ? 3 : 1;
+    static constexpr int NG = G0 + GT * L;
+    __host__ __device__ static constexpr int t_of(int g) { return g < G0 ? 0 : 1 + (g - G0) / GT; }
+    __host__ __device__ static constexpr int kind_of(int g) { return g < G0 ? (g == 0 ? 0 : 3) : (g - G0) % GT; }
+    __host__ __device__ static constexpr int lmin(int g) { return kind_of(g) == 3 ? 1 : t_of(g); }
+    __host__ __device__ static constexpr int size(int g) { return L + 1 - lmin(g); }
+    __host__ __device__ static constexpr int slot(int g) {
+        return t_of(g) == 0 ? (kind_of(g) == 0 ? 0 : 2) : T0 + PER_T * (t_of(g) - 1) + 2 * kind_of(g);
+    }
+};
+
+template <int L, bool SPIN, int NW>
+constexpr Owners<PairShape<L, SPIN>::NG> assign_pair_owners() {
+    using P = PairShape<L, SPIN>;
+    Owners<P::NG> o{};
+    int load[NW] = {};
+    bool done[P::NG] = {};
+    for (int n = 0; n < P::NG; ++n) {
+        int best = -1;
+        for (int g = 0; g < P::NG; ++g)
+            if (!done[g] && (best < 0 || P::size(g) > P::size(best))) best = g;
+        int w = 0;
+        for (int k = 1; k < NW; ++k)
+            if (load[k] < load[w]) w = k;
+        o.owner[best] = w;
+        load[w] += P::size(best);
+        done[best] = true;
+    }
+    return o;
+}
+
+template <int L, bool SPIN, typename TIO>
+__global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pair_kernel(
+    const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units,
+    const float* __restrict__ tab) {
+    using P = PairShape<L, SPIN>;
+    constexpr Layout Y = P::Y;
+    constexpr int TM1 = Y.TM + 1;
+    constexpr int BO = (L + 1) * (L + 1);
+    __shared__ float lds[P::LDS_FLOATS];
+    float* X1 = lds;
+    float* X2 = X1 + P::UNITS * P::ST;
+    float* YT = lds + P::REGION;
+    float* TR = YT + P::UNITS * P::ST;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int u = lane >> 1;
+    const int sub = lane & 1;
+    const int node = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t u0 = static_cast<int64_t>(blockIdx.x) * P::UNITS;
+    const int nvalid = static_cast<int>(units - u0 < P::UNITS ? units - u0 : P::UNITS);
+    const float* __restrict__ g = tab;
+
+    for (int i = tid; i < P::UNITS * P::ST; i += P::THREADS) YT[i] = 0.f;
+    for (int i = tid; i < P::TRIG; i += P::THREADS) {
+        const int sb = i / (P::NP * (L + 1));
+        const int r = i - sb * (P::NP * (L + 1));
+        const int k = r / (L + 1), t = r - k * (L + 1);
+        TR[i] = g[(sb ? Y.sinT : Y.cosT) + k * TM1 + t];
+    }
+    load_tile<P::NC, P::ST>(x1 + u0 * P::NC, nvalid, X1, tid, P::THREADS);
+    load_tile<P::NC, P::ST>(x2 + u0 * P::NC, nvalid, X2, tid, P::THREADS);
+    __syncthreads();
+
+    const float* __restrict__ tb = tab + Y.glob + node * Y.pb;
+    float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
+    coef_to_theta_fourier<L, L, SPIN>((sub ? X2 : X1) + u * P::ST, tb, g + Y.n0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2,
+                                      dl, ep);
+    const float sg = sub ? -1.f : 1.f;
+    const float* trl = TR + sub * (P::NP * (L + 1));
+
+    // accumulators: cosine spectra on the even lane, sine spectra on the odd lane
+    float Q0[L + 1], Q1[L + 1], Q2[L + 1];
+#pragma unroll
+    for (int t = 0; t <= L; ++t) Q0[t] = Q1[t] = Q2[t] = 0.f;
+
+    auto accumulate = [&](float vr, float v1, float v2, const float* tr) {
+#pragma unroll
+        for (int t = 0; t <= L; ++t) {
+            const float w = tr[t];
+            Q0[t] = fmaf(vr, w, Q0[t]);
+            if constexpr (SPIN) {
+                Q1[t] = fmaf(v1, w, Q1[t]);
+                Q2[t] = fmaf(v2, w, Q2[t]);
+            }
+        }
+    };
+    // phi = 0 (and phi = pi when n_phi is even): a single point
+    auto single_point = [&](int k, float sgn_t_odd) {
+        float o0 = 0.f, o1 = 0.f, o2 = 0.f;
+#pragma unroll
+        for (int t = 0; t <= L; ++t) {
+            const float c = (t & 1) ? sgn_t_odd : 1.f;
+            o0 = fmaf(c, Pc0[t], o0);
+            if constexpr (SPIN) o1 = fmaf(c, Pc1[t], o1), o2 = fmaf(c, Pc2[t], o2);
+        }
+        const float p0 = swap_pair(o0);
+        float r0 = o0 * p0, q1 = 0.f, q2 = 0.f;
+        if constexpr (SPIN) {
+            const float p1 = swap_pair(o1), p2 = swap_pair(o2);
+            r0 = fmaf(o1, p1, fmaf(o2, p2, r0));
+            q1 = fmaf(o0, p1, p0 * o1);
+            q2 = fmaf(o0, p2, p0 * o2);
+        }
+        accumulate(r0, q1, q2, trl + k * (L + 1));
+    };
+    single_point(0, 1.f);
+#pragma unroll 1
+    for (int k = 1; k <= P::KP; ++k) {
+        const float* __restrict__ cs = g + Y.cosT + k * TM1;
+        const float* __restrict__ sn = g + Y.sinT + k * TM1;
+        float o0p, o0m, o1p = 0.f, o1m = 0.f, o2p = 0.f, o2m = 0.f;
+        synth<L>(Pc0, Ps0, cs, sn, o0p, o0m);
+        if constexpr (SPIN) {
+            synth<L>(Pc1, Ps1, cs, sn, o1p, o1m);
+            synth<L>(Pc2, Ps2, cs, sn, o2p, o2m);
+        }
+        const float p0p = swap_pair(o0p), p0m = swap_pair(o0m);
+        float r0p = o0p * p0p, r0m = o0m * p0m, q1p = 0.f, q1m = 0.f, q2p = 0.f, q2m = 0.f;
+        if constexpr (SPIN) {
+            const float p1p = swap_pair(o1p), p1m = swap_pair(o1m);
+            const float p2p = swap_pair(o2p), p2m = swap_pair(o2m);
+            r0p = fmaf(o1p, p1p, fmaf(o2p, p2p, r0p));
+            r0m = fmaf(o1m, p1m, fmaf(o2m, p2m, r0m));
+            q1p = fmaf(o0p, p1p, p0p * o1p);
+            q1m = fmaf(o0m, p1m, p0m * o1m);
+            q2p = fmaf(o0p, p2p, p0p * o2p);
+            q2m = fmaf(o0m, p2m, p0m * o2m);
+        }
+        // even lane: sums (cosine), odd lane: differences (sine)
+        accumulate(fmaf(sg, r0m, r0p), fmaf(sg, q1m, q1p), fmaf(sg, q2m, q2p), trl + k * (L + 1));
+    }
+    if constexpr (P::NP % 2 == 0) single_point(P::NP / 2, -1.f);
+
+    // publish the spectra (step E input); the even lane holds every t = 0 term
+    float* D = X1 + (node * P::UNITS + u) * P::DS;
+    const float a0p = swap_pair(Pc0[0]);
+    float zslot = 0.f;
+    if constexpr (SPIN) {
+        const float dlp = swap_pair(dl), epp = swap_pair(ep);
+        Q0[0] = fmaf(-0.5f * P::NP, fmaf(dl, dlp, ep * epp), Q0[0]);
+        const float sP1 = 1.41421356237309505f * Q1[0];
+        const float sP2 = 1.41421356237309505f * Q2[0];
+        const float sP4 = -static_cast<float>(P::NP) * fmaf(dlp, Pc0[0], dl * a0p);
+        const float sP3 = static_cast<float>(P::NP) * fmaf(epp, Pc0[0], ep * a0p);
+        const float v0 = 0.5f * (sP1 + sP4), v1 = 0.5f * (sP3 + sP2);
+        const float v2 = 0.5f * (sP1 - sP4), v3 = 0.5f * (sP3 - sP2);
+        const float* m0 = g + Y.m0;
+        const float zp = fmaf(m0[0], v0, fmaf(m0[1], v1, fmaf(m0[2], v2, m0[3] * v3)));
+        const float zm = fmaf(m0[4], v0, fmaf(m0[5], v1, fmaf(m0[6], v2, m0[7] * v3)));
+        const float zm_even = swap_pair(zm);  // all lanes active: DPP reads the even lane
+        zslot = sub ? zm_even : zp;
+    }
+    float b[L + 1];
+#pragma unroll
+    for (int t = 0; t <= L; ++t) b[t] = SPIN ? swap_pair(Q2[t]) : 0.f;
+    __syncthreads();  // every wave is past step (A): the input tiles are free
+    D[sub] = Q0[0];
+    if constexpr (SPIN) D[2 + sub] = zslot;
+#pragma unroll
+    for (int t = 1; t <= L; ++t) {
+        float* d = D + P::T0 + P::PER_T * (t - 1);
+        d[sub] = sg * Q0[t];
+        if constexpr (SPIN) {
+            d[2 + sub] = fmaf(sg, Q1[t], b[t]);
+            d[4 + sub] = fmaf(sg, Q1[t], -b[t]);
+        }
+    }
+    __syncthreads();
+
+    constexpr Owners<P::NG> own = assign_pair_owners<L, SPIN, P::WAVES>();
+    float* yr = YT + u * P::ST;
+#pragma unroll
+    for (int gi = 0; gi < P::NG; ++gi) {
+        if (own.owner[gi] != node) continue;
+        const int t = P::t_of(gi), kind = P::kind_of(gi);
+        float dv[P::NT];
+#pragma unroll
+        for (int j = 0; j < P::NT; ++j) dv[j] = X1[(j * P::UNITS + u) * P::DS + P::slot(gi) + sub];
+        int tab_base = Y.e0c, blk = SPIN ? BO : 0;
+        if (kind == 1) tab_base = Y.e1p, blk = 2 * BO;
+        if (kind == 2) tab_base = Y.e1m, blk = 0;
+        if (kind == 3) tab_base = Y.e1z, blk = sub ? 0 : 2 * BO;
+        const bool write = !(t == 0 && kind == 0 && sub);
+#pragma unroll
+        for (int l = P::lmin(gi); l <= L; ++l) {
+            const int toff = kind == 3 ? tab_base + l : tab_base + tri(L, t, l);
+            float acc = 0.f;
+#pragma unroll
+            for (int j = 0; j < P::NT; ++j) acc = fmaf(tab[Y.glob + j * Y.pb + toff], dv[j], acc);
+            if (write) yr[blk + l * l + l + (sub ? -t : t)] = acc;
+        }
+    }
+    __syncthreads();
+    store_tile<P::NC, P::ST>(out + u0 * P::NC, nvalid, YT, tid, P::THREADS);
+}
+
+template <int L, bool SPIN, typename TIO>
+hipError_t launch_pair(const void* x1, const void* x2, void* out, int64_t units, const float* tab,
+                       hipStream_t stream) {
+    using P = PairShape<L, SPIN>;
+    const int64_t blocks = (units + P::UNITS - 1) / P::UNITS;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((spingtp_fwd_pair_kernel<L, SPIN, TIO>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(P::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
+                       static_cast<TIO*>(out), units, tab);
+    return hipGetLastError();
+}
+
 template <int L1, int L2, int LO, bool SPIN, typename TIO>
 hipError_t launch(const void* x1, const void* x2, void* out, int64_t units, const float* tab, hipStream_t stream) {
     using S = Shape<L1, L2, LO, SPIN>;
@@ -505,12 +759,22 @@ constexpr Registered reg() {
 
 #define SPINGTP_REG(L1, L2, LO, SPIN) reg<L1, L2, LO, SPIN, float>(), reg<L1, L2, LO, SPIN, uint16_t>()
 
+template <int L, bool SPIN, typename TIO>
+constexpr Registered reg_pair() {
+    using P = PairShape<L, SPIN>;
+    return Registered{L, L, L, SPIN ? 1 : 0, sizeof(TIO) == 4 ? 0 : 1,
+                      KernelEntry{P::WAVES, P::UNITS, static_cast<int>(P::LDS_FLOATS * sizeof(float)), 2,
+                                  &launch_pair<L, SPIN, TIO>}};
+}
+#define SPINGTP_REG_PAIR(L, SPIN) reg_pair<L, SPIN, float>(), reg_pair<L, SPIN, uint16_t>()
+
 const Registered kRegistry[] = {
     SPINGTP_REG(0, 0, 0, false), SPINGTP_REG(1, 1, 1, false), SPINGTP_REG(2, 2, 2, false),
     SPINGTP_REG(3, 3, 3, false), SPINGTP_REG(4, 4, 4, false), SPINGTP_REG(6, 6, 6, false),
     SPINGTP_REG(1, 1, 1, true),  SPINGTP_REG(2, 2, 2, true),  SPINGTP_REG(3, 3, 3, true),
     SPINGTP_REG(4, 4, 4, true),  SPINGTP_REG(5, 5, 5, true),  SPINGTP_REG(6, 6, 6, true),
-    SPINGTP_REG(1, 3, 3, true),  SPINGTP_REG(2, 1, 3, true),
+    SPINGTP_REG(1, 3, 3, true),  SPINGTP_REG(2, 1, 3, true),  SPINGTP_REG(8, 8, 8, false),
+    SPINGTP_REG_PAIR(7, true),   SPINGTP_REG_PAIR(8, true),
 };
 
 }  // namespace

@@ -61,14 +61,14 @@ def sample_units(U, n_random, seed):
     return np.unique(np.concatenate([head, tail, rnd]))
 
 
-@pytest.mark.parametrize("L", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("L", [1, 2, 3, 4, 5, 6, 7, 8])
 @pytest.mark.parametrize("basis", [0, 1])
 def test_ragged_spin_shapes(L, basis):
     # 37 * 3 = 111 units: one full 64-unit tile and a ragged tail of 47
     run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=L)
 
 
-@pytest.mark.parametrize("L", [0, 1, 2, 3, 4, 6])
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 4, 6, 8])
 def test_ragged_scalar_shapes(L):
     run_and_compare(L, L, L, (0,), 29, 5, "fp32", 0, seed=10 + L)
 
@@ -78,7 +78,7 @@ def test_mixed_degrees(L1, L2, LO):
     run_and_compare(L1, L2, LO, S3, 50, 7, "fp32", 0, seed=20 + L1)
 
 
-@pytest.mark.parametrize("L", [2, 4, 6])
+@pytest.mark.parametrize("L", [2, 4, 6, 8])
 def test_bf16_small(L):
     run_and_compare(L, L, L, S3, 45, 6, "bf16", 0, seed=30 + L)
 
@@ -92,10 +92,12 @@ def test_small_workload_all_units():
     assert rel_l2(y.double().cpu().numpy(), ref) <= 1e-5
 
 
-@pytest.mark.parametrize("name,dtype", [("molecule", "fp32"), ("organic", "fp32"), ("organic", "bf16")])
-def test_full_size_sampled(name, dtype):
-    print(f"[parity] full-size {name} {dtype}", flush=True)
-    x1, x2, m = workloads.make_pair(name, dtype=dtype, device="cuda")
+@pytest.mark.parametrize("name,dtype,L", [("molecule", "fp32", None), ("organic", "fp32", None),
+                                          ("organic", "bf16", None), ("catalyst", "bf16", None),
+                                          ("sweep", "fp32", 2), ("sweep", "fp32", 4), ("sweep", "fp32", 8)])
+def test_full_size_sampled(name, dtype, L):
+    print(f"[parity] full-size {name} {dtype} L={L}", flush=True)
+    x1, x2, m = workloads.make_pair(name, dtype=dtype, L=L, device="cuda")
     L, U = m["L"], m["N"] * m["C"]
     plan = Plan(L, L, L, S3, dtype)
     y = plan.forward(x1, x2)
