@@ -554,49 +554,25 @@ constexpr Owners<PairShape<L, SPIN>::NG> assign_pair_owners() {
     return o;
 }
 
-template <int L, bool SPIN, typename TIO>
-__global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pair_kernel(
-    const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units,
-    const float* __restrict__ tab) {
-    using P = PairShape<L, SPIN>;
-    constexpr Layout Y = P::Y;
+// Steps (A)-(D) of one unit at one node for the lane pair (see above).  On
+// return Q0/Q1/Q2 hold the exchanged slot values of this lane:
+//   Q0[t]: R0c[t] (even lane) or -R0s[t] (odd lane), t >= 1; Q0[0] = R0c[0]
+//   Q1[t]: P1c+P2s (even) or P2c-P1s (odd);  Q2[t]: P1c-P2s (even) or -P2c-P1s (odd)
+//   zslot: Z+ (even lane) or Z- (odd lane), the m3 = 0, |s3| = 1 sums.
+template <int L, bool SPIN>
+__device__ __forceinline__ void pair_spectra(const float* xr, const float* __restrict__ tb,
+                                             const float* __restrict__ g, const float* trl, int sub,
+                                             float (&Q0)[L + 1], float (&Q1)[L + 1], float (&Q2)[L + 1],
+                                             float& zslot) {
+    constexpr Layout Y = make_layout(L, L, L);
     constexpr int TM1 = Y.TM + 1;
-    constexpr int BO = (L + 1) * (L + 1);
-    __shared__ float lds[P::LDS_FLOATS];
-    float* X1 = lds;
-    float* X2 = X1 + P::UNITS * P::ST;
-    float* YT = lds + P::REGION;
-    float* TR = YT + P::UNITS * P::ST;
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int u = lane >> 1;
-    const int sub = lane & 1;
-    const int node = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t u0 = static_cast<int64_t>(blockIdx.x) * P::UNITS;
-    const int nvalid = static_cast<int>(units - u0 < P::UNITS ? units - u0 : P::UNITS);
-    const float* __restrict__ g = tab;
-
-    for (int i = tid; i < P::UNITS * P::ST; i += P::THREADS) YT[i] = 0.f;
-    for (int i = tid; i < P::TRIG; i += P::THREADS) {
-        const int sb = i / (P::NP * (L + 1));
-        const int r = i - sb * (P::NP * (L + 1));
-        const int k = r / (L + 1), t = r - k * (L + 1);
-        TR[i] = g[(sb ? Y.sinT : Y.cosT) + k * TM1 + t];
-    }
-    load_tile<P::NC, P::ST>(x1 + u0 * P::NC, nvalid, X1, tid, P::THREADS);
-    load_tile<P::NC, P::ST>(x2 + u0 * P::NC, nvalid, X2, tid, P::THREADS);
-    __syncthreads();
-
-    const float* __restrict__ tb = tab + Y.glob + node * Y.pb;
+    constexpr int NP = Y.NP;
+    constexpr int KP = (NP - 1) / 2;
     float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
-    coef_to_theta_fourier<L, L, SPIN>((sub ? X2 : X1) + u * P::ST, tb, g + Y.n0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2,
-                                      dl, ep);
+    coef_to_theta_fourier<L, L, SPIN>(xr, tb, g + Y.n0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
     const float sg = sub ? -1.f : 1.f;
-    const float* trl = TR + sub * (P::NP * (L + 1));
 
     // accumulators: cosine spectra on the even lane, sine spectra on the odd lane
-    float Q0[L + 1], Q1[L + 1], Q2[L + 1];
 #pragma unroll
     for (int t = 0; t <= L; ++t) Q0[t] = Q1[t] = Q2[t] = 0.f;
 
@@ -632,7 +608,7 @@ __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pai
     };
     single_point(0, 1.f);
 #pragma unroll 1
-    for (int k = 1; k <= P::KP; ++k) {
+    for (int k = 1; k <= KP; ++k) {
         const float* __restrict__ cs = g + Y.cosT + k * TM1;
         const float* __restrict__ sn = g + Y.sinT + k * TM1;
         float o0p, o0m, o1p = 0.f, o1m = 0.f, o2p = 0.f, o2m = 0.f;
@@ -656,19 +632,18 @@ __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pai
         // even lane: sums (cosine), odd lane: differences (sine)
         accumulate(fmaf(sg, r0m, r0p), fmaf(sg, q1m, q1p), fmaf(sg, q2m, q2p), trl + k * (L + 1));
     }
-    if constexpr (P::NP % 2 == 0) single_point(P::NP / 2, -1.f);
+    if constexpr (NP % 2 == 0) single_point(NP / 2, -1.f);
 
-    // publish the spectra (step E input); the even lane holds every t = 0 term
-    float* D = X1 + (node * P::UNITS + u) * P::DS;
-    const float a0p = swap_pair(Pc0[0]);
-    float zslot = 0.f;
+    // t = 0 terms (valid on the even lane, which holds input 1 and every cosine spectrum)
+    zslot = 0.f;
     if constexpr (SPIN) {
+        const float a0p = swap_pair(Pc0[0]);
         const float dlp = swap_pair(dl), epp = swap_pair(ep);
-        Q0[0] = fmaf(-0.5f * P::NP, fmaf(dl, dlp, ep * epp), Q0[0]);
+        Q0[0] = fmaf(-0.5f * NP, fmaf(dl, dlp, ep * epp), Q0[0]);
         const float sP1 = 1.41421356237309505f * Q1[0];
         const float sP2 = 1.41421356237309505f * Q2[0];
-        const float sP4 = -static_cast<float>(P::NP) * fmaf(dlp, Pc0[0], dl * a0p);
-        const float sP3 = static_cast<float>(P::NP) * fmaf(epp, Pc0[0], ep * a0p);
+        const float sP4 = -static_cast<float>(NP) * fmaf(dlp, Pc0[0], dl * a0p);
+        const float sP3 = static_cast<float>(NP) * fmaf(epp, Pc0[0], ep * a0p);
         const float v0 = 0.5f * (sP1 + sP4), v1 = 0.5f * (sP3 + sP2);
         const float v2 = 0.5f * (sP1 - sP4), v3 = 0.5f * (sP3 - sP2);
         const float* m0 = g + Y.m0;
@@ -676,22 +651,76 @@ __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pai
         const float zm = fmaf(m0[4], v0, fmaf(m0[5], v1, fmaf(m0[6], v2, m0[7] * v3)));
         const float zm_even = swap_pair(zm);  // all lanes active: DPP reads the even lane
         zslot = sub ? zm_even : zp;
-    }
-    float b[L + 1];
+        // cross terms: the even lane needs P2s, the odd lane P2c
 #pragma unroll
-    for (int t = 0; t <= L; ++t) b[t] = SPIN ? swap_pair(Q2[t]) : 0.f;
-    __syncthreads();  // every wave is past step (A): the input tiles are free
+        for (int t = 1; t <= L; ++t) {
+            const float b = swap_pair(Q2[t]);
+            const float p1 = Q1[t];
+            Q1[t] = fmaf(sg, p1, b);
+            Q2[t] = fmaf(sg, p1, -b);
+        }
+    }
+#pragma unroll
+    for (int t = 1; t <= L; ++t) Q0[t] *= sg;
+}
+
+// Writes one unit's slot record (layout of PairShape) for this lane.
+template <int L, bool SPIN>
+__device__ __forceinline__ void pair_publish(float* D, int sub, const float (&Q0)[L + 1], const float (&Q1)[L + 1],
+                                             const float (&Q2)[L + 1], float zslot) {
+    constexpr int T0 = SPIN ? 4 : 2, PER_T = SPIN ? 6 : 2;
     D[sub] = Q0[0];
     if constexpr (SPIN) D[2 + sub] = zslot;
 #pragma unroll
     for (int t = 1; t <= L; ++t) {
-        float* d = D + P::T0 + P::PER_T * (t - 1);
-        d[sub] = sg * Q0[t];
+        float* d = D + T0 + PER_T * (t - 1);
+        d[sub] = Q0[t];
         if constexpr (SPIN) {
-            d[2 + sub] = fmaf(sg, Q1[t], b[t]);
-            d[4 + sub] = fmaf(sg, Q1[t], -b[t]);
+            d[2 + sub] = Q1[t];
+            d[4 + sub] = Q2[t];
         }
     }
+}
+
+template <int L, bool SPIN, typename TIO>
+__global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pair_kernel(
+    const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units,
+    const float* __restrict__ tab) {
+    using P = PairShape<L, SPIN>;
+    constexpr Layout Y = P::Y;
+    constexpr int TM1 = Y.TM + 1;
+    constexpr int BO = (L + 1) * (L + 1);
+    __shared__ float lds[P::LDS_FLOATS];
+    float* X1 = lds;
+    float* X2 = X1 + P::UNITS * P::ST;
+    float* YT = lds + P::REGION;
+    float* TR = YT + P::UNITS * P::ST;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int u = lane >> 1;
+    const int sub = lane & 1;
+    const int node = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t u0 = static_cast<int64_t>(blockIdx.x) * P::UNITS;
+    const int nvalid = static_cast<int>(units - u0 < P::UNITS ? units - u0 : P::UNITS);
+    const float* __restrict__ g = tab;
+
+    for (int i = tid; i < P::UNITS * P::ST; i += P::THREADS) YT[i] = 0.f;
+    for (int i = tid; i < P::TRIG; i += P::THREADS) {
+        const int sb = i / (P::NP * (L + 1));
+        const int r = i - sb * (P::NP * (L + 1));
+        const int k = r / (L + 1), t = r - k * (L + 1);
+        TR[i] = g[(sb ? Y.sinT : Y.cosT) + k * TM1 + t];
+    }
+    load_tile<P::NC, P::ST>(x1 + u0 * P::NC, nvalid, X1, tid, P::THREADS);
+    load_tile<P::NC, P::ST>(x2 + u0 * P::NC, nvalid, X2, tid, P::THREADS);
+    __syncthreads();
+
+    const float* __restrict__ tb = tab + Y.glob + node * Y.pb;
+    float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
+    pair_spectra<L, SPIN>((sub ? X2 : X1) + u * P::ST, tb, g, TR + sub * (P::NP * (L + 1)), sub, Q0, Q1, Q2, zslot);
+    __syncthreads();  // every wave is past step (A): the input tiles are free
+    pair_publish<L, SPIN>(X1 + (node * P::UNITS + u) * P::DS, sub, Q0, Q1, Q2, zslot);
     __syncthreads();
 
     constexpr Owners<P::NG> own = assign_pair_owners<L, SPIN, P::WAVES>();
@@ -733,6 +762,123 @@ hipError_t launch_pair(const void* x1, const void* x2, void* out, int64_t units,
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Large-degree kernel (L = 9..16, fp32 I/O).  More nodes than a workgroup has
+// waves, and 32-unit input tiles that no longer fit in LDS: the nodes are
+// processed in rounds of W waves, each lane pair reads its unit's input rows
+// straight from global memory (cached in L1/L2), the spectra of one round are
+// exchanged in LDS, and every output group's owner lane accumulates the
+// round's contribution into the output row (written in round 0, then read,
+// added and written by the same lane in later rounds: ordered, deterministic).
+// ---------------------------------------------------------------------------
+template <int L, bool SPIN, int W>
+struct BigShape {
+    using PS = PairShape<L, SPIN>;
+    static constexpr Layout Y = make_layout(L, L, L);
+    static constexpr int NC = PS::NC;
+    static constexpr int NT = Y.NT;
+    static constexpr int NP = Y.NP;
+    static constexpr int UNITS = 32;
+    static constexpr int WAVES = W;
+    static constexpr int THREADS = 64 * W;
+    static constexpr int ROUNDS = (NT + W - 1) / W;
+    static constexpr int DF = W * UNITS * PS::DS;
+    static constexpr int TRIG = 2 * NP * (L + 1);
+    static constexpr int LDS_FLOATS = DF + TRIG;
+};
+
+template <int L, bool SPIN, int W>
+__global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_big_kernel(
+    const float* __restrict__ x1, const float* __restrict__ x2, float* __restrict__ out, int64_t units,
+    const float* __restrict__ tab) {
+    using B = BigShape<L, SPIN, W>;
+    using P = typename B::PS;
+    constexpr Layout Y = B::Y;
+    constexpr int TM1 = Y.TM + 1;
+    constexpr int BO = (L + 1) * (L + 1);
+    __shared__ float lds[B::LDS_FLOATS];
+    float* D = lds;
+    float* TR = lds + B::DF;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int u = lane >> 1;
+    const int sub = lane & 1;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t u0 = static_cast<int64_t>(blockIdx.x) * B::UNITS;
+    const int nvalid = static_cast<int>(units - u0 < B::UNITS ? units - u0 : B::UNITS);
+    const bool valid = u < nvalid;
+    const int64_t row = u0 + (valid ? u : 0);  // invalid lanes compute on a valid row, store nothing
+    const float* g = tab;
+    const float* xr = (sub ? x2 : x1) + row * B::NC;
+    float* orow = out + row * B::NC;
+
+    for (int i = tid; i < B::TRIG; i += B::THREADS) {
+        const int sb = i / (B::NP * (L + 1));
+        const int r = i - sb * (B::NP * (L + 1));
+        const int k = r / (L + 1), t = r - k * (L + 1);
+        TR[i] = g[(sb ? Y.sinT : Y.cosT) + k * TM1 + t];
+    }
+    if constexpr (SPIN) {
+        if (wave == 0 && valid) orow[sub ? 2 * BO : 0] = 0.f;  // l = 0 slots of the |s| = 1 blocks
+    }
+    __syncthreads();
+
+    constexpr Owners<P::NG> own = assign_pair_owners<L, SPIN, W>();
+#pragma unroll 1
+    for (int r = 0; r < B::ROUNDS; ++r) {
+        const int node = r * W + wave;
+        const int nr = (B::NT - r * W) < W ? (B::NT - r * W) : W;
+        if (node < B::NT) {
+            float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
+            pair_spectra<L, SPIN>(xr, tab + Y.glob + node * Y.pb, g, TR + sub * (B::NP * (L + 1)), sub, Q0, Q1,
+                                  Q2, zslot);
+            pair_publish<L, SPIN>(D + (wave * B::UNITS + u) * P::DS, sub, Q0, Q1, Q2, zslot);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int gi = 0; gi < P::NG; ++gi) {
+            if (own.owner[gi] != wave) continue;
+            const int t = P::t_of(gi), kind = P::kind_of(gi);
+            int tab_base = Y.e0c, blk = SPIN ? BO : 0;
+            if (kind == 1) tab_base = Y.e1p, blk = 2 * BO;
+            if (kind == 2) tab_base = Y.e1m, blk = 0;
+            if (kind == 3) tab_base = Y.e1z, blk = sub ? 0 : 2 * BO;
+            float acc[L + 1];
+#pragma unroll
+            for (int l = 0; l <= L; ++l) acc[l] = 0.f;
+#pragma unroll 1
+            for (int jj = 0; jj < nr; ++jj) {
+                const float d = D[(jj * B::UNITS + u) * P::DS + P::slot(gi) + sub];
+                const float* te = tab + Y.glob + (r * W + jj) * Y.pb;
+#pragma unroll
+                for (int l = P::lmin(gi); l <= L; ++l)
+                    acc[l] = fmaf(te[kind == 3 ? tab_base + l : tab_base + tri(L, t, l)], d, acc[l]);
+            }
+            if (valid && !(t == 0 && kind == 0 && sub)) {
+#pragma unroll
+                for (int l = P::lmin(gi); l <= L; ++l) {
+                    float* o = orow + blk + l * l + l + (sub ? -t : t);
+                    *o = (r == 0) ? acc[l] : *o + acc[l];
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+template <int L, bool SPIN, int W>
+hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, const float* tab,
+                      hipStream_t stream) {
+    using B = BigShape<L, SPIN, W>;
+    const int64_t blocks = (units + B::UNITS - 1) / B::UNITS;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W>), dim3(static_cast<unsigned>(blocks)), dim3(B::THREADS),
+                       0, stream, static_cast<const float*>(x1), static_cast<const float*>(x2),
+                       static_cast<float*>(out), units, tab);
+    return hipGetLastError();
+}
+
 template <int L1, int L2, int LO, bool SPIN, typename TIO>
 hipError_t launch(const void* x1, const void* x2, void* out, int64_t units, const float* tab, hipStream_t stream) {
     using S = Shape<L1, L2, LO, SPIN>;
@@ -768,13 +914,25 @@ constexpr Registered reg_pair() {
 }
 #define SPINGTP_REG_PAIR(L, SPIN) reg_pair<L, SPIN, float>(), reg_pair<L, SPIN, uint16_t>()
 
+template <int L, bool SPIN, int W>
+constexpr Registered reg_big() {
+    using B = BigShape<L, SPIN, W>;
+    return Registered{L, L, L, SPIN ? 1 : 0, 0,
+                      KernelEntry{B::WAVES, B::UNITS, static_cast<int>(B::LDS_FLOATS * sizeof(float)), 3,
+                                  &launch_big<L, SPIN, W>}};
+}
+#define SPINGTP_REG_BIG(L) reg_big<L, true, 5>(), reg_big<L, false, 5>()
+
 const Registered kRegistry[] = {
     SPINGTP_REG(0, 0, 0, false), SPINGTP_REG(1, 1, 1, false), SPINGTP_REG(2, 2, 2, false),
     SPINGTP_REG(3, 3, 3, false), SPINGTP_REG(4, 4, 4, false), SPINGTP_REG(6, 6, 6, false),
     SPINGTP_REG(1, 1, 1, true),  SPINGTP_REG(2, 2, 2, true),  SPINGTP_REG(3, 3, 3, true),
     SPINGTP_REG(4, 4, 4, true),  SPINGTP_REG(5, 5, 5, true),  SPINGTP_REG(6, 6, 6, true),
     SPINGTP_REG(1, 3, 3, true),  SPINGTP_REG(2, 1, 3, true),  SPINGTP_REG(8, 8, 8, false),
-    SPINGTP_REG_PAIR(7, true),   SPINGTP_REG_PAIR(8, true),
+    SPINGTP_REG_PAIR(7, true),   SPINGTP_REG_PAIR(8, true),   SPINGTP_REG_BIG(9),
+    SPINGTP_REG_BIG(10),         SPINGTP_REG_BIG(11),         SPINGTP_REG_BIG(12),
+    SPINGTP_REG_BIG(13),         SPINGTP_REG_BIG(14),         SPINGTP_REG_BIG(15),
+    SPINGTP_REG_BIG(16),
 };
 
 }  // namespace

@@ -175,7 +175,7 @@ def emulate_kernel(x1, x2, L1, L2, LO, spin, basis):
 @pytest.mark.parametrize("L1,L2,LO,spin,basis", [
     (2, 2, 2, True, 0), (2, 2, 2, True, 1), (1, 1, 1, True, 0), (3, 2, 4, True, 0), (2, 3, 1, True, 1),
     (4, 4, 4, True, 0), (6, 6, 6, True, 0), (2, 2, 2, False, 0), (3, 1, 2, False, 0), (0, 0, 0, False, 0),
-    (1, 3, 3, True, 0), (8, 8, 8, True, 0),
+    (1, 3, 3, True, 0), (8, 8, 8, True, 0), (12, 12, 12, True, 1),
 ])
 def test_plan_tables_reproduce_oracle(built_library, L1, L2, LO, spin, basis):
     S = (-1, 0, 1) if spin else (0,)

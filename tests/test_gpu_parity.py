@@ -34,6 +34,7 @@ def rel_l2(y, ref):
 
 
 def run_and_compare(L1, L2, LO, spins, N, C, dtype="fp32", basis=0, seed=0, scale="unit", units=None):
+    from oracle.spingtp import _cached_tensor
     print(f"[parity] L=({L1},{L2},{LO}) spins={spins} N={N} C={C} {dtype} basis={basis}", flush=True)
     x1 = workloads.draw(L1, N, C, 7000 + seed, dtype, spins, scale, "cuda")
     x2 = workloads.draw(L2, N, C, 8000 + seed, dtype, spins, scale, "cuda")
@@ -46,7 +47,7 @@ def run_and_compare(L1, L2, LO, spins, N, C, dtype="fp32", basis=0, seed=0, scal
     a = x1.view(U, -1)[ti].double().cpu().numpy()
     b = x2.view(U, -1)[ti].double().cpu().numpy()
     g = y.view(U, -1)[ti].double().cpu().numpy()
-    ref = oracle.RealGauntTensor(L1, L2, LO, spins, basis).apply(a, b).reshape(len(idx), -1)
+    ref = _cached_tensor(L1, L2, LO, tuple(spins), basis).apply(a, b).reshape(len(idx), -1)
     err = rel_l2(g, ref)
     print(f"[parity]   rel_l2={err:.3e}", flush=True)
     assert err <= TOL[dtype], err
@@ -68,7 +69,13 @@ def test_ragged_spin_shapes(L, basis):
     run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=L)
 
 
-@pytest.mark.parametrize("L", [0, 1, 2, 3, 4, 6, 8])
+@pytest.mark.parametrize("L,basis", [(9, 0), (9, 1), (12, 0), (16, 0)])
+def test_ragged_large_degree(L, basis):
+    # 37 * 3 = 111 units: three full 32-unit tiles and a ragged tail of 15
+    run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=L)
+
+
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 4, 6, 8, 12])
 def test_ragged_scalar_shapes(L):
     run_and_compare(L, L, L, (0,), 29, 5, "fp32", 0, seed=10 + L)
 
@@ -94,7 +101,8 @@ def test_small_workload_all_units():
 
 @pytest.mark.parametrize("name,dtype,L", [("molecule", "fp32", None), ("organic", "fp32", None),
                                           ("organic", "bf16", None), ("catalyst", "bf16", None),
-                                          ("sweep", "fp32", 2), ("sweep", "fp32", 4), ("sweep", "fp32", 8)])
+                                          ("sweep", "fp32", 2), ("sweep", "fp32", 4), ("sweep", "fp32", 8),
+                                          ("sweep", "fp32", 12), ("sweep", "fp32", 16)])
 def test_full_size_sampled(name, dtype, L):
     print(f"[parity] full-size {name} {dtype} L={L}", flush=True)
     x1, x2, m = workloads.make_pair(name, dtype=dtype, L=L, device="cuda")
@@ -102,7 +110,7 @@ def test_full_size_sampled(name, dtype, L):
     plan = Plan(L, L, L, S3, dtype)
     y = plan.forward(x1, x2)
     torch.cuda.synchronize()
-    idx = sample_units(U, 8192, 99)
+    idx = sample_units(U, 8192 if L <= 8 else 1024, 99)
     ti = torch.as_tensor(idx, device="cuda")
     a = x1.view(U, -1)[ti].double().cpu().numpy()
     b = x2.view(U, -1)[ti].double().cpu().numpy()
