@@ -73,10 +73,14 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload, dtype, units):
+def profile_tag(workload, dtype, L):
+    return f"{workload}_L{L}_{dtype}" if workload == "sweep" else f"{workload}_{dtype}"
+
+
+def measured_traffic(workload, dtype, units, L):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it
     was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"traffic_spingtp_fwd_{workload}_{dtype}.json")
+    path = os.path.join(ROOT, "profiles", f"traffic_spingtp_fwd_{profile_tag(workload, dtype, L)}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -182,7 +186,9 @@ def main():
     flops_unit = route_flops(L, L, L, True)
     achieved_tflops = flops_unit * U / (avg_launch_ms / 1e3) / 1e12
     bytes_unit = hbm_bytes_per_unit(L, L, L, args.dtype)
-    traffic = measured_traffic(meta["workload"], args.dtype, U)
+    traffic = measured_traffic(meta["workload"], args.dtype, U, L)
+    kinfo = plan.kernel_info()
+    kname = {1: "spingtp_fwd_kernel", 2: "spingtp_fwd_pair_kernel", 3: "spingtp_fwd_big_kernel"}[kinfo["family"]]
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib * (1 << 20) // 4
@@ -233,7 +239,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,
             "traffic": traffic,
-            "kernel": "spingtp_fwd_kernel",
+            "kernel": kname,
             "avg_launch_ms": avg_launch_ms,
             "flops_per_unit": flops_unit,
             "hbm_bytes_per_unit": bytes_unit,
