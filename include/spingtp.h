@@ -114,9 +114,26 @@ spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spi
                                         size_t* n_tables, int* dims);
 
 /*
+ * The explicit real bilinear tensor of the operation, dense, in float64, on the host
+ * (no GPU needed): out[k3] = sum_{k1,k2} T[k1][k2][k3] x1[k1] x2[k2] with
+ * k1 < NC1 = n_spins (L1+1)^2, k2 < NC2, k3 < NCO in the layout above.  T is built
+ * from the spin-weighted Gaunt coefficients G (Sec. 3.2 eq. generalized_gaunt, by
+ * exact Gauss-Legendre quadrature of triple SWSH products) mapped through the real
+ * basis (App. C): T = Re(conj(Q3) G Q1 Q2).  It is the direct (Clebsch-Gordan
+ * style) form of the product, used as the O(L^6) comparator of the benchmark and
+ * for inspection; the forward path never uses it.  Same argument rules as
+ * spingtp_plan_create.  Writes min(capacity, NC1 NC2 NCO) doubles to `tensor`
+ * (may be NULL when capacity is 0) and the full count to *count.
+ */
+spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                         unsigned flags, double* tensor, size_t capacity, size_t* count);
+
+/*
  * Describe the kernel a plan launches: writes the waves per workgroup, units per
- * workgroup, LDS bytes per workgroup and a kernel-family id (1 = register-tiled
- * fixed-degree kernel) to the 4 ints of `info`.
+ * workgroup, LDS bytes per workgroup and a kernel-family id to the 4 ints of
+ * `info`.  Families: 1 = one lane per unit, one wave per quadrature node (L <= 6
+ * and the mixed-degree shapes); 2 = lane pairs per unit (L = 7, 8); 3 = lane
+ * pairs with the nodes processed in rounds (L = 9..16, fp32 only).
  */
 spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info);
 

@@ -9,7 +9,7 @@ SPINGTP_OK = 0
 STATUS_NAMES = {0: "OK", 1: "ERR_INVALID_ARG", 2: "ERR_UNSUPPORTED", 3: "ERR_OUT_OF_MEMORY",
                 4: "ERR_HIP", 5: "ERR_INTERNAL"}
 EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "spingtp_status_string",
-            "spingtp_plan_tables_host", "spingtp_plan_kernel_info")
+            "spingtp_plan_tables_host", "spingtp_plan_kernel_info", "spingtp_dense_tensor_host")
 
 _lib = None
 
@@ -42,6 +42,10 @@ def lib() -> ctypes.CDLL:
                                                ctypes.c_uint, ctypes.POINTER(ctypes.c_double), ctypes.c_size_t,
                                                ctypes.POINTER(ctypes.c_size_t), c_int_p]
         L.spingtp_plan_tables_host.restype = ctypes.c_int
+        L.spingtp_dense_tensor_host.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, c_int_p, ctypes.c_int,
+                                                ctypes.c_uint, ctypes.POINTER(ctypes.c_double), ctypes.c_size_t,
+                                                ctypes.POINTER(ctypes.c_size_t)]
+        L.spingtp_dense_tensor_host.restype = ctypes.c_int
         L.spingtp_plan_kernel_info.argtypes = [ctypes.c_void_p, c_int_p]
         L.spingtp_plan_kernel_info.restype = ctypes.c_int
         _lib = L

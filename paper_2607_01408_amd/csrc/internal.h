@@ -28,6 +28,10 @@ const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype)
 // self-check.  spin_mode: 0 = {0}, 1 = {-1, 0, +1}.
 bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::vector<double>& out);
 
+// Dense real tensor of the operation (see spingtp_dense_tensor_host), float64.
+void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                        std::vector<double>& T);
+
 }  // namespace spingtp
 
 struct spingtp_plan_s {

@@ -201,6 +201,110 @@ bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::ve
     return true;
 }
 
+// Dense real tensor T[k1][k2][k3] = Re sum conj(Q3) G Q1 Q2 (see spingtp.h).
+// G^{(l3,m3,s3)}_{(l1,m1,s1)(l2,m2,s2)} = 2 pi sum_j w_j Y1(theta_j) Y2(theta_j) Y3(theta_j) for
+// s3 = s1 + s2, m3 = m1 + m2 (the phi integral of the other combinations vanishes), on the
+// Gauss-Legendre rule of the plan, which is exact for these triple products.
+void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                        std::vector<double>& T) {
+    const int nb1 = (L1 + 1) * (L1 + 1), nb2 = (L2 + 1) * (L2 + 1), nbo = (LO + 1) * (LO + 1);
+    const size_t nc1 = static_cast<size_t>(n_spins) * nb1, nc2 = static_cast<size_t>(n_spins) * nb2,
+                 nco = static_cast<size_t>(n_spins) * nbo;
+    T.assign(nc1 * nc2 * nco, 0.0);
+    const Layout Y = make_layout(L1, L2, LO);
+    std::vector<double> gx, gw;
+    gauss_legendre(Y.NT, gx, gw);
+    const int LM = std::max(std::max(L1, L2), LO);
+    auto sidx = [&](int s) {
+        for (int i = 0; i < n_spins; ++i)
+            if (spins[i] == s) return i;
+        return -1;
+    };
+    // Theta tables [spin index][l][m + LM][node]
+    std::vector<double> th(static_cast<size_t>(n_spins) * (LM + 1) * (2 * LM + 1) * Y.NT, 0.0);
+    auto TH = [&](int si, int l, int m, int j) -> double& {
+        return th[((static_cast<size_t>(si) * (LM + 1) + l) * (2 * LM + 1) + (m + LM)) * Y.NT + j];
+    };
+    for (int si = 0; si < n_spins; ++si)
+        for (int l = std::abs(spins[si]); l <= LM; ++l)
+            for (int m = -l; m <= l; ++m)
+                for (int j = 0; j < Y.NT; ++j) TH(si, l, m, j) = swsh_theta(spins[si], l, m, std::acos(gx[j]));
+    // real column (sigma, l, k) -> up to two complex rows (s, m) with values (eq. real_swsh, App. C)
+    struct Ent {
+        int s, m;
+        Cplx q;
+    };
+    auto column = [&](int sigma, int k, Ent* e) -> int {
+        const double h = 1.0 / kSqrt2;
+        if (k > 0) {
+            e[0] = {sigma, k, {h, 0.0}};
+            e[1] = {-sigma, -k, {(((k + sigma) % 2) != 0 ? -h : h), 0.0}};
+            return sigma == 0 ? 2 : 2;
+        }
+        if (k < 0) {
+            const int a = -k;
+            e[0] = {sigma, a, {0.0, h}};
+            e[1] = {-sigma, k, {0.0, (((a + sigma) % 2) != 0 ? h : -h)}};
+            return 2;
+        }
+        if (sigma == 0 || flags == SPINGTP_BASIS_REAL_PAPER) {
+            e[0] = {sigma, 0, {1.0, 0.0}};
+            return 1;
+        }
+        const int sa = std::abs(sigma);
+        e[0] = {sa, 0, q_m0(flags, 1, sigma)};
+        e[1] = {-sa, 0, q_m0(flags, -1, sigma)};
+        return 2;
+    };
+    auto cmul = [](Cplx a, Cplx b) { return Cplx{a.re * b.re - a.im * b.im, a.re * b.im + a.im * b.re}; };
+    // loop over real (k1, k2) and complex expansions; G picks m3 = m1 + m2, s3 = s1 + s2
+    for (int i1 = 0; i1 < n_spins; ++i1)
+        for (int l1 = std::abs(spins[i1]); l1 <= L1; ++l1)
+            for (int k1 = -l1; k1 <= l1; ++k1) {
+                Ent e1[2];
+                const int n1 = column(spins[i1], k1, e1);
+                const size_t c1 = static_cast<size_t>(i1) * nb1 + l1 * l1 + l1 + k1;
+                for (int i2 = 0; i2 < n_spins; ++i2)
+                    for (int l2 = std::abs(spins[i2]); l2 <= L2; ++l2)
+                        for (int k2 = -l2; k2 <= l2; ++k2) {
+                            Ent e2[2];
+                            const int n2 = column(spins[i2], k2, e2);
+                            const size_t c2 = static_cast<size_t>(i2) * nb2 + l2 * l2 + l2 + k2;
+                            double* trow = T.data() + (c1 * nc2 + c2) * nco;
+                            for (int a = 0; a < n1; ++a)
+                                for (int b = 0; b < n2; ++b) {
+                                    const int s3 = e1[a].s + e2[b].s, m3 = e1[a].m + e2[b].m;
+                                    const int i3 = sidx(s3);
+                                    if (i3 < 0) continue;
+                                    const int ia = sidx(e1[a].s), ib = sidx(e2[b].s);
+                                    const Cplx qq = cmul(e1[a].q, e2[b].q);
+                                    const int l3lo = std::max(std::max(std::abs(s3), std::abs(m3)), std::abs(l1 - l2));
+                                    for (int l3 = l3lo; l3 <= std::min(LO, l1 + l2); ++l3) {
+                                        double gint = 0.0;
+                                        for (int j = 0; j < Y.NT; ++j)
+                                            gint += gw[j] * TH(ia, l1, e1[a].m, j) * TH(ib, l2, e2[b].m, j) *
+                                                    TH(i3, l3, m3, j);
+                                        gint *= 2.0 * kPi;
+                                        // output real columns k3 whose expansion contains (s3, m3)
+                                        for (int k3 = -l3; k3 <= l3; ++k3)
+                                            for (int i3r = 0; i3r < n_spins; ++i3r) {
+                                                if (std::abs(spins[i3r]) != std::abs(s3) || l3 < std::abs(spins[i3r]))
+                                                    continue;
+                                                Ent e3[2];
+                                                const int n3 = column(spins[i3r], k3, e3);
+                                                for (int c = 0; c < n3; ++c)
+                                                    if (e3[c].s == s3 && e3[c].m == m3) {
+                                                        const Cplx z = cmul(qq, Cplx{e3[c].q.re, -e3[c].q.im});
+                                                        trow[static_cast<size_t>(i3r) * nbo + l3 * l3 + l3 + k3] +=
+                                                            z.re * gint;
+                                                    }
+                                            }
+                                    }
+                                }
+                        }
+            }
+}
+
 }  // namespace spingtp
 
 namespace {
@@ -266,6 +370,29 @@ spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spi
         const spingtp::Layout Y = spingtp::make_layout(L1, L2, Lout);
         const int d[8] = {Y.NT, Y.NP, L1, L2, Lout, n_spins, Y.pb, Y.glob};
         std::memcpy(dims, d, sizeof(d));
+    }
+    return SPINGTP_OK;
+}
+
+spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                         unsigned flags, double* tensor, size_t capacity, size_t* count) {
+    int spin_mode = 0;
+    spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
+    if (st != SPINGTP_OK) return st;
+    if (count == nullptr || (capacity > 0 && tensor == nullptr)) return SPINGTP_ERR_INVALID_ARG;
+    const size_t nc1 = static_cast<size_t>(n_spins) * (L1 + 1) * (L1 + 1);
+    const size_t nc2 = static_cast<size_t>(n_spins) * (L2 + 1) * (L2 + 1);
+    const size_t nco = static_cast<size_t>(n_spins) * (Lout + 1) * (Lout + 1);
+    const size_t total = nc1 * nc2 * nco;
+    *count = total;
+    if (capacity == 0) return SPINGTP_OK;
+    try {
+        std::vector<double> T;
+        spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, flags, T);
+        const size_t n = total < capacity ? total : capacity;
+        std::memcpy(tensor, T.data(), n * sizeof(double));
+    } catch (const std::bad_alloc&) {
+        return SPINGTP_ERR_OUT_OF_MEMORY;
     }
     return SPINGTP_OK;
 }

@@ -36,6 +36,20 @@ def plan_tables_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
     return out, dict(zip(keys, list(dims)))
 
 
+def dense_tensor_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Dense float64 T[k1, k2, k3] of the operation (host only, no GPU needed)."""
+    arr, n = _spin_array(spins)
+    count = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().spingtp_dense_tensor_host(L1, L2, Lout, arr, n, basis, None, 0, ctypes.byref(count)),
+               "spingtp_dense_tensor_host")
+    T = np.zeros(count.value, dtype=np.float64)
+    _lib.check(_lib.lib().spingtp_dense_tensor_host(L1, L2, Lout, arr, n, basis,
+                                                    T.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), T.size,
+                                                    ctypes.byref(count)), "spingtp_dense_tensor_host")
+    nc = lambda L: len(spins) * (L + 1) ** 2  # noqa: E731
+    return T.reshape(nc(L1), nc(L2), nc(Lout))
+
+
 class Plan:
     """spingtp_plan_create / spingtp_forward / spingtp_plan_destroy."""
 

@@ -17,7 +17,7 @@ import pytest
 
 import oracle
 from paper_2607_01408_amd import _lib
-from paper_2607_01408_amd.spingtp import plan_tables_host
+from paper_2607_01408_amd.spingtp import dense_tensor_host, plan_tables_host
 from tests.oracle_helpers import valid_mask
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -185,3 +185,15 @@ def test_plan_tables_reproduce_oracle(built_library, L1, L2, LO, spin, basis):
     y = emulate_kernel(x1, x2, L1, L2, LO, spin, basis)
     yo = oracle.RealGauntTensor(L1, L2, LO, S, basis).apply(x1, x2).reshape(6, -1)
     assert np.abs(y - yo).max() <= 1e-12 * max(1.0, np.abs(yo).max())
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [
+    (2, 2, 2, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 1), (3, 2, 4, (-1, 0, 1), 0), (4, 4, 4, (-1, 0, 1), 1),
+    (3, 1, 2, (0,), 0), (1, 1, 1, (-1, 0, 1), 0),
+])
+def test_dense_tensor_matches_oracle(built_library, L1, L2, LO, spins, basis):
+    """The library's explicit tensor (its own quadrature, the benchmark's comparator) equals the oracle's."""
+    T = dense_tensor_host(L1, L2, LO, spins, basis)
+    To = oracle.RealGauntTensor(L1, L2, LO, spins, basis).dense()
+    assert T.shape == To.shape
+    assert np.abs(T - To).max() < 1e-13
