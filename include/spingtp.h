@@ -62,15 +62,25 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
 #define SPINGTP_BASIS_REAL_PAPER 0u
 #define SPINGTP_BASIS_REAL_M0_PAIRED 1u
 
+/* Kernel choice, OR-ed into the flags of spingtp_plan_create: use the fp32
+ * vector-ALU kernels even where a matrix-core kernel is built (family 4 below).
+ * The other entry points accept and ignore it. */
+#define SPINGTP_KERNEL_VALU 0x100u
+
 /*
  * Create a plan for degrees (L1, L2, Lout) and a spin set.
  *   0 <= L1, L2 <= 16, 0 <= Lout <= L1 + L2 (the product of degrees l1, l2 has
  *   degree <= l1 + l2, App. B proof); otherwise SPINGTP_ERR_INVALID_ARG.
  *   spins/n_spins: host array, strictly ascending and symmetric; {0} and
  *   {-1, 0, +1} are supported, other valid sets give SPINGTP_ERR_UNSUPPORTED.
- *   dtype: element type of x1, x2 and out.  bf16 plans compute in fp32 and round
- *   the output to bf16 (round to nearest even).
- *   flags: one SPINGTP_BASIS_* value.
+ *   dtype: element type of x1, x2 and out.  Arithmetic: the vector-ALU kernels
+ *   compute in fp32.  The matrix-core kernel (L1 = L2 = Lout = 6, spins
+ *   {-1, 0, +1}) runs the two phi transforms as fp16 matrix products with fp32
+ *   accumulation: for fp32 plans every operand is split into fp16 high and low
+ *   parts (three products per term, relative error near 2^-21 per term, like
+ *   fp32), for bf16 plans only the high parts are used (near 2^-11).  Every
+ *   other step is fp32.  bf16 output is rounded to nearest even.
+ *   flags: one SPINGTP_BASIS_* value, optionally OR SPINGTP_KERNEL_VALU.
  * The plan tables (Gauss-Legendre weights and SWSH values on the quadrature
  * nodes, trigonometric tables, real-basis mixing constants) are computed in
  * float64 on the host, rounded to fp32 and copied synchronously to the current
@@ -133,7 +143,9 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
  * workgroup, LDS bytes per workgroup and a kernel-family id to the 4 ints of
  * `info`.  Families: 1 = one lane per unit, one wave per quadrature node (L <= 6
  * and the mixed-degree shapes); 2 = lane pairs per unit (L = 7, 8); 3 = lane
- * pairs with the nodes processed in rounds (L = 9..16, fp32 only).
+ * pairs with the nodes processed in rounds (L = 9..16, fp32 only); 4 = the
+ * matrix-core kernel (L1 = L2 = Lout = 6, spins {-1, 0, +1}; the default there
+ * unless SPINGTP_KERNEL_VALU is given).
  */
 spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info);
 

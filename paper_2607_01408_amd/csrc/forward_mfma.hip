@@ -1,0 +1,463 @@
+// Matrix-core SpinGTP forward kernel for L1 = L2 = Lout = L, spins {-1, 0, +1},
+// on gfx950 (CDNA4).
+//
+// The five steps are those of the vector-ALU kernel (paper App. B, proof of the
+// runtime proposition; Sec. 3.2 eq. generalized_gaunt): (A) theta-Fourier form
+// of the six real trigonometric polynomials (three per input) at a Gauss node,
+// (B) synthesis at the n_phi uniform points, (C) the three product combinations,
+// (D) analysis onto cos/sin(t phi), (E) projection onto the output coefficients
+// with the node's weight.  Steps (B) and (D) -- two thirds of the arithmetic --
+// are contractions with tables shared by every unit, so they run as fp16
+// matrix-core products with fp32 accumulation, the unit index being the N
+// dimension of v_mfma_f32_32x32x16_f16:
+//   (B)  field[point, unit] = TB[point, kappa] * F[kappa, unit]
+//   (D)  spec[row, unit]    = TD[row, point]   * H[point, unit]
+// kappa runs over the 16 coefficient slots of one polynomial (cos t = 0..L at
+// 0..7, sin t at 8 + t); rows of (D) are cos/sin spectra t' = 0..L.
+//
+// Precision.  For fp32 I/O every operand is split into fp16 high and low parts
+// and each product is hi*hi + hi*lo + lo*hi (each exact in the fp32 accumulator),
+// which leaves a relative error near 2^-21 per term -- fp32-like.  bf16 I/O uses
+// the high parts only (2^-11).  fp16 has a narrow exponent range, so each input
+// row of every unit is first scaled by a power of two that puts its largest
+// magnitude in [1/2, 1); by Cauchy-Schwarz every field is then bounded by
+// sqrt(sum_lm |Y_lm|^2 * n_coef) < 64 and every product combination by < 2^14,
+// well inside fp16, and the output is scaled back exactly.
+//
+// Work mapping.  A workgroup owns 64 units and has four waves (one per SIMD, two
+// workgroups per CU).  Wave w takes units 32 (w & 1) .. +31 and the Gauss nodes
+// j = (w >> 1) + 2k.  In a wave, lane u (< 32) works on input 1 and lane u + 32
+// on input 2 of unit u in step (A); a half-wave swap (v_permlane32_swap) then
+// turns the two halves into the (B) operands, whose K layout puts kappa 0..7 in
+// lanes 0..31 and 8..15 in lanes 32..63.  The (B) accumulator of lane u + 32h
+// holds rows (points) 8i + 4h + r, so the products are lane-local, and the same
+// registers, re-split, are the (D) operand.  The (D) tables put the cosine rows
+// of R0 and P1 and the sine rows of P2 in the h = 0 accumulator positions and the
+// other type in h = 1 (row t' = 0 is cos 0 in both), so every lane forms its
+// output slots from its own registers: the h = 0 half accumulates the m3 >= 0
+// outputs and the h = 1 half the m3 < 0 outputs (plus the m3 = 0, s3 = -1 ones),
+// over its nodes, with table values that are the same for all 64 lanes (scalar
+// loads).  The two waves of a unit tile add their partial outputs in LDS at the
+// end, in a fixed order.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "device_common.h"
+#include "internal.h"
+
+namespace spingtp {
+namespace {
+
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+template <int L>
+struct MShape {
+    static constexpr Layout Y = make_layout(L, L, L);
+    static constexpr int NT = Y.NT;
+    static constexpr int NP = Y.NP;
+    static constexpr int BLK = (L + 1) * (L + 1);
+    static constexpr int NC = 3 * BLK;
+    static constexpr int ST = NC | 1;           // odd row stride: conflict-free per-lane row reads
+    static constexpr int UNITS = 64;
+    static constexpr int WAVES = 4;
+    static constexpr int THREADS = 64 * WAVES;
+    static constexpr int X2 = UNITS * ST + 32;  // input-2 tile: lane u + 32 reads 32 banks away from lane u
+    static constexpr int XF = X2 + UNITS * ST;
+    static constexpr int YB = UNITS * ST;       // second partial-output tile (the first is at 0)
+    static constexpr int REGION = XF > 2 * YB ? XF : 2 * YB;
+    static constexpr int SCALE = REGION;        // 2 x UNITS power-of-two exponents
+    static constexpr int LDS_FLOATS = REGION + 2 * UNITS;
+    static constexpr int NB = (NP + 15) / 16;   // K blocks of step (D)
+    static constexpr int NPW = (NT + 1) / 2;    // nodes per wave
+    static constexpr int TB_WORDS = 64 * 8;     // one lane: 4 words hi, 4 words lo
+    static_assert(L >= 1 && L <= 7, "a polynomial's cos/sin slots must fit one 16-wide K block");
+    static_assert(NP <= 32, "the phi points must fit the 32 rows of one step-(B) tile");
+    static_assert(LDS_FLOATS * 4 <= 80 * 1024, "two workgroups per CU");
+    // step-(B) accumulator position v holds point 8 (v/4) + 4h + v%4; it carries a
+    // point (for h = 0, hence possibly for h = 1) when that row is < n_phi
+    __host__ __device__ static constexpr bool holds_point(int v) { return 8 * (v / 4) + (v % 4) < NP; }
+};
+
+__device__ __forceinline__ float swap_adjacent(float v) {
+    // quad_perm [1,0,3,2]: value of the neighbouring lane (all lanes active)
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+}
+
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+
+// (a, b) split as fp16 hi + lo: hw = (fp16(a), fp16(b)) rounded to nearest,
+// lw = (fp16(a - hi_a), fp16(b - hi_b)), each residual formed in fp32 and
+// rounded once by v_fma_mix{lo,hi}_f16; |x - hi - lo| <= 2^-22 |x| for normal x.
+__device__ __forceinline__ void split_pair(float a, float b, uint32_t& hw, uint32_t& lw) {
+    const h2 hp = {static_cast<_Float16>(a), static_cast<_Float16>(b)};
+    hw = __builtin_bit_cast(uint32_t, hp);
+    asm("v_fma_mixlo_f16 %0, %1, -1.0, %2 op_sel_hi:[1,0,0]" : "=v"(lw) : "v"(hw), "v"(a));
+    asm("v_fma_mixhi_f16 %0, %1, -1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "+v"(lw) : "v"(hw), "v"(b));
+}
+
+__device__ __forceinline__ uint32_t pack_hi(float a, float b) {
+    const h2 hp = {static_cast<_Float16>(a), static_cast<_Float16>(b)};
+    return __builtin_bit_cast(uint32_t, hp);
+}
+
+// Eight values (v[0..7]; zero where !live) -> hi and (SPLIT == 3) lo operands.
+template <int SPLIT>
+__device__ __forceinline__ void split8(const float (&v)[8], const bool (&live)[8], v8h& hi, v8h& lo) {
+    v4u h, l;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        if (!live[2 * w] && !live[2 * w + 1]) {
+            h[w] = 0u;
+            l[w] = 0u;
+        } else if constexpr (SPLIT == 3) {
+            uint32_t hw, lw;
+            split_pair(v[2 * w], v[2 * w + 1], hw, lw);
+            h[w] = hw;
+            l[w] = lw;
+        } else {
+            h[w] = pack_hi(v[2 * w], v[2 * w + 1]);
+            l[w] = 0u;
+        }
+    }
+    hi = __builtin_bit_cast(v8h, h);
+    lo = __builtin_bit_cast(v8h, l);
+}
+
+// (a, b) -> (a with its upper half-wave replaced by b's lower half,
+//            b with its lower half-wave replaced by a's upper half)
+__device__ __forceinline__ void swap_halves(const v8h& a, const v8h& b, v8h& r0, v8h& r1) {
+    const v4u ua = __builtin_bit_cast(v4u, a), ub = __builtin_bit_cast(v4u, b);
+    v4u o0, o1;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const auto r = __builtin_amdgcn_permlane32_swap(ua[w], ub[w], false, false);
+        o0[w] = r[0];
+        o1[w] = r[1];
+    }
+    r0 = __builtin_bit_cast(v8h, o0);
+    r1 = __builtin_bit_cast(v8h, o1);
+}
+
+// Value of lanes 0..31 (lo) and of lanes 32..63 (hi) of x, in every lane.
+__device__ __forceinline__ void bcast_halves(float x, float& lo, float& hi) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    lo = __uint_as_float(r[0]);
+    hi = __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ v16f mfma(const v8h& a, const v8h& b, const v16f& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+// Output tile: (partial A + partial B) * 2^(e1 + e2) per unit, coalesced 16-byte stores.
+template <int NC, int ST>
+__device__ __forceinline__ float out_value(const float* lds, int yb, const int* ex, int e) {
+    const int u = e / NC;
+    const int o = u * ST + (e - u * NC);
+    return ldexpf(lds[o] + lds[yb + o], ex[u] + ex[64 + u]);
+}
+
+template <int NC, int ST>
+__device__ __forceinline__ void store_out(float* __restrict__ dst, int nvalid, const float* lds, int yb,
+                                          const int* ex, int tid, int nthr) {
+    const int n = nvalid * NC;
+    const int n4 = n >> 2;
+    v4f* d4 = reinterpret_cast<v4f*>(dst);
+    for (int i = tid; i < n4; i += nthr) {
+        const int e = 4 * i;
+        v4f v;
+        v.x = out_value<NC, ST>(lds, yb, ex, e);
+        v.y = out_value<NC, ST>(lds, yb, ex, e + 1);
+        v.z = out_value<NC, ST>(lds, yb, ex, e + 2);
+        v.w = out_value<NC, ST>(lds, yb, ex, e + 3);
+        __builtin_nontemporal_store(v, d4 + i);
+    }
+    for (int e = 4 * n4 + tid; e < n; e += nthr) dst[e] = out_value<NC, ST>(lds, yb, ex, e);
+}
+
+template <int NC, int ST>
+__device__ __forceinline__ void store_out(uint16_t* __restrict__ dst, int nvalid, const float* lds, int yb,
+                                          const int* ex, int tid, int nthr) {
+    const int n = nvalid * NC;
+    const int n8 = n >> 3;
+    v4u* d8 = reinterpret_cast<v4u*>(dst);
+    for (int i = tid; i < n8; i += nthr) {
+        const int e = 8 * i;
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            w[q] = static_cast<uint32_t>(f32_to_bf16(out_value<NC, ST>(lds, yb, ex, e + 2 * q))) |
+                   (static_cast<uint32_t>(f32_to_bf16(out_value<NC, ST>(lds, yb, ex, e + 2 * q + 1))) << 16);
+        const v4u v = {w[0], w[1], w[2], w[3]};
+        __builtin_nontemporal_store(v, d8 + i);
+    }
+    for (int e = 8 * n8 + tid; e < n; e += nthr) dst[e] = f32_to_bf16(out_value<NC, ST>(lds, yb, ex, e));
+}
+
+// SPLIT = 3: hi*hi + hi*lo + lo*hi (fp32 I/O); SPLIT = 1: hi*hi (bf16 I/O).
+template <int L, typename TIO, int SPLIT>
+__global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __restrict__ x1,
+                                                                   const TIO* __restrict__ x2,
+                                                                   TIO* __restrict__ out, int64_t units,
+                                                                   const float* __restrict__ tab,
+                                                                   const uint32_t* __restrict__ aux) {
+    using S = MShape<L>;
+    constexpr Layout Y = S::Y;
+    constexpr int NC = S::NC, ST = S::ST, BLK = S::BLK, NB = S::NB;
+    __shared__ float lds[S::LDS_FLOATS];
+    int* ex = reinterpret_cast<int*>(lds + S::SCALE);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t u0 = static_cast<int64_t>(blockIdx.x) * S::UNITS;
+    const int nvalid = static_cast<int>(units - u0 < S::UNITS ? units - u0 : S::UNITS);
+
+    // (1) input tiles -> LDS; rows past the end of the batch are zero
+    load_two_tiles<NC, ST, S::UNITS, S::THREADS>(x1 + u0 * NC, x2 + u0 * NC, nvalid, lds, lds + S::X2, tid);
+    for (int i = tid; i < (S::UNITS - nvalid) * ST; i += S::THREADS) {
+        lds[nvalid * ST + i] = 0.f;
+        lds[S::X2 + nvalid * ST + i] = 0.f;
+    }
+    __syncthreads();
+
+    // (2) per unit and input: scale the row by 2^-e so that its largest valid
+    //     magnitude is in [1/2, 1).  Two threads per row; the l = 0 slots of the
+    //     |s| = 1 sectors are not data and are skipped.
+    {
+        constexpr int HALF = (NC + 1) / 2;
+        const int row = tid >> 1;  // 0..127: input row >> 6, unit row & 63
+        const bool odd = (tid & 1) != 0;
+        float* xr = lds + ((row >> 6) ? S::X2 : 0) + (row & 63) * ST + (odd ? HALF : 0);
+        float v[HALF];
+        float m = 0.f;
+#pragma unroll
+        for (int i = 0; i < HALF; ++i) {
+            const bool last = i + HALF >= NC;  // past the row end in the second half
+            v[i] = (last && odd) ? 0.f : xr[i];
+            bool skip = false;  // l = 0 slots of the s = -1 (index 0) and s = +1 (index 2 BLK) blocks
+            if (i == 0) skip = !odd;
+            if (i == 2 * BLK) skip = skip || !odd;
+            if (i == 2 * BLK - HALF) skip = skip || odd;
+            m = fmaxf(m, skip ? 0.f : fabsf(v[i]));
+        }
+        m = fmaxf(m, swap_adjacent(m));
+        int e = 0;
+        if (m > 0.f && m <= 3.0e38f) (void)frexpf(m, &e);
+        e = e < -100 ? -100 : (e > 100 ? 100 : e);
+#pragma unroll
+        for (int i = 0; i < HALF; ++i) {
+            const bool last = i + HALF >= NC;
+            if (!(last && odd)) xr[i] = ldexpf(v[i], -e);
+        }
+        if (!odd) ex[row] = e;
+    }
+    __syncthreads();
+
+    const int h = lane >> 5;  // (A): input h + 1; (D)-(E): accumulator type
+    const int T = wave & 1;   // unit tile of this wave
+    const float* xr = lds + (h ? S::X2 : 0) + (32 * T + (lane & 31)) * ST;
+    const float sg = h ? -1.f : 1.f;
+    const v4u* __restrict__ ops = reinterpret_cast<const v4u*>(aux);
+    const v8h TBh = __builtin_bit_cast(v8h, ops[2 * lane]);
+    const v8h TBl = __builtin_bit_cast(v8h, ops[2 * lane + 1]);
+    const v16f zero16 = {};
+
+    // output accumulators of this lane: m3 >= 0 (h = 0) or m3 < 0 (h = 1)
+    float oA[L + 1], oZ[L + 1], oR[L + 1][L + 1], oP[L + 1][L + 1], oM[L + 1][L + 1];
+#pragma unroll
+    for (int a = 0; a <= L; ++a) {
+        oA[a] = oZ[a] = 0.f;
+#pragma unroll
+        for (int b = 0; b <= L; ++b) oR[a][b] = oP[a][b] = oM[a][b] = 0.f;
+    }
+
+#pragma unroll 1
+    for (int k = 0; k < S::NPW; ++k) {
+        const int j = (wave >> 1) + 2 * k;
+        if (j >= S::NT) break;
+        const float* __restrict__ tb = tab + Y.glob + j * Y.pb;
+
+        // (A) this lane's input at node j
+        float Pc[3][L + 1], Ps[3][L + 1], dl, ep;
+        coef_to_theta_fourier<L, L, true>(xr, tb, tab + Y.n0, Pc[0], Ps[0], Pc[1], Ps[1], Pc[2], Ps[2], dl, ep);
+
+        // step-(B) operands of the three polynomials of both inputs
+        v8h oh[2][3], ol[2][3];
+#pragma unroll
+        for (int p = 0; p < 3; ++p) {
+            float cv[8], sv[8];
+            bool cl_[8], sl_[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                cl_[e] = e <= L;
+                sl_[e] = e >= 1 && e <= L;
+                cv[e] = cl_[e] ? Pc[p][e] : 0.f;
+                sv[e] = sl_[e] ? Ps[p][e] : 0.f;
+            }
+            v8h ch, cl, sh, sl;
+            split8<SPLIT>(cv, cl_, ch, cl);
+            split8<SPLIT>(sv, sl_, sh, sl);
+            swap_halves(ch, sh, oh[0][p], oh[1][p]);
+            if constexpr (SPLIT == 3) swap_halves(cl, sl, ol[0][p], ol[1][p]);
+        }
+
+        // (B) fields of the six polynomials at the n_phi points
+        v16f fb[2][3];
+#pragma unroll
+        for (int in = 0; in < 2; ++in)
+#pragma unroll
+            for (int p = 0; p < 3; ++p) {
+                fb[in][p] = mfma(TBh, oh[in][p], zero16);
+                if constexpr (SPLIT == 3) {
+                    fb[in][p] = mfma(TBh, ol[in][p], fb[in][p]);
+                    fb[in][p] = mfma(TBl, oh[in][p], fb[in][p]);
+                }
+            }
+
+        // (C) R0 = A a + B b + C c, P1 = A b + a B, P2 = A c + a C, lane-local
+        float H[3][16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            if (S::holds_point(v)) {
+                const float A = fb[0][0][v], B = fb[0][1][v], C = fb[0][2][v];
+                const float a = fb[1][0][v], b = fb[1][1][v], c = fb[1][2][v];
+                H[0][v] = fmaf(C, c, fmaf(B, b, A * a));
+                H[1][v] = fmaf(A, b, a * B);
+                H[2][v] = fmaf(A, c, a * C);
+            } else {
+                H[0][v] = H[1][v] = H[2][v] = 0.f;
+            }
+        }
+
+        // (D) spectra: R0 and P1 with table type 0, P2 with type 1
+        v16f sp[3];
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+            sp[q] = zero16;
+            const int qt = q == 2 ? 1 : 0;
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                float hv[8];
+                bool live[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    live[e] = 8 * b + e < 16 && S::holds_point(8 * b + e);
+                    hv[e] = live[e] ? H[q][8 * b + e] : 0.f;
+                }
+                v8h hh, hl;
+                split8<SPLIT>(hv, live, hh, hl);
+                const v4u* td = ops + 2 * (64 + (qt * NB + b) * 64 + lane);
+                const v8h tdh = __builtin_bit_cast(v8h, td[0]);
+                sp[q] = mfma(tdh, hh, sp[q]);
+                if constexpr (SPLIT == 3) {
+                    const v8h tdl = __builtin_bit_cast(v8h, td[1]);
+                    sp[q] = mfma(tdh, hl, sp[q]);
+                    sp[q] = mfma(tdl, hh, sp[q]);
+                }
+            }
+        }
+
+        // m3 = 0 closed forms (both halves hold the t' = 0 cosine sums)
+        float d_1, d_2, e_1, e_2, a_1, a_2;
+        bcast_halves(dl, d_1, d_2);
+        bcast_halves(ep, e_1, e_2);
+        bcast_halves(Pc[0][0], a_1, a_2);
+        constexpr float NPf = static_cast<float>(S::NP);
+        const float r0c0 = fmaf(-0.5f * NPf, fmaf(d_1, d_2, e_1 * e_2), sp[0][0]);
+        const float sP1 = 1.41421356237309505f * sp[1][0];
+        const float sP2 = 1.41421356237309505f * sp[2][0];
+        const float sP4 = -NPf * fmaf(d_2, a_1, d_1 * a_2);
+        const float sP3 = NPf * fmaf(e_2, a_1, e_1 * a_2);
+        const float w0 = 0.5f * (sP1 + sP4), w1 = 0.5f * (sP3 + sP2);
+        const float w2 = 0.5f * (sP1 - sP4), w3 = 0.5f * (sP3 - sP2);
+        const float* __restrict__ m0 = tab + Y.m0;
+        const float zp = fmaf(m0[0], w0, fmaf(m0[1], w1, fmaf(m0[2], w2, m0[3] * w3)));
+        const float zm = fmaf(m0[4], w0, fmaf(m0[5], w1, fmaf(m0[6], w2, m0[7] * w3)));
+        const float zs = h ? zm : zp;
+
+        // (E) this node's share of the lane's outputs
+#pragma unroll
+        for (int l = 0; l <= L; ++l) oA[l] = fmaf(tb[Y.e0c + tri(L, 0, l)], r0c0, oA[l]);
+#pragma unroll
+        for (int l = 1; l <= L; ++l) oZ[l] = fmaf(tb[Y.e1z + l], zs, oZ[l]);
+#pragma unroll
+        for (int t = 1; t <= L; ++t) {
+            const float sr = sg * sp[0][t];
+            const float spp = fmaf(sg, sp[1][t], sp[2][t]);
+            const float smm = fmaf(sg, sp[1][t], -sp[2][t]);
+#pragma unroll
+            for (int l = t; l <= L; ++l) {
+                oR[t][l] = fmaf(tb[Y.e0c + tri(L, t, l)], sr, oR[t][l]);
+                oP[t][l] = fmaf(tb[Y.e1p + tri(L, t, l)], spp, oP[t][l]);
+                oM[t][l] = fmaf(tb[Y.e1m + tri(L, t, l)], smm, oM[t][l]);
+            }
+        }
+    }
+
+    // partial outputs -> LDS (tile of waves 0, 1 at 0, of waves 2, 3 at YB)
+    __syncthreads();  // every wave is done with the input tiles
+    float* yr = lds + (wave >> 1) * S::YB + (32 * T + (lane & 31)) * ST;
+    if (h == 0) {
+        yr[0] = 0.f;        // l = 0 of s = -1
+        yr[2 * BLK] = 0.f;  // l = 0 of s = +1
+#pragma unroll
+        for (int l = 0; l <= L; ++l) yr[BLK + l * l + l] = oA[l];
+#pragma unroll
+        for (int l = 1; l <= L; ++l) yr[2 * BLK + l * l + l] = oZ[l];
+    } else {
+#pragma unroll
+        for (int l = 1; l <= L; ++l) yr[l * l + l] = oZ[l];
+    }
+    const int sm = h ? -1 : 1;
+#pragma unroll
+    for (int t = 1; t <= L; ++t)
+#pragma unroll
+        for (int l = t; l <= L; ++l) {
+            yr[BLK + l * l + l + sm * t] = oR[t][l];
+            yr[2 * BLK + l * l + l + sm * t] = oP[t][l];
+            yr[l * l + l + sm * t] = oM[t][l];
+        }
+    __syncthreads();
+    store_out<NC, ST>(out + u0 * NC, nvalid, lds, S::YB, ex, tid, S::THREADS);
+}
+
+template <int L, typename TIO, int SPLIT>
+hipError_t launch_mfma(const void* x1, const void* x2, void* out, int64_t units, const float* tab,
+                       const uint32_t* aux, hipStream_t stream) {
+    using S = MShape<L>;
+    const int64_t blocks = (units + S::UNITS - 1) / S::UNITS;
+    if (blocks > 0x7fffffff || aux == nullptr) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((spingtp_fwd_mfma_kernel<L, TIO, SPLIT>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(S::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
+                       static_cast<TIO*>(out), units, tab, aux);
+    return hipGetLastError();
+}
+
+struct MRegistered {
+    int L, dtype;
+    KernelEntry entry;
+};
+
+template <int L, typename TIO>
+constexpr MRegistered reg_mfma() {
+    using S = MShape<L>;
+    return MRegistered{L, sizeof(TIO) == 4 ? 0 : 1,
+                       KernelEntry{S::WAVES, S::UNITS, static_cast<int>(S::LDS_FLOATS * sizeof(float)), 4,
+                                   &launch_mfma<L, TIO, sizeof(TIO) == 4 ? 3 : 1>}};
+}
+
+const MRegistered kMfmaRegistry[] = {reg_mfma<6, float>(), reg_mfma<6, uint16_t>()};
+
+}  // namespace
+
+const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int dtype) {
+    if (L1 != L2 || L1 != LO || spin_mode != 1) return nullptr;
+    for (const MRegistered& r : kMfmaRegistry)
+        if (r.L == L1 && r.dtype == dtype) return &r.entry;
+    return nullptr;
+}
+
+}  // namespace spingtp

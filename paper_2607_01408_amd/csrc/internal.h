@@ -16,13 +16,22 @@ struct KernelEntry {
     int waves;        // waves (64 lanes) per workgroup
     int units;        // units per workgroup (one per lane)
     int lds_bytes;    // dynamic LDS per workgroup
-    int family;       // 1 = register-tiled fixed-degree kernel
+    int family;       // see spingtp_plan_kernel_info
+    // tab: the fp32 plan tables (layout.h); aux: the matrix-core operand tables
+    // (build_mfma_operands), nullptr for the vector-ALU families.
     hipError_t (*launch)(const void* x1, const void* x2, void* out, int64_t units, const float* tab,
-                         hipStream_t stream);
+                         const uint32_t* aux, hipStream_t stream);
 };
 
 // Finds the instantiation for (L1, L2, Lout, spin mode, dtype); nullptr if none.
+// find_kernel returns the vector-ALU kernels, find_mfma_kernel the matrix-core
+// kernel where one is built.
 const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
+const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
+
+// Per-lane A operands of the matrix-core kernel for L1 = L2 = Lout = L, spins
+// {-1, 0, +1}: packed fp16 (hi, lo) words; layout in forward_mfma.hip.
+void build_mfma_operands(int L, std::vector<uint32_t>& out);
 
 // Builds the float64 tables (layout.h) into `out`; returns false on a failed
 // self-check.  spin_mode: 0 = {0}, 1 = {-1, 0, +1}.
@@ -43,5 +52,6 @@ struct spingtp_plan_s {
     int device;
     float* d_tab;
     size_t n_tab;
+    uint32_t* d_aux;  // matrix-core operand tables, nullptr for the vector-ALU kernels
     const spingtp::KernelEntry* kernel;
 };

@@ -201,6 +201,71 @@ bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::ve
     return true;
 }
 
+// Operand tables of the matrix-core kernel (forward_mfma.hip), as packed fp16
+// words (element 2w in the low half of word w).  fp32 values are split as
+// hi = fp16(v), lo = fp16(v - hi), both rounded to nearest.
+//   TB, 64 lanes x 8 words: lane l is row l % 32 of the step-(B) table (the phi
+//     point phi_k, k = row, zero for k >= n_phi) and its K elements
+//     8 (l / 32) + e, e = 0..7, are kappa = 8 (l / 32) + e: cos(kappa phi_k) for
+//     kappa <= L, sin((kappa - 8) phi_k) for 1 <= kappa - 8 <= L, else 0.
+//     Words 0..3 hold hi, 4..7 lo.
+//   TD[type][block], 2 x NB blocks of 64 lanes x 8 words: lane l is row
+//     r' = l % 32 = 8i + 4h' + r of the step-(D) table, the spectrum t' = 4i + r
+//     (zero for t' > L); K element e of lane l in block b is the point held by
+//     step-(B) accumulator position v = 8b + e of half h'' = l / 32, i.e.
+//     k = 8 (v / 4) + 4 h'' + v % 4 (zero for k >= n_phi).  Type 0 (R0, P1) rows
+//     with h' = 0 are cos(t' phi_k) and with h' = 1 sin(t' phi_k); type 1 (P2)
+//     swaps the two; the t' = 0 rows are cos 0 = 1 in both halves.
+void build_mfma_operands(int L, std::vector<uint32_t>& out) {
+    const int NP = 3 * L + 1;
+    const int NB = (NP + 15) / 16;
+    out.assign(512 + static_cast<size_t>(2 * NB) * 512, 0u);
+    auto trig = [&](bool cosine, int t, int k) {
+        const double ang = 2.0 * kPi * static_cast<double>((k * t) % NP) / NP;
+        return cosine ? std::cos(ang) : std::sin(ang);
+    };
+    auto put = [&](size_t word0, int e, double v) {
+        const _Float16 hi = static_cast<_Float16>(v);
+        const _Float16 lo = static_cast<_Float16>(v - static_cast<double>(hi));
+        uint16_t bh, bl;
+        std::memcpy(&bh, &hi, 2);
+        std::memcpy(&bl, &lo, 2);
+        const int sh = 16 * (e & 1);
+        out[word0 + e / 2] |= static_cast<uint32_t>(bh) << sh;
+        out[word0 + 4 + e / 2] |= static_cast<uint32_t>(bl) << sh;
+    };
+    for (int lane = 0; lane < 64; ++lane) {
+        const int k = lane % 32, half = lane / 32;
+        for (int e = 0; e < 8; ++e) {
+            const int kappa = 8 * half + e;
+            double v = 0.0;
+            if (k < NP) {
+                if (kappa < 8 && kappa <= L) v = trig(true, kappa, k);
+                if (kappa >= 9 && kappa - 8 <= L) v = trig(false, kappa - 8, k);
+            }
+            put(static_cast<size_t>(lane) * 8, e, v);
+        }
+    }
+    for (int type = 0; type < 2; ++type)
+        for (int b = 0; b < NB; ++b)
+            for (int lane = 0; lane < 64; ++lane) {
+                const int rr = lane % 32;
+                const int i = rr / 8, hp = (rr / 4) % 2, r = rr % 4;
+                const int tp = 4 * i + r;
+                const size_t w0 = 512 + (static_cast<size_t>(type * NB + b) * 64 + lane) * 8;
+                for (int e = 0; e < 8; ++e) {
+                    const int v = 8 * b + e;
+                    const int k = 8 * (v / 4) + 4 * (lane / 32) + v % 4;
+                    double val = 0.0;
+                    if (tp <= L && k < NP) {
+                        const bool cosine = tp == 0 || (type == 0 ? hp == 0 : hp == 1);
+                        val = trig(cosine, tp, k);
+                    }
+                    put(w0, e, val);
+                }
+            }
+}
+
 // Dense real tensor T[k1][k2][k3] = Re sum conj(Q3) G Q1 Q2 (see spingtp.h).
 // G^{(l3,m3,s3)}_{(l1,m1,s1)(l2,m2,s2)} = 2 pi sum_j w_j Y1(theta_j) Y2(theta_j) Y3(theta_j) for
 // s3 = s1 + s2, m3 = m1 + m2 (the phi integral of the other combinations vanishes), on the
@@ -313,8 +378,8 @@ spingtp_status check_args(int L1, int L2, int Lout, const int* spins, int n_spin
                           int* spin_mode) {
     if (L1 < 0 || L2 < 0 || L1 > 16 || L2 > 16 || Lout < 0 || Lout > L1 + L2) return SPINGTP_ERR_INVALID_ARG;
     if (spins == nullptr || n_spins <= 0 || n_spins > 64) return SPINGTP_ERR_INVALID_ARG;
-    if (flags != SPINGTP_BASIS_REAL_PAPER && flags != SPINGTP_BASIS_REAL_M0_PAIRED)
-        return SPINGTP_ERR_INVALID_ARG;
+    const unsigned basis = flags & ~SPINGTP_KERNEL_VALU;
+    if (basis != SPINGTP_BASIS_REAL_PAPER && basis != SPINGTP_BASIS_REAL_M0_PAIRED) return SPINGTP_ERR_INVALID_ARG;
     bool has0 = false;
     for (int i = 0; i < n_spins; ++i) {
         if (i > 0 && spins[i] <= spins[i - 1]) return SPINGTP_ERR_INVALID_ARG;
@@ -359,7 +424,8 @@ spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spi
     if (n_tables == nullptr || (capacity > 0 && tables == nullptr)) return SPINGTP_ERR_INVALID_ARG;
     std::vector<double> tab;
     try {
-        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags, tab)) return SPINGTP_ERR_INTERNAL;
+        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags & ~SPINGTP_KERNEL_VALU, tab))
+            return SPINGTP_ERR_INTERNAL;
     } catch (const std::bad_alloc&) {
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
@@ -388,7 +454,7 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
     if (capacity == 0) return SPINGTP_OK;
     try {
         std::vector<double> T;
-        spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, flags, T);
+        spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, flags & ~SPINGTP_KERNEL_VALU, T);
         const size_t n = total < capacity ? total : capacity;
         std::memcpy(tensor, T.data(), n * sizeof(double));
     } catch (const std::bad_alloc&) {
@@ -405,12 +471,18 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
     if (dtype != SPINGTP_FP32 && dtype != SPINGTP_BF16) return SPINGTP_ERR_INVALID_ARG;
-    const spingtp::KernelEntry* k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
+    const spingtp::KernelEntry* k = nullptr;
+    if ((flags & SPINGTP_KERNEL_VALU) == 0)
+        k = spingtp::find_mfma_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
+    if (k == nullptr) k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
     if (k == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    const unsigned basis = flags & ~SPINGTP_KERNEL_VALU;
 
     std::vector<double> tab;
+    std::vector<uint32_t> aux;
     try {
-        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags, tab)) return SPINGTP_ERR_INTERNAL;
+        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
+        if (k->family == 4) spingtp::build_mfma_operands(L1, aux);
     } catch (const std::bad_alloc&) {
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
@@ -427,8 +499,21 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
         (void)hipFree(d);
         return SPINGTP_ERR_HIP;
     }
+    uint32_t* da = nullptr;
+    if (!aux.empty()) {
+        e = hipMalloc(&da, aux.size() * sizeof(uint32_t));
+        if (e == hipSuccess &&
+            hipMemcpy(da, aux.data(), aux.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess)
+            e = hipErrorUnknown;
+        if (e != hipSuccess) {
+            if (da != nullptr) (void)hipFree(da);
+            (void)hipFree(d);
+            return e == hipErrorOutOfMemory ? SPINGTP_ERR_OUT_OF_MEMORY : SPINGTP_ERR_HIP;
+        }
+    }
     spingtp_plan p = new (std::nothrow) spingtp_plan_s;
     if (p == nullptr) {
+        if (da != nullptr) (void)hipFree(da);
         (void)hipFree(d);
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
@@ -442,6 +527,7 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     p->device = dev;
     p->d_tab = d;
     p->n_tab = tabf.size();
+    p->d_aux = da;
     p->kernel = k;
     *out_plan = p;
     return SPINGTP_OK;
@@ -453,6 +539,7 @@ spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
     hipError_t e = hipGetDevice(&cur);
     if (e == hipSuccess && cur != plan->device) e = hipSetDevice(plan->device);
     if (e == hipSuccess) e = hipFree(plan->d_tab);
+    if (e == hipSuccess && plan->d_aux != nullptr) e = hipFree(plan->d_aux);
     if (cur != plan->device) (void)hipSetDevice(cur);
     delete plan;
     return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;

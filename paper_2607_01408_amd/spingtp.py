@@ -12,6 +12,7 @@ from . import _lib
 
 BASIS_PAPER = 0
 BASIS_M0_PAIRED = 1
+KERNEL_VALU = 0x100  # force the fp32 vector-ALU kernels (spingtp.h)
 FP32 = 0
 BF16 = 1
 
@@ -51,9 +52,13 @@ def dense_tensor_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
 
 
 class Plan:
-    """spingtp_plan_create / spingtp_forward / spingtp_plan_destroy."""
+    """spingtp_plan_create / spingtp_forward / spingtp_plan_destroy.
 
-    def __init__(self, L1, L2, Lout, spins=(-1, 0, 1), dtype="fp32", basis=BASIS_PAPER):
+    ``valu_only`` sets SPINGTP_KERNEL_VALU: the fp32 vector-ALU kernels even where
+    the matrix-core kernel is the default.
+    """
+
+    def __init__(self, L1, L2, Lout, spins=(-1, 0, 1), dtype="fp32", basis=BASIS_PAPER, valu_only=False):
         import torch  # device memory and streams only
 
         self.L1, self.L2, self.Lout = int(L1), int(L2), int(Lout)
@@ -61,10 +66,12 @@ class Plan:
         self.dtype_name = {"fp32": "fp32", "float32": "fp32", "bf16": "bf16", "bfloat16": "bf16"}[str(dtype)]
         self.torch_dtype = torch.float32 if self.dtype_name == "fp32" else torch.bfloat16
         self.basis = int(basis)
+        self.valu_only = bool(valu_only)
         self._handle = ctypes.c_void_p()
         arr, n = _spin_array(self.spins)
         code = FP32 if self.dtype_name == "fp32" else BF16
-        _lib.check(_lib.lib().spingtp_plan_create(self.L1, self.L2, self.Lout, arr, n, code, self.basis,
+        _lib.check(_lib.lib().spingtp_plan_create(self.L1, self.L2, self.Lout, arr, n, code,
+                                                  self.basis | (KERNEL_VALU if self.valu_only else 0),
                                                   ctypes.byref(self._handle)), "spingtp_plan_create")
         self.device = torch.cuda.current_device()
 
