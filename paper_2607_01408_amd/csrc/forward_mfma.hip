@@ -151,49 +151,97 @@ __device__ __forceinline__ v16f mfma(const v8h& a, const v8h& b, const v16f& c) 
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
-// Output tile: (partial A + partial B) * 2^(e1 + e2) per unit, coalesced 16-byte stores.
+// Output tile = partial tile A + partial tile B (row stride ST), coalesced
+// 16-byte stores.  Full tiles: all LDS reads of a thread are issued before its
+// first store, so the LDS latency is paid once.
 template <int NC, int ST>
-__device__ __forceinline__ float out_value(const float* lds, int yb, const int* ex, int e) {
-    const int u = e / NC;
-    const int o = u * ST + (e - u * NC);
-    return ldexpf(lds[o] + lds[yb + o], ex[u] + ex[64 + u]);
+__device__ __forceinline__ int lds_off(int e) {
+    if constexpr (ST == NC) {
+        return e;
+    } else {
+        const int u = e / NC;
+        return u * ST + (e - u * NC);
+    }
 }
 
-template <int NC, int ST>
-__device__ __forceinline__ void store_out(float* __restrict__ dst, int nvalid, const float* lds, int yb,
-                                          const int* ex, int tid, int nthr) {
+template <int NC, int ST, int VEC>
+__device__ __forceinline__ void gather_sum(const float* lds, int yb, int e, float (&v)[VEC]) {
+#pragma unroll
+    for (int q = 0; q < VEC; ++q) {
+        const int o = lds_off<NC, ST>(e + q);
+        v[q] = lds[o] + lds[yb + o];
+    }
+}
+
+template <int NC, int ST, int UNITS, int NTHR>
+__device__ __forceinline__ void store_out(float* __restrict__ dst, int nvalid, const float* lds, int yb, int tid) {
+    v4f* d4 = reinterpret_cast<v4f*>(dst);
+    if (nvalid == UNITS) {
+        static_assert((UNITS * NC) % 4 == 0, "whole 16-byte chunks");
+        constexpr int N4 = UNITS * NC / 4;
+        constexpr int IT = (N4 + NTHR - 1) / NTHR;
+        float v[IT][4];
+#pragma unroll
+        for (int it = 0; it < IT; ++it)
+            if (it < IT - 1 || tid + it * NTHR < N4) gather_sum<NC, ST, 4>(lds, yb, 4 * (tid + it * NTHR), v[it]);
+#pragma unroll
+        for (int it = 0; it < IT; ++it)
+            if (it < IT - 1 || tid + it * NTHR < N4) {
+                const v4f w = {v[it][0], v[it][1], v[it][2], v[it][3]};
+                __builtin_nontemporal_store(w, d4 + tid + it * NTHR);
+            }
+        return;
+    }
     const int n = nvalid * NC;
     const int n4 = n >> 2;
-    v4f* d4 = reinterpret_cast<v4f*>(dst);
-    for (int i = tid; i < n4; i += nthr) {
-        const int e = 4 * i;
-        v4f v;
-        v.x = out_value<NC, ST>(lds, yb, ex, e);
-        v.y = out_value<NC, ST>(lds, yb, ex, e + 1);
-        v.z = out_value<NC, ST>(lds, yb, ex, e + 2);
-        v.w = out_value<NC, ST>(lds, yb, ex, e + 3);
-        __builtin_nontemporal_store(v, d4 + i);
+    for (int i = tid; i < n4; i += NTHR) {
+        float v[4];
+        gather_sum<NC, ST, 4>(lds, yb, 4 * i, v);
+        const v4f w = {v[0], v[1], v[2], v[3]};
+        __builtin_nontemporal_store(w, d4 + i);
     }
-    for (int e = 4 * n4 + tid; e < n; e += nthr) dst[e] = out_value<NC, ST>(lds, yb, ex, e);
+    for (int e = 4 * n4 + tid; e < n; e += NTHR) {
+        const int o = lds_off<NC, ST>(e);
+        dst[e] = lds[o] + lds[yb + o];
+    }
 }
 
-template <int NC, int ST>
-__device__ __forceinline__ void store_out(uint16_t* __restrict__ dst, int nvalid, const float* lds, int yb,
-                                          const int* ex, int tid, int nthr) {
+__device__ __forceinline__ uint32_t bf16x2(float a, float b) {
+    return static_cast<uint32_t>(f32_to_bf16(a)) | (static_cast<uint32_t>(f32_to_bf16(b)) << 16);
+}
+
+template <int NC, int ST, int UNITS, int NTHR>
+__device__ __forceinline__ void store_out(uint16_t* __restrict__ dst, int nvalid, const float* lds, int yb, int tid) {
+    v4u* d8 = reinterpret_cast<v4u*>(dst);
+    if (nvalid == UNITS) {
+        static_assert((UNITS * NC) % 8 == 0, "whole 16-byte chunks");
+        constexpr int N8 = UNITS * NC / 8;
+        constexpr int IT = (N8 + NTHR - 1) / NTHR;
+        float v[IT][8];
+#pragma unroll
+        for (int it = 0; it < IT; ++it)
+            if (it < IT - 1 || tid + it * NTHR < N8) gather_sum<NC, ST, 8>(lds, yb, 8 * (tid + it * NTHR), v[it]);
+#pragma unroll
+        for (int it = 0; it < IT; ++it)
+            if (it < IT - 1 || tid + it * NTHR < N8) {
+                const v4u w = {bf16x2(v[it][0], v[it][1]), bf16x2(v[it][2], v[it][3]), bf16x2(v[it][4], v[it][5]),
+                               bf16x2(v[it][6], v[it][7])};
+                __builtin_nontemporal_store(w, d8 + tid + it * NTHR);
+            }
+        return;
+    }
     const int n = nvalid * NC;
     const int n8 = n >> 3;
-    v4u* d8 = reinterpret_cast<v4u*>(dst);
-    for (int i = tid; i < n8; i += nthr) {
-        const int e = 8 * i;
-        uint32_t w[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            w[q] = static_cast<uint32_t>(f32_to_bf16(out_value<NC, ST>(lds, yb, ex, e + 2 * q))) |
-                   (static_cast<uint32_t>(f32_to_bf16(out_value<NC, ST>(lds, yb, ex, e + 2 * q + 1))) << 16);
-        const v4u v = {w[0], w[1], w[2], w[3]};
-        __builtin_nontemporal_store(v, d8 + i);
+    for (int i = tid; i < n8; i += NTHR) {
+        float v[8];
+        gather_sum<NC, ST, 8>(lds, yb, 8 * i, v);
+        const v4u w = {bf16x2(v[0], v[1]), bf16x2(v[2], v[3]), bf16x2(v[4], v[5]), bf16x2(v[6], v[7])};
+        __builtin_nontemporal_store(w, d8 + i);
     }
-    for (int e = 8 * n8 + tid; e < n; e += nthr) dst[e] = f32_to_bf16(out_value<NC, ST>(lds, yb, ex, e));
+    for (int e = 8 * n8 + tid; e < n; e += NTHR) {
+        const int o = lds_off<NC, ST>(e);
+        dst[e] = f32_to_bf16(lds[o] + lds[yb + o]);
+    }
 }
 
 // SPLIT = 3: hi*hi + hi*lo + lo*hi (fp32 I/O); SPLIT = 1: hi*hi (bf16 I/O).
@@ -399,29 +447,32 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
 
     // partial outputs -> LDS (tile of waves 0, 1 at 0, of waves 2, 3 at YB)
     __syncthreads();  // every wave is done with the input tiles
-    float* yr = lds + (wave >> 1) * S::YB + (32 * T + (lane & 31)) * ST;
+    // undo the input scaling: the output of a unit scales with 2^(e1 + e2)
+    const int unit = 32 * T + (lane & 31);
+    const int es = ex[unit] + ex[64 + unit];
+    float* yr = lds + (wave >> 1) * S::YB + unit * ST;
     if (h == 0) {
         yr[0] = 0.f;        // l = 0 of s = -1
         yr[2 * BLK] = 0.f;  // l = 0 of s = +1
 #pragma unroll
-        for (int l = 0; l <= L; ++l) yr[BLK + l * l + l] = oA[l];
+        for (int l = 0; l <= L; ++l) yr[BLK + l * l + l] = ldexpf(oA[l], es);
 #pragma unroll
-        for (int l = 1; l <= L; ++l) yr[2 * BLK + l * l + l] = oZ[l];
+        for (int l = 1; l <= L; ++l) yr[2 * BLK + l * l + l] = ldexpf(oZ[l], es);
     } else {
 #pragma unroll
-        for (int l = 1; l <= L; ++l) yr[l * l + l] = oZ[l];
+        for (int l = 1; l <= L; ++l) yr[l * l + l] = ldexpf(oZ[l], es);
     }
     const int sm = h ? -1 : 1;
 #pragma unroll
     for (int t = 1; t <= L; ++t)
 #pragma unroll
         for (int l = t; l <= L; ++l) {
-            yr[BLK + l * l + l + sm * t] = oR[t][l];
-            yr[2 * BLK + l * l + l + sm * t] = oP[t][l];
-            yr[l * l + l + sm * t] = oM[t][l];
+            yr[BLK + l * l + l + sm * t] = ldexpf(oR[t][l], es);
+            yr[2 * BLK + l * l + l + sm * t] = ldexpf(oP[t][l], es);
+            yr[l * l + l + sm * t] = ldexpf(oM[t][l], es);
         }
     __syncthreads();
-    store_out<NC, ST>(out + u0 * NC, nvalid, lds, S::YB, ex, tid, S::THREADS);
+    store_out<NC, ST, S::UNITS, S::THREADS>(out + u0 * NC, nvalid, lds, S::YB, tid);
 }
 
 template <int L, typename TIO, int SPLIT>
