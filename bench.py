@@ -74,19 +74,22 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def profile_tag(workload, dtype, L):
-    return f"{workload}_L{L}_{dtype}" if workload == "sweep" else f"{workload}_{dtype}"
+def profile_tag(workload, dtype, L, valu=False):
+    tag = f"{workload}_L{L}_{dtype}" if workload == "sweep" else f"{workload}_{dtype}"
+    return tag + "_valu" if valu else tag
 
 
-def measured_traffic(workload, dtype, units, L):
+def measured_traffic(workload, dtype, units, L, kname, valu=False):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"traffic_spingtp_fwd_{profile_tag(workload, dtype, L)}.json")
+    was taken on the current kernel source and the same kernel; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_spingtp_fwd_{profile_tag(workload, dtype, L, valu)}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
     if rec.get("kernel_source_hash") != kernel_source_hash() or rec.get("units") != units:
+        return None
+    if kname + "<" not in rec.get("kernel", ""):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -231,6 +234,8 @@ def main():
     ap.add_argument("--parity-units", type=int, default=2048)
     ap.add_argument("--sweep", action="store_true", help="run the degree sweep against the dense CG comparator")
     ap.add_argument("--sweep-degrees", type=int, nargs="+", default=[2, 4, 8, 12, 16])
+    ap.add_argument("--valu", action="store_true",
+                    help="force the fp32 vector-ALU kernel (SPINGTP_KERNEL_VALU) where a matrix-core kernel exists")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -254,7 +259,7 @@ def main():
     x1, x2, meta = workloads.make_pair(args.workload, dtype=args.dtype, L=args.L, device="cuda:0")
     L = meta["L"]
     U = meta["N"] * meta["C"]
-    plan = Plan(L, L, L, workloads.SPINS, args.dtype)
+    plan = Plan(L, L, L, workloads.SPINS, args.dtype, valu_only=args.valu)
     out = torch.empty((meta["N"], meta["C"], 3, (L + 1) ** 2), dtype=x1.dtype, device="cuda:0")
     print(f"[bench] {meta['workload']} L={L} N={meta['N']} C={meta['C']} {args.dtype} units={U} "
           f"kernel={plan.kernel_info()}", file=sys.stderr, flush=True)
@@ -282,9 +287,17 @@ def main():
     flops_unit = route_flops(L, L, L, True)
     achieved_tflops = flops_unit * U / (avg_launch_ms / 1e3) / 1e12
     bytes_unit = hbm_bytes_per_unit(L, L, L, args.dtype)
-    traffic = measured_traffic(meta["workload"], args.dtype, U, L)
     kinfo = plan.kernel_info()
-    kname = {1: "spingtp_fwd_kernel", 2: "spingtp_fwd_pair_kernel", 3: "spingtp_fwd_big_kernel"}[kinfo["family"]]
+    kname = {1: "spingtp_fwd_kernel", 2: "spingtp_fwd_pair_kernel", 3: "spingtp_fwd_big_kernel",
+             4: "spingtp_fwd_mfma_kernel"}[kinfo["family"]]
+    # arithmetic of the path: the matrix-core kernel runs the two phi transforms as fp16
+    # products with fp32 accumulation (three split products per term for fp32 I/O)
+    if kinfo["family"] == 4:
+        compute = "f32 (phi transforms: fp16x3 split matrix products, fp32 accumulate)" if args.dtype == "fp32" \
+            else "f32 (phi transforms: fp16 matrix products, fp32 accumulate)"
+    else:
+        compute = "f32"
+    traffic = measured_traffic(meta["workload"], args.dtype, U, L, kname, args.valu)
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib * (1 << 20) // 4
@@ -319,7 +332,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32" if (kinfo["family"] != 4 or args.dtype == "fp32") else "f16/f32",
+        "compute": compute,
         "io_dtype": args.dtype,
         "data": "synthetic",
         "config": {
@@ -336,6 +350,7 @@ def main():
             "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,
             "traffic": traffic,
             "kernel": kname,
+            "kernel_family": kinfo["family"],
             "avg_launch_ms": avg_launch_ms,
             "flops_per_unit": flops_unit,
             "hbm_bytes_per_unit": bytes_unit,

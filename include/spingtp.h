@@ -74,8 +74,8 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  *   spins/n_spins: host array, strictly ascending and symmetric; {0} and
  *   {-1, 0, +1} are supported, other valid sets give SPINGTP_ERR_UNSUPPORTED.
  *   dtype: element type of x1, x2 and out.  Arithmetic: the vector-ALU kernels
- *   compute in fp32.  The matrix-core kernel (L1 = L2 = Lout = 6, spins
- *   {-1, 0, +1}) runs the two phi transforms as fp16 matrix products with fp32
+ *   compute in fp32.  The matrix-core kernel (L1 = L2 = Lout = 5 or 6, and
+ *   4 for bf16; spins {-1, 0, +1}) runs the two phi transforms as fp16 matrix products with fp32
  *   accumulation: for fp32 plans every operand is split into fp16 high and low
  *   parts (three products per term, relative error near 2^-21 per term, like
  *   fp32), for bf16 plans only the high parts are used (near 2^-11).  Every
@@ -144,8 +144,8 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
  * `info`.  Families: 1 = one lane per unit, one wave per quadrature node (L <= 6
  * and the mixed-degree shapes); 2 = lane pairs per unit (L = 7, 8); 3 = lane
  * pairs with the nodes processed in rounds (L = 9..16, fp32 only); 4 = the
- * matrix-core kernel (L1 = L2 = Lout = 6, spins {-1, 0, +1}; the default there
- * unless SPINGTP_KERNEL_VALU is given).
+ * matrix-core kernel (L1 = L2 = Lout = 5, 6, and 4 for bf16; spins {-1, 0, +1};
+ * the default there unless SPINGTP_KERNEL_VALU is given).
  */
 spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info);
 

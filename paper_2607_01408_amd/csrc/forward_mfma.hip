@@ -125,6 +125,24 @@ __device__ __forceinline__ void split8(const float (&v)[8], const bool (&live)[8
     lo = __builtin_bit_cast(v8h, l);
 }
 
+// v_permlane32_swap with two wait states on each side, kept in place by
+// scheduling barriers.  Without them the ROCm 7.2 compiler can emit the swap
+// next to the VALU writes of its operands (or the reads of its results); those
+// schedules gave silently wrong operand words on gfx950 (relative errors near
+// 5e-5 instead of 2e-7), and the wait states remove the error in every build
+// tried.
+__device__ __forceinline__ void permlane32_swap_guarded(uint32_t a, uint32_t b, uint32_t& r0, uint32_t& r1) {
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 1" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    const auto r = __builtin_amdgcn_permlane32_swap(a, b, false, false);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 1" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    r0 = r[0];
+    r1 = r[1];
+}
+
 // (a, b) -> (a with its upper half-wave replaced by b's lower half,
 //            b with its lower half-wave replaced by a's upper half)
 __device__ __forceinline__ void swap_halves(const v8h& a, const v8h& b, v8h& r0, v8h& r1) {
@@ -132,9 +150,10 @@ __device__ __forceinline__ void swap_halves(const v8h& a, const v8h& b, v8h& r0,
     v4u o0, o1;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-        const auto r = __builtin_amdgcn_permlane32_swap(ua[w], ub[w], false, false);
-        o0[w] = r[0];
-        o1[w] = r[1];
+        uint32_t x, y;
+        permlane32_swap_guarded(ua[w], ub[w], x, y);
+        o0[w] = x;
+        o1[w] = y;
     }
     r0 = __builtin_bit_cast(v8h, o0);
     r1 = __builtin_bit_cast(v8h, o1);
@@ -142,9 +161,10 @@ __device__ __forceinline__ void swap_halves(const v8h& a, const v8h& b, v8h& r0,
 
 // Value of lanes 0..31 (lo) and of lanes 32..63 (hi) of x, in every lane.
 __device__ __forceinline__ void bcast_halves(float x, float& lo, float& hi) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    lo = __uint_as_float(r[0]);
-    hi = __uint_as_float(r[1]);
+    uint32_t a, b;
+    permlane32_swap_guarded(__float_as_uint(x), __float_as_uint(x), a, b);
+    lo = __uint_as_float(a);
+    hi = __uint_as_float(b);
 }
 
 __device__ __forceinline__ v16f mfma(const v8h& a, const v8h& b, const v16f& c) {
@@ -500,7 +520,9 @@ constexpr MRegistered reg_mfma() {
                                    &launch_mfma<L, TIO, sizeof(TIO) == 4 ? 3 : 1>}};
 }
 
-const MRegistered kMfmaRegistry[] = {reg_mfma<6, float>(), reg_mfma<6, uint16_t>()};
+// L = 4 fp32 stays on the vector-ALU kernel, which is as fast there (0.37 ns/unit).
+const MRegistered kMfmaRegistry[] = {reg_mfma<4, uint16_t>(), reg_mfma<5, float>(), reg_mfma<5, uint16_t>(),
+                                     reg_mfma<6, float>(), reg_mfma<6, uint16_t>()};
 
 }  // namespace
 
