@@ -139,6 +139,21 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
                                          unsigned flags, double* tensor, size_t capacity, size_t* count);
 
 /*
+ * Host-only inspection of the matrix-core operand tables of the kernel for
+ * L1 = L2 = Lout = L and spins {-1, 0, +1} (family 4 below), exactly as
+ * spingtp_plan_create uploads them.  Needs no GPU.  Words are packed fp16
+ * pairs (element 2w in the low half of word w); layout, per 64 lanes x 8 words
+ * (4 words hi, 4 words lo):
+ *   [0, 512)                 the step-(B) trig operand, lane l = row l % 32
+ *                            (phi point), K elements 8 (l / 32) + e;
+ *   [512 + 512 (type NB + b), ...)  the step-(D) operand of table type 0 (R0, P1)
+ *                            or 1 (P2) and K block b, NB = ceil((3L + 1) / 16).
+ * 1 <= L <= 7, else SPINGTP_ERR_INVALID_ARG.  Writes min(capacity, total) words
+ * to `words` (may be NULL when capacity is 0) and the total to *count.
+ */
+spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacity, size_t* count);
+
+/*
  * Describe the kernel a plan launches: writes the waves per workgroup, units per
  * workgroup, LDS bytes per workgroup and a kernel-family id to the 4 ints of
  * `info`.  Families: 1 = one lane per unit, one wave per quadrature node (L <= 6

@@ -463,6 +463,20 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
     return SPINGTP_OK;
 }
 
+spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacity, size_t* count) {
+    if (L < 1 || L > 7 || count == nullptr || (capacity > 0 && words == nullptr)) return SPINGTP_ERR_INVALID_ARG;
+    try {
+        std::vector<uint32_t> w;
+        spingtp::build_mfma_operands(L, w);
+        *count = w.size();
+        const size_t n = w.size() < capacity ? w.size() : capacity;
+        if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));
+    } catch (const std::bad_alloc&) {
+        return SPINGTP_ERR_OUT_OF_MEMORY;
+    }
+    return SPINGTP_OK;
+}
+
 spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, int n_spins,
                                    spingtp_dtype dtype, unsigned flags, spingtp_plan* out_plan) {
     if (out_plan == nullptr) return SPINGTP_ERR_INVALID_ARG;

@@ -51,6 +51,16 @@ def dense_tensor_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
     return T.reshape(nc(L1), nc(L2), nc(Lout))
 
 
+def mfma_operands_host(L):
+    """spingtp_mfma_operands_host: the packed fp16 operand words of the matrix-core kernel (uint32)."""
+    count = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().spingtp_mfma_operands_host(L, None, 0, ctypes.byref(count)), "spingtp_mfma_operands_host")
+    out = np.zeros(count.value, dtype=np.uint32)
+    _lib.check(_lib.lib().spingtp_mfma_operands_host(L, out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
+                                                     out.size, ctypes.byref(count)), "spingtp_mfma_operands_host")
+    return out
+
+
 class Plan:
     """spingtp_plan_create / spingtp_forward / spingtp_plan_destroy.
 
