@@ -26,6 +26,7 @@ PEAK_FP32_VECTOR_TFLOPS = 157.3  # MI355X published fp32 vector peak
 PEAK_HBM_GBS = 8000.0
 METRIC = "edge·channel tensor products/sec at L=6 fp32; % HBM/MFMA roofline"
 KERNEL_SOURCES = ("paper_2607_01408_amd/csrc/forward.hip", "paper_2607_01408_amd/csrc/forward_mfma.hip",
+                  "paper_2607_01408_amd/csrc/forward_pre.hip",
                   "paper_2607_01408_amd/csrc/device_common.h", "paper_2607_01408_amd/csrc/layout.h")
 
 

@@ -67,6 +67,11 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  * The other entry points accept and ignore it. */
 #define SPINGTP_KERNEL_VALU 0x100u
 
+/* Route of spingtp_forward_v1, OR-ed into the flags of spingtp_plan_create: the
+ * Fourier-route kernels (the ones spingtp_forward uses, reading x2 per edge)
+ * even where the precontracted kernel is built (family 5 below). */
+#define SPINGTP_V1_FOURIER 0x200u
+
 /*
  * Create a plan for degrees (L1, L2, Lout) and a spin set.
  *   0 <= L1, L2 <= 16, 0 <= Lout <= L1 + L2 (the product of degrees l1, l2 has
@@ -80,7 +85,12 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  *   parts (three products per term, relative error near 2^-21 per term, like
  *   fp32), for bf16 plans only the high parts are used (near 2^-11).  Every
  *   other step is fp32.  bf16 output is rounded to nearest even.
- *   flags: one SPINGTP_BASIS_* value, optionally OR SPINGTP_KERNEL_VALU.
+ *   flags: one SPINGTP_BASIS_* value, optionally OR SPINGTP_KERNEL_VALU and
+ *   SPINGTP_V1_FOURIER.
+ * A shape that only the precontracted kernel of spingtp_forward_v1 covers (any
+ * L1, L2, Lout with n_spins (L+1)^2 <= 75) gives a plan for that entry point;
+ * spingtp_forward and spingtp_plan_kernel_info then return
+ * SPINGTP_ERR_UNSUPPORTED.
  * The plan tables (Gauss-Legendre weights and SWSH values on the quadrature
  * nodes, trigonometric tables, real-basis mixing constants) are computed in
  * float64 on the host, rounded to fp32 and copied synchronously to the current
@@ -99,10 +109,28 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
  *   memory.  Null pointers (when N*C > 0), misalignment or negative sizes give
  *   SPINGTP_ERR_INVALID_ARG before anything is launched.
  * out is overwritten (not accumulated).  No allocation and no host
- * synchronisation.  A launch failure gives SPINGTP_ERR_HIP.
+ * synchronisation.  A launch failure gives SPINGTP_ERR_HIP; a plan whose shape
+ * only spingtp_forward_v1 supports gives SPINGTP_ERR_UNSUPPORTED.
  */
 spingtp_status spingtp_forward(spingtp_plan plan, const void* x1, const void* x2, void* out,
                                int64_t N, int64_t C, void* stream);
+
+/*
+ * out = SpinGTP(x1, x2) when the second input is an edge feature shared by the C
+ * channels of its edge (edge multiplicity V = 1; paper Sec. 3.4, the
+ * precontraction equations, and App. E, depthwise mode with unit weights):
+ *   out[n][c] = SpinGTP(x1[n][c], x2[n]),
+ *   x1 [N][C][n_spins][(L1+1)^2],  x2 [N][n_spins][(L2+1)^2],
+ *   out [N][C][n_spins][(Lout+1)^2];  same dtype, same slot conventions.
+ * Route: for n_spins (L+1)^2 <= 75 in all three degrees (L <= 4 with spins
+ * {-1, 0, +1}) the precontracted kernel (family 5: per edge
+ * K[k1][k3] = sum_k2 T[k1][k2][k3] x2[n][k2], then out[n][c] = x1[n][c] K, fp32
+ * arithmetic); otherwise, or with SPINGTP_V1_FOURIER, the kernel of
+ * spingtp_forward reading x2 once per edge.  Arguments, alignment, asynchrony and
+ * errors as for spingtp_forward; no allocation.
+ */
+spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void* x2, void* out,
+                                  int64_t N, int64_t C, void* stream);
 
 /* Free the plan's device tables.  The caller must ensure that no forward using
  * the plan is still running.  NULL is accepted (no-op). */
@@ -163,6 +191,10 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  * the default there unless SPINGTP_KERNEL_VALU is given).
  */
 spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info);
+
+/* The same four ints for the kernel of spingtp_forward_v1.  Family 5 = the
+ * precontracted kernel: one workgroup per edge, `units` = 1 (edge). */
+spingtp_status spingtp_plan_kernel_info_v1(spingtp_plan plan, int* info);
 
 #ifdef __cplusplus
 }

@@ -10,7 +10,7 @@ STATUS_NAMES = {0: "OK", 1: "ERR_INVALID_ARG", 2: "ERR_UNSUPPORTED", 3: "ERR_OUT
                 4: "ERR_HIP", 5: "ERR_INTERNAL"}
 EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "spingtp_status_string",
             "spingtp_plan_tables_host", "spingtp_plan_kernel_info", "spingtp_dense_tensor_host",
-            "spingtp_mfma_operands_host")
+            "spingtp_mfma_operands_host", "spingtp_forward_v1", "spingtp_plan_kernel_info_v1")
 
 _lib = None
 
@@ -52,6 +52,10 @@ def lib() -> ctypes.CDLL:
         L.spingtp_mfma_operands_host.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_uint32), ctypes.c_size_t,
                                                  ctypes.POINTER(ctypes.c_size_t)]
         L.spingtp_mfma_operands_host.restype = ctypes.c_int
+        L.spingtp_forward_v1.argtypes = list(L.spingtp_forward.argtypes)
+        L.spingtp_forward_v1.restype = ctypes.c_int
+        L.spingtp_plan_kernel_info_v1.argtypes = [ctypes.c_void_p, c_int_p]
+        L.spingtp_plan_kernel_info_v1.restype = ctypes.c_int
         _lib = L
     return _lib
 

@@ -134,6 +134,20 @@ __device__ __forceinline__ void load_two_full_tiles(const uint16_t* __restrict__
     }
 }
 
+// Tile of an input shared by groups of cpx consecutive units (edge multiplicity
+// one: unit u reads row u / cpx of src).  One wave per row, coalesced along the row.
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
+
+template <int NC, int ST, typename TIO>
+__device__ __forceinline__ void load_tile_shared(const TIO* __restrict__ src, int64_t u0, int nvalid, int64_t cpx,
+                                                 float* dst, int tid, int nthr) {
+    for (int r = tid >> 6; r < nvalid; r += nthr >> 6) {
+        const TIO* __restrict__ s = src + ((u0 + r) / cpx) * NC;
+        for (int c = tid & 63; c < NC; c += 64) dst[r * ST + c] = to_f32(s[c]);
+    }
+}
+
 // Both input tiles of a workgroup: the batched path for full tiles, the
 // element-exact loop for the ragged last tile.
 template <int NC, int ST, int UNITS, int NTHR, typename TIO>

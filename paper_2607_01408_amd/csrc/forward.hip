@@ -125,7 +125,7 @@ struct Shape {
 
 template <int L1, int L2, int LO, bool SPIN, typename TIO>
 __global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fwd_kernel(
-    const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units,
+    const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units, int64_t cpx2,
     const float* __restrict__ tab) {
     using S = Shape<L1, L2, LO, SPIN>;
     constexpr Layout Y = S::Y;
@@ -144,7 +144,10 @@ __global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fw
 
     for (int i = tid; i < 64 * S::STO; i += S::THREADS) YT[i] = 0.f;
     load_tile<S::NC1, S::ST1>(x1 + u0 * S::NC1, nvalid, X1, tid, S::THREADS);
-    load_tile<S::NC2, S::ST2>(x2 + u0 * S::NC2, nvalid, X2, tid, S::THREADS);
+    if (cpx2 == 1)
+        load_tile<S::NC2, S::ST2>(x2 + u0 * S::NC2, nvalid, X2, tid, S::THREADS);
+    else
+        load_tile_shared<S::NC2, S::ST2>(x2, u0, nvalid, cpx2, X2, tid, S::THREADS);
     __syncthreads();
 
     const float* __restrict__ g = tab;
@@ -531,7 +534,7 @@ __device__ __forceinline__ void pair_publish(float* D, int sub, const float (&Q0
 
 template <int L, bool SPIN, typename TIO>
 __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pair_kernel(
-    const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units,
+    const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units, int64_t cpx2,
     const float* __restrict__ tab) {
     using P = PairShape<L, SPIN>;
     constexpr Layout Y = P::Y;
@@ -560,7 +563,10 @@ __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pai
         TR[i] = g[(sb ? Y.sinT : Y.cosT) + k * TM1 + t];
     }
     load_tile<P::NC, P::ST>(x1 + u0 * P::NC, nvalid, X1, tid, P::THREADS);
-    load_tile<P::NC, P::ST>(x2 + u0 * P::NC, nvalid, X2, tid, P::THREADS);
+    if (cpx2 == 1)
+        load_tile<P::NC, P::ST>(x2 + u0 * P::NC, nvalid, X2, tid, P::THREADS);
+    else
+        load_tile_shared<P::NC, P::ST>(x2, u0, nvalid, cpx2, X2, tid, P::THREADS);
     __syncthreads();
 
     const float* __restrict__ tb = tab + Y.glob + node * Y.pb;
@@ -598,14 +604,14 @@ __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pai
 }
 
 template <int L, bool SPIN, typename TIO>
-hipError_t launch_pair(const void* x1, const void* x2, void* out, int64_t units, const float* tab,
+hipError_t launch_pair(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                        const uint32_t*, hipStream_t stream) {
     using P = PairShape<L, SPIN>;
     const int64_t blocks = (units + P::UNITS - 1) / P::UNITS;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL((spingtp_fwd_pair_kernel<L, SPIN, TIO>), dim3(static_cast<unsigned>(blocks)),
                        dim3(P::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
-                       static_cast<TIO*>(out), units, tab);
+                       static_cast<TIO*>(out), units, cpx2, tab);
     return hipGetLastError();
 }
 
@@ -636,7 +642,7 @@ struct BigShape {
 
 template <int L, bool SPIN, int W>
 __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_big_kernel(
-    const float* __restrict__ x1, const float* __restrict__ x2, float* __restrict__ out, int64_t units,
+    const float* __restrict__ x1, const float* __restrict__ x2, float* __restrict__ out, int64_t units, int64_t cpx2,
     const float* __restrict__ tab) {
     using B = BigShape<L, SPIN, W>;
     using P = typename B::PS;
@@ -657,7 +663,7 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     const bool valid = u < nvalid;
     const int64_t row = u0 + (valid ? u : 0);  // invalid lanes compute on a valid row, store nothing
     const float* g = tab;
-    const float* xr = (sub ? x2 : x1) + row * B::NC;
+    const float* xr = sub ? x2 + (row / cpx2) * B::NC : x1 + row * B::NC;
     float* orow = out + row * B::NC;
 
     for (int i = tid; i < B::TRIG; i += B::THREADS) {
@@ -715,26 +721,26 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
 }
 
 template <int L, bool SPIN, int W>
-hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, const float* tab,
+hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                       const uint32_t*, hipStream_t stream) {
     using B = BigShape<L, SPIN, W>;
     const int64_t blocks = (units + B::UNITS - 1) / B::UNITS;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W>), dim3(static_cast<unsigned>(blocks)), dim3(B::THREADS),
                        0, stream, static_cast<const float*>(x1), static_cast<const float*>(x2),
-                       static_cast<float*>(out), units, tab);
+                       static_cast<float*>(out), units, cpx2, tab);
     return hipGetLastError();
 }
 
 template <int L1, int L2, int LO, bool SPIN, typename TIO>
-hipError_t launch(const void* x1, const void* x2, void* out, int64_t units, const float* tab, const uint32_t*,
-                  hipStream_t stream) {
+hipError_t launch(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
+                  const uint32_t*, hipStream_t stream) {
     using S = Shape<L1, L2, LO, SPIN>;
     const int64_t blocks = (units + 63) / 64;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL((spingtp_fwd_kernel<L1, L2, LO, SPIN, TIO>), dim3(static_cast<unsigned>(blocks)),
                        dim3(S::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
-                       static_cast<TIO*>(out), units, tab);
+                       static_cast<TIO*>(out), units, cpx2, tab);
     return hipGetLastError();
 }
 
@@ -793,18 +799,34 @@ const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype)
 
 }  // namespace spingtp
 
-extern "C" spingtp_status spingtp_forward(spingtp_plan plan, const void* x1, const void* x2, void* out, int64_t N,
-                                          int64_t C, void* stream) {
+namespace {
+
+spingtp_status forward_impl(spingtp_plan plan, const spingtp::KernelEntry* k, const void* x1, const void* x2,
+                            void* out, int64_t N, int64_t C, bool shared_x2, void* stream) {
     if (plan == nullptr || N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
     if (N == 0 || C == 0) return SPINGTP_OK;
     if (N > (int64_t{1} << 40) / C) return SPINGTP_ERR_INVALID_ARG;
     if (x1 == nullptr || x2 == nullptr || out == nullptr) return SPINGTP_ERR_INVALID_ARG;
     const auto misaligned = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; };
     if (misaligned(x1) || misaligned(x2) || misaligned(out)) return SPINGTP_ERR_INVALID_ARG;
+    if (k == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
     if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
+    const uint32_t* aux = k->family == 5 ? plan->d_pre : plan->d_aux;
     const hipError_t e =
-        plan->kernel->launch(x1, x2, out, N * C, plan->d_tab, plan->d_aux, static_cast<hipStream_t>(stream));
+        k->launch(x1, x2, out, N * C, shared_x2 ? C : 1, plan->d_tab, aux, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" spingtp_status spingtp_forward(spingtp_plan plan, const void* x1, const void* x2, void* out, int64_t N,
+                                          int64_t C, void* stream) {
+    return forward_impl(plan, plan ? plan->kernel : nullptr, x1, x2, out, N, C, false, stream);
+}
+
+extern "C" spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void* x2, void* out,
+                                             int64_t N, int64_t C, void* stream) {
+    return forward_impl(plan, plan ? plan->kernel_v1 : nullptr, x1, x2, out, N, C, true, stream);
 }

@@ -269,7 +269,7 @@ template <int L, typename TIO, int SPLIT>
 __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __restrict__ x1,
                                                                    const TIO* __restrict__ x2,
                                                                    TIO* __restrict__ out, int64_t units,
-                                                                   const float* __restrict__ tab,
+                                                                   int64_t cpx2, const float* __restrict__ tab,
                                                                    const uint32_t* __restrict__ aux) {
     using S = MShape<L>;
     constexpr Layout Y = S::Y;
@@ -284,7 +284,12 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
     const int nvalid = static_cast<int>(units - u0 < S::UNITS ? units - u0 : S::UNITS);
 
     // (1) input tiles -> LDS; rows past the end of the batch are zero
-    load_two_tiles<NC, ST, S::UNITS, S::THREADS>(x1 + u0 * NC, x2 + u0 * NC, nvalid, lds, lds + S::X2, tid);
+    if (cpx2 == 1) {
+        load_two_tiles<NC, ST, S::UNITS, S::THREADS>(x1 + u0 * NC, x2 + u0 * NC, nvalid, lds, lds + S::X2, tid);
+    } else {  // x2 shared by the cpx2 channels of an edge
+        load_tile<NC, ST>(x1 + u0 * NC, nvalid, lds, tid, S::THREADS);
+        load_tile_shared<NC, ST>(x2, u0, nvalid, cpx2, lds + S::X2, tid, S::THREADS);
+    }
     for (int i = tid; i < (S::UNITS - nvalid) * ST; i += S::THREADS) {
         lds[nvalid * ST + i] = 0.f;
         lds[S::X2 + nvalid * ST + i] = 0.f;
@@ -496,14 +501,14 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
 }
 
 template <int L, typename TIO, int SPLIT>
-hipError_t launch_mfma(const void* x1, const void* x2, void* out, int64_t units, const float* tab,
+hipError_t launch_mfma(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                        const uint32_t* aux, hipStream_t stream) {
     using S = MShape<L>;
     const int64_t blocks = (units + S::UNITS - 1) / S::UNITS;
     if (blocks > 0x7fffffff || aux == nullptr) return hipErrorInvalidValue;
     hipLaunchKernelGGL((spingtp_fwd_mfma_kernel<L, TIO, SPLIT>), dim3(static_cast<unsigned>(blocks)),
                        dim3(S::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
-                       static_cast<TIO*>(out), units, tab, aux);
+                       static_cast<TIO*>(out), units, cpx2, tab, aux);
     return hipGetLastError();
 }
 

@@ -19,15 +19,28 @@ struct KernelEntry {
     int family;       // see spingtp_plan_kernel_info
     // tab: the fp32 plan tables (layout.h); aux: the matrix-core operand tables
     // (build_mfma_operands), nullptr for the vector-ALU families.
-    hipError_t (*launch)(const void* x1, const void* x2, void* out, int64_t units, const float* tab,
+    // cpx2: units per row of x2 (1: one x2 row per unit; C: one per edge, shared by
+    // its C channels)
+    hipError_t (*launch)(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                          const uint32_t* aux, hipStream_t stream);
 };
+
+// Largest row length (n_spins (L+1)^2) of the precontracted kernel: L <= 4 with
+// spins {-1, 0, +1}.
+constexpr int kPreMaxNC = 75;
 
 // Finds the instantiation for (L1, L2, Lout, spin mode, dtype); nullptr if none.
 // find_kernel returns the vector-ALU kernels, find_mfma_kernel the matrix-core
 // kernel where one is built.
 const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
 const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
+// The precontracted kernel of spingtp_forward_v1 (x2 shared by the channels of an edge).
+const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
+
+// Sparse tensor of the precontracted kernel (forward_pre.hip): header words
+// NC1, NC2, NCO, nnz, BLK1, then CSR rows over (k1, k3), k2 indices, values.
+void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                      std::vector<uint32_t>& out);
 
 // Per-lane A operands of the matrix-core kernel for L1 = L2 = Lout = L, spins
 // {-1, 0, +1}: packed fp16 (hi, lo) words; layout in forward_mfma.hip.
@@ -53,5 +66,7 @@ struct spingtp_plan_s {
     float* d_tab;
     size_t n_tab;
     uint32_t* d_aux;  // matrix-core operand tables, nullptr for the vector-ALU kernels
-    const spingtp::KernelEntry* kernel;
+    uint32_t* d_pre;  // sparse tensor of the precontracted kernel, nullptr if not used
+    const spingtp::KernelEntry* kernel;     // spingtp_forward
+    const spingtp::KernelEntry* kernel_v1;  // spingtp_forward_v1 (x2 shared by the channels of an edge)
 };

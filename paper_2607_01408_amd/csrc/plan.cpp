@@ -266,6 +266,41 @@ void build_mfma_operands(int L, std::vector<uint32_t>& out) {
             }
 }
 
+void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                      std::vector<uint32_t>& out) {
+    std::vector<double> T;
+    build_dense_tensor(L1, L2, LO, spins, n_spins, flags, T);
+    const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
+    const int nco = n_spins * (LO + 1) * (LO + 1);
+    std::vector<int> rows(static_cast<size_t>(nc1) * nco + 1, 0), k2s;
+    std::vector<float> vals;
+    for (int k1 = 0; k1 < nc1; ++k1)
+        for (int k3 = 0; k3 < nco; ++k3) {
+            for (int k2 = 0; k2 < nc2; ++k2) {
+                const double v = T[(static_cast<size_t>(k1) * nc2 + k2) * nco + k3];
+                if (std::fabs(v) > 1e-12) {
+                    k2s.push_back(k2);
+                    vals.push_back(static_cast<float>(v));
+                }
+            }
+            rows[static_cast<size_t>(k1) * nco + k3 + 1] = static_cast<int>(k2s.size());
+        }
+    const int nnz = static_cast<int>(k2s.size());
+    out.clear();
+    out.push_back(static_cast<uint32_t>(nc1));
+    out.push_back(static_cast<uint32_t>(nc2));
+    out.push_back(static_cast<uint32_t>(nco));
+    out.push_back(static_cast<uint32_t>(nnz));
+    out.push_back(static_cast<uint32_t>(n_spins == 3 ? (L1 + 1) * (L1 + 1) : 0));
+    for (int r : rows) out.push_back(static_cast<uint32_t>(r));
+    for (int k : k2s) out.push_back(static_cast<uint32_t>(k));
+    for (float v : vals) {
+        uint32_t w;
+        std::memcpy(&w, &v, 4);
+        out.push_back(w);
+    }
+}
+
 // Dense real tensor T[k1][k2][k3] = Re sum conj(Q3) G Q1 Q2 (see spingtp.h).
 // G^{(l3,m3,s3)}_{(l1,m1,s1)(l2,m2,s2)} = 2 pi sum_j w_j Y1(theta_j) Y2(theta_j) Y3(theta_j) for
 // s3 = s1 + s2, m3 = m1 + m2 (the phi integral of the other combinations vanishes), on the
@@ -378,7 +413,7 @@ spingtp_status check_args(int L1, int L2, int Lout, const int* spins, int n_spin
                           int* spin_mode) {
     if (L1 < 0 || L2 < 0 || L1 > 16 || L2 > 16 || Lout < 0 || Lout > L1 + L2) return SPINGTP_ERR_INVALID_ARG;
     if (spins == nullptr || n_spins <= 0 || n_spins > 64) return SPINGTP_ERR_INVALID_ARG;
-    const unsigned basis = flags & ~SPINGTP_KERNEL_VALU;
+    const unsigned basis = flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER);
     if (basis != SPINGTP_BASIS_REAL_PAPER && basis != SPINGTP_BASIS_REAL_M0_PAIRED) return SPINGTP_ERR_INVALID_ARG;
     bool has0 = false;
     for (int i = 0; i < n_spins; ++i) {
@@ -424,7 +459,7 @@ spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spi
     if (n_tables == nullptr || (capacity > 0 && tables == nullptr)) return SPINGTP_ERR_INVALID_ARG;
     std::vector<double> tab;
     try {
-        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags & ~SPINGTP_KERNEL_VALU, tab))
+        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER), tab))
             return SPINGTP_ERR_INTERNAL;
     } catch (const std::bad_alloc&) {
         return SPINGTP_ERR_OUT_OF_MEMORY;
@@ -454,7 +489,7 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
     if (capacity == 0) return SPINGTP_OK;
     try {
         std::vector<double> T;
-        spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, flags & ~SPINGTP_KERNEL_VALU, T);
+        spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER), T);
         const size_t n = total < capacity ? total : capacity;
         std::memcpy(tensor, T.data(), n * sizeof(double));
     } catch (const std::bad_alloc&) {
@@ -489,14 +524,20 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     if ((flags & SPINGTP_KERNEL_VALU) == 0)
         k = spingtp::find_mfma_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
     if (k == nullptr) k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
-    if (k == nullptr) return SPINGTP_ERR_UNSUPPORTED;
-    const unsigned basis = flags & ~SPINGTP_KERNEL_VALU;
+    const spingtp::KernelEntry* kv1 = nullptr;
+    if ((flags & SPINGTP_V1_FOURIER) == 0)
+        kv1 = spingtp::find_pre_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
+    if (kv1 == nullptr) kv1 = k;
+    // a shape only the precontracted kernel covers serves spingtp_forward_v1 alone
+    if (kv1 == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    const unsigned basis = flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER);
 
     std::vector<double> tab;
-    std::vector<uint32_t> aux;
+    std::vector<uint32_t> aux, pre;
     try {
         if (!spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
-        if (k->family == 4) spingtp::build_mfma_operands(L1, aux);
+        if (k != nullptr && k->family == 4) spingtp::build_mfma_operands(L1, aux);
+        if (kv1->family == 5) spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre);
     } catch (const std::bad_alloc&) {
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
@@ -513,21 +554,30 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
         (void)hipFree(d);
         return SPINGTP_ERR_HIP;
     }
-    uint32_t* da = nullptr;
-    if (!aux.empty()) {
-        e = hipMalloc(&da, aux.size() * sizeof(uint32_t));
-        if (e == hipSuccess &&
-            hipMemcpy(da, aux.data(), aux.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess)
-            e = hipErrorUnknown;
-        if (e != hipSuccess) {
-            if (da != nullptr) (void)hipFree(da);
-            (void)hipFree(d);
-            return e == hipErrorOutOfMemory ? SPINGTP_ERR_OUT_OF_MEMORY : SPINGTP_ERR_HIP;
+    // device copy of a host word table; nullptr for an empty one
+    auto upload = [](const std::vector<uint32_t>& h, uint32_t** dp) -> hipError_t {
+        *dp = nullptr;
+        if (h.empty()) return hipSuccess;
+        hipError_t err = hipMalloc(dp, h.size() * sizeof(uint32_t));
+        if (err == hipSuccess) err = hipMemcpy(*dp, h.data(), h.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
+        if (err != hipSuccess && *dp != nullptr) {
+            (void)hipFree(*dp);
+            *dp = nullptr;
         }
+        return err;
+    };
+    uint32_t *da = nullptr, *dpre = nullptr;
+    e = upload(aux, &da);
+    if (e == hipSuccess) e = upload(pre, &dpre);
+    if (e != hipSuccess) {
+        if (da != nullptr) (void)hipFree(da);
+        (void)hipFree(d);
+        return e == hipErrorOutOfMemory ? SPINGTP_ERR_OUT_OF_MEMORY : SPINGTP_ERR_HIP;
     }
     spingtp_plan p = new (std::nothrow) spingtp_plan_s;
     if (p == nullptr) {
         if (da != nullptr) (void)hipFree(da);
+        if (dpre != nullptr) (void)hipFree(dpre);
         (void)hipFree(d);
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
@@ -542,7 +592,9 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     p->d_tab = d;
     p->n_tab = tabf.size();
     p->d_aux = da;
+    p->d_pre = dpre;
     p->kernel = k;
+    p->kernel_v1 = kv1;
     *out_plan = p;
     return SPINGTP_OK;
 }
@@ -554,6 +606,7 @@ spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
     if (e == hipSuccess && cur != plan->device) e = hipSetDevice(plan->device);
     if (e == hipSuccess) e = hipFree(plan->d_tab);
     if (e == hipSuccess && plan->d_aux != nullptr) e = hipFree(plan->d_aux);
+    if (e == hipSuccess && plan->d_pre != nullptr) e = hipFree(plan->d_pre);
     if (cur != plan->device) (void)hipSetDevice(cur);
     delete plan;
     return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
@@ -561,10 +614,20 @@ spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
 
 spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info) {
     if (plan == nullptr || info == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    if (plan->kernel == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     info[0] = plan->kernel->waves;
     info[1] = plan->kernel->units;
     info[2] = plan->kernel->lds_bytes;
     info[3] = plan->kernel->family;
+    return SPINGTP_OK;
+}
+
+spingtp_status spingtp_plan_kernel_info_v1(spingtp_plan plan, int* info) {
+    if (plan == nullptr || info == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    info[0] = plan->kernel_v1->waves;
+    info[1] = plan->kernel_v1->units;
+    info[2] = plan->kernel_v1->lds_bytes;
+    info[3] = plan->kernel_v1->family;
     return SPINGTP_OK;
 }
 

@@ -13,6 +13,7 @@ from . import _lib
 BASIS_PAPER = 0
 BASIS_M0_PAIRED = 1
 KERNEL_VALU = 0x100  # force the fp32 vector-ALU kernels (spingtp.h)
+V1_FOURIER = 0x200  # spingtp_forward_v1 on the Fourier route (spingtp.h)
 FP32 = 0
 BF16 = 1
 
@@ -65,10 +66,12 @@ class Plan:
     """spingtp_plan_create / spingtp_forward / spingtp_plan_destroy.
 
     ``valu_only`` sets SPINGTP_KERNEL_VALU: the fp32 vector-ALU kernels even where
-    the matrix-core kernel is the default.
+    the matrix-core kernel is the default.  ``v1_fourier`` sets SPINGTP_V1_FOURIER:
+    ``forward_v1`` on the Fourier route even where the precontracted kernel exists.
     """
 
-    def __init__(self, L1, L2, Lout, spins=(-1, 0, 1), dtype="fp32", basis=BASIS_PAPER, valu_only=False):
+    def __init__(self, L1, L2, Lout, spins=(-1, 0, 1), dtype="fp32", basis=BASIS_PAPER, valu_only=False,
+                 v1_fourier=False):
         import torch  # device memory and streams only
 
         self.L1, self.L2, self.Lout = int(L1), int(L2), int(Lout)
@@ -77,11 +80,13 @@ class Plan:
         self.torch_dtype = torch.float32 if self.dtype_name == "fp32" else torch.bfloat16
         self.basis = int(basis)
         self.valu_only = bool(valu_only)
+        self.v1_fourier = bool(v1_fourier)
         self._handle = ctypes.c_void_p()
         arr, n = _spin_array(self.spins)
         code = FP32 if self.dtype_name == "fp32" else BF16
         _lib.check(_lib.lib().spingtp_plan_create(self.L1, self.L2, self.Lout, arr, n, code,
-                                                  self.basis | (KERNEL_VALU if self.valu_only else 0),
+                                                  self.basis | (KERNEL_VALU if self.valu_only else 0)
+                                                  | (V1_FOURIER if self.v1_fourier else 0),
                                                   ctypes.byref(self._handle)), "spingtp_plan_create")
         self.device = torch.cuda.current_device()
 
@@ -102,8 +107,22 @@ class Plan:
         _lib.check(_lib.lib().spingtp_plan_kernel_info(self._handle, info), "spingtp_plan_kernel_info")
         return {"waves": info[0], "units_per_workgroup": info[1], "lds_bytes": info[2], "family": info[3]}
 
+    def kernel_info_v1(self):
+        info = (ctypes.c_int * 4)()
+        _lib.check(_lib.lib().spingtp_plan_kernel_info_v1(self._handle, info), "spingtp_plan_kernel_info_v1")
+        return {"waves": info[0], "units_per_workgroup": info[1], "lds_bytes": info[2], "family": info[3]}
+
     def forward(self, x1, x2, out=None, stream=None):
         """out[N, C, n_spins, (Lout+1)^2] = SpinGTP(x1, x2) on the current (or given) stream."""
+        return self._run(x1, x2, out, stream, False)
+
+    def forward_v1(self, x1, x2, out=None, stream=None):
+        """spingtp_forward_v1: x2 is [N, n_spins, (L2+1)^2] (or [N, 1, ...]), shared by the C channels."""
+        if x2.dim() == 3:
+            x2 = x2.unsqueeze(1)
+        return self._run(x1, x2, out, stream, True)
+
+    def _run(self, x1, x2, out, stream, shared):
         import torch
 
         if x1.dim() != 4 or x2.dim() != 4:
@@ -112,8 +131,8 @@ class Plan:
         if tuple(x1.shape[2:]) != self.shape_in(1) or tuple(x2.shape[2:]) != self.shape_in(2):
             raise ValueError(f"trailing shapes {tuple(x1.shape[2:])}, {tuple(x2.shape[2:])} do not match "
                              f"{self.shape_in(1)}, {self.shape_in(2)}")
-        if tuple(x2.shape[:2]) != (N, C):
-            raise ValueError("x1 and x2 must share [N, C]")
+        if tuple(x2.shape[:2]) != ((N, 1) if shared else (N, C)):
+            raise ValueError("x2 must be [N, 1, ...] (forward_v1) or [N, C, ...] (forward)")
         for t in (x1, x2):
             if t.dtype != self.torch_dtype or not t.is_cuda or not t.is_contiguous():
                 raise ValueError(f"inputs must be contiguous {self.torch_dtype} device tensors")
@@ -124,8 +143,9 @@ class Plan:
             raise ValueError("out has the wrong shape, dtype or layout")
         if stream is None:
             stream = torch.cuda.current_stream(x1.device)
-        _lib.check(_lib.lib().spingtp_forward(self._handle, x1.data_ptr(), x2.data_ptr(), out.data_ptr(),
-                                              N, C, ctypes.c_void_p(stream.cuda_stream)), "spingtp_forward")
+        fn = _lib.lib().spingtp_forward_v1 if shared else _lib.lib().spingtp_forward
+        _lib.check(fn(self._handle, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, C,
+                      ctypes.c_void_p(stream.cuda_stream)), "spingtp_forward_v1" if shared else "spingtp_forward")
         return out
 
     __call__ = forward

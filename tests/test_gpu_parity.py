@@ -237,3 +237,113 @@ def test_bitwise_deterministic():
     b = plan.forward(x1, x2)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+# --- edge multiplicity one: x2 shared by the channels of an edge (spingtp_forward_v1) ---
+
+def run_v1(L1, L2, LO, spins, N, C, dtype="fp32", fourier=False, seed=0):
+    from oracle.spingtp import _cached_tensor
+    print(f"[parity-v1] L=({L1},{L2},{LO}) N={N} C={C} {dtype} fourier={fourier}", flush=True)
+    x1 = workloads.draw(L1, N, C, 9000 + seed, dtype, spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, 1, 9500 + seed, dtype, spins, "unit", "cuda")
+    plan = Plan(L1, L2, LO, spins, dtype, 0, v1_fourier=fourier)
+    fam = plan.kernel_info_v1()["family"]
+    y = plan.forward_v1(x1, x2)
+    torch.cuda.synchronize()
+    U = N * C
+    a = x1.view(U, -1).double().cpu().numpy()
+    b = np.repeat(x2.view(N, -1).double().cpu().numpy(), C, axis=0)
+    ref = _cached_tensor(L1, L2, LO, tuple(spins), 0).apply(a, b).reshape(U, -1)
+    err = rel_l2(y.view(U, -1).double().cpu().numpy(), ref)
+    print(f"[parity-v1]   rel_l2={err:.3e} family={fam}", flush=True)
+    assert err <= TOL[dtype], err
+    check_matrix_core(Plan(L1, L2, LO, spins, dtype, 0), dtype, err) if (fourier and fam == 4) else None
+    return fam, err
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1), (2, 2, 2), (1, 3, 3)])
+@pytest.mark.parametrize("C", [16, 64, 128])
+@pytest.mark.parametrize("fourier", [False, True])
+def test_v1_table_shapes(shape, C, fourier):
+    # the depthwise V = 1 shapes of the paper's tensor-product runtime table (App. E)
+    fam, _ = run_v1(*shape, S3, 37, C, "fp32", fourier, seed=sum(shape) + C)
+    assert (fam == 5) == (not fourier)
+
+
+@pytest.mark.parametrize("shape,C", [((2, 2, 2), 1), ((2, 2, 2), 3), ((2, 2, 2), 65), ((4, 4, 4), 65),
+                                     ((3, 1, 2), 9), ((0, 0, 0), 5)])
+def test_v1_channel_counts(shape, C):
+    # one channel, fewer than a chunk, one past a 64-channel chunk, mixed degrees, L = 0
+    fam, _ = run_v1(*shape, S3, 11, C, "fp32", False, seed=3 * C)
+    assert fam == 5
+
+
+@pytest.mark.parametrize("shape", [(2, 2, 2), (4, 4, 4)])
+@pytest.mark.parametrize("fourier", [False, True])
+def test_v1_bf16(shape, fourier):
+    run_v1(*shape, S3, 23, 48, "bf16", fourier, seed=7)
+
+
+@pytest.mark.parametrize("L,C", [(5, 7), (6, 7), (6, 64), (8, 5), (12, 3)])
+def test_v1_fourier_route_large_degree(L, C):
+    # beyond the precontracted kernel's size the v1 entry runs the forward kernel with x2 per edge
+    fam, _ = run_v1(L, L, L, S3, 19, C, "fp32", False, seed=L)
+    assert fam != 5
+
+
+def test_v1_scalar_spins():
+    fam, _ = run_v1(3, 3, 3, (0,), 29, 17, "fp32", False, seed=1)
+    assert fam == 5
+
+
+def test_v1_fourier_equals_forward_with_repeated_x2():
+    """The Fourier route of forward_v1 reads x2 per edge; with x2 repeated over the
+    channels, forward runs the same kernel on the same values: bitwise equal."""
+    L, N, C = 6, 13, 9
+    x1 = workloads.draw(L, N, C, 61, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(L, N, 1, 62, "fp32", S3, "unit", "cuda")
+    plan = Plan(L, L, L, S3, "fp32", v1_fourier=True)
+    a = plan.forward_v1(x1, x2)
+    b = plan.forward(x1, x2.expand(N, C, *x2.shape[2:]).contiguous())
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_v1_invalid_slots_and_poisoned_output():
+    L, N, C = 3, 17, 70
+    x1 = workloads.draw(L, N, C, 71, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(L, N, 1, 72, "fp32", S3, "unit", "cuda")
+    plan = Plan(L, L, L, S3, "fp32")
+    assert plan.kernel_info_v1()["family"] == 5
+    ref = plan.forward_v1(x1, x2).clone()
+    inv = torch.as_tensor(~valid_mask(S3, L), device="cuda").view(3, -1)
+    g1, g2 = x1.clone(), x2.clone()
+    g1[:, :, inv] = float("nan")
+    g2[:, :, inv] = 1e30
+    out = torch.full_like(ref, float("nan"))
+    plan.forward_v1(g1, g2, out=out)
+    torch.cuda.synchronize()
+    assert not torch.isnan(out).any()
+    assert torch.equal(out, ref)
+    assert (out[:, :, inv] == 0).all()
+
+
+def test_v1_argument_checks():
+    plan = Plan(2, 2, 2, S3, "fp32")
+    L = _lib.lib()
+    x = torch.zeros((4, 2, 3, 9), device="cuda")
+    x2 = torch.zeros((4, 1, 3, 9), device="cuda")
+    y = torch.zeros_like(x)
+    assert L.spingtp_forward_v1(plan.handle, x.data_ptr(), None, y.data_ptr(), 4, 2, None) == 1
+    assert L.spingtp_forward_v1(plan.handle, x.data_ptr() + 4, x2.data_ptr(), y.data_ptr(), 4, 2, None) == 1
+    assert L.spingtp_forward_v1(plan.handle, None, None, None, 0, 2, None) == 0
+    with pytest.raises(ValueError):
+        plan.forward_v1(x, x)  # x2 must be [N, 1, ...]
+    only_v1 = Plan(3, 1, 2, S3, "fp32")  # no Fourier-route kernel for this shape
+    assert only_v1.kernel_info_v1()["family"] == 5
+    with pytest.raises(SpinGTPError):
+        only_v1.kernel_info()
+    a = torch.zeros((2, 3, 3, 16), device="cuda")
+    b = torch.zeros((2, 3, 3, 4), device="cuda")
+    with pytest.raises(SpinGTPError):
+        only_v1.forward(a, b)
