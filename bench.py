@@ -133,6 +133,98 @@ def cpu_baseline(L, x1, x2, seconds):
     }
 
 
+# Depthwise V = 1 tensor-product shapes of the paper's backend runtime table (App. E):
+# (L1, L2, Lout, multiplicity U = channels C, edges B, and the paper's H200 medians in ms for
+# direct Gaunt, precontracted and Triton-fused precontracted execution -- context only).
+V1_TABLE = [
+    (1, 1, 1, 16, 128, 5.460, 0.537, 0.120), (1, 1, 1, 64, 128, 5.493, 0.466, 0.119),
+    (1, 1, 1, 128, 128, 4.562, 0.443, 0.115), (2, 2, 2, 16, 32, 21.570, 0.997, 0.259),
+    (2, 2, 2, 64, 32, 29.912, 1.769, 0.748), (2, 2, 2, 128, 32, 33.528, 1.837, 0.559),
+    (2, 2, 2, 16, 128, 16.144, 0.999, 0.258), (2, 2, 2, 64, 128, 29.561, 1.771, 0.752),
+    (2, 2, 2, 128, 128, 33.306, 1.838, 0.572), (1, 3, 3, 16, 128, 12.714, 0.678, 0.228),
+    (1, 3, 3, 64, 128, 20.610, 1.080, 0.608), (1, 3, 3, 128, 128, 22.546, 1.344, 0.681),
+    (2, 2, 2, 64, 1024, 29.912, 1.777, 2.090), (1, 3, 3, 64, 1024, 23.941, 1.394, 1.865),
+    (1, 3, 3, 128, 1024, 22.628, 1.350, 2.240),
+]
+
+
+def run_v1(args):
+    """spingtp_forward_v1 (x2 shared by the channels of an edge): the paper's V = 1 table
+    shapes and a degree sweep, on the precontracted route and on the Fourier route.
+    Times are HIP-event averages over back-to-back calls of the C entry point."""
+    import ctypes
+
+    import numpy as np
+    import torch
+
+    from oracle.spingtp import _cached_tensor
+    from paper_2607_01408_amd import Plan, _lib, workloads
+
+    torch.cuda.set_device(0)
+    fn = _lib.lib().spingtp_forward_v1
+
+    def measure(L1, L2, LO, C, B, fourier, seed):
+        x1 = workloads.draw(L1, B, C, 9100 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        x2 = workloads.draw(L2, B, 1, 9200 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        try:
+            plan = Plan(L1, L2, LO, workloads.SPINS, "fp32", v1_fourier=fourier)
+        except Exception:
+            return None
+        if fourier and plan.kernel_info_v1()["family"] == 5:
+            return None
+        if not fourier and plan.kernel_info_v1()["family"] != 5:
+            return None
+        out = torch.empty((B, C, 3, (LO + 1) ** 2), device="cuda:0")
+        st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        call = (plan.handle, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), B, C, st)
+        for _ in range(args.warmup):
+            assert fn(*call) == 0
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(args.steps):
+            fn(*call)
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / args.steps
+        U = B * C
+        idx = np.unique(np.concatenate([np.arange(min(U, 64)), np.arange(max(0, U - 64), U)]))
+        a = x1.view(U, -1)[torch.as_tensor(idx, device="cuda:0")].double().cpu().numpy()
+        b = x2.view(B, -1).double().cpu().numpy()[idx // C]
+        ref = _cached_tensor(L1, L2, LO, workloads.SPINS, 0).apply(a, b).reshape(len(idx), -1)
+        got = out.view(U, -1)[torch.as_tensor(idx, device="cuda:0")].double().cpu().numpy()
+        parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+        return {"ms": ms, "family": plan.kernel_info_v1()["family"], "parity_rel_l2": parity,
+                "tp_per_s": U / (ms / 1e3)}
+
+    table = []
+    for (L1, L2, LO, C, B, p_direct, p_pre, p_triton) in V1_TABLE:
+        row = {"L1": L1, "L2": L2, "Lout": LO, "C": C, "B": B,
+               "paper_h200_ms": {"direct": p_direct, "precontracted": p_pre, "triton_precontracted": p_triton}}
+        for name, fourier in (("precontracted", False), ("fourier", True)):
+            row[name] = measure(L1, L2, LO, C, B, fourier, L1 + 3 * L2 + C)
+        table.append(row)
+        print(f"[v1] ({L1},{L2},{LO}) C={C} B={B}: pre {row['precontracted']['ms'] * 1e3:.1f} us, "
+              f"fourier {row['fourier']['ms'] * 1e3:.1f} us", file=sys.stderr, flush=True)
+    sweep = []
+    for L in args.v1_sweep_degrees:
+        row = {"L": L, "C": args.v1_sweep_channels, "B": args.v1_sweep_edges}
+        for name, fourier in (("precontracted", False), ("fourier", True)):
+            row[name] = measure(L, L, L, args.v1_sweep_channels, args.v1_sweep_edges, fourier, 50 + L)
+        sweep.append(row)
+        pre = row["precontracted"]
+        print(f"[v1-sweep] L={L}: pre {pre['ms'] if pre else float('nan'):.3f} ms, "
+              f"fourier {row['fourier']['ms']:.3f} ms", file=sys.stderr, flush=True)
+    print(json.dumps({
+        "metric": "spingtp_forward_v1 time: precontracted vs Fourier route (x2 shared by the C channels)",
+        "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": False,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "paper App. E depthwise V = 1 shapes, spins (-1,0,+1), N(0,1) coefficients; "
+                               f"sweep L1=L2=Lout in {list(args.v1_sweep_degrees)}, "
+                               f"{args.v1_sweep_edges} edges x {args.v1_sweep_channels} channels"},
+        "table": table, "sweep": sweep}), flush=True)
+
+
 def run_sweep(args):
     """The degree sweep: SpinGTP kernel vs the direct O(L^6) dense contraction.
 
@@ -235,6 +327,11 @@ def main():
     ap.add_argument("--parity-units", type=int, default=2048)
     ap.add_argument("--sweep", action="store_true", help="run the degree sweep against the dense CG comparator")
     ap.add_argument("--sweep-degrees", type=int, nargs="+", default=[2, 4, 8, 12, 16])
+    ap.add_argument("--v1", action="store_true",
+                    help="spingtp_forward_v1: the paper's V = 1 shapes and a degree sweep, both routes")
+    ap.add_argument("--v1-sweep-degrees", type=int, nargs="+", default=[1, 2, 3, 4, 5, 6])
+    ap.add_argument("--v1-sweep-edges", type=int, default=8192)
+    ap.add_argument("--v1-sweep-channels", type=int, default=128)
     ap.add_argument("--valu", action="store_true",
                     help="force the fp32 vector-ALU kernel (SPINGTP_KERNEL_VALU) where a matrix-core kernel exists")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -249,6 +346,9 @@ def main():
 
     if args.sweep:
         run_sweep(args)
+        return
+    if args.v1:
+        run_v1(args)
         return
 
     import numpy as np

@@ -182,6 +182,26 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
 spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacity, size_t* count);
 
 /*
+ * Host-only inspection of the tensor table of the precontracted kernel of
+ * spingtp_forward_v1 (family 5 below), exactly as spingtp_plan_create uploads it.
+ * Needs no GPU.  Same argument rules as spingtp_plan_create; shapes the kernel does
+ * not cover (a row length n_spins (L+1)^2 above 75) give SPINGTP_ERR_UNSUPPORTED.
+ * Word layout, with P = 256 (threads of one workgroup):
+ *   [0, 8)                 NC1, NC2, NCO, BLK1 ((L1+1)^2 for spins {-1, 0, +1},
+ *                          else 0), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT (a
+ *                          multiple of 8), KST = 16 KS + 4;
+ *   [8, 8 + IPT P)         item words [item][thread]: dst | k2 << 16 | last << 24;
+ *   [8 + IPT P, 8 + 2 IPT P)  fp32 values (bits) [item][thread].
+ * Thread t adds value * x2[k2] for its items in order to a running sum; an item
+ * with `last` set stores the sum as the edge kernel entry K[k1][k3] with
+ * dst = k3 KST + k1, and restarts the sum at 0.  Padding items are all-zero words.
+ * Writes min(capacity, total) words to `words` (may be NULL when capacity is 0)
+ * and the total to *count.
+ */
+spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
+                                      uint32_t* words, size_t capacity, size_t* count);
+
+/*
  * Describe the kernel a plan launches: writes the waves per workgroup, units per
  * workgroup, LDS bytes per workgroup and a kernel-family id to the 4 ints of
  * `info`.  Families: 1 = one lane per unit, one wave per quadrature node (L <= 6

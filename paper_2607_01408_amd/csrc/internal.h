@@ -26,8 +26,12 @@ struct KernelEntry {
 };
 
 // Largest row length (n_spins (L+1)^2) of the precontracted kernel: L <= 4 with
-// spins {-1, 0, +1}.
+// spins {-1, 0, +1}, L <= 7 with spin {0}.
 constexpr int kPreMaxNC = 75;
+// Threads per workgroup of the precontracted kernel (its tensor items are laid out
+// for exactly this many threads) and the words of its table header.
+constexpr int kPreThreads = 256;
+constexpr int kPreHeader = 8;
 
 // Finds the instantiation for (L1, L2, Lout, spin mode, dtype); nullptr if none.
 // find_kernel returns the vector-ALU kernels, find_mfma_kernel the matrix-core
@@ -37,8 +41,14 @@ const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int d
 // The precontracted kernel of spingtp_forward_v1 (x2 shared by the channels of an edge).
 const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
 
-// Sparse tensor of the precontracted kernel (forward_pre.hip): header words
-// NC1, NC2, NCO, nnz, BLK1, then CSR rows over (k1, k3), k2 indices, values.
+// Sparse tensor of the precontracted kernel (forward_pre.hip).  Header words NC1,
+// NC2, NCO, BLK1 (0 for spins {0}), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT,
+// KST = 16 KS + 4; then IPT x kPreThreads item words and IPT x kPreThreads fp32
+// values, both [item][thread].  An item word is dst | k2 << 16 | last << 24: it
+// adds value * x2[k2] to the thread's running sum, and `last` stores the sum to the
+// transposed edge kernel at LDS index dst = k3 KST + k1 and restarts it.  Whole
+// (k1, k3) lists go to one thread (longest first, to the least loaded thread), so
+// every entry has one writer; lists are padded with zero items.
 void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
                       std::vector<uint32_t>& out);
 

@@ -9,10 +9,12 @@
 // maps from eq. real_swsh and App. C.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "internal.h"
@@ -182,10 +184,13 @@ bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::ve
             for (int l = 1; l <= LO; ++l) b[Y.e1z + l] = wc * swsh_theta(1, l, 0, th);
     }
 
-    // Self-checks: the weights integrate 1 exactly, and the rule reproduces
-    // orthonormality of the highest-degree harmonics it has to integrate.
+    // Self-checks: the weights integrate 1 exactly, and the rule reproduces the
+    // orthonormality of the highest-degree harmonics whose squares (degree 2l in
+    // cos theta) it integrates exactly: l <= NT - 1.  The triple products of the
+    // operation have degree L1 + L2 + Lout <= 2 NT - 1, which may be below 2 Lmax
+    // when one degree exceeds the sum of the other two.
     if (std::fabs(wsum - 2.0) > 1e-13) return false;
-    const int lmax = Y.TM;
+    const int lmax = std::min(Y.TM, Y.NT - 1);
     for (int s = 0; s <= spin_mode; ++s) {
         for (int m = 0; m <= lmax; m += (lmax > 0 ? lmax : 1)) {
             for (int l = std::max(std::abs(s), m); l <= lmax; ++l) {
@@ -272,32 +277,55 @@ void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
     build_dense_tensor(L1, L2, LO, spins, n_spins, flags, T);
     const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
     const int nco = n_spins * (LO + 1) * (LO + 1);
-    std::vector<int> rows(static_cast<size_t>(nc1) * nco + 1, 0), k2s;
-    std::vector<float> vals;
+    const int ks = (nc1 + 15) / 16, nt = (nco + 15) / 16, kst = 16 * ks + 4;
+    // nonzero lists per kernel entry (k1, k3)
+    struct Entry {
+        int dst;
+        std::vector<std::pair<int, float>> items;
+    };
+    std::vector<Entry> entries;
     for (int k1 = 0; k1 < nc1; ++k1)
         for (int k3 = 0; k3 < nco; ++k3) {
+            Entry e{k3 * kst + k1, {}};
             for (int k2 = 0; k2 < nc2; ++k2) {
                 const double v = T[(static_cast<size_t>(k1) * nc2 + k2) * nco + k3];
-                if (std::fabs(v) > 1e-12) {
-                    k2s.push_back(k2);
-                    vals.push_back(static_cast<float>(v));
-                }
+                if (std::fabs(v) > 1e-12) e.items.emplace_back(k2, static_cast<float>(v));
             }
-            rows[static_cast<size_t>(k1) * nco + k3 + 1] = static_cast<int>(k2s.size());
+            if (!e.items.empty()) entries.push_back(std::move(e));
         }
-    const int nnz = static_cast<int>(k2s.size());
-    out.clear();
-    out.push_back(static_cast<uint32_t>(nc1));
-    out.push_back(static_cast<uint32_t>(nc2));
-    out.push_back(static_cast<uint32_t>(nco));
-    out.push_back(static_cast<uint32_t>(nnz));
-    out.push_back(static_cast<uint32_t>(n_spins == 3 ? (L1 + 1) * (L1 + 1) : 0));
-    for (int r : rows) out.push_back(static_cast<uint32_t>(r));
-    for (int k : k2s) out.push_back(static_cast<uint32_t>(k));
-    for (float v : vals) {
-        uint32_t w;
-        std::memcpy(&w, &v, 4);
-        out.push_back(w);
+    // longest-first greedy balance of whole entries over the threads of a workgroup
+    std::stable_sort(entries.begin(), entries.end(),
+                     [](const Entry& a, const Entry& b) { return a.items.size() > b.items.size(); });
+    std::vector<std::vector<const Entry*>> per(kPreThreads);
+    std::vector<size_t> load(kPreThreads, 0);
+    for (const Entry& e : entries) {
+        const size_t t = static_cast<size_t>(std::min_element(load.begin(), load.end()) - load.begin());
+        per[t].push_back(&e);
+        load[t] += e.items.size();
+    }
+    size_t ipt = *std::max_element(load.begin(), load.end());
+    ipt = std::max<size_t>(8, (ipt + 7) / 8 * 8);
+    out.assign(kPreHeader + 2 * ipt * kPreThreads, 0u);  // padding items: value 0, never stored
+    out[0] = static_cast<uint32_t>(nc1);
+    out[1] = static_cast<uint32_t>(nc2);
+    out[2] = static_cast<uint32_t>(nco);
+    out[3] = static_cast<uint32_t>(n_spins == 3 ? (L1 + 1) * (L1 + 1) : 0);
+    out[4] = static_cast<uint32_t>(ks);
+    out[5] = static_cast<uint32_t>(nt);
+    out[6] = static_cast<uint32_t>(ipt);
+    out[7] = static_cast<uint32_t>(kst);
+    uint32_t* words = out.data() + kPreHeader;
+    uint32_t* vals = words + ipt * kPreThreads;
+    for (int t = 0; t < kPreThreads; ++t) {
+        size_t i = 0;
+        for (const Entry* e : per[t])
+            for (size_t j = 0; j < e->items.size(); ++j, ++i) {
+                const bool last = j + 1 == e->items.size();
+                words[i * kPreThreads + t] = static_cast<uint32_t>(e->dst) |
+                                             (static_cast<uint32_t>(e->items[j].first) << 16) |
+                                             (last ? 1u << 24 : 0u);
+                std::memcpy(&vals[i * kPreThreads + t], &e->items[j].second, 4);
+            }
     }
 }
 
@@ -503,6 +531,25 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
     try {
         std::vector<uint32_t> w;
         spingtp::build_mfma_operands(L, w);
+        *count = w.size();
+        const size_t n = w.size() < capacity ? w.size() : capacity;
+        if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));
+    } catch (const std::bad_alloc&) {
+        return SPINGTP_ERR_OUT_OF_MEMORY;
+    }
+    return SPINGTP_OK;
+}
+
+spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
+                                      uint32_t* words, size_t capacity, size_t* count) {
+    if (count == nullptr || (capacity > 0 && words == nullptr)) return SPINGTP_ERR_INVALID_ARG;
+    int spin_mode = 0;
+    const spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
+    if (st != SPINGTP_OK) return st;
+    if (spingtp::find_pre_kernel(L1, L2, Lout, spin_mode, 0) == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    try {
+        std::vector<uint32_t> w;
+        spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER), w);
         *count = w.size();
         const size_t n = w.size() < capacity ? w.size() : capacity;
         if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));

@@ -62,6 +62,19 @@ def mfma_operands_host(L):
     return out
 
 
+def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """spingtp_pre_table_host: the tensor table of the precontracted kernel (uint32 words)."""
+    arr, n = _spin_array(spins)
+    count = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, basis, None, 0, ctypes.byref(count)),
+               "spingtp_pre_table_host")
+    out = np.zeros(count.value, dtype=np.uint32)
+    _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, basis,
+                                                 out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), out.size,
+                                                 ctypes.byref(count)), "spingtp_pre_table_host")
+    return out
+
+
 class Plan:
     """spingtp_plan_create / spingtp_forward / spingtp_plan_destroy.
 

@@ -17,7 +17,7 @@ import pytest
 
 import oracle
 from paper_2607_01408_amd import _lib
-from paper_2607_01408_amd.spingtp import dense_tensor_host, mfma_operands_host, plan_tables_host
+from paper_2607_01408_amd.spingtp import dense_tensor_host, mfma_operands_host, plan_tables_host, pre_table_host
 from tests.oracle_helpers import valid_mask
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -175,7 +175,8 @@ def emulate_kernel(x1, x2, L1, L2, LO, spin, basis):
 @pytest.mark.parametrize("L1,L2,LO,spin,basis", [
     (2, 2, 2, True, 0), (2, 2, 2, True, 1), (1, 1, 1, True, 0), (3, 2, 4, True, 0), (2, 3, 1, True, 1),
     (4, 4, 4, True, 0), (6, 6, 6, True, 0), (2, 2, 2, False, 0), (3, 1, 2, False, 0), (0, 0, 0, False, 0),
-    (1, 3, 3, True, 0), (8, 8, 8, True, 0), (12, 12, 12, True, 1),
+    (1, 3, 3, True, 0), (8, 8, 8, True, 0), (12, 12, 12, True, 1), (2, 4, 1, True, 0), (4, 1, 2, True, 1),
+    (1, 3, 0, False, 0), (6, 1, 3, True, 0),
 ])
 def test_plan_tables_reproduce_oracle(built_library, L1, L2, LO, spin, basis):
     S = (-1, 0, 1) if spin else (0,)
@@ -347,3 +348,83 @@ def test_mfma_operands_argument_checks(built_library):
     assert built_library.spingtp_mfma_operands_host(6, None, 0, None) == 1
     assert built_library.spingtp_mfma_operands_host(6, None, 0, ctypes.byref(count)) == 0
     assert count.value == 512 * (1 + 2 * 2)  # L = 6: n_phi = 19 points, two K blocks
+
+
+PRE_THREADS = 256
+
+
+def emulate_pre_kernel(words, x1, x2):
+    """The precontracted kernel's data flow on the CPU with the exact table words:
+    each thread's running fp32 sum over its items, stored at `last`, builds the
+    transposed edge kernel; the product runs in float64 with the invalid x1 slots
+    read as 0.  x1 [C, NC1] of one edge, x2 [NC2]."""
+    nc1, nc2, nco, blk1, ks, nt, ipt, kst = (int(v) for v in words[:8])
+    items = words[8:8 + ipt * PRE_THREADS].reshape(ipt, PRE_THREADS)
+    vals = words[8 + ipt * PRE_THREADS:].view(np.float32).reshape(ipt, PRE_THREADS)
+    X2 = x2.astype(np.float32)
+    Kt = np.zeros(16 * nt * kst, dtype=np.float32)
+    acc = np.zeros(PRE_THREADS, dtype=np.float32)
+    for i in range(ipt):
+        w = items[i]
+        acc = (vals[i].astype(np.float64) * X2[(w >> 16) & 0xFF] + acc).astype(np.float32)  # one fp32 rounding
+        last = (w >> 24) != 0
+        Kt[(w & 0xFFFF)[last]] = acc[last]
+        acc[last] = 0.0
+    K = Kt.reshape(16 * nt, kst)[:nco, :nc1].T.astype(np.float64)
+    k = np.arange(nc1)
+    x1 = np.where((blk1 > 0) & ((k == 0) | (k == 2 * blk1)), 0.0, x1)
+    return x1 @ K, K
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [
+    (1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 0), (1, 3, 3, (-1, 0, 1), 0), (3, 1, 2, (-1, 0, 1), 0),
+    (4, 4, 4, (-1, 0, 1), 0), (4, 2, 3, (-1, 0, 1), 1), (3, 3, 3, (-1, 0, 1), 1), (7, 7, 7, (0,), 0),
+    (5, 2, 6, (0,), 0)])
+def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
+    """The precontracted kernel's table, re-enacted on the CPU, gives the oracle's
+    edge kernel K[k1, k3] = sum_k2 T x2 and the oracle's outputs for channels that
+    share x2; every entry has one writer, inside the padded LDS block."""
+    words = pre_table_host(L1, L2, LO, spins, basis)
+    nc1, nc2, nco, blk1, ks, nt, ipt, kst = (int(v) for v in words[:8])
+    ns = len(spins)
+    assert (nc1, nc2, nco) == (ns * (L1 + 1) ** 2, ns * (L2 + 1) ** 2, ns * (LO + 1) ** 2)
+    assert blk1 == ((L1 + 1) ** 2 if ns == 3 else 0)
+    assert (ks, nt, kst) == (-(-nc1 // 16), -(-nco // 16), 16 * -(-nc1 // 16) + 4)
+    assert ipt % 8 == 0 and words.size == 8 + 2 * ipt * PRE_THREADS
+    items = words[8:8 + ipt * PRE_THREADS]
+    vals = words[8 + ipt * PRE_THREADS:].view(np.float32)
+    stores = items[(items >> 24) != 0] & 0xFFFF
+    assert len(np.unique(stores)) == len(stores)  # one writer per entry
+    assert np.all(stores % kst < nc1) and np.all(stores // kst < nco)
+    assert np.all(((items >> 16) & 0xFF) < nc2)
+    assert np.all(items[vals == 0] == 0)  # padding items are all-zero
+    T = oracle.RealGauntTensor(L1, L2, LO, spins, basis).dense()
+    pattern = np.abs(T).max(axis=1) > 1e-12  # entries (k1, k3) with a nonzero list
+    assert len(stores) == pattern.sum()
+    assert np.array_equal(np.sort(stores), np.sort((np.nonzero(pattern.T)[0] * kst + np.nonzero(pattern.T)[1])))
+    rng = np.random.default_rng(31 + L1 + 7 * L2 + 49 * LO)
+    C = 5
+    x1 = rng.standard_normal((C, nc1))
+    x2 = rng.standard_normal(nc2) * valid_mask(spins, L2)
+    y, K = emulate_pre_kernel(words, x1 * valid_mask(spins, L1), x2)
+    Kref = np.einsum("akb,k->ab", T, x2)
+    assert np.abs(K - Kref).max() <= 1e-6 * np.abs(Kref).max()
+    yo = oracle.RealGauntTensor(L1, L2, LO, spins, basis).apply(x1 * valid_mask(spins, L1),
+                                                                np.broadcast_to(x2, (C, nc2))).reshape(C, -1)
+    rel = np.linalg.norm(y - yo) / np.linalg.norm(yo)
+    assert rel <= 1e-6, rel
+    # the kernel ignores what the invalid slots of x1 hold
+    if ns == 3:
+        poisoned = x1.copy()
+        poisoned[:, ~valid_mask(spins, L1)] = 1e30
+        assert np.array_equal(emulate_pre_kernel(words, poisoned * 1.0, x2)[0], y)
+
+
+def test_pre_table_argument_checks(built_library):
+    count = ctypes.c_size_t(0)
+    S = (ctypes.c_int * 3)(-1, 0, 1)
+    assert built_library.spingtp_pre_table_host(5, 5, 5, S, 3, 0, None, 0, ctypes.byref(count)) == 2  # NC 108 > 75
+    assert built_library.spingtp_pre_table_host(4, 4, 4, S, 3, 0, None, 0, None) == 1
+    assert built_library.spingtp_pre_table_host(-1, 4, 4, S, 3, 0, None, 0, ctypes.byref(count)) == 1
+    assert built_library.spingtp_pre_table_host(4, 4, 4, S, 3, 0, None, 0, ctypes.byref(count)) == 0
+    assert count.value > 8
