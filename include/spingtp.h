@@ -190,8 +190,8 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  *   [0, 8)                 NC1, NC2, NCO, BLK1 ((L1+1)^2 for spins {-1, 0, +1},
  *                          else 0), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT (a
  *                          multiple of 8), KST = 16 KS + 4;
- *   [8, 8 + IPT P)         item words [item][thread]: dst | k2 << 16 | last << 24;
- *   [8 + IPT P, 8 + 2 IPT P)  fp32 values (bits) [item][thread].
+ *   [8, 8 + 2 IPT P)       items [item][thread], two words each: dst | k2 << 16 |
+ *                          last << 24, then the fp32 value (bits).
  * Thread t adds value * x2[k2] for its items in order to a running sum; an item
  * with `last` set stores the sum as the edge kernel entry K[k1][k3] with
  * dst = k3 KST + k1, and restarts the sum at 0.  Padding items are all-zero words.

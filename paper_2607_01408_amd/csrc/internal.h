@@ -43,8 +43,8 @@ const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int spin_mode, int dt
 
 // Sparse tensor of the precontracted kernel (forward_pre.hip).  Header words NC1,
 // NC2, NCO, BLK1 (0 for spins {0}), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT,
-// KST = 16 KS + 4; then IPT x kPreThreads item words and IPT x kPreThreads fp32
-// values, both [item][thread].  An item word is dst | k2 << 16 | last << 24: it
+// KST = 16 KS + 4; then IPT x kPreThreads items [item][thread], each the two
+// words dst | k2 << 16 | last << 24 and an fp32 value.  An item
 // adds value * x2[k2] to the thread's running sum, and `last` stores the sum to the
 // transposed edge kernel at LDS index dst = k3 KST + k1 and restarts it.  Whole
 // (k1, k3) lists go to one thread (longest first, to the least loaded thread), so

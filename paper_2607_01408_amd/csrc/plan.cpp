@@ -314,17 +314,16 @@ void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
     out[5] = static_cast<uint32_t>(nt);
     out[6] = static_cast<uint32_t>(ipt);
     out[7] = static_cast<uint32_t>(kst);
-    uint32_t* words = out.data() + kPreHeader;
-    uint32_t* vals = words + ipt * kPreThreads;
+    uint32_t* items = out.data() + kPreHeader;
     for (int t = 0; t < kPreThreads; ++t) {
         size_t i = 0;
         for (const Entry* e : per[t])
             for (size_t j = 0; j < e->items.size(); ++j, ++i) {
                 const bool last = j + 1 == e->items.size();
-                words[i * kPreThreads + t] = static_cast<uint32_t>(e->dst) |
-                                             (static_cast<uint32_t>(e->items[j].first) << 16) |
-                                             (last ? 1u << 24 : 0u);
-                std::memcpy(&vals[i * kPreThreads + t], &e->items[j].second, 4);
+                uint32_t* it = items + 2 * (i * kPreThreads + t);
+                it[0] = static_cast<uint32_t>(e->dst) | (static_cast<uint32_t>(e->items[j].first) << 16) |
+                        (last ? 1u << 24 : 0u);
+                std::memcpy(&it[1], &e->items[j].second, 4);
             }
     }
 }

@@ -359,8 +359,9 @@ def emulate_pre_kernel(words, x1, x2):
     transposed edge kernel; the product runs in float64 with the invalid x1 slots
     read as 0.  x1 [C, NC1] of one edge, x2 [NC2]."""
     nc1, nc2, nco, blk1, ks, nt, ipt, kst = (int(v) for v in words[:8])
-    items = words[8:8 + ipt * PRE_THREADS].reshape(ipt, PRE_THREADS)
-    vals = words[8 + ipt * PRE_THREADS:].view(np.float32).reshape(ipt, PRE_THREADS)
+    pairs = words[8:].reshape(ipt, PRE_THREADS, 2)
+    items = pairs[:, :, 0]
+    vals = pairs[:, :, 1].copy().view(np.float32)
     X2 = x2.astype(np.float32)
     Kt = np.zeros(16 * nt * kst, dtype=np.float32)
     acc = np.zeros(PRE_THREADS, dtype=np.float32)
@@ -391,8 +392,8 @@ def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
     assert blk1 == ((L1 + 1) ** 2 if ns == 3 else 0)
     assert (ks, nt, kst) == (-(-nc1 // 16), -(-nco // 16), 16 * -(-nc1 // 16) + 4)
     assert ipt % 8 == 0 and words.size == 8 + 2 * ipt * PRE_THREADS
-    items = words[8:8 + ipt * PRE_THREADS]
-    vals = words[8 + ipt * PRE_THREADS:].view(np.float32)
+    items = words[8::2]
+    vals = words[9::2].copy().view(np.float32)
     stores = items[(items >> 24) != 0] & 0xFFFF
     assert len(np.unique(stores)) == len(stores)  # one writer per entry
     assert np.all(stores % kst < nc1) and np.all(stores // kst < nco)
