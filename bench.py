@@ -25,8 +25,9 @@ if ROOT not in sys.path:
 PEAK_FP32_VECTOR_TFLOPS = 157.3  # MI355X published fp32 vector peak
 PEAK_HBM_GBS = 8000.0
 METRIC = "edge·channel tensor products/sec at L=6 fp32; % HBM/MFMA roofline"
+# sources of the spingtp_forward kernels (families 1-4): a stored traffic record
+# is used only while their hash is unchanged
 KERNEL_SOURCES = ("paper_2607_01408_amd/csrc/forward.hip", "paper_2607_01408_amd/csrc/forward_mfma.hip",
-                  "paper_2607_01408_amd/csrc/forward_pre.hip",
                   "paper_2607_01408_amd/csrc/device_common.h", "paper_2607_01408_amd/csrc/layout.h")
 
 
@@ -167,7 +168,7 @@ def run_v1(args):
         x1 = workloads.draw(L1, B, C, 9100 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
         x2 = workloads.draw(L2, B, 1, 9200 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
         try:
-            plan = Plan(L1, L2, LO, workloads.SPINS, "fp32", v1_fourier=fourier)
+            plan = Plan(L1, L2, LO, workloads.SPINS, "fp32", v1_fourier=fourier, v1_precontract=not fourier)
         except Exception:
             return None
         if fourier and plan.kernel_info_v1()["family"] == 5:

@@ -67,10 +67,16 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  * The other entry points accept and ignore it. */
 #define SPINGTP_KERNEL_VALU 0x100u
 
-/* Route of spingtp_forward_v1, OR-ed into the flags of spingtp_plan_create: the
- * Fourier-route kernels (the ones spingtp_forward uses, reading x2 per edge)
- * even where the precontracted kernel is built (family 5 below). */
+/* Route of spingtp_forward_v1, OR-ed into the flags of spingtp_plan_create
+ * (at most one of the two): SPINGTP_V1_FOURIER takes the Fourier-route kernels
+ * (the ones spingtp_forward uses, reading x2 per edge) even where the
+ * precontracted kernel (family 5 below) is the default; SPINGTP_V1_PRECONTRACT
+ * takes the precontracted kernel wherever it is built (SPINGTP_ERR_UNSUPPORTED
+ * where it is not).  Without either, the precontracted kernel is used for row
+ * lengths n_spins (L+1)^2 <= 80 in L1 and Lout (where it is the faster route)
+ * and for shapes with no Fourier-route kernel. */
 #define SPINGTP_V1_FOURIER 0x200u
+#define SPINGTP_V1_PRECONTRACT 0x400u
 
 /*
  * Create a plan for degrees (L1, L2, Lout) and a spin set.
@@ -85,10 +91,11 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  *   parts (three products per term, relative error near 2^-21 per term, like
  *   fp32), for bf16 plans only the high parts are used (near 2^-11).  Every
  *   other step is fp32.  bf16 output is rounded to nearest even.
- *   flags: one SPINGTP_BASIS_* value, optionally OR SPINGTP_KERNEL_VALU and
- *   SPINGTP_V1_FOURIER.
+ *   flags: one SPINGTP_BASIS_* value, optionally OR SPINGTP_KERNEL_VALU and one of
+ *   SPINGTP_V1_FOURIER, SPINGTP_V1_PRECONTRACT.
  * A shape that only the precontracted kernel of spingtp_forward_v1 covers (any
- * L1, L2, Lout with n_spins (L+1)^2 <= 75) gives a plan for that entry point;
+ * L1, L2, Lout up to 6 with spins {-1, 0, +1}, up to 7 with spin {0}) gives a
+ * plan for that entry point;
  * spingtp_forward and spingtp_plan_kernel_info then return
  * SPINGTP_ERR_UNSUPPORTED.
  * The plan tables (Gauss-Legendre weights and SWSH values on the quadrature
@@ -122,11 +129,11 @@ spingtp_status spingtp_forward(spingtp_plan plan, const void* x1, const void* x2
  *   out[n][c] = SpinGTP(x1[n][c], x2[n]),
  *   x1 [N][C][n_spins][(L1+1)^2],  x2 [N][n_spins][(L2+1)^2],
  *   out [N][C][n_spins][(Lout+1)^2];  same dtype, same slot conventions.
- * Route: for n_spins (L+1)^2 <= 75 in all three degrees (L <= 4 with spins
- * {-1, 0, +1}) the precontracted kernel (family 5: per edge
+ * Route: the precontracted kernel (family 5: per edge
  * K[k1][k3] = sum_k2 T[k1][k2][k3] x2[n][k2], then out[n][c] = x1[n][c] K, fp32
- * arithmetic); otherwise, or with SPINGTP_V1_FOURIER, the kernel of
- * spingtp_forward reading x2 once per edge.  Arguments, alignment, asynchrony and
+ * arithmetic; built for degrees <= 6 with spins {-1, 0, +1}, <= 7 with spin {0})
+ * or the kernel of spingtp_forward reading x2 once per edge, as chosen at plan
+ * creation (SPINGTP_V1_FOURIER / SPINGTP_V1_PRECONTRACT above).  Arguments, alignment, asynchrony and
  * errors as for spingtp_forward; no allocation.
  */
 spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void* x2, void* out,
@@ -185,7 +192,8 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  * Host-only inspection of the tensor table of the precontracted kernel of
  * spingtp_forward_v1 (family 5 below), exactly as spingtp_plan_create uploads it.
  * Needs no GPU.  Same argument rules as spingtp_plan_create; shapes the kernel does
- * not cover (a row length n_spins (L+1)^2 above 75) give SPINGTP_ERR_UNSUPPORTED.
+ * not cover (a degree above 6 with spins {-1, 0, +1}, above 7 with spin {0}) give
+ * SPINGTP_ERR_UNSUPPORTED.
  * Word layout, with P = 256 (threads of one workgroup):
  *   [0, 8)                 NC1, NC2, NCO, BLK1 ((L1+1)^2 for spins {-1, 0, +1},
  *                          else 0), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT (a

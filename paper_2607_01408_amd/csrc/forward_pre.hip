@@ -1,274 +1,17 @@
-// Precontracted SpinGTP for an edge input shared by the channels of an edge
-// (edge multiplicity V = 1; paper Sec. 3.4, the precontraction equations, and
-// App. E, depthwise mode with V = 1 and unit weights).
-//
-// With x2 the same for every channel c of edge n, the bilinear map
-//   out[n,c,k3] = sum_{k1,k2} T[k1,k2,k3] x1[n,c,k1] x2[n,k2]
-// factors into an edge kernel K_n[k1,k3] = sum_{k2} T[k1,k2,k3] x2[n,k2] (built
-// once per edge) and a dense product out[n,c,:] = x1[n,c,:] K_n over the
-// channels.  T is the real tensor of the operation (Sec. 3.2 eq. generalized_gaunt
-// through the real basis of App. C), built on the host in float64 by the plan.
-//
-// Workgroups of 256 threads, each taking one edge at a time.
-//  1. The x2 row goes to LDS and the transposed kernel Kt[k3][k1] (16 NT rows of
-//     KST = 16 KS + 4 floats, zero padded) is cleared.
-//  2. Kernel build: each thread walks its own list of tensor items (laid out
-//     [item][thread], so every load is coalesced and independent of the sums),
-//     keeps a running sum and stores it when an entry's list ends.  Whole entries
-//     belong to one thread: the build is deterministic and needs no atomics.
-//  3. Product on the matrix cores, fp32 in and out (v_mfma_f32_16x16x4_f32): each
-//     wave takes tiles of 16 channels and forms D[k3][c] = sum_k1 Kt[k3][k1] x1[c][k1]
-//     for 16-row strips of k3.  The contraction index of MFMA step (s, j) for lane
-//     group g = lane / 16 is k1 = 16 s + 4 g + j, so a lane reads its four Kt values
-//     with one 16-byte LDS load and its four x1 values from one 16-byte run of its
-//     channel's row; the accumulator of a lane then holds four consecutive k3 of one
-//     channel.
-// The l = 0 slots of the |s| = 1 sectors are not data: x1 values there are never
-// read (taken as 0), and T has no entries for them, so those outputs are written
-// as 0 and x2 values there are never used.
-#include <hip/hip_runtime.h>
-
-#include <atomic>
-#include <cstdint>
-
-#include "device_common.h"
-#include "internal.h"
+// Family 5 instantiations with KS, NT <= 5 (row lengths <= 80) and the lookup of
+// the precontracted kernel; the kernel is in forward_pre.h.
+#include "forward_pre.h"
 
 namespace spingtp {
 namespace {
 
-template <typename TIO>
-__device__ __forceinline__ TIO from_f32(float v);
-template <>
-__device__ __forceinline__ float from_f32<float>(float v) {
-    return v;
-}
-template <>
-__device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) {
-    return f32_to_bf16(v);
-}
-
-// Orders a wave's LDS accesses across its lanes (LDS executes a wave's
-// instructions in order; this keeps the compiler from moving them).
-__device__ __forceinline__ void wave_lds_order() {
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-}
-
-// KS = ceil(NC1 / 16) contraction blocks, NT = ceil(NCO / 16) output strips.
-// Workgroups are persistent: workgroup b takes edges b, b + grid, ...; while an
-// edge's product runs, the next edge's x2 row and each wave's first x1 tile of
-// the next edge are already loading.
-template <typename TIO, int KS, int NT>
-__global__ __launch_bounds__(kPreThreads) void spingtp_fwd_pre_kernel(const TIO* __restrict__ x1,
-                                                                      const TIO* __restrict__ x2,
-                                                                      TIO* __restrict__ out, int64_t C,
-                                                                      int64_t edges,
-                                                                      const uint32_t* __restrict__ aux) {
-    constexpr int KST = 16 * KS + 4;
-    constexpr int KT_FLOATS = 16 * NT * KST;
-    constexpr int RS = 16 * (KS > NT ? KS : NT) + 4;  // row stride of a wave's staging tile
-    constexpr int NW = kPreThreads / 64;
-    constexpr int PF = 4 * KS;  // x1 values per lane of a 16-channel tile: 16 NC1 / 64 <= 4 KS
-    constexpr int PO = 4 * NT;  // output values per lane of a tile
-    __shared__ __align__(16) float Kt[KT_FLOATS];
-    __shared__ __align__(16) float Stage[NW * 16 * RS];
-    __shared__ float X2[kPreMaxNC];
-
-    const int NC1 = static_cast<int>(aux[0]), NC2 = static_cast<int>(aux[1]), NCO = static_cast<int>(aux[2]);
-    const int blk1 = static_cast<int>(aux[3]), ipt = static_cast<int>(aux[6]);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 15, g = lane >> 4;
-    const int64_t tiles = (C + 15) / 16;
-    const int64_t stride = gridDim.x;
-    float* __restrict__ st = Stage + wave * 16 * RS;
-    const uint2* __restrict__ items = reinterpret_cast<const uint2*>(aux + kPreHeader) + tid;
-
-    float pf[PF];
-    auto prefetch = [&](int64_t n, int64_t m) {
-        const int cnt = static_cast<int>((C - 16 * m < 16 ? C - 16 * m : 16)) * NC1;
-        const TIO* __restrict__ src = x1 + (n * C + 16 * m) * NC1;
-#pragma unroll
-        for (int q = 0; q < PF; ++q) {
-            const int e = lane + 64 * q;
-            pf[q] = e < cnt ? to_f32(src[e]) : 0.f;
-        }
-    };
-    // Per-lane position of element lane + 64 q of a tile stored row-major in rows
-    // of length nc, stepped by 64 = q nc + r.
-    const int q1 = 64 / NC1, r1 = 64 - q1 * NC1, qo = 64 / NCO, ro = 64 - qo * NCO;
-    const int row1 = lane / NC1, k1l = lane - row1 * NC1, rowo = lane / NCO, k3l = lane - rowo * NCO;
-
-    int64_t n = blockIdx.x;
-    float x2v = (n < edges && tid < NC2) ? to_f32(x2[n * NC2 + tid]) : 0.f;
-    if (n < edges && wave < tiles) prefetch(n, wave);
-    for (; n < edges; n += stride) {
-        const int64_t nn = n + stride;
-        uint2 ia[8], ib[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) ia[j] = items[j * kPreThreads];
-        for (int i = tid; i < KT_FLOATS / 4; i += kPreThreads)
-            reinterpret_cast<v4f*>(Kt)[i] = v4f{0.f, 0.f, 0.f, 0.f};
-        if (tid < NC2) X2[tid] = x2v;
-        __syncthreads();
-
-        // Kernel build: the next 8 items load while the current 8 are summed; the
-        // 8 x2 reads of a group are issued before its sums.
-        {
-            float acc = 0.f;
-            auto consume = [&](const uint2 (&it)[8]) {
-                float xv[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) xv[j] = X2[(it[j].x >> 16) & 0xffu];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    acc = fmaf(__uint_as_float(it[j].y), xv[j], acc);
-                    if (it[j].x >> 24) {
-                        Kt[it[j].x & 0xffffu] = acc;
-                        acc = 0.f;
-                    }
-                }
-            };
-            for (int i = 0; i < ipt; i += 16) {  // ipt is a multiple of 8
-                const bool second = i + 8 < ipt;
-                if (second)
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) ib[j] = items[(i + 8 + j) * kPreThreads];
-                consume(ia);
-                if (i + 16 < ipt)
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) ia[j] = items[(i + 16 + j) * kPreThreads];
-                if (second) consume(ib);
-            }
-        }
-        if (nn < edges && tid < NC2) x2v = to_f32(x2[nn * NC2 + tid]);
-        __syncthreads();
-
-        TIO* __restrict__ oe = out + n * C * NCO;
-        for (int64_t m = wave; m < tiles; m += NW) {
-            const int rows = static_cast<int>(C - 16 * m < 16 ? C - 16 * m : 16);
-            {  // x1 tile -> staging rows
-                int r = row1, k = k1l;
-#pragma unroll
-                for (int q = 0; q < PF; ++q) {
-                    if (lane + 64 * q < rows * NC1) st[r * RS + k] = pf[q];
-                    r += q1;
-                    k += r1;
-                    if (k >= NC1) {
-                        k -= NC1;
-                        ++r;
-                    }
-                }
-            }
-            wave_lds_order();
-            float b[KS][4];
-#pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                const v4f v = *reinterpret_cast<const v4f*>(&st[col * RS + 16 * s + 4 * g]);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int k1 = 16 * s + 4 * g + j;
-                    const bool ok = k1 < NC1 && !(blk1 > 0 && (k1 == 0 || k1 == 2 * blk1));
-                    b[s][j] = ok ? v[j] : 0.f;
-                }
-            }
-            if (m + NW < tiles)
-                prefetch(n, m + NW);
-            else if (nn < edges)
-                prefetch(nn, wave);
-            v4f acc[NT];
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int s = 0; s < KS; ++s) {
-                    const v4f a = *reinterpret_cast<const v4f*>(&Kt[(16 * t + col) * KST + 16 * s + 4 * g]);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[s][j], acc[t], 0, 0, 0);
-                }
-            }
-            wave_lds_order();
-            // outputs -> staging rows (lane: channel col, k3 = 16 t + 4 g + i), then
-            // coalesced stores of the tile's contiguous output block
-#pragma unroll
-            for (int t = 0; t < NT; ++t) *reinterpret_cast<v4f*>(&st[col * RS + 16 * t + 4 * g]) = acc[t];
-            wave_lds_order();
-            {
-                TIO* __restrict__ dst = oe + 16 * m * NCO;
-                int r = rowo, k = k3l;
-#pragma unroll
-                for (int q = 0; q < PO; ++q) {
-                    const int e = lane + 64 * q;
-                    if (e < rows * NCO) dst[e] = from_f32<TIO>(st[r * RS + k]);
-                    r += qo;
-                    k += ro;
-                    if (k >= NCO) {
-                        k -= NCO;
-                        ++r;
-                    }
-                }
-            }
-            wave_lds_order();
-        }
-        __syncthreads();  // Kt and X2 are rewritten for the next edge
-    }
-}
-
-// Resident workgroups of one instantiation on the current device (cached per
-// device; 0 on failure).
-template <typename TIO, int KS, int NT>
-int64_t pre_resident_groups() {
-    constexpr int kMaxDevices = 64;
-    static std::atomic<int64_t> cache[kMaxDevices];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
-    int64_t v = cache[dev].load(std::memory_order_relaxed);
-    if (v > 0) return v;
-    int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, spingtp_fwd_pre_kernel<TIO, KS, NT>, kPreThreads, 0) !=
-            hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return 0;
-    v = static_cast<int64_t>(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
-    cache[dev].store(v, std::memory_order_relaxed);
-    return v;
-}
-
-template <typename TIO, int KS, int NT>
-hipError_t launch_pre(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float*,
-                      const uint32_t* aux, hipStream_t stream) {
-    if (aux == nullptr || cpx2 <= 0 || units % cpx2 != 0) return hipErrorInvalidValue;
-    const int64_t edges = units / cpx2;
-    if (edges == 0) return hipSuccess;
-    const int64_t resident = pre_resident_groups<TIO, KS, NT>();
-    if (resident <= 0) return hipErrorInvalidValue;
-    const int64_t grid = edges < resident ? edges : resident;
-    hipLaunchKernelGGL((spingtp_fwd_pre_kernel<TIO, KS, NT>), dim3(static_cast<unsigned>(grid)), dim3(kPreThreads), 0,
-                       stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), static_cast<TIO*>(out), cpx2,
-                       edges, aux);
-    return hipGetLastError();
-}
-
-template <int KS, int NT>
-constexpr int pre_lds_bytes() {
-    return (16 * NT * (16 * KS + 4) + (kPreThreads / 64) * 16 * (16 * (KS > NT ? KS : NT) + 4) + kPreMaxNC) * 4;
-}
-
-#define SPINGTP_PRE_ROW(KS)                                                                      \
-    {{KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 1>(), 5, &launch_pre<float, KS, 1>},     \
-      KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 1>(), 5, &launch_pre<uint16_t, KS, 1>}}, \
-     {KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 2>(), 5, &launch_pre<float, KS, 2>},     \
-      KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 2>(), 5, &launch_pre<uint16_t, KS, 2>}}, \
-     {KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 3>(), 5, &launch_pre<float, KS, 3>},     \
-      KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 3>(), 5, &launch_pre<uint16_t, KS, 3>}}, \
-     {KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 4>(), 5, &launch_pre<float, KS, 4>},     \
-      KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 4>(), 5, &launch_pre<uint16_t, KS, 4>}}, \
-     {KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 5>(), 5, &launch_pre<float, KS, 5>},     \
-      KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, 5>(), 5, &launch_pre<uint16_t, KS, 5>}}}
+#define SPINGTP_PRE_ROW(KS)                                                                        \
+    {SPINGTP_PRE_PAIR(KS, 1), SPINGTP_PRE_PAIR(KS, 2), SPINGTP_PRE_PAIR(KS, 3), SPINGTP_PRE_PAIR(KS, 4), \
+     SPINGTP_PRE_PAIR(KS, 5)}
 
 // [KS - 1][NT - 1][dtype]
-const KernelEntry kPre[5][5][2] = {SPINGTP_PRE_ROW(1), SPINGTP_PRE_ROW(2), SPINGTP_PRE_ROW(3), SPINGTP_PRE_ROW(4),
-                                   SPINGTP_PRE_ROW(5)};
+const KernelEntry kPreSmall[5][5][2] = {SPINGTP_PRE_ROW(1), SPINGTP_PRE_ROW(2), SPINGTP_PRE_ROW(3),
+                                        SPINGTP_PRE_ROW(4), SPINGTP_PRE_ROW(5)};
 #undef SPINGTP_PRE_ROW
 
 }  // namespace
@@ -277,7 +20,9 @@ const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int spin_mode, int dt
     const int ns = spin_mode ? 3 : 1;
     const int nc1 = ns * (L1 + 1) * (L1 + 1), nc2 = ns * (L2 + 1) * (L2 + 1), nco = ns * (LO + 1) * (LO + 1);
     if (nc1 > kPreMaxNC || nc2 > kPreMaxNC || nco > kPreMaxNC || dtype < 0 || dtype > 1) return nullptr;
-    return &kPre[(nc1 + 15) / 16 - 1][(nco + 15) / 16 - 1][dtype];
+    const int ks = (nc1 + 15) / 16, nt = (nco + 15) / 16;
+    if (ks <= 5 && nt <= 5) return &kPreSmall[ks - 1][nt - 1][dtype];
+    return find_pre_kernel_large(ks, nt, dtype);
 }
 
 }  // namespace spingtp

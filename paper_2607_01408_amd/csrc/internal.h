@@ -25,9 +25,11 @@ struct KernelEntry {
                          const uint32_t* aux, hipStream_t stream);
 };
 
-// Largest row length (n_spins (L+1)^2) of the precontracted kernel: L <= 4 with
-// spins {-1, 0, +1}, L <= 7 with spin {0}.
-constexpr int kPreMaxNC = 75;
+// Largest row length (n_spins (L+1)^2) of the precontracted kernel: L <= 6 with
+// spins {-1, 0, +1}.  Its instantiations cover KS = ceil(NC1/16) and
+// NT = ceil(NCO/16) in {1, 2, 3, 4, 5, 7, 10}: L <= 6 with spins {-1, 0, +1},
+// L <= 7 with spin {0}.
+constexpr int kPreMaxNC = 147;
 // Threads per workgroup of the precontracted kernel (its tensor items are laid out
 // for exactly this many threads) and the words of its table header.
 constexpr int kPreThreads = 256;
@@ -40,6 +42,8 @@ const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype)
 const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
 // The precontracted kernel of spingtp_forward_v1 (x2 shared by the channels of an edge).
 const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
+// The instantiations with KS or NT in {7, 10} (forward_pre_large.hip); nullptr if none.
+const KernelEntry* find_pre_kernel_large(int ks, int nt, int dtype);
 
 // Sparse tensor of the precontracted kernel (forward_pre.hip).  Header words NC1,
 // NC2, NCO, BLK1 (0 for spins {0}), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT,

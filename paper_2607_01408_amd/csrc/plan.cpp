@@ -436,12 +436,16 @@ void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, u
 
 namespace {
 
+// flag bits that choose kernels, not the operation
+constexpr unsigned kRouteFlags = SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER | SPINGTP_V1_PRECONTRACT;
+
 spingtp_status check_args(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
                           int* spin_mode) {
     if (L1 < 0 || L2 < 0 || L1 > 16 || L2 > 16 || Lout < 0 || Lout > L1 + L2) return SPINGTP_ERR_INVALID_ARG;
     if (spins == nullptr || n_spins <= 0 || n_spins > 64) return SPINGTP_ERR_INVALID_ARG;
-    const unsigned basis = flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER);
+    const unsigned basis = flags & ~kRouteFlags;
     if (basis != SPINGTP_BASIS_REAL_PAPER && basis != SPINGTP_BASIS_REAL_M0_PAIRED) return SPINGTP_ERR_INVALID_ARG;
+    if ((flags & SPINGTP_V1_FOURIER) && (flags & SPINGTP_V1_PRECONTRACT)) return SPINGTP_ERR_INVALID_ARG;
     bool has0 = false;
     for (int i = 0; i < n_spins; ++i) {
         if (i > 0 && spins[i] <= spins[i - 1]) return SPINGTP_ERR_INVALID_ARG;
@@ -486,7 +490,7 @@ spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spi
     if (n_tables == nullptr || (capacity > 0 && tables == nullptr)) return SPINGTP_ERR_INVALID_ARG;
     std::vector<double> tab;
     try {
-        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER), tab))
+        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags & ~kRouteFlags, tab))
             return SPINGTP_ERR_INTERNAL;
     } catch (const std::bad_alloc&) {
         return SPINGTP_ERR_OUT_OF_MEMORY;
@@ -516,7 +520,7 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
     if (capacity == 0) return SPINGTP_OK;
     try {
         std::vector<double> T;
-        spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER), T);
+        spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, T);
         const size_t n = total < capacity ? total : capacity;
         std::memcpy(tensor, T.data(), n * sizeof(double));
     } catch (const std::bad_alloc&) {
@@ -548,7 +552,7 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
     if (spingtp::find_pre_kernel(L1, L2, Lout, spin_mode, 0) == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     try {
         std::vector<uint32_t> w;
-        spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER), w);
+        spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, w);
         *count = w.size();
         const size_t n = w.size() < capacity ? w.size() : capacity;
         if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));
@@ -571,12 +575,17 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
         k = spingtp::find_mfma_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
     if (k == nullptr) k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
     const spingtp::KernelEntry* kv1 = nullptr;
-    if ((flags & SPINGTP_V1_FOURIER) == 0)
+    if ((flags & SPINGTP_V1_FOURIER) == 0) {
         kv1 = spingtp::find_pre_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
+        // measured crossover: with larger rows the Fourier route is faster
+        const int rows = (spin_mode ? 3 : 1) * (std::max(L1, Lout) + 1) * (std::max(L1, Lout) + 1);
+        if (kv1 != nullptr && k != nullptr && rows > 80 && (flags & SPINGTP_V1_PRECONTRACT) == 0) kv1 = nullptr;
+        if (kv1 == nullptr && (flags & SPINGTP_V1_PRECONTRACT)) return SPINGTP_ERR_UNSUPPORTED;
+    }
     if (kv1 == nullptr) kv1 = k;
     // a shape only the precontracted kernel covers serves spingtp_forward_v1 alone
     if (kv1 == nullptr) return SPINGTP_ERR_UNSUPPORTED;
-    const unsigned basis = flags & ~(SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER);
+    const unsigned basis = flags & ~kRouteFlags;
 
     std::vector<double> tab;
     std::vector<uint32_t> aux, pre;

@@ -14,6 +14,7 @@ BASIS_PAPER = 0
 BASIS_M0_PAIRED = 1
 KERNEL_VALU = 0x100  # force the fp32 vector-ALU kernels (spingtp.h)
 V1_FOURIER = 0x200  # spingtp_forward_v1 on the Fourier route (spingtp.h)
+V1_PRECONTRACT = 0x400  # spingtp_forward_v1 on the precontracted kernel wherever it is built
 FP32 = 0
 BF16 = 1
 
@@ -80,11 +81,13 @@ class Plan:
 
     ``valu_only`` sets SPINGTP_KERNEL_VALU: the fp32 vector-ALU kernels even where
     the matrix-core kernel is the default.  ``v1_fourier`` sets SPINGTP_V1_FOURIER:
-    ``forward_v1`` on the Fourier route even where the precontracted kernel exists.
+    ``forward_v1`` on the Fourier route even where the precontracted kernel is the
+    default; ``v1_precontract`` sets SPINGTP_V1_PRECONTRACT: the precontracted kernel
+    wherever it is built.
     """
 
     def __init__(self, L1, L2, Lout, spins=(-1, 0, 1), dtype="fp32", basis=BASIS_PAPER, valu_only=False,
-                 v1_fourier=False):
+                 v1_fourier=False, v1_precontract=False):
         import torch  # device memory and streams only
 
         self.L1, self.L2, self.Lout = int(L1), int(L2), int(Lout)
@@ -94,12 +97,14 @@ class Plan:
         self.basis = int(basis)
         self.valu_only = bool(valu_only)
         self.v1_fourier = bool(v1_fourier)
+        self.v1_precontract = bool(v1_precontract)
         self._handle = ctypes.c_void_p()
         arr, n = _spin_array(self.spins)
         code = FP32 if self.dtype_name == "fp32" else BF16
         _lib.check(_lib.lib().spingtp_plan_create(self.L1, self.L2, self.Lout, arr, n, code,
                                                   self.basis | (KERNEL_VALU if self.valu_only else 0)
-                                                  | (V1_FOURIER if self.v1_fourier else 0),
+                                                  | (V1_FOURIER if self.v1_fourier else 0)
+                                                  | (V1_PRECONTRACT if self.v1_precontract else 0),
                                                   ctypes.byref(self._handle)), "spingtp_plan_create")
         self.device = torch.cuda.current_device()
 

@@ -380,7 +380,8 @@ def emulate_pre_kernel(words, x1, x2):
 @pytest.mark.parametrize("L1,L2,LO,spins,basis", [
     (1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 0), (1, 3, 3, (-1, 0, 1), 0), (3, 1, 2, (-1, 0, 1), 0),
     (4, 4, 4, (-1, 0, 1), 0), (4, 2, 3, (-1, 0, 1), 1), (3, 3, 3, (-1, 0, 1), 1), (7, 7, 7, (0,), 0),
-    (5, 2, 6, (0,), 0)])
+    (5, 2, 6, (0,), 0), (5, 5, 5, (-1, 0, 1), 0), (6, 6, 6, (-1, 0, 1), 1), (1, 6, 6, (-1, 0, 1), 0),
+    (6, 2, 5, (-1, 0, 1), 0)])
 def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
     """The precontracted kernel's table, re-enacted on the CPU, gives the oracle's
     edge kernel K[k1, k3] = sum_k2 T x2 and the oracle's outputs for channels that
@@ -424,8 +425,24 @@ def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
 def test_pre_table_argument_checks(built_library):
     count = ctypes.c_size_t(0)
     S = (ctypes.c_int * 3)(-1, 0, 1)
-    assert built_library.spingtp_pre_table_host(5, 5, 5, S, 3, 0, None, 0, ctypes.byref(count)) == 2  # NC 108 > 75
+    assert built_library.spingtp_pre_table_host(7, 7, 7, S, 3, 0, None, 0, ctypes.byref(count)) == 2  # NC 192
+    assert built_library.spingtp_pre_table_host(6, 7, 6, S, 3, 0, None, 0, ctypes.byref(count)) == 2
+    S0 = (ctypes.c_int * 1)(0)
+    assert built_library.spingtp_pre_table_host(8, 8, 8, S0, 1, 0, None, 0, ctypes.byref(count)) == 2  # KS = 6
+    assert built_library.spingtp_pre_table_host(6, 6, 6, S, 3, 0, None, 0, ctypes.byref(count)) == 0
     assert built_library.spingtp_pre_table_host(4, 4, 4, S, 3, 0, None, 0, None) == 1
     assert built_library.spingtp_pre_table_host(-1, 4, 4, S, 3, 0, None, 0, ctypes.byref(count)) == 1
     assert built_library.spingtp_pre_table_host(4, 4, 4, S, 3, 0, None, 0, ctypes.byref(count)) == 0
     assert count.value > 8
+
+
+def test_plan_create_route_flags(built_library):
+    """Flag checks of spingtp_plan_create that return before any device call."""
+    S = (ctypes.c_int * 3)(-1, 0, 1)
+    plan = ctypes.c_void_p()
+    # SPINGTP_V1_FOURIER and SPINGTP_V1_PRECONTRACT together
+    assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x200 | 0x400, ctypes.byref(plan)) == 1
+    # precontraction forced where no precontracted kernel is built (rows of 192)
+    assert built_library.spingtp_plan_create(7, 7, 7, S, 3, 0, 0x400, ctypes.byref(plan)) == 2
+    assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x800, ctypes.byref(plan)) == 1  # unknown bit
+    assert not plan.value

@@ -241,12 +241,12 @@ def test_bitwise_deterministic():
 
 # --- edge multiplicity one: x2 shared by the channels of an edge (spingtp_forward_v1) ---
 
-def run_v1(L1, L2, LO, spins, N, C, dtype="fp32", fourier=False, seed=0):
+def run_v1(L1, L2, LO, spins, N, C, dtype="fp32", fourier=False, seed=0, precontract=False):
     from oracle.spingtp import _cached_tensor
     print(f"[parity-v1] L=({L1},{L2},{LO}) N={N} C={C} {dtype} fourier={fourier}", flush=True)
     x1 = workloads.draw(L1, N, C, 9000 + seed, dtype, spins, "unit", "cuda")
     x2 = workloads.draw(L2, N, 1, 9500 + seed, dtype, spins, "unit", "cuda")
-    plan = Plan(L1, L2, LO, spins, dtype, 0, v1_fourier=fourier)
+    plan = Plan(L1, L2, LO, spins, dtype, 0, v1_fourier=fourier, v1_precontract=precontract)
     fam = plan.kernel_info_v1()["family"]
     y = plan.forward_v1(x1, x2)
     torch.cuda.synchronize()
@@ -283,17 +283,35 @@ def test_v1_channel_counts(shape, C):
     assert fam == 5
 
 
-@pytest.mark.parametrize("shape", [(2, 2, 2), (4, 4, 4)])
+@pytest.mark.parametrize("shape", [(2, 2, 2), (4, 4, 4), (6, 6, 6)])
 @pytest.mark.parametrize("fourier", [False, True])
 def test_v1_bf16(shape, fourier):
     run_v1(*shape, S3, 23, 48, "bf16", fourier, seed=7)
 
 
-@pytest.mark.parametrize("L,C", [(5, 7), (6, 7), (6, 64), (8, 5), (12, 3)])
+@pytest.mark.parametrize("L,C", [(7, 5), (8, 5), (12, 3)])
 def test_v1_fourier_route_large_degree(L, C):
     # beyond the precontracted kernel's size the v1 entry runs the forward kernel with x2 per edge
     fam, _ = run_v1(L, L, L, S3, 19, C, "fp32", False, seed=L)
     assert fam != 5
+
+
+@pytest.mark.parametrize("shape,C,fourier", [
+    ((5, 5, 5), 7, False), ((5, 5, 5), 130, False), ((6, 6, 6), 7, False), ((6, 6, 6), 128, False),
+    ((1, 6, 6), 33, False), ((6, 2, 5), 17, False), ((6, 6, 4), 40, False), ((5, 5, 5), 130, True),
+    ((6, 6, 6), 128, True)])
+def test_v1_degree_5_and_6(shape, C, fourier):
+    # the large precontracted instantiations (one resident workgroup per CU), forced where the Fourier
+    # route is the default; mixed degrees here have no Fourier kernel, so this is their only route
+    fam, _ = run_v1(*shape, S3, 21, C, "fp32", fourier, seed=C + sum(shape), precontract=not fourier)
+    assert (fam == 5) == (not fourier)
+
+
+@pytest.mark.parametrize("shape,family", [((4, 4, 4), 5), ((1, 3, 3), 5), ((5, 5, 5), 4), ((6, 6, 6), 4),
+                                          ((6, 2, 5), 5)])
+def test_v1_default_route(shape, family):
+    # precontracted for rows <= 80 and where no Fourier kernel exists, the Fourier route beyond
+    assert Plan(*shape, S3, "fp32").kernel_info_v1()["family"] == family
 
 
 @pytest.mark.parametrize("shape,C", [((3, 3, 3), 17), ((7, 7, 7), 33), ((5, 2, 6), 16)])
