@@ -16,7 +16,8 @@ The oracle computes the plain definition of the operation and nothing else:
 * ``spingtp``   -- the real bilinear map y = Re(Q^dagger c), c = sum G a1 a2,
                    a = Q x, written as an explicit sparse tensor T (paper
                    Sec. 3.5, eq. spin_gtp with unit weights and the elementwise
-                   channel mode of App. E.1).
+                   channel mode of App. E.1); ``vjp`` / ``spingtp_vjp`` give its
+                   reverse-mode derivative by the chain rule on that definition.
 
 Readings of points where the paper is silent or ambiguous are listed in the
 docstrings of the functions that take them.  Every function here is pinned by
@@ -25,9 +26,9 @@ library routines (scipy, sympy).
 """
 
 from .swsh import swsh, theta_part, goldberg_prefactor
-from .realbasis import q_matrix, real_index, BASIS_PAPER, BASIS_M0_PAIRED
+from .realbasis import q_matrix, real_index, conjugation_map, BASIS_PAPER, BASIS_M0_PAIRED
 from .gaunt import gauss_legendre_grid, gaunt_block, gaunt_full_quadrature
-from .spingtp import RealGauntTensor, spingtp
+from .spingtp import RealGauntTensor, spingtp, spingtp_vjp
 
 __all__ = [
     "swsh", "theta_part", "goldberg_prefactor",

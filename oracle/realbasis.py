@@ -84,3 +84,28 @@ def q_matrix(spins, L, basis=BASIS_PAPER) -> np.ndarray:
                     else:
                         raise ValueError("unknown basis convention")
     return Q
+
+
+def conjugation_map(spins, L, basis=BASIS_PAPER) -> np.ndarray:
+    """Real matrix J with conj(f) = sum_k (J x)[k] R_k for f = sum_k x[k] R_k.
+
+    From the conjugation relation of App. A.1, conj(sY_lm) = (-1)^(s+m) (-s)Y_l(-m):
+    conjugating the complex column Q[:, k] gives the column Q'[:, k] with
+    Q'[(-s, l, -m), k] = (-1)^(s+m) conj(Q[(s, l, m), k]), and J = Q^-1 Q' on the
+    existing slots (zero rows and columns at l < |s|).  Raises if J is not real.
+    """
+    spins = tuple(spins)
+    Q = q_matrix(spins, L, basis)
+    n = Q.shape[0]
+    Qc = np.zeros_like(Q)
+    for s in spins:
+        for l in range(abs(s), L + 1):
+            for m in range(-l, l + 1):
+                Qc[real_index(spins, L, -s, l, -m), :] = (-1.0) ** ((s + m) % 2) * np.conj(
+                    Q[real_index(spins, L, s, l, m), :])
+    live = [i for i in range(n) if np.abs(Q[:, i]).sum() > 0]
+    J = np.zeros((n, n), dtype=np.complex128)
+    J[np.ix_(live, live)] = np.linalg.solve(Q[np.ix_(live, live)], Qc[np.ix_(live, live)])
+    if np.abs(J.imag).max() > 1e-12:
+        raise AssertionError("conjugation is not a real map in this basis")
+    return J.real

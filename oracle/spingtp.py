@@ -160,6 +160,36 @@ class RealGauntTensor:
         return Y.reshape(lead + (len(self.spins), (self.Lout + 1) ** 2))
 
 
+    def vjp(self, x1, x2, g, chunk=None):
+        """Reverse-mode derivative of the bilinear map (float64).
+
+        For a scalar loss with dL/dy = g, the chain rule on
+        y[u,k3] = sum T[k1,k2,k3] x1[u,k1] x2[u,k2] gives
+          gx1[u,k1] = sum_{k2,k3} T[k1,k2,k3] x2[u,k2] g[u,k3],
+          gx2[u,k2] = sum_{k1,k3} T[k1,k2,k3] x1[u,k1] g[u,k3].
+        Returns (gx1, gx2) shaped like x1 and x2.
+        """
+        x1 = np.asarray(x1, dtype=np.float64)
+        x2 = np.asarray(x2, dtype=np.float64)
+        X1 = x1.reshape(-1, self.n1)
+        X2 = x2.reshape(-1, self.n2)
+        G = np.asarray(g, dtype=np.float64).reshape(-1, self.n3)
+        if not (X1.shape[0] == X2.shape[0] == G.shape[0]):
+            raise ValueError("x1, x2 and g hold different numbers of units")
+        U = X1.shape[0]
+        if chunk is None:
+            chunk = max(1, min(U, (1 << 24) // max(1, self.n1 * self.n2)))
+        MT = self.matrix.T.tocsr()  # [k3, (k1, k2)]
+        gx1 = np.empty((U, self.n1))
+        gx2 = np.empty((U, self.n2))
+        for u0 in range(0, U, chunk):
+            u1 = min(U, u0 + chunk)
+            R = np.asarray(G[u0:u1] @ MT).reshape(u1 - u0, self.n1, self.n2)  # sum_k3 T g
+            gx1[u0:u1] = np.einsum("uab,ub->ua", R, X2[u0:u1])
+            gx2[u0:u1] = np.einsum("uab,ua->ub", R, X1[u0:u1])
+        return gx1.reshape(x1.shape), gx2.reshape(x2.shape)
+
+
 @functools.lru_cache(maxsize=16)
 def _cached_tensor(L1, L2, Lout, spins, basis):
     return RealGauntTensor(L1, L2, Lout, spins, basis)
@@ -168,3 +198,8 @@ def _cached_tensor(L1, L2, Lout, spins, basis):
 def spingtp(x1, x2, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER) -> np.ndarray:
     """Oracle value of the SpinGTP forward for a batch of units (float64)."""
     return _cached_tensor(L1, L2, Lout, tuple(spins), basis).apply(x1, x2)
+
+
+def spingtp_vjp(x1, x2, g, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Oracle gradients (gx1, gx2) of sum(g * spingtp(x1, x2)) (float64)."""
+    return _cached_tensor(L1, L2, Lout, tuple(spins), basis).vjp(x1, x2, g)
