@@ -226,6 +226,72 @@ def run_v1(args):
         "table": table, "sweep": sweep}), flush=True)
 
 
+def run_backward(args):
+    """spingtp_backward on a forward workload: grad_x1 and grad_x2 of a loss with a
+    random dLoss/dout, timed per call of the C entry point (HIP events on the
+    launch stream, output buffers allocated before timing)."""
+    import ctypes
+
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2607_01408_amd import Plan, _lib, workloads
+
+    torch.cuda.set_device(0)
+    x1, x2, meta = workloads.make_pair(args.workload, dtype=args.dtype, L=args.L, device="cuda:0")
+    L, N, C = meta["L"], meta["N"], meta["C"]
+    U = N * C
+    g = workloads.draw(L, N, C, 6001, args.dtype, workloads.SPINS, "unit", "cuda:0")
+    plan = Plan(L, L, L, workloads.SPINS, args.dtype, valu_only=args.valu)
+    gx1, gx2 = torch.empty_like(x1), torch.empty_like(x2)
+    stream = torch.cuda.current_stream()
+    fn = _lib.lib().spingtp_backward
+    call = (plan.handle, x1.data_ptr(), x2.data_ptr(), g.data_ptr(), gx1.data_ptr(), gx2.data_ptr(), N, C,
+            ctypes.c_void_p(stream.cuda_stream))
+    print(f"[bench] backward {meta['workload']} L={L} units={U} {args.dtype} kernel={plan.kernel_info()}",
+          file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        assert fn(*call) == 0
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        fn(*call)
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    avg_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(starts, ends)]))
+    rng = np.random.default_rng(78)
+    idx = np.unique(np.concatenate([np.arange(min(64, U)), np.arange(max(0, U - 64), U),
+                                    rng.choice(U, size=min(U, args.parity_units), replace=False)]))
+    ti = torch.as_tensor(idx, device="cuda:0")
+    a, b, c = (t.view(U, -1)[ti].double().cpu().numpy() for t in (x1, x2, g))
+    r1, r2 = oracle.spingtp_vjp(a, b, c, L, L, L, workloads.SPINS)
+    got = np.concatenate([gx1.view(U, -1)[ti].double().cpu().numpy(), gx2.view(U, -1)[ti].double().cpu().numpy()])
+    ref = np.concatenate([r1, r2])
+    parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+    elem = 4 if args.dtype == "fp32" else 2
+    nc = 3 * (L + 1) ** 2
+    min_bytes = 5 * nc * elem  # read x1, x2, grad_out; write grad_x1, grad_x2
+    route_bytes = 6 * nc * elem  # two forward launches (grad_out read twice)
+    print(json.dumps({
+        "metric": f"backward (grad_x1 and grad_x2) edge-channel units/sec at L={L} {args.dtype}",
+        "value": U / (ms_per_step / 1e3), "unit": "units/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "avg_call_ms": avg_ms, "higher_is_better": True,
+        "dtype": args.dtype, "data": "synthetic",
+        "config": {"workload": meta["workload"], "L": L, "N": N, "C": C, "units": U,
+                   "kernel_family": plan.kernel_info()["family"]},
+        "hbm": {"min_bytes_per_unit": min_bytes, "route_bytes_per_unit": route_bytes,
+                "min_frac": min_bytes * U / (avg_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
+                "route_gbs": route_bytes * U / (avg_ms / 1e3) / 1e9},
+        "route_tflops": 2 * route_flops(L, L, L, True) * U / (avg_ms / 1e3) / 1e12,
+        "parity_rel_l2": parity, "parity_units": int(len(idx))}), flush=True)
+
+
 def run_sweep(args):
     """The degree sweep: SpinGTP kernel vs the direct O(L^6) dense contraction.
 
@@ -328,6 +394,8 @@ def main():
     ap.add_argument("--parity-units", type=int, default=2048)
     ap.add_argument("--sweep", action="store_true", help="run the degree sweep against the dense CG comparator")
     ap.add_argument("--sweep-degrees", type=int, nargs="+", default=[2, 4, 8, 12, 16])
+    ap.add_argument("--backward", action="store_true",
+                    help="time spingtp_backward (both gradients) on the chosen workload")
     ap.add_argument("--v1", action="store_true",
                     help="spingtp_forward_v1: the paper's V = 1 shapes and a degree sweep, both routes")
     ap.add_argument("--v1-sweep-degrees", type=int, nargs="+", default=[1, 2, 3, 4, 5, 6])
@@ -350,6 +418,9 @@ def main():
         return
     if args.v1:
         run_v1(args)
+        return
+    if args.backward:
+        run_backward(args)
         return
 
     import numpy as np

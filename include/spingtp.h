@@ -78,6 +78,10 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
 #define SPINGTP_V1_FOURIER 0x200u
 #define SPINGTP_V1_PRECONTRACT 0x400u
 
+/* For spingtp_plan_tables_host only: return the tables spingtp_backward uses
+ * (input 2's m = 0 mixing with the conjugation folded in). */
+#define SPINGTP_TABLES_BACKWARD 0x800u
+
 /*
  * Create a plan for degrees (L1, L2, Lout) and a spin set.
  *   0 <= L1, L2 <= 16, 0 <= Lout <= L1 + L2 (the product of degrees l1, l2 has
@@ -139,6 +143,45 @@ spingtp_status spingtp_forward(spingtp_plan plan, const void* x1, const void* x2
 spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void* x2, void* out,
                                   int64_t N, int64_t C, void* stream);
 
+/*
+ * Gradients of a scalar loss through out = SpinGTP(x1, x2) of spingtp_forward:
+ * given grad_out = dLoss/dout, writes
+ *   grad_x1[n][c][k1] = sum_{k2,k3} T[k1][k2][k3] x2[n][c][k2] grad_out[n][c][k3],
+ *   grad_x2[n][c][k2] = sum_{k1,k3} T[k1][k2][k3] x1[n][c][k1] grad_out[n][c][k3]
+ * (the chain rule on the real bilinear map T of spingtp_dense_tensor_host).
+ * Route: let J be the real matrix of complex conjugation on real-basis
+ * coefficients (App. A.1: conj(sY_lm) = (-1)^(s+m) (-s)Y_l(-m); a signed
+ * permutation, see spingtp_conj_map_host).  Conjugating the Gaunt integral of
+ * Sec. 3.2 eq. generalized_gaunt gives T[k1][k2][k3] = sum_j T'[k3][j][k1] J[j][k2]
+ * with T' the tensor of degrees (Lout, L2, L1), so grad_x1 = SpinGTP'(grad_out,
+ * J x2) and grad_x2 = SpinGTP''(grad_out, J x1): one launch of the plan's forward
+ * kernel each, on backward tables where J is folded into the input-2 mixing of
+ * the m = 0 slots of the |s| = 1 sectors (the only slots J moves: with
+ * SPINGTP_BASIS_REAL_PAPER they swap between s = +1 and -1 with a sign change; J is
+ * the identity for SPINGTP_BASIS_REAL_M0_PAIRED and spins {0}).  Built for plans
+ * with L1 = L2 = Lout that have a spingtp_forward kernel; otherwise
+ * SPINGTP_ERR_UNSUPPORTED.
+ *   x1, x2, grad_out: as x1, x2, out of spingtp_forward; grad_x1, grad_x2: same
+ *   shapes as x1, x2 (either may be NULL: not computed), overwritten; slots with
+ *   l < |s| are written 0.  Same dtype, 16-byte alignment and error rules as
+ *   spingtp_forward; outputs must not overlap inputs.
+ * Asynchronous on `stream`, ordered on it; no allocation; same arithmetic as the
+ * forward kernel of the plan.
+ */
+spingtp_status spingtp_backward(spingtp_plan plan, const void* x1, const void* x2, const void* grad_out,
+                                void* grad_x1, void* grad_x2, int64_t N, int64_t C, void* stream);
+
+/*
+ * Host-only: the conjugation map J of degree L (one word per destination slot j
+ * of a [n_spins][(L+1)^2] vector: (J x)[j] = x[w & 0xffff], negated if bit 16 of
+ * w is set, 0 if bit 17 is set (slots with l < |s|)), derived from the real basis
+ * columns of App. C and the conjugation relation of App. A.1.  Same argument
+ * rules as spingtp_plan_create with L1 = L2 = Lout = L.  Writes min(capacity,
+ * total) words to `words` (may be NULL when capacity is 0) and the total to *count.
+ */
+spingtp_status spingtp_conj_map_host(int L, const int* spins, int n_spins, unsigned flags, uint32_t* words,
+                                     size_t capacity, size_t* count);
+
 /* Free the plan's device tables.  The caller must ensure that no forward using
  * the plan is still running.  NULL is accepted (no-op). */
 spingtp_status spingtp_plan_destroy(spingtp_plan plan);
@@ -153,6 +196,8 @@ const char* spingtp_status_string(spingtp_status s);
  * *n_tables; `dims` (may be NULL) receives 8 ints:
  *   {n_theta, n_phi, L1, L2, Lout, n_spins, per_theta_block, global_block}.
  * The table layout is the one documented in csrc/layout.h of the library source.
+ * With SPINGTP_TABLES_BACKWARD in `flags`: the tables of spingtp_backward
+ * (SPINGTP_ERR_UNSUPPORTED if the conjugation map cannot be folded into them).
  */
 spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spins, int n_spins,
                                         unsigned flags, double* tables, size_t capacity,

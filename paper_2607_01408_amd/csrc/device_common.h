@@ -204,10 +204,12 @@ __device__ __forceinline__ void store_tile(uint16_t* __restrict__ dst, int nvali
 
 // Step (A) for one input of degree L at one theta node.
 //   xr  : this lane's LDS row ([n_spins][(L+1)^2], spin order -1, 0, +1)
-//   tb  : the node's table block; n0: the global N0 mixing.
+//   tb  : the node's table block; n0: the global N0 mixing of input 1, followed by
+//         that of input 2 (equal except in the tables of spingtp_backward);
+//   second: this lane transforms input 2.
 template <int L, int LA, bool SPIN>
 __device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const float* __restrict__ tb,
-                                                      const float* __restrict__ n0, float (&Ac)[L + 1],
+                                                      const float* __restrict__ n0, bool second, float (&Ac)[L + 1],
                                                       float (&As)[L + 1], float (&Bc)[L + 1], float (&Bs)[L + 1],
                                                       float (&Cc)[L + 1], float (&Cs)[L + 1], float& dl, float& ep) {
     constexpr Layout Y = make_layout(LA, 0, 0);  // only the per-node A offsets are used
@@ -251,10 +253,13 @@ __device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const flo
             wpl = fmaf(xp[l * l + l], w, wpl);
             wmi = fmaf(xm[l * l + l], w, wmi);
         }
-        Bc[0] = fmaf(n0[0], wpl, n0[1] * wmi);
-        Cc[0] = fmaf(n0[2], wpl, n0[3] * wmi);
-        dl = fmaf(n0[4], wpl, n0[5] * wmi);
-        ep = fmaf(n0[6], wpl, n0[7] * wmi);
+        float c[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = second ? n0[8 + i] : n0[i];
+        Bc[0] = fmaf(c[0], wpl, c[1] * wmi);
+        Cc[0] = fmaf(c[2], wpl, c[3] * wmi);
+        dl = fmaf(c[4], wpl, c[5] * wmi);
+        ep = fmaf(c[6], wpl, c[7] * wmi);
         Bs[0] = 0.f;
         Cs[0] = 0.f;
     } else {

@@ -156,8 +156,8 @@ __global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fw
     // (A) both inputs at this node
     float Ac[L1 + 1], As[L1 + 1], Bc[L1 + 1], Bs[L1 + 1], Cc[L1 + 1], Cs[L1 + 1], d1, e1;
     float ac[L2 + 1], as[L2 + 1], bc[L2 + 1], bs[L2 + 1], cc[L2 + 1], cs2[L2 + 1], d2, e2;
-    coef_to_theta_fourier<L1, LA, SPIN>(X1 + lane * S::ST1, tb, g + Y.n0, Ac, As, Bc, Bs, Cc, Cs, d1, e1);
-    coef_to_theta_fourier<L2, LA, SPIN>(X2 + lane * S::ST2, tb, g + Y.n0, ac, as, bc, bs, cc, cs2, d2, e2);
+    coef_to_theta_fourier<L1, LA, SPIN>(X1 + lane * S::ST1, tb, g + Y.n0, false, Ac, As, Bc, Bs, Cc, Cs, d1, e1);
+    coef_to_theta_fourier<L2, LA, SPIN>(X2 + lane * S::ST2, tb, g + Y.n0, true, ac, as, bc, bs, cc, cs2, d2, e2);
 
     // (B)-(D) over the phi nodes, k and n_phi - k together
     float R0c[LO + 1], R0s[LO + 1], P1c[LO + 1], P1s[LO + 1], P2c[LO + 1], P2s[LO + 1];
@@ -419,7 +419,7 @@ __device__ __forceinline__ void pair_spectra(const float* xr, const float* __res
     constexpr int NP = Y.NP;
     constexpr int KP = (NP - 1) / 2;
     float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
-    coef_to_theta_fourier<L, L, SPIN>(xr, tb, g + Y.n0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
+    coef_to_theta_fourier<L, L, SPIN>(xr, tb, g + Y.n0, sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
     const float sg = sub ? -1.f : 1.f;
 
     // accumulators: cosine spectra on the even lane, sine spectra on the odd lane
@@ -798,35 +798,3 @@ const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype)
 }
 
 }  // namespace spingtp
-
-namespace {
-
-spingtp_status forward_impl(spingtp_plan plan, const spingtp::KernelEntry* k, const void* x1, const void* x2,
-                            void* out, int64_t N, int64_t C, bool shared_x2, void* stream) {
-    if (plan == nullptr || N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
-    if (N == 0 || C == 0) return SPINGTP_OK;
-    if (N > (int64_t{1} << 40) / C) return SPINGTP_ERR_INVALID_ARG;
-    if (x1 == nullptr || x2 == nullptr || out == nullptr) return SPINGTP_ERR_INVALID_ARG;
-    const auto misaligned = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; };
-    if (misaligned(x1) || misaligned(x2) || misaligned(out)) return SPINGTP_ERR_INVALID_ARG;
-    if (k == nullptr) return SPINGTP_ERR_UNSUPPORTED;
-    int cur = -1;
-    if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
-    if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
-    const uint32_t* aux = k->family == 5 ? plan->d_pre : plan->d_aux;
-    const hipError_t e =
-        k->launch(x1, x2, out, N * C, shared_x2 ? C : 1, plan->d_tab, aux, static_cast<hipStream_t>(stream));
-    return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
-}
-
-}  // namespace
-
-extern "C" spingtp_status spingtp_forward(spingtp_plan plan, const void* x1, const void* x2, void* out, int64_t N,
-                                          int64_t C, void* stream) {
-    return forward_impl(plan, plan ? plan->kernel : nullptr, x1, x2, out, N, C, false, stream);
-}
-
-extern "C" spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void* x2, void* out,
-                                             int64_t N, int64_t C, void* stream) {
-    return forward_impl(plan, plan ? plan->kernel_v1 : nullptr, x1, x2, out, N, C, true, stream);
-}

@@ -355,7 +355,8 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
 
         // (A) this lane's input at node j
         float Pc[3][L + 1], Ps[3][L + 1], dl, ep;
-        coef_to_theta_fourier<L, L, true>(xr, tb, tab + Y.n0, Pc[0], Ps[0], Pc[1], Ps[1], Pc[2], Ps[2], dl, ep);
+        coef_to_theta_fourier<L, L, true>(xr, tb, tab + Y.n0, h != 0, Pc[0], Ps[0], Pc[1], Ps[1], Pc[2], Ps[2], dl,
+                                          ep);
 
         // step-(B) operands of the three polynomials of both inputs
         v8h oh[2][3], ol[2][3];

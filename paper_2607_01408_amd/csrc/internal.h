@@ -61,8 +61,26 @@ void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
 void build_mfma_operands(int L, std::vector<uint32_t>& out);
 
 // Builds the float64 tables (layout.h) into `out`; returns false on a failed
-// self-check.  spin_mode: 0 = {0}, 1 = {-1, 0, +1}.
-bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::vector<double>& out);
+// self-check.  spin_mode: 0 = {0}, 1 = {-1, 0, +1}.  conj_input2: the tables of
+// spingtp_backward, where input 2 enters conjugated (its N0 mixing absorbs the
+// conjugation map; false if that map is not of the form this needs).
+bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::vector<double>& out,
+                  bool conj_input2 = false);
+
+// Real matrix J of complex conjugation on real-basis coefficients of degree <= L
+// (conj of sum x[k] R_k is sum (J x)[k] R_k; App. A.1 conjugation relation), as
+// one word per destination slot j: (J x)[j] = +-x[src] with src in the low 16 bits,
+// kConjNeg for the sign, kConjZero for slots with l < |s| (written 0).  Returns
+// false if J is not a signed permutation.
+constexpr uint32_t kConjNeg = 1u << 16;
+constexpr uint32_t kConjZero = 1u << 17;
+bool build_conj_map(int L, const int* spins, int n_spins, unsigned flags, std::vector<uint32_t>& out);
+
+// Argument checks and launch of one forward kernel (api.cpp).  shared_x2: x2
+// holds one row per edge (spingtp_forward_v1), else one per unit.  tab: the
+// plan tables to use (the plan's own when nullptr).
+spingtp_status run_forward(spingtp_plan plan, const KernelEntry* k, const void* x1, const void* x2, void* out,
+                           int64_t N, int64_t C, bool shared_x2, void* stream, const float* tab = nullptr);
 
 // Dense real tensor of the operation (see spingtp_dense_tensor_host), float64.
 void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
@@ -81,6 +99,8 @@ struct spingtp_plan_s {
     size_t n_tab;
     uint32_t* d_aux;  // matrix-core operand tables, nullptr for the vector-ALU kernels
     uint32_t* d_pre;  // sparse tensor of the precontracted kernel, nullptr if not used
+    float* d_tab_bwd;  // tables of spingtp_backward (d_tab when equal), nullptr without a backward
+    bool own_tab_bwd;  // d_tab_bwd is a separate allocation
     const spingtp::KernelEntry* kernel;     // spingtp_forward
     const spingtp::KernelEntry* kernel_v1;  // spingtp_forward_v1 (x2 shared by the channels of an edge)
 };

@@ -28,7 +28,7 @@ namespace spingtp {
 struct Layout {
     int L1, L2, LO, LA, TM, NT, NP;
     int triA, triO;
-    int n0, m0, cosT, sinT, glob;
+    int n0, n0b, m0, cosT, sinT, glob;
     int a0c, a0s, aup, aum, aw, e0c, e0s, e1p, e1m, e1z, pb;
     int total;
 };
@@ -50,8 +50,9 @@ __host__ __device__ constexpr Layout make_layout(int L1, int L2, int LO) {
     y.triA = tri_size(y.LA);
     y.triO = tri_size(LO);
     y.n0 = 0;
-    y.m0 = 8;
-    y.cosT = 16;
+    y.n0b = 8;
+    y.m0 = 16;
+    y.cosT = 24;
     y.sinT = y.cosT + y.NP * (y.TM + 1);
     y.glob = round4(y.sinT + y.NP * (y.TM + 1));
     y.a0c = 0;

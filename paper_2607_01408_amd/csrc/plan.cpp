@@ -107,9 +107,85 @@ Cplx q_m0(unsigned flags, int s, int sigma) {
     return Cplx{0.0, h};
 }
 
+// Complex expansion of the real basis column (sigma, l, k) (eq. real_swsh, App. C):
+// up to two entries (s, m, Q[(s,l,m),(sigma,l,k)]); returns their number.
+struct QEnt {
+    int s, m;
+    Cplx q;
+};
+int real_column(int sigma, int k, unsigned flags, QEnt* e) {
+    const double h = 1.0 / kSqrt2;
+    if (k > 0) {
+        e[0] = {sigma, k, {h, 0.0}};
+        e[1] = {-sigma, -k, {(((k + sigma) % 2) != 0 ? -h : h), 0.0}};
+        return 2;
+    }
+    if (k < 0) {
+        const int a = -k;
+        e[0] = {sigma, a, {0.0, h}};
+        e[1] = {-sigma, k, {0.0, (((a + sigma) % 2) != 0 ? h : -h)}};
+        return 2;
+    }
+    if (sigma == 0 || flags == SPINGTP_BASIS_REAL_PAPER) {
+        e[0] = {sigma, 0, {1.0, 0.0}};
+        return 1;
+    }
+    const int sa = std::abs(sigma);
+    e[0] = {sa, 0, q_m0(flags, 1, sigma)};
+    e[1] = {-sa, 0, q_m0(flags, -1, sigma)};
+    return 2;
+}
+
 }  // namespace
 
-bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::vector<double>& out) {
+bool build_conj_map(int L, const int* spins, int n_spins, unsigned flags, std::vector<uint32_t>& out) {
+    const int nb = (L + 1) * (L + 1);
+    out.assign(static_cast<size_t>(n_spins) * nb, kConjZero);
+    auto slot = [&](int si, int l, int k) { return si * nb + l * l + l + k; };
+    for (int si = 0; si < n_spins; ++si)
+        for (int l = std::abs(spins[si]); l <= L; ++l)
+            for (int k = -l; k <= l; ++k) {
+                // conjugated column: conj(sY_lm) = (-1)^(s+m) (-s)Y_l(-m) (App. A.1)
+                QEnt e[2], c[2];
+                const int n = real_column(spins[si], k, flags, e);
+                for (int i = 0; i < n; ++i) {
+                    const double sg = ((e[i].s + e[i].m) % 2 != 0) ? -1.0 : 1.0;
+                    c[i] = {-e[i].s, -e[i].m, {sg * e[i].q.re, -sg * e[i].q.im}};
+                }
+                // the real column j with Q[:, j] = +-(conjugated column): J[j][k] = +-1
+                bool found = false;
+                for (int sj = 0; sj < n_spins && !found; ++sj) {
+                    if (std::abs(spins[sj]) > l) continue;
+                    for (int kj = -l; kj <= l && !found; ++kj) {
+                        QEnt f[2];
+                        const int nf = real_column(spins[sj], kj, flags, f);
+                        if (nf != n) continue;
+                        for (double sign : {1.0, -1.0}) {
+                            bool all = true;
+                            for (int i = 0; i < n && all; ++i) {
+                                bool hit = false;
+                                for (int q = 0; q < nf; ++q)
+                                    hit |= f[q].s == c[i].s && f[q].m == c[i].m &&
+                                           std::fabs(sign * f[q].q.re - c[i].q.re) < 1e-12 &&
+                                           std::fabs(sign * f[q].q.im - c[i].q.im) < 1e-12;
+                                all = hit;
+                            }
+                            if (all) {
+                                // (J x)[j] = sign x[k]
+                                out[slot(sj, l, kj)] = static_cast<uint32_t>(slot(si, l, k)) | (sign < 0 ? kConjNeg : 0u);
+                                found = true;
+                                break;
+                            }
+                        }
+                    }
+                }
+                if (!found) return false;
+            }
+    return true;
+}
+
+bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::vector<double>& out,
+                  bool conj_input2) {
     const Layout Y = make_layout(L1, L2, LO);
     out.assign(Y.total, 0.0);
     const double sq2 = kSqrt2;
@@ -140,6 +216,46 @@ bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::ve
             out[Y.m0 + row * 4 + 3] = -qm.im;
         }
     }
+    // Input 2's copy of the N0 mixing.  For spingtp_backward input 2 enters
+    // conjugated (J x2): J must act on the m = 0 slots of the |s| = 1 sectors only,
+    // as (J x)[(sigma,l,0)] = sign_sigma x[(pi(sigma),l,0)] for every l, so that
+    // W'_sigma = sign_sigma W_pi(sigma) folds into the two columns of N0.
+    for (int i = 0; i < 8; ++i) out[Y.n0b + i] = out[Y.n0 + i];
+    if (conj_input2) {
+        const int s3[3] = {-1, 0, 1}, s1[1] = {0};
+        std::vector<uint32_t> J;
+        if (!build_conj_map(L2, spin_mode ? s3 : s1, spin_mode ? 3 : 1, flags, J)) return false;
+        const int nb = (L2 + 1) * (L2 + 1);
+        int pi[2] = {0, 1};
+        double sg[2] = {1.0, 1.0};
+        for (int j = 0; j < static_cast<int>(J.size()); ++j) {
+            if (J[j] & kConjZero) continue;
+            const int si = j / nb, r = j % nb, l = static_cast<int>(std::sqrt(static_cast<double>(r)) + 1e-9);
+            const bool m0_spin = spin_mode == 1 && si != 1 && r == l * l + l;
+            const int src = static_cast<int>(J[j] & 0xffffu);
+            const double sign = (J[j] & kConjNeg) ? -1.0 : 1.0;
+            if (!m0_spin) {
+                if (src != j || sign != 1.0) return false;
+                continue;
+            }
+            // column 0 of N0 is sigma = +1 (spin block 2), column 1 is sigma = -1 (block 0)
+            const int col = si == 2 ? 0 : 1;
+            const int ssi = src / nb, sr = src % nb;
+            if (sr != r || ssi == 1) return false;
+            const int scol = ssi == 2 ? 0 : 1;
+            if (l == 1) {
+                pi[col] = scol;
+                sg[col] = sign;
+            } else if (pi[col] != scol || sg[col] != sign) {
+                return false;
+            }
+        }
+        double n0b[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int q = 0; q < 4; ++q)
+            for (int c = 0; c < 2; ++c) n0b[2 * q + pi[c]] += out[Y.n0 + 2 * q + c] * sg[c];
+        for (int i = 0; i < 8; ++i) out[Y.n0b + i] = n0b[i];
+    }
+
     for (int k = 0; k < Y.NP; ++k) {
         for (int t = 0; t <= Y.TM; ++t) {
             const double ang = 2.0 * kPi * static_cast<double>((k * t) % Y.NP) / Y.NP;
@@ -356,33 +472,8 @@ void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, u
         for (int l = std::abs(spins[si]); l <= LM; ++l)
             for (int m = -l; m <= l; ++m)
                 for (int j = 0; j < Y.NT; ++j) TH(si, l, m, j) = swsh_theta(spins[si], l, m, std::acos(gx[j]));
-    // real column (sigma, l, k) -> up to two complex rows (s, m) with values (eq. real_swsh, App. C)
-    struct Ent {
-        int s, m;
-        Cplx q;
-    };
-    auto column = [&](int sigma, int k, Ent* e) -> int {
-        const double h = 1.0 / kSqrt2;
-        if (k > 0) {
-            e[0] = {sigma, k, {h, 0.0}};
-            e[1] = {-sigma, -k, {(((k + sigma) % 2) != 0 ? -h : h), 0.0}};
-            return sigma == 0 ? 2 : 2;
-        }
-        if (k < 0) {
-            const int a = -k;
-            e[0] = {sigma, a, {0.0, h}};
-            e[1] = {-sigma, k, {0.0, (((a + sigma) % 2) != 0 ? h : -h)}};
-            return 2;
-        }
-        if (sigma == 0 || flags == SPINGTP_BASIS_REAL_PAPER) {
-            e[0] = {sigma, 0, {1.0, 0.0}};
-            return 1;
-        }
-        const int sa = std::abs(sigma);
-        e[0] = {sa, 0, q_m0(flags, 1, sigma)};
-        e[1] = {-sa, 0, q_m0(flags, -1, sigma)};
-        return 2;
-    };
+    using Ent = QEnt;
+    auto column = [&](int sigma, int k, Ent* e) -> int { return real_column(sigma, k, flags, e); };
     auto cmul = [](Cplx a, Cplx b) { return Cplx{a.re * b.re - a.im * b.im, a.re * b.im + a.im * b.re}; };
     // loop over real (k1, k2) and complex expansions; G picks m3 = m1 + m2, s3 = s1 + s2
     for (int i1 = 0; i1 < n_spins; ++i1)
@@ -484,14 +575,16 @@ const char* spingtp_status_string(spingtp_status s) {
 spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spins, int n_spins,
                                         unsigned flags, double* tables, size_t capacity,
                                         size_t* n_tables, int* dims) {
+    const bool backward = (flags & SPINGTP_TABLES_BACKWARD) != 0;
+    flags &= ~SPINGTP_TABLES_BACKWARD;
     int spin_mode = 0;
     spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
     if (n_tables == nullptr || (capacity > 0 && tables == nullptr)) return SPINGTP_ERR_INVALID_ARG;
     std::vector<double> tab;
     try {
-        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags & ~kRouteFlags, tab))
-            return SPINGTP_ERR_INTERNAL;
+        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags & ~kRouteFlags, tab, backward))
+            return backward ? SPINGTP_ERR_UNSUPPORTED : SPINGTP_ERR_INTERNAL;
     } catch (const std::bad_alloc&) {
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
@@ -562,6 +655,24 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
     return SPINGTP_OK;
 }
 
+spingtp_status spingtp_conj_map_host(int L, const int* spins, int n_spins, unsigned flags, uint32_t* words,
+                                     size_t capacity, size_t* count) {
+    if (count == nullptr || (capacity > 0 && words == nullptr)) return SPINGTP_ERR_INVALID_ARG;
+    int spin_mode = 0;
+    const spingtp_status st = check_args(L, L, L, spins, n_spins, flags, &spin_mode);
+    if (st != SPINGTP_OK) return st;
+    try {
+        std::vector<uint32_t> w;
+        if (!spingtp::build_conj_map(L, spins, n_spins, flags & ~kRouteFlags, w)) return SPINGTP_ERR_INTERNAL;
+        *count = w.size();
+        const size_t n = w.size() < capacity ? w.size() : capacity;
+        if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));
+    } catch (const std::bad_alloc&) {
+        return SPINGTP_ERR_OUT_OF_MEMORY;
+    }
+    return SPINGTP_OK;
+}
+
 spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, int n_spins,
                                    spingtp_dtype dtype, unsigned flags, spingtp_plan* out_plan) {
     if (out_plan == nullptr) return SPINGTP_ERR_INVALID_ARG;
@@ -588,11 +699,19 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     const unsigned basis = flags & ~kRouteFlags;
 
     std::vector<double> tab;
+    std::vector<double> tab_bwd;
     std::vector<uint32_t> aux, pre;
+    bool has_backward = false, same_bwd = false;
     try {
         if (!spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
         if (k != nullptr && k->family == 4) spingtp::build_mfma_operands(L1, aux);
         if (kv1->family == 5) spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre);
+        // spingtp_backward: square plans with a forward kernel, input 2 conjugated
+        if (k != nullptr && L1 == L2 && L2 == Lout &&
+            spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab_bwd, true)) {
+            has_backward = true;
+            same_bwd = tab_bwd == tab;
+        }
     } catch (const std::bad_alloc&) {
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
@@ -622,18 +741,28 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
         return err;
     };
     uint32_t *da = nullptr, *dpre = nullptr;
+    float* dbwd = nullptr;
     e = upload(aux, &da);
     if (e == hipSuccess) e = upload(pre, &dpre);
-    if (e != hipSuccess) {
+    if (e == hipSuccess && has_backward && !same_bwd) {
+        std::vector<float> f(tab_bwd.size());
+        for (size_t i = 0; i < tab_bwd.size(); ++i) f[i] = static_cast<float>(tab_bwd[i]);
+        e = hipMalloc(&dbwd, f.size() * sizeof(float));
+        if (e == hipSuccess) e = hipMemcpy(dbwd, f.data(), f.size() * sizeof(float), hipMemcpyHostToDevice);
+    }
+    auto release = [&]() {
         if (da != nullptr) (void)hipFree(da);
+        if (dpre != nullptr) (void)hipFree(dpre);
+        if (dbwd != nullptr) (void)hipFree(dbwd);
         (void)hipFree(d);
+    };
+    if (e != hipSuccess) {
+        release();
         return e == hipErrorOutOfMemory ? SPINGTP_ERR_OUT_OF_MEMORY : SPINGTP_ERR_HIP;
     }
     spingtp_plan p = new (std::nothrow) spingtp_plan_s;
     if (p == nullptr) {
-        if (da != nullptr) (void)hipFree(da);
-        if (dpre != nullptr) (void)hipFree(dpre);
-        (void)hipFree(d);
+        release();
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
     p->L1 = L1;
@@ -648,6 +777,8 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     p->n_tab = tabf.size();
     p->d_aux = da;
     p->d_pre = dpre;
+    p->d_tab_bwd = has_backward ? (same_bwd ? d : dbwd) : nullptr;
+    p->own_tab_bwd = dbwd != nullptr;
     p->kernel = k;
     p->kernel_v1 = kv1;
     *out_plan = p;
@@ -662,6 +793,7 @@ spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
     if (e == hipSuccess) e = hipFree(plan->d_tab);
     if (e == hipSuccess && plan->d_aux != nullptr) e = hipFree(plan->d_aux);
     if (e == hipSuccess && plan->d_pre != nullptr) e = hipFree(plan->d_pre);
+    if (e == hipSuccess && plan->own_tab_bwd) e = hipFree(plan->d_tab_bwd);
     if (cur != plan->device) (void)hipSetDevice(cur);
     delete plan;
     return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;

@@ -76,6 +76,18 @@ def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
     return out
 
 
+def conj_map_host(L, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """spingtp_conj_map_host: the conjugation map words of degree L (uint32)."""
+    arr, n = _spin_array(spins)
+    count = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().spingtp_conj_map_host(L, arr, n, basis, None, 0, ctypes.byref(count)),
+               "spingtp_conj_map_host")
+    out = np.zeros(count.value, dtype=np.uint32)
+    _lib.check(_lib.lib().spingtp_conj_map_host(L, arr, n, basis, out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
+                                                out.size, ctypes.byref(count)), "spingtp_conj_map_host")
+    return out
+
+
 class Plan:
     """spingtp_plan_create / spingtp_forward / spingtp_plan_destroy.
 
@@ -165,6 +177,27 @@ class Plan:
         _lib.check(fn(self._handle, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, C,
                       ctypes.c_void_p(stream.cuda_stream)), "spingtp_forward_v1" if shared else "spingtp_forward")
         return out
+
+    def backward(self, x1, x2, grad_out, need_x1=True, need_x2=True, stream=None):
+        """spingtp_backward: (grad_x1, grad_x2) of a loss with dLoss/dout = grad_out (None where not
+        requested)."""
+        import torch
+
+        N, C = x1.shape[0], x1.shape[1]
+        for t, shape in ((x1, self.shape_in(1)), (x2, self.shape_in(2)), (grad_out, self.shape_out)):
+            if (t.dim() != 4 or tuple(t.shape) != (N, C) + tuple(shape) or t.dtype != self.torch_dtype
+                    or not t.is_cuda or not t.is_contiguous()):
+                raise ValueError("x1, x2, grad_out must be contiguous [N, C, n_spins, (L+1)^2] device tensors "
+                                 "of the plan's dtype")
+        gx1 = torch.empty_like(x1) if need_x1 else None
+        gx2 = torch.empty_like(x2) if need_x2 else None
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+        _lib.check(_lib.lib().spingtp_backward(self._handle, x1.data_ptr(), x2.data_ptr(), grad_out.data_ptr(),
+                                               gx1.data_ptr() if gx1 is not None else None,
+                                               gx2.data_ptr() if gx2 is not None else None, N, C,
+                                               ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward")
+        return gx1, gx2
 
     __call__ = forward
 

@@ -75,9 +75,10 @@ def test_status_strings(built_library):
         assert len(_lib.message(s)) >= 2
 
 
-def emulate_kernel(x1, x2, L1, L2, LO, spin, basis):
-    """float64 re-enactment of the forward kernel from the host tables (layout.h)."""
-    tab, dims = plan_tables_host(L1, L2, LO, (-1, 0, 1) if spin else (0,), basis)
+def emulate_kernel(x1, x2, L1, L2, LO, spin, basis, backward=False):
+    """float64 re-enactment of the forward kernel from the host tables (layout.h);
+    with backward=True on the tables of spingtp_backward."""
+    tab, dims = plan_tables_host(L1, L2, LO, (-1, 0, 1) if spin else (0,), basis | (0x800 if backward else 0))
     NT, NP, PB, GLOB = dims["n_theta"], dims["n_phi"], dims["per_theta_block"], dims["global_block"]
     LA, TM = max(L1, L2), max(L1, L2, LO)
     triA, triO = (LA + 1) * (LA + 2) // 2, (LO + 1) * (LO + 2) // 2
@@ -85,17 +86,17 @@ def emulate_kernel(x1, x2, L1, L2, LO, spin, basis):
     a0c, a0s, aup, aum, aw = 0, triA, 2 * triA, 3 * triA, 4 * triA
     e0c = aw + LA + 1
     e0s, e1p, e1m, e1z = e0c + triO, e0c + 2 * triO, e0c + 3 * triO, e0c + 4 * triO
-    N0 = tab[0:8].reshape(4, 2)
-    M0 = tab[8:16].reshape(2, 4)
-    COS = tab[16:16 + NP * (TM + 1)].reshape(NP, TM + 1)
-    SIN = tab[16 + NP * (TM + 1):16 + 2 * NP * (TM + 1)].reshape(NP, TM + 1)
+    N0 = (tab[0:8].reshape(4, 2), tab[8:16].reshape(4, 2))  # input 1, input 2
+    M0 = tab[16:24].reshape(2, 4)
+    COS = tab[24:24 + NP * (TM + 1)].reshape(NP, TM + 1)
+    SIN = tab[24 + NP * (TM + 1):24 + 2 * NP * (TM + 1)].reshape(NP, TM + 1)
     NS = 3 if spin else 1
     U = x1.shape[0]
 
     def block(x, L, si):
         return x[:, si * (L + 1) ** 2:(si + 1) * (L + 1) ** 2]
 
-    def fourier(x, L, tb):
+    def fourier(x, L, tb, n0):
         x0 = block(x, L, 1 if spin else 0)
         P = {k: np.zeros((U, L + 1)) for k in ("Ac", "As", "Bc", "Bs", "Cc", "Cs")}
         for t in range(L + 1):
@@ -118,15 +119,15 @@ def emulate_kernel(x1, x2, L1, L2, LO, spin, basis):
                 P["Cc"][:, t], P["Cs"][:, t] = vp - vm, up - um
             wpl = sum(xp[:, l * l + l] * tb[aw + l] for l in range(1, L + 1)) if L else np.zeros(U)
             wmi = sum(xm[:, l * l + l] * tb[aw + l] for l in range(1, L + 1)) if L else np.zeros(U)
-            v = N0 @ np.stack([wpl, wmi])
+            v = n0 @ np.stack([wpl, wmi])
             P["Bc"][:, 0], P["Cc"][:, 0], d, e = v
         return P, d, e
 
     y = np.zeros((U, NS * (LO + 1) ** 2))
     for j in range(NT):
         tb = tab[GLOB + j * PB:GLOB + (j + 1) * PB]
-        F1, d1, e1 = fourier(x1, L1, tb)
-        F2, d2, e2 = fourier(x2, L2, tb)
+        F1, d1, e1 = fourier(x1, L1, tb, N0[0])
+        F2, d2, e2 = fourier(x2, L2, tb, N0[1])
 
         def val(P, key, L, k):
             return P[key + "c"] @ COS[k, :L + 1] + P[key + "s"] @ SIN[k, :L + 1]
@@ -243,7 +244,7 @@ def emulate_mfma_kernel(x1, x2, L, basis):
     a0c, a0s, aup, aum, aw = 0, triA, 2 * triA, 3 * triA, 4 * triA
     e0c = aw + L + 1
     e1p, e1m, e1z = e0c + 2 * triA, e0c + 3 * triA, e0c + 4 * triA
-    N0, M0 = tab[0:8].reshape(4, 2), tab[8:16].reshape(2, 4)
+    N0, M0 = tab[0:8].reshape(4, 2), tab[16:24].reshape(2, 4)  # forward tables: input 2 mixing = input 1
     BO = (L + 1) ** 2
     U = x1.shape[0]
 
@@ -444,5 +445,47 @@ def test_plan_create_route_flags(built_library):
     assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x200 | 0x400, ctypes.byref(plan)) == 1
     # precontraction forced where no precontracted kernel is built (rows of 192)
     assert built_library.spingtp_plan_create(7, 7, 7, S, 3, 0, 0x400, ctypes.byref(plan)) == 2
-    assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x800, ctypes.byref(plan)) == 1  # unknown bit
+    assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x800, ctypes.byref(plan)) == 1  # tables-only bit
+    assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x1000, ctypes.byref(plan)) == 1  # unknown bit
     assert not plan.value
+
+
+@pytest.mark.parametrize("L", [0, 1, 2, 4, 6, 16])
+@pytest.mark.parametrize("spins,basis", [((-1, 0, 1), 0), ((-1, 0, 1), 1), ((0,), 0)])
+def test_conj_map_matches_oracle(built_library, L, spins, basis):
+    """The library's conjugation map (used by spingtp_backward) equals the oracle's J."""
+    from oracle.realbasis import conjugation_map
+    from paper_2607_01408_amd.spingtp import conj_map_host
+
+    words = conj_map_host(L, spins, basis)
+    n = len(spins) * (L + 1) ** 2
+    assert words.size == n
+    J = np.zeros((n, n))
+    for j, w in enumerate(words):
+        if w & (1 << 17):
+            continue
+        J[j, w & 0xFFFF] = -1.0 if w & (1 << 16) else 1.0
+    if L <= 6:
+        assert np.array_equal(J, conjugation_map(spins, L, basis))
+    live = valid_mask(spins, L)
+    assert np.array_equal((words & (1 << 17)) == 0, live)
+
+
+@pytest.mark.parametrize("L,spin,basis", [(1, True, 0), (2, True, 0), (3, True, 1), (4, True, 0), (6, True, 0),
+                                          (3, False, 0), (8, True, 0)])
+def test_backward_tables_reproduce_oracle(built_library, L, spin, basis):
+    """spingtp_backward runs the forward kernel on (grad_out, x2) with its backward
+    tables; re-enacted on the CPU from those tables this is the oracle's grad_x1
+    (and, with x1 in place of x2, its grad_x2)."""
+    spins = (-1, 0, 1) if spin else (0,)
+    rng = np.random.default_rng(70 + L)
+    n = len(spins) * (L + 1) ** 2
+    x1, x2, g = (rng.standard_normal((4, n)) * valid_mask(spins, L) for _ in range(3))
+    r1, r2 = oracle.RealGauntTensor(L, L, L, spins, basis).vjp(x1, x2, g)
+    y1 = emulate_kernel(g, x2, L, L, L, spin, basis, backward=True)
+    y2 = emulate_kernel(g, x1, L, L, L, spin, basis, backward=True)
+    assert np.abs(y1 - r1).max() <= 1e-12 * max(1.0, np.abs(r1).max())
+    assert np.abs(y2 - r2).max() <= 1e-12 * max(1.0, np.abs(r2).max())
+    if spin and basis == 0 and L > 0:
+        # the paper basis needs the conjugation: the forward tables alone give a different map
+        assert np.abs(emulate_kernel(g, x2, L, L, L, spin, basis) - r1).max() > 1e-3
