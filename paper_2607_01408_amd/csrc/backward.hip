@@ -7,9 +7,10 @@
 // T[k1,k2,k3] = sum_j T'[k3,j,k1] J[j,k2], with T' the tensor of degrees
 // (Lout, L2, L1) and J the real matrix of conjugation on real-basis coefficients.
 // So gx1 = SpinGTP'(g, J x2) and gx2 = SpinGTP''(g, J x1).  For L1 = L2 = Lout
-// both are launches of the plan's own forward kernel on the plan's backward
-// tables, in which input 2's m = 0 mixing of the |s| = 1 sectors absorbs J (the
-// only slots J moves); no copy of J x is made.
+// both are launches of the plan's own forward kernel (the instantiation whose
+// input-2 lanes read the second copy of the m = 0 mixing of the |s| = 1 sectors)
+// on the plan's backward tables, where that copy absorbs J (J moves no other
+// slots); no copy of J x is made.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -33,12 +34,14 @@ extern "C" spingtp_status spingtp_backward(spingtp_plan plan, const void* x1, co
     // run_forward checks the rest (sizes, pointers, alignment, device)
     if (grad_x1 != nullptr) {
         const spingtp_status r =
-            spingtp::run_forward(plan, plan->kernel, grad_out, x2, grad_x1, N, C, false, stream, plan->d_tab_bwd);
+            spingtp::run_forward(plan, plan->kernel, grad_out, x2, grad_x1, N, C, false, stream, plan->d_tab_bwd,
+                                 true);
         if (r != SPINGTP_OK) return r;
     }
     if (grad_x2 != nullptr) {
         const spingtp_status r =
-            spingtp::run_forward(plan, plan->kernel, grad_out, x1, grad_x2, N, C, false, stream, plan->d_tab_bwd);
+            spingtp::run_forward(plan, plan->kernel, grad_out, x1, grad_x2, N, C, false, stream, plan->d_tab_bwd,
+                                 true);
         if (r != SPINGTP_OK) return r;
     }
     return SPINGTP_OK;

@@ -409,7 +409,7 @@ constexpr Owners<PairShape<L, SPIN>::NG> assign_pair_owners() {
 //   Q0[t]: R0c[t] (even lane) or -R0s[t] (odd lane), t >= 1; Q0[0] = R0c[0]
 //   Q1[t]: P1c+P2s (even) or P2c-P1s (odd);  Q2[t]: P1c-P2s (even) or -P2c-P1s (odd)
 //   zslot: Z+ (even lane) or Z- (odd lane), the m3 = 0, |s3| = 1 sums.
-template <int L, bool SPIN>
+template <int L, bool SPIN, bool BWD>
 __device__ __forceinline__ void pair_spectra(const float* xr, const float* __restrict__ tb,
                                              const float* __restrict__ g, const float* trl, int sub,
                                              float (&Q0)[L + 1], float (&Q1)[L + 1], float (&Q2)[L + 1],
@@ -419,7 +419,7 @@ __device__ __forceinline__ void pair_spectra(const float* xr, const float* __res
     constexpr int NP = Y.NP;
     constexpr int KP = (NP - 1) / 2;
     float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
-    coef_to_theta_fourier<L, L, SPIN>(xr, tb, g + Y.n0, sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
+    coef_to_theta_fourier<L, L, SPIN>(xr, tb, g + Y.n0, BWD && sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
     const float sg = sub ? -1.f : 1.f;
 
     // accumulators: cosine spectra on the even lane, sine spectra on the odd lane
@@ -532,7 +532,7 @@ __device__ __forceinline__ void pair_publish(float* D, int sub, const float (&Q0
     }
 }
 
-template <int L, bool SPIN, typename TIO>
+template <int L, bool SPIN, typename TIO, bool BWD>
 __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pair_kernel(
     const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units, int64_t cpx2,
     const float* __restrict__ tab) {
@@ -571,7 +571,7 @@ __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pai
 
     const float* __restrict__ tb = tab + Y.glob + node * Y.pb;
     float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
-    pair_spectra<L, SPIN>((sub ? X2 : X1) + u * P::ST, tb, g, TR + sub * (P::NP * (L + 1)), sub, Q0, Q1, Q2, zslot);
+    pair_spectra<L, SPIN, BWD>((sub ? X2 : X1) + u * P::ST, tb, g, TR + sub * (P::NP * (L + 1)), sub, Q0, Q1, Q2, zslot);
     __syncthreads();  // every wave is past step (A): the input tiles are free
     pair_publish<L, SPIN>(X1 + (node * P::UNITS + u) * P::DS, sub, Q0, Q1, Q2, zslot);
     __syncthreads();
@@ -603,13 +603,13 @@ __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pai
     store_tile<P::NC, P::ST>(out + u0 * P::NC, nvalid, YT, tid, P::THREADS);
 }
 
-template <int L, bool SPIN, typename TIO>
+template <int L, bool SPIN, typename TIO, bool BWD>
 hipError_t launch_pair(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                        const uint32_t*, hipStream_t stream) {
     using P = PairShape<L, SPIN>;
     const int64_t blocks = (units + P::UNITS - 1) / P::UNITS;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((spingtp_fwd_pair_kernel<L, SPIN, TIO>), dim3(static_cast<unsigned>(blocks)),
+    hipLaunchKernelGGL((spingtp_fwd_pair_kernel<L, SPIN, TIO, BWD>), dim3(static_cast<unsigned>(blocks)),
                        dim3(P::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
                        static_cast<TIO*>(out), units, cpx2, tab);
     return hipGetLastError();
@@ -640,7 +640,7 @@ struct BigShape {
     static constexpr int LDS_FLOATS = DF + TRIG;
 };
 
-template <int L, bool SPIN, int W>
+template <int L, bool SPIN, int W, bool BWD>
 __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_big_kernel(
     const float* __restrict__ x1, const float* __restrict__ x2, float* __restrict__ out, int64_t units, int64_t cpx2,
     const float* __restrict__ tab) {
@@ -684,7 +684,7 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
         const int nr = (B::NT - r * W) < W ? (B::NT - r * W) : W;
         if (node < B::NT) {
             float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
-            pair_spectra<L, SPIN>(xr, tab + Y.glob + node * Y.pb, g, TR + sub * (B::NP * (L + 1)), sub, Q0, Q1,
+            pair_spectra<L, SPIN, BWD>(xr, tab + Y.glob + node * Y.pb, g, TR + sub * (B::NP * (L + 1)), sub, Q0, Q1,
                                   Q2, zslot);
             pair_publish<L, SPIN>(D + (wave * B::UNITS + u) * P::DS, sub, Q0, Q1, Q2, zslot);
         }
@@ -720,13 +720,13 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     }
 }
 
-template <int L, bool SPIN, int W>
+template <int L, bool SPIN, int W, bool BWD>
 hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                       const uint32_t*, hipStream_t stream) {
     using B = BigShape<L, SPIN, W>;
     const int64_t blocks = (units + B::UNITS - 1) / B::UNITS;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W>), dim3(static_cast<unsigned>(blocks)), dim3(B::THREADS),
+    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W, BWD>), dim3(static_cast<unsigned>(blocks)), dim3(B::THREADS),
                        0, stream, static_cast<const float*>(x1), static_cast<const float*>(x2),
                        static_cast<float*>(out), units, cpx2, tab);
     return hipGetLastError();
@@ -754,7 +754,7 @@ constexpr Registered reg() {
     using S = Shape<L1, L2, LO, SPIN>;
     return Registered{L1, L2, LO, SPIN ? 1 : 0, sizeof(TIO) == 4 ? 0 : 1,
                       KernelEntry{S::WAVES, 64, static_cast<int>(S::LDS_FLOATS * sizeof(float)), 1,
-                                  &launch<L1, L2, LO, SPIN, TIO>}};
+                                  &launch<L1, L2, LO, SPIN, TIO>, &launch<L1, L2, LO, SPIN, TIO>}};
 }
 
 #define SPINGTP_REG(L1, L2, LO, SPIN) reg<L1, L2, LO, SPIN, float>(), reg<L1, L2, LO, SPIN, uint16_t>()
@@ -764,7 +764,7 @@ constexpr Registered reg_pair() {
     using P = PairShape<L, SPIN>;
     return Registered{L, L, L, SPIN ? 1 : 0, sizeof(TIO) == 4 ? 0 : 1,
                       KernelEntry{P::WAVES, P::UNITS, static_cast<int>(P::LDS_FLOATS * sizeof(float)), 2,
-                                  &launch_pair<L, SPIN, TIO>}};
+                                  &launch_pair<L, SPIN, TIO, false>, &launch_pair<L, SPIN, TIO, true>}};
 }
 #define SPINGTP_REG_PAIR(L, SPIN) reg_pair<L, SPIN, float>(), reg_pair<L, SPIN, uint16_t>()
 
@@ -773,7 +773,7 @@ constexpr Registered reg_big() {
     using B = BigShape<L, SPIN, W>;
     return Registered{L, L, L, SPIN ? 1 : 0, 0,
                       KernelEntry{B::WAVES, B::UNITS, static_cast<int>(B::LDS_FLOATS * sizeof(float)), 3,
-                                  &launch_big<L, SPIN, W>}};
+                                  &launch_big<L, SPIN, W, false>, &launch_big<L, SPIN, W, true>}};
 }
 #define SPINGTP_REG_BIG(L) reg_big<L, true, 5>(), reg_big<L, false, 5>()
 

@@ -265,7 +265,7 @@ __device__ __forceinline__ void store_out(uint16_t* __restrict__ dst, int nvalid
 }
 
 // SPLIT = 3: hi*hi + hi*lo + lo*hi (fp32 I/O); SPLIT = 1: hi*hi (bf16 I/O).
-template <int L, typename TIO, int SPLIT>
+template <int L, typename TIO, int SPLIT, bool BWD>
 __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __restrict__ x1,
                                                                    const TIO* __restrict__ x2,
                                                                    TIO* __restrict__ out, int64_t units,
@@ -355,8 +355,8 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
 
         // (A) this lane's input at node j
         float Pc[3][L + 1], Ps[3][L + 1], dl, ep;
-        coef_to_theta_fourier<L, L, true>(xr, tb, tab + Y.n0, h != 0, Pc[0], Ps[0], Pc[1], Ps[1], Pc[2], Ps[2], dl,
-                                          ep);
+        coef_to_theta_fourier<L, L, true>(xr, tb, tab + Y.n0, BWD && h != 0, Pc[0], Ps[0], Pc[1], Ps[1], Pc[2],
+                                          Ps[2], dl, ep);
 
         // step-(B) operands of the three polynomials of both inputs
         v8h oh[2][3], ol[2][3];
@@ -501,13 +501,13 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
     store_out<NC, ST, S::UNITS, S::THREADS>(out + u0 * NC, nvalid, lds, S::YB, tid);
 }
 
-template <int L, typename TIO, int SPLIT>
+template <int L, typename TIO, int SPLIT, bool BWD>
 hipError_t launch_mfma(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                        const uint32_t* aux, hipStream_t stream) {
     using S = MShape<L>;
     const int64_t blocks = (units + S::UNITS - 1) / S::UNITS;
     if (blocks > 0x7fffffff || aux == nullptr) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((spingtp_fwd_mfma_kernel<L, TIO, SPLIT>), dim3(static_cast<unsigned>(blocks)),
+    hipLaunchKernelGGL((spingtp_fwd_mfma_kernel<L, TIO, SPLIT, BWD>), dim3(static_cast<unsigned>(blocks)),
                        dim3(S::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
                        static_cast<TIO*>(out), units, cpx2, tab, aux);
     return hipGetLastError();
@@ -523,7 +523,8 @@ constexpr MRegistered reg_mfma() {
     using S = MShape<L>;
     return MRegistered{L, sizeof(TIO) == 4 ? 0 : 1,
                        KernelEntry{S::WAVES, S::UNITS, static_cast<int>(S::LDS_FLOATS * sizeof(float)), 4,
-                                   &launch_mfma<L, TIO, sizeof(TIO) == 4 ? 3 : 1>}};
+                                   &launch_mfma<L, TIO, sizeof(TIO) == 4 ? 3 : 1, false>,
+                                   &launch_mfma<L, TIO, sizeof(TIO) == 4 ? 3 : 1, true>}};
 }
 
 // L = 4 fp32 stays on the vector-ALU kernel, which is as fast there (0.37 ns/unit).

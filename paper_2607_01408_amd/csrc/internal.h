@@ -23,6 +23,10 @@ struct KernelEntry {
     // its C channels)
     hipError_t (*launch)(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                          const uint32_t* aux, hipStream_t stream);
+    // the instantiation spingtp_backward launches: input-2 lanes take the second
+    // copy of the m = 0 mixing (layout.h n0b); nullptr where there is none
+    hipError_t (*launch_bwd)(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2,
+                             const float* tab, const uint32_t* aux, hipStream_t stream);
 };
 
 // Largest row length (n_spins (L+1)^2) of the precontracted kernel: L <= 6 with
@@ -78,9 +82,11 @@ bool build_conj_map(int L, const int* spins, int n_spins, unsigned flags, std::v
 
 // Argument checks and launch of one forward kernel (api.cpp).  shared_x2: x2
 // holds one row per edge (spingtp_forward_v1), else one per unit.  tab: the
-// plan tables to use (the plan's own when nullptr).
+// plan tables to use (the plan's own when nullptr); backward: launch the
+// entry's launch_bwd instantiation.
 spingtp_status run_forward(spingtp_plan plan, const KernelEntry* k, const void* x1, const void* x2, void* out,
-                           int64_t N, int64_t C, bool shared_x2, void* stream, const float* tab = nullptr);
+                           int64_t N, int64_t C, bool shared_x2, void* stream, const float* tab = nullptr,
+                           bool backward = false);
 
 // Dense real tensor of the operation (see spingtp_dense_tensor_host), float64.
 void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
