@@ -73,8 +73,9 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  * precontracted kernel (family 5 below) is the default; SPINGTP_V1_PRECONTRACT
  * takes the precontracted kernel wherever it is built (SPINGTP_ERR_UNSUPPORTED
  * where it is not).  Without either, the precontracted kernel is used for row
- * lengths n_spins (L+1)^2 <= 80 in L1 and Lout (where it is the faster route)
- * and for shapes with no Fourier-route kernel. */
+ * lengths n_spins (L+1)^2 <= 112 in L1 and Lout (degree <= 5 with spins
+ * {-1, 0, +1}, where it is the faster route) and for shapes with no
+ * Fourier-route kernel. */
 #define SPINGTP_V1_FOURIER 0x200u
 #define SPINGTP_V1_PRECONTRACT 0x400u
 
@@ -240,14 +241,20 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  * not cover (a degree above 6 with spins {-1, 0, +1}, above 7 with spin {0}) give
  * SPINGTP_ERR_UNSUPPORTED.
  * Word layout, with P = 256 (threads of one workgroup):
- *   [0, 8)                 NC1, NC2, NCO, BLK1 ((L1+1)^2 for spins {-1, 0, +1},
- *                          else 0), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT (a
- *                          multiple of 8), KST = 16 KS + 4;
- *   [8, 8 + 2 IPT P)       items [item][thread], two words each: dst | k2 << 16 |
- *                          last << 24, then the fp32 value (bits).
- * Thread t adds value * x2[k2] for its items in order to a running sum; an item
- * with `last` set stores the sum as the edge kernel entry K[k1][k3] with
- * dst = k3 KST + k1, and restarts the sum at 0.  Padding items are all-zero words.
+ *   [0, 12)                NC1, NC2, NCO, BLK1 ((L1+1)^2 for spins {-1, 0, +1},
+ *                          else 0), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT,
+ *                          KST = 16 KS + 4, NB3, RB, STRIDE, 0: the k3 rows of the
+ *                          edge kernel come in NB3 blocks of RB rows (one block of
+ *                          16 NT rows when KS, NT <= 5, else blocks of 48 rows);
+ *                          each block holds STRIDE items per thread, IPT of them
+ *                          used (STRIDE = IPT, a multiple of 8, for one block;
+ *                          else IPT is a multiple of 16 and STRIDE = IPT + 16);
+ *   [12, 12 + 2 NB3 STRIDE P)  per block b, items [item][thread], two words each:
+ *                          dst | k2 << 16 | last << 24, then the fp32 value (bits).
+ * Thread t adds value * x2[k2] for the items of a block in order to a running
+ * sum; an item with `last` set stores the sum as the edge kernel entry K[k1][k3]
+ * with dst = (k3 - RB b) KST + k1, and restarts the sum at 0.  Padding items are
+ * all-zero words.
  * Writes min(capacity, total) words to `words` (may be NULL when capacity is 0)
  * and the total to *count.
  */

@@ -220,10 +220,186 @@ __global__ __launch_bounds__(kPreThreads) void spingtp_fwd_pre_kernel(const TIO*
     }
 }
 
-// Resident workgroups of one instantiation on the current device (cached per
-// device; 0 on failure).
+// Blocked variant for KS or NT above 5 (rows longer than 80: degree 5 or 6 with
+// spins {-1, 0, +1}).  The whole transposed kernel would not leave room for two
+// workgroups per CU, so its k3 rows are built and used in blocks of
+// kPreBlockRows (48): per edge and per group of 128 channels, each wave first
+// loads the operands of its two 16-channel tiles into registers (through its
+// LDS tile), then for every block the workgroup builds the block in LDS from
+// that block's items and each wave multiplies its tiles with it and writes the
+// block's output columns (coalesced along the rows' 48-value segments).  Two
+// resident workgroups per CU keep the matrix cores of one busy while the other
+// builds.  Channels beyond 128 per edge take further groups and rebuild the
+// blocks.
 template <typename TIO, int KS, int NT>
-int64_t pre_resident_groups() {
+__global__ __launch_bounds__(kPreThreads, 2) void spingtp_fwd_pre_blocked_kernel(const TIO* __restrict__ x1,
+                                                                                 const TIO* __restrict__ x2,
+                                                                                 TIO* __restrict__ out, int64_t C,
+                                                                                 int64_t edges,
+                                                                                 const uint32_t* __restrict__ aux) {
+    constexpr int KST = 16 * KS + 4;
+    constexpr int RB = kPreBlockRows;
+    constexpr int SB = RB / 16;  // strips per block
+    constexpr int NB3 = (16 * NT + RB - 1) / RB;
+    constexpr int RS = 16 * KS + 4;  // x1 tile row stride
+    constexpr int RSO = RB + 4;      // output tile row stride
+    constexpr int STG = 16 * (RS > RSO ? RS : RSO);
+    constexpr int NW = kPreThreads / 64;
+    constexpr int TPW = 2;  // tiles per wave per channel group
+    constexpr int PF = 4 * KS;
+    constexpr int PO = RB / 4;  // output values per lane of a tile block
+    __shared__ __align__(16) float Kb[RB * KST + kPreThreads];  // + one spare slot per thread
+    __shared__ __align__(16) float Stage[NW * STG];
+    __shared__ float X2[kPreMaxNC];
+
+    const int NC1 = static_cast<int>(aux[0]), NC2 = static_cast<int>(aux[1]), NCO = static_cast<int>(aux[2]);
+    const int blk1 = static_cast<int>(aux[3]), ipt = static_cast<int>(aux[6]), stride = static_cast<int>(aux[10]);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 15, g = lane >> 4;
+    const int64_t tiles = (C + 15) / 16;
+    float* __restrict__ st = Stage + wave * STG;
+    const uint2* __restrict__ items0 = reinterpret_cast<const uint2*>(aux + kPreHeader) + tid;
+    const int q1 = 64 / NC1, r1 = 64 - q1 * NC1;
+    const int row1 = lane / NC1, k1l = lane - row1 * NC1;
+
+    for (int64_t n = blockIdx.x; n < edges; n += gridDim.x) {
+        const TIO* __restrict__ xe = x1 + n * C * NC1;
+        TIO* __restrict__ oe = out + n * C * NCO;
+        for (int64_t g0 = 0; g0 < tiles; g0 += NW * TPW) {
+            // operands of this wave's tiles, through its LDS tile
+            float b[TPW][KS][4];
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) {
+                const int64_t m = g0 + wave + NW * i;
+                if (m < tiles) {
+                    const int rows = static_cast<int>(C - 16 * m < 16 ? C - 16 * m : 16);
+                    const TIO* __restrict__ src = xe + 16 * m * NC1;
+                    float pf[PF];
+#pragma unroll
+                    for (int q = 0; q < PF; ++q) {
+                        const int e = lane + 64 * q;
+                        pf[q] = e < rows * NC1 ? to_f32(src[e]) : 0.f;
+                    }
+                    int r = row1, k = k1l;
+#pragma unroll
+                    for (int q = 0; q < PF; ++q) {
+                        if (lane + 64 * q < rows * NC1) st[r * RS + k] = pf[q];
+                        r += q1;
+                        k += r1;
+                        if (k >= NC1) {
+                            k -= NC1;
+                            ++r;
+                        }
+                    }
+                    wave_lds_order();
+#pragma unroll
+                    for (int s = 0; s < KS; ++s) {
+                        const v4f v = *reinterpret_cast<const v4f*>(&st[col * RS + 16 * s + 4 * g]);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            const int k1 = 16 * s + 4 * g + j;
+                            const bool ok = k1 < NC1 && !(blk1 > 0 && (k1 == 0 || k1 == 2 * blk1));
+                            b[i][s][j] = ok ? v[j] : 0.f;
+                        }
+                    }
+                    wave_lds_order();
+                } else {
+#pragma unroll
+                    for (int s = 0; s < KS; ++s)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) b[i][s][j] = 0.f;
+                }
+            }
+            for (int blk = 0; blk < NB3; ++blk) {
+                __syncthreads();  // the previous block (or edge) is no longer read
+                for (int i = tid; i < RB * KST / 4; i += kPreThreads)
+                    reinterpret_cast<v4f*>(Kb)[i] = v4f{0.f, 0.f, 0.f, 0.f};
+                if (blk == 0 && g0 == 0 && tid < NC2) X2[tid] = to_f32(x2[n * NC2 + tid]);
+                __syncthreads();
+                {  // build block blk
+                    const uint2* __restrict__ items = items0 + static_cast<int64_t>(blk) * stride * kPreThreads;
+                    float acc = 0.f;
+                    uint2 ia[8], ib[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) ia[j] = items[j * kPreThreads];
+                    auto consume = [&](const uint2 (&it)[8]) {
+                        float xv[8];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) xv[j] = X2[(it[j].x >> 16) & 0xffu];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) {
+                            acc = fmaf(__uint_as_float(it[j].y), xv[j], acc);
+                            const bool last = (it[j].x >> 24) != 0;
+                            Kb[last ? static_cast<int>(it[j].x & 0xffffu) : RB * KST + tid] = acc;
+                            acc = last ? 0.f : acc;
+                        }
+                    };
+                    // ipt is a multiple of 16 and 16 zero items follow each block: every
+                    // load is unconditional and runs 8 items ahead of the sums, and the
+                    // stores are branch-free (a list's last item stores the sum, the
+                    // others write this thread's spare slot)
+                    for (int i = 0; i < ipt; i += 16) {
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) ib[j] = items[(i + 8 + j) * kPreThreads];
+                        consume(ia);
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) ia[j] = items[(i + 16 + j) * kPreThreads];
+                        consume(ib);
+                    }
+                }
+                __syncthreads();
+                // products of this wave's tiles with block blk
+                v4f acc[TPW][SB];
+#pragma unroll
+                for (int i = 0; i < TPW; ++i)
+#pragma unroll
+                    for (int t = 0; t < SB; ++t) acc[i][t] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s = 0; s < KS; ++s)
+#pragma unroll
+                    for (int t = 0; t < SB; ++t) {
+                        if (SB * blk + t >= NT) continue;
+                        const v4f a = *reinterpret_cast<const v4f*>(&Kb[(16 * t + col) * KST + 16 * s + 4 * g]);
+#pragma unroll
+                        for (int i = 0; i < TPW; ++i)
+#pragma unroll
+                            for (int j = 0; j < 4; ++j)
+                                acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[i][s][j], acc[i][t], 0, 0, 0);
+                    }
+                const int bw = NCO - RB * blk < RB ? NCO - RB * blk : RB;  // output columns of this block
+                const int qo = 64 / bw, ro = 64 - qo * bw;
+                const int rowo = lane / bw, kol = lane - rowo * bw;
+#pragma unroll
+                for (int i = 0; i < TPW; ++i) {
+                    const int64_t m = g0 + wave + NW * i;
+                    if (m >= tiles) continue;
+                    const int rows = static_cast<int>(C - 16 * m < 16 ? C - 16 * m : 16);
+#pragma unroll
+                    for (int t = 0; t < SB; ++t)
+                        if (SB * blk + t < NT) *reinterpret_cast<v4f*>(&st[col * RSO + 16 * t + 4 * g]) = acc[i][t];
+                    wave_lds_order();
+                    TIO* __restrict__ dst = oe + 16 * m * NCO + RB * blk;
+                    int r = rowo, k = kol;
+#pragma unroll
+                    for (int q = 0; q < PO; ++q) {
+                        if (lane + 64 * q < rows * bw) dst[static_cast<int64_t>(r) * NCO + k] = from_f32<TIO>(st[r * RSO + k]);
+                        r += qo;
+                        k += ro;
+                        if (k >= bw) {
+                            k -= bw;
+                            ++r;
+                        }
+                    }
+                    wave_lds_order();
+                }
+            }
+        }
+    }
+}
+
+// Resident workgroups of a kernel on the current device (cached per device and
+// kernel; 0 on failure).
+template <auto Kernel>
+int64_t resident_groups() {
     constexpr int kMaxDevices = 64;
     static std::atomic<int64_t> cache[kMaxDevices];
     int dev = 0;
@@ -231,8 +407,7 @@ int64_t pre_resident_groups() {
     int64_t v = cache[dev].load(std::memory_order_relaxed);
     if (v > 0) return v;
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, spingtp_fwd_pre_kernel<TIO, KS, NT>, kPreThreads, 0) !=
-            hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, Kernel, kPreThreads, 0) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
     v = static_cast<int64_t>(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
@@ -246,18 +421,34 @@ hipError_t launch_pre(const void* x1, const void* x2, void* out, int64_t units, 
     if (aux == nullptr || cpx2 <= 0 || units % cpx2 != 0) return hipErrorInvalidValue;
     const int64_t edges = units / cpx2;
     if (edges == 0) return hipSuccess;
-    const int64_t resident = pre_resident_groups<TIO, KS, NT>();
+    constexpr bool kBlocked = KS > 5 || NT > 5;
+    int64_t resident = 0;
+    if constexpr (kBlocked)
+        resident = resident_groups<spingtp_fwd_pre_blocked_kernel<TIO, KS, NT>>();
+    else
+        resident = resident_groups<spingtp_fwd_pre_kernel<TIO, KS, NT>>();
     if (resident <= 0) return hipErrorInvalidValue;
     const int64_t grid = edges < resident ? edges : resident;
-    hipLaunchKernelGGL((spingtp_fwd_pre_kernel<TIO, KS, NT>), dim3(static_cast<unsigned>(grid)), dim3(kPreThreads), 0,
-                       stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), static_cast<TIO*>(out), cpx2,
-                       edges, aux);
+    if constexpr (kBlocked)
+        hipLaunchKernelGGL((spingtp_fwd_pre_blocked_kernel<TIO, KS, NT>), dim3(static_cast<unsigned>(grid)),
+                           dim3(kPreThreads), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
+                           static_cast<TIO*>(out), cpx2, edges, aux);
+    else
+        hipLaunchKernelGGL((spingtp_fwd_pre_kernel<TIO, KS, NT>), dim3(static_cast<unsigned>(grid)), dim3(kPreThreads),
+                           0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
+                           static_cast<TIO*>(out), cpx2, edges, aux);
     return hipGetLastError();
 }
 
 template <int KS, int NT>
 constexpr int pre_lds_bytes() {
-    return (16 * NT * (16 * KS + 4) + (kPreThreads / 64) * 16 * (16 * (KS > NT ? KS : NT) + 4) + kPreMaxNC) * 4;
+    if constexpr (KS > 5 || NT > 5) {
+        constexpr int RS = 16 * KS + 4, RSO = kPreBlockRows + 4;
+        return (kPreBlockRows * (16 * KS + 4) + kPreThreads + (kPreThreads / 64) * 16 * (RS > RSO ? RS : RSO) +
+                kPreMaxNC) * 4;
+    } else {
+        return (16 * NT * (16 * KS + 4) + (kPreThreads / 64) * 16 * (16 * (KS > NT ? KS : NT) + 4) + kPreMaxNC) * 4;
+    }
 }
 
 // Launch entries {fp32, bf16} of one (KS, NT) instantiation.

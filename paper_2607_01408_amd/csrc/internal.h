@@ -37,7 +37,9 @@ constexpr int kPreMaxNC = 147;
 // Threads per workgroup of the precontracted kernel (its tensor items are laid out
 // for exactly this many threads) and the words of its table header.
 constexpr int kPreThreads = 256;
-constexpr int kPreHeader = 8;
+constexpr int kPreHeader = 12;
+// k3 rows per kernel block of the large instantiations (KS or NT above 5)
+constexpr int kPreBlockRows = 48;
 
 // Finds the instantiation for (L1, L2, Lout, spin mode, dtype); nullptr if none.
 // find_kernel returns the vector-ALU kernels, find_mfma_kernel the matrix-core
@@ -49,10 +51,16 @@ const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int spin_mode, int dt
 // The instantiations with KS or NT in {7, 10} (forward_pre_large.hip); nullptr if none.
 const KernelEntry* find_pre_kernel_large(int ks, int nt, int dtype);
 
-// Sparse tensor of the precontracted kernel (forward_pre.hip).  Header words NC1,
+// Sparse tensor of the precontracted kernel (forward_pre.h).  Header words NC1,
 // NC2, NCO, BLK1 (0 for spins {0}), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT,
-// KST = 16 KS + 4; then IPT x kPreThreads items [item][thread], each the two
-// words dst | k2 << 16 | last << 24 and an fp32 value.  An item
+// KST = 16 KS + 4, NB3, RB, STRIDE, 0: the kernel's k3 rows come in NB3 blocks
+// of RB rows (one block of 16 NT rows for KS, NT <= 5; kPreBlockRows otherwise).
+// Then per block STRIDE x kPreThreads items [item][thread]: IPT items (a multiple
+// of 8) for the one-block kernel, STRIDE = IPT; for the blocked kernel IPT is a
+// multiple of 16 and 16 zero items follow (STRIDE = IPT + 16), which that kernel
+// loads ahead without conditions.  Each item is the two words
+// dst | k2 << 16 | last << 24 (dst = (k3 - RB b) KST + k1 within block b) and an
+// fp32 value.  An item
 // adds value * x2[k2] to the thread's running sum, and `last` stores the sum to the
 // transposed edge kernel at LDS index dst = k3 KST + k1 and restarts it.  Whole
 // (k1, k3) lists go to one thread (longest first, to the least loaded thread), so

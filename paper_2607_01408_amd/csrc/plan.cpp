@@ -394,34 +394,46 @@ void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
     const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
     const int nco = n_spins * (LO + 1) * (LO + 1);
     const int ks = (nc1 + 15) / 16, nt = (nco + 15) / 16, kst = 16 * ks + 4;
-    // nonzero lists per kernel entry (k1, k3)
+    // k3 rows per block: the whole kernel, or blocks of kPreBlockRows for the
+    // large instantiations (KS or NT above 5)
+    const int rb = (ks > 5 || nt > 5) ? kPreBlockRows : 16 * nt;
+    const int nb3 = (16 * nt + rb - 1) / rb;
+    // nonzero lists per kernel entry (k1, k3), per block
     struct Entry {
         int dst;
         std::vector<std::pair<int, float>> items;
     };
-    std::vector<Entry> entries;
+    std::vector<std::vector<Entry>> entries(nb3);
     for (int k1 = 0; k1 < nc1; ++k1)
         for (int k3 = 0; k3 < nco; ++k3) {
-            Entry e{k3 * kst + k1, {}};
+            const int b = k3 / rb;
+            Entry e{(k3 - b * rb) * kst + k1, {}};
             for (int k2 = 0; k2 < nc2; ++k2) {
                 const double v = T[(static_cast<size_t>(k1) * nc2 + k2) * nco + k3];
                 if (std::fabs(v) > 1e-12) e.items.emplace_back(k2, static_cast<float>(v));
             }
-            if (!e.items.empty()) entries.push_back(std::move(e));
+            if (!e.items.empty()) entries[b].push_back(std::move(e));
         }
-    // longest-first greedy balance of whole entries over the threads of a workgroup
-    std::stable_sort(entries.begin(), entries.end(),
-                     [](const Entry& a, const Entry& b) { return a.items.size() > b.items.size(); });
-    std::vector<std::vector<const Entry*>> per(kPreThreads);
-    std::vector<size_t> load(kPreThreads, 0);
-    for (const Entry& e : entries) {
-        const size_t t = static_cast<size_t>(std::min_element(load.begin(), load.end()) - load.begin());
-        per[t].push_back(&e);
-        load[t] += e.items.size();
+    // per block: longest-first greedy balance of whole entries over the threads
+    std::vector<std::vector<std::vector<const Entry*>>> per(nb3, std::vector<std::vector<const Entry*>>(kPreThreads));
+    // the blocked kernel loads 16 items ahead without conditions: IPT a multiple
+    // of 16 and 16 zero items after each block; the other kernel: multiple of 8
+    const bool blocked = nb3 > 1 || rb != 16 * nt;
+    const size_t quantum = blocked ? 16 : 8;
+    size_t ipt = quantum;
+    for (int b = 0; b < nb3; ++b) {
+        std::stable_sort(entries[b].begin(), entries[b].end(),
+                         [](const Entry& a, const Entry& c) { return a.items.size() > c.items.size(); });
+        std::vector<size_t> load(kPreThreads, 0);
+        for (const Entry& e : entries[b]) {
+            const size_t t = static_cast<size_t>(std::min_element(load.begin(), load.end()) - load.begin());
+            per[b][t].push_back(&e);
+            load[t] += e.items.size();
+        }
+        ipt = std::max(ipt, (*std::max_element(load.begin(), load.end()) + quantum - 1) / quantum * quantum);
     }
-    size_t ipt = *std::max_element(load.begin(), load.end());
-    ipt = std::max<size_t>(8, (ipt + 7) / 8 * 8);
-    out.assign(kPreHeader + 2 * ipt * kPreThreads, 0u);  // padding items: value 0, never stored
+    const size_t stride = blocked ? ipt + 16 : ipt;  // items per thread and block
+    out.assign(kPreHeader + 2 * nb3 * stride * kPreThreads, 0u);  // padding items: value 0, never stored
     out[0] = static_cast<uint32_t>(nc1);
     out[1] = static_cast<uint32_t>(nc2);
     out[2] = static_cast<uint32_t>(nco);
@@ -430,17 +442,22 @@ void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
     out[5] = static_cast<uint32_t>(nt);
     out[6] = static_cast<uint32_t>(ipt);
     out[7] = static_cast<uint32_t>(kst);
-    uint32_t* items = out.data() + kPreHeader;
-    for (int t = 0; t < kPreThreads; ++t) {
-        size_t i = 0;
-        for (const Entry* e : per[t])
-            for (size_t j = 0; j < e->items.size(); ++j, ++i) {
-                const bool last = j + 1 == e->items.size();
-                uint32_t* it = items + 2 * (i * kPreThreads + t);
-                it[0] = static_cast<uint32_t>(e->dst) | (static_cast<uint32_t>(e->items[j].first) << 16) |
-                        (last ? 1u << 24 : 0u);
-                std::memcpy(&it[1], &e->items[j].second, 4);
-            }
+    out[8] = static_cast<uint32_t>(nb3);
+    out[9] = static_cast<uint32_t>(rb);
+    out[10] = static_cast<uint32_t>(stride);
+    for (int b = 0; b < nb3; ++b) {
+        uint32_t* items = out.data() + kPreHeader + 2 * static_cast<size_t>(b) * stride * kPreThreads;
+        for (int t = 0; t < kPreThreads; ++t) {
+            size_t i = 0;
+            for (const Entry* e : per[b][t])
+                for (size_t j = 0; j < e->items.size(); ++j, ++i) {
+                    const bool last = j + 1 == e->items.size();
+                    uint32_t* it = items + 2 * (i * kPreThreads + t);
+                    it[0] = static_cast<uint32_t>(e->dst) | (static_cast<uint32_t>(e->items[j].first) << 16) |
+                            (last ? 1u << 24 : 0u);
+                    std::memcpy(&it[1], &e->items[j].second, 4);
+                }
+        }
     }
 }
 
@@ -690,7 +707,7 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
         kv1 = spingtp::find_pre_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
         // measured crossover: with larger rows the Fourier route is faster
         const int rows = (spin_mode ? 3 : 1) * (std::max(L1, Lout) + 1) * (std::max(L1, Lout) + 1);
-        if (kv1 != nullptr && k != nullptr && rows > 80 && (flags & SPINGTP_V1_PRECONTRACT) == 0) kv1 = nullptr;
+        if (kv1 != nullptr && k != nullptr && rows > 112 && (flags & SPINGTP_V1_PRECONTRACT) == 0) kv1 = nullptr;
         if (kv1 == nullptr && (flags & SPINGTP_V1_PRECONTRACT)) return SPINGTP_ERR_UNSUPPORTED;
     }
     if (kv1 == nullptr) kv1 = k;

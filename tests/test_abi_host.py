@@ -356,23 +356,26 @@ PRE_THREADS = 256
 
 def emulate_pre_kernel(words, x1, x2):
     """The precontracted kernel's data flow on the CPU with the exact table words:
-    each thread's running fp32 sum over its items, stored at `last`, builds the
-    transposed edge kernel; the product runs in float64 with the invalid x1 slots
-    read as 0.  x1 [C, NC1] of one edge, x2 [NC2]."""
-    nc1, nc2, nco, blk1, ks, nt, ipt, kst = (int(v) for v in words[:8])
-    pairs = words[8:].reshape(ipt, PRE_THREADS, 2)
-    items = pairs[:, :, 0]
-    vals = pairs[:, :, 1].copy().view(np.float32)
+    per k3 block, each thread's running fp32 sum over its items, stored at `last`,
+    builds that block of the transposed edge kernel; the product runs in float64
+    with the invalid x1 slots read as 0.  x1 [C, NC1] of one edge, x2 [NC2]."""
+    nc1, nc2, nco, blk1, ks, nt, ipt, kst, nb3, rb, stride = (int(v) for v in words[:11])
+    pairs = words[12:].reshape(nb3, stride, PRE_THREADS, 2)
     X2 = x2.astype(np.float32)
-    Kt = np.zeros(16 * nt * kst, dtype=np.float32)
-    acc = np.zeros(PRE_THREADS, dtype=np.float32)
-    for i in range(ipt):
-        w = items[i]
-        acc = (vals[i].astype(np.float64) * X2[(w >> 16) & 0xFF] + acc).astype(np.float32)  # one fp32 rounding
-        last = (w >> 24) != 0
-        Kt[(w & 0xFFFF)[last]] = acc[last]
-        acc[last] = 0.0
-    K = Kt.reshape(16 * nt, kst)[:nco, :nc1].T.astype(np.float64)
+    Kt = np.zeros((nb3 * rb, kst), dtype=np.float32)
+    for b in range(nb3):
+        items = pairs[b, :, :, 0]
+        vals = pairs[b, :, :, 1].copy().view(np.float32)
+        blk = np.zeros(rb * kst, dtype=np.float32)
+        acc = np.zeros(PRE_THREADS, dtype=np.float32)
+        for i in range(stride):
+            w = items[i]
+            acc = (vals[i].astype(np.float64) * X2[(w >> 16) & 0xFF] + acc).astype(np.float32)  # one fp32 rounding
+            last = (w >> 24) != 0
+            blk[(w & 0xFFFF)[last]] = acc[last]
+            acc[last] = 0.0
+        Kt[b * rb:(b + 1) * rb] = blk.reshape(rb, kst)
+    K = Kt[:nco, :nc1].T.astype(np.float64)
     k = np.arange(nc1)
     x1 = np.where((blk1 > 0) & ((k == 0) | (k == 2 * blk1)), 0.0, x1)
     return x1 @ K, K
@@ -388,16 +391,24 @@ def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
     edge kernel K[k1, k3] = sum_k2 T x2 and the oracle's outputs for channels that
     share x2; every entry has one writer, inside the padded LDS block."""
     words = pre_table_host(L1, L2, LO, spins, basis)
-    nc1, nc2, nco, blk1, ks, nt, ipt, kst = (int(v) for v in words[:8])
+    nc1, nc2, nco, blk1, ks, nt, ipt, kst, nb3, rb, stride = (int(v) for v in words[:11])
     ns = len(spins)
     assert (nc1, nc2, nco) == (ns * (L1 + 1) ** 2, ns * (L2 + 1) ** 2, ns * (LO + 1) ** 2)
     assert blk1 == ((L1 + 1) ** 2 if ns == 3 else 0)
     assert (ks, nt, kst) == (-(-nc1 // 16), -(-nco // 16), 16 * -(-nc1 // 16) + 4)
-    assert ipt % 8 == 0 and words.size == 8 + 2 * ipt * PRE_THREADS
-    items = words[8::2]
-    vals = words[9::2].copy().view(np.float32)
-    stores = items[(items >> 24) != 0] & 0xFFFF
+    assert (nb3, rb) == ((1, 16 * nt) if ks <= 5 and nt <= 5 else (-(-16 * nt // 48), 48))
+    blocked = ks > 5 or nt > 5
+    assert stride == (ipt + 16 if blocked else ipt) and ipt % (16 if blocked else 8) == 0
+    assert words.size == 12 + 2 * nb3 * stride * PRE_THREADS
+    assert not words[12:].reshape(nb3, stride, PRE_THREADS, 2)[:, ipt:].any()  # zero padding
+    items = words[12::2].reshape(nb3, -1)
+    vals = words[13::2].copy().view(np.float32)
+    blocks = np.repeat(np.arange(nb3), items.shape[1]).reshape(nb3, -1)
+    last = (items >> 24) != 0
+    stores = (items & 0xFFFF)[last] + (blocks * rb * kst)[last]  # position in the whole kernel
     assert len(np.unique(stores)) == len(stores)  # one writer per entry
+    assert np.all((items & 0xFFFF)[last] < rb * kst)  # inside the block
+    items = items.ravel()
     assert np.all(stores % kst < nc1) and np.all(stores // kst < nco)
     assert np.all(((items >> 16) & 0xFF) < nc2)
     assert np.all(items[vals == 0] == 0)  # padding items are all-zero
