@@ -198,6 +198,31 @@ def run_v1(args):
         return {"ms": ms, "family": plan.kernel_info_v1()["family"], "parity_rel_l2": parity,
                 "tp_per_s": U / (ms / 1e3)}
 
+    def measure_backward(L, C, B, seed):
+        """spingtp_backward_v1 (both gradients) on the default route, preallocated buffers."""
+        x1 = workloads.draw(L, B, C, 9300 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        x2 = workloads.draw(L, B, 1, 9400 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        g = workloads.draw(L, B, C, 9500 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        plan = Plan(L, L, L, workloads.SPINS, "fp32")
+        gx1, gx2 = torch.empty_like(x1), torch.empty_like(x2)
+        n = ctypes.c_size_t(0)
+        assert _lib.lib().spingtp_backward_v1_workspace_size(plan.handle, B, C, ctypes.byref(n)) == 0
+        ws = torch.empty(n.value, dtype=torch.uint8, device="cuda:0")
+        st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        call = (plan.handle, x1.data_ptr(), x2.data_ptr(), g.data_ptr(), gx1.data_ptr(), gx2.data_ptr(),
+                ws.data_ptr(), n.value, B, C, st)
+        bfn = _lib.lib().spingtp_backward_v1
+        for _ in range(args.warmup):
+            assert bfn(*call) == 0
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(args.steps):
+            bfn(*call)
+        e.record()
+        torch.cuda.synchronize()
+        return {"ms": s.elapsed_time(e) / args.steps, "v1_family": plan.kernel_info_v1()["family"]}
+
     table = []
     for (L1, L2, LO, C, B, p_direct, p_pre, p_triton) in V1_TABLE:
         row = {"L1": L1, "L2": L2, "Lout": LO, "C": C, "B": B,
@@ -212,10 +237,12 @@ def run_v1(args):
         row = {"L": L, "C": args.v1_sweep_channels, "B": args.v1_sweep_edges}
         for name, fourier in (("precontracted", False), ("fourier", True)):
             row[name] = measure(L, L, L, args.v1_sweep_channels, args.v1_sweep_edges, fourier, 50 + L)
+        row["backward"] = measure_backward(L, args.v1_sweep_channels, args.v1_sweep_edges, 60 + L)
         sweep.append(row)
         pre = row["precontracted"]
         print(f"[v1-sweep] L={L}: pre {pre['ms'] if pre else float('nan'):.3f} ms, "
-              f"fourier {row['fourier']['ms']:.3f} ms", file=sys.stderr, flush=True)
+              f"fourier {row['fourier']['ms']:.3f} ms, backward {row['backward']['ms']:.3f} ms",
+              file=sys.stderr, flush=True)
     print(json.dumps({
         "metric": "spingtp_forward_v1 time: precontracted vs Fourier route (x2 shared by the C channels)",
         "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": False,

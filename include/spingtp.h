@@ -173,6 +173,37 @@ spingtp_status spingtp_backward(spingtp_plan plan, const void* x1, const void* x
                                 void* grad_x1, void* grad_x2, int64_t N, int64_t C, void* stream);
 
 /*
+ * Gradients through spingtp_forward_v1 (x2 shared by the C channels of an edge):
+ *   grad_x1[n][c][k1] = sum_{k2,k3} T[k1][k2][k3] x2[n][k2] grad_out[n][c][k3],
+ *   grad_x2[n][k2]    = sum_c sum_{k1,k3} T[k1][k2][k3] x1[n][c][k1] grad_out[n][c][k3].
+ * Route (same identity as spingtp_backward): grad_x1 = SpinGTP_v1(grad_out, J x2) on
+ * the plan's spingtp_forward_v1 kernel (the precontracted kernel reads a second
+ * tensor table with J folded into its x2 indices and signs; the Fourier kernel
+ * reads the backward tables); grad_x2: the per-unit products
+ * SpinGTP(grad_out[n][c], J x1[n][c]) of the plan's spingtp_forward kernel go to
+ * `workspace` ([N][C][n_spins (L2+1)^2], the plan's dtype), then a second kernel
+ * sums them over c in order (fp32 sums; bf16 output rounded to nearest even).
+ * Built for plans with L1 = L2 = Lout that have a spingtp_forward kernel;
+ * otherwise SPINGTP_ERR_UNSUPPORTED.
+ *   x1 [N][C][...], x2 [N][...], grad_out [N][C][...]; grad_x1 [N][C][...] and
+ *   grad_x2 [N][n_spins (L2+1)^2] (either may be NULL: not computed), overwritten;
+ *   slots with l < |s| are written 0.  C = 0 writes grad_x2 = 0.
+ *   workspace: device memory of spingtp_backward_v1_workspace_size bytes or more,
+ *   16-byte aligned, overlapping no other argument (needed only for grad_x2; may
+ *   be NULL otherwise).  Too small or missing: SPINGTP_ERR_INVALID_ARG.
+ * Same dtype, alignment and error rules as spingtp_forward; asynchronous on
+ * `stream`, ordered on it; no allocation.
+ */
+spingtp_status spingtp_backward_v1(spingtp_plan plan, const void* x1, const void* x2, const void* grad_out,
+                                   void* grad_x1, void* grad_x2, void* workspace, size_t workspace_bytes,
+                                   int64_t N, int64_t C, void* stream);
+
+/* Bytes of workspace spingtp_backward_v1 needs for grad_x2 with N x C units:
+ * N C n_spins (L2+1)^2 elements of the plan's dtype.  SPINGTP_ERR_UNSUPPORTED as
+ * for spingtp_backward_v1. */
+spingtp_status spingtp_backward_v1_workspace_size(spingtp_plan plan, int64_t N, int64_t C, size_t* bytes);
+
+/*
  * Host-only: the conjugation map J of degree L (one word per destination slot j
  * of a [n_spins][(L+1)^2] vector: (J x)[j] = x[w & 0xffff], negated if bit 16 of
  * w is set, 0 if bit 17 is set (slots with l < |s|)), derived from the real basis
@@ -255,6 +286,9 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  * sum; an item with `last` set stores the sum as the edge kernel entry K[k1][k3]
  * with dst = (k3 - RB b) KST + k1, and restarts the sum at 0.  Padding items are
  * all-zero words.
+ * With SPINGTP_TABLES_BACKWARD in `flags` (L1 = L2 = Lout only): the table of
+ * spingtp_backward_v1, whose items use J x2 (k2 replaced by J's source slot, the
+ * value by J's sign times the value; see spingtp_conj_map_host).
  * Writes min(capacity, total) words to `words` (may be NULL when capacity is 0)
  * and the total to *count.
  */

@@ -11,7 +11,8 @@ STATUS_NAMES = {0: "OK", 1: "ERR_INVALID_ARG", 2: "ERR_UNSUPPORTED", 3: "ERR_OUT
 EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "spingtp_status_string",
             "spingtp_plan_tables_host", "spingtp_plan_kernel_info", "spingtp_dense_tensor_host",
             "spingtp_mfma_operands_host", "spingtp_forward_v1", "spingtp_plan_kernel_info_v1",
-            "spingtp_pre_table_host", "spingtp_backward", "spingtp_conj_map_host")
+            "spingtp_pre_table_host", "spingtp_backward", "spingtp_conj_map_host", "spingtp_backward_v1",
+            "spingtp_backward_v1_workspace_size")
 
 _lib = None
 
@@ -61,6 +62,13 @@ def lib() -> ctypes.CDLL:
                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                        ctypes.c_void_p]
         L.spingtp_backward.restype = ctypes.c_int
+        L.spingtp_backward_v1.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                          ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        L.spingtp_backward_v1.restype = ctypes.c_int
+        L.spingtp_backward_v1_workspace_size.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                                         ctypes.POINTER(ctypes.c_size_t)]
+        L.spingtp_backward_v1_workspace_size.restype = ctypes.c_int
         L.spingtp_conj_map_host.argtypes = [ctypes.c_int, c_int_p, ctypes.c_int, ctypes.c_uint,
                                             ctypes.POINTER(ctypes.c_uint32), ctypes.c_size_t,
                                             ctypes.POINTER(ctypes.c_size_t)]

@@ -9,20 +9,22 @@
 
 spingtp_status spingtp::run_forward(spingtp_plan plan, const spingtp::KernelEntry* k, const void* x1, const void* x2,
                                     void* out, int64_t N, int64_t C, bool shared_x2, void* stream,
-                                    const float* tab, bool backward) {
+                                    const float* tab, bool backward, const uint32_t* aux_override) {
     if (plan == nullptr || N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
     if (N == 0 || C == 0) return SPINGTP_OK;
     if (N > (int64_t{1} << 40) / C) return SPINGTP_ERR_INVALID_ARG;
     if (x1 == nullptr || x2 == nullptr || out == nullptr) return SPINGTP_ERR_INVALID_ARG;
     const auto misaligned = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; };
     if (misaligned(x1) || misaligned(x2) || misaligned(out)) return SPINGTP_ERR_INVALID_ARG;
-    if (k == nullptr || (backward && k->launch_bwd == nullptr)) return SPINGTP_ERR_UNSUPPORTED;
+    if (k == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    const bool bwd_launch = backward && k->family != 5;  // family 5 takes J through its table
+    if (bwd_launch && k->launch_bwd == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
     if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
-    const uint32_t* aux = k->family == 5 ? plan->d_pre : plan->d_aux;
+    const uint32_t* aux = aux_override != nullptr ? aux_override : (k->family == 5 ? plan->d_pre : plan->d_aux);
     const hipError_t e =
-        (backward ? k->launch_bwd : k->launch)(x1, x2, out, N * C, shared_x2 ? C : 1, tab != nullptr ? tab : plan->d_tab, aux,
+        (bwd_launch ? k->launch_bwd : k->launch)(x1, x2, out, N * C, shared_x2 ? C : 1, tab != nullptr ? tab : plan->d_tab, aux,
                   static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
 }

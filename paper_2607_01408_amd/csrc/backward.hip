@@ -10,7 +10,8 @@
 // both are launches of the plan's own forward kernel (the instantiation whose
 // input-2 lanes read the second copy of the m = 0 mixing of the |s| = 1 sectors)
 // on the plan's backward tables, where that copy absorbs J (J moves no other
-// slots); no copy of J x is made.
+// slots); no copy of J x is made.  The shared-x2 form (spingtp_backward_v1) is
+// at the end of the file.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -43,6 +44,129 @@ extern "C" spingtp_status spingtp_backward(spingtp_plan plan, const void* x1, co
             spingtp::run_forward(plan, plan->kernel, grad_out, x1, grad_x2, N, C, false, stream, plan->d_tab_bwd,
                                  true);
         if (r != SPINGTP_OK) return r;
+    }
+    return SPINGTP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Edge input shared by the channels of an edge (spingtp_forward_v1).
+//   grad_x1[n,c] = SpinGTP'(g[n,c], J x2[n])                 (x2 shared: the v1 route)
+//   grad_x2[n]   = sum_c SpinGTP''(g[n,c], J x1[n,c])          (per unit, then summed)
+// The per-unit products of grad_x2 go to the caller's workspace [N][C][NC2] and a
+// reduction kernel sums them over the channels in a fixed order.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr int kSumThreads = 256;
+
+template <typename T>
+__device__ __forceinline__ float load_f32(const T* p);
+template <>
+__device__ __forceinline__ float load_f32<float>(const float* p) {
+    return *p;
+}
+template <>
+__device__ __forceinline__ float load_f32<uint16_t>(const uint16_t* p) {  // bf16 bits
+    return __uint_as_float(static_cast<uint32_t>(*p) << 16);
+}
+template <typename T>
+__device__ __forceinline__ T store_f32(float v);
+template <>
+__device__ __forceinline__ float store_f32<float>(float v) {
+    return v;
+}
+template <>
+__device__ __forceinline__ uint16_t store_f32<uint16_t>(float v) {  // round to nearest even
+    uint32_t u = __float_as_uint(v);
+    if ((u & 0x7f800000u) == 0x7f800000u) return static_cast<uint16_t>((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+// out[n][k] = sum_{c < C} in[n][c][k], fp32 sums in channel order; one thread per (n, k).
+template <typename T>
+__global__ __launch_bounds__(kSumThreads) void spingtp_sum_channels_kernel(const T* __restrict__ in,
+                                                                          T* __restrict__ out, int64_t N,
+                                                                          int64_t C, int nc) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kSumThreads + threadIdx.x;
+    if (i >= N * nc) return;
+    const int64_t n = i / nc;
+    const int k = static_cast<int>(i - n * nc);
+    const T* __restrict__ p = in + n * C * nc + k;
+    float acc = 0.f;
+    for (int64_t c = 0; c < C; ++c) acc += load_f32<T>(p + c * nc);
+    out[i] = store_f32<T>(acc);
+}
+
+hipError_t launch_sum_channels(const void* in, void* out, int64_t N, int64_t C, int nc, int dtype,
+                               hipStream_t stream) {
+    const int64_t blocks = (N * nc + kSumThreads - 1) / kSumThreads;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    if (dtype == SPINGTP_FP32)
+        hipLaunchKernelGGL(spingtp_sum_channels_kernel<float>, dim3(static_cast<unsigned>(blocks)), dim3(kSumThreads),
+                           0, stream, static_cast<const float*>(in), static_cast<float*>(out), N, C, nc);
+    else
+        hipLaunchKernelGGL(spingtp_sum_channels_kernel<uint16_t>, dim3(static_cast<unsigned>(blocks)),
+                           dim3(kSumThreads), 0, stream, static_cast<const uint16_t*>(in),
+                           static_cast<uint16_t*>(out), N, C, nc);
+    return hipGetLastError();
+}
+
+int64_t row_length(const spingtp_plan_s* p) {
+    return static_cast<int64_t>(p->n_spins) * (p->L2 + 1) * (p->L2 + 1);
+}
+
+}  // namespace
+
+extern "C" spingtp_status spingtp_backward_v1_workspace_size(spingtp_plan plan, int64_t N, int64_t C,
+                                                             size_t* bytes) {
+    if (plan == nullptr || bytes == nullptr || N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
+    if (plan->d_tab_bwd == nullptr || plan->kernel == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    if (N > 0 && C > 0 && N > (int64_t{1} << 40) / C) return SPINGTP_ERR_INVALID_ARG;
+    const size_t elem = plan->dtype == SPINGTP_FP32 ? 4 : 2;
+    *bytes = static_cast<size_t>(N) * static_cast<size_t>(C) * static_cast<size_t>(row_length(plan)) * elem;
+    return SPINGTP_OK;
+}
+
+extern "C" spingtp_status spingtp_backward_v1(spingtp_plan plan, const void* x1, const void* x2,
+                                              const void* grad_out, void* grad_x1, void* grad_x2, void* workspace,
+                                              size_t workspace_bytes, int64_t N, int64_t C, void* stream) {
+    size_t need = 0;
+    const spingtp_status st = spingtp_backward_v1_workspace_size(plan, N, C, &need);
+    if (st != SPINGTP_OK) return st;
+    if (N == 0 || (grad_x1 == nullptr && grad_x2 == nullptr)) return SPINGTP_OK;
+    if (misaligned(grad_x1) || misaligned(grad_x2)) return SPINGTP_ERR_INVALID_ARG;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (C == 0) {  // no channels: grad_x2 is an empty sum, written as zeros
+        if (grad_x2 == nullptr) return SPINGTP_OK;
+        int cur = -1;
+        if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
+        if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
+        return launch_sum_channels(nullptr, grad_x2, N, 0, static_cast<int>(row_length(plan)), plan->dtype, s) ==
+                       hipSuccess
+                   ? SPINGTP_OK
+                   : SPINGTP_ERR_HIP;
+    }
+    if (grad_x1 != nullptr) {
+        const spingtp::KernelEntry* k = plan->kernel_v1;
+        spingtp_status r;
+        if (k != nullptr && k->family == 5) {
+            if (plan->d_pre_bwd == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+            r = spingtp::run_forward(plan, k, grad_out, x2, grad_x1, N, C, true, stream, nullptr, true,
+                                     plan->d_pre_bwd);
+        } else {
+            r = spingtp::run_forward(plan, k, grad_out, x2, grad_x1, N, C, true, stream, plan->d_tab_bwd, true);
+        }
+        if (r != SPINGTP_OK) return r;
+    }
+    if (grad_x2 != nullptr) {
+        if (workspace == nullptr || misaligned(workspace) || workspace_bytes < need) return SPINGTP_ERR_INVALID_ARG;
+        const spingtp_status r = spingtp::run_forward(plan, plan->kernel, grad_out, x1, workspace, N, C, false,
+                                                      stream, plan->d_tab_bwd, true);
+        if (r != SPINGTP_OK) return r;
+        if (launch_sum_channels(workspace, grad_x2, N, C, static_cast<int>(row_length(plan)), plan->dtype, s) !=
+            hipSuccess)
+            return SPINGTP_ERR_HIP;
     }
     return SPINGTP_OK;
 }

@@ -65,8 +65,10 @@ const KernelEntry* find_pre_kernel_large(int ks, int nt, int dtype);
 // transposed edge kernel at LDS index dst = k3 KST + k1 and restarts it.  Whole
 // (k1, k3) lists go to one thread (longest first, to the least loaded thread), so
 // every entry has one writer; lists are padded with zero items.
-void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
-                      std::vector<uint32_t>& out);
+// conj_x2: the table of spingtp_backward_v1, whose kernel reads x2 but must use
+// J x2 (build_conj_map); false if J cannot be built.
+bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                      std::vector<uint32_t>& out, bool conj_x2 = false);
 
 // Per-lane A operands of the matrix-core kernel for L1 = L2 = Lout = L, spins
 // {-1, 0, +1}: packed fp16 (hi, lo) words; layout in forward_mfma.hip.
@@ -91,10 +93,11 @@ bool build_conj_map(int L, const int* spins, int n_spins, unsigned flags, std::v
 // Argument checks and launch of one forward kernel (api.cpp).  shared_x2: x2
 // holds one row per edge (spingtp_forward_v1), else one per unit.  tab: the
 // plan tables to use (the plan's own when nullptr); backward: launch the
-// entry's launch_bwd instantiation.
+// entry's launch_bwd instantiation (the matrix-core and vector-ALU families);
+// aux: the operand or tensor table to pass (the plan's own when nullptr).
 spingtp_status run_forward(spingtp_plan plan, const KernelEntry* k, const void* x1, const void* x2, void* out,
                            int64_t N, int64_t C, bool shared_x2, void* stream, const float* tab = nullptr,
-                           bool backward = false);
+                           bool backward = false, const uint32_t* aux = nullptr);
 
 // Dense real tensor of the operation (see spingtp_dense_tensor_host), float64.
 void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
@@ -113,6 +116,7 @@ struct spingtp_plan_s {
     size_t n_tab;
     uint32_t* d_aux;  // matrix-core operand tables, nullptr for the vector-ALU kernels
     uint32_t* d_pre;  // sparse tensor of the precontracted kernel, nullptr if not used
+    uint32_t* d_pre_bwd;  // the same with J x2 (spingtp_backward_v1), nullptr if not used
     float* d_tab_bwd;  // tables of spingtp_backward (d_tab when equal), nullptr without a backward
     bool own_tab_bwd;  // d_tab_bwd is a separate allocation
     const spingtp::KernelEntry* kernel;     // spingtp_forward

@@ -387,10 +387,14 @@ void build_mfma_operands(int L, std::vector<uint32_t>& out) {
             }
 }
 
-void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
-                      std::vector<uint32_t>& out) {
+bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                      std::vector<uint32_t>& out, bool conj_x2) {
     std::vector<double> T;
     build_dense_tensor(L1, L2, LO, spins, n_spins, flags, T);
+    // conj_x2: the kernel reads x2 but must use J x2 (spingtp_backward_v1), so
+    // each item's k2 becomes J's source slot and its value takes J's sign
+    std::vector<uint32_t> J;
+    if (conj_x2 && !build_conj_map(L2, spins, n_spins, flags, J)) return false;
     const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
     const int nco = n_spins * (LO + 1) * (LO + 1);
     const int ks = (nc1 + 15) / 16, nt = (nco + 15) / 16, kst = 16 * ks + 4;
@@ -410,7 +414,14 @@ void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
             Entry e{(k3 - b * rb) * kst + k1, {}};
             for (int k2 = 0; k2 < nc2; ++k2) {
                 const double v = T[(static_cast<size_t>(k1) * nc2 + k2) * nco + k3];
-                if (std::fabs(v) > 1e-12) e.items.emplace_back(k2, static_cast<float>(v));
+                if (std::fabs(v) <= 1e-12) continue;
+                if (conj_x2) {
+                    if (J[k2] & kConjZero) continue;  // J x2 is 0 there
+                    const double sign = (J[k2] & kConjNeg) ? -1.0 : 1.0;
+                    e.items.emplace_back(static_cast<int>(J[k2] & 0xffffu), static_cast<float>(sign * v));
+                } else {
+                    e.items.emplace_back(k2, static_cast<float>(v));
+                }
             }
             if (!e.items.empty()) entries[b].push_back(std::move(e));
         }
@@ -459,6 +470,7 @@ void build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
                 }
         }
     }
+    return true;
 }
 
 // Dense real tensor T[k1][k2][k3] = Re sum conj(Q3) G Q1 Q2 (see spingtp.h).
@@ -656,13 +668,17 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
 spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
                                       uint32_t* words, size_t capacity, size_t* count) {
     if (count == nullptr || (capacity > 0 && words == nullptr)) return SPINGTP_ERR_INVALID_ARG;
+    const bool backward = (flags & SPINGTP_TABLES_BACKWARD) != 0;
+    flags &= ~SPINGTP_TABLES_BACKWARD;
+    if (backward && (L1 != L2 || L2 != Lout)) return SPINGTP_ERR_UNSUPPORTED;
     int spin_mode = 0;
     const spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
     if (spingtp::find_pre_kernel(L1, L2, Lout, spin_mode, 0) == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     try {
         std::vector<uint32_t> w;
-        spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, w);
+        if (!spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, w, backward))
+            return SPINGTP_ERR_UNSUPPORTED;
         *count = w.size();
         const size_t n = w.size() < capacity ? w.size() : capacity;
         if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));
@@ -717,12 +733,16 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
 
     std::vector<double> tab;
     std::vector<double> tab_bwd;
-    std::vector<uint32_t> aux, pre;
+    std::vector<uint32_t> aux, pre, pre_bwd;
     bool has_backward = false, same_bwd = false;
     try {
         if (!spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
         if (k != nullptr && k->family == 4) spingtp::build_mfma_operands(L1, aux);
         if (kv1->family == 5) spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre);
+        // spingtp_backward_v1 on the precontracted kernel: the same table with J x2
+        if (kv1->family == 5 && L1 == L2 && L2 == Lout &&
+            !spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre_bwd, true))
+            pre_bwd.clear();
         // spingtp_backward: square plans with a forward kernel, input 2 conjugated
         if (k != nullptr && L1 == L2 && L2 == Lout &&
             spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab_bwd, true)) {
@@ -757,10 +777,11 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
         }
         return err;
     };
-    uint32_t *da = nullptr, *dpre = nullptr;
+    uint32_t *da = nullptr, *dpre = nullptr, *dpreb = nullptr;
     float* dbwd = nullptr;
     e = upload(aux, &da);
     if (e == hipSuccess) e = upload(pre, &dpre);
+    if (e == hipSuccess) e = upload(pre_bwd, &dpreb);
     if (e == hipSuccess && has_backward && !same_bwd) {
         std::vector<float> f(tab_bwd.size());
         for (size_t i = 0; i < tab_bwd.size(); ++i) f[i] = static_cast<float>(tab_bwd[i]);
@@ -770,6 +791,7 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     auto release = [&]() {
         if (da != nullptr) (void)hipFree(da);
         if (dpre != nullptr) (void)hipFree(dpre);
+        if (dpreb != nullptr) (void)hipFree(dpreb);
         if (dbwd != nullptr) (void)hipFree(dbwd);
         (void)hipFree(d);
     };
@@ -794,6 +816,7 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     p->n_tab = tabf.size();
     p->d_aux = da;
     p->d_pre = dpre;
+    p->d_pre_bwd = dpreb;
     p->d_tab_bwd = has_backward ? (same_bwd ? d : dbwd) : nullptr;
     p->own_tab_bwd = dbwd != nullptr;
     p->kernel = k;
@@ -810,6 +833,7 @@ spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
     if (e == hipSuccess) e = hipFree(plan->d_tab);
     if (e == hipSuccess && plan->d_aux != nullptr) e = hipFree(plan->d_aux);
     if (e == hipSuccess && plan->d_pre != nullptr) e = hipFree(plan->d_pre);
+    if (e == hipSuccess && plan->d_pre_bwd != nullptr) e = hipFree(plan->d_pre_bwd);
     if (e == hipSuccess && plan->own_tab_bwd) e = hipFree(plan->d_tab_bwd);
     if (cur != plan->device) (void)hipSetDevice(cur);
     delete plan;

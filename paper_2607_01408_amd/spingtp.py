@@ -63,9 +63,11 @@ def mfma_operands_host(L):
     return out
 
 
-def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
-    """spingtp_pre_table_host: the tensor table of the precontracted kernel (uint32 words)."""
+def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, backward=False):
+    """spingtp_pre_table_host: the tensor table of the precontracted kernel (uint32 words); with
+    backward=True the table of spingtp_backward_v1."""
     arr, n = _spin_array(spins)
+    basis = basis | (0x800 if backward else 0)
     count = ctypes.c_size_t(0)
     _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, basis, None, 0, ctypes.byref(count)),
                "spingtp_pre_table_host")
@@ -197,6 +199,36 @@ class Plan:
                                                gx1.data_ptr() if gx1 is not None else None,
                                                gx2.data_ptr() if gx2 is not None else None, N, C,
                                                ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward")
+        return gx1, gx2
+
+    def backward_v1(self, x1, x2, grad_out, need_x1=True, need_x2=True, stream=None):
+        """spingtp_backward_v1: (grad_x1 [N, C, ...], grad_x2 [N, 1, ...]) through forward_v1; the workspace
+        for grad_x2 comes from torch's allocator."""
+        import torch
+
+        if x2.dim() == 3:
+            x2 = x2.unsqueeze(1)
+        N, C = x1.shape[0], x1.shape[1]
+        for t, shape in ((x1, (N, C) + tuple(self.shape_in(1))), (x2, (N, 1) + tuple(self.shape_in(2))),
+                         (grad_out, (N, C) + tuple(self.shape_out))):
+            if (tuple(t.shape) != shape or t.dtype != self.torch_dtype or not t.is_cuda
+                    or not t.is_contiguous()):
+                raise ValueError("x1 [N, C, ...], x2 [N, 1, ...], grad_out [N, C, ...] must be contiguous device "
+                                 "tensors of the plan's dtype")
+        gx1 = torch.empty_like(x1) if need_x1 else None
+        gx2 = torch.empty_like(x2) if need_x2 else None
+        n = ctypes.c_size_t(0)
+        _lib.check(_lib.lib().spingtp_backward_v1_workspace_size(self._handle, N, C, ctypes.byref(n)),
+                   "spingtp_backward_v1_workspace_size")
+        ws = torch.empty(max(1, n.value), dtype=torch.uint8, device=x1.device) if need_x2 else None
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+        _lib.check(_lib.lib().spingtp_backward_v1(self._handle, x1.data_ptr(), x2.data_ptr(), grad_out.data_ptr(),
+                                                  gx1.data_ptr() if gx1 is not None else None,
+                                                  gx2.data_ptr() if gx2 is not None else None,
+                                                  ws.data_ptr() if ws is not None else None,
+                                                  n.value if ws is not None else 0, N, C,
+                                                  ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_v1")
         return gx1, gx2
 
     __call__ = forward

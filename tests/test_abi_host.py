@@ -500,3 +500,21 @@ def test_backward_tables_reproduce_oracle(built_library, L, spin, basis):
     if spin and basis == 0 and L > 0:
         # the paper basis needs the conjugation: the forward tables alone give a different map
         assert np.abs(emulate_kernel(g, x2, L, L, L, spin, basis) - r1).max() > 1e-3
+
+
+@pytest.mark.parametrize("L,spins,basis", [(1, (-1, 0, 1), 0), (3, (-1, 0, 1), 0), (4, (-1, 0, 1), 1),
+                                           (5, (-1, 0, 1), 0), (6, (-1, 0, 1), 0), (4, (0,), 0)])
+def test_backward_pre_table_reproduces_oracle(built_library, L, spins, basis):
+    """spingtp_backward_v1's grad_x1 on the precontracted kernel: its table (x2
+    indices and signs through J), re-enacted on (grad_out, x2), gives the oracle's
+    grad_x1 for channels that share x2."""
+    words = pre_table_host(L, L, L, spins, basis, backward=True)
+    rng = np.random.default_rng(200 + L)
+    n = len(spins) * (L + 1) ** 2
+    C = 3
+    x1 = rng.standard_normal((C, n)) * valid_mask(spins, L)
+    x2 = rng.standard_normal(n) * valid_mask(spins, L)
+    g = rng.standard_normal((C, n)) * valid_mask(spins, L)
+    y, _ = emulate_pre_kernel(words, g, x2)
+    r1, _ = oracle.RealGauntTensor(L, L, L, spins, basis).vjp(x1, np.broadcast_to(x2, (C, n)), g)
+    assert np.abs(y - r1).max() <= 1e-6 * max(1.0, np.abs(r1).max())

@@ -6,6 +6,8 @@ bf16, 1e-6 for the matrix-core kernel (family 4) in fp32.  The oracle sees the
 dtype-rounded inputs read back from the device.
 """
 
+import ctypes
+
 import numpy as np
 import pytest
 
@@ -159,3 +161,83 @@ def test_backward_full_size_organic_sampled():
     e2 = rel_l2(gx2.view(U, -1)[ti].double().cpu().numpy(), r2)
     print(f"[backward] organic full size: rel_l2 {e1:.3e} {e2:.3e}", flush=True)
     assert e1 <= 1e-6 and e2 <= 1e-6
+
+
+# ---------------------------------------------------------------------------
+# spingtp_backward_v1: x2 shared by the channels of an edge
+# ---------------------------------------------------------------------------
+
+def run_backward_v1(L, spins, N, C, dtype="fp32", basis=0, seed=0, fourier=False, precontract=False):
+    print(f"[backward-v1] L={L} spins={spins} N={N} C={C} {dtype} basis={basis} fourier={fourier} "
+          f"precontract={precontract}", flush=True)
+    x1 = workloads.draw(L, N, C, 610 + seed, dtype, spins, "unit", "cuda")
+    x2 = workloads.draw(L, N, 1, 710 + seed, dtype, spins, "unit", "cuda")
+    g = workloads.draw(L, N, C, 810 + seed, dtype, spins, "unit", "cuda")
+    plan = Plan(L, L, L, spins, dtype, basis, v1_fourier=fourier, v1_precontract=precontract)
+    gx1, gx2 = plan.backward_v1(x1, x2, g)
+    torch.cuda.synchronize()
+    U, n = N * C, len(spins) * (L + 1) ** 2
+    a = x1.view(U, n).double().cpu().numpy()
+    b = np.repeat(x2.view(N, n).double().cpu().numpy(), C, axis=0)
+    c = g.view(U, n).double().cpu().numpy()
+    r1, r2 = oracle.RealGauntTensor(L, L, L, spins, basis).vjp(a, b, c)
+    r2 = r2.reshape(N, C, n).sum(axis=1)
+    e1 = rel_l2(gx1.view(U, n).double().cpu().numpy(), r1)
+    e2 = rel_l2(gx2.view(N, n).double().cpu().numpy(), r2)
+    fam = plan.kernel_info_v1()["family"]
+    print(f"[backward-v1]   rel_l2 {e1:.3e} {e2:.3e} v1 family={fam}", flush=True)
+    assert e1 <= TOL[dtype] and e2 <= TOL[dtype], (e1, e2)
+    return fam, (e1, e2)
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("basis", [0, 1])
+def test_backward_v1_matches_oracle(L, basis):
+    # default route: precontracted up to L = 5, Fourier at L = 6
+    fam, _ = run_backward_v1(L, S3, 13, 17, "fp32", basis, seed=L + 10 * basis)
+    assert (fam == 5) == (L <= 5)
+
+
+@pytest.mark.parametrize("L,C,fourier,precontract", [(3, 40, True, False), (4, 1, True, False),
+                                                     (6, 33, False, True), (2, 130, False, False)])
+def test_backward_v1_routes_and_channel_counts(L, C, fourier, precontract):
+    run_backward_v1(L, S3, 7, C, "fp32", 0, seed=3 * L + C, fourier=fourier, precontract=precontract)
+
+
+@pytest.mark.parametrize("L", [3, 6])
+def test_backward_v1_scalar_spin_and_bf16(L):
+    run_backward_v1(L, (0,), 9, 20, "fp32", 0, seed=L)
+    run_backward_v1(L, S3, 9, 20, "bf16", 0, seed=L + 1)
+
+
+def test_backward_v1_rules():
+    L = 2
+    N, C = 5, 6
+    plan = Plan(L, L, L, S3, "fp32")
+    x1 = workloads.draw(L, N, C, 1, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(L, N, 1, 2, "fp32", S3, "unit", "cuda")
+    g = workloads.draw(L, N, C, 3, "fp32", S3, "unit", "cuda")
+    full1, full2 = plan.backward_v1(x1, x2, g)
+    only1, none2 = plan.backward_v1(x1, x2, g, need_x2=False)
+    torch.cuda.synchronize()
+    assert none2 is None and torch.equal(only1, full1)
+    lib = _lib.lib()
+    gx2 = torch.empty_like(x2)
+    need = ctypes.c_size_t(0)
+    assert lib.spingtp_backward_v1_workspace_size(plan.handle, N, C, ctypes.byref(need)) == 0
+    assert need.value == N * C * 27 * 4
+    ws = torch.empty(need.value, dtype=torch.uint8, device="cuda")
+    args = (plan.handle, x1.data_ptr(), x2.data_ptr(), g.data_ptr(), None, gx2.data_ptr())
+    assert lib.spingtp_backward_v1(*args, None, 0, N, C, None) == 1  # workspace missing
+    assert lib.spingtp_backward_v1(*args, ws.data_ptr(), need.value - 1, N, C, None) == 1  # too small
+    assert lib.spingtp_backward_v1(*args, ws.data_ptr(), need.value, N, C, None) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(gx2, full2)
+    # no channels: grad_x2 is the empty sum
+    gx2.fill_(7.0)
+    assert lib.spingtp_backward_v1(*args, None, 0, N, 0, None) == 0
+    torch.cuda.synchronize()
+    assert (gx2 == 0).all()
+    # a plan whose shape has no spingtp_forward kernel has no backward
+    mixed = Plan(3, 1, 2, S3, "fp32")
+    assert lib.spingtp_backward_v1_workspace_size(mixed.handle, N, C, ctypes.byref(need)) == 2
