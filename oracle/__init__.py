@@ -26,13 +26,13 @@ library routines (scipy, sympy).
 """
 
 from .swsh import swsh, theta_part, goldberg_prefactor
-from .realbasis import q_matrix, real_index, conjugation_map, BASIS_PAPER, BASIS_M0_PAIRED
+from .realbasis import q_matrix, real_index, conjugation_map, parity_mix, BASIS_PAPER, BASIS_M0_PAIRED, BASIS_PARITY
 from .gaunt import gauss_legendre_grid, gaunt_block, gaunt_full_quadrature
 from .spingtp import RealGauntTensor, spingtp, spingtp_vjp
 
 __all__ = [
     "swsh", "theta_part", "goldberg_prefactor",
-    "q_matrix", "real_index", "BASIS_PAPER", "BASIS_M0_PAIRED",
+    "q_matrix", "real_index", "parity_mix", "BASIS_PAPER", "BASIS_M0_PAIRED", "BASIS_PARITY",
     "gauss_legendre_grid", "gaunt_block", "gaunt_full_quadrature",
     "RealGauntTensor", "spingtp",
 ]

@@ -35,6 +35,7 @@ import numpy as np
 
 BASIS_PAPER = 0
 BASIS_M0_PAIRED = 1
+BASIS_PARITY = 2
 
 _R2 = 1.0 / math.sqrt(2.0)
 
@@ -45,13 +46,41 @@ def real_index(spins, L, s, l, k) -> int:
     return si * (L + 1) ** 2 + l * l + l + k
 
 
+def parity_mix(spins, L) -> np.ndarray:
+    """Real orthogonal P with x_real = P x_parity for the parity-labelled basis.
+
+    Sec. 3.4 eq. parity_basis / App. D: for |s| > 0,
+    R_p^{s,l,m} = (R_{-s,l,m} + p (-1)^l R_{s,l,m}) / sqrt2, p = +-1.  Storage
+    reading: the coefficient of p = +1 sits in the -|s| block, that of p = -1 in
+    the +|s| block (App. C orders the -|s| sector first); s = 0 is unchanged.  So a
+    function sum_p c_p R_p has real-basis coefficients
+    x[-s,l,m] = (c_+ + c_-)/sqrt2 and x[s,l,m] = (-1)^l (c_+ - c_-)/sqrt2.
+    """
+    spins = tuple(spins)
+    n = len(spins) * (L + 1) ** 2
+    P = np.eye(n)
+    for s in spins:
+        if s <= 0:
+            continue
+        for l in range(s, L + 1):
+            t = (-1.0) ** (l % 2)
+            for m in range(-l, l + 1):
+                a, b = real_index(spins, L, -s, l, m), real_index(spins, L, s, l, m)
+                P[a, a], P[a, b] = _R2, _R2
+                P[b, a], P[b, b] = t * _R2, -t * _R2
+    return P
+
+
 def q_matrix(spins, L, basis=BASIS_PAPER) -> np.ndarray:
     """Dense complex Q of shape [n, n], n = len(spins) * (L+1)^2.
 
     ``spins`` must be symmetric (contain -s for every s) so that every |s| > 0
-    sector is doubled as the paper requires.
+    sector is doubled as the paper requires.  BASIS_PARITY is the parity-labelled
+    basis built on the paper's literal real basis: Q = Q_paper P (parity_mix).
     """
     spins = tuple(spins)
+    if basis == BASIS_PARITY:
+        return q_matrix(spins, L, BASIS_PAPER) @ parity_mix(spins, L)
     for s in spins:
         if -s not in spins:
             raise ValueError("spin set must be symmetric")

@@ -38,14 +38,14 @@ _PRUNE = 1e-13
 
 
 def _row_lists(Q):
-    """Nonzero (column, value) pairs of each row of Q, padded to 2 per row."""
+    """Nonzero (column, value) pairs of each row of Q, padded to the longest row
+    (two for the real bases of eq. real_swsh, four for the parity-labelled one)."""
     n = Q.shape[0]
-    cols = np.zeros((n, 2), dtype=np.int64)
-    vals = np.zeros((n, 2), dtype=np.complex128)
+    width = max(1, max(len(np.nonzero(Q[r])[0]) for r in range(n)))
+    cols = np.zeros((n, width), dtype=np.int64)
+    vals = np.zeros((n, width), dtype=np.complex128)
     for r in range(n):
         nz = np.nonzero(Q[r])[0]
-        if len(nz) > 2:
-            raise AssertionError("Q row with more than two entries")
         cols[r, :len(nz)] = nz
         vals[r, :len(nz)] = Q[r, nz]
     return cols, vals
@@ -97,9 +97,9 @@ class RealGauntTensor:
         c2, v2 = _row_lists(q_matrix(spins, L2, basis))
         c3, v3 = _row_lists(q_matrix(spins, Lout, basis))
         K1, K2, K3, V = [], [], [], []
-        for i in range(2):
-            for j in range(2):
-                for l in range(2):
+        for i in range(c1.shape[1]):
+            for j in range(c2.shape[1]):
+                for l in range(c3.shape[1]):
                     val = (v1[A, i] * v2[B, j] * Gv * np.conj(v3[E, l])).real
                     keep = val != 0.0
                     K1.append(c1[A, i][keep])
