@@ -76,15 +76,20 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def profile_tag(workload, dtype, L, valu=False):
+BASES = {"paper": 0, "m0_paired": 1, "parity": 2}
+
+
+def profile_tag(workload, dtype, L, valu=False, basis="paper"):
     tag = f"{workload}_L{L}_{dtype}" if workload == "sweep" else f"{workload}_{dtype}"
+    if basis != "paper":
+        tag += f"_{basis}"
     return tag + "_valu" if valu else tag
 
 
-def measured_traffic(workload, dtype, units, L, kname, valu=False):
+def measured_traffic(workload, dtype, units, L, kname, valu=False, basis="paper"):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it
     was taken on the current kernel source and the same kernel; else None."""
-    path = os.path.join(ROOT, "profiles", f"traffic_spingtp_fwd_{profile_tag(workload, dtype, L, valu)}.json")
+    path = os.path.join(ROOT, "profiles", f"traffic_spingtp_fwd_{profile_tag(workload, dtype, L, valu, basis)}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -415,6 +420,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="organic")
     ap.add_argument("--dtype", default="fp32")
+    ap.add_argument("--basis", default="paper", choices=sorted(BASES),
+                    help="real basis of the coefficients (parity: the parity-labelled basis)")
     ap.add_argument("--L", type=int, default=None, help="degree (sweep workload only)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -459,7 +466,7 @@ def main():
     x1, x2, meta = workloads.make_pair(args.workload, dtype=args.dtype, L=args.L, device="cuda:0")
     L = meta["L"]
     U = meta["N"] * meta["C"]
-    plan = Plan(L, L, L, workloads.SPINS, args.dtype, valu_only=args.valu)
+    plan = Plan(L, L, L, workloads.SPINS, args.dtype, BASES[args.basis], valu_only=args.valu)
     out = torch.empty((meta["N"], meta["C"], 3, (L + 1) ** 2), dtype=x1.dtype, device="cuda:0")
     print(f"[bench] {meta['workload']} L={L} N={meta['N']} C={meta['C']} {args.dtype} units={U} "
           f"kernel={plan.kernel_info()}", file=sys.stderr, flush=True)
@@ -497,7 +504,7 @@ def main():
             else "f32 (phi transforms: fp16 matrix products, fp32 accumulate)"
     else:
         compute = "f32"
-    traffic = measured_traffic(meta["workload"], args.dtype, U, L, kname, args.valu)
+    traffic = measured_traffic(meta["workload"], args.dtype, U, L, kname, args.valu, args.basis)
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib * (1 << 20) // 4
@@ -518,7 +525,7 @@ def main():
     ti = torch.as_tensor(idx, device="cuda:0")
     ya = out.view(U, -1)[ti].double().cpu().numpy()
     ref = oracle.spingtp(x1.view(U, -1)[ti].double().cpu().numpy(), x2.view(U, -1)[ti].double().cpu().numpy(),
-                         L, L, L, workloads.SPINS).reshape(len(idx), -1)
+                         L, L, L, workloads.SPINS, BASES[args.basis]).reshape(len(idx), -1)
     parity = float(np.linalg.norm(ya - ref) / np.linalg.norm(ref))
 
     result = {
@@ -539,7 +546,7 @@ def main():
         "config": {
             "workload": f"{meta['workload']}: L1=L2=Lout={L}, spins (-1,0,+1), N={meta['N']} edges x "
                         f"C={meta['C']} channels ({U} units), {args.dtype} I/O, N(0,1) coefficients",
-            "L1": L, "L2": L, "Lout": L, "N": meta["N"], "C": meta["C"], "units": U,
+            "L1": L, "L2": L, "Lout": L, "N": meta["N"], "C": meta["C"], "units": U, "basis": args.basis,
             "seeds": list(meta["seeds"]),
         },
         "roofline": {

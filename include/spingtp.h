@@ -30,7 +30,16 @@
  *   SPINGTP_BASIS_REAL_PAPER      that definition literally (default);
  *   SPINGTP_BASIS_REAL_M0_PAIRED  the m = 0 pair (s,0),(-s,0) mixed as
  *                                 (1/sqrt2)(1, (-1)^s) and (i/sqrt2)(1, -(-1)^s),
- *                                 which makes the real basis closed under rotation.
+ *                                 which makes the real basis closed under rotation;
+ *   SPINGTP_BASIS_PARITY          the parity-labelled basis of Sec. 3.4 eq.
+ *                                 parity_basis, built on the paper basis:
+ *                                 R_p = (R_{-s} + p (-1)^l R_s)/sqrt2, p = +-1, for
+ *                                 |s| > 0; the coefficient of p = +1 is stored in
+ *                                 the -|s| block and that of p = -1 in the +|s|
+ *                                 block (s = 0 unchanged).  Not built for the
+ *                                 large-degree kernels (spingtp_forward with
+ *                                 max(L1, L2, Lout) >= 9 and spins {-1,0,1}
+ *                                 returns SPINGTP_ERR_UNSUPPORTED at plan creation).
  *
  * Threading and ownership: a plan is immutable after creation; concurrent
  * spingtp_forward calls with one plan on different streams or threads are safe.
@@ -61,6 +70,7 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
 
 #define SPINGTP_BASIS_REAL_PAPER 0u
 #define SPINGTP_BASIS_REAL_M0_PAIRED 1u
+#define SPINGTP_BASIS_PARITY 2u
 
 /* Kernel choice, OR-ed into the flags of spingtp_plan_create: use the fp32
  * vector-ALU kernels even where a matrix-core kernel is built (family 4 below).
@@ -159,7 +169,9 @@ spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void*
  * kernel each, on backward tables where J is folded into the input-2 mixing of
  * the m = 0 slots of the |s| = 1 sectors (the only slots J moves: with
  * SPINGTP_BASIS_REAL_PAPER they swap between s = +1 and -1 with a sign change; J is
- * the identity for SPINGTP_BASIS_REAL_M0_PAIRED and spins {0}).  Built for plans
+ * the identity for SPINGTP_BASIS_REAL_M0_PAIRED and spins {0}; with
+ * SPINGTP_BASIS_PARITY the kernel mixes its tiles into the paper basis first, where
+ * that J applies, since P^T J P x = P^T J (P x)).  Built for plans
  * with L1 = L2 = Lout that have a spingtp_forward kernel; otherwise
  * SPINGTP_ERR_UNSUPPORTED.
  *   x1, x2, grad_out: as x1, x2, out of spingtp_forward; grad_x1, grad_x2: same

@@ -202,6 +202,35 @@ __device__ __forceinline__ void store_tile(uint16_t* __restrict__ dst, int nvali
     for (int e = 8 * n8 + tid; e < n; e += nthr) dst[e] = f32_to_bf16(get<NC, ST>(src, e));
 }
 
+// Parity-labelled basis (paper Sec. 3.4 eq. parity_basis): in a tile of rows
+// [spin -1 | 0 | +1][(L+1)^2] at stride st, map parity-basis coefficients to the
+// real basis the kernels compute in (x = P x_p; inverse = false) or real-basis
+// outputs back to the parity basis (y_p = P^T y; inverse = true).  Per slot of
+// degree l >= 1 of the -1 and +1 blocks (c_+ stored in the -1 block, c_- in +1):
+// x[-1] = (c_+ + c_-)/sqrt2, x[+1] = (-1)^l (c_+ - c_-)/sqrt2.
+template <int L>
+__device__ void parity_mix_rows(float* tile, int st, int rows, bool inverse, int tid, int nthr) {
+    constexpr int B = (L + 1) * (L + 1);
+    constexpr int NQ = B - 1;  // slots with l >= 1 in one spin block
+    const float h = 0.70710678118654752440f;
+    for (int i = tid; i < rows * NQ; i += nthr) {
+        const int r = i / NQ, q = i - r * NQ + 1;
+        int l = static_cast<int>(sqrtf(static_cast<float>(q)));
+        if ((l + 1) * (l + 1) <= q) ++l;
+        if (l * l > q) --l;
+        const float t = (l & 1) ? -1.f : 1.f;
+        float* row = tile + static_cast<int64_t>(r) * st;
+        const float a = row[q], b = row[2 * B + q];
+        if (!inverse) {
+            row[q] = (a + b) * h;
+            row[2 * B + q] = t * (a - b) * h;
+        } else {
+            row[q] = fmaf(t, b, a) * h;
+            row[2 * B + q] = fmaf(-t, b, a) * h;
+        }
+    }
+}
+
 // Step (A) for one input of degree L at one theta node.
 //   xr  : this lane's LDS row ([n_spins][(L+1)^2], spin order -1, 0, +1)
 //   tb  : the node's table block; n0: the global N0 mixing of input 1, followed by

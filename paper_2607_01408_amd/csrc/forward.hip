@@ -149,6 +149,15 @@ __global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fw
     else
         load_tile_shared<S::NC2, S::ST2>(x2, u0, nvalid, cpx2, X2, tid, S::THREADS);
     __syncthreads();
+    bool parity = false;  // uniform
+    if constexpr (SPIN) {
+        parity = tab[Y.par] != 0.f;
+        if (parity) {
+            parity_mix_rows<L1>(X1, S::ST1, nvalid, false, tid, S::THREADS);
+            parity_mix_rows<L2>(X2, S::ST2, nvalid, false, tid, S::THREADS);
+            __syncthreads();
+        }
+    }
 
     const float* __restrict__ g = tab;
     const float* __restrict__ tb = tab + Y.glob + node * Y.pb;
@@ -326,6 +335,12 @@ __global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fw
         }
     }
     __syncthreads();
+    if constexpr (SPIN) {
+        if (parity) {
+            parity_mix_rows<LO>(YT, S::STO, nvalid, true, tid, S::THREADS);
+            __syncthreads();
+        }
+    }
     store_tile<S::NCO, S::STO>(out + u0 * S::NCO, nvalid, YT, tid, S::THREADS);
 }
 
@@ -568,6 +583,15 @@ __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pai
     else
         load_tile_shared<P::NC, P::ST>(x2, u0, nvalid, cpx2, X2, tid, P::THREADS);
     __syncthreads();
+    bool parity = false;  // uniform
+    if constexpr (SPIN) {
+        parity = tab[Y.par] != 0.f;
+        if (parity) {
+            parity_mix_rows<L>(X1, P::ST, nvalid, false, tid, P::THREADS);
+            parity_mix_rows<L>(X2, P::ST, nvalid, false, tid, P::THREADS);
+            __syncthreads();
+        }
+    }
 
     const float* __restrict__ tb = tab + Y.glob + node * Y.pb;
     float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
@@ -600,6 +624,12 @@ __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pai
         }
     }
     __syncthreads();
+    if constexpr (SPIN) {
+        if (parity) {
+            parity_mix_rows<L>(YT, P::ST, nvalid, true, tid, P::THREADS);
+            __syncthreads();
+        }
+    }
     store_tile<P::NC, P::ST>(out + u0 * P::NC, nvalid, YT, tid, P::THREADS);
 }
 

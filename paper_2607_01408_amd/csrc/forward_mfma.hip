@@ -295,6 +295,12 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
         lds[S::X2 + nvalid * ST + i] = 0.f;
     }
     __syncthreads();
+    const bool parity = tab[Y.par] != 0.f;  // uniform
+    if (parity) {
+        parity_mix_rows<L>(lds, ST, nvalid, false, tid, S::THREADS);
+        parity_mix_rows<L>(lds + S::X2, ST, nvalid, false, tid, S::THREADS);
+        __syncthreads();
+    }
 
     // (2) per unit and input: scale the row by 2^-e so that its largest valid
     //     magnitude is in [1/2, 1).  Two threads per row; the l = 0 slots of the
@@ -498,6 +504,11 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
             yr[l * l + l + sm * t] = ldexpf(oM[t][l], es);
         }
     __syncthreads();
+    if (parity) {  // each partial tile to the parity basis (the map is linear)
+        parity_mix_rows<L>(lds, ST, nvalid, true, tid, S::THREADS);
+        parity_mix_rows<L>(lds + S::YB, ST, nvalid, true, tid, S::THREADS);
+        __syncthreads();
+    }
     store_out<NC, ST, S::UNITS, S::THREADS>(out + u0 * NC, nvalid, lds, S::YB, tid);
 }
 

@@ -12,8 +12,11 @@
 //   global part (offsets from 0):
 //     N0[4][2]   t = 0 mixing of the |s| = 1 sector on input:
 //                (W+, W-) -> (B~c0, C~c0, delta, eps)
+//     N0B[4][2]  the same for input 2 (absorbs conjugation on backward tables)
 //     M0[2][4]   t = 0 mixing of the |s| = 1 sector on output:
 //                (sum hR+, sum hI+, sum hR-, sum hI-) -> (Z+, Z-)
+//     PAR[4]     PAR[0] = 1: the plan's basis is the parity-labelled one and the
+//                kernels mix tiles by P on load and by P^T before the store
 //     COS[n_phi][TM+1], SIN[n_phi][TM+1]   cos(t phi_k), sin(t phi_k)
 //   then one block per theta node j (offset glob + j * pb):
 //     A0C, A0S, AUP, AUM   triangles over (t, l), l >= t, degree LA = max(L1, L2)
@@ -28,7 +31,7 @@ namespace spingtp {
 struct Layout {
     int L1, L2, LO, LA, TM, NT, NP;
     int triA, triO;
-    int n0, n0b, m0, cosT, sinT, glob;
+    int n0, n0b, m0, par, cosT, sinT, glob;
     int a0c, a0s, aup, aum, aw, e0c, e0s, e1p, e1m, e1z, pb;
     int total;
 };
@@ -52,7 +55,8 @@ __host__ __device__ constexpr Layout make_layout(int L1, int L2, int LO) {
     y.n0 = 0;
     y.n0b = 8;
     y.m0 = 16;
-    y.cosT = 24;
+    y.par = 24;  // 1: the plan's basis is the parity-labelled one (tiles are mixed on load and store)
+    y.cosT = 28;
     y.sinT = y.cosT + y.NP * (y.TM + 1);
     y.glob = round4(y.sinT + y.NP * (y.TM + 1));
     y.a0c = 0;

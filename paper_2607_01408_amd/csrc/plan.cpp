@@ -136,10 +136,73 @@ int real_column(int sigma, int k, unsigned flags, QEnt* e) {
     return 2;
 }
 
+// The parity-labelled basis (Sec. 3.4 eq. parity_basis) is the paper's real
+// basis followed by the orthogonal map P, x_real = P x_parity: per slot (l, m)
+// with l >= |s| > 0, x[-s] = (c_+ + c_-)/sqrt2 and x[s] = (-1)^l (c_+ - c_-)/sqrt2,
+// c_+ stored in the -|s| block and c_- in the +|s| block.  Every table of a
+// parity plan is derived from the paper basis through P.
+unsigned literal_basis(unsigned flags) {
+    return flags == SPINGTP_BASIS_PARITY ? SPINGTP_BASIS_REAL_PAPER : flags;
+}
+
+// v <- P^T v (transpose = true) or v <- P v, along one axis of a strided array:
+// element i of the axis sits at base + i * stride.
+void parity_axis(double* base, size_t stride, int L, const int* spins, int n_spins, bool transpose) {
+    const int nb = (L + 1) * (L + 1);
+    const double h = 1.0 / kSqrt2;
+    for (int a = 0; a < n_spins; ++a) {
+        const int s = spins[a];
+        if (s <= 0) continue;
+        int b = -1;  // block of -s
+        for (int i = 0; i < n_spins; ++i)
+            if (spins[i] == -s) b = i;
+        for (int l = s; l <= L; ++l) {
+            const double t = (l % 2) ? -1.0 : 1.0;
+            for (int m = -l; m <= l; ++m) {
+                double& xm = base[(static_cast<size_t>(b) * nb + l * l + l + m) * stride];  // -s block
+                double& xp = base[(static_cast<size_t>(a) * nb + l * l + l + m) * stride];  // +s block
+                const double u = xm, v = xp;
+                if (transpose) {
+                    xm = (u + t * v) * h;
+                    xp = (u - t * v) * h;
+                } else {
+                    xm = (u + v) * h;
+                    xp = t * (u - v) * h;
+                }
+            }
+        }
+    }
+}
+
 }  // namespace
 
 bool build_conj_map(int L, const int* spins, int n_spins, unsigned flags, std::vector<uint32_t>& out) {
     const int nb = (L + 1) * (L + 1);
+    if (flags == SPINGTP_BASIS_PARITY) {
+        // J_parity = P^T J P, again a signed permutation (or zero) row by row
+        std::vector<uint32_t> lit;
+        if (!build_conj_map(L, spins, n_spins, SPINGTP_BASIS_REAL_PAPER, lit)) return false;
+        const size_t n = lit.size();
+        std::vector<double> Jd(n * n, 0.0);
+        for (size_t j = 0; j < n; ++j)
+            if (!(lit[j] & kConjZero)) Jd[j * n + (lit[j] & 0xffffu)] = (lit[j] & kConjNeg) ? -1.0 : 1.0;
+        // (J P)[r, :] = P^T applied to row r; then P^T (J P) column by column
+        for (size_t r = 0; r < n; ++r) parity_axis(Jd.data() + r * n, 1, L, spins, n_spins, true);
+        for (size_t c = 0; c < n; ++c) parity_axis(Jd.data() + c, n, L, spins, n_spins, true);
+        out.assign(n, kConjZero);
+        for (size_t j = 0; j < n; ++j) {
+            int hits = 0;
+            for (size_t i = 0; i < n; ++i) {
+                const double v = Jd[j * n + i];
+                if (std::fabs(v) < 1e-9) continue;
+                if (std::fabs(std::fabs(v) - 1.0) > 1e-9) return false;
+                out[j] = static_cast<uint32_t>(i) | (v < 0 ? kConjNeg : 0u);
+                ++hits;
+            }
+            if (hits > 1) return false;
+        }
+        return true;
+    }
     out.assign(static_cast<size_t>(n_spins) * nb, kConjZero);
     auto slot = [&](int si, int l, int k) { return si * nb + l * l + l + k; };
     for (int si = 0; si < n_spins; ++si)
@@ -188,6 +251,11 @@ bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::ve
                   bool conj_input2) {
     const Layout Y = make_layout(L1, L2, LO);
     out.assign(Y.total, 0.0);
+    // a parity plan runs the paper basis's tables on tiles mixed by P (inputs) and
+    // P^T (output); the conjugation folded below is then the paper basis's J,
+    // since P^T J P x = P^T J (P x)
+    out[Y.par] = (flags == SPINGTP_BASIS_PARITY && spin_mode == 1) ? 1.0 : 0.0;
+    flags = literal_basis(flags);
     const double sq2 = kSqrt2;
 
     if (spin_mode == 1) {
@@ -480,6 +548,18 @@ bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
 void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
                         std::vector<double>& T) {
     const int nb1 = (L1 + 1) * (L1 + 1), nb2 = (L2 + 1) * (L2 + 1), nbo = (LO + 1) * (LO + 1);
+    if (flags == SPINGTP_BASIS_PARITY) {
+        // T_parity[k1,k2,k3] = sum P[a,k1] P[b,k2] P[c,k3] T[a,b,c]: P^T along each axis
+        build_dense_tensor(L1, L2, LO, spins, n_spins, SPINGTP_BASIS_REAL_PAPER, T);
+        const size_t n1 = static_cast<size_t>(n_spins) * nb1, n2 = static_cast<size_t>(n_spins) * nb2,
+                     n3 = static_cast<size_t>(n_spins) * nbo;
+        for (size_t i = 0; i < n1 * n2; ++i) parity_axis(T.data() + i * n3, 1, LO, spins, n_spins, true);
+        for (size_t i = 0; i < n1; ++i)
+            for (size_t c = 0; c < n3; ++c)
+                parity_axis(T.data() + i * n2 * n3 + c, n3, L2, spins, n_spins, true);
+        for (size_t r = 0; r < n2 * n3; ++r) parity_axis(T.data() + r, n2 * n3, L1, spins, n_spins, true);
+        return;
+    }
     const size_t nc1 = static_cast<size_t>(n_spins) * nb1, nc2 = static_cast<size_t>(n_spins) * nb2,
                  nco = static_cast<size_t>(n_spins) * nbo;
     T.assign(nc1 * nc2 * nco, 0.0);
@@ -564,7 +644,8 @@ spingtp_status check_args(int L1, int L2, int Lout, const int* spins, int n_spin
     if (L1 < 0 || L2 < 0 || L1 > 16 || L2 > 16 || Lout < 0 || Lout > L1 + L2) return SPINGTP_ERR_INVALID_ARG;
     if (spins == nullptr || n_spins <= 0 || n_spins > 64) return SPINGTP_ERR_INVALID_ARG;
     const unsigned basis = flags & ~kRouteFlags;
-    if (basis != SPINGTP_BASIS_REAL_PAPER && basis != SPINGTP_BASIS_REAL_M0_PAIRED) return SPINGTP_ERR_INVALID_ARG;
+    if (basis != SPINGTP_BASIS_REAL_PAPER && basis != SPINGTP_BASIS_REAL_M0_PAIRED && basis != SPINGTP_BASIS_PARITY)
+        return SPINGTP_ERR_INVALID_ARG;
     if ((flags & SPINGTP_V1_FOURIER) && (flags & SPINGTP_V1_PRECONTRACT)) return SPINGTP_ERR_INVALID_ARG;
     bool has0 = false;
     for (int i = 0; i < n_spins; ++i) {
@@ -718,6 +799,9 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     if ((flags & SPINGTP_KERNEL_VALU) == 0)
         k = spingtp::find_mfma_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
     if (k == nullptr) k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
+    // the large-degree kernels have no parity mixing of their tiles
+    if (k != nullptr && k->family == 3 && spin_mode == 1 && (flags & ~kRouteFlags) == SPINGTP_BASIS_PARITY)
+        k = nullptr;
     const spingtp::KernelEntry* kv1 = nullptr;
     if ((flags & SPINGTP_V1_FOURIER) == 0) {
         kv1 = spingtp::find_pre_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));

@@ -12,6 +12,7 @@ from . import _lib
 
 BASIS_PAPER = 0
 BASIS_M0_PAIRED = 1
+BASIS_PARITY = 2
 KERNEL_VALU = 0x100  # force the fp32 vector-ALU kernels (spingtp.h)
 V1_FOURIER = 0x200  # spingtp_forward_v1 on the Fourier route (spingtp.h)
 V1_PRECONTRACT = 0x400  # spingtp_forward_v1 on the precontracted kernel wherever it is built

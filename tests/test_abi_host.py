@@ -59,6 +59,8 @@ def _spins(s):
     ((2, 2, 2, (-1, 1), 0), 1),         # no spin 0
     ((2, 2, 2, (-2, -1, 0, 1, 2), 0), 2),  # valid, not built
     ((2, 2, 2, (-1, 0, 1), 7), 1),      # unknown basis flag
+    ((2, 2, 2, (-1, 0, 1), 3), 1),      # unknown basis flag
+    ((2, 2, 2, (-1, 0, 1), 2), 0),      # parity-labelled basis
     ((2, 2, 2, (-1, 0, 1), 0), 0),
     ((3, 1, 4, (0,), 1), 0),
 ])
@@ -75,6 +77,24 @@ def test_status_strings(built_library):
         assert len(_lib.message(s)) >= 2
 
 
+def kernel_parity_mix(x, L, inverse):
+    """The kernels' in-LDS mixing of a [rows][3 (L+1)^2] tile for the parity basis:
+    per slot of degree l >= 1, (a, b) of the -1 and +1 blocks become
+    ((a + b)/sqrt2, (-1)^l (a - b)/sqrt2) on load and ((a + (-1)^l b)/sqrt2,
+    (a - (-1)^l b)/sqrt2) before the store."""
+    B = (L + 1) ** 2
+    y = np.array(x, dtype=np.float64, copy=True)
+    h = 1.0 / math.sqrt(2.0)
+    for q in range(1, B):
+        t = -1.0 if int(math.isqrt(q)) % 2 else 1.0
+        a, b = x[:, q], x[:, 2 * B + q]
+        if inverse:
+            y[:, q], y[:, 2 * B + q] = (a + t * b) * h, (a - t * b) * h
+        else:
+            y[:, q], y[:, 2 * B + q] = (a + b) * h, t * (a - b) * h
+    return y
+
+
 def emulate_kernel(x1, x2, L1, L2, LO, spin, basis, backward=False):
     """float64 re-enactment of the forward kernel from the host tables (layout.h);
     with backward=True on the tables of spingtp_backward."""
@@ -88,10 +108,14 @@ def emulate_kernel(x1, x2, L1, L2, LO, spin, basis, backward=False):
     e0s, e1p, e1m, e1z = e0c + triO, e0c + 2 * triO, e0c + 3 * triO, e0c + 4 * triO
     N0 = (tab[0:8].reshape(4, 2), tab[8:16].reshape(4, 2))  # input 1, input 2
     M0 = tab[16:24].reshape(2, 4)
-    COS = tab[24:24 + NP * (TM + 1)].reshape(NP, TM + 1)
-    SIN = tab[24 + NP * (TM + 1):24 + 2 * NP * (TM + 1)].reshape(NP, TM + 1)
+    parity = tab[24] != 0.0
+    COS = tab[28:28 + NP * (TM + 1)].reshape(NP, TM + 1)
+    SIN = tab[28 + NP * (TM + 1):28 + 2 * NP * (TM + 1)].reshape(NP, TM + 1)
     NS = 3 if spin else 1
     U = x1.shape[0]
+    assert parity == (spin and basis == 2)
+    if parity:
+        x1, x2 = kernel_parity_mix(x1, L1, False), kernel_parity_mix(x2, L2, False)
 
     def block(x, L, si):
         return x[:, si * (L + 1) ** 2:(si + 1) * (L + 1) ** 2]
@@ -170,14 +194,15 @@ def emulate_kernel(x1, x2, L1, L2, LO, spin, basis, backward=False):
             for l in range(1, LO + 1):
                 yp[:, l * l + l] += tb[e1z + l] * Z[0]
                 ym[:, l * l + l] += tb[e1z + l] * Z[1]
-    return y
+    return kernel_parity_mix(y, LO, True) if parity else y
 
 
 @pytest.mark.parametrize("L1,L2,LO,spin,basis", [
     (2, 2, 2, True, 0), (2, 2, 2, True, 1), (1, 1, 1, True, 0), (3, 2, 4, True, 0), (2, 3, 1, True, 1),
     (4, 4, 4, True, 0), (6, 6, 6, True, 0), (2, 2, 2, False, 0), (3, 1, 2, False, 0), (0, 0, 0, False, 0),
     (1, 3, 3, True, 0), (8, 8, 8, True, 0), (12, 12, 12, True, 1), (2, 4, 1, True, 0), (4, 1, 2, True, 1),
-    (1, 3, 0, False, 0), (6, 1, 3, True, 0),
+    (1, 3, 0, False, 0), (6, 1, 3, True, 0), (2, 2, 2, True, 2), (3, 2, 4, True, 2), (5, 5, 5, True, 2),
+    (8, 8, 8, True, 2), (2, 3, 1, False, 2),
 ])
 def test_plan_tables_reproduce_oracle(built_library, L1, L2, LO, spin, basis):
     S = (-1, 0, 1) if spin else (0,)
@@ -191,7 +216,8 @@ def test_plan_tables_reproduce_oracle(built_library, L1, L2, LO, spin, basis):
 
 @pytest.mark.parametrize("L1,L2,LO,spins,basis", [
     (2, 2, 2, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 1), (3, 2, 4, (-1, 0, 1), 0), (4, 4, 4, (-1, 0, 1), 1),
-    (3, 1, 2, (0,), 0), (1, 1, 1, (-1, 0, 1), 0),
+    (3, 1, 2, (0,), 0), (1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 2), (3, 2, 4, (-1, 0, 1), 2),
+    (2, 1, 2, (0,), 2),
 ])
 def test_dense_tensor_matches_oracle(built_library, L1, L2, LO, spins, basis):
     """The library's explicit tensor (its own quadrature, the benchmark's comparator) equals the oracle's."""
@@ -247,6 +273,10 @@ def emulate_mfma_kernel(x1, x2, L, basis):
     N0, M0 = tab[0:8].reshape(4, 2), tab[16:24].reshape(2, 4)  # forward tables: input 2 mixing = input 1
     BO = (L + 1) ** 2
     U = x1.shape[0]
+    parity = tab[24] != 0.0
+    assert parity == (basis == 2)
+    if parity:
+        x1, x2 = kernel_parity_mix(x1, L, False), kernel_parity_mix(x2, L, False)
 
     def scale(x):
         valid = valid_mask((-1, 0, 1), L).astype(bool)
@@ -324,10 +354,11 @@ def emulate_mfma_kernel(x1, x2, L, basis):
                     y[:, BO + l * l + l + m3] += tb[e0c + tri(t, l)] * sr
                     y[:, 2 * BO + l * l + l + m3] += tb[e1p + tri(t, l)] * sp
                     y[:, l * l + l + m3] += tb[e1m + tri(t, l)] * sm
-    return y * np.ldexp(1.0, ex1 + ex2)[:, None]
+    y = y * np.ldexp(1.0, ex1 + ex2)[:, None]
+    return kernel_parity_mix(y, L, True) if parity else y
 
 
-@pytest.mark.parametrize("L,basis", [(4, 0), (5, 0), (6, 0), (6, 1), (7, 0)])
+@pytest.mark.parametrize("L,basis", [(4, 0), (5, 0), (6, 0), (6, 1), (7, 0), (5, 2), (6, 2)])
 def test_mfma_operand_tables_reproduce_oracle(built_library, L, basis):
     """The matrix-core kernel's data flow, re-enacted on the CPU with the exact fp16
     operand words the plan uploads, matches the oracle to fp32-like accuracy; a
@@ -385,7 +416,7 @@ def emulate_pre_kernel(words, x1, x2):
     (1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 0), (1, 3, 3, (-1, 0, 1), 0), (3, 1, 2, (-1, 0, 1), 0),
     (4, 4, 4, (-1, 0, 1), 0), (4, 2, 3, (-1, 0, 1), 1), (3, 3, 3, (-1, 0, 1), 1), (7, 7, 7, (0,), 0),
     (5, 2, 6, (0,), 0), (5, 5, 5, (-1, 0, 1), 0), (6, 6, 6, (-1, 0, 1), 1), (1, 6, 6, (-1, 0, 1), 0),
-    (6, 2, 5, (-1, 0, 1), 0)])
+    (6, 2, 5, (-1, 0, 1), 0), (3, 3, 3, (-1, 0, 1), 2), (6, 6, 6, (-1, 0, 1), 2), (2, 4, 3, (-1, 0, 1), 2)])
 def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
     """The precontracted kernel's table, re-enacted on the CPU, gives the oracle's
     edge kernel K[k1, k3] = sum_k2 T x2 and the oracle's outputs for channels that
@@ -458,11 +489,13 @@ def test_plan_create_route_flags(built_library):
     assert built_library.spingtp_plan_create(7, 7, 7, S, 3, 0, 0x400, ctypes.byref(plan)) == 2
     assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x800, ctypes.byref(plan)) == 1  # tables-only bit
     assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x1000, ctypes.byref(plan)) == 1  # unknown bit
+    # parity-labelled basis on the large-degree kernels (no tile mixing there)
+    assert built_library.spingtp_plan_create(9, 9, 9, S, 3, 0, 2, ctypes.byref(plan)) == 2
     assert not plan.value
 
 
 @pytest.mark.parametrize("L", [0, 1, 2, 4, 6, 16])
-@pytest.mark.parametrize("spins,basis", [((-1, 0, 1), 0), ((-1, 0, 1), 1), ((0,), 0)])
+@pytest.mark.parametrize("spins,basis", [((-1, 0, 1), 0), ((-1, 0, 1), 1), ((0,), 0), ((-1, 0, 1), 2)])
 def test_conj_map_matches_oracle(built_library, L, spins, basis):
     """The library's conjugation map (used by spingtp_backward) equals the oracle's J."""
     from oracle.realbasis import conjugation_map
@@ -483,7 +516,7 @@ def test_conj_map_matches_oracle(built_library, L, spins, basis):
 
 
 @pytest.mark.parametrize("L,spin,basis", [(1, True, 0), (2, True, 0), (3, True, 1), (4, True, 0), (6, True, 0),
-                                          (3, False, 0), (8, True, 0)])
+                                          (3, False, 0), (8, True, 0), (2, True, 2), (5, True, 2), (8, True, 2)])
 def test_backward_tables_reproduce_oracle(built_library, L, spin, basis):
     """spingtp_backward runs the forward kernel on (grad_out, x2) with its backward
     tables; re-enacted on the CPU from those tables this is the oracle's grad_x1
@@ -503,7 +536,8 @@ def test_backward_tables_reproduce_oracle(built_library, L, spin, basis):
 
 
 @pytest.mark.parametrize("L,spins,basis", [(1, (-1, 0, 1), 0), (3, (-1, 0, 1), 0), (4, (-1, 0, 1), 1),
-                                           (5, (-1, 0, 1), 0), (6, (-1, 0, 1), 0), (4, (0,), 0)])
+                                           (5, (-1, 0, 1), 0), (6, (-1, 0, 1), 0), (4, (0,), 0),
+                                           (3, (-1, 0, 1), 2), (6, (-1, 0, 1), 2)])
 def test_backward_pre_table_reproduces_oracle(built_library, L, spins, basis):
     """spingtp_backward_v1's grad_x1 on the precontracted kernel: its table (x2
     indices and signs through J), re-enacted on (grad_out, x2), gives the oracle's

@@ -58,7 +58,7 @@ def run_backward(L, spins, N, C, dtype="fp32", basis=0, seed=0):
 
 
 @pytest.mark.parametrize("L", [1, 2, 3, 4, 5, 6])
-@pytest.mark.parametrize("basis", [0, 1])
+@pytest.mark.parametrize("basis", [0, 1, 2])
 def test_backward_matches_oracle(L, basis):
     run_backward(L, S3, 37, 3, "fp32", basis, seed=L + 10 * basis)
 
@@ -67,6 +67,11 @@ def test_backward_matches_oracle(L, basis):
 def test_backward_large_degree(L, N, C):
     # the lane-pair (L = 8) and large-L (L = 12) kernel families
     run_backward(L, S3, N, C, "fp32", 0, seed=L)
+
+
+@pytest.mark.parametrize("L,dtype", [(7, "fp32"), (8, "fp32"), (4, "bf16"), (6, "bf16")])
+def test_backward_parity_basis(L, dtype):
+    run_backward(L, S3, 17, 3, dtype, 2, seed=90 + L)
 
 
 @pytest.mark.parametrize("L", [0, 3, 6])
@@ -191,7 +196,7 @@ def run_backward_v1(L, spins, N, C, dtype="fp32", basis=0, seed=0, fourier=False
 
 
 @pytest.mark.parametrize("L", [1, 2, 3, 4, 5, 6])
-@pytest.mark.parametrize("basis", [0, 1])
+@pytest.mark.parametrize("basis", [0, 1, 2])
 def test_backward_v1_matches_oracle(L, basis):
     # default route: precontracted up to L = 5, Fourier at L = 6
     fam, _ = run_backward_v1(L, S3, 13, 17, "fp32", basis, seed=L + 10 * basis)

@@ -76,14 +76,14 @@ def sample_units(U, n_random, seed):
 
 
 @pytest.mark.parametrize("L", [1, 2, 3, 4, 5, 6, 7, 8])
-@pytest.mark.parametrize("basis", [0, 1])
+@pytest.mark.parametrize("basis", [0, 1, 2])
 def test_ragged_spin_shapes(L, basis):
     # 37 * 3 = 111 units: one full 64-unit tile and a ragged tail of 47
     run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=L)
 
 
 @pytest.mark.parametrize("L", [5, 6])
-@pytest.mark.parametrize("basis", [0, 1])
+@pytest.mark.parametrize("basis", [0, 1, 2])
 def test_ragged_valu_kernels(L, basis):
     # the fp32 vector-ALU kernels of the degrees that default to the matrix-core kernel
     run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=40 + L, valu_only=True)
@@ -116,6 +116,38 @@ def test_mixed_degrees(L1, L2, LO):
 @pytest.mark.parametrize("L", [2, 4, 6, 8])
 def test_bf16_small(L):
     run_and_compare(L, L, L, S3, 45, 6, "bf16", 0, seed=30 + L)
+
+
+# --- the parity-labelled basis (Sec. 3.4): kernels mix their tiles on load and store ---
+
+@pytest.mark.parametrize("L1,L2,LO", [(1, 3, 3), (2, 1, 3)])
+def test_parity_basis_mixed_degrees(L1, L2, LO):
+    run_and_compare(L1, L2, LO, S3, 50, 7, "fp32", 2, seed=60 + L1)
+
+
+@pytest.mark.parametrize("L", [4, 6, 8])
+def test_parity_basis_bf16(L):
+    run_and_compare(L, L, L, S3, 45, 6, "bf16", 2, seed=70 + L)
+
+
+@pytest.mark.parametrize("L", [5, 6])
+def test_parity_basis_matrix_core_many_tiles(L):
+    run_and_compare(L, L, L, S3, 125, 8, "fp32", 2, seed=80 + L)
+
+
+def test_parity_basis_changes_the_map():
+    # the same coefficients read in the two bases give different products (the mixing is applied)
+    x1 = workloads.draw(4, 9, 2, 5, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(4, 9, 2, 6, "fp32", S3, "unit", "cuda")
+    y0 = Plan(4, 4, 4, S3, "fp32", 0).forward(x1, x2)
+    y2 = Plan(4, 4, 4, S3, "fp32", 2).forward(x1, x2)
+    assert float((y0 - y2).abs().max()) > 1e-2
+
+
+def test_parity_basis_large_degree_unsupported():
+    with pytest.raises(SpinGTPError):
+        Plan(9, 9, 9, S3, "fp32", 2)
+    Plan(9, 9, 9, (0,), "fp32", 2)  # no |s| > 0 sector: nothing to mix
 
 
 def test_small_workload_all_units():
@@ -241,23 +273,23 @@ def test_bitwise_deterministic():
 
 # --- edge multiplicity one: x2 shared by the channels of an edge (spingtp_forward_v1) ---
 
-def run_v1(L1, L2, LO, spins, N, C, dtype="fp32", fourier=False, seed=0, precontract=False):
+def run_v1(L1, L2, LO, spins, N, C, dtype="fp32", fourier=False, seed=0, precontract=False, basis=0):
     from oracle.spingtp import _cached_tensor
-    print(f"[parity-v1] L=({L1},{L2},{LO}) N={N} C={C} {dtype} fourier={fourier}", flush=True)
+    print(f"[parity-v1] L=({L1},{L2},{LO}) N={N} C={C} {dtype} fourier={fourier} basis={basis}", flush=True)
     x1 = workloads.draw(L1, N, C, 9000 + seed, dtype, spins, "unit", "cuda")
     x2 = workloads.draw(L2, N, 1, 9500 + seed, dtype, spins, "unit", "cuda")
-    plan = Plan(L1, L2, LO, spins, dtype, 0, v1_fourier=fourier, v1_precontract=precontract)
+    plan = Plan(L1, L2, LO, spins, dtype, basis, v1_fourier=fourier, v1_precontract=precontract)
     fam = plan.kernel_info_v1()["family"]
     y = plan.forward_v1(x1, x2)
     torch.cuda.synchronize()
     U = N * C
     a = x1.view(U, -1).double().cpu().numpy()
     b = np.repeat(x2.view(N, -1).double().cpu().numpy(), C, axis=0)
-    ref = _cached_tensor(L1, L2, LO, tuple(spins), 0).apply(a, b).reshape(U, -1)
+    ref = _cached_tensor(L1, L2, LO, tuple(spins), basis).apply(a, b).reshape(U, -1)
     err = rel_l2(y.view(U, -1).double().cpu().numpy(), ref)
     print(f"[parity-v1]   rel_l2={err:.3e} family={fam}", flush=True)
     assert err <= TOL[dtype], err
-    check_matrix_core(Plan(L1, L2, LO, spins, dtype, 0), dtype, err) if (fourier and fam == 4) else None
+    check_matrix_core(Plan(L1, L2, LO, spins, dtype, basis), dtype, err) if (fourier and fam == 4) else None
     if fam == 5 and dtype == "fp32":
         # fp32 products on the matrix cores and fp32 sums: well inside the fp32 bar
         assert err <= MATRIX_CORE_FP32_TOL, err
@@ -312,6 +344,15 @@ def test_v1_degree_5_and_6(shape, C, fourier):
 def test_v1_default_route(shape, family):
     # precontracted for rows <= 112 and where no Fourier kernel exists, the Fourier route beyond
     assert Plan(*shape, S3, "fp32").kernel_info_v1()["family"] == family
+
+
+@pytest.mark.parametrize("shape,C,fourier,precontract", [
+    ((2, 2, 2), 16, False, False), ((4, 4, 4), 65, False, False), ((5, 5, 5), 130, False, False),
+    ((6, 6, 6), 128, False, True), ((6, 2, 5), 17, False, False), ((6, 6, 6), 40, False, False),
+    ((3, 3, 3), 33, True, False), ((8, 8, 8), 5, False, False)])
+def test_v1_parity_basis(shape, C, fourier, precontract):
+    # the precontracted tables hold the parity-basis tensor itself; the Fourier route mixes tiles
+    run_v1(*shape, S3, 19, C, "fp32", fourier, seed=C, precontract=precontract, basis=2)
 
 
 @pytest.mark.parametrize("shape,C", [((3, 3, 3), 17), ((7, 7, 7), 33), ((5, 2, 6), 16)])
