@@ -27,8 +27,13 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "edge·channel tensor products/sec at L=6 fp32; % HBM/MFMA roofline"
 # sources of the spingtp_forward kernels (families 1-4): a stored traffic record
 # is used only while their hash is unchanged
-KERNEL_SOURCES = ("paper_2607_01408_amd/csrc/forward.hip", "paper_2607_01408_amd/csrc/forward_mfma.hip",
-                  "paper_2607_01408_amd/csrc/device_common.h", "paper_2607_01408_amd/csrc/layout.h")
+_CSRC = "paper_2607_01408_amd/csrc/"
+
+
+def kernel_sources(kname):
+    """The source files a forward kernel is compiled from (its counters go stale when they change)."""
+    main = "forward_mfma.hip" if kname == "spingtp_fwd_mfma_kernel" else "forward.hip"
+    return tuple(_CSRC + f for f in (main, "device_common.h", "layout.h"))
 
 
 def route_flops(L1, L2, LO, spin=True):
@@ -68,9 +73,9 @@ def hbm_bytes_per_unit(L1, L2, LO, dtype, n_spins=3):
     return es * n_spins * ((L1 + 1) ** 2 + (L2 + 1) ** 2 + (LO + 1) ** 2)
 
 
-def kernel_source_hash():
+def kernel_source_hash(kname):
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in kernel_sources(kname):
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -94,7 +99,7 @@ def measured_traffic(workload, dtype, units, L, kname, valu=False, basis="paper"
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_source_hash") != kernel_source_hash() or rec.get("units") != units:
+    if rec.get("kernel_source_hash") != kernel_source_hash(kname) or rec.get("units") != units:
         return None
     if kname + "<" not in rec.get("kernel", ""):
         return None

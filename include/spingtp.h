@@ -97,8 +97,10 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  * Create a plan for degrees (L1, L2, Lout) and a spin set.
  *   0 <= L1, L2 <= 16, 0 <= Lout <= L1 + L2 (the product of degrees l1, l2 has
  *   degree <= l1 + l2, App. B proof); otherwise SPINGTP_ERR_INVALID_ARG.
- *   spins/n_spins: host array, strictly ascending and symmetric; {0} and
- *   {-1, 0, +1} are supported, other valid sets give SPINGTP_ERR_UNSUPPORTED.
+ *   spins/n_spins: host array, strictly ascending and symmetric; {0},
+ *   {-1, 0, +1} and {-2, -1, 0, +1, +2} (s_max = 2) are supported, other valid
+ *   sets give SPINGTP_ERR_UNSUPPORTED.  Spins {-2..2} run on the direct kernel
+ *   (family 6) and, for spingtp_forward_v1, on the precontracted kernel.
  *   dtype: element type of x1, x2 and out.  Arithmetic: the vector-ALU kernels
  *   compute in fp32.  The matrix-core kernel (L1 = L2 = Lout = 5 or 6, and
  *   4 for bf16; spins {-1, 0, +1}) runs the two phi transforms as fp16 matrix products with fp32
@@ -108,10 +110,11 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  *   other step is fp32.  bf16 output is rounded to nearest even.
  *   flags: one SPINGTP_BASIS_* value, optionally OR SPINGTP_KERNEL_VALU and one of
  *   SPINGTP_V1_FOURIER, SPINGTP_V1_PRECONTRACT.
- * A shape that only the precontracted kernel of spingtp_forward_v1 covers (any
- * L1, L2, Lout up to 6 with spins {-1, 0, +1}, up to 7 with spin {0}) gives a
- * plan for that entry point;
- * spingtp_forward and spingtp_plan_kernel_info then return
+ * A shape with no Fourier kernel (families 1-4) runs spingtp_forward on the
+ * direct kernel (family 6) where its LDS tile fits (64 n_spins ((L1+1)^2 +
+ * (L2+1)^2 + (Lout+1)^2) floats plus padding within 160 KB); a shape that only
+ * the precontracted kernel of spingtp_forward_v1 covers gives a plan for that
+ * entry point, and spingtp_forward and spingtp_plan_kernel_info then return
  * SPINGTP_ERR_UNSUPPORTED.
  * The plan tables (Gauss-Legendre weights and SWSH values on the quadrature
  * nodes, trigonometric tables, real-basis mixing constants) are computed in
@@ -171,9 +174,12 @@ spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void*
  * SPINGTP_BASIS_REAL_PAPER they swap between s = +1 and -1 with a sign change; J is
  * the identity for SPINGTP_BASIS_REAL_M0_PAIRED and spins {0}; with
  * SPINGTP_BASIS_PARITY the kernel mixes its tiles into the paper basis first, where
- * that J applies, since P^T J P x = P^T J (P x)).  Built for plans
- * with L1 = L2 = Lout that have a spingtp_forward kernel; otherwise
- * SPINGTP_ERR_UNSUPPORTED.
+ * that J applies, since P^T J P x = P^T J (P x)).  That route serves plans with
+ * L1 = L2 = Lout and a Fourier spingtp_forward kernel.  Other plans whose tile
+ * fits the direct kernel (family 6: spins {-2..2}, shapes without a Fourier
+ * kernel, mixed degrees) run the two gradients on it, from tables listing the
+ * nonzeros of T by k1 and by k2 (spingtp_direct_table_host roles 1 and 2; no J).
+ * Otherwise SPINGTP_ERR_UNSUPPORTED.
  *   x1, x2, grad_out: as x1, x2, out of spingtp_forward; grad_x1, grad_x2: same
  *   shapes as x1, x2 (either may be NULL: not computed), overwritten; slots with
  *   l < |s| are written 0.  Same dtype, 16-byte alignment and error rules as
@@ -195,8 +201,10 @@ spingtp_status spingtp_backward(spingtp_plan plan, const void* x1, const void* x
  * SpinGTP(grad_out[n][c], J x1[n][c]) of the plan's spingtp_forward kernel go to
  * `workspace` ([N][C][n_spins (L2+1)^2], the plan's dtype), then a second kernel
  * sums them over c in order (fp32 sums; bf16 output rounded to nearest even).
- * Built for plans with L1 = L2 = Lout that have a spingtp_forward kernel;
- * otherwise SPINGTP_ERR_UNSUPPORTED.
+ * On plans whose gradients run on the direct kernel (see spingtp_backward), both
+ * steps use its role tables instead (grad_x1 with x2 read once per edge), except
+ * that grad_x1 stays on the precontracted kernel where the plan has its
+ * conjugated table.  Plans with neither: SPINGTP_ERR_UNSUPPORTED.
  *   x1 [N][C][...], x2 [N][...], grad_out [N][C][...]; grad_x1 [N][C][...] and
  *   grad_x2 [N][n_spins (L2+1)^2] (either may be NULL: not computed), overwritten;
  *   slots with l < |s| are written 0.  C = 0 writes grad_x2 = 0.
@@ -308,13 +316,39 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
                                       uint32_t* words, size_t capacity, size_t* count);
 
 /*
+ * Host-only inspection of the entry table of the direct kernel (family 6) for one
+ * role of the tensor T[k1][k2][k3] of spingtp_dense_tensor_host, exactly as
+ * spingtp_plan_create uploads it.  Needs no GPU.  Same argument rules as
+ * spingtp_plan_create; role 0 = forward (out[k3] from A = x1 at a = k1, B = x2
+ * at b = k2), 1 = gradient w.r.t. x1 (out[k1] from A = grad_out at a = k3,
+ * B = x2 at b = k2), 2 = gradient w.r.t. x2 (out[k2] from A = grad_out at
+ * a = k3, B = x1 at b = k1); another role gives SPINGTP_ERR_INVALID_ARG, a
+ * shape whose tile does not fit the kernel's LDS SPINGTP_ERR_UNSUPPORTED.
+ * Word layout:
+ *   [0, 8)         NCA, NCB, NCO (widths of A, B, out), STA, STB, STO (odd LDS
+ *                  row strides, each above its width: column NCA of A and NCB
+ *                  of B hold 0), NBATCH, 0;
+ *   [8, 8 + NCO)   batches of 8 entries per output slot, in output order;
+ *   then NBATCH batches of 16 words: 8 entry words a | b << 16, then their 8
+ *   fp32 values (bits), and 16 zero words.  out[o] = sum over the entries of slot o of
+ *   value * A[a] * B[b]; entries are the nonzeros of T in ascending (a, b) order,
+ *   padded with (NCA, NCB, 0) entries.
+ * Writes min(capacity, total) words to `words` (may be NULL when capacity is 0)
+ * and the total to *count.
+ */
+spingtp_status spingtp_direct_table_host(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
+                                         int role, uint32_t* words, size_t capacity, size_t* count);
+
+/*
  * Describe the kernel a plan launches: writes the waves per workgroup, units per
  * workgroup, LDS bytes per workgroup and a kernel-family id to the 4 ints of
  * `info`.  Families: 1 = one lane per unit, one wave per quadrature node (L <= 6
  * and the mixed-degree shapes); 2 = lane pairs per unit (L = 7, 8); 3 = lane
  * pairs with the nodes processed in rounds (L = 9..16, fp32 only); 4 = the
  * matrix-core kernel (L1 = L2 = Lout = 5, 6, and 4 for bf16; spins {-1, 0, +1};
- * the default there unless SPINGTP_KERNEL_VALU is given).
+ * the default there unless SPINGTP_KERNEL_VALU is given); 6 = the direct
+ * sparse-tensor kernel (one wave per 64 units; shapes without a Fourier kernel,
+ * spins {-2..2}).
  */
 spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info);
 

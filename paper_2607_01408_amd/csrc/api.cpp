@@ -22,10 +22,16 @@ spingtp_status spingtp::run_forward(spingtp_plan plan, const spingtp::KernelEntr
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
     if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
-    const uint32_t* aux = aux_override != nullptr ? aux_override : (k->family == 5 ? plan->d_pre : plan->d_aux);
+    const uint32_t* aux =
+        aux_override != nullptr ? aux_override
+                                : (k->family == 5 ? plan->d_pre : (k->family == 6 ? plan->d_dir : plan->d_aux));
     const hipError_t e =
-        (bwd_launch ? k->launch_bwd : k->launch)(x1, x2, out, N * C, shared_x2 ? C : 1, tab != nullptr ? tab : plan->d_tab, aux,
-                  static_cast<hipStream_t>(stream));
+        k->launch_lds != nullptr
+            ? k->launch_lds(x1, x2, out, N * C, shared_x2 ? C : 1, aux, plan->dir_lds_floats,
+                            static_cast<hipStream_t>(stream))
+            : (bwd_launch ? k->launch_bwd : k->launch)(x1, x2, out, N * C, shared_x2 ? C : 1,
+                                                       tab != nullptr ? tab : plan->d_tab, aux,
+                                                       static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
 }
 

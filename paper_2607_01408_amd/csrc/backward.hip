@@ -10,8 +10,11 @@
 // both are launches of the plan's own forward kernel (the instantiation whose
 // input-2 lanes read the second copy of the m = 0 mixing of the |s| = 1 sectors)
 // on the plan's backward tables, where that copy absorbs J (J moves no other
-// slots); no copy of J x is made.  The shared-x2 form (spingtp_backward_v1) is
-// at the end of the file.
+// slots); no copy of J x is made.  Plans on the direct sparse-tensor kernel, and
+// non-square plans whose transposed degrees have no Fourier kernel, run the two
+// gradients as that kernel on the tensor's other two roles (entries of T listed
+// by k1 and by k2), which needs no conjugation.  The shared-x2 form
+// (spingtp_backward_v1) is at the end of the file.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -29,10 +32,21 @@ bool misaligned(const void* p) {
 extern "C" spingtp_status spingtp_backward(spingtp_plan plan, const void* x1, const void* x2, const void* grad_out,
                                            void* grad_x1, void* grad_x2, int64_t N, int64_t C, void* stream) {
     if (plan == nullptr || N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
-    if (plan->d_tab_bwd == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    if (plan->d_tab_bwd == nullptr && plan->d_dir_b1 == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     if (N == 0 || C == 0 || (grad_x1 == nullptr && grad_x2 == nullptr)) return SPINGTP_OK;
     if (misaligned(grad_x1) || misaligned(grad_x2)) return SPINGTP_ERR_INVALID_ARG;
     // run_forward checks the rest (sizes, pointers, alignment, device)
+    if (plan->d_tab_bwd == nullptr) {  // the direct kernel on the gradient roles of T
+        if (grad_x1 != nullptr) {
+            const spingtp_status r = spingtp::run_forward(plan, plan->kernel_dir, grad_out, x2, grad_x1, N, C, false,
+                                                          stream, nullptr, false, plan->d_dir_b1);
+            if (r != SPINGTP_OK) return r;
+        }
+        if (grad_x2 != nullptr)
+            return spingtp::run_forward(plan, plan->kernel_dir, grad_out, x1, grad_x2, N, C, false, stream, nullptr,
+                                        false, plan->d_dir_b2);
+        return SPINGTP_OK;
+    }
     if (grad_x1 != nullptr) {
         const spingtp_status r =
             spingtp::run_forward(plan, plan->kernel, grad_out, x2, grad_x1, N, C, false, stream, plan->d_tab_bwd,
@@ -121,7 +135,8 @@ int64_t row_length(const spingtp_plan_s* p) {
 extern "C" spingtp_status spingtp_backward_v1_workspace_size(spingtp_plan plan, int64_t N, int64_t C,
                                                              size_t* bytes) {
     if (plan == nullptr || bytes == nullptr || N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
-    if (plan->d_tab_bwd == nullptr || plan->kernel == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    if ((plan->d_tab_bwd == nullptr || plan->kernel == nullptr) && plan->d_dir_b1 == nullptr)
+        return SPINGTP_ERR_UNSUPPORTED;
     if (N > 0 && C > 0 && N > (int64_t{1} << 40) / C) return SPINGTP_ERR_INVALID_ARG;
     const size_t elem = plan->dtype == SPINGTP_FP32 ? 4 : 2;
     *bytes = static_cast<size_t>(N) * static_cast<size_t>(C) * static_cast<size_t>(row_length(plan)) * elem;
@@ -150,19 +165,28 @@ extern "C" spingtp_status spingtp_backward_v1(spingtp_plan plan, const void* x1,
     if (grad_x1 != nullptr) {
         const spingtp::KernelEntry* k = plan->kernel_v1;
         spingtp_status r;
-        if (k != nullptr && k->family == 5) {
-            if (plan->d_pre_bwd == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+        if (k != nullptr && k->family == 5 && plan->d_pre_bwd != nullptr) {
             r = spingtp::run_forward(plan, k, grad_out, x2, grad_x1, N, C, true, stream, nullptr, true,
                                      plan->d_pre_bwd);
+        } else if (plan->d_tab_bwd != nullptr) {  // the Fourier kernel, x2 read once per edge
+            const spingtp::KernelEntry* kf = (k != nullptr && k->family != 5) ? k : plan->kernel;
+            r = spingtp::run_forward(plan, kf, grad_out, x2, grad_x1, N, C, true, stream, plan->d_tab_bwd, true);
+        } else if (plan->d_dir_b1 != nullptr) {  // the direct kernel, x2 shared by the channels
+            r = spingtp::run_forward(plan, plan->kernel_dir, grad_out, x2, grad_x1, N, C, true, stream, nullptr,
+                                     false, plan->d_dir_b1);
         } else {
-            r = spingtp::run_forward(plan, k, grad_out, x2, grad_x1, N, C, true, stream, plan->d_tab_bwd, true);
+            return SPINGTP_ERR_UNSUPPORTED;
         }
         if (r != SPINGTP_OK) return r;
     }
     if (grad_x2 != nullptr) {
         if (workspace == nullptr || misaligned(workspace) || workspace_bytes < need) return SPINGTP_ERR_INVALID_ARG;
-        const spingtp_status r = spingtp::run_forward(plan, plan->kernel, grad_out, x1, workspace, N, C, false,
-                                                      stream, plan->d_tab_bwd, true);
+        const spingtp_status r =
+            plan->d_tab_bwd != nullptr
+                ? spingtp::run_forward(plan, plan->kernel, grad_out, x1, workspace, N, C, false, stream,
+                                       plan->d_tab_bwd, true)
+                : spingtp::run_forward(plan, plan->kernel_dir, grad_out, x1, workspace, N, C, false, stream,
+                                       nullptr, false, plan->d_dir_b2);
         if (r != SPINGTP_OK) return r;
         if (launch_sum_channels(workspace, grad_x2, N, C, static_cast<int>(row_length(plan)), plan->dtype, s) !=
             hipSuccess)

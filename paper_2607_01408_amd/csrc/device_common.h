@@ -215,9 +215,9 @@ __device__ void parity_mix_rows(float* tile, int st, int rows, bool inverse, int
     const float h = 0.70710678118654752440f;
     for (int i = tid; i < rows * NQ; i += nthr) {
         const int r = i / NQ, q = i - r * NQ + 1;
-        int l = static_cast<int>(sqrtf(static_cast<float>(q)));
-        if ((l + 1) * (l + 1) <= q) ++l;
-        if (l * l > q) --l;
+        int l = 0;  // degree of slot q: the number of k >= 1 with k^2 <= q
+#pragma unroll
+        for (int k = 1; k <= L; ++k) l += q >= k * k ? 1 : 0;
         const float t = (l & 1) ? -1.f : 1.f;
         float* row = tile + static_cast<int64_t>(r) * st;
         const float a = row[q], b = row[2 * B + q];

@@ -296,11 +296,6 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
     }
     __syncthreads();
     const bool parity = tab[Y.par] != 0.f;  // uniform
-    if (parity) {
-        parity_mix_rows<L>(lds, ST, nvalid, false, tid, S::THREADS);
-        parity_mix_rows<L>(lds + S::X2, ST, nvalid, false, tid, S::THREADS);
-        __syncthreads();
-    }
 
     // (2) per unit and input: scale the row by 2^-e so that its largest valid
     //     magnitude is in [1/2, 1).  Two threads per row; the l = 0 slots of the
@@ -316,6 +311,26 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
         for (int i = 0; i < HALF; ++i) {
             const bool last = i + HALF >= NC;  // past the row end in the second half
             v[i] = (last && odd) ? 0.f : xr[i];
+        }
+        if (parity) {
+            // parity-labelled basis: slot q of the s = -1 block (first half, v[q]) and
+            // of the s = +1 block (second half, v[2 BLK + q - HALF]) become
+            // ((a + b)/sqrt2, (-1)^l (a - b)/sqrt2), a = x[q], b = x[2 BLK + q]
+#pragma unroll
+            for (int l = 1; l <= L; ++l)
+#pragma unroll
+                for (int q = l * l; q < (l + 1) * (l + 1); ++q) {
+                    const float mine = odd ? v[2 * BLK + q - HALF] : v[q];
+                    const float other = swap_adjacent(mine);
+                    const float a = odd ? other : mine, b = odd ? mine : other;
+                    if (odd)
+                        v[2 * BLK + q - HALF] = ((l & 1) ? (b - a) : (a - b)) * 0.70710678118654752440f;
+                    else
+                        v[q] = (a + b) * 0.70710678118654752440f;
+                }
+        }
+#pragma unroll
+        for (int i = 0; i < HALF; ++i) {
             bool skip = false;  // l = 0 slots of the s = -1 (index 0) and s = +1 (index 2 BLK) blocks
             if (i == 0) skip = !odd;
             if (i == 2 * BLK) skip = skip || !odd;
@@ -483,6 +498,27 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
     const int unit = 32 * T + (lane & 31);
     const int es = ex[unit] + ex[64 + unit];
     float* yr = lds + (wave >> 1) * S::YB + unit * ST;
+    if (parity) {
+        // back to the parity-labelled basis (P^T, linear, so on the partial tiles):
+        // (a, b) of the s = -1, +1 blocks become ((a + (-1)^l b)/sqrt2, (a - (-1)^l b)/sqrt2).
+        // At m = +-t both sit in this lane (oM, oP); at m = 0 lane h = 1 holds a and
+        // lane h = 0 holds b of the same unit, 32 lanes apart.
+        const float hs = 0.70710678118654752440f;
+#pragma unroll
+        for (int t = 1; t <= L; ++t)
+#pragma unroll
+            for (int l = t; l <= L; ++l) {
+                const float a = oM[t][l], b = (l & 1) ? -oP[t][l] : oP[t][l];
+                oM[t][l] = (a + b) * hs;
+                oP[t][l] = (a - b) * hs;
+            }
+#pragma unroll
+        for (int l = 1; l <= L; ++l) {
+            const float other = __shfl_xor(oZ[l], 32);
+            const float a = h ? oZ[l] : other, b = (l & 1) ? -(h ? other : oZ[l]) : (h ? other : oZ[l]);
+            oZ[l] = (h ? (a + b) : (a - b)) * hs;
+        }
+    }
     if (h == 0) {
         yr[0] = 0.f;        // l = 0 of s = -1
         yr[2 * BLK] = 0.f;  // l = 0 of s = +1
@@ -504,11 +540,6 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
             yr[l * l + l + sm * t] = ldexpf(oM[t][l], es);
         }
     __syncthreads();
-    if (parity) {  // each partial tile to the parity basis (the map is linear)
-        parity_mix_rows<L>(lds, ST, nvalid, true, tid, S::THREADS);
-        parity_mix_rows<L>(lds + S::YB, ST, nvalid, true, tid, S::THREADS);
-        __syncthreads();
-    }
     store_out<NC, ST, S::UNITS, S::THREADS>(out + u0 * NC, nvalid, lds, S::YB, tid);
 }
 

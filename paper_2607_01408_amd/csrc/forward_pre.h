@@ -27,9 +27,9 @@
 //     with one 16-byte LDS load and its four x1 values from one 16-byte run of its
 //     channel's row; the accumulator of a lane then holds four consecutive k3 of one
 //     channel.
-// The l = 0 slots of the |s| = 1 sectors are not data: x1 values there are never
-// read (taken as 0), and T has no entries for them, so those outputs are written
-// as 0 and x2 values there are never used.
+// The slots with l < |s| are not data: x1 values there are never read (taken as
+// 0), and T has no entries for them, so those outputs are written as 0 and x2
+// values there are never used.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -61,6 +61,24 @@ __device__ __forceinline__ void wave_lds_order() {
     __builtin_amdgcn_wave_barrier();
 }
 
+// Bit 4 s + j is set when x1 slot k1 = 16 s + 4 g + j (MFMA step (s, j) of lane
+// group g) is data: k1 < nc1 and, in its spin block of blk1 slots (spins -S..S in
+// order, so |s| = |b - ns / 2| for block b), degree l >= |s|, i.e. in-block index
+// l^2 + l + m >= s^2.
+template <int KS>
+__device__ __forceinline__ uint64_t x1_data_mask(int nc1, int blk1, int ns, int g) {
+    uint64_t m = 0;
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int k1 = 16 * s + 4 * g + j;
+            const int b = k1 / blk1, r = k1 - b * blk1, sa = b > ns / 2 ? b - ns / 2 : ns / 2 - b;
+            if (k1 < nc1 && r >= sa * sa) m |= uint64_t{1} << (4 * s + j);
+        }
+    return m;
+}
+
 // KS = ceil(NC1 / 16) contraction blocks, NT = ceil(NCO / 16) output strips.
 // Workgroups are persistent: workgroup b takes edges b, b + grid, ...; while an
 // edge's product runs, the next edge's x2 row and each wave's first x1 tile of
@@ -82,8 +100,9 @@ __global__ __launch_bounds__(kPreThreads) void spingtp_fwd_pre_kernel(const TIO*
     __shared__ float X2[kPreMaxNC];
 
     const int NC1 = static_cast<int>(aux[0]), NC2 = static_cast<int>(aux[1]), NCO = static_cast<int>(aux[2]);
-    const int blk1 = static_cast<int>(aux[3]), ipt = static_cast<int>(aux[6]);
+    const int blk1 = static_cast<int>(aux[3]), ipt = static_cast<int>(aux[6]), ns = static_cast<int>(aux[11]);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 15, g = lane >> 4;
+    const uint64_t vmask = x1_data_mask<KS>(NC1, blk1, ns, g);
     const int64_t tiles = (C + 15) / 16;
     const int64_t stride = gridDim.x;
     float* __restrict__ st = Stage + wave * 16 * RS;
@@ -172,9 +191,7 @@ __global__ __launch_bounds__(kPreThreads) void spingtp_fwd_pre_kernel(const TIO*
                 const v4f v = *reinterpret_cast<const v4f*>(&st[col * RS + 16 * s + 4 * g]);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    const int k1 = 16 * s + 4 * g + j;
-                    const bool ok = k1 < NC1 && !(blk1 > 0 && (k1 == 0 || k1 == 2 * blk1));
-                    b[s][j] = ok ? v[j] : 0.f;
+                    b[s][j] = ((vmask >> (4 * s + j)) & 1u) ? v[j] : 0.f;
                 }
             }
             if (m + NW < tiles)
@@ -254,7 +271,9 @@ __global__ __launch_bounds__(kPreThreads, 2) void spingtp_fwd_pre_blocked_kernel
 
     const int NC1 = static_cast<int>(aux[0]), NC2 = static_cast<int>(aux[1]), NCO = static_cast<int>(aux[2]);
     const int blk1 = static_cast<int>(aux[3]), ipt = static_cast<int>(aux[6]), stride = static_cast<int>(aux[10]);
+    const int ns = static_cast<int>(aux[11]);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 15, g = lane >> 4;
+    const uint64_t vmask = x1_data_mask<KS>(NC1, blk1, ns, g);
     const int64_t tiles = (C + 15) / 16;
     float* __restrict__ st = Stage + wave * STG;
     const uint2* __restrict__ items0 = reinterpret_cast<const uint2*>(aux + kPreHeader) + tid;
@@ -296,9 +315,7 @@ __global__ __launch_bounds__(kPreThreads, 2) void spingtp_fwd_pre_blocked_kernel
                         const v4f v = *reinterpret_cast<const v4f*>(&st[col * RS + 16 * s + 4 * g]);
 #pragma unroll
                         for (int j = 0; j < 4; ++j) {
-                            const int k1 = 16 * s + 4 * g + j;
-                            const bool ok = k1 < NC1 && !(blk1 > 0 && (k1 == 0 || k1 == 2 * blk1));
-                            b[i][s][j] = ok ? v[j] : 0.f;
+                            b[i][s][j] = ((vmask >> (4 * s + j)) & 1u) ? v[j] : 0.f;
                         }
                     }
                     wave_lds_order();

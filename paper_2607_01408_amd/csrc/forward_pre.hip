@@ -16,8 +16,7 @@ const KernelEntry kPreSmall[5][5][2] = {SPINGTP_PRE_ROW(1), SPINGTP_PRE_ROW(2), 
 
 }  // namespace
 
-const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int spin_mode, int dtype) {
-    const int ns = spin_mode ? 3 : 1;
+const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int ns, int dtype) {
     const int nc1 = ns * (L1 + 1) * (L1 + 1), nc2 = ns * (L2 + 1) * (L2 + 1), nco = ns * (LO + 1) * (LO + 1);
     if (nc1 > kPreMaxNC || nc2 > kPreMaxNC || nco > kPreMaxNC || dtype < 0 || dtype > 1) return nullptr;
     const int ks = (nc1 + 15) / 16, nt = (nco + 15) / 16;

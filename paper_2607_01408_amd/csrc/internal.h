@@ -27,12 +27,16 @@ struct KernelEntry {
     // copy of the m = 0 mixing (layout.h n0b); nullptr where there is none
     hipError_t (*launch_bwd)(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2,
                              const float* tab, const uint32_t* aux, hipStream_t stream);
+    // the direct kernel (family 6) instead of `launch`: its LDS size comes with the
+    // call (the plan's, from its entry table); nullptr for the other families
+    hipError_t (*launch_lds)(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2,
+                             const uint32_t* aux, int lds_floats, hipStream_t stream);
 };
 
 // Largest row length (n_spins (L+1)^2) of the precontracted kernel: L <= 6 with
 // spins {-1, 0, +1}.  Its instantiations cover KS = ceil(NC1/16) and
-// NT = ceil(NCO/16) in {1, 2, 3, 4, 5, 7, 10}: L <= 6 with spins {-1, 0, +1},
-// L <= 7 with spin {0}.
+// NT = ceil(NCO/16) in {1, 2, 3, 4, 5, 7, 10}, and 8 paired with {1, 2, 3, 5, 8}:
+// L <= 6 with spins {-1, 0, +1}, L <= 7 with spin {0}, L <= 4 with spins {-2..2}.
 constexpr int kPreMaxNC = 147;
 // Threads per workgroup of the precontracted kernel (its tensor items are laid out
 // for exactly this many threads) and the words of its table header.
@@ -41,13 +45,28 @@ constexpr int kPreHeader = 12;
 // k3 rows per kernel block of the large instantiations (KS or NT above 5)
 constexpr int kPreBlockRows = 48;
 
+// Direct sparse-tensor kernel (family 6, forward_direct.hip): units per workgroup
+// (one wave) and the largest LDS tile it takes (160 KB).
+constexpr int kDirectUnits = 64;
+constexpr int kDirectMaxLdsFloats = 40960;
+// The direct kernel for an LDS tile of `lds_floats`; nullptr if it does not fit.
+const KernelEntry* find_direct_kernel(int lds_floats, int dtype);
+// Entry table of the direct kernel for one role of the tensor T[k1][k2][k3]:
+// role 0 (forward) A = x1, B = x2, output k3; role 1 (grad x1) A = grad_out,
+// B = x2, output k1; role 2 (grad x2) A = grad_out, B = x1, output k2.  Layout in
+// forward_direct.hip; entries per output in ascending (a, b) order, padded to
+// batches of 8 with zero entries on the zero column past each row.  *lds_floats:
+// the LDS the kernel needs for it.
+void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags, int role,
+                        std::vector<uint32_t>& out, int* lds_floats);
+
 // Finds the instantiation for (L1, L2, Lout, spin mode, dtype); nullptr if none.
 // find_kernel returns the vector-ALU kernels, find_mfma_kernel the matrix-core
 // kernel where one is built.
 const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
 const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
 // The precontracted kernel of spingtp_forward_v1 (x2 shared by the channels of an edge).
-const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
+const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int n_spins, int dtype);
 // The instantiations with KS or NT in {7, 10} (forward_pre_large.hip); nullptr if none.
 const KernelEntry* find_pre_kernel_large(int ks, int nt, int dtype);
 
@@ -119,6 +138,11 @@ struct spingtp_plan_s {
     uint32_t* d_pre_bwd;  // the same with J x2 (spingtp_backward_v1), nullptr if not used
     float* d_tab_bwd;  // tables of spingtp_backward (d_tab when equal), nullptr without a backward
     bool own_tab_bwd;  // d_tab_bwd is a separate allocation
+    uint32_t* d_dir;     // direct-kernel entry table of the forward (family 6), nullptr if not used
+    uint32_t* d_dir_b1;  // direct-kernel tables of the gradients w.r.t. x1 and x2, nullptr unless
+    uint32_t* d_dir_b2;  //   the gradients run on the direct kernel
+    const spingtp::KernelEntry* kernel_dir;  // the direct kernel of d_dir_b1 and d_dir_b2
+    int dir_lds_floats;  // LDS of the direct kernel's tiles (the same for its three tables)
     const spingtp::KernelEntry* kernel;     // spingtp_forward
     const spingtp::KernelEntry* kernel_v1;  // spingtp_forward_v1 (x2 shared by the channels of an edge)
 };

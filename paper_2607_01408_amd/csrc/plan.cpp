@@ -98,13 +98,15 @@ void gauss_legendre(int n, std::vector<double>& x, std::vector<double>& w) {
 struct Cplx {
     double re, im;
 };
+// s: the sign of the row's spin (+|sigma| or -|sigma|).
 Cplx q_m0(unsigned flags, int s, int sigma) {
     const double h = 1.0 / kSqrt2;
-    if (flags == SPINGTP_BASIS_REAL_PAPER) return (s == sigma) ? Cplx{1.0, 0.0} : Cplx{0.0, 0.0};
-    // paired, |s| = 1: column (+1,0) -> (h, -h) on rows (+1,0), (-1,0);
-    //                   column (-1,0) -> (i h, i h)
-    if (sigma > 0) return (s > 0) ? Cplx{h, 0.0} : Cplx{-h, 0.0};
-    return Cplx{0.0, h};
+    if (flags == SPINGTP_BASIS_REAL_PAPER) return ((s > 0) == (sigma > 0)) ? Cplx{1.0, 0.0} : Cplx{0.0, 0.0};
+    // paired: column (+|s|,0) -> (h, (-1)^s h) on rows (+|s|,0), (-|s|,0);
+    //         column (-|s|,0) -> (i h, -i (-1)^s h)
+    const double sg = (std::abs(sigma) % 2) ? -1.0 : 1.0;
+    if (sigma > 0) return (s > 0) ? Cplx{h, 0.0} : Cplx{sg * h, 0.0};
+    return (s > 0) ? Cplx{0.0, h} : Cplx{0.0, -sg * h};
 }
 
 // Complex expansion of the real basis column (sigma, l, k) (eq. real_swsh, App. C):
@@ -249,6 +251,7 @@ bool build_conj_map(int L, const int* spins, int n_spins, unsigned flags, std::v
 
 bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::vector<double>& out,
                   bool conj_input2) {
+    if (spin_mode > 1) return false;  // the Fourier kernels cover spins {0} and {-1, 0, +1}
     const Layout Y = make_layout(L1, L2, LO);
     out.assign(Y.total, 0.0);
     // a parity plan runs the paper basis's tables on tiles mixed by P (inputs) and
@@ -516,7 +519,7 @@ bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
     out[0] = static_cast<uint32_t>(nc1);
     out[1] = static_cast<uint32_t>(nc2);
     out[2] = static_cast<uint32_t>(nco);
-    out[3] = static_cast<uint32_t>(n_spins == 3 ? (L1 + 1) * (L1 + 1) : 0);
+    out[3] = static_cast<uint32_t>((L1 + 1) * (L1 + 1));
     out[4] = static_cast<uint32_t>(ks);
     out[5] = static_cast<uint32_t>(nt);
     out[6] = static_cast<uint32_t>(ipt);
@@ -524,6 +527,7 @@ bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
     out[8] = static_cast<uint32_t>(nb3);
     out[9] = static_cast<uint32_t>(rb);
     out[10] = static_cast<uint32_t>(stride);
+    out[11] = static_cast<uint32_t>(n_spins);
     for (int b = 0; b < nb3; ++b) {
         uint32_t* items = out.data() + kPreHeader + 2 * static_cast<size_t>(b) * stride * kPreThreads;
         for (int t = 0; t < kPreThreads; ++t) {
@@ -632,6 +636,57 @@ void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, u
             }
 }
 
+void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags, int role,
+                        std::vector<uint32_t>& out, int* lds_floats) {
+    std::vector<double> T;
+    build_dense_tensor(L1, L2, LO, spins, n_spins, flags, T);
+    const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
+    const int nco = n_spins * (LO + 1) * (LO + 1);
+    // (A, B, output) widths of the role and the index map from (a, b, o) to T
+    const int na = role == 0 ? nc1 : nco, nb = role == 2 ? nc1 : nc2, no = role == 0 ? nco : (role == 1 ? nc1 : nc2);
+    auto at = [&](int a, int b, int o) -> double {
+        int k1 = a, k2 = b, k3 = o;  // role 0
+        if (role == 1) k1 = o, k2 = b, k3 = a;
+        if (role == 2) k1 = b, k2 = o, k3 = a;
+        return T[(static_cast<size_t>(k1) * nc2 + k2) * nco + k3];
+    };
+    auto odd_stride = [](int n) { return (n % 2) ? n + 2 : n + 1; };  // odd, with a zero column at n
+    const int sta = odd_stride(na), stb = odd_stride(nb), sto = odd_stride(no);
+    out.assign(8 + no, 0u);
+    out[0] = static_cast<uint32_t>(na);
+    out[1] = static_cast<uint32_t>(nb);
+    out[2] = static_cast<uint32_t>(no);
+    out[3] = static_cast<uint32_t>(sta);
+    out[4] = static_cast<uint32_t>(stb);
+    out[5] = static_cast<uint32_t>(sto);
+    uint32_t nbatch = 0;
+    for (int o = 0; o < no; ++o) {
+        std::vector<std::pair<uint32_t, float>> ent;
+        for (int a = 0; a < na; ++a)
+            for (int b = 0; b < nb; ++b) {
+                const double v = at(a, b, o);
+                if (std::fabs(v) > 1e-12)  // the rest is quadrature round-off of exact zeros
+                    ent.emplace_back(static_cast<uint32_t>(a) | (static_cast<uint32_t>(b) << 16),
+                                     static_cast<float>(v));
+            }
+        while (ent.size() % 8) ent.emplace_back(static_cast<uint32_t>(na) | (static_cast<uint32_t>(nb) << 16), 0.f);
+        const size_t batches = ent.size() / 8;
+        out[8 + o] = static_cast<uint32_t>(batches);
+        nbatch += static_cast<uint32_t>(batches);
+        for (size_t q = 0; q < batches; ++q) {
+            for (int i = 0; i < 8; ++i) out.push_back(ent[q * 8 + i].first);
+            for (int i = 0; i < 8; ++i) {
+                uint32_t bits;
+                std::memcpy(&bits, &ent[q * 8 + i].second, 4);
+                out.push_back(bits);
+            }
+        }
+    }
+    out[6] = nbatch;
+    out.insert(out.end(), 16, 0u);  // a zero batch that the kernel's look-ahead load reads last
+    *lds_floats = kDirectUnits * (sta + stb + sto);
+}
+
 }  // namespace spingtp
 
 namespace {
@@ -660,6 +715,8 @@ spingtp_status check_args(int L1, int L2, int Lout, const int* spins, int n_spin
         *spin_mode = 0;
     } else if (n_spins == 3 && spins[0] == -1 && spins[2] == 1) {
         *spin_mode = 1;
+    } else if (n_spins == 5 && spins[0] == -2 && spins[1] == -1 && spins[3] == 1 && spins[4] == 2) {
+        *spin_mode = 2;  // s_max = 2: the direct and precontracted kernels only
     } else {
         return SPINGTP_ERR_UNSUPPORTED;
     }
@@ -693,6 +750,7 @@ spingtp_status spingtp_plan_tables_host(int L1, int L2, int Lout, const int* spi
     if (n_tables == nullptr || (capacity > 0 && tables == nullptr)) return SPINGTP_ERR_INVALID_ARG;
     std::vector<double> tab;
     try {
+        if (spin_mode > 1) return SPINGTP_ERR_UNSUPPORTED;
         if (!spingtp::build_tables(L1, L2, Lout, spin_mode, flags & ~kRouteFlags, tab, backward))
             return backward ? SPINGTP_ERR_UNSUPPORTED : SPINGTP_ERR_INTERNAL;
     } catch (const std::bad_alloc&) {
@@ -755,11 +813,31 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
     int spin_mode = 0;
     const spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
-    if (spingtp::find_pre_kernel(L1, L2, Lout, spin_mode, 0) == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    if (spingtp::find_pre_kernel(L1, L2, Lout, n_spins, 0) == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     try {
         std::vector<uint32_t> w;
         if (!spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, w, backward))
             return SPINGTP_ERR_UNSUPPORTED;
+        *count = w.size();
+        const size_t n = w.size() < capacity ? w.size() : capacity;
+        if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));
+    } catch (const std::bad_alloc&) {
+        return SPINGTP_ERR_OUT_OF_MEMORY;
+    }
+    return SPINGTP_OK;
+}
+
+spingtp_status spingtp_direct_table_host(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
+                                         int role, uint32_t* words, size_t capacity, size_t* count) {
+    if (count == nullptr || (capacity > 0 && words == nullptr) || role < 0 || role > 2) return SPINGTP_ERR_INVALID_ARG;
+    int spin_mode = 0;
+    const spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
+    if (st != SPINGTP_OK) return st;
+    try {
+        std::vector<uint32_t> w;
+        int lds_floats = 0;
+        spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, role, w, &lds_floats);
+        if (spingtp::find_direct_kernel(lds_floats, 0) == nullptr) return SPINGTP_ERR_UNSUPPORTED;
         *count = w.size();
         const size_t n = w.size() < capacity ? w.size() : capacity;
         if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));
@@ -802,25 +880,41 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     // the large-degree kernels have no parity mixing of their tiles
     if (k != nullptr && k->family == 3 && spin_mode == 1 && (flags & ~kRouteFlags) == SPINGTP_BASIS_PARITY)
         k = nullptr;
+    // the direct kernel: shapes without a Fourier kernel, and the gradients of shapes
+    // whose transposed degrees have none, where its LDS tile fits
+    auto odd_stride = [](int n) { return (n % 2) ? n + 2 : n + 1; };
+    const int bsz = (L1 + 1) * (L1 + 1), bsz2 = (L2 + 1) * (L2 + 1), bszo = (Lout + 1) * (Lout + 1);
+    const int dir_lds =
+        spingtp::kDirectUnits * (odd_stride(n_spins * bsz) + odd_stride(n_spins * bsz2) + odd_stride(n_spins * bszo));
+    const spingtp::KernelEntry* kd = spingtp::find_direct_kernel(dir_lds, static_cast<int>(dtype));
+    const bool fourier_bwd = k != nullptr && L1 == L2 && L2 == Lout;
+    if (k == nullptr) k = kd;
     const spingtp::KernelEntry* kv1 = nullptr;
     if ((flags & SPINGTP_V1_FOURIER) == 0) {
-        kv1 = spingtp::find_pre_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
+        kv1 = spingtp::find_pre_kernel(L1, L2, Lout, n_spins, static_cast<int>(dtype));
         // measured crossover: with larger rows the Fourier route is faster
-        const int rows = (spin_mode ? 3 : 1) * (std::max(L1, Lout) + 1) * (std::max(L1, Lout) + 1);
-        if (kv1 != nullptr && k != nullptr && rows > 112 && (flags & SPINGTP_V1_PRECONTRACT) == 0) kv1 = nullptr;
+        const int rows = n_spins * (std::max(L1, Lout) + 1) * (std::max(L1, Lout) + 1);
+        if (kv1 != nullptr && k != nullptr && k->family != 6 && rows > 112 && (flags & SPINGTP_V1_PRECONTRACT) == 0)
+            kv1 = nullptr;
         if (kv1 == nullptr && (flags & SPINGTP_V1_PRECONTRACT)) return SPINGTP_ERR_UNSUPPORTED;
     }
     if (kv1 == nullptr) kv1 = k;
-    // a shape only the precontracted kernel covers serves spingtp_forward_v1 alone
     if (kv1 == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     const unsigned basis = flags & ~kRouteFlags;
 
     std::vector<double> tab;
     std::vector<double> tab_bwd;
-    std::vector<uint32_t> aux, pre, pre_bwd;
+    std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2;
     bool has_backward = false, same_bwd = false;
     try {
-        if (!spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
+        if (spin_mode < 2 && !spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
+        int lds_floats = 0;
+        if (k != nullptr && k->family == 6)
+            spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 0, dir, &lds_floats);
+        if (kd != nullptr && !fourier_bwd) {
+            spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 1, dir_b1, &lds_floats);
+            spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 2, dir_b2, &lds_floats);
+        }
         if (k != nullptr && k->family == 4) spingtp::build_mfma_operands(L1, aux);
         if (kv1->family == 5) spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre);
         // spingtp_backward_v1 on the precontracted kernel: the same table with J x2
@@ -828,8 +922,7 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
             !spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre_bwd, true))
             pre_bwd.clear();
         // spingtp_backward: square plans with a forward kernel, input 2 conjugated
-        if (k != nullptr && L1 == L2 && L2 == Lout &&
-            spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab_bwd, true)) {
+        if (fourier_bwd && spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab_bwd, true)) {
             has_backward = true;
             same_bwd = tab_bwd == tab;
         }
@@ -842,12 +935,15 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return SPINGTP_ERR_HIP;
     float* d = nullptr;
-    hipError_t e = hipMalloc(&d, tabf.size() * sizeof(float));
-    if (e == hipErrorOutOfMemory) return SPINGTP_ERR_OUT_OF_MEMORY;
-    if (e != hipSuccess) return SPINGTP_ERR_HIP;
-    if (hipMemcpy(d, tabf.data(), tabf.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess) {
-        (void)hipFree(d);
-        return SPINGTP_ERR_HIP;
+    hipError_t e = hipSuccess;
+    if (!tabf.empty()) {
+        e = hipMalloc(&d, tabf.size() * sizeof(float));
+        if (e == hipErrorOutOfMemory) return SPINGTP_ERR_OUT_OF_MEMORY;
+        if (e != hipSuccess) return SPINGTP_ERR_HIP;
+        if (hipMemcpy(d, tabf.data(), tabf.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess) {
+            (void)hipFree(d);
+            return SPINGTP_ERR_HIP;
+        }
     }
     // device copy of a host word table; nullptr for an empty one
     auto upload = [](const std::vector<uint32_t>& h, uint32_t** dp) -> hipError_t {
@@ -861,11 +957,14 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
         }
         return err;
     };
-    uint32_t *da = nullptr, *dpre = nullptr, *dpreb = nullptr;
+    uint32_t *da = nullptr, *dpre = nullptr, *dpreb = nullptr, *ddir = nullptr, *ddir1 = nullptr, *ddir2 = nullptr;
     float* dbwd = nullptr;
     e = upload(aux, &da);
     if (e == hipSuccess) e = upload(pre, &dpre);
     if (e == hipSuccess) e = upload(pre_bwd, &dpreb);
+    if (e == hipSuccess) e = upload(dir, &ddir);
+    if (e == hipSuccess) e = upload(dir_b1, &ddir1);
+    if (e == hipSuccess) e = upload(dir_b2, &ddir2);
     if (e == hipSuccess && has_backward && !same_bwd) {
         std::vector<float> f(tab_bwd.size());
         for (size_t i = 0; i < tab_bwd.size(); ++i) f[i] = static_cast<float>(tab_bwd[i]);
@@ -877,7 +976,10 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
         if (dpre != nullptr) (void)hipFree(dpre);
         if (dpreb != nullptr) (void)hipFree(dpreb);
         if (dbwd != nullptr) (void)hipFree(dbwd);
-        (void)hipFree(d);
+        if (ddir != nullptr) (void)hipFree(ddir);
+        if (ddir1 != nullptr) (void)hipFree(ddir1);
+        if (ddir2 != nullptr) (void)hipFree(ddir2);
+        if (d != nullptr) (void)hipFree(d);
     };
     if (e != hipSuccess) {
         release();
@@ -903,6 +1005,11 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     p->d_pre_bwd = dpreb;
     p->d_tab_bwd = has_backward ? (same_bwd ? d : dbwd) : nullptr;
     p->own_tab_bwd = dbwd != nullptr;
+    p->d_dir = ddir;
+    p->d_dir_b1 = ddir1;
+    p->d_dir_b2 = ddir2;
+    p->kernel_dir = ddir1 != nullptr ? kd : nullptr;
+    p->dir_lds_floats = dir_lds;
     p->kernel = k;
     p->kernel_v1 = kv1;
     *out_plan = p;
@@ -914,8 +1021,11 @@ spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
     int cur = 0;
     hipError_t e = hipGetDevice(&cur);
     if (e == hipSuccess && cur != plan->device) e = hipSetDevice(plan->device);
-    if (e == hipSuccess) e = hipFree(plan->d_tab);
+    if (e == hipSuccess && plan->d_tab != nullptr) e = hipFree(plan->d_tab);
     if (e == hipSuccess && plan->d_aux != nullptr) e = hipFree(plan->d_aux);
+    if (e == hipSuccess && plan->d_dir != nullptr) e = hipFree(plan->d_dir);
+    if (e == hipSuccess && plan->d_dir_b1 != nullptr) e = hipFree(plan->d_dir_b1);
+    if (e == hipSuccess && plan->d_dir_b2 != nullptr) e = hipFree(plan->d_dir_b2);
     if (e == hipSuccess && plan->d_pre != nullptr) e = hipFree(plan->d_pre);
     if (e == hipSuccess && plan->d_pre_bwd != nullptr) e = hipFree(plan->d_pre_bwd);
     if (e == hipSuccess && plan->own_tab_bwd) e = hipFree(plan->d_tab_bwd);
@@ -929,7 +1039,7 @@ spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info) {
     if (plan->kernel == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     info[0] = plan->kernel->waves;
     info[1] = plan->kernel->units;
-    info[2] = plan->kernel->lds_bytes;
+    info[2] = plan->kernel->family == 6 ? plan->dir_lds_floats * 4 : plan->kernel->lds_bytes;
     info[3] = plan->kernel->family;
     return SPINGTP_OK;
 }
@@ -938,7 +1048,7 @@ spingtp_status spingtp_plan_kernel_info_v1(spingtp_plan plan, int* info) {
     if (plan == nullptr || info == nullptr) return SPINGTP_ERR_INVALID_ARG;
     info[0] = plan->kernel_v1->waves;
     info[1] = plan->kernel_v1->units;
-    info[2] = plan->kernel_v1->lds_bytes;
+    info[2] = plan->kernel_v1->family == 6 ? plan->dir_lds_floats * 4 : plan->kernel_v1->lds_bytes;
     info[3] = plan->kernel_v1->family;
     return SPINGTP_OK;
 }

@@ -79,6 +79,20 @@ def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, backward=F
     return out
 
 
+def direct_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, role=0):
+    """spingtp_direct_table_host: the entry table of the direct kernel for one role of T
+    (0 forward, 1 gradient w.r.t. x1, 2 gradient w.r.t. x2; uint32 words)."""
+    arr, n = _spin_array(spins)
+    count = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().spingtp_direct_table_host(L1, L2, Lout, arr, n, basis, role, None, 0, ctypes.byref(count)),
+               "spingtp_direct_table_host")
+    out = np.zeros(count.value, dtype=np.uint32)
+    _lib.check(_lib.lib().spingtp_direct_table_host(L1, L2, Lout, arr, n, basis, role,
+                                                    out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), out.size,
+                                                    ctypes.byref(count)), "spingtp_direct_table_host")
+    return out
+
+
 def conj_map_host(L, spins=(-1, 0, 1), basis=BASIS_PAPER):
     """spingtp_conj_map_host: the conjugation map words of degree L (uint32)."""
     arr, n = _spin_array(spins)

@@ -21,6 +21,7 @@ from paper_2607_01408_amd.spingtp import dense_tensor_host, mfma_operands_host, 
 from tests.oracle_helpers import valid_mask
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+S5 = (-2, -1, 0, 1, 2)
 HEADER = os.path.join(ROOT, "include", "spingtp.h")
 
 
@@ -57,7 +58,8 @@ def _spins(s):
     ((2, 2, 2, (0, 1), 0), 1),          # not symmetric
     ((2, 2, 2, (1, 0, -1), 0), 1),      # not ascending
     ((2, 2, 2, (-1, 1), 0), 1),         # no spin 0
-    ((2, 2, 2, (-2, -1, 0, 1, 2), 0), 2),  # valid, not built
+    ((2, 2, 2, (-2, -1, 0, 1, 2), 0), 2),  # valid; no Fourier tables for s_max = 2
+    ((2, 2, 2, (-2, 0, 2), 0), 2),      # valid, not built
     ((2, 2, 2, (-1, 0, 1), 7), 1),      # unknown basis flag
     ((2, 2, 2, (-1, 0, 1), 3), 1),      # unknown basis flag
     ((2, 2, 2, (-1, 0, 1), 2), 0),      # parity-labelled basis
@@ -217,7 +219,7 @@ def test_plan_tables_reproduce_oracle(built_library, L1, L2, LO, spin, basis):
 @pytest.mark.parametrize("L1,L2,LO,spins,basis", [
     (2, 2, 2, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 1), (3, 2, 4, (-1, 0, 1), 0), (4, 4, 4, (-1, 0, 1), 1),
     (3, 1, 2, (0,), 0), (1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 2), (3, 2, 4, (-1, 0, 1), 2),
-    (2, 1, 2, (0,), 2),
+    (2, 1, 2, (0,), 2), (2, 2, 2, S5, 0), (2, 2, 2, S5, 1), (2, 2, 2, S5, 2), (3, 1, 3, S5, 1),
 ])
 def test_dense_tensor_matches_oracle(built_library, L1, L2, LO, spins, basis):
     """The library's explicit tensor (its own quadrature, the benchmark's comparator) equals the oracle's."""
@@ -407,8 +409,10 @@ def emulate_pre_kernel(words, x1, x2):
             acc[last] = 0.0
         Kt[b * rb:(b + 1) * rb] = blk.reshape(rb, kst)
     K = Kt[:nco, :nc1].T.astype(np.float64)
+    ns = int(words[11])
     k = np.arange(nc1)
-    x1 = np.where((blk1 > 0) & ((k == 0) | (k == 2 * blk1)), 0.0, x1)
+    sa = np.abs(k // blk1 - ns // 2)
+    x1 = np.where(k % blk1 >= sa * sa, x1, 0.0)  # slots with l < |s| are read as 0
     return x1 @ K, K
 
 
@@ -416,7 +420,9 @@ def emulate_pre_kernel(words, x1, x2):
     (1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 0), (1, 3, 3, (-1, 0, 1), 0), (3, 1, 2, (-1, 0, 1), 0),
     (4, 4, 4, (-1, 0, 1), 0), (4, 2, 3, (-1, 0, 1), 1), (3, 3, 3, (-1, 0, 1), 1), (7, 7, 7, (0,), 0),
     (5, 2, 6, (0,), 0), (5, 5, 5, (-1, 0, 1), 0), (6, 6, 6, (-1, 0, 1), 1), (1, 6, 6, (-1, 0, 1), 0),
-    (6, 2, 5, (-1, 0, 1), 0), (3, 3, 3, (-1, 0, 1), 2), (6, 6, 6, (-1, 0, 1), 2), (2, 4, 3, (-1, 0, 1), 2)])
+    (6, 2, 5, (-1, 0, 1), 0), (3, 3, 3, (-1, 0, 1), 2), (6, 6, 6, (-1, 0, 1), 2), (2, 4, 3, (-1, 0, 1), 2),
+    (2, 2, 2, S5, 0), (3, 3, 3, S5, 1), (4, 4, 4, S5, 0), (4, 4, 4, S5, 2), (1, 2, 3, S5, 0), (2, 1, 2, S5, 2),
+    (0, 2, 2, S5, 0)])
 def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
     """The precontracted kernel's table, re-enacted on the CPU, gives the oracle's
     edge kernel K[k1, k3] = sum_k2 T x2 and the oracle's outputs for channels that
@@ -425,7 +431,7 @@ def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
     nc1, nc2, nco, blk1, ks, nt, ipt, kst, nb3, rb, stride = (int(v) for v in words[:11])
     ns = len(spins)
     assert (nc1, nc2, nco) == (ns * (L1 + 1) ** 2, ns * (L2 + 1) ** 2, ns * (LO + 1) ** 2)
-    assert blk1 == ((L1 + 1) ** 2 if ns == 3 else 0)
+    assert blk1 == (L1 + 1) ** 2 and int(words[11]) == ns
     assert (ks, nt, kst) == (-(-nc1 // 16), -(-nco // 16), 16 * -(-nc1 // 16) + 4)
     assert (nb3, rb) == ((1, 16 * nt) if ks <= 5 and nt <= 5 else (-(-16 * nt // 48), 48))
     blocked = ks > 5 or nt > 5
@@ -459,7 +465,7 @@ def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
     rel = np.linalg.norm(y - yo) / np.linalg.norm(yo)
     assert rel <= 1e-6, rel
     # the kernel ignores what the invalid slots of x1 hold
-    if ns == 3:
+    if ns > 1:
         poisoned = x1.copy()
         poisoned[:, ~valid_mask(spins, L1)] = 1e30
         assert np.array_equal(emulate_pre_kernel(words, poisoned * 1.0, x2)[0], y)
@@ -495,7 +501,8 @@ def test_plan_create_route_flags(built_library):
 
 
 @pytest.mark.parametrize("L", [0, 1, 2, 4, 6, 16])
-@pytest.mark.parametrize("spins,basis", [((-1, 0, 1), 0), ((-1, 0, 1), 1), ((0,), 0), ((-1, 0, 1), 2)])
+@pytest.mark.parametrize("spins,basis", [((-1, 0, 1), 0), ((-1, 0, 1), 1), ((0,), 0), ((-1, 0, 1), 2), (S5, 0),
+                                         (S5, 1), (S5, 2)])
 def test_conj_map_matches_oracle(built_library, L, spins, basis):
     """The library's conjugation map (used by spingtp_backward) equals the oracle's J."""
     from oracle.realbasis import conjugation_map
@@ -552,3 +559,93 @@ def test_backward_pre_table_reproduces_oracle(built_library, L, spins, basis):
     y, _ = emulate_pre_kernel(words, g, x2)
     r1, _ = oracle.RealGauntTensor(L, L, L, spins, basis).vjp(x1, np.broadcast_to(x2, (C, n)), g)
     assert np.abs(y - r1).max() <= 1e-6 * max(1.0, np.abs(r1).max())
+
+
+def emulate_direct_kernel(words, A, B):
+    """The direct kernel (family 6) on the CPU from its exact table words: per
+    output slot, its 8-entry batches in order, products A[a] * B[b] rounded to fp32
+    and added with one fp32 fma each into two alternating sums (entries 0, 2, 4, 6
+    of a batch to the first), which are added at the end of the slot."""
+    na, nb, no, sta, stb, sto, nbatch = (int(v) for v in words[:7])
+    counts = words[8:8 + no].astype(np.int64)
+    assert counts.sum() == nbatch
+    body = words[8 + no:]
+    assert body.size == 16 * (nbatch + 1) and not body[16 * nbatch:].any()  # the trailing zero batch
+    batches = body[:16 * nbatch].reshape(nbatch, 16)
+    ent, val = batches[:, :8], batches[:, 8:].copy().view(np.float32)
+    U = A.shape[0]
+    Az = np.zeros((U, sta), dtype=np.float32)
+    Bz = np.zeros((U, stb), dtype=np.float32)
+    Az[:, :na], Bz[:, :nb] = A, B
+    out = np.zeros((U, no), dtype=np.float32)
+    q = 0
+    for o in range(no):
+        acc = [np.zeros(U, dtype=np.float32), np.zeros(U, dtype=np.float32)]
+        for _ in range(counts[o]):
+            for i in range(8):
+                a, b = int(ent[q, i] & 0xFFFF), int(ent[q, i] >> 16)
+                p = (Az[:, a] * Bz[:, b]).astype(np.float32)
+                acc[i % 2] = (val[q, i].astype(np.float64) * p + acc[i % 2]).astype(np.float32)
+            q += 1
+        out[:, o] = acc[0] + acc[1]
+    return out.astype(np.float64)
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [
+    (2, 2, 2, S5, 0), (2, 2, 2, S5, 1), (2, 2, 2, S5, 2), (3, 3, 3, S5, 0), (1, 2, 2, S5, 0), (2, 1, 3, S5, 2),
+    (0, 2, 2, S5, 0), (4, 4, 4, S5, 0), (3, 2, 4, (-1, 0, 1), 0), (2, 4, 3, (-1, 0, 1), 1), (5, 5, 5, (0,), 0),
+    (2, 3, 4, (0,), 0)])
+def test_direct_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
+    """The direct kernel's three tables, re-enacted on the CPU from the exact words,
+    give the oracle's forward and both gradients (fp32 arithmetic: 1e-6); entries
+    are exactly the nonzeros of T, padding points at the zero columns, and what the
+    l < |s| input slots hold is never read."""
+    from paper_2607_01408_amd.spingtp import direct_table_host
+
+    ns = len(spins)
+    n1, n2, no = ns * (L1 + 1) ** 2, ns * (L2 + 1) ** 2, ns * (LO + 1) ** 2
+    G = oracle.RealGauntTensor(L1, L2, LO, spins, basis)
+    T = G.dense()
+    rng = np.random.default_rng(5 + L1 + 3 * L2 + 9 * LO + 27 * basis)
+    U = 7
+    x1 = rng.standard_normal((U, n1)) * valid_mask(spins, L1)
+    x2 = rng.standard_normal((U, n2)) * valid_mask(spins, L2)
+    g = rng.standard_normal((U, no)) * valid_mask(spins, LO)
+    r1, r2 = G.vjp(x1, x2, g)
+    y = G.apply(x1, x2).reshape(U, -1)
+    for role, (A, B, ref, widths) in enumerate([(x1, x2, y, (n1, n2, no)), (g, x2, r1, (no, n2, n1)),
+                                                (g, x1, r2, (no, n1, n2))]):
+        w = direct_table_host(L1, L2, LO, spins, basis, role)
+        na, nb, nout, sta, stb, sto, nbatch = (int(v) for v in w[:7])
+        assert (na, nb, nout) == widths and w[7] == 0
+        for n, st in ((na, sta), (nb, stb), (nout, sto)):
+            assert st % 2 == 1 and st > n
+        ent = w[8 + nout:8 + nout + 16 * nbatch].reshape(nbatch, 16)[:, :8].ravel()
+        val = w[8 + nout:8 + nout + 16 * nbatch].reshape(nbatch, 16)[:, 8:].copy().view(np.float32).ravel()
+        pad = val == 0
+        assert np.all(ent[pad] == (na | (nb << 16)))
+        # the entries are the nonzeros of T in this role (k1, k2, k3 permuted)
+        perm = [(0, 1, 2), (2, 1, 0), (2, 0, 1)][role]
+        Tr = np.transpose(T, perm)  # [a][b][o] with a, b, o the role's indices
+        assert (~pad).sum() == (np.abs(Tr) > 0).sum()
+        out = emulate_direct_kernel(w, A, B)
+        assert np.linalg.norm(out - ref) <= 1e-6 * max(np.linalg.norm(ref), 1e-30), role
+        if ns > 1:  # poisoned invalid slots are never read
+            Ap = np.where(valid_mask(spins, (L1, LO, LO)[role]), A, 1e30)
+            Bp = np.where(valid_mask(spins, (L2, L2, L1)[role]), B, 1e30)
+            assert np.array_equal(emulate_direct_kernel(w, Ap, Bp), out)
+
+
+def test_direct_table_argument_checks(built_library):
+    count = ctypes.c_size_t(0)
+    S = (ctypes.c_int * 5)(-2, -1, 0, 1, 2)
+    assert built_library.spingtp_direct_table_host(2, 2, 2, S, 5, 0, 3, None, 0, ctypes.byref(count)) == 1
+    assert built_library.spingtp_direct_table_host(2, 2, 2, S, 5, 0, -1, None, 0, ctypes.byref(count)) == 1
+    assert built_library.spingtp_direct_table_host(2, 2, 2, S, 5, 0, 0, None, 0, None) == 1
+    # a tile beyond the kernel's LDS: 64 x 3 x 247 floats at degree 6 with spins {-2..2}
+    assert built_library.spingtp_direct_table_host(6, 6, 6, S, 5, 0, 0, None, 0, ctypes.byref(count)) == 2
+    assert built_library.spingtp_direct_table_host(2, 2, 2, S, 5, 0, 0, None, 0, ctypes.byref(count)) == 0
+    assert count.value > 8
+    # the Fourier tables do not exist for spins {-2..2}
+    n = ctypes.c_size_t(0)
+    assert built_library.spingtp_plan_tables_host(2, 2, 2, S, 5, 0, None, 0, ctypes.byref(n), None) == 2

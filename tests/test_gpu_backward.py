@@ -127,12 +127,16 @@ def test_backward_one_side_and_argument_rules():
     paired = Plan(L, L, L, S3, "fp32", 1)
     p1, _ = paired.backward(x1, x2, g, need_x2=False)
     assert torch.equal(p1, paired.forward(g, x2))
-    # mixed degrees have no backward
+    # mixed degrees: the gradients run on the direct kernel (their numerics: test_gpu_direct.py)
     mixed = Plan(1, 3, 3, S3, "fp32")
-    assert lib.spingtp_backward(mixed.handle, None, None, None, None, None, 4, 4, None) == 2
-    with pytest.raises(SpinGTPError):
-        mixed.backward(torch.zeros((2, 1, 3, 4), device="cuda"), torch.zeros((2, 1, 3, 16), device="cuda"),
-                       torch.zeros((2, 1, 3, 16), device="cuda"))
+    assert lib.spingtp_backward(mixed.handle, None, None, None, None, None, 4, 4, None) == 0  # nothing asked
+    m1 = torch.zeros((2, 1, 3, 4), device="cuda")
+    m2, mg = torch.zeros((2, 1, 3, 16), device="cuda"), torch.zeros((2, 1, 3, 16), device="cuda")
+    assert lib.spingtp_backward(mixed.handle, m1.data_ptr(), m2.data_ptr(), None, m1.data_ptr(), None, 2, 1,
+                                None) == 1  # grad_out missing
+    g1, g2 = mixed.backward(m1, m2, mg)
+    torch.cuda.synchronize()
+    assert not g1.any() and not g2.any()
 
 
 def test_backward_invalid_slots():
@@ -243,6 +247,7 @@ def test_backward_v1_rules():
     assert lib.spingtp_backward_v1(*args, None, 0, N, 0, None) == 0
     torch.cuda.synchronize()
     assert (gx2 == 0).all()
-    # a plan whose shape has no spingtp_forward kernel has no backward
+    # a shape without a Fourier kernel: its gradients run on the direct kernel, workspace [N][C][NC2]
     mixed = Plan(3, 1, 2, S3, "fp32")
-    assert lib.spingtp_backward_v1_workspace_size(mixed.handle, N, C, ctypes.byref(need)) == 2
+    assert lib.spingtp_backward_v1_workspace_size(mixed.handle, N, C, ctypes.byref(need)) == 0
+    assert need.value == N * C * 3 * 4 * 4

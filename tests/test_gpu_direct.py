@@ -1,0 +1,217 @@
+"""GPU parity of the direct sparse-tensor kernel (family 6) and of spins {-2..2}.
+
+The direct kernel serves shapes the Fourier kernels do not cover: the spin set
+{-2, -1, 0, 1, 2} (s_max = 2, the setting of the paper's chirality experiments,
+App. F), degree triples without a Fourier instantiation, and the gradients of
+non-square shapes.  Spins {-2..2} also run forward_v1 on the precontracted
+kernel.  Everything is compared with the float64 oracle on the dtype-rounded
+inputs read back from the device; bars as elsewhere: relative L2 1e-5 (fp32),
+2e-2 (bf16).
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from tests.oracle_helpers import valid_mask
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU visible", allow_module_level=True)
+
+from paper_2607_01408_amd import Plan, SpinGTPError, workloads  # noqa: E402
+
+S5 = (-2, -1, 0, 1, 2)
+S3 = (-1, 0, 1)
+TOL = {"fp32": 1e-5, "bf16": 2e-2}
+
+
+def rel_l2(y, ref):
+    return float(np.linalg.norm(y - ref) / max(np.linalg.norm(ref), 1e-300))
+
+
+def host(t, rows):
+    return t.reshape(rows, -1).double().cpu().numpy()
+
+
+def run_forward(L1, L2, LO, spins, N, C, dtype="fp32", basis=0, seed=0, family=6):
+    print(f"[direct] L=({L1},{L2},{LO}) spins={spins} N={N} C={C} {dtype} basis={basis}", flush=True)
+    x1 = workloads.draw(L1, N, C, 100 + seed, dtype, spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, C, 200 + seed, dtype, spins, "unit", "cuda")
+    plan = Plan(L1, L2, LO, spins, dtype, basis)
+    assert plan.kernel_info()["family"] == family
+    y = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    U = N * C
+    ref = oracle.RealGauntTensor(L1, L2, LO, spins, basis).apply(host(x1, U), host(x2, U)).reshape(U, -1)
+    err = rel_l2(host(y, U), ref)
+    print(f"[direct]   rel_l2={err:.3e}", flush=True)
+    assert err <= TOL[dtype], err
+    return plan, (x1, x2, y)
+
+
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("basis", [0, 1, 2])
+def test_spin2_forward(L, basis):
+    # 37 x 3 = 111 units: one full 64-unit tile and a ragged tail
+    run_forward(L, L, L, S5, 37, 3, "fp32", basis, seed=L + 10 * basis)
+
+
+@pytest.mark.parametrize("L1,L2,LO", [(1, 2, 2), (2, 1, 3), (2, 2, 0), (0, 2, 2), (3, 1, 2)])
+def test_spin2_mixed_degrees(L1, L2, LO):
+    run_forward(L1, L2, LO, S5, 29, 5, "fp32", 0, seed=L1 + 3 * L2 + 9 * LO)
+
+
+@pytest.mark.parametrize("L", [2, 3])
+def test_spin2_bf16(L):
+    run_forward(L, L, L, S5, 41, 4, "bf16", 0, seed=50 + L)
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins", [((3, 2, 4) + (S3,)), ((2, 4, 3) + (S3,)), ((4, 1, 3) + (S3,)),
+                                            ((5, 5, 5) + ((0,),)), ((7, 7, 7) + ((0,),)), ((2, 3, 4) + ((0,),))])
+def test_direct_kernel_shapes_without_fourier_kernel(L1, L2, LO, spins):
+    run_forward(L1, L2, LO, spins, 33, 5, "fp32", 0, seed=7 * L1 + L2)
+
+
+def test_direct_many_tiles_and_grid_stride():
+    # 1,500,001 units: more tiles than the grid (2^20 workgroups), so workgroups loop
+    N, C = 1_500_001, 1
+    x1 = workloads.draw(2, N, C, 300, "fp32", S5, "unit", "cuda")
+    x2 = workloads.draw(2, N, C, 301, "fp32", S5, "unit", "cuda")
+    y = Plan(2, 2, 2, S5, "fp32").forward(x1, x2)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(9)
+    idx = np.unique(np.concatenate([np.arange(256), np.arange(N - 256, N), rng.choice(N, 4096, replace=False)]))
+    ti = torch.as_tensor(idx, device="cuda")
+    a, b, g = (t.view(N, -1)[ti].double().cpu().numpy() for t in (x1, x2, y))
+    ref = oracle.RealGauntTensor(2, 2, 2, S5).apply(a, b).reshape(len(idx), -1)
+    err = rel_l2(g, ref)
+    print(f"[direct] 1.5M units sampled rel_l2={err:.3e}", flush=True)
+    assert err <= 1e-5
+
+
+def test_direct_invalid_slots_and_poisoned_output():
+    N, C, L = 9, 8, 2
+    x1 = workloads.draw(L, N, C, 400, "fp32", S5, "unit", "cuda")
+    x2 = workloads.draw(L, N, C, 401, "fp32", S5, "unit", "cuda")
+    plan = Plan(L, L, L, S5, "fp32")
+    y0 = plan.forward(x1, x2)
+    bad = torch.as_tensor(~valid_mask(S5, L), device="cuda")
+    p1, p2 = x1.clone(), x2.clone()
+    p1.view(N * C, -1)[:, bad] = float("nan")
+    p2.view(N * C, -1)[:, bad] = 1e30
+    out = torch.full_like(y0, float("nan"))
+    plan.forward(p1, p2, out)
+    torch.cuda.synchronize()
+    assert torch.equal(out, y0)
+    assert torch.all(out.view(N * C, -1)[:, bad] == 0)
+
+
+def test_direct_bitwise_deterministic():
+    x1 = workloads.draw(3, 50, 7, 500, "fp32", S5, "unit", "cuda")
+    x2 = workloads.draw(3, 50, 7, 501, "fp32", S5, "unit", "cuda")
+    plan = Plan(3, 3, 3, S5, "fp32")
+    assert torch.equal(plan.forward(x1, x2), plan.forward(x1, x2))
+
+
+def test_spin2_unsupported_beyond_the_tile():
+    # degree 6 with spins {-2..2}: the tile exceeds the direct kernel's LDS and no other kernel exists
+    with pytest.raises(SpinGTPError):
+        Plan(6, 6, 6, S5, "fp32")
+
+
+# --- forward_v1 with spins {-2..2}: the precontracted kernel ---
+
+@pytest.mark.parametrize("shape,C", [((1, 1, 1), 16), ((2, 2, 2), 64), ((2, 2, 2), 129), ((3, 3, 3), 33),
+                                     ((4, 4, 4), 40), ((1, 2, 3), 17)])
+@pytest.mark.parametrize("basis", [0, 2])
+def test_spin2_v1_precontracted(shape, C, basis):
+    L1, L2, LO = shape
+    N = 13
+    print(f"[direct-v1] L={shape} C={C} basis={basis}", flush=True)
+    x1 = workloads.draw(L1, N, C, 600 + C, "fp32", S5, "unit", "cuda")
+    x2 = workloads.draw(L2, N, 1, 700 + C, "fp32", S5, "unit", "cuda")
+    plan = Plan(L1, L2, LO, S5, "fp32", basis)
+    assert plan.kernel_info_v1()["family"] == 5
+    y = plan.forward_v1(x1, x2)
+    torch.cuda.synchronize()
+    U = N * C
+    b = np.repeat(host(x2, N), C, axis=0)
+    ref = oracle.RealGauntTensor(L1, L2, LO, S5, basis).apply(host(x1, U), b).reshape(U, -1)
+    err = rel_l2(host(y, U), ref)
+    print(f"[direct-v1]   rel_l2={err:.3e}", flush=True)
+    assert err <= 1e-6, err
+
+
+def test_v1_on_the_direct_kernel():
+    # beyond the precontracted kernel's rows (147), V = 1 runs the direct kernel with x2 per edge
+    L1, L2, LO, spins, N, C = 8, 1, 8, S3, 7, 5
+    plan = Plan(L1, L2, LO, spins, "fp32")
+    assert plan.kernel_info_v1()["family"] == 6
+    x1 = workloads.draw(L1, N, C, 800, "fp32", spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, 1, 801, "fp32", spins, "unit", "cuda")
+    y = plan.forward_v1(x1, x2)
+    torch.cuda.synchronize()
+    U = N * C
+    ref = oracle.RealGauntTensor(L1, L2, LO, spins).apply(host(x1, U), np.repeat(host(x2, N), C, axis=0))
+    err = rel_l2(host(y, U), ref.reshape(U, -1))
+    assert err <= 1e-5, err
+
+
+# --- gradients on the direct kernel ---
+
+def run_backward(L1, L2, LO, spins, N, C, dtype="fp32", basis=0, seed=0):
+    print(f"[direct-bwd] L=({L1},{L2},{LO}) spins={spins} N={N} C={C} {dtype} basis={basis}", flush=True)
+    x1 = workloads.draw(L1, N, C, 900 + seed, dtype, spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, C, 950 + seed, dtype, spins, "unit", "cuda")
+    g = workloads.draw(LO, N, C, 990 + seed, dtype, spins, "unit", "cuda")
+    plan = Plan(L1, L2, LO, spins, dtype, basis)
+    gx1, gx2 = plan.backward(x1, x2, g)
+    torch.cuda.synchronize()
+    U = N * C
+    r1, r2 = oracle.RealGauntTensor(L1, L2, LO, spins, basis).vjp(host(x1, U), host(x2, U), host(g, U))
+    e1, e2 = rel_l2(host(gx1, U), r1), rel_l2(host(gx2, U), r2)
+    print(f"[direct-bwd]   rel_l2 {e1:.3e} {e2:.3e}", flush=True)
+    assert e1 <= TOL[dtype] and e2 <= TOL[dtype], (e1, e2)
+
+
+@pytest.mark.parametrize("L", [1, 2, 3])
+@pytest.mark.parametrize("basis", [0, 1, 2])
+def test_spin2_backward(L, basis):
+    run_backward(L, L, L, S5, 23, 3, "fp32", basis, seed=L + 5 * basis)
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins", [((1, 3, 3) + (S3,)), ((2, 1, 3) + (S3,)), ((3, 2, 4) + (S3,)),
+                                            ((2, 1, 2) + (S5,)), ((5, 2, 6) + ((0,),))])
+def test_backward_mixed_degrees(L1, L2, LO, spins):
+    # non-square shapes, also those whose forward runs on a Fourier kernel
+    run_backward(L1, L2, LO, spins, 19, 4, "fp32", 0, seed=L1 + 4 * L2)
+
+
+def test_spin2_backward_bf16():
+    run_backward(2, 2, 2, S5, 31, 4, "bf16", 0, seed=77)
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,C", [(2, 2, 2, S5, 17), (3, 3, 3, S5, 1), (1, 3, 3, S3, 9),
+                                              (3, 2, 4, S3, 6)])
+def test_backward_v1_direct_routes(L1, L2, LO, spins, C):
+    # spins {-2..2}: grad_x1 on the conjugated precontracted table, grad_x2 on the direct kernel;
+    # mixed degrees: both on the direct kernel (grad_x1 with x2 read once per edge)
+    N = 11
+    print(f"[direct-bwd-v1] L=({L1},{L2},{LO}) spins={spins} C={C}", flush=True)
+    x1 = workloads.draw(L1, N, C, 1100 + C, "fp32", spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, 1, 1200 + C, "fp32", spins, "unit", "cuda")
+    g = workloads.draw(LO, N, C, 1300 + C, "fp32", spins, "unit", "cuda")
+    plan = Plan(L1, L2, LO, spins, "fp32")
+    gx1, gx2 = plan.backward_v1(x1, x2, g)
+    torch.cuda.synchronize()
+    U = N * C
+    r1, r2 = oracle.RealGauntTensor(L1, L2, LO, spins).vjp(host(x1, U), np.repeat(host(x2, N), C, axis=0),
+                                                            host(g, U))
+    r2 = r2.reshape(N, C, -1).sum(axis=1)
+    e1, e2 = rel_l2(host(gx1, U), r1), rel_l2(host(gx2, N), r2)
+    print(f"[direct-bwd-v1]   rel_l2 {e1:.3e} {e2:.3e}", flush=True)
+    assert e1 <= 1e-5 and e2 <= 1e-5, (e1, e2)
