@@ -32,7 +32,8 @@ _CSRC = "paper_2607_01408_amd/csrc/"
 
 def kernel_sources(kname):
     """The source files a forward kernel is compiled from (its counters go stale when they change)."""
-    main = "forward_mfma.hip" if kname == "spingtp_fwd_mfma_kernel" else "forward.hip"
+    main = {"spingtp_fwd_mfma_kernel": "forward_mfma.hip",
+            "spingtp_fwd_direct_kernel": "forward_direct.hip"}.get(kname, "forward.hip")
     return tuple(_CSRC + f for f in (main, "device_common.h", "layout.h"))
 
 
@@ -106,14 +107,14 @@ def measured_traffic(workload, dtype, units, L, kname, valu=False, basis="paper"
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(L, x1, x2, seconds):
+def cpu_baseline(L, x1, x2, seconds, spins=(-1, 0, 1), basis=0):
     """The CPU oracle on a bounded sample of the same inputs, on the host cores."""
     import numpy as np
 
     import oracle
 
     t0 = time.perf_counter()
-    T = oracle.RealGauntTensor(L, L, L, (-1, 0, 1))
+    T = oracle.RealGauntTensor(L, L, L, spins, basis)
     build_s = time.perf_counter() - t0
     U = x1.shape[0] * x1.shape[1]
     a = x1.reshape(U, -1)
@@ -471,8 +472,9 @@ def main():
     x1, x2, meta = workloads.make_pair(args.workload, dtype=args.dtype, L=args.L, device="cuda:0")
     L = meta["L"]
     U = meta["N"] * meta["C"]
-    plan = Plan(L, L, L, workloads.SPINS, args.dtype, BASES[args.basis], valu_only=args.valu)
-    out = torch.empty((meta["N"], meta["C"], 3, (L + 1) ** 2), dtype=x1.dtype, device="cuda:0")
+    spins = meta["spins"]
+    plan = Plan(L, L, L, spins, args.dtype, BASES[args.basis], valu_only=args.valu)
+    out = torch.empty((meta["N"], meta["C"], len(spins), (L + 1) ** 2), dtype=x1.dtype, device="cuda:0")
     print(f"[bench] {meta['workload']} L={L} N={meta['N']} C={meta['C']} {args.dtype} units={U} "
           f"kernel={plan.kernel_info()}", file=sys.stderr, flush=True)
 
@@ -496,12 +498,21 @@ def main():
     avg_launch_ms = float(np.mean(launch_ms))
     value = U / (ms_per_step / 1e3)
 
-    flops_unit = route_flops(L, L, L, True)
-    achieved_tflops = flops_unit * U / (avg_launch_ms / 1e3) / 1e12
-    bytes_unit = hbm_bytes_per_unit(L, L, L, args.dtype)
     kinfo = plan.kernel_info()
     kname = {1: "spingtp_fwd_kernel", 2: "spingtp_fwd_pair_kernel", 3: "spingtp_fwd_big_kernel",
-             4: "spingtp_fwd_mfma_kernel"}[kinfo["family"]]
+             4: "spingtp_fwd_mfma_kernel", 6: "spingtp_fwd_direct_kernel"}[kinfo["family"]]
+    bytes_unit = hbm_bytes_per_unit(L, L, L, args.dtype, len(spins))
+    if kinfo["family"] == 6:
+        # the direct kernel: one product and one fma per nonzero of T (entries of its table)
+        from paper_2607_01408_amd import direct_table_host
+
+        w = direct_table_host(L, L, L, spins, BASES[args.basis], 0)
+        nco, nbatch = int(w[2]), int(w[6])
+        vals = w[8 + nco:8 + nco + 24 * nbatch].reshape(nbatch, 24)[:, 8:]
+        flops_unit = 3 * int((vals != 0).sum())
+    else:
+        flops_unit = route_flops(L, L, L, True)
+    achieved_tflops = flops_unit * U / (avg_launch_ms / 1e3) / 1e12
     # arithmetic of the path: the matrix-core kernel runs the two phi transforms as fp16
     # products with fp32 accumulation (three split products per term for fp32 I/O)
     if kinfo["family"] == 4:
@@ -530,7 +541,7 @@ def main():
     ti = torch.as_tensor(idx, device="cuda:0")
     ya = out.view(U, -1)[ti].double().cpu().numpy()
     ref = oracle.spingtp(x1.view(U, -1)[ti].double().cpu().numpy(), x2.view(U, -1)[ti].double().cpu().numpy(),
-                         L, L, L, workloads.SPINS, BASES[args.basis]).reshape(len(idx), -1)
+                         L, L, L, spins, BASES[args.basis]).reshape(len(idx), -1)
     parity = float(np.linalg.norm(ya - ref) / np.linalg.norm(ref))
 
     result = {
@@ -549,7 +560,7 @@ def main():
         "io_dtype": args.dtype,
         "data": "synthetic",
         "config": {
-            "workload": f"{meta['workload']}: L1=L2=Lout={L}, spins (-1,0,+1), N={meta['N']} edges x "
+            "workload": f"{meta['workload']}: L1=L2=Lout={L}, spins {spins}, N={meta['N']} edges x "
                         f"C={meta['C']} channels ({U} units), {args.dtype} I/O, N(0,1) coefficients",
             "L1": L, "L2": L, "Lout": L, "N": meta["N"], "C": meta["C"], "units": U, "basis": args.basis,
             "seeds": list(meta["seeds"]),
@@ -560,6 +571,18 @@ def main():
             "peak": PEAK_FP32_VECTOR_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,
+        } if kinfo["family"] != 6 else {
+            # the direct kernel moves more bytes per flop than the fp32 ridge point: HBM bound
+            "bound": "hbm",
+            "achieved": bytes_unit * U / (avg_launch_ms / 1e3) / 1e9,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": bytes_unit * U / (avg_launch_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
+            "alu_tflops": achieved_tflops,
+            "alu_frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,
+        },
+    }
+    result["roofline"].update({
             "traffic": traffic,
             "kernel": kname,
             "kernel_family": kinfo["family"],
@@ -568,12 +591,11 @@ def main():
             "hbm_bytes_per_unit": bytes_unit,
             "hbm_achieved_gbs": bytes_unit * U / (avg_launch_ms / 1e3) / 1e9,
             "hbm_frac": bytes_unit * U / (avg_launch_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
-        },
-        "parity_rel_l2": parity,
-        "parity_units": int(len(idx)),
-    }
+    })
+    result["parity_rel_l2"] = parity
+    result["parity_units"] = int(len(idx))
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(L, x1, x2, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(L, x1, x2, args.cpu_seconds, spins, BASES[args.basis])
     print(json.dumps(result), flush=True)
 
 

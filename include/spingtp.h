@@ -327,12 +327,14 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
  * Word layout:
  *   [0, 8)         NCA, NCB, NCO (widths of A, B, out), STA, STB, STO (odd LDS
  *                  row strides, each above its width: column NCA of A and NCB
- *                  of B hold 0), NBATCH, 0;
- *   [8, 8 + NCO)   batches of 8 entries per output slot, in output order;
- *   then NBATCH batches of 16 words: 8 entry words a | b << 16, then their 8
- *   fp32 values (bits), and 16 zero words.  out[o] = sum over the entries of slot o of
- *   value * A[a] * B[b]; entries are the nonzeros of T in ascending (a, b) order,
- *   padded with (NCA, NCB, 0) entries.
+ *                  of B hold 0), NBATCH, 16 (entries per batch);
+ *   [8, 8 + NCO)   batches per output slot, in output order;
+ *   then NBATCH batches of 24 words: 8 index words (entry 2i in the low 16 bits
+ *   of word i, entry 2i + 1 in the high 16 bits, each a | b << 8), then the 16
+ *   fp32 values (bits); and 48 zero words.  out[o] = sum over the entries of
+ *   slot o of value * A[a] * B[b]; entries are the nonzeros of T in ascending
+ *   (a, b) order, padded with (NCA, NCB, 0) entries.  Rows longer than 254
+ *   (8-bit indices) give SPINGTP_ERR_UNSUPPORTED.
  * Writes min(capacity, total) words to `words` (may be NULL when capacity is 0)
  * and the total to *count.
  */

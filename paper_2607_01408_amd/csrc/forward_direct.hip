@@ -15,15 +15,21 @@
 // One wave per workgroup, one unit per lane, 64 units per tile.  The A and B rows
 // of the tile sit in LDS at odd strides (conflict-free per-lane gathers), with a
 // zero column past each row that padding entries point at.  The entry list is
-// wave-uniform: its words come in through scalar loads, 8 entries per 64-byte
-// batch, and every lane gathers its own A and B values.  Outputs are summed in
-// registers per output slot, staged in LDS and stored row-contiguously.
+// wave-uniform: it comes in through scalar loads, 16 entries per 96-byte batch,
+// one batch ahead, and every lane gathers its own A and B values.  Entries take
+// 6 bytes (two 8-bit indices, an fp32 value) so that the list of the small
+// shapes this kernel serves stays inside the scalar cache (16 KB; 2,003 entries
+// at degree 2 with spins {-2..2}): misses there, not arithmetic, set the pace.
+// Outputs are summed in registers per output slot and stored by each lane to its
+// own row as soon as the slot is complete (no output tile in LDS, which keeps
+// more waves resident).
 //
 // Table (uint32 words, built by build_direct_table):
-//   [0, 8)   NCA, NCB, NCO, STA, STB, STO, NBATCH, 0
+//   [0, 8)   NCA, NCB, NCO, STA, STB, STO, NBATCH, 16 (entries per batch)
 //   [8, 8 + NCO)  batches per output slot, in output order
-//   then NBATCH batches of 16 words: 8 entry words a | b << 16, 8 fp32 values,
-//   and one zero batch.
+//   then NBATCH batches of 24 words: 8 index words (entry 2i in the low half of
+//   word i, entry 2i + 1 in the high half; each half a | b << 8), 16 fp32 values;
+//   and two zero batches.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -36,22 +42,46 @@ namespace {
 
 __device__ __forceinline__ float direct_load(const float* p) { return *p; }
 __device__ __forceinline__ float direct_load(const uint16_t* p) { return bf16_to_f32(*p); }
-__device__ __forceinline__ void direct_store(float* p, float v) { *p = v; }
-__device__ __forceinline__ void direct_store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+// Bounds-checked stores through a buffer resource: lanes whose byte offset is at or
+// past the resource's size write nothing, so the store needs no divergent branch.
+__device__ __forceinline__ void direct_store(__amdgpu_buffer_rsrc_t r, int idx, float v, float*) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, idx * 4, 0, 0);
+}
+__device__ __forceinline__ void direct_store(__amdgpu_buffer_rsrc_t r, int idx, float v, uint16_t*) {
+    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(v), r, idx * 2, 0, 0);
+}
+// word 3 of a raw (untyped, stride 0) buffer resource: 32-bit data format
+constexpr int kRawBufferWord3 = 0x00020000;
 
 // Rows [row0, row0 + nvalid) of a [rows][nc] array into an LDS tile of stride st;
 // row r of the tile reads source row (row0 + r) / per_row.  Columns nc..st-1 and
-// rows past nvalid are zero.
+// rows past nvalid are zero.  Elements go in chunks of 16 per lane, all loads of a
+// chunk issued before its LDS stores.
 template <typename TIO>
 __device__ void direct_load_tile(const TIO* __restrict__ src, int64_t row0, int64_t per_row, int nvalid, int nc,
                                  int st, float* dst, int lane) {
-    if (per_row == 1) {
-        const TIO* s = src + row0 * nc;
-        const int n = nvalid * nc;
-        int r = lane / nc, c = lane - (lane / nc) * nc;
-        const int dr = kDirectUnits / nc, dc = kDirectUnits - (kDirectUnits / nc) * nc;
-        for (int e = lane; e < n; e += kDirectUnits) {
-            dst[r * st + c] = direct_load(s + e);
+    constexpr int K = 16;
+    const int n = nvalid * nc;
+    int r = lane / nc, c = lane - (lane / nc) * nc;  // tile position of element e = lane + 64 i
+    const int dr = kDirectUnits / nc, dc = kDirectUnits - (kDirectUnits / nc) * nc;
+    for (int e0 = 0; e0 < n; e0 += K * kDirectUnits) {
+        float v[K];
+        int rr = r, cc = c;
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            const int e = e0 + lane + kDirectUnits * i;
+            const int64_t at = per_row == 1 ? row0 * nc + e : ((row0 + rr) / per_row) * nc + cc;
+            v[i] = e < n ? direct_load(src + at) : 0.f;
+            rr += dr;
+            cc += dc;
+            if (cc >= nc) {
+                cc -= nc;
+                ++rr;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            if (e0 + lane + kDirectUnits * i < n) dst[r * st + c] = v[i];
             r += dr;
             c += dc;
             if (c >= nc) {
@@ -59,17 +89,12 @@ __device__ void direct_load_tile(const TIO* __restrict__ src, int64_t row0, int6
                 ++r;
             }
         }
-    } else {
-        for (int r = 0; r < nvalid; ++r) {
-            const TIO* s = src + ((row0 + r) / per_row) * nc;
-            for (int c = lane; c < nc; c += kDirectUnits) dst[r * st + c] = direct_load(s + c);
-        }
     }
     for (int r = 0; r < kDirectUnits; ++r)
         for (int c = (r < nvalid ? nc : 0) + lane; c < st; c += kDirectUnits) dst[r * st + c] = 0.f;
 }
 
-// LDS (dynamic, sized by the launch): A, B and output tiles of 64 rows each.
+// LDS (dynamic, sized by the launch): A and B tiles of 64 rows each.
 template <typename TIO>
 __global__ __launch_bounds__(kDirectUnits) void spingtp_fwd_direct_kernel(const TIO* __restrict__ a,
                                                                           const TIO* __restrict__ b,
@@ -79,14 +104,13 @@ __global__ __launch_bounds__(kDirectUnits) void spingtp_fwd_direct_kernel(const 
                                                                           int lds_floats) {
     extern __shared__ float lds[];
     const int nca = static_cast<int>(tab[0]), ncb = static_cast<int>(tab[1]), nco = static_cast<int>(tab[2]);
-    const int sta = static_cast<int>(tab[3]), stb = static_cast<int>(tab[4]), sto = static_cast<int>(tab[5]);
-    if (kDirectUnits * (sta + stb + sto) > lds_floats) return;  // the launch sizes LDS from the same table
+    const int sta = static_cast<int>(tab[3]), stb = static_cast<int>(tab[4]);
+    if (kDirectUnits * (sta + stb) > lds_floats) return;  // the launch sizes LDS from the same table
     const int nbatch = static_cast<int>(tab[6]);
     const uint32_t* __restrict__ counts = tab + 8;
     const uint32_t* __restrict__ batches = tab + 8 + nco;
     float* A = lds;
     float* B = A + kDirectUnits * sta;
-    float* Y = B + kDirectUnits * stb;
     const int lane = threadIdx.x;
     const float* Arow = A + lane * sta;
     const float* Brow = B + lane * stb;
@@ -95,57 +119,50 @@ __global__ __launch_bounds__(kDirectUnits) void spingtp_fwd_direct_kernel(const 
     for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
         const int64_t u0 = tile * kDirectUnits;
         const int nvalid = static_cast<int>(units - u0 < kDirectUnits ? units - u0 : kDirectUnits);
-        __syncthreads();  // the previous tile's output is stored
+        __syncthreads();  // every lane is done with the previous tile's rows
         direct_load_tile(a, u0, 1, nvalid, nca, sta, A, lane);
         direct_load_tile(b, u0, cpb, nvalid, ncb, stb, B, lane);
         __syncthreads();
 
-        // one pass over all batches; the next batch's words load while this one runs
-        // (the table ends with one zero batch, so that load stays inside it)
+        // one pass over all batches, two buffers: the next batch's words load while this
+        // one runs (the table ends with two zero batches, so those loads stay inside it).
+        // Each lane stores its own output row; rows past nvalid fall outside the buffer.
+        const __amdgpu_buffer_rsrc_t dst = __builtin_amdgcn_make_buffer_rsrc(
+            out + u0 * nco, 0, nvalid * nco * static_cast<int>(sizeof(TIO)), kRawBufferWord3);
+        const int row = lane * nco;
         int o = 0, left = static_cast<int>(counts[0]);
         float acc0 = 0.f, acc1 = 0.f;
-        uint32_t cur[16];
+        auto next_output = [&]() {  // output o is complete
+            direct_store(dst, row + o, acc0 + acc1, out);
+            acc0 = acc1 = 0.f;
+            ++o;
+            left = static_cast<int>(counts[o]);
+        };
+        auto run = [&](const uint32_t* w) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) cur[i] = batches[i];
-        for (int j = 0; j < nbatch; ++j) {
-            while (left == 0) {  // output o is complete
-                Y[lane * sto + o] = acc0 + acc1;
-                acc0 = acc1 = 0.f;
-                ++o;
-                left = static_cast<int>(counts[o]);
+            for (int i = 0; i < 8; ++i) {
+                acc0 = fmaf(__uint_as_float(w[8 + 2 * i]), Arow[w[i] & 0xffu] * Brow[(w[i] >> 8) & 0xffu], acc0);
+                acc1 = fmaf(__uint_as_float(w[9 + 2 * i]), Arow[(w[i] >> 16) & 0xffu] * Brow[w[i] >> 24], acc1);
             }
-            uint32_t nxt[16];
+        };
+        uint32_t b0[24], b1[24];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) nxt[i] = batches[16 * (j + 1) + i];
+        for (int i = 0; i < 24; ++i) b0[i] = batches[i];
+        for (int j = 0; j < nbatch; j += 2) {
 #pragma unroll
-            for (int i = 0; i < 8; i += 2) {
-                const uint32_t w0 = cur[i], w1 = cur[i + 1];
-                acc0 = fmaf(__uint_as_float(cur[8 + i]), Arow[w0 & 0xffffu] * Brow[w0 >> 16], acc0);
-                acc1 = fmaf(__uint_as_float(cur[9 + i]), Arow[w1 & 0xffffu] * Brow[w1 >> 16], acc1);
-            }
+            for (int i = 0; i < 24; ++i) b1[i] = batches[24 * (j + 1) + i];
+            while (left == 0) next_output();
+            run(b0);
+            --left;
+            if (j + 1 >= nbatch) break;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) cur[i] = nxt[i];
+            for (int i = 0; i < 24; ++i) b0[i] = batches[24 * (j + 2) + i];
+            while (left == 0) next_output();
+            run(b1);
             --left;
         }
-        for (; o < nco; ++o) {  // the last output with entries, then those without
-            Y[lane * sto + o] = acc0 + acc1;
-            acc0 = acc1 = 0.f;
-        }
-        __syncthreads();
-
-        TIO* dst = out + u0 * nco;
-        const int n = nvalid * nco;
-        int r = lane / nco, c = lane - (lane / nco) * nco;
-        const int dr = kDirectUnits / nco, dc = kDirectUnits - (kDirectUnits / nco) * nco;
-        for (int e = lane; e < n; e += kDirectUnits) {
-            direct_store(dst + e, Y[r * sto + c]);
-            r += dr;
-            c += dc;
-            if (c >= nco) {
-                c -= nco;
-                ++r;
-            }
-        }
+        direct_store(dst, row + o, acc0 + acc1, out);  // the last output with entries
+        for (++o; o < nco; ++o) direct_store(dst, row + o, 0.f, out);  // then those without
     }
 }
 

@@ -49,16 +49,22 @@ constexpr int kPreBlockRows = 48;
 // (one wave) and the largest LDS tile it takes (160 KB).
 constexpr int kDirectUnits = 64;
 constexpr int kDirectMaxLdsFloats = 40960;
+// entries per batch of its table, and the longest row its 8-bit entry indices reach
+// (a row's zero column sits at index row length)
+constexpr int kDirectBatch = 16;
+constexpr int kDirectMaxRow = 254;
 // The direct kernel for an LDS tile of `lds_floats`; nullptr if it does not fit.
 const KernelEntry* find_direct_kernel(int lds_floats, int dtype);
 // Entry table of the direct kernel for one role of the tensor T[k1][k2][k3]:
 // role 0 (forward) A = x1, B = x2, output k3; role 1 (grad x1) A = grad_out,
 // B = x2, output k1; role 2 (grad x2) A = grad_out, B = x1, output k2.  Layout in
 // forward_direct.hip; entries per output in ascending (a, b) order, padded to
-// batches of 8 with zero entries on the zero column past each row.  *lds_floats:
-// the LDS the kernel needs for it.
+// batches of 16 with zero entries on the zero column past each row.  *lds_floats:
+// the LDS the kernel needs for it (its A and B tiles).
+// `dense`: the tensor of build_dense_tensor for these arguments if the caller has
+// it (built here otherwise).
 void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags, int role,
-                        std::vector<uint32_t>& out, int* lds_floats);
+                        std::vector<uint32_t>& out, int* lds_floats, const std::vector<double>* dense = nullptr);
 
 // Finds the instantiation for (L1, L2, Lout, spin mode, dtype); nullptr if none.
 // find_kernel returns the vector-ALU kernels, find_mfma_kernel the matrix-core

@@ -637,9 +637,10 @@ void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, u
 }
 
 void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags, int role,
-                        std::vector<uint32_t>& out, int* lds_floats) {
-    std::vector<double> T;
-    build_dense_tensor(L1, L2, LO, spins, n_spins, flags, T);
+                        std::vector<uint32_t>& out, int* lds_floats, const std::vector<double>* dense) {
+    std::vector<double> own;
+    if (dense == nullptr) build_dense_tensor(L1, L2, LO, spins, n_spins, flags, own);
+    const std::vector<double>& T = dense != nullptr ? *dense : own;
     const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
     const int nco = n_spins * (LO + 1) * (LO + 1);
     // (A, B, output) widths of the role and the index map from (a, b, o) to T
@@ -659,32 +660,34 @@ void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, u
     out[3] = static_cast<uint32_t>(sta);
     out[4] = static_cast<uint32_t>(stb);
     out[5] = static_cast<uint32_t>(sto);
+    out[7] = kDirectBatch;
     uint32_t nbatch = 0;
     for (int o = 0; o < no; ++o) {
-        std::vector<std::pair<uint32_t, float>> ent;
+        std::vector<std::pair<uint32_t, float>> ent;  // (a | b << 8, value)
         for (int a = 0; a < na; ++a)
             for (int b = 0; b < nb; ++b) {
                 const double v = at(a, b, o);
                 if (std::fabs(v) > 1e-12)  // the rest is quadrature round-off of exact zeros
-                    ent.emplace_back(static_cast<uint32_t>(a) | (static_cast<uint32_t>(b) << 16),
+                    ent.emplace_back(static_cast<uint32_t>(a) | (static_cast<uint32_t>(b) << 8),
                                      static_cast<float>(v));
             }
-        while (ent.size() % 8) ent.emplace_back(static_cast<uint32_t>(na) | (static_cast<uint32_t>(nb) << 16), 0.f);
-        const size_t batches = ent.size() / 8;
+        while (ent.size() % kDirectBatch) ent.emplace_back(static_cast<uint32_t>(na) | (static_cast<uint32_t>(nb) << 8), 0.f);
+        const size_t batches = ent.size() / kDirectBatch;
         out[8 + o] = static_cast<uint32_t>(batches);
         nbatch += static_cast<uint32_t>(batches);
         for (size_t q = 0; q < batches; ++q) {
-            for (int i = 0; i < 8; ++i) out.push_back(ent[q * 8 + i].first);
-            for (int i = 0; i < 8; ++i) {
+            const auto* e = &ent[q * kDirectBatch];
+            for (int i = 0; i < kDirectBatch / 2; ++i) out.push_back(e[2 * i].first | (e[2 * i + 1].first << 16));
+            for (int i = 0; i < kDirectBatch; ++i) {
                 uint32_t bits;
-                std::memcpy(&bits, &ent[q * 8 + i].second, 4);
+                std::memcpy(&bits, &e[i].second, 4);
                 out.push_back(bits);
             }
         }
     }
     out[6] = nbatch;
-    out.insert(out.end(), 16, 0u);  // a zero batch that the kernel's look-ahead load reads last
-    *lds_floats = kDirectUnits * (sta + stb + sto);
+    out.insert(out.end(), kDirectBatch * 3, 0u);  // two zero batches that the kernel's look-ahead loads reach
+    *lds_floats = kDirectUnits * (sta + stb);
 }
 
 }  // namespace spingtp
@@ -836,6 +839,8 @@ spingtp_status spingtp_direct_table_host(int L1, int L2, int Lout, const int* sp
     try {
         std::vector<uint32_t> w;
         int lds_floats = 0;
+        const int nmax = n_spins * (std::max(L1, std::max(L2, Lout)) + 1) * (std::max(L1, std::max(L2, Lout)) + 1);
+        if (nmax > spingtp::kDirectMaxRow) return SPINGTP_ERR_UNSUPPORTED;
         spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, role, w, &lds_floats);
         if (spingtp::find_direct_kernel(lds_floats, 0) == nullptr) return SPINGTP_ERR_UNSUPPORTED;
         *count = w.size();
@@ -884,9 +889,12 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     // whose transposed degrees have none, where its LDS tile fits
     auto odd_stride = [](int n) { return (n % 2) ? n + 2 : n + 1; };
     const int bsz = (L1 + 1) * (L1 + 1), bsz2 = (L2 + 1) * (L2 + 1), bszo = (Lout + 1) * (Lout + 1);
-    const int dir_lds =
-        spingtp::kDirectUnits * (odd_stride(n_spins * bsz) + odd_stride(n_spins * bsz2) + odd_stride(n_spins * bszo));
-    const spingtp::KernelEntry* kd = spingtp::find_direct_kernel(dir_lds, static_cast<int>(dtype));
+    // (the LDS holds two of the three rows; every role pairs a different two, so size for the largest pair,
+    // and the entry indices are 8-bit)
+    const int r1 = odd_stride(n_spins * bsz), r2 = odd_stride(n_spins * bsz2), ro = odd_stride(n_spins * bszo);
+    const int dir_lds = spingtp::kDirectUnits * (r1 + r2 + ro - std::min(r1, std::min(r2, ro)));
+    const bool dir_idx_ok = n_spins * std::max(bsz, std::max(bsz2, bszo)) <= spingtp::kDirectMaxRow;
+    const spingtp::KernelEntry* kd = dir_idx_ok ? spingtp::find_direct_kernel(dir_lds, static_cast<int>(dtype)) : nullptr;
     const bool fourier_bwd = k != nullptr && L1 == L2 && L2 == Lout;
     if (k == nullptr) k = kd;
     const spingtp::KernelEntry* kv1 = nullptr;
@@ -909,11 +917,14 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     try {
         if (spin_mode < 2 && !spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
         int lds_floats = 0;
+        std::vector<double> dense;  // built once for the direct kernel's tables
+        if ((k != nullptr && k->family == 6) || (kd != nullptr && !fourier_bwd))
+            spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, basis, dense);
         if (k != nullptr && k->family == 6)
-            spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 0, dir, &lds_floats);
+            spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 0, dir, &lds_floats, &dense);
         if (kd != nullptr && !fourier_bwd) {
-            spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 1, dir_b1, &lds_floats);
-            spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 2, dir_b2, &lds_floats);
+            spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 1, dir_b1, &lds_floats, &dense);
+            spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 2, dir_b2, &lds_floats, &dense);
         }
         if (k != nullptr && k->family == 4) spingtp::build_mfma_operands(L1, aux);
         if (kv1->family == 5) spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre);

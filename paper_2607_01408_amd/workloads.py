@@ -15,7 +15,11 @@ matter -- the paper's molecular datasets are not needed and none are read):
   catalyst  L=8,  N=400,000, C=128, bf16 in / fp32 accumulate, N(0,1)  seeds 4001/4002
             (~80 atoms x <=40 neighbours x 128 graphs)
   sweep     L in {2,4,8,12,16}, N=8,192, C=32, fp32, N(0,1)          seeds 5001+L/5101+L
-Layout [N, C, n_spins, (L+1)^2] with spins (-1, 0, +1).
+  chiral    L=2, spins (-2..2), N=200,000, C=64, fp32, N(0,1)          seeds 6001/6002
+            (the s_max = 2, L_max = 2 setting of the chirality experiments,
+            App. F: small organic molecules, 64 channels)
+Layout [N, C, n_spins, (L+1)^2] with spins (-1, 0, +1) unless a workload names
+its own.
 """
 
 import math
@@ -28,6 +32,8 @@ WORKLOADS = {
     "organic": dict(L=6, N=100_000, C=128, dtypes=("fp32", "bf16"), scale="unit", seeds=(3001, 3002)),
     "catalyst": dict(L=8, N=400_000, C=128, dtypes=("bf16",), scale="unit", seeds=(4001, 4002)),
     "sweep": dict(L=(2, 4, 8, 12, 16), N=8_192, C=32, dtypes=("fp32",), scale="unit", seeds=(5001, 5101)),
+    "chiral": dict(L=2, N=200_000, C=64, dtypes=("fp32",), scale="unit", seeds=(6001, 6002),
+                   spins=(-2, -1, 0, 1, 2)),
 }
 
 _CHUNK_UNITS = 1 << 20  # units drawn per generator seed
@@ -79,7 +85,8 @@ def make_pair(name, dtype=None, L=None, device="cuda", N=None, C=None):
     dtype = dtype or w["dtypes"][0]
     N = N or w["N"]
     C = C or w["C"]
-    x1 = draw(L, N, C, s1, dtype, SPINS, w["scale"], device)
-    x2 = draw(L, N, C, s2, dtype, SPINS, w["scale"], device)
-    meta = dict(workload=name, L=L, N=N, C=C, dtype=dtype, scale=w["scale"], seeds=(s1, s2))
+    spins = w.get("spins", SPINS)
+    x1 = draw(L, N, C, s1, dtype, spins, w["scale"], device)
+    x2 = draw(L, N, C, s2, dtype, spins, w["scale"], device)
+    meta = dict(workload=name, L=L, N=N, C=C, dtype=dtype, scale=w["scale"], seeds=(s1, s2), spins=spins)
     return x1, x2, meta

@@ -563,16 +563,19 @@ def test_backward_pre_table_reproduces_oracle(built_library, L, spins, basis):
 
 def emulate_direct_kernel(words, A, B):
     """The direct kernel (family 6) on the CPU from its exact table words: per
-    output slot, its 8-entry batches in order, products A[a] * B[b] rounded to fp32
-    and added with one fp32 fma each into two alternating sums (entries 0, 2, 4, 6
+    output slot, its 16-entry batches in order, products A[a] * B[b] rounded to
+    fp32 and added with one fp32 fma each into two alternating sums (even entries
     of a batch to the first), which are added at the end of the slot."""
-    na, nb, no, sta, stb, sto, nbatch = (int(v) for v in words[:7])
+    na, nb, no, sta, stb, sto, nbatch, per = (int(v) for v in words[:8])
+    assert per == 16
     counts = words[8:8 + no].astype(np.int64)
     assert counts.sum() == nbatch
     body = words[8 + no:]
-    assert body.size == 16 * (nbatch + 1) and not body[16 * nbatch:].any()  # the trailing zero batch
-    batches = body[:16 * nbatch].reshape(nbatch, 16)
-    ent, val = batches[:, :8], batches[:, 8:].copy().view(np.float32)
+    assert body.size == 24 * (nbatch + 2) and not body[24 * nbatch:].any()  # the trailing zero batches
+    batches = body[:24 * nbatch].reshape(nbatch, 24)
+    idx = np.stack([batches[:, :8] & 0xFFFF, batches[:, :8] >> 16], axis=2).reshape(nbatch, 16)
+    ent = (idx & 0xFF) | ((idx >> 8) << 16)  # as a | b << 16
+    val = batches[:, 8:].copy().view(np.float32)
     U = A.shape[0]
     Az = np.zeros((U, sta), dtype=np.float32)
     Bz = np.zeros((U, stb), dtype=np.float32)
@@ -582,7 +585,7 @@ def emulate_direct_kernel(words, A, B):
     for o in range(no):
         acc = [np.zeros(U, dtype=np.float32), np.zeros(U, dtype=np.float32)]
         for _ in range(counts[o]):
-            for i in range(8):
+            for i in range(16):
                 a, b = int(ent[q, i] & 0xFFFF), int(ent[q, i] >> 16)
                 p = (Az[:, a] * Bz[:, b]).astype(np.float32)
                 acc[i % 2] = (val[q, i].astype(np.float64) * p + acc[i % 2]).astype(np.float32)
@@ -617,13 +620,14 @@ def test_direct_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis)
                                                 (g, x1, r2, (no, n1, n2))]):
         w = direct_table_host(L1, L2, LO, spins, basis, role)
         na, nb, nout, sta, stb, sto, nbatch = (int(v) for v in w[:7])
-        assert (na, nb, nout) == widths and w[7] == 0
+        assert (na, nb, nout) == widths and w[7] == 16
         for n, st in ((na, sta), (nb, stb), (nout, sto)):
             assert st % 2 == 1 and st > n
-        ent = w[8 + nout:8 + nout + 16 * nbatch].reshape(nbatch, 16)[:, :8].ravel()
-        val = w[8 + nout:8 + nout + 16 * nbatch].reshape(nbatch, 16)[:, 8:].copy().view(np.float32).ravel()
+        body = w[8 + nout:8 + nout + 24 * nbatch].reshape(nbatch, 24)
+        ent = np.stack([body[:, :8] & 0xFFFF, body[:, :8] >> 16], axis=2).ravel()
+        val = body[:, 8:].copy().view(np.float32).ravel()
         pad = val == 0
-        assert np.all(ent[pad] == (na | (nb << 16)))
+        assert np.all(ent[pad] == (na | (nb << 8)))
         # the entries are the nonzeros of T in this role (k1, k2, k3 permuted)
         perm = [(0, 1, 2), (2, 1, 0), (2, 0, 1)][role]
         Tr = np.transpose(T, perm)  # [a][b][o] with a, b, o the role's indices
@@ -642,8 +646,8 @@ def test_direct_table_argument_checks(built_library):
     assert built_library.spingtp_direct_table_host(2, 2, 2, S, 5, 0, 3, None, 0, ctypes.byref(count)) == 1
     assert built_library.spingtp_direct_table_host(2, 2, 2, S, 5, 0, -1, None, 0, ctypes.byref(count)) == 1
     assert built_library.spingtp_direct_table_host(2, 2, 2, S, 5, 0, 0, None, 0, None) == 1
-    # a tile beyond the kernel's LDS: 64 x 3 x 247 floats at degree 6 with spins {-2..2}
-    assert built_library.spingtp_direct_table_host(6, 6, 6, S, 5, 0, 0, None, 0, ctypes.byref(count)) == 2
+    # rows beyond the 8-bit entry indices: 320 slots at degree 7 with spins {-2..2}
+    assert built_library.spingtp_direct_table_host(7, 7, 7, S, 5, 0, 0, None, 0, ctypes.byref(count)) == 2
     assert built_library.spingtp_direct_table_host(2, 2, 2, S, 5, 0, 0, None, 0, ctypes.byref(count)) == 0
     assert count.value > 8
     # the Fourier tables do not exist for spins {-2..2}

@@ -117,10 +117,16 @@ def test_direct_bitwise_deterministic():
     assert torch.equal(plan.forward(x1, x2), plan.forward(x1, x2))
 
 
-def test_spin2_unsupported_beyond_the_tile():
-    # degree 6 with spins {-2..2}: the tile exceeds the direct kernel's LDS and no other kernel exists
+def test_spin2_unsupported_beyond_the_rows():
+    # degree 7 with spins {-2..2}: rows of 320 slots exceed the direct kernel's 8-bit entry indices and no
+    # other kernel exists
     with pytest.raises(SpinGTPError):
-        Plan(6, 6, 6, S5, "fp32")
+        Plan(7, 7, 7, S5, "fp32")
+
+
+def test_spin2_degree_5():
+    # the largest rows below the index limit that the tests cover (180 slots; 0.6 MB entry table)
+    run_forward(5, 5, 5, S5, 9, 3, "fp32", 0, seed=5)
 
 
 # --- forward_v1 with spins {-2..2}: the precontracted kernel ---
