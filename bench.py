@@ -507,8 +507,8 @@ def main():
         from paper_2607_01408_amd import direct_table_host
 
         w = direct_table_host(L, L, L, spins, BASES[args.basis], 0)
-        nco, nbatch = int(w[2]), int(w[6])
-        vals = w[8 + nco:8 + nco + 24 * nbatch].reshape(nbatch, 24)[:, 8:]
+        nco, nbatch, hdr = int(w[2]), int(w[6]), 18
+        vals = w[hdr + nco:hdr + nco + 24 * nbatch].reshape(nbatch, 24)[:, 8:]
         flops_unit = 3 * int((vals != 0).sum())
     else:
         flops_unit = route_flops(L, L, L, True)

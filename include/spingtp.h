@@ -328,7 +328,10 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
  *   [0, 8)         NCA, NCB, NCO (widths of A, B, out), STA, STB, STO (odd LDS
  *                  row strides, each above its width: column NCA of A and NCB
  *                  of B hold 0), NBATCH, 16 (entries per batch);
- *   [8, 8 + NCO)   batches per output slot, in output order;
+ *   [8, 13)        output-slot boundaries o_0 = 0 <= ... <= o_4 = NCO of the four
+ *                  waves of a workgroup (wave w computes slots [o_w, o_(w+1)));
+ *   [13, 18)       the first batch of each wave's range, and NBATCH;
+ *   [18, 18 + NCO) batches per output slot, in output order;
  *   then NBATCH batches of 24 words: 8 index words (entry 2i in the low 16 bits
  *   of word i, entry 2i + 1 in the high 16 bits, each a | b << 8), then the 16
  *   fp32 values (bits); and 48 zero words.  out[o] = sum over the entries of

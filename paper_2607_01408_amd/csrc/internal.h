@@ -48,6 +48,8 @@ constexpr int kPreBlockRows = 48;
 // Direct sparse-tensor kernel (family 6, forward_direct.hip): units per workgroup
 // (one wave) and the largest LDS tile it takes (160 KB).
 constexpr int kDirectUnits = 64;
+constexpr int kDirectWaves = 4;  // waves of a workgroup, sharing its tile, each with a range of outputs
+constexpr int kDirectThreads = 64 * kDirectWaves;
 constexpr int kDirectMaxLdsFloats = 40960;
 // entries per batch of its table, and the longest row its 8-bit entry indices reach
 // (a row's zero column sits at index row length)

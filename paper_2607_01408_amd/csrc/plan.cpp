@@ -653,7 +653,8 @@ void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, u
     };
     auto odd_stride = [](int n) { return (n % 2) ? n + 2 : n + 1; };  // odd, with a zero column at n
     const int sta = odd_stride(na), stb = odd_stride(nb), sto = odd_stride(no);
-    out.assign(8 + no, 0u);
+    const int hdr = 8 + 2 * (kDirectWaves + 1);  // + output and batch boundaries of the waves
+    out.assign(hdr + no, 0u);
     out[0] = static_cast<uint32_t>(na);
     out[1] = static_cast<uint32_t>(nb);
     out[2] = static_cast<uint32_t>(no);
@@ -673,7 +674,7 @@ void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, u
             }
         while (ent.size() % kDirectBatch) ent.emplace_back(static_cast<uint32_t>(na) | (static_cast<uint32_t>(nb) << 8), 0.f);
         const size_t batches = ent.size() / kDirectBatch;
-        out[8 + o] = static_cast<uint32_t>(batches);
+        out[hdr + o] = static_cast<uint32_t>(batches);
         nbatch += static_cast<uint32_t>(batches);
         for (size_t q = 0; q < batches; ++q) {
             const auto* e = &ent[q * kDirectBatch];
@@ -687,6 +688,26 @@ void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, u
     }
     out[6] = nbatch;
     out.insert(out.end(), kDirectBatch * 3, 0u);  // two zero batches that the kernel's look-ahead loads reach
+    // wave w takes the whole output slots [o_w, o_(w+1)), cut where the running batch count
+    // passes w+1 quarters of the total
+    uint32_t seen = 0;
+    int w = 1;
+    out[8] = 0;
+    out[8 + kDirectWaves + 1] = 0;
+    for (int o = 0; o < no && w < kDirectWaves; ++o) {
+        seen += out[hdr + o];
+        while (w < kDirectWaves && static_cast<uint64_t>(seen) * kDirectWaves >= static_cast<uint64_t>(nbatch) * w) {
+            out[8 + w] = static_cast<uint32_t>(o + 1);
+            out[8 + kDirectWaves + 1 + w] = seen;
+            ++w;
+        }
+    }
+    for (; w < kDirectWaves; ++w) {  // fewer slots than waves
+        out[8 + w] = static_cast<uint32_t>(no);
+        out[8 + kDirectWaves + 1 + w] = nbatch;
+    }
+    out[8 + kDirectWaves] = static_cast<uint32_t>(no);
+    out[8 + 2 * kDirectWaves + 1] = nbatch;
     *lds_floats = kDirectUnits * (sta + stb);
 }
 

@@ -568,9 +568,14 @@ def emulate_direct_kernel(words, A, B):
     of a batch to the first), which are added at the end of the slot."""
     na, nb, no, sta, stb, sto, nbatch, per = (int(v) for v in words[:8])
     assert per == 16
-    counts = words[8:8 + no].astype(np.int64)
+    W = 4  # waves per workgroup, each with a contiguous range of output slots
+    oseg, bseg = words[8:8 + W + 1].astype(np.int64), words[8 + W + 1:8 + 2 * W + 2].astype(np.int64)
+    hdr = 8 + 2 * (W + 1)
+    counts = words[hdr:hdr + no].astype(np.int64)
     assert counts.sum() == nbatch
-    body = words[8 + no:]
+    assert oseg[0] == 0 and oseg[-1] == no and np.all(np.diff(oseg) >= 0)
+    assert np.array_equal(bseg, np.concatenate([[0], np.cumsum(counts)])[oseg])  # batch start of each range
+    body = words[hdr + no:]
     assert body.size == 24 * (nbatch + 2) and not body[24 * nbatch:].any()  # the trailing zero batches
     batches = body[:24 * nbatch].reshape(nbatch, 24)
     idx = np.stack([batches[:, :8] & 0xFFFF, batches[:, :8] >> 16], axis=2).reshape(nbatch, 16)
@@ -623,7 +628,11 @@ def test_direct_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis)
         assert (na, nb, nout) == widths and w[7] == 16
         for n, st in ((na, sta), (nb, stb), (nout, sto)):
             assert st % 2 == 1 and st > n
-        body = w[8 + nout:8 + nout + 24 * nbatch].reshape(nbatch, 24)
+        hdr = 18
+        body = w[hdr + nout:hdr + nout + 24 * nbatch].reshape(nbatch, 24)
+        # the four waves' shares of the batches are balanced (whole output slots each)
+        shares = np.diff(w[13:18].astype(np.int64))
+        assert shares.max() <= nbatch / 4 + w[hdr:hdr + nout].max()
         ent = np.stack([body[:, :8] & 0xFFFF, body[:, :8] >> 16], axis=2).ravel()
         val = body[:, 8:].copy().view(np.float32).ravel()
         pad = val == 0
