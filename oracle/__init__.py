@@ -17,7 +17,9 @@ The oracle computes the plain definition of the operation and nothing else:
                    a = Q x, written as an explicit sparse tensor T (paper
                    Sec. 3.5, eq. spin_gtp with unit weights and the elementwise
                    channel mode of App. E.1); ``vjp`` / ``spingtp_vjp`` give its
-                   reverse-mode derivative by the chain rule on that definition.
+                   reverse-mode derivative by the chain rule on that definition;
+                   ``PathWeightedTensor`` scales it by one weight per path
+                   (block triple) of eq. spin_gtp.
 
 Readings of points where the paper is silent or ambiguous are listed in the
 docstrings of the functions that take them.  Every function here is pinned by
@@ -28,11 +30,11 @@ library routines (scipy, sympy).
 from .swsh import swsh, theta_part, goldberg_prefactor
 from .realbasis import q_matrix, real_index, conjugation_map, parity_mix, BASIS_PAPER, BASIS_M0_PAIRED, BASIS_PARITY
 from .gaunt import gauss_legendre_grid, gaunt_block, gaunt_full_quadrature
-from .spingtp import RealGauntTensor, spingtp, spingtp_vjp
+from .spingtp import RealGauntTensor, PathWeightedTensor, slot_blocks, spingtp, spingtp_vjp
 
 __all__ = [
     "swsh", "theta_part", "goldberg_prefactor",
     "q_matrix", "real_index", "parity_mix", "BASIS_PAPER", "BASIS_M0_PAIRED", "BASIS_PARITY",
     "gauss_legendre_grid", "gaunt_block", "gaunt_full_quadrature",
-    "RealGauntTensor", "spingtp",
+    "RealGauntTensor", "PathWeightedTensor", "slot_blocks", "spingtp",
 ]

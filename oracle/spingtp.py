@@ -203,3 +203,51 @@ def spingtp(x1, x2, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER) -> np.nda
 def spingtp_vjp(x1, x2, g, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
     """Oracle gradients (gx1, gx2) of sum(g * spingtp(x1, x2)) (float64)."""
     return _cached_tensor(L1, L2, Lout, tuple(spins), basis).vjp(x1, x2, g)
+
+
+def slot_blocks(spins, L) -> np.ndarray:
+    """Block label of every slot of a [n_spins][(L+1)^2] vector: the irrep block
+    (spin index i, degree l) as i (L+1) + l, and -1 on the slots with l < |s|.
+
+    In the parity-labelled basis these blocks are the irreps (l, |s|, p) of the
+    paper (Sec. 3.4; the -|s| block holds p = +1, the +|s| block p = -1); in the
+    other bases they are the (signed spin, degree) sectors of the layout."""
+    spins = tuple(spins)
+    out = np.full(len(spins) * (L + 1) ** 2, -1, dtype=np.int64)
+    for i, s in enumerate(spins):
+        for l in range(abs(s), L + 1):
+            out[i * (L + 1) ** 2 + l * l:i * (L + 1) ** 2 + (l + 1) ** 2] = i * (L + 1) + l
+    return out
+
+
+class PathWeightedTensor:
+    """The instruction-weighted product of eq. spin_gtp (Sec. 3.4) with one weight
+    per path (block triple rho1, rho2 -> rho3) shared by all channels:
+    T_W[k1,k2,k3] = W[path(k1,k2,k3)] T[k1,k2,k3], path(k) = (block(k1), block(k2),
+    block(k3)) of ``slot_blocks``.
+
+    Paths are the block triples on which T has a nonzero entry, in ascending
+    lexicographic order; ``weights`` holds one value per path in that order.
+    Reading: the paper's W_uvw also mixes channels; this is its per-path part
+    with the channel wiring of the unweighted product (elementwise, one weight
+    for every channel)."""
+
+    def __init__(self, L1, L2, Lout, spins, basis=BASIS_PAPER, weights=None):
+        self.base = _cached_tensor(L1, L2, Lout, tuple(spins), basis)
+        b = self.base
+        M = b.matrix.tocoo()
+        k1, k2 = M.row // b.n2, M.row % b.n2
+        trip = np.stack([slot_blocks(spins, L1)[k1], slot_blocks(spins, L2)[k2],
+                         slot_blocks(spins, Lout)[M.col]], axis=1)
+        self.paths, index = np.unique(trip, axis=0, return_inverse=True)
+        index = np.asarray(index).ravel()
+        w = np.ones(len(self.paths)) if weights is None else np.asarray(weights, dtype=np.float64)
+        if w.shape != (len(self.paths),):
+            raise ValueError(f"{len(self.paths)} path weights expected")
+        self.matrix = sp.csr_matrix((M.data * w[index], (M.row, M.col)), shape=M.shape)
+        self.L1, self.L2, self.Lout, self.spins = L1, L2, Lout, tuple(spins)
+        self.n1, self.n2, self.n3 = b.n1, b.n2, b.n3
+
+    dense = RealGauntTensor.dense
+    apply = RealGauntTensor.apply
+    vjp = RealGauntTensor.vjp

@@ -1,0 +1,83 @@
+"""Pins of the oracle's path-weighted product (eq. spin_gtp, Sec. 3.4).
+
+The weighted tensor scales each entry of the unweighted T by the weight of its
+path (block triple rho1, rho2 -> rho3).  Pinned against the unweighted oracle
+(itself pinned to the paper) through properties a wrong block label, a dropped
+path or a transposed role would break:
+* unit weights reproduce the unweighted product exactly;
+* the weight of one path alone gives the unweighted product of the inputs masked
+  to that path's input blocks, read on its output block;
+* the single-path products add up to the unweighted product (the paths partition
+  T), and the product is linear in the weights;
+* the gradients satisfy the bilinear identity <g, y> = <gx1, x1> = <gx2, x2>;
+* every path obeys the degree triangle and the spin rule s3 = s1 + s2 of some
+  signed spins of its blocks.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle.spingtp import slot_blocks
+from tests.oracle_helpers import valid_mask
+
+S3 = (-1, 0, 1)
+S5 = (-2, -1, 0, 1, 2)
+CASES = [(2, 2, 2, S3, 0), (2, 1, 3, S3, 1), (2, 2, 2, S3, 2), (1, 2, 2, S5, 0), (2, 2, 2, S5, 2), (3, 2, 1, (0,), 0)]
+
+
+def draw(spins, L, n, seed):
+    return np.random.default_rng(seed).standard_normal((n, len(spins) * (L + 1) ** 2)) * valid_mask(spins, L)
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CASES)
+def test_unit_weights_are_the_unweighted_product(L1, L2, LO, spins, basis):
+    W = oracle.PathWeightedTensor(L1, L2, LO, spins, basis)
+    x1, x2 = draw(spins, L1, 5, 1), draw(spins, L2, 5, 2)
+    assert np.array_equal(W.apply(x1, x2), W.base.apply(x1, x2))
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CASES)
+def test_one_path_is_the_block_restricted_product(L1, L2, LO, spins, basis):
+    W0 = oracle.PathWeightedTensor(L1, L2, LO, spins, basis)
+    P = W0.paths
+    b1, b2, b3 = slot_blocks(spins, L1), slot_blocks(spins, L2), slot_blocks(spins, LO)
+    x1, x2 = draw(spins, L1, 4, 3), draw(spins, L2, 4, 4)
+    rng = np.random.default_rng(len(P))
+    total = np.zeros((4, len(spins) * (LO + 1) ** 2))
+    for p in range(len(P)):
+        w = np.zeros(len(P))
+        w[p] = 1.0
+        y = oracle.PathWeightedTensor(L1, L2, LO, spins, basis, w).apply(x1, x2).reshape(4, -1)
+        total += y
+        if p in set(rng.choice(len(P), size=min(12, len(P)), replace=False).tolist()):
+            ref = W0.base.apply(x1 * (b1 == P[p, 0]), x2 * (b2 == P[p, 1])).reshape(4, -1) * (b3 == P[p, 2])
+            assert np.abs(y - ref).max() <= 1e-13 * max(1.0, np.abs(ref).max())
+    assert np.abs(total - W0.base.apply(x1, x2).reshape(4, -1)).max() <= 1e-12
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CASES)
+def test_linear_in_the_weights_and_gradients(L1, L2, LO, spins, basis):
+    n = len(oracle.PathWeightedTensor(L1, L2, LO, spins, basis).paths)
+    rng = np.random.default_rng(n)
+    wa, wb = rng.standard_normal(n), rng.standard_normal(n)
+    A = oracle.PathWeightedTensor(L1, L2, LO, spins, basis, wa)
+    B = oracle.PathWeightedTensor(L1, L2, LO, spins, basis, wb)
+    C = oracle.PathWeightedTensor(L1, L2, LO, spins, basis, 2.0 * wa - 3.0 * wb)
+    x1, x2 = draw(spins, L1, 3, 5), draw(spins, L2, 3, 6)
+    g = draw(spins, LO, 3, 7)
+    assert np.abs(C.apply(x1, x2) - (2.0 * A.apply(x1, x2) - 3.0 * B.apply(x1, x2))).max() <= 1e-12
+    gx1, gx2 = A.vjp(x1, x2, g)
+    e = float((g * A.apply(x1, x2).reshape(3, -1)).sum())
+    assert abs(float((gx1 * x1).sum()) - e) <= 1e-12 * max(1.0, abs(e))
+    assert abs(float((gx2 * x2).sum()) - e) <= 1e-12 * max(1.0, abs(e))
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CASES)
+def test_paths_obey_the_selection_rules(L1, L2, LO, spins, basis):
+    P = oracle.PathWeightedTensor(L1, L2, LO, spins, basis).paths
+    assert len(P) == len({tuple(p) for p in P.tolist()})
+    for i1, i2, i3 in P.tolist():
+        (s1, l1), (s2, l2), (s3, l3) = ((spins[i // (L + 1)], i % (L + 1)) for i, L in ((i1, L1), (i2, L2), (i3, LO)))
+        assert abs(l1 - l2) <= l3 <= l1 + l2
+        assert any(a * s1 + b * s2 == c * s3 for a in (1, -1) for b in (1, -1) for c in (1, -1))
