@@ -126,6 +126,38 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
                                    spingtp_dtype dtype, unsigned flags, spingtp_plan* out_plan);
 
 /*
+ * Paths of the instruction-weighted product (Sec. 3.4 eq. spin_gtp): the block
+ * triples (rho1, rho2 -> rho3) on which the tensor T of spingtp_dense_tensor_host
+ * has a nonzero entry.  A block is the set of slots of one spin index i and degree
+ * l, labelled i (L+1) + l with the L of its input or output (in the parity basis
+ * these blocks are the irreps (l, |s|, p) of the paper).  Host only, no GPU; same
+ * argument rules as spingtp_plan_create.  Writes min(capacity, total) triples
+ * (b1, b2, b3), 3 ints each, to `triples` (may be NULL when capacity is 0) in
+ * ascending lexicographic order and the total to *count.
+ */
+spingtp_status spingtp_paths_host(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
+                                  int* triples, size_t capacity, size_t* count);
+
+/*
+ * A plan for the path-weighted product y[k3] = sum W[path(k1,k2,k3)] T[k1][k2][k3]
+ * x1[k1] x2[k2]: one weight per path of spingtp_paths_host, in its order, shared
+ * by every channel (the per-instruction weights of Sec. 3.4 eq. spin_gtp in the
+ * elementwise channel mode; channel mixing is not part of this call).  weights:
+ * host float64 array of n_weights finite values; n_weights must equal the path
+ * count, else SPINGTP_ERR_INVALID_ARG.  The weights are folded into the plan's
+ * tensor tables, so a plan holds one weight set.  Routes: spingtp_forward and both
+ * gradients on the direct kernel (family 6), spingtp_forward_v1 on the
+ * precontracted kernel where built (else the direct kernel); the Fourier kernels
+ * compute the unweighted sum over all paths and are not used
+ * (SPINGTP_V1_FOURIER gives SPINGTP_ERR_UNSUPPORTED).  Shapes the direct kernel
+ * does not fit give a plan for spingtp_forward_v1 only, or
+ * SPINGTP_ERR_UNSUPPORTED.  Otherwise as spingtp_plan_create.
+ */
+spingtp_status spingtp_plan_create_weighted(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                            spingtp_dtype dtype, unsigned flags, const double* weights,
+                                            size_t n_weights, spingtp_plan* out_plan);
+
+/*
  * out = SpinGTP(x1, x2) for N*C units, asynchronously on `stream` (a hipStream_t;
  * NULL = the null stream of the plan's device).
  *   x1, x2, out: device pointers of the plan's dtype in the layout above, each

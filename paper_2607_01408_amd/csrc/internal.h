@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <array>
 #include <cstdint>
 #include <vector>
 
@@ -94,8 +95,9 @@ const KernelEntry* find_pre_kernel_large(int ks, int nt, int dtype);
 // every entry has one writer; lists are padded with zero items.
 // conj_x2: the table of spingtp_backward_v1, whose kernel reads x2 but must use
 // J x2 (build_conj_map); false if J cannot be built.
+// dense: the tensor to tabulate (the plan's, e.g. path-weighted); built here when nullptr.
 bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
-                      std::vector<uint32_t>& out, bool conj_x2 = false);
+                      std::vector<uint32_t>& out, bool conj_x2 = false, const std::vector<double>* dense = nullptr);
 
 // Per-lane A operands of the matrix-core kernel for L1 = L2 = Lout = L, spins
 // {-1, 0, +1}: packed fp16 (hi, lo) words; layout in forward_mfma.hip.
@@ -125,6 +127,16 @@ bool build_conj_map(int L, const int* spins, int n_spins, unsigned flags, std::v
 spingtp_status run_forward(spingtp_plan plan, const KernelEntry* k, const void* x1, const void* x2, void* out,
                            int64_t N, int64_t C, bool shared_x2, void* stream, const float* tab = nullptr,
                            bool backward = false, const uint32_t* aux = nullptr);
+
+// Paths of the instruction-weighted product (spingtp_paths_host): the block triples
+// (i (L+1) + l of spin index i and degree l, per input and output) on which T has
+// a nonzero entry, in ascending lexicographic order.
+void tensor_paths(int L1, int L2, int LO, const int* spins, int n_spins, const std::vector<double>& T,
+                  std::vector<std::array<int, 3>>& paths);
+// T[k1][k2][k3] *= w[p] with p the path of (k1, k2, k3); entries at quadrature
+// round-off level are set to 0.
+void weight_paths(int L1, int L2, int LO, const int* spins, int n_spins, const std::vector<std::array<int, 3>>& paths,
+                  const double* w, std::vector<double>& T);
 
 // Dense real tensor of the operation (see spingtp_dense_tensor_host), float64.
 void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,

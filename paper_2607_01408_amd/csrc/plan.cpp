@@ -10,7 +10,10 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
+#include <map>
+#include <set>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -459,9 +462,10 @@ void build_mfma_operands(int L, std::vector<uint32_t>& out) {
 }
 
 bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
-                      std::vector<uint32_t>& out, bool conj_x2) {
-    std::vector<double> T;
-    build_dense_tensor(L1, L2, LO, spins, n_spins, flags, T);
+                      std::vector<uint32_t>& out, bool conj_x2, const std::vector<double>* dense) {
+    std::vector<double> own;
+    if (dense == nullptr) build_dense_tensor(L1, L2, LO, spins, n_spins, flags, own);
+    const std::vector<double>& T = dense != nullptr ? *dense : own;
     // conj_x2: the kernel reads x2 but must use J x2 (spingtp_backward_v1), so
     // each item's k2 becomes J's source slot and its value takes J's sign
     std::vector<uint32_t> J;
@@ -633,6 +637,49 @@ void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, u
                                     }
                                 }
                         }
+            }
+}
+
+// Block label of each slot of a row of degree L: i (L+1) + l for spin index i and
+// degree l, -1 on the slots with l < |s|.
+std::vector<int> slot_blocks(int L, const int* spins, int n_spins) {
+    const int nb = (L + 1) * (L + 1);
+    std::vector<int> out(static_cast<size_t>(n_spins) * nb, -1);
+    for (int i = 0; i < n_spins; ++i)
+        for (int l = std::abs(spins[i]); l <= L; ++l)
+            for (int q = l * l; q < (l + 1) * (l + 1); ++q) out[static_cast<size_t>(i) * nb + q] = i * (L + 1) + l;
+    return out;
+}
+
+void tensor_paths(int L1, int L2, int LO, const int* spins, int n_spins, const std::vector<double>& T,
+                  std::vector<std::array<int, 3>>& paths) {
+    const std::vector<int> b1 = slot_blocks(L1, spins, n_spins), b2 = slot_blocks(L2, spins, n_spins),
+                           b3 = slot_blocks(LO, spins, n_spins);
+    const size_t n2 = b2.size(), n3 = b3.size();
+    std::set<std::array<int, 3>> seen;
+    for (size_t k1 = 0; k1 < b1.size(); ++k1)
+        for (size_t k2 = 0; k2 < n2; ++k2)
+            for (size_t k3 = 0; k3 < n3; ++k3)
+                if (std::fabs(T[(k1 * n2 + k2) * n3 + k3]) > 1e-12) seen.insert({b1[k1], b2[k2], b3[k3]});
+    paths.assign(seen.begin(), seen.end());  // std::set orders lexicographically
+}
+
+void weight_paths(int L1, int L2, int LO, const int* spins, int n_spins, const std::vector<std::array<int, 3>>& paths,
+                  const double* w, std::vector<double>& T) {
+    const std::vector<int> b1 = slot_blocks(L1, spins, n_spins), b2 = slot_blocks(L2, spins, n_spins),
+                           b3 = slot_blocks(LO, spins, n_spins);
+    const size_t n2 = b2.size(), n3 = b3.size();
+    std::map<std::array<int, 3>, double> weight;
+    for (size_t p = 0; p < paths.size(); ++p) weight[paths[p]] = w[p];
+    for (size_t k1 = 0; k1 < b1.size(); ++k1)
+        for (size_t k2 = 0; k2 < n2; ++k2)
+            for (size_t k3 = 0; k3 < n3; ++k3) {
+                double& v = T[(k1 * n2 + k2) * n3 + k3];
+                if (std::fabs(v) <= 1e-12) {
+                    v = 0.0;  // quadrature round-off of an exact zero
+                    continue;
+                }
+                v *= weight.at({b1[k1], b2[k2], b3[k3]});
             }
 }
 
@@ -891,18 +938,23 @@ spingtp_status spingtp_conj_map_host(int L, const int* spins, int n_spins, unsig
     return SPINGTP_OK;
 }
 
-spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, int n_spins,
-                                   spingtp_dtype dtype, unsigned flags, spingtp_plan* out_plan) {
+// weights: one per path of spingtp_paths_host (n_weights of them), or nullptr for the
+// unweighted product.
+static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, int n_spins, spingtp_dtype dtype,
+                                  unsigned flags, const double* weights, size_t n_weights, spingtp_plan* out_plan) {
     if (out_plan == nullptr) return SPINGTP_ERR_INVALID_ARG;
     *out_plan = nullptr;
     int spin_mode = 0;
     spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
     if (dtype != SPINGTP_FP32 && dtype != SPINGTP_BF16) return SPINGTP_ERR_INVALID_ARG;
+    const bool weighted = weights != nullptr;
+    // weighted plans: the Fourier route computes the unweighted sum over all paths at once
+    if (weighted && (flags & SPINGTP_V1_FOURIER)) return SPINGTP_ERR_UNSUPPORTED;
     const spingtp::KernelEntry* k = nullptr;
-    if ((flags & SPINGTP_KERNEL_VALU) == 0)
+    if ((flags & SPINGTP_KERNEL_VALU) == 0 && !weighted)
         k = spingtp::find_mfma_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
-    if (k == nullptr) k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
+    if (k == nullptr && !weighted) k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
     // the large-degree kernels have no parity mixing of their tiles
     if (k != nullptr && k->family == 3 && spin_mode == 1 && (flags & ~kRouteFlags) == SPINGTP_BASIS_PARITY)
         k = nullptr;
@@ -936,11 +988,20 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2;
     bool has_backward = false, same_bwd = false;
     try {
-        if (spin_mode < 2 && !spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
+        if (spin_mode < 2 && !weighted && !spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab))
+            return SPINGTP_ERR_INTERNAL;
         int lds_floats = 0;
-        std::vector<double> dense;  // built once for the direct kernel's tables
-        if ((k != nullptr && k->family == 6) || (kd != nullptr && !fourier_bwd))
+        std::vector<double> dense;  // built once for the direct kernel's tables (and weighted plans)
+        if ((k != nullptr && k->family == 6) || (kd != nullptr && !fourier_bwd) || weighted)
             spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, basis, dense);
+        if (weighted) {
+            std::vector<std::array<int, 3>> paths;
+            spingtp::tensor_paths(L1, L2, Lout, spins, n_spins, dense, paths);
+            if (n_weights != paths.size()) return SPINGTP_ERR_INVALID_ARG;
+            for (size_t i = 0; i < n_weights; ++i)
+                if (!std::isfinite(weights[i])) return SPINGTP_ERR_INVALID_ARG;
+            spingtp::weight_paths(L1, L2, Lout, spins, n_spins, paths, weights, dense);
+        }
         if (k != nullptr && k->family == 6)
             spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 0, dir, &lds_floats, &dense);
         if (kd != nullptr && !fourier_bwd) {
@@ -948,9 +1009,11 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
             spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 2, dir_b2, &lds_floats, &dense);
         }
         if (k != nullptr && k->family == 4) spingtp::build_mfma_operands(L1, aux);
-        if (kv1->family == 5) spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre);
-        // spingtp_backward_v1 on the precontracted kernel: the same table with J x2
-        if (kv1->family == 5 && L1 == L2 && L2 == Lout &&
+        if (kv1->family == 5)
+            spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre, false, weighted ? &dense : nullptr);
+        // spingtp_backward_v1 on the precontracted kernel: the same table with J x2 (the
+        // conjugation identity holds for the unweighted tensor only)
+        if (kv1->family == 5 && L1 == L2 && L2 == Lout && !weighted &&
             !spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre_bwd, true))
             pre_bwd.clear();
         // spingtp_backward: square plans with a forward kernel, input 2 conjugated
@@ -1045,6 +1108,42 @@ spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, i
     p->kernel = k;
     p->kernel_v1 = kv1;
     *out_plan = p;
+    return SPINGTP_OK;
+}
+
+spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                   spingtp_dtype dtype, unsigned flags, spingtp_plan* out_plan) {
+    return create_plan(L1, L2, Lout, spins, n_spins, dtype, flags, nullptr, 0, out_plan);
+}
+
+spingtp_status spingtp_plan_create_weighted(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                            spingtp_dtype dtype, unsigned flags, const double* weights,
+                                            size_t n_weights, spingtp_plan* out_plan) {
+    if (weights == nullptr) {
+        if (out_plan != nullptr) *out_plan = nullptr;
+        return SPINGTP_ERR_INVALID_ARG;
+    }
+    return create_plan(L1, L2, Lout, spins, n_spins, dtype, flags, weights, n_weights, out_plan);
+}
+
+spingtp_status spingtp_paths_host(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
+                                  int* triples, size_t capacity, size_t* count) {
+    if (count == nullptr || (capacity > 0 && triples == nullptr)) return SPINGTP_ERR_INVALID_ARG;
+    int spin_mode = 0;
+    const spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
+    if (st != SPINGTP_OK) return st;
+    try {
+        std::vector<double> T;
+        spingtp::build_dense_tensor(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, T);
+        std::vector<std::array<int, 3>> paths;
+        spingtp::tensor_paths(L1, L2, Lout, spins, n_spins, T, paths);
+        *count = paths.size();
+        const size_t n = paths.size() < capacity ? paths.size() : capacity;
+        for (size_t i = 0; i < n; ++i)
+            for (int j = 0; j < 3; ++j) triples[3 * i + j] = paths[i][j];
+    } catch (const std::bad_alloc&) {
+        return SPINGTP_ERR_OUT_OF_MEMORY;
+    }
     return SPINGTP_OK;
 }
 

@@ -79,6 +79,19 @@ def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, backward=F
     return out
 
 
+def paths_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """spingtp_paths_host: the [n_paths, 3] block triples of the path-weighted product."""
+    arr, n = _spin_array(spins)
+    count = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().spingtp_paths_host(L1, L2, Lout, arr, n, basis, None, 0, ctypes.byref(count)),
+               "spingtp_paths_host")
+    out = np.zeros((count.value, 3), dtype=np.int32)
+    _lib.check(_lib.lib().spingtp_paths_host(L1, L2, Lout, arr, n, basis,
+                                             out.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), count.value,
+                                             ctypes.byref(count)), "spingtp_paths_host")
+    return out
+
+
 def direct_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, role=0):
     """spingtp_direct_table_host: the entry table of the direct kernel for one role of T
     (0 forward, 1 gradient w.r.t. x1, 2 gradient w.r.t. x2; uint32 words)."""
@@ -116,7 +129,7 @@ class Plan:
     """
 
     def __init__(self, L1, L2, Lout, spins=(-1, 0, 1), dtype="fp32", basis=BASIS_PAPER, valu_only=False,
-                 v1_fourier=False, v1_precontract=False):
+                 v1_fourier=False, v1_precontract=False, weights=None):
         import torch  # device memory and streams only
 
         self.L1, self.L2, self.Lout = int(L1), int(L2), int(Lout)
@@ -130,11 +143,16 @@ class Plan:
         self._handle = ctypes.c_void_p()
         arr, n = _spin_array(self.spins)
         code = FP32 if self.dtype_name == "fp32" else BF16
-        _lib.check(_lib.lib().spingtp_plan_create(self.L1, self.L2, self.Lout, arr, n, code,
-                                                  self.basis | (KERNEL_VALU if self.valu_only else 0)
-                                                  | (V1_FOURIER if self.v1_fourier else 0)
-                                                  | (V1_PRECONTRACT if self.v1_precontract else 0),
-                                                  ctypes.byref(self._handle)), "spingtp_plan_create")
+        flags = (self.basis | (KERNEL_VALU if self.valu_only else 0) | (V1_FOURIER if self.v1_fourier else 0)
+                 | (V1_PRECONTRACT if self.v1_precontract else 0))
+        if weights is None:
+            _lib.check(_lib.lib().spingtp_plan_create(self.L1, self.L2, self.Lout, arr, n, code, flags,
+                                                      ctypes.byref(self._handle)), "spingtp_plan_create")
+        else:  # one weight per path of paths_host, shared by the channels
+            w = np.ascontiguousarray(np.asarray(weights, dtype=np.float64).ravel())
+            _lib.check(_lib.lib().spingtp_plan_create_weighted(
+                self.L1, self.L2, self.Lout, arr, n, code, flags, w.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                w.size, ctypes.byref(self._handle)), "spingtp_plan_create_weighted")
         self.device = torch.cuda.current_device()
 
     @property

@@ -662,3 +662,30 @@ def test_direct_table_argument_checks(built_library):
     # the Fourier tables do not exist for spins {-2..2}
     n = ctypes.c_size_t(0)
     assert built_library.spingtp_plan_tables_host(2, 2, 2, S, 5, 0, None, 0, ctypes.byref(n), None) == 2
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [(2, 2, 2, S5, 0), (2, 1, 3, (-1, 0, 1), 1), (2, 2, 2, (-1, 0, 1), 2),
+                                                   (3, 2, 1, (0,), 0), (4, 4, 4, (-1, 0, 1), 0)])
+def test_paths_match_oracle(built_library, L1, L2, LO, spins, basis):
+    """The library's path list (block triples with a nonzero tensor entry, in order) is the oracle's."""
+    from paper_2607_01408_amd.spingtp import paths_host
+
+    assert np.array_equal(paths_host(L1, L2, LO, spins, basis), oracle.PathWeightedTensor(L1, L2, LO, spins, basis).paths)
+
+
+def test_weighted_plan_argument_checks(built_library):
+    """Checks of spingtp_plan_create_weighted that return before any device call."""
+    from paper_2607_01408_amd.spingtp import paths_host
+
+    S = (ctypes.c_int * 3)(-1, 0, 1)
+    plan = ctypes.c_void_p()
+    n = len(paths_host(2, 2, 2))
+    w = (ctypes.c_double * (n + 1))(*([1.0] * (n + 1)))
+    f = built_library.spingtp_plan_create_weighted
+    assert f(2, 2, 2, S, 3, 0, 0, None, n, ctypes.byref(plan)) == 1  # no weights
+    assert f(2, 2, 2, S, 3, 0, 0, w, n + 1, ctypes.byref(plan)) == 1  # one per path
+    assert f(2, 2, 2, S, 3, 0, 0, w, n - 1, ctypes.byref(plan)) == 1
+    assert f(2, 2, 2, S, 3, 0, 0x200, w, n, ctypes.byref(plan)) == 2  # the Fourier route has no path weights
+    w[3] = float("nan")
+    assert f(2, 2, 2, S, 3, 0, 0, w, n, ctypes.byref(plan)) == 1  # weights must be finite
+    assert not plan.value
