@@ -805,7 +805,10 @@ constexpr Registered reg_big() {
                       KernelEntry{B::WAVES, B::UNITS, static_cast<int>(B::LDS_FLOATS * sizeof(float)), 3,
                                   &launch_big<L, SPIN, W, false>, &launch_big<L, SPIN, W, true>}};
 }
-#define SPINGTP_REG_BIG(L) reg_big<L, true, 5>(), reg_big<L, false, 5>()
+// eight waves (nodes) per round: two waves per SIMD at up to 256 VGPRs, and one round
+// fewer than with five (L = 12: 3 rounds for 19 nodes; L = 16: 4 for 25), each round
+// re-reading the inputs and updating the outputs in global memory
+#define SPINGTP_REG_BIG(L) reg_big<L, true, 8>(), reg_big<L, false, 8>()
 
 const Registered kRegistry[] = {
     SPINGTP_REG(0, 0, 0, false), SPINGTP_REG(1, 1, 1, false), SPINGTP_REG(2, 2, 2, false),
