@@ -36,6 +36,7 @@
 //   and two zero batches.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 
 #include "device_common.h"
@@ -185,10 +186,19 @@ hipError_t launch_direct(const void* x1, const void* x2, void* out, int64_t unit
     if (aux == nullptr || cpx2 <= 0 || units % cpx2 != 0 || lds_floats <= 0 || lds_floats > kDirectMaxLdsFloats)
         return hipErrorInvalidValue;
     const size_t bytes = static_cast<size_t>(lds_floats) * sizeof(float);
-    if (bytes > 65536) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&spingtp_fwd_direct_kernel<TIO>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes));
-        if (e != hipSuccess) return e;
+    if (bytes > 65536) {  // raise the dynamic LDS limit once per device (to the kernel's maximum)
+        constexpr int kMaxDevices = 64;
+        static std::atomic<bool> raised[kMaxDevices];
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+        if (!raised[dev].load(std::memory_order_acquire)) {
+            const hipError_t e =
+                hipFuncSetAttribute(reinterpret_cast<const void*>(&spingtp_fwd_direct_kernel<TIO>),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    static_cast<int>(kDirectMaxLdsFloats * sizeof(float)));
+            if (e != hipSuccess) return e;
+            raised[dev].store(true, std::memory_order_release);
+        }
     }
     const int64_t tiles = (units + kDirectUnits - 1) / kDirectUnits;
     const int64_t grid = tiles < (int64_t{1} << 20) ? tiles : (int64_t{1} << 20);
