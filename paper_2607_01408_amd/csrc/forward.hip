@@ -653,6 +653,9 @@ hipError_t launch_pair(const void* x1, const void* x2, void* out, int64_t units,
 // exchanged in LDS, and every output group's owner lane accumulates the
 // round's contribution into the output row (written in round 0, then read,
 // added and written by the same lane in later rounds: ordered, deterministic).
+// Where LDS has room for it (L <= 12) the output rows of the tile live in LDS
+// across the rounds and leave in one coalesced store; above that they are
+// updated in global memory.
 // ---------------------------------------------------------------------------
 template <int L, bool SPIN, int W>
 struct BigShape {
@@ -667,7 +670,9 @@ struct BigShape {
     static constexpr int ROUNDS = (NT + W - 1) / W;
     static constexpr int DF = W * UNITS * PS::DS;
     static constexpr int TRIG = 2 * NP * (L + 1);
-    static constexpr int LDS_FLOATS = DF + TRIG;
+    static constexpr int STO = NC | 1;  // odd row stride of the output tile
+    static constexpr bool OUT_LDS = (DF + TRIG + UNITS * STO) * 4 <= 160 * 1024;
+    static constexpr int LDS_FLOATS = DF + TRIG + (OUT_LDS ? UNITS * STO : 0);
 };
 
 template <int L, bool SPIN, int W, bool BWD>
@@ -682,6 +687,7 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     __shared__ float lds[B::LDS_FLOATS];
     float* D = lds;
     float* TR = lds + B::DF;
+    float* YT = TR + B::TRIG;  // output tile (OUT_LDS only)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -702,8 +708,12 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
         const int k = r / (L + 1), t = r - k * (L + 1);
         TR[i] = g[(sb ? Y.sinT : Y.cosT) + k * TM1 + t];
     }
-    if constexpr (SPIN) {
-        if (wave == 0 && valid) orow[sub ? 2 * BO : 0] = 0.f;  // l = 0 slots of the |s| = 1 blocks
+    if constexpr (SPIN) {  // l = 0 slots of the |s| = 1 blocks
+        if constexpr (B::OUT_LDS) {
+            if (wave == 0) YT[u * B::STO + (sub ? 2 * BO : 0)] = 0.f;
+        } else {
+            if (wave == 0 && valid) orow[sub ? 2 * BO : 0] = 0.f;
+        }
     }
     __syncthreads();
 
@@ -739,15 +749,17 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
                     acc[l] = fmaf(te[kind == 3 ? tab_base + l : tab_base + tri(L, t, l)], d, acc[l]);
             }
             if (valid && !(t == 0 && kind == 0 && sub)) {
+                float* yrow = B::OUT_LDS ? YT + u * B::STO : orow;
 #pragma unroll
                 for (int l = P::lmin(gi); l <= L; ++l) {
-                    float* o = orow + blk + l * l + l + (sub ? -t : t);
+                    float* o = yrow + blk + l * l + l + (sub ? -t : t);
                     *o = (r == 0) ? acc[l] : *o + acc[l];
                 }
             }
         }
         __syncthreads();
     }
+    if constexpr (B::OUT_LDS) store_tile<B::NC, B::STO>(out + u0 * B::NC, nvalid, YT, tid, B::THREADS);
 }
 
 template <int L, bool SPIN, int W, bool BWD>
