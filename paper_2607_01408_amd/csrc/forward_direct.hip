@@ -21,7 +21,9 @@
 // one batch ahead, and every lane gathers its own A and B values.  Entries take
 // 6 bytes (two 8-bit indices, an fp32 value) so that the list of the small
 // shapes this kernel serves stays inside the scalar cache (16 KB; 2,003 entries
-// at degree 2 with spins {-2..2}): misses there, not arithmetic, set the pace.
+// at degree 2 with spins {-2..2}); with 8-byte entries misses there set the pace.
+// The bound is then the per-entry work: two LDS gathers and four VALU
+// instructions (two address adds, a product, an fma).
 // Outputs are summed in registers per output slot and stored by each lane to its
 // own row as soon as the slot is complete (no output tile in LDS, which keeps
 // more waves resident).

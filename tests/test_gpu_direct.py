@@ -221,3 +221,21 @@ def test_backward_v1_direct_routes(L1, L2, LO, spins, C):
     e1, e2 = rel_l2(host(gx1, U), r1), rel_l2(host(gx2, N), r2)
     print(f"[direct-bwd-v1]   rel_l2 {e1:.3e} {e2:.3e}", flush=True)
     assert e1 <= 1e-5 and e2 <= 1e-5, (e1, e2)
+
+
+def test_chiral_workload_full_size_sampled():
+    # the benchmark's chiral workload (degree 2, spins {-2..2}, 200,000 edges x 64 channels) in the launch
+    # configuration it times, checked on the first and last 512 units and 8,192 random ones
+    x1, x2, meta = workloads.make_pair("chiral", device="cuda")
+    U = meta["N"] * meta["C"]
+    plan = Plan(2, 2, 2, S5, "fp32")
+    y = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(11)
+    idx = np.unique(np.concatenate([np.arange(512), np.arange(U - 512, U), rng.choice(U, 8192, replace=False)]))
+    ti = torch.as_tensor(idx, device="cuda")
+    a, b, g = (t.view(U, -1)[ti].double().cpu().numpy() for t in (x1, x2, y))
+    ref = oracle.RealGauntTensor(2, 2, 2, S5).apply(a, b).reshape(len(idx), -1)
+    err = rel_l2(g, ref)
+    print(f"[direct] chiral full size sampled rel_l2={err:.3e}", flush=True)
+    assert err <= 1e-5
