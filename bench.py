@@ -209,6 +209,44 @@ def run_v1(args):
         return {"ms": ms, "family": plan.kernel_info_v1()["family"], "parity_rel_l2": parity,
                 "tp_per_s": U / (ms / 1e3)}
 
+    def measure_weighted(L1, L2, LO, C, B, basis, seed):
+        """spingtp_forward_v1_weighted (per-channel path weights) on the precontracted kernel."""
+        import oracle
+        from paper_2607_01408_amd import paths_host
+
+        x1 = workloads.draw(L1, B, C, 9100 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        x2 = workloads.draw(L2, B, 1, 9200 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        try:
+            plan = Plan(L1, L2, LO, workloads.SPINS, "fp32", basis, channel_weights=True)
+        except Exception:
+            return None
+        n_paths = len(paths_host(L1, L2, LO, workloads.SPINS, basis))
+        w = torch.randn((C, n_paths), generator=torch.Generator().manual_seed(seed)).to("cuda:0")
+        out = torch.empty((B, C, 3, (LO + 1) ** 2), device="cuda:0")
+        st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        wfn = _lib.lib().spingtp_forward_v1_weighted
+        call = (plan.handle, x1.data_ptr(), x2.data_ptr(), w.data_ptr(), out.data_ptr(), B, C, st)
+        for _ in range(args.warmup):
+            assert wfn(*call) == 0
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(args.steps):
+            wfn(*call)
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / args.steps
+        U = B * C
+        idx = np.unique(np.concatenate([np.arange(min(U, 32)), np.arange(max(0, U - 32), U)]))
+        W = w.double().cpu().numpy()
+        a = x1.view(U, -1).double().cpu().numpy()[idx]
+        b = x2.view(B, -1).double().cpu().numpy()[idx // C]
+        ref = np.stack([oracle.PathWeightedTensor(L1, L2, LO, workloads.SPINS, basis, W[u % C])
+                        .apply(a[i:i + 1], b[i:i + 1]).reshape(-1) for i, u in enumerate(idx)])
+        got = out.view(U, -1).double().cpu().numpy()[idx]
+        return {"ms": ms, "paths": n_paths, "basis": basis,
+                "parity_rel_l2": float(np.linalg.norm(got - ref) / np.linalg.norm(ref)), "tp_per_s": U / (ms / 1e3)}
+
     def measure_backward(L, C, B, seed):
         """spingtp_backward_v1 (both gradients) on the default route, preallocated buffers."""
         x1 = workloads.draw(L, B, C, 9300 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
@@ -240,9 +278,13 @@ def run_v1(args):
                "paper_h200_ms": {"direct": p_direct, "precontracted": p_pre, "triton_precontracted": p_triton}}
         for name, fourier in (("precontracted", False), ("fourier", True)):
             row[name] = measure(L1, L2, LO, C, B, fourier, L1 + 3 * L2 + C)
+        for name, basis in (("channel_weighted_parity_basis", 2), ("channel_weighted_paper_basis", 0)):
+            row[name] = measure_weighted(L1, L2, LO, C, B, basis, L1 + 3 * L2 + C)
         table.append(row)
         print(f"[v1] ({L1},{L2},{LO}) C={C} B={B}: pre {row['precontracted']['ms'] * 1e3:.1f} us, "
-              f"fourier {row['fourier']['ms'] * 1e3:.1f} us", file=sys.stderr, flush=True)
+              f"fourier {row['fourier']['ms'] * 1e3:.1f} us, weighted (parity / paper basis) "
+              f"{row['channel_weighted_parity_basis']['ms'] * 1e3:.1f} / "
+              f"{row['channel_weighted_paper_basis']['ms'] * 1e3:.1f} us", file=sys.stderr, flush=True)
     sweep = []
     for L in args.v1_sweep_degrees:
         row = {"L": L, "C": args.v1_sweep_channels, "B": args.v1_sweep_edges}

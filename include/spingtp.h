@@ -89,6 +89,10 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
 #define SPINGTP_V1_FOURIER 0x200u
 #define SPINGTP_V1_PRECONTRACT 0x400u
 
+/* Also build the tables of spingtp_forward_v1_weighted (per-channel path weights),
+ * OR-ed into the flags of spingtp_plan_create. */
+#define SPINGTP_CHANNEL_WEIGHTS 0x1000u
+
 /* For spingtp_plan_tables_host only: return the tables spingtp_backward uses
  * (input 2's m = 0 mixing with the conjugation folded in). */
 #define SPINGTP_TABLES_BACKWARD 0x800u
@@ -188,6 +192,29 @@ spingtp_status spingtp_forward(spingtp_plan plan, const void* x1, const void* x2
  */
 spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void* x2, void* out,
                                   int64_t N, int64_t C, void* stream);
+
+/*
+ * The depthwise product with per-channel path weights and the edge input shared
+ * by the channels (Sec. 3.4, the precontraction equations; App. E.1, mode uvu with
+ * V = 1):
+ *   out[n][c][k3] = sum over paths p of weights[c][p] sum_{k1,k2 on p}
+ *                   T[k1][k2][k3] x1[n][c][k1] x2[n][k2],
+ * paths p in the order of spingtp_paths_host (block triples rho1, rho2 -> rho3).
+ *   weights: device fp32 [C][n_paths], 4-byte aligned, read only.
+ *   x1, x2, out, N, C, stream: as spingtp_forward_v1.
+ * Needs a plan created with SPINGTP_CHANNEL_WEIGHTS (else SPINGTP_ERR_UNSUPPORTED).
+ * Route: the precontracted kernel over path slots q = (p, k1): per edge the kernel
+ * K[q][k3] = sum_{k2 on p} T x2 is built once, and each channel's operand is
+ * weights[c][p] x1[c][k1]; the contraction then runs over all path slots (at L = 2
+ * with spins {-1, 0, +1}: 263 in the parity basis, 471 in the paper basis, whose
+ * +-1 blocks split paths; 27 without weights).  Built for shapes whose
+ * path slots fit 480 and output rows 48 (the depthwise runtime table's shapes,
+ * degree <= 2 with spins {-1, 0, +1}, (1, 3, 3), degree <= 4 with spin {0});
+ * plan creation with the flag fails with SPINGTP_ERR_UNSUPPORTED otherwise.
+ * Forward only (no gradients).  Asynchronous, no allocation.
+ */
+spingtp_status spingtp_forward_v1_weighted(spingtp_plan plan, const void* x1, const void* x2,
+                                           const float* weights, void* out, int64_t N, int64_t C, void* stream);
 
 /*
  * Gradients of a scalar loss through out = SpinGTP(x1, x2) of spingtp_forward:
@@ -324,15 +351,15 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  * not cover (a degree above 6 with spins {-1, 0, +1}, above 7 with spin {0}) give
  * SPINGTP_ERR_UNSUPPORTED.
  * Word layout, with P = 256 (threads of one workgroup):
- *   [0, 12)                NC1, NC2, NCO, BLK1 ((L1+1)^2 for spins {-1, 0, +1},
- *                          else 0), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT,
- *                          KST = 16 KS + 4, NB3, RB, STRIDE, 0: the k3 rows of the
+ *   [0, 16)                NC1, NC2, NCO, BLK1 = (L1+1)^2, KS = ceil(NC1/16),
+ *                          NT = ceil(NCO/16), IPT, KST = 16 KS + 4, NB3, RB,
+ *                          STRIDE, n_spins, NC1, 0, 0, 0: the k3 rows of the
  *                          edge kernel come in NB3 blocks of RB rows (one block of
  *                          16 NT rows when KS, NT <= 5, else blocks of 48 rows);
  *                          each block holds STRIDE items per thread, IPT of them
  *                          used (STRIDE = IPT, a multiple of 8, for one block;
  *                          else IPT is a multiple of 16 and STRIDE = IPT + 16);
- *   [12, 12 + 2 NB3 STRIDE P)  per block b, items [item][thread], two words each:
+ *   [16, 16 + 2 NB3 STRIDE P)  per block b, items [item][thread], two words each:
  *                          dst | k2 << 16 | last << 24, then the fp32 value (bits).
  * Thread t adds value * x2[k2] for the items of a block in order to a running
  * sum; an item with `last` set stores the sum as the edge kernel entry K[k1][k3]
@@ -341,6 +368,11 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  * With SPINGTP_TABLES_BACKWARD in `flags` (L1 = L2 = Lout only): the table of
  * spingtp_backward_v1, whose items use J x2 (k2 replaced by J's source slot, the
  * value by J's sign times the value; see spingtp_conj_map_host).
+ * With SPINGTP_CHANNEL_WEIGHTS: the table of spingtp_forward_v1_weighted.  Word 0
+ * is then the number of path slots Q (the contraction length; KS covers it, from
+ * the kernel's instantiations), word 13 the number of paths and word 14 the
+ * offset of Q words after the items: path slot q = x1 slot | path << 16, listed
+ * path by path; an item's kernel position is dst = k3 KST + q.
  * Writes min(capacity, total) words to `words` (may be NULL when capacity is 0)
  * and the total to *count.
  */

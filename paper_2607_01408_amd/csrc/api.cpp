@@ -44,3 +44,15 @@ extern "C" spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, 
                                              int64_t N, int64_t C, void* stream) {
     return spingtp::run_forward(plan, plan ? plan->kernel_v1 : nullptr, x1, x2, out, N, C, true, stream);
 }
+
+extern "C" spingtp_status spingtp_forward_v1_weighted(spingtp_plan plan, const void* x1, const void* x2,
+                                                      const float* weights, void* out, int64_t N, int64_t C,
+                                                      void* stream) {
+    if (plan == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    if (plan->kernel_v1w == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    if (N > 0 && C > 0 && (weights == nullptr || (reinterpret_cast<uintptr_t>(weights) & 3u) != 0))
+        return SPINGTP_ERR_INVALID_ARG;
+    // the weighted kernel takes the weights in place of the plan tables
+    return spingtp::run_forward(plan, plan->kernel_v1w, x1, x2, out, N, C, true, stream, weights, false,
+                                plan->d_pre_w);
+}

@@ -83,26 +83,43 @@ __device__ __forceinline__ uint64_t x1_data_mask(int nc1, int blk1, int ns, int 
 // Workgroups are persistent: workgroup b takes edges b, b + grid, ...; while an
 // edge's product runs, the next edge's x2 row and each wave's first x1 tile of
 // the next edge are already loading.
-template <typename TIO, int KS, int NT>
+// WGT: per-channel path weights (spingtp_forward_v1_weighted).  The contraction
+// index then runs over path slots q = (path p, x1 slot k1), the edge kernel's
+// entry (q, k3) holds path p's share, and the operand of channel c at q is
+// wts[c][p] x1[c][k1] (slot list in LDS), so each path is weighted per channel.
+template <typename TIO, int KS, int NT, bool WGT = false>
 __global__ __launch_bounds__(kPreThreads) void spingtp_fwd_pre_kernel(const TIO* __restrict__ x1,
                                                                       const TIO* __restrict__ x2,
                                                                       TIO* __restrict__ out, int64_t C,
                                                                       int64_t edges,
-                                                                      const uint32_t* __restrict__ aux) {
+                                                                      const uint32_t* __restrict__ aux,
+                                                                      const float* __restrict__ wts) {
     constexpr int KST = 16 * KS + 4;
     constexpr int KT_FLOATS = 16 * NT * KST;
-    constexpr int RS = 16 * (KS > NT ? KS : NT) + 4;  // row stride of a wave's staging tile
+    // row stride of a wave's staging tile (x1 rows, then output rows); the weighted
+    // kernel's contraction is longer than an x1 row (at most kPreMaxNC slots)
+    constexpr int RS = WGT ? (16 * NT > kPreMaxNC + 1 ? 16 * NT : kPreMaxNC + 1) + 4 : 16 * (KS > NT ? KS : NT) + 4;
     constexpr int NW = kPreThreads / 64;
-    constexpr int PF = 4 * KS;  // x1 values per lane of a 16-channel tile: 16 NC1 / 64 <= 4 KS
+    // x1 values per lane of a 16-channel tile: 16 NC1 / 64 <= 4 KS (weighted: NC1 <= 160)
+    constexpr int PF = WGT ? 40 : 4 * KS;
     constexpr int PO = 4 * NT;  // output values per lane of a tile
     __shared__ __align__(16) float Kt[KT_FLOATS];
     __shared__ __align__(16) float Stage[NW * 16 * RS];
     __shared__ float X2[kPreMaxNC];
+    __shared__ uint32_t QM[WGT ? 16 * KS : 1];  // path slots: x1 slot | path << 16
 
-    const int NC1 = static_cast<int>(aux[0]), NC2 = static_cast<int>(aux[1]), NCO = static_cast<int>(aux[2]);
+    // NCOL: contraction length; NC1: x1 row length (the same without weights)
+    const int NCOL = static_cast<int>(aux[0]), NC2 = static_cast<int>(aux[1]), NCO = static_cast<int>(aux[2]);
+    const int NC1 = WGT ? static_cast<int>(aux[12]) : NCOL;
     const int blk1 = static_cast<int>(aux[3]), ipt = static_cast<int>(aux[6]), ns = static_cast<int>(aux[11]);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 15, g = lane >> 4;
-    const uint64_t vmask = x1_data_mask<KS>(NC1, blk1, ns, g);
+    // (64 mask bits hold KS <= 16; the weighted kernel compares q with NCOL instead)
+    const uint64_t vmask = WGT ? 0 : x1_data_mask<(KS <= 16 ? KS : 16)>(NCOL, blk1, ns, g);
+    const int npaths = WGT ? static_cast<int>(aux[13]) : 0;
+    if constexpr (WGT) {
+        const uint32_t* __restrict__ qs = aux + aux[14];
+        for (int i = tid; i < 16 * KS; i += kPreThreads) QM[i] = i < NCOL ? qs[i] : 0u;  // read after a barrier
+    }
     const int64_t tiles = (C + 15) / 16;
     const int64_t stride = gridDim.x;
     float* __restrict__ st = Stage + wave * 16 * RS;
@@ -185,29 +202,59 @@ __global__ __launch_bounds__(kPreThreads) void spingtp_fwd_pre_kernel(const TIO*
                 }
             }
             wave_lds_order();
-            float b[KS][4];
-#pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                const v4f v = *reinterpret_cast<const v4f*>(&st[col * RS + 16 * s + 4 * g]);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    b[s][j] = ((vmask >> (4 * s + j)) & 1u) ? v[j] : 0.f;
-                }
-            }
-            if (m + NW < tiles)
-                prefetch(n, m + NW);
-            else if (nn < edges)
-                prefetch(nn, wave);
             v4f acc[NT];
 #pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+            for (int t = 0; t < NT; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+            if constexpr (WGT) {
+                // operands formed block by block from the staged x1 rows: channel c's value
+                // at path slot q is wts[c][path] x1[c][slot]; the staged rows stay untouched
+                // until the output staging below
+                if (m + NW < tiles)
+                    prefetch(n, m + NW);
+                else if (nn < edges)
+                    prefetch(nn, wave);
+                const int64_t ch = 16 * m + col;  // this lane's channel of the edge
+                const float* __restrict__ wc = wts + (ch < C ? ch : 0) * npaths;
+#pragma unroll 2
+                for (int s = 0; s < KS; ++s) {
+                    float bs[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const uint32_t e = QM[16 * s + 4 * g + j];  // 0 past the slots: in-bounds reads
+                        const bool use = 16 * s + 4 * g + j < NCOL && ch < C;
+                        bs[j] = use ? st[col * RS + (e & 0xffffu)] * wc[e >> 16] : 0.f;
+                    }
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+                        const v4f a = *reinterpret_cast<const v4f*>(&Kt[(16 * t + col) * KST + 16 * s + 4 * g]);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], bs[j], acc[t], 0, 0, 0);
+                    }
+                }
+            } else {
+                float b[KS][4];
 #pragma unroll
                 for (int s = 0; s < KS; ++s) {
-                    const v4f a = *reinterpret_cast<const v4f*>(&Kt[(16 * t + col) * KST + 16 * s + 4 * g]);
+                    const v4f v = *reinterpret_cast<const v4f*>(&st[col * RS + 16 * s + 4 * g]);
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[s][j], acc[t], 0, 0, 0);
+                    for (int j = 0; j < 4; ++j) {
+                        b[s][j] = ((vmask >> (4 * s + j)) & 1u) ? v[j] : 0.f;
+                    }
+                }
+                if (m + NW < tiles)
+                    prefetch(n, m + NW);
+                else if (nn < edges)
+                    prefetch(nn, wave);
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                    for (int s = 0; s < KS; ++s) {
+                        const v4f a = *reinterpret_cast<const v4f*>(&Kt[(16 * t + col) * KST + 16 * s + 4 * g]);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[s][j], acc[t], 0, 0, 0);
+                    }
                 }
             }
             wave_lds_order();
@@ -453,7 +500,24 @@ hipError_t launch_pre(const void* x1, const void* x2, void* out, int64_t units, 
     else
         hipLaunchKernelGGL((spingtp_fwd_pre_kernel<TIO, KS, NT>), dim3(static_cast<unsigned>(grid)), dim3(kPreThreads),
                            0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
-                           static_cast<TIO*>(out), cpx2, edges, aux);
+                           static_cast<TIO*>(out), cpx2, edges, aux, nullptr);
+    return hipGetLastError();
+}
+
+// The per-channel path-weighted kernel (one block of rows): `wts` carries the
+// channel weights [C][NPATHS] (fp32) in place of the plan tables.
+template <typename TIO, int KS, int NT>
+hipError_t launch_pre_weighted(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2,
+                               const float* wts, const uint32_t* aux, hipStream_t stream) {
+    if (aux == nullptr || wts == nullptr || cpx2 <= 0 || units % cpx2 != 0) return hipErrorInvalidValue;
+    const int64_t edges = units / cpx2;
+    if (edges == 0) return hipSuccess;
+    const int64_t resident = resident_groups<spingtp_fwd_pre_kernel<TIO, KS, NT, true>>();
+    if (resident <= 0) return hipErrorInvalidValue;
+    const int64_t grid = edges < resident ? edges : resident;
+    hipLaunchKernelGGL((spingtp_fwd_pre_kernel<TIO, KS, NT, true>), dim3(static_cast<unsigned>(grid)),
+                       dim3(kPreThreads), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
+                       static_cast<TIO*>(out), cpx2, edges, aux, wts);
     return hipGetLastError();
 }
 
@@ -472,6 +536,14 @@ constexpr int pre_lds_bytes() {
 #define SPINGTP_PRE_PAIR(KS, NT)                                                               \
     {KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, NT>(), 5, &launch_pre<float, KS, NT>}, \
      KernelEntry{kPreThreads / 64, 1, pre_lds_bytes<KS, NT>(), 5, &launch_pre<uint16_t, KS, NT>}}
+// ... of the per-channel path-weighted kernel (always the one-block kernel)
+#define SPINGTP_PRE_W_PAIR(KS, NT)                                                                         \
+    {KernelEntry{kPreThreads / 64, 1,                                                                     \
+                 (16 * NT * (16 * KS + 4) + (kPreThreads / 64) * 16 * (kPreMaxNC + 5) + kPreMaxNC + 16 * KS) * 4, \
+                 5, &launch_pre_weighted<float, KS, NT>},                                                   \
+     KernelEntry{kPreThreads / 64, 1,                                                                     \
+                 (16 * NT * (16 * KS + 4) + (kPreThreads / 64) * 16 * (kPreMaxNC + 5) + kPreMaxNC + 16 * KS) * 4, \
+                 5, &launch_pre_weighted<uint16_t, KS, NT>}}
 
 }  // namespace
 }  // namespace spingtp

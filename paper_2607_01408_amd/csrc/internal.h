@@ -42,7 +42,7 @@ constexpr int kPreMaxNC = 147;
 // Threads per workgroup of the precontracted kernel (its tensor items are laid out
 // for exactly this many threads) and the words of its table header.
 constexpr int kPreThreads = 256;
-constexpr int kPreHeader = 12;
+constexpr int kPreHeader = 16;
 // k3 rows per kernel block of the large instantiations (KS or NT above 5)
 constexpr int kPreBlockRows = 48;
 
@@ -76,12 +76,19 @@ const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype)
 const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
 // The precontracted kernel of spingtp_forward_v1 (x2 shared by the channels of an edge).
 const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int n_spins, int dtype);
+// The per-channel path-weighted kernel (forward_pre_weighted.hip): the smallest
+// instantiation with KS >= ks_min and NT >= nt_min (its KS and NT to *ks, *nt);
+// nullptr if none (KS up to 30, NT up to 3).
+const KernelEntry* find_pre_weighted_kernel(int ks_min, int nt_min, int dtype, int* ks, int* nt);
 // The instantiations with KS or NT in {7, 10} (forward_pre_large.hip); nullptr if none.
 const KernelEntry* find_pre_kernel_large(int ks, int nt, int dtype);
 
-// Sparse tensor of the precontracted kernel (forward_pre.h).  Header words NC1,
-// NC2, NCO, BLK1 (0 for spins {0}), KS = ceil(NC1/16), NT = ceil(NCO/16), IPT,
-// KST = 16 KS + 4, NB3, RB, STRIDE, 0: the kernel's k3 rows come in NB3 blocks
+// Sparse tensor of the precontracted kernel (forward_pre.h).  Header words NCOL
+// (the contraction length: NC1, or the path slots of the per-channel weighted
+// table), NC2, NCO, BLK1 = (L1+1)^2, KS = ceil(NCOL/16) (or the instantiation's),
+// NT = ceil(NCO/16), IPT, KST = 16 KS + 4, NB3, RB, STRIDE, n_spins, NC1 (x1 row
+// length), NPATHS (0 unweighted), the word offset of the path slots (0
+// unweighted), 0: the kernel's k3 rows come in NB3 blocks
 // of RB rows (one block of 16 NT rows for KS, NT <= 5; kPreBlockRows otherwise).
 // Then per block STRIDE x kPreThreads items [item][thread]: IPT items (a multiple
 // of 8) for the one-block kernel, STRIDE = IPT; for the blocked kernel IPT is a
@@ -95,6 +102,16 @@ const KernelEntry* find_pre_kernel_large(int ks, int nt, int dtype);
 // every entry has one writer; lists are padded with zero items.
 // conj_x2: the table of spingtp_backward_v1, whose kernel reads x2 but must use
 // J x2 (build_conj_map); false if J cannot be built.
+// The table of the per-channel path-weighted kernel (spingtp_forward_v1_weighted):
+// the contraction runs over path slots q = (path p, x1 slot k1 of p's input-1
+// block), listed path by path (paths in spingtp_paths_host order, k1 ascending);
+// entry (q, k3) sums T[k1, k2, k3] x2[k2] over k2 of p's input-2 block, for k3 of
+// p's output block.  ks: the instantiation's contraction blocks (16 ks >= the
+// number of path slots, written to *n_rows; false otherwise).  One block of rows.
+// The path slots follow the items: x1 slot | path << 16.
+bool build_pre_tables_channel_weighted(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                                       int ks, std::vector<uint32_t>& out, int* n_rows);
+std::vector<int> slot_blocks(int L, const int* spins, int n_spins);
 // dense: the tensor to tabulate (the plan's, e.g. path-weighted); built here when nullptr.
 bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
                       std::vector<uint32_t>& out, bool conj_x2 = false, const std::vector<double>* dense = nullptr);
@@ -156,6 +173,8 @@ struct spingtp_plan_s {
     uint32_t* d_aux;  // matrix-core operand tables, nullptr for the vector-ALU kernels
     uint32_t* d_pre;  // sparse tensor of the precontracted kernel, nullptr if not used
     uint32_t* d_pre_bwd;  // the same with J x2 (spingtp_backward_v1), nullptr if not used
+    uint32_t* d_pre_w;    // the per-channel path-weighted table (SPINGTP_CHANNEL_WEIGHTS), nullptr if not built
+    const spingtp::KernelEntry* kernel_v1w;  // its kernel (spingtp_forward_v1_weighted)
     float* d_tab_bwd;  // tables of spingtp_backward (d_tab when equal), nullptr without a backward
     bool own_tab_bwd;  // d_tab_bwd is a separate allocation
     uint32_t* d_dir;     // direct-kernel entry table of the forward (family 6), nullptr if not used

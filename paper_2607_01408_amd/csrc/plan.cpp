@@ -461,45 +461,53 @@ void build_mfma_operands(int L, std::vector<uint32_t>& out) {
             }
 }
 
-bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
-                      std::vector<uint32_t>& out, bool conj_x2, const std::vector<double>* dense) {
-    std::vector<double> own;
-    if (dense == nullptr) build_dense_tensor(L1, L2, LO, spins, n_spins, flags, own);
-    const std::vector<double>& T = dense != nullptr ? *dense : own;
-    // conj_x2: the kernel reads x2 but must use J x2 (spingtp_backward_v1), so
-    // each item's k2 becomes J's source slot and its value takes J's sign
-    std::vector<uint32_t> J;
-    if (conj_x2 && !build_conj_map(L2, spins, n_spins, flags, J)) return false;
-    const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
-    const int nco = n_spins * (LO + 1) * (LO + 1);
-    const int ks = (nc1 + 15) / 16, nt = (nco + 15) / 16, kst = 16 * ks + 4;
+namespace {
+
+// One contraction row of the precontracted kernel: x1 slot k1, and (for the
+// per-channel weighted table) the path's input-2 and output blocks that the row's
+// entries are restricted to (-1: no restriction).
+struct PreRow {
+    int k1, b2, b3, path;
+};
+
+// The item table of the precontracted kernel for the given contraction rows (see
+// build_pre_tables): entry (q, k3) = sum over k2 of T[k1(q), k2, k3] x2[k2].
+bool pre_table_from_rows(const std::vector<double>& T, int nc1, int nc2, int nco, int blk1, int n_spins,
+                         const std::vector<PreRow>& rows, int ks, const std::vector<int>& blk2,
+                         const std::vector<int>& blko, const std::vector<uint32_t>* J, int npaths,
+                         std::vector<uint32_t>& out) {
+    const int nt = (nco + 15) / 16, kst = 16 * ks + 4;
     // k3 rows per block: the whole kernel, or blocks of kPreBlockRows for the
-    // large instantiations (KS or NT above 5)
-    const int rb = (ks > 5 || nt > 5) ? kPreBlockRows : 16 * nt;
+    // large instantiations (KS or NT above 5); the weighted kernel always takes one block
+    const int rb = ((ks > 5 || nt > 5) && npaths == 0) ? kPreBlockRows : 16 * nt;
     const int nb3 = (16 * nt + rb - 1) / rb;
-    // nonzero lists per kernel entry (k1, k3), per block
+    if (static_cast<int64_t>(rb) * kst > 0xffff) return false;  // 16-bit entry positions
     struct Entry {
         int dst;
         std::vector<std::pair<int, float>> items;
     };
     std::vector<std::vector<Entry>> entries(nb3);
-    for (int k1 = 0; k1 < nc1; ++k1)
+    for (int q = 0; q < static_cast<int>(rows.size()); ++q) {
+        const PreRow& rw = rows[q];
         for (int k3 = 0; k3 < nco; ++k3) {
+            if (rw.b3 >= 0 && blko[k3] != rw.b3) continue;
             const int b = k3 / rb;
-            Entry e{(k3 - b * rb) * kst + k1, {}};
+            Entry e{(k3 - b * rb) * kst + q, {}};
             for (int k2 = 0; k2 < nc2; ++k2) {
-                const double v = T[(static_cast<size_t>(k1) * nc2 + k2) * nco + k3];
+                if (rw.b2 >= 0 && blk2[k2] != rw.b2) continue;
+                const double v = T[(static_cast<size_t>(rw.k1) * nc2 + k2) * nco + k3];
                 if (std::fabs(v) <= 1e-12) continue;
-                if (conj_x2) {
-                    if (J[k2] & kConjZero) continue;  // J x2 is 0 there
-                    const double sign = (J[k2] & kConjNeg) ? -1.0 : 1.0;
-                    e.items.emplace_back(static_cast<int>(J[k2] & 0xffffu), static_cast<float>(sign * v));
+                if (J != nullptr) {
+                    if ((*J)[k2] & kConjZero) continue;  // J x2 is 0 there
+                    const double sign = ((*J)[k2] & kConjNeg) ? -1.0 : 1.0;
+                    e.items.emplace_back(static_cast<int>((*J)[k2] & 0xffffu), static_cast<float>(sign * v));
                 } else {
                     e.items.emplace_back(k2, static_cast<float>(v));
                 }
             }
             if (!e.items.empty()) entries[b].push_back(std::move(e));
         }
+    }
     // per block: longest-first greedy balance of whole entries over the threads
     std::vector<std::vector<std::vector<const Entry*>>> per(nb3, std::vector<std::vector<const Entry*>>(kPreThreads));
     // the blocked kernel loads 16 items ahead without conditions: IPT a multiple
@@ -519,11 +527,12 @@ bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
         ipt = std::max(ipt, (*std::max_element(load.begin(), load.end()) + quantum - 1) / quantum * quantum);
     }
     const size_t stride = blocked ? ipt + 16 : ipt;  // items per thread and block
-    out.assign(kPreHeader + 2 * nb3 * stride * kPreThreads, 0u);  // padding items: value 0, never stored
-    out[0] = static_cast<uint32_t>(nc1);
+    const size_t item_words = 2 * nb3 * stride * kPreThreads;
+    out.assign(kPreHeader + item_words + (npaths > 0 ? rows.size() : 0), 0u);  // padding items: value 0
+    out[0] = static_cast<uint32_t>(rows.size());
     out[1] = static_cast<uint32_t>(nc2);
     out[2] = static_cast<uint32_t>(nco);
-    out[3] = static_cast<uint32_t>((L1 + 1) * (L1 + 1));
+    out[3] = static_cast<uint32_t>(blk1);
     out[4] = static_cast<uint32_t>(ks);
     out[5] = static_cast<uint32_t>(nt);
     out[6] = static_cast<uint32_t>(ipt);
@@ -532,6 +541,9 @@ bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
     out[9] = static_cast<uint32_t>(rb);
     out[10] = static_cast<uint32_t>(stride);
     out[11] = static_cast<uint32_t>(n_spins);
+    out[12] = static_cast<uint32_t>(nc1);
+    out[13] = static_cast<uint32_t>(npaths);
+    out[14] = npaths > 0 ? static_cast<uint32_t>(kPreHeader + item_words) : 0u;
     for (int b = 0; b < nb3; ++b) {
         uint32_t* items = out.data() + kPreHeader + 2 * static_cast<size_t>(b) * stride * kPreThreads;
         for (int t = 0; t < kPreThreads; ++t) {
@@ -546,7 +558,50 @@ bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, uns
                 }
         }
     }
+    if (npaths > 0)  // the contraction rows: x1 slot | path << 16
+        for (size_t q = 0; q < rows.size(); ++q)
+            out[kPreHeader + item_words + q] =
+                static_cast<uint32_t>(rows[q].k1) | (static_cast<uint32_t>(rows[q].path) << 16);
     return true;
+}
+
+}  // namespace
+
+bool build_pre_tables(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                      std::vector<uint32_t>& out, bool conj_x2, const std::vector<double>* dense) {
+    std::vector<double> own;
+    if (dense == nullptr) build_dense_tensor(L1, L2, LO, spins, n_spins, flags, own);
+    const std::vector<double>& T = dense != nullptr ? *dense : own;
+    // conj_x2: the kernel reads x2 but must use J x2 (spingtp_backward_v1), so
+    // each item's k2 becomes J's source slot and its value takes J's sign
+    std::vector<uint32_t> J;
+    if (conj_x2 && !build_conj_map(L2, spins, n_spins, flags, J)) return false;
+    const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
+    const int nco = n_spins * (LO + 1) * (LO + 1);
+    std::vector<PreRow> rows(nc1);
+    for (int k1 = 0; k1 < nc1; ++k1) rows[k1] = {k1, -1, -1, 0};
+    return pre_table_from_rows(T, nc1, nc2, nco, (L1 + 1) * (L1 + 1), n_spins, rows, (nc1 + 15) / 16, {}, {},
+                               conj_x2 ? &J : nullptr, 0, out);
+}
+
+bool build_pre_tables_channel_weighted(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                                       int ks, std::vector<uint32_t>& out, int* n_rows) {
+    std::vector<double> T;
+    build_dense_tensor(L1, L2, LO, spins, n_spins, flags, T);
+    std::vector<std::array<int, 3>> paths;
+    tensor_paths(L1, L2, LO, spins, n_spins, T, paths);
+    const std::vector<int> b1 = slot_blocks(L1, spins, n_spins), b2 = slot_blocks(L2, spins, n_spins),
+                           bo = slot_blocks(LO, spins, n_spins);
+    std::vector<PreRow> rows;
+    for (int p = 0; p < static_cast<int>(paths.size()); ++p)
+        for (int k1 = 0; k1 < static_cast<int>(b1.size()); ++k1)
+            if (b1[k1] == paths[p][0]) rows.push_back({k1, paths[p][1], paths[p][2], p});
+    *n_rows = static_cast<int>(rows.size());
+    if (static_cast<int>(rows.size()) > 16 * ks || static_cast<int>(b1.size()) > 16 * ks || paths.size() > 0xffff)
+        return false;
+    const int nc1 = static_cast<int>(b1.size()), nc2 = static_cast<int>(b2.size()), nco = static_cast<int>(bo.size());
+    return pre_table_from_rows(T, nc1, nc2, nco, (L1 + 1) * (L1 + 1), n_spins, rows, ks, b2, bo, nullptr,
+                               static_cast<int>(paths.size()), out);
 }
 
 // Dense real tensor T[k1][k2][k3] = Re sum conj(Q3) G Q1 Q2 (see spingtp.h).
@@ -763,7 +818,8 @@ void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, u
 namespace {
 
 // flag bits that choose kernels, not the operation
-constexpr unsigned kRouteFlags = SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER | SPINGTP_V1_PRECONTRACT;
+constexpr unsigned kRouteFlags =
+    SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER | SPINGTP_V1_PRECONTRACT | SPINGTP_CHANNEL_WEIGHTS;
 
 spingtp_status check_args(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
                           int* spin_mode) {
@@ -884,11 +940,27 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
     int spin_mode = 0;
     const spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
-    if (spingtp::find_pre_kernel(L1, L2, Lout, n_spins, 0) == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    const bool channel_weights = (flags & SPINGTP_CHANNEL_WEIGHTS) != 0;
+    if (channel_weights && backward) return SPINGTP_ERR_INVALID_ARG;
+    if (!channel_weights && spingtp::find_pre_kernel(L1, L2, Lout, n_spins, 0) == nullptr)
+        return SPINGTP_ERR_UNSUPPORTED;
     try {
         std::vector<uint32_t> w;
-        if (!spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, w, backward))
+        if (channel_weights) {  // the table of spingtp_forward_v1_weighted, as a plan with the flag builds it
+            const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
+            const int nco = n_spins * (Lout + 1) * (Lout + 1);
+            int rows = 0, ks = 0, nt = 0;
+            (void)spingtp::build_pre_tables_channel_weighted(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, 0, w,
+                                                             &rows);
+            if (nc2 > spingtp::kPreMaxNC ||
+                spingtp::find_pre_weighted_kernel((std::max(rows, nc1) + 15) / 16, (nco + 15) / 16, 0, &ks, &nt) ==
+                    nullptr ||
+                !spingtp::build_pre_tables_channel_weighted(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, ks, w,
+                                                            &rows))
+                return SPINGTP_ERR_UNSUPPORTED;
+        } else if (!spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, w, backward)) {
             return SPINGTP_ERR_UNSUPPORTED;
+        }
         *count = w.size();
         const size_t n = w.size() < capacity ? w.size() : capacity;
         if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));
@@ -951,6 +1023,9 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     const bool weighted = weights != nullptr;
     // weighted plans: the Fourier route computes the unweighted sum over all paths at once
     if (weighted && (flags & SPINGTP_V1_FOURIER)) return SPINGTP_ERR_UNSUPPORTED;
+    // per-channel path weights are given at each call; not combined with plan-level ones
+    const bool channel_weights = (flags & SPINGTP_CHANNEL_WEIGHTS) != 0;
+    if (channel_weights && weighted) return SPINGTP_ERR_INVALID_ARG;
     const spingtp::KernelEntry* k = nullptr;
     if ((flags & SPINGTP_KERNEL_VALU) == 0 && !weighted)
         k = spingtp::find_mfma_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
@@ -985,7 +1060,8 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
 
     std::vector<double> tab;
     std::vector<double> tab_bwd;
-    std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2;
+    std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2, pre_w;
+    const spingtp::KernelEntry* kw = nullptr;
     bool has_backward = false, same_bwd = false;
     try {
         if (spin_mode < 2 && !weighted && !spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab))
@@ -1004,6 +1080,19 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
         }
         if (k != nullptr && k->family == 6)
             spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 0, dir, &lds_floats, &dense);
+        if (channel_weights) {  // path slots first, then the instantiation that holds them
+            const int nc2 = n_spins * (L2 + 1) * (L2 + 1), nco = n_spins * (Lout + 1) * (Lout + 1);
+            const int nc1 = n_spins * (L1 + 1) * (L1 + 1);
+            int rows = 0, ks = 0, nt = 0;
+            if (nc2 > spingtp::kPreMaxNC) return SPINGTP_ERR_UNSUPPORTED;
+            // with ks = 0 the builder only counts the path slots
+            (void)spingtp::build_pre_tables_channel_weighted(L1, L2, Lout, spins, n_spins, basis, 0, pre_w, &rows);
+            kw = spingtp::find_pre_weighted_kernel((std::max(rows, nc1) + 15) / 16, (nco + 15) / 16,
+                                                   static_cast<int>(dtype), &ks, &nt);
+            if (kw == nullptr ||
+                !spingtp::build_pre_tables_channel_weighted(L1, L2, Lout, spins, n_spins, basis, ks, pre_w, &rows))
+                return SPINGTP_ERR_UNSUPPORTED;
+        }
         if (kd != nullptr && !fourier_bwd) {
             spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 1, dir_b1, &lds_floats, &dense);
             spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 2, dir_b2, &lds_floats, &dense);
@@ -1060,6 +1149,8 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     if (e == hipSuccess) e = upload(dir, &ddir);
     if (e == hipSuccess) e = upload(dir_b1, &ddir1);
     if (e == hipSuccess) e = upload(dir_b2, &ddir2);
+    uint32_t* dprew = nullptr;
+    if (e == hipSuccess) e = upload(pre_w, &dprew);
     if (e == hipSuccess && has_backward && !same_bwd) {
         std::vector<float> f(tab_bwd.size());
         for (size_t i = 0; i < tab_bwd.size(); ++i) f[i] = static_cast<float>(tab_bwd[i]);
@@ -1074,6 +1165,7 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
         if (ddir != nullptr) (void)hipFree(ddir);
         if (ddir1 != nullptr) (void)hipFree(ddir1);
         if (ddir2 != nullptr) (void)hipFree(ddir2);
+        if (dprew != nullptr) (void)hipFree(dprew);
         if (d != nullptr) (void)hipFree(d);
     };
     if (e != hipSuccess) {
@@ -1105,6 +1197,8 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     p->d_dir_b2 = ddir2;
     p->kernel_dir = ddir1 != nullptr ? kd : nullptr;
     p->dir_lds_floats = dir_lds;
+    p->d_pre_w = dprew;
+    p->kernel_v1w = dprew != nullptr ? kw : nullptr;
     p->kernel = k;
     p->kernel_v1 = kv1;
     *out_plan = p;
@@ -1157,6 +1251,7 @@ spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
     if (e == hipSuccess && plan->d_dir != nullptr) e = hipFree(plan->d_dir);
     if (e == hipSuccess && plan->d_dir_b1 != nullptr) e = hipFree(plan->d_dir_b1);
     if (e == hipSuccess && plan->d_dir_b2 != nullptr) e = hipFree(plan->d_dir_b2);
+    if (e == hipSuccess && plan->d_pre_w != nullptr) e = hipFree(plan->d_pre_w);
     if (e == hipSuccess && plan->d_pre != nullptr) e = hipFree(plan->d_pre);
     if (e == hipSuccess && plan->d_pre_bwd != nullptr) e = hipFree(plan->d_pre_bwd);
     if (e == hipSuccess && plan->own_tab_bwd) e = hipFree(plan->d_tab_bwd);

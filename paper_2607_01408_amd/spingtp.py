@@ -14,6 +14,7 @@ BASIS_PAPER = 0
 BASIS_M0_PAIRED = 1
 BASIS_PARITY = 2
 KERNEL_VALU = 0x100  # force the fp32 vector-ALU kernels (spingtp.h)
+CHANNEL_WEIGHTS = 0x1000  # also build the per-channel path-weighted table (spingtp.h)
 V1_FOURIER = 0x200  # spingtp_forward_v1 on the Fourier route (spingtp.h)
 V1_PRECONTRACT = 0x400  # spingtp_forward_v1 on the precontracted kernel wherever it is built
 FP32 = 0
@@ -64,11 +65,12 @@ def mfma_operands_host(L):
     return out
 
 
-def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, backward=False):
+def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, backward=False, channel_weights=False):
     """spingtp_pre_table_host: the tensor table of the precontracted kernel (uint32 words); with
-    backward=True the table of spingtp_backward_v1."""
+    backward=True the table of spingtp_backward_v1, with channel_weights=True that of
+    spingtp_forward_v1_weighted."""
     arr, n = _spin_array(spins)
-    basis = basis | (0x800 if backward else 0)
+    basis = basis | (0x800 if backward else 0) | (CHANNEL_WEIGHTS if channel_weights else 0)
     count = ctypes.c_size_t(0)
     _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, basis, None, 0, ctypes.byref(count)),
                "spingtp_pre_table_host")
@@ -129,7 +131,7 @@ class Plan:
     """
 
     def __init__(self, L1, L2, Lout, spins=(-1, 0, 1), dtype="fp32", basis=BASIS_PAPER, valu_only=False,
-                 v1_fourier=False, v1_precontract=False, weights=None):
+                 v1_fourier=False, v1_precontract=False, weights=None, channel_weights=False):
         import torch  # device memory and streams only
 
         self.L1, self.L2, self.Lout = int(L1), int(L2), int(Lout)
@@ -144,7 +146,7 @@ class Plan:
         arr, n = _spin_array(self.spins)
         code = FP32 if self.dtype_name == "fp32" else BF16
         flags = (self.basis | (KERNEL_VALU if self.valu_only else 0) | (V1_FOURIER if self.v1_fourier else 0)
-                 | (V1_PRECONTRACT if self.v1_precontract else 0))
+                 | (V1_PRECONTRACT if self.v1_precontract else 0) | (CHANNEL_WEIGHTS if channel_weights else 0))
         if weights is None:
             _lib.check(_lib.lib().spingtp_plan_create(self.L1, self.L2, self.Lout, arr, n, code, flags,
                                                       ctypes.byref(self._handle)), "spingtp_plan_create")
@@ -154,6 +156,8 @@ class Plan:
                 self.L1, self.L2, self.Lout, arr, n, code, flags, w.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
                 w.size, ctypes.byref(self._handle)), "spingtp_plan_create_weighted")
         self.device = torch.cuda.current_device()
+        # paths of the per-channel weights (their count bounds the kernel's reads of a weight row)
+        self.n_paths = len(paths_host(self.L1, self.L2, self.Lout, self.spins, self.basis)) if channel_weights else 0
 
     @property
     def handle(self):
@@ -187,7 +191,21 @@ class Plan:
             x2 = x2.unsqueeze(1)
         return self._run(x1, x2, out, stream, True)
 
-    def _run(self, x1, x2, out, stream, shared):
+    def forward_v1_weighted(self, x1, x2, weights, out=None, stream=None):
+        """spingtp_forward_v1_weighted: x2 shared by the C channels of an edge, weights a contiguous fp32
+        [C, n_paths] device tensor (paths in paths_host order); the plan needs channel_weights=True."""
+        import torch
+
+        if x2.dim() == 3:
+            x2 = x2.unsqueeze(1)
+        C = x1.shape[1]
+        if (weights.dtype != torch.float32 or not weights.is_contiguous() or tuple(weights.shape) != (C, self.n_paths)
+                or weights.device != x1.device):
+            raise ValueError(f"weights must be a contiguous fp32 [C, {self.n_paths}] tensor on the inputs' device "
+                             "(a plan created with channel_weights=True)")
+        return self._run(x1, x2, out, stream, True, weights)
+
+    def _run(self, x1, x2, out, stream, shared, weights=None):
         import torch
 
         if x1.dim() != 4 or x2.dim() != 4:
@@ -208,6 +226,12 @@ class Plan:
             raise ValueError("out has the wrong shape, dtype or layout")
         if stream is None:
             stream = torch.cuda.current_stream(x1.device)
+        if weights is not None:
+            _lib.check(_lib.lib().spingtp_forward_v1_weighted(self._handle, x1.data_ptr(), x2.data_ptr(),
+                                                              weights.data_ptr(), out.data_ptr(), N, C,
+                                                              ctypes.c_void_p(stream.cuda_stream)),
+                       "spingtp_forward_v1_weighted")
+            return out
         fn = _lib.lib().spingtp_forward_v1 if shared else _lib.lib().spingtp_forward
         _lib.check(fn(self._handle, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, C,
                       ctypes.c_void_p(stream.cuda_stream)), "spingtp_forward_v1" if shared else "spingtp_forward")

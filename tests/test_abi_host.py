@@ -393,7 +393,7 @@ def emulate_pre_kernel(words, x1, x2):
     builds that block of the transposed edge kernel; the product runs in float64
     with the invalid x1 slots read as 0.  x1 [C, NC1] of one edge, x2 [NC2]."""
     nc1, nc2, nco, blk1, ks, nt, ipt, kst, nb3, rb, stride = (int(v) for v in words[:11])
-    pairs = words[12:].reshape(nb3, stride, PRE_THREADS, 2)
+    pairs = words[16:16 + 2 * nb3 * stride * PRE_THREADS].reshape(nb3, stride, PRE_THREADS, 2)
     X2 = x2.astype(np.float32)
     Kt = np.zeros((nb3 * rb, kst), dtype=np.float32)
     for b in range(nb3):
@@ -436,10 +436,11 @@ def test_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
     assert (nb3, rb) == ((1, 16 * nt) if ks <= 5 and nt <= 5 else (-(-16 * nt // 48), 48))
     blocked = ks > 5 or nt > 5
     assert stride == (ipt + 16 if blocked else ipt) and ipt % (16 if blocked else 8) == 0
-    assert words.size == 12 + 2 * nb3 * stride * PRE_THREADS
-    assert not words[12:].reshape(nb3, stride, PRE_THREADS, 2)[:, ipt:].any()  # zero padding
-    items = words[12::2].reshape(nb3, -1)
-    vals = words[13::2].copy().view(np.float32)
+    assert words.size == 16 + 2 * nb3 * stride * PRE_THREADS
+    assert int(words[12]) == nc1 and not words[13:16].any()
+    assert not words[16:].reshape(nb3, stride, PRE_THREADS, 2)[:, ipt:].any()  # zero padding
+    items = words[16::2].reshape(nb3, -1)
+    vals = words[17::2].copy().view(np.float32)
     blocks = np.repeat(np.arange(nb3), items.shape[1]).reshape(nb3, -1)
     last = (items >> 24) != 0
     stores = (items & 0xFFFF)[last] + (blocks * rb * kst)[last]  # position in the whole kernel
@@ -494,7 +495,7 @@ def test_plan_create_route_flags(built_library):
     # precontraction forced where no precontracted kernel is built (rows of 192)
     assert built_library.spingtp_plan_create(7, 7, 7, S, 3, 0, 0x400, ctypes.byref(plan)) == 2
     assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x800, ctypes.byref(plan)) == 1  # tables-only bit
-    assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x1000, ctypes.byref(plan)) == 1  # unknown bit
+    assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x2000, ctypes.byref(plan)) == 1  # unknown bit
     # parity-labelled basis on the large-degree kernels (no tile mixing there)
     assert built_library.spingtp_plan_create(9, 9, 9, S, 3, 0, 2, ctypes.byref(plan)) == 2
     assert not plan.value
@@ -689,3 +690,51 @@ def test_weighted_plan_argument_checks(built_library):
     w[3] = float("nan")
     assert f(2, 2, 2, S, 3, 0, 0, w, n, ctypes.byref(plan)) == 1  # weights must be finite
     assert not plan.value
+
+
+def emulate_pre_weighted(words, x1, x2, W):
+    """The per-channel path-weighted precontracted kernel on the CPU from its exact
+    table words: the edge kernel K[q][k3] over path slots q built like the unweighted
+    one (fp32 running sums per thread), then out[c] = sum_q K[q] W[c, path(q)] x1[c, k1(q)]
+    in float64.  x1 [C, NC1], x2 [NC2], W [C, n_paths]."""
+    Q, nc2, nco, blk1, ks, nt, ipt, kst, nb3, rb, stride, ns, nc1, npaths, qoff = (int(v) for v in words[:15])
+    assert nb3 == 1 and rb == 16 * nt and stride == ipt and Q <= 16 * ks
+    pairs = words[16:16 + 2 * stride * PRE_THREADS].reshape(stride, PRE_THREADS, 2)
+    X2 = x2.astype(np.float32)
+    blk = np.zeros(rb * kst, dtype=np.float32)
+    acc = np.zeros(PRE_THREADS, dtype=np.float32)
+    vals = pairs[:, :, 1].copy().view(np.float32)
+    for i in range(stride):
+        w = pairs[i, :, 0]
+        acc = (vals[i].astype(np.float64) * X2[(w >> 16) & 0xFF] + acc).astype(np.float32)
+        last = (w >> 24) != 0
+        blk[(w & 0xFFFF)[last]] = acc[last]
+        acc[last] = 0.0
+    K = blk.reshape(rb, kst)[:nco, :Q].T.astype(np.float64)  # [q, k3]
+    qm = words[qoff:qoff + Q]
+    k1, path = (qm & 0xFFFF).astype(np.int64), (qm >> 16).astype(np.int64)
+    assert path.max() < npaths and k1.max() < nc1
+    A = W[:, path] * x1[:, k1]  # [C, Q]
+    return A @ K
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [(1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 0),
+                                                   (1, 3, 3, (-1, 0, 1), 1), (2, 2, 2, (0,), 0),
+                                                   (4, 4, 4, (0,), 0), (2, 1, 2, (-1, 0, 1), 2)])
+def test_channel_weighted_pre_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
+    """spingtp_forward_v1_weighted's table, re-enacted on the CPU with per-channel weights, gives for
+    every channel the oracle's path-weighted product with that channel's weights."""
+    from paper_2607_01408_amd.spingtp import paths_host
+
+    words = pre_table_host(L1, L2, LO, spins, basis, channel_weights=True)
+    P = paths_host(L1, L2, LO, spins, basis)
+    assert int(words[13]) == len(P)
+    rng = np.random.default_rng(3 + L1 + 5 * L2 + 25 * LO)
+    C = 4
+    W = rng.standard_normal((C, len(P)))
+    x1 = rng.standard_normal((C, len(spins) * (L1 + 1) ** 2)) * valid_mask(spins, L1)
+    x2 = rng.standard_normal(len(spins) * (L2 + 1) ** 2) * valid_mask(spins, L2)
+    y = emulate_pre_weighted(words, x1, x2, W)
+    for c in range(C):
+        yo = oracle.PathWeightedTensor(L1, L2, LO, spins, basis, W[c]).apply(x1[c:c + 1], x2[None]).reshape(-1)
+        assert np.linalg.norm(y[c] - yo) <= 1e-6 * np.linalg.norm(yo), c
