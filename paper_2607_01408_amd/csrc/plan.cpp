@@ -1098,8 +1098,9 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
             spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 2, dir_b2, &lds_floats, &dense);
         }
         if (k != nullptr && k->family == 4) spingtp::build_mfma_operands(L1, aux);
-        if (kv1->family == 5)
-            spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre, false, weighted ? &dense : nullptr);
+        if (kv1->family == 5 &&
+            !spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre, false, weighted ? &dense : nullptr))
+            return SPINGTP_ERR_INTERNAL;
         // spingtp_backward_v1 on the precontracted kernel: the same table with J x2 (the
         // conjugation identity holds for the unweighted tensor only)
         if (kv1->family == 5 && L1 == L2 && L2 == Lout && !weighted &&
