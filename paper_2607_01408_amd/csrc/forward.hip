@@ -817,10 +817,22 @@ constexpr Registered reg_big() {
                       KernelEntry{B::WAVES, B::UNITS, static_cast<int>(B::LDS_FLOATS * sizeof(float)), 3,
                                   &launch_big<L, SPIN, W, false>, &launch_big<L, SPIN, W, true>}};
 }
-// eight waves (nodes) per round: two waves per SIMD at up to 256 VGPRs, and one round
-// fewer than with five (L = 12: 3 rounds for 19 nodes; L = 16: 4 for 25), each round
-// re-reading the inputs and updating the outputs in global memory
-#define SPINGTP_REG_BIG(L) reg_big<L, true, 8>(), reg_big<L, false, 8>()
+// Nodes per round: eight (two waves per SIMD at up to 256 VGPRs) where the output tile
+// fits in LDS next to eight waves' spectra; for spins at L = 13, 14 the most waves (7, 6)
+// that still leave room for the tile, since a global read-modify-write of the outputs
+// per round costs more than the extra rounds' input re-reads. Below 6 waves (L = 15, 16)
+// the lost latency hiding costs more than the tile saves, so those keep 8 waves and
+// accumulate into global memory.
+template <int L, bool SPIN>
+constexpr int big_waves() {
+    for (int w = 8; w >= 6; --w) {
+        const int spectra = w * 32 * PairShape<L, SPIN>::DS, trig = 2 * (3 * L + 1) * (L + 1);
+        const int tile = 32 * (PairShape<L, SPIN>::NC | 1);
+        if ((spectra + trig + tile) * 4 <= 160 * 1024) return w;
+    }
+    return 8;
+}
+#define SPINGTP_REG_BIG(L) reg_big<L, true, big_waves<L, true>()>(), reg_big<L, false, big_waves<L, false>()>()
 
 const Registered kRegistry[] = {
     SPINGTP_REG(0, 0, 0, false), SPINGTP_REG(1, 1, 1, false), SPINGTP_REG(2, 2, 2, false),
