@@ -36,10 +36,7 @@
  *                                 R_p = (R_{-s} + p (-1)^l R_s)/sqrt2, p = +-1, for
  *                                 |s| > 0; the coefficient of p = +1 is stored in
  *                                 the -|s| block and that of p = -1 in the +|s|
- *                                 block (s = 0 unchanged).  Not built for the
- *                                 large-degree kernels (spingtp_forward with
- *                                 max(L1, L2, Lout) >= 9 and spins {-1,0,1}
- *                                 returns SPINGTP_ERR_UNSUPPORTED at plan creation).
+ *                                 block (s = 0 unchanged).
  *
  * Threading and ownership: a plan is immutable after creation; concurrent
  * spingtp_forward calls with one plan on different streams or threads are safe.

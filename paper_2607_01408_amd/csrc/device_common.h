@@ -236,7 +236,10 @@ __device__ void parity_mix_rows(float* tile, int st, int rows, bool inverse, int
 //   tb  : the node's table block; n0: the global N0 mixing of input 1, followed by
 //         that of input 2 (equal except in the tables of spingtp_backward);
 //   second: this lane transforms input 2.
-template <int L, int LA, bool SPIN>
+//   PAR : the row holds parity-basis coefficients; the |s| = 1 blocks are mixed by
+//         P as they are read (the kernels that stage tiles in LDS mix them there
+//         instead and pass false).
+template <int L, int LA, bool SPIN, bool PAR = false>
 __device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const float* __restrict__ tb,
                                                       const float* __restrict__ n0, bool second, float (&Ac)[L + 1],
                                                       float (&As)[L + 1], float (&Bc)[L + 1], float (&Bs)[L + 1],
@@ -258,6 +261,12 @@ __device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const flo
     if constexpr (SPIN) {
         const float* xm = xr;
         const float* xp = xr + 2 * B;
+        // paper-basis -1 and +1 values of slot q (degree l), up to the factor hs: with
+        // c_+ stored in the -1 block and c_- in the +1 block, x[-1] = (c_+ + c_-)/sqrt2
+        // and x[+1] = (-1)^l (c_+ - c_-)/sqrt2
+        auto vm_of = [&](int q) { return PAR ? xm[q] + xp[q] : xm[q]; };
+        auto vp_of = [&](int q, int l) { return PAR ? ((l & 1) ? xp[q] - xm[q] : xm[q] - xp[q]) : xp[q]; };
+        const float hs = PAR ? 0.70710678118654752440f : 1.f;
 #pragma unroll
         for (int t = 1; t <= L; ++t) {
             float up = 0.f, vp = 0.f, um = 0.f, vm = 0.f;
@@ -265,11 +274,12 @@ __device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const flo
             for (int l = t; l <= L; ++l) {
                 const float wp = tb[Y.aup + tri(LA, t, l)];
                 const float wm = tb[Y.aum + tri(LA, t, l)];
-                up = fmaf(xp[l * l + l + t], wp, up);
-                vp = fmaf(xp[l * l + l - t], wp, vp);
-                um = fmaf(xm[l * l + l + t], wm, um);
-                vm = fmaf(xm[l * l + l - t], wm, vm);
+                up = fmaf(vp_of(l * l + l + t, l), wp, up);
+                vp = fmaf(vp_of(l * l + l - t, l), wp, vp);
+                um = fmaf(vm_of(l * l + l + t), wm, um);
+                vm = fmaf(vm_of(l * l + l - t), wm, vm);
             }
+            if constexpr (PAR) up *= hs, vp *= hs, um *= hs, vm *= hs;
             Bc[t] = up + um;
             Bs[t] = -(vp + vm);
             Cc[t] = vp - vm;
@@ -279,9 +289,10 @@ __device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const flo
 #pragma unroll
         for (int l = 1; l <= L; ++l) {
             const float w = tb[Y.aw + l];
-            wpl = fmaf(xp[l * l + l], w, wpl);
-            wmi = fmaf(xm[l * l + l], w, wmi);
+            wpl = fmaf(vp_of(l * l + l, l), w, wpl);
+            wmi = fmaf(vm_of(l * l + l), w, wmi);
         }
+        if constexpr (PAR) wpl *= hs, wmi *= hs;
         float c[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) c[i] = second ? n0[8 + i] : n0[i];

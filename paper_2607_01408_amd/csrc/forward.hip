@@ -424,7 +424,7 @@ constexpr Owners<PairShape<L, SPIN>::NG> assign_pair_owners() {
 //   Q0[t]: R0c[t] (even lane) or -R0s[t] (odd lane), t >= 1; Q0[0] = R0c[0]
 //   Q1[t]: P1c+P2s (even) or P2c-P1s (odd);  Q2[t]: P1c-P2s (even) or -P2c-P1s (odd)
 //   zslot: Z+ (even lane) or Z- (odd lane), the m3 = 0, |s3| = 1 sums.
-template <int L, bool SPIN, bool BWD>
+template <int L, bool SPIN, bool BWD, bool PAR = false>
 __device__ __forceinline__ void pair_spectra(const float* xr, const float* __restrict__ tb,
                                              const float* __restrict__ g, const float* trl, int sub,
                                              float (&Q0)[L + 1], float (&Q1)[L + 1], float (&Q2)[L + 1],
@@ -434,7 +434,7 @@ __device__ __forceinline__ void pair_spectra(const float* xr, const float* __res
     constexpr int NP = Y.NP;
     constexpr int KP = (NP - 1) / 2;
     float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
-    coef_to_theta_fourier<L, L, SPIN>(xr, tb, g + Y.n0, BWD && sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
+    coef_to_theta_fourier<L, L, SPIN, PAR>(xr, tb, g + Y.n0, BWD && sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
     const float sg = sub ? -1.f : 1.f;
 
     // accumulators: cosine spectra on the even lane, sine spectra on the odd lane
@@ -675,7 +675,10 @@ struct BigShape {
     static constexpr int LDS_FLOATS = DF + TRIG + (OUT_LDS ? UNITS * STO : 0);
 };
 
-template <int L, bool SPIN, int W, bool BWD>
+// PAR (spins only): the plan's basis is the parity-labelled one; a separate
+// instantiation, since a run-time switch between the two step-(A) forms costs the
+// paper-basis kernels registers.
+template <int L, bool SPIN, int W, bool BWD, bool PAR>
 __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_big_kernel(
     const float* __restrict__ x1, const float* __restrict__ x2, float* __restrict__ out, int64_t units, int64_t cpx2,
     const float* __restrict__ tab) {
@@ -708,6 +711,9 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
         const int k = r / (L + 1), t = r - k * (L + 1);
         TR[i] = g[(sb ? Y.sinT : Y.cosT) + k * TM1 + t];
     }
+    // parity basis: the |s| = 1 blocks of each input row are mixed by P as step (A)
+    // reads them, and the finished output rows by P^T before they are final
+    static_assert(SPIN || !PAR, "the parity basis only mixes |s| = 1 blocks");
     if constexpr (SPIN) {  // l = 0 slots of the |s| = 1 blocks
         if constexpr (B::OUT_LDS) {
             if (wave == 0) YT[u * B::STO + (sub ? 2 * BO : 0)] = 0.f;
@@ -724,8 +730,9 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
         const int nr = (B::NT - r * W) < W ? (B::NT - r * W) : W;
         if (node < B::NT) {
             float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
-            pair_spectra<L, SPIN, BWD>(xr, tab + Y.glob + node * Y.pb, g, TR + sub * (B::NP * (L + 1)), sub, Q0, Q1,
-                                  Q2, zslot);
+            const float* tb = tab + Y.glob + node * Y.pb;
+            const float* trl = TR + sub * (B::NP * (L + 1));
+            pair_spectra<L, SPIN, BWD, PAR>(xr, tb, g, trl, sub, Q0, Q1, Q2, zslot);
             pair_publish<L, SPIN>(D + (wave * B::UNITS + u) * P::DS, sub, Q0, Q1, Q2, zslot);
         }
         __syncthreads();
@@ -759,16 +766,26 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
         }
         __syncthreads();
     }
-    if constexpr (B::OUT_LDS) store_tile<B::NC, B::STO>(out + u0 * B::NC, nvalid, YT, tid, B::THREADS);
+    if constexpr (B::OUT_LDS) {
+        if constexpr (PAR) {
+            parity_mix_rows<L>(YT, B::STO, nvalid, true, tid, B::THREADS);
+            __syncthreads();
+        }
+        store_tile<B::NC, B::STO>(out + u0 * B::NC, nvalid, YT, tid, B::THREADS);
+    } else if constexpr (PAR) {
+        // the rows were accumulated in global memory by several waves; the barrier
+        // that ends the last round orders those stores before these reads
+        parity_mix_rows<L>(out + u0 * B::NC, B::NC, nvalid, true, tid, B::THREADS);
+    }
 }
 
-template <int L, bool SPIN, int W, bool BWD>
+template <int L, bool SPIN, int W, bool BWD, bool PAR>
 hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                       const uint32_t*, hipStream_t stream) {
     using B = BigShape<L, SPIN, W>;
     const int64_t blocks = (units + B::UNITS - 1) / B::UNITS;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W, BWD>), dim3(static_cast<unsigned>(blocks)), dim3(B::THREADS),
+    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W, BWD, PAR>), dim3(static_cast<unsigned>(blocks)), dim3(B::THREADS),
                        0, stream, static_cast<const float*>(x1), static_cast<const float*>(x2),
                        static_cast<float*>(out), units, cpx2, tab);
     return hipGetLastError();
@@ -789,6 +806,9 @@ hipError_t launch(const void* x1, const void* x2, void* out, int64_t units, int6
 struct Registered {
     int L1, L2, LO, spin, dtype;
     KernelEntry entry;
+    // bases served: -1 every basis (the tiles are mixed in LDS under the plan's
+    // table flag, or there is no |s| = 1 sector), 0 the two paper bases, 1 the parity one
+    int basis_par = -1;
 };
 
 template <int L1, int L2, int LO, bool SPIN, typename TIO>
@@ -810,12 +830,13 @@ constexpr Registered reg_pair() {
 }
 #define SPINGTP_REG_PAIR(L, SPIN) reg_pair<L, SPIN, float>(), reg_pair<L, SPIN, uint16_t>()
 
-template <int L, bool SPIN, int W>
+template <int L, bool SPIN, int W, bool PAR = false>
 constexpr Registered reg_big() {
     using B = BigShape<L, SPIN, W>;
     return Registered{L, L, L, SPIN ? 1 : 0, 0,
                       KernelEntry{B::WAVES, B::UNITS, static_cast<int>(B::LDS_FLOATS * sizeof(float)), 3,
-                                  &launch_big<L, SPIN, W, false>, &launch_big<L, SPIN, W, true>}};
+                                  &launch_big<L, SPIN, W, false, PAR>, &launch_big<L, SPIN, W, true, PAR>},
+                      SPIN ? (PAR ? 1 : 0) : -1};
 }
 // Nodes per round: eight (two waves per SIMD at up to 256 VGPRs) where the output tile
 // fits in LDS next to eight waves' spectra; for spins at L = 13, 14 the most waves (7, 6)
@@ -832,7 +853,9 @@ constexpr int big_waves() {
     }
     return 8;
 }
-#define SPINGTP_REG_BIG(L) reg_big<L, true, big_waves<L, true>()>(), reg_big<L, false, big_waves<L, false>()>()
+#define SPINGTP_REG_BIG(L)                                                                   \
+    reg_big<L, true, big_waves<L, true>()>(), reg_big<L, true, big_waves<L, true>(), true>(), \
+        reg_big<L, false, big_waves<L, false>()>()
 
 const Registered kRegistry[] = {
     SPINGTP_REG(0, 0, 0, false), SPINGTP_REG(1, 1, 1, false), SPINGTP_REG(2, 2, 2, false),
@@ -848,9 +871,11 @@ const Registered kRegistry[] = {
 
 }  // namespace
 
-const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype) {
+const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype, bool parity) {
     for (const Registered& r : kRegistry)
-        if (r.L1 == L1 && r.L2 == L2 && r.LO == LO && r.spin == spin_mode && r.dtype == dtype) return &r.entry;
+        if (r.L1 == L1 && r.L2 == L2 && r.LO == LO && r.spin == spin_mode && r.dtype == dtype &&
+            (r.basis_par < 0 || r.basis_par == (parity ? 1 : 0)))
+            return &r.entry;
     return nullptr;
 }
 

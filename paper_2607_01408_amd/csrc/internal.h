@@ -71,8 +71,9 @@ void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, u
 
 // Finds the instantiation for (L1, L2, Lout, spin mode, dtype); nullptr if none.
 // find_kernel returns the vector-ALU kernels, find_mfma_kernel the matrix-core
-// kernel where one is built.
-const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
+// kernel where one is built.  parity: the plan's basis is the parity-labelled one
+// with an |s| = 1 sector (the large-degree family has a separate instantiation).
+const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype, bool parity);
 const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
 // The precontracted kernel of spingtp_forward_v1 (x2 shared by the channels of an edge).
 const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int n_spins, int dtype);

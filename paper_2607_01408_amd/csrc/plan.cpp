@@ -1029,10 +1029,9 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     const spingtp::KernelEntry* k = nullptr;
     if ((flags & SPINGTP_KERNEL_VALU) == 0 && !weighted)
         k = spingtp::find_mfma_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
-    if (k == nullptr && !weighted) k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype));
-    // the large-degree kernels have no parity mixing of their tiles
-    if (k != nullptr && k->family == 3 && spin_mode == 1 && (flags & ~kRouteFlags) == SPINGTP_BASIS_PARITY)
-        k = nullptr;
+    const bool parity_tiles = spin_mode == 1 && (flags & ~kRouteFlags) == SPINGTP_BASIS_PARITY;
+    if (k == nullptr && !weighted)
+        k = spingtp::find_kernel(L1, L2, Lout, spin_mode, static_cast<int>(dtype), parity_tiles);
     // the direct kernel: shapes without a Fourier kernel, and the gradients of shapes
     // whose transposed degrees have none, where its LDS tile fits
     auto odd_stride = [](int n) { return (n % 2) ? n + 2 : n + 1; };

@@ -496,9 +496,6 @@ def test_plan_create_route_flags(built_library):
     assert built_library.spingtp_plan_create(7, 7, 7, S, 3, 0, 0x400, ctypes.byref(plan)) == 2
     assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x800, ctypes.byref(plan)) == 1  # tables-only bit
     assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x2000, ctypes.byref(plan)) == 1  # unknown bit
-    # parity-labelled basis on the large-degree kernels (no tile mixing there)
-    assert built_library.spingtp_plan_create(9, 9, 9, S, 3, 0, 2, ctypes.byref(plan)) == 2
-    assert not plan.value
 
 
 @pytest.mark.parametrize("L", [0, 1, 2, 4, 6, 16])

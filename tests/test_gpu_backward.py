@@ -69,7 +69,8 @@ def test_backward_large_degree(L, N, C):
     run_backward(L, S3, N, C, "fp32", 0, seed=L)
 
 
-@pytest.mark.parametrize("L,dtype", [(7, "fp32"), (8, "fp32"), (4, "bf16"), (6, "bf16")])
+@pytest.mark.parametrize("L,dtype", [(7, "fp32"), (8, "fp32"), (4, "bf16"), (6, "bf16"), (12, "fp32"),
+                                     (16, "fp32")])
 def test_backward_parity_basis(L, dtype):
     run_backward(L, S3, 17, 3, dtype, 2, seed=90 + L)
 

@@ -144,10 +144,16 @@ def test_parity_basis_changes_the_map():
     assert float((y0 - y2).abs().max()) > 1e-2
 
 
-def test_parity_basis_large_degree_unsupported():
-    with pytest.raises(SpinGTPError):
-        Plan(9, 9, 9, S3, "fp32", 2)
-    Plan(9, 9, 9, (0,), "fp32", 2)  # no |s| > 0 sector: nothing to mix
+@pytest.mark.parametrize("L", [9, 12, 13, 16])
+def test_parity_basis_large_degree(L):
+    # the large-degree kernels mix the input rows as they read them; the output tile
+    # in LDS (L = 9, 12 with 8 waves, L = 13 with 7) or accumulated in global memory (L = 16)
+    run_and_compare(L, L, L, S3, 37, 3, "fp32", 2, seed=100 + L)
+
+
+def test_parity_basis_scalar_spin_large_degree():
+    # no |s| = 1 sector: the paper-basis kernel serves the parity plan
+    run_and_compare(9, 9, 9, (0,), 29, 5, "fp32", 2, seed=109)
 
 
 def test_small_workload_all_units():
