@@ -251,3 +251,64 @@ class PathWeightedTensor:
     dense = RealGauntTensor.dense
     apply = RealGauntTensor.apply
     vjp = RealGauntTensor.vjp
+
+
+def _path_entries(L1, L2, Lout, spins, basis):
+    """The nonzeros of the unweighted T with their path: (k1, k2, k3, value, path),
+    paths numbered as in PathWeightedTensor (ascending block triples)."""
+    w = PathWeightedTensor(L1, L2, Lout, spins, basis)
+    b = w.base
+    M = b.matrix.tocoo()
+    k1, k2, k3 = M.row // b.n2, M.row % b.n2, M.col
+    trip = np.stack([slot_blocks(spins, L1)[k1], slot_blocks(spins, L2)[k2], slot_blocks(spins, Lout)[k3]], axis=1)
+    lookup = {tuple(p): i for i, p in enumerate(w.paths.tolist())}
+    path = np.array([lookup[tuple(t)] for t in trip.tolist()], dtype=np.int64)
+    return k1, k2, k3, M.data.astype(np.float64), path, len(w.paths)
+
+
+def channel_weighted_v1(x1, x2, weights, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Depthwise product with one weight per (channel, path) and the edge input
+    shared by the channels (App. E.1 mode uvu with V = 1, eq. spin_gtp with
+    per-channel path weights): out[n, c] = T_{W[c]}(x1[n, c], x2[n]), where
+    T_{W[c]} is the PathWeightedTensor of channel c's weights.
+
+    x1 [N, C, ...] (n1 values per unit), x2 [N, ...] (n2 per edge), weights [C, P]."""
+    spins = tuple(spins)
+    x1 = np.asarray(x1, dtype=np.float64)
+    N, C = x1.shape[:2]
+    X1 = x1.reshape(N, C, -1)
+    X2 = np.asarray(x2, dtype=np.float64).reshape(N, -1)
+    W = np.asarray(weights, dtype=np.float64).reshape(C, -1)
+    out = np.stack([PathWeightedTensor(L1, L2, Lout, spins, basis, W[c]).apply(X1[:, c], X2).reshape(N, -1)
+                    for c in range(C)], axis=1) if C else np.zeros((N, 0, len(spins) * (Lout + 1) ** 2))
+    return out.reshape((N, C, len(spins), (Lout + 1) ** 2))
+
+
+def channel_weighted_v1_vjp(x1, x2, weights, g, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Reverse-mode derivative of channel_weighted_v1 for dL/dout = g (float64).
+
+    The product is linear in each of x1, x2 and W, so with T_c = T_{W[c]}:
+      gx1[n,c,k1] = sum_{k2,k3} T_c[k1,k2,k3] x2[n,k2] g[n,c,k3],
+      gx2[n,k2]   = sum_c sum_{k1,k3} T_c[k1,k2,k3] x1[n,c,k1] g[n,c,k3]  (x2 is shared),
+      gW[c,p]     = sum_n sum_{(k1,k2,k3) in path p} T[k1,k2,k3] x1[n,c,k1] x2[n,k2] g[n,c,k3].
+    Returns (gx1 shaped like x1, gx2 shaped like x2, gW [C, P])."""
+    spins = tuple(spins)
+    x1 = np.asarray(x1, dtype=np.float64)
+    x2 = np.asarray(x2, dtype=np.float64)
+    N, C = x1.shape[:2]
+    X1 = x1.reshape(N, C, -1)
+    X2 = x2.reshape(N, -1)
+    G = np.asarray(g, dtype=np.float64).reshape(N, C, -1)
+    W = np.asarray(weights, dtype=np.float64).reshape(C, -1)
+    k1, k2, k3, val, path, n_paths = _path_entries(L1, L2, Lout, spins, basis)
+    gx1 = np.zeros_like(X1)
+    gx2 = np.zeros_like(X2)
+    gW = np.zeros((C, n_paths))
+    for c in range(C):
+        a, b = PathWeightedTensor(L1, L2, Lout, spins, basis, W[c]).vjp(X1[:, c], X2, G[:, c])
+        gx1[:, c] = a
+        gx2 += b
+        # per entry: sum over the edges of x1 x2 g, times T; then summed per path
+        per_entry = (X1[:, c, k1] * X2[:, k2] * G[:, c, k3]).sum(axis=0) * val
+        gW[c] = np.bincount(path, weights=per_entry, minlength=n_paths)
+    return gx1.reshape(x1.shape), gx2.reshape(x2.shape), gW

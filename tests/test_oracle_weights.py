@@ -81,3 +81,76 @@ def test_paths_obey_the_selection_rules(L1, L2, LO, spins, basis):
         (s1, l1), (s2, l2), (s3, l3) = ((spins[i // (L + 1)], i % (L + 1)) for i, L in ((i1, L1), (i2, L2), (i3, LO)))
         assert abs(l1 - l2) <= l3 <= l1 + l2
         assert any(a * s1 + b * s2 == c * s3 for a in (1, -1) for b in (1, -1) for c in (1, -1))
+
+
+# --- per-channel path weights with the edge input shared by the channels (V = 1) ---
+# Pinned against the path-weighted product above (itself pinned to the unweighted
+# oracle) and by central differences of that forward: the product is linear in each
+# of x1, x2 and W, so a central difference is exact up to rounding, and a gradient
+# entry on a wrong path, slot or channel fails it.
+
+CW_CASES = [(1, 1, 1, S3, 0), (2, 2, 2, S3, 2), (1, 3, 3, S3, 0), (2, 1, 2, S5, 1)]
+
+
+def cw_inputs(L1, L2, LO, spins, basis, N, C, seed):
+    P = len(oracle.PathWeightedTensor(L1, L2, LO, spins, basis).paths)
+    rng = np.random.default_rng(seed)
+    x1 = draw(spins, L1, N * C, seed + 1).reshape(N, C, -1)
+    x2 = draw(spins, L2, N, seed + 2)
+    g = draw(spins, LO, N * C, seed + 3).reshape(N, C, -1)
+    return x1, x2, rng.standard_normal((C, P)), g
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CW_CASES)
+def test_channel_weighted_v1_is_the_path_weighted_product_per_channel(L1, L2, LO, spins, basis):
+    x1, x2, W, _ = cw_inputs(L1, L2, LO, spins, basis, 3, 4, 11)
+    y = oracle.channel_weighted_v1(x1, x2, W, L1, L2, LO, spins, basis).reshape(3, 4, -1)
+    for c in range(4):
+        ref = oracle.PathWeightedTensor(L1, L2, LO, spins, basis, W[c]).apply(x1[:, c], x2).reshape(3, -1)
+        assert np.abs(y[:, c] - ref).max() <= 1e-13 * max(1.0, np.abs(ref).max())
+    ones = np.ones_like(W)
+    y1 = oracle.channel_weighted_v1(x1, x2, ones, L1, L2, LO, spins, basis).reshape(3, 4, -1)
+    base = oracle.spingtp(x1.reshape(12, -1), np.repeat(x2, 4, axis=0), L1, L2, LO, spins, basis).reshape(3, 4, -1)
+    assert np.abs(y1 - base).max() <= 1e-12
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CW_CASES)
+def test_channel_weighted_v1_gradients_homogeneity(L1, L2, LO, spins, basis):
+    x1, x2, W, g = cw_inputs(L1, L2, LO, spins, basis, 4, 3, 21)
+    y = oracle.channel_weighted_v1(x1, x2, W, L1, L2, LO, spins, basis).reshape(4, 3, -1)
+    gx1, gx2, gW = oracle.channel_weighted_v1_vjp(x1, x2, W, g, L1, L2, LO, spins, basis)
+    e = float((g * y).sum())
+    for grad, val in ((gx1, x1), (gx2, x2), (gW, W)):
+        assert grad.shape == val.shape
+        assert abs(float((grad * val).sum()) - e) <= 1e-11 * max(1.0, abs(e))
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CW_CASES)
+def test_channel_weighted_v1_gradients_central_differences(L1, L2, LO, spins, basis):
+    N, C = 3, 2
+    x1, x2, W, g = cw_inputs(L1, L2, LO, spins, basis, N, C, 31)
+    gx1, gx2, gW = oracle.channel_weighted_v1_vjp(x1, x2, W, g, L1, L2, LO, spins, basis)
+
+    def f(a, b, w):
+        return float((g * oracle.channel_weighted_v1(a, b, w, L1, L2, LO, spins, basis).reshape(N, C, -1)).sum())
+
+    rng = np.random.default_rng(7)
+    for _ in range(6):  # weights: every sampled (channel, path)
+        c, p = int(rng.integers(C)), int(rng.integers(W.shape[1]))
+        d = np.zeros_like(W)
+        d[c, p] = 1.0
+        fd = (f(x1, x2, W + d) - f(x1, x2, W - d)) / 2.0
+        assert abs(fd - gW[c, p]) <= 1e-11 * max(1.0, abs(fd))
+    valid1 = np.flatnonzero(valid_mask(spins, L1).ravel())
+    valid2 = np.flatnonzero(valid_mask(spins, L2).ravel())
+    for _ in range(4):  # per-unit input and shared edge input
+        n, c, k = int(rng.integers(N)), int(rng.integers(C)), int(rng.choice(valid1))
+        d = np.zeros_like(x1)
+        d[n, c, k] = 1.0
+        fd = (f(x1 + d, x2, W) - f(x1 - d, x2, W)) / 2.0
+        assert abs(fd - gx1[n, c, k]) <= 1e-11 * max(1.0, abs(fd))
+        n, k = int(rng.integers(N)), int(rng.choice(valid2))
+        d = np.zeros_like(x2)
+        d[n, k] = 1.0
+        fd = (f(x1, x2 + d, W) - f(x1, x2 - d, W)) / 2.0
+        assert abs(fd - gx2[n, k]) <= 1e-11 * max(1.0, abs(fd))
