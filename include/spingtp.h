@@ -208,10 +208,40 @@ spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void*
  * path slots fit 480 and output rows 48 (the depthwise runtime table's shapes,
  * degree <= 2 with spins {-1, 0, +1}, (1, 3, 3), degree <= 4 with spin {0});
  * plan creation with the flag fails with SPINGTP_ERR_UNSUPPORTED otherwise.
- * Forward only (no gradients).  Asynchronous, no allocation.
+ * Gradients: spingtp_backward_v1_weighted.  Asynchronous, no allocation.
  */
 spingtp_status spingtp_forward_v1_weighted(spingtp_plan plan, const void* x1, const void* x2,
                                            const float* weights, void* out, int64_t N, int64_t C, void* stream);
+
+/*
+ * Gradients of spingtp_forward_v1_weighted for dL/dout = grad_out.  The product is
+ * linear in each of x1, x2 and the weights, so
+ *   grad_x1[n][c][k1]  = sum_p weights[c][p] sum_{k2,k3 on p} T x2[n][k2] grad_out[n][c][k3],
+ *   grad_x2[n][k2]     = sum_c sum_p weights[c][p] sum_{k1,k3 on p} T x1[n][c][k1] grad_out[n][c][k3],
+ *   grad_weights[c][p] = sum_n sum_{k1,k2,k3 on p} T x1[n][c][k1] x2[n][k2] grad_out[n][c][k3].
+ *   x1, grad_out, grad_x1: device [N][C][n_spins][(L+1)^2] of the plan's dtype (L1,
+ *     Lout, L1), 16-byte aligned; x2, grad_x2: [N][n_spins][(L2+1)^2];
+ *   weights: device fp32 [C][n_paths] (as the forward), grad_weights: device fp32
+ *     [C][n_paths] (written, not accumulated; zero when N = 0); 4-byte aligned;
+ *   workspace: device memory of spingtp_backward_v1_weighted_workspace_size bytes
+ *     or more, 4-byte aligned, overwritten (partial sums over channel tiles and
+ *     edge ranges, added in a fixed order, so results do not depend on scheduling).
+ * All three outputs are required and must not overlap the inputs.  Kernel: one
+ * wave per 64-channel tile and range of edges walks the tensor's nonzeros in three
+ * orders (by k1, by k2, by path) with the tile's weights in LDS; built where the
+ * slot counts and the path count are <= 1022 and the LDS tile fits 160 KB (the
+ * depthwise runtime table's shapes), otherwise SPINGTP_ERR_UNSUPPORTED, as for
+ * plans created without SPINGTP_CHANNEL_WEIGHTS.  Asynchronous on `stream`, no
+ * allocation.
+ */
+spingtp_status spingtp_backward_v1_weighted(spingtp_plan plan, const void* x1, const void* x2,
+                                            const float* weights, const void* grad_out, void* grad_x1,
+                                            void* grad_x2, float* grad_weights, void* workspace,
+                                            size_t workspace_bytes, int64_t N, int64_t C, void* stream);
+
+/* Bytes of workspace spingtp_backward_v1_weighted needs for N edges x C channels
+ * (fp32 partial sums; 0 when N or C is 0).  SPINGTP_ERR_UNSUPPORTED as for it. */
+spingtp_status spingtp_backward_v1_weighted_workspace_size(spingtp_plan plan, int64_t N, int64_t C, size_t* bytes);
 
 /*
  * Gradients of a scalar loss through out = SpinGTP(x1, x2) of spingtp_forward:
@@ -370,6 +400,14 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  * the kernel's instantiations), word 13 the number of paths and word 14 the
  * offset of Q words after the items: path slot q = x1 slot | path << 16, listed
  * path by path; an item's kernel position is dst = k3 KST + q.
+ * With both flags: the entry lists of spingtp_backward_v1_weighted (any degrees):
+ * words [0, 16) NC1, NC2, NCO, NP (paths), NNZ (nonzeros of T), the word offsets of
+ * SEG1, SEG2, SEGP (NC1 + 1, NC2 + 1, NP + 1 list boundaries, counted in entries)
+ * and of LIST1, LIST2, LISTP, zeros.  An entry is two words, a | b << 10 | c << 20
+ * and an fp32 value: LIST1 holds per k1 (path, k2, k3), LIST2 per k2 (path, k1, k3),
+ * LISTP per path (k1, k2, k3); each segment is padded to a multiple of 8 entries
+ * of value 0 whose fields are the row lengths (NP, NC1, NC2 or NCO: the zero
+ * columns).  SPINGTP_ERR_UNSUPPORTED where the kernel does not take the shape.
  * Writes min(capacity, total) words to `words` (may be NULL when capacity is 0)
  * and the total to *count.
  */

@@ -13,7 +13,8 @@ EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "s
             "spingtp_mfma_operands_host", "spingtp_forward_v1", "spingtp_plan_kernel_info_v1",
             "spingtp_pre_table_host", "spingtp_backward", "spingtp_conj_map_host", "spingtp_backward_v1",
             "spingtp_backward_v1_workspace_size", "spingtp_direct_table_host", "spingtp_paths_host",
-            "spingtp_plan_create_weighted", "spingtp_forward_v1_weighted")
+            "spingtp_plan_create_weighted", "spingtp_forward_v1_weighted", "spingtp_backward_v1_weighted",
+            "spingtp_backward_v1_weighted_workspace_size")
 
 _lib = None
 
@@ -45,6 +46,12 @@ def lib() -> ctypes.CDLL:
         L.spingtp_forward_v1_weighted.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                                   ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
         L.spingtp_forward_v1_weighted.restype = ctypes.c_int
+        L.spingtp_backward_v1_weighted.argtypes = [ctypes.c_void_p] + [ctypes.c_void_p] * 8 + [
+            ctypes.c_size_t, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        L.spingtp_backward_v1_weighted.restype = ctypes.c_int
+        L.spingtp_backward_v1_weighted_workspace_size.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                                                  ctypes.POINTER(ctypes.c_size_t)]
+        L.spingtp_backward_v1_weighted_workspace_size.restype = ctypes.c_int
         L.spingtp_forward.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
         L.spingtp_forward.restype = ctypes.c_int

@@ -9,7 +9,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libspingtp.so")
-SOURCES = ["plan.cpp", "api.cpp", "forward.hip", "forward_mfma.hip", "forward_pre.hip", "forward_pre_large.hip", "forward_pre_weighted.hip", "forward_direct.hip", "backward.hip"]
+SOURCES = ["plan.cpp", "api.cpp", "forward.hip", "forward_mfma.hip", "forward_pre.hip", "forward_pre_large.hip", "forward_pre_weighted.hip", "forward_direct.hip", "backward.hip", "backward_v1w.hip"]
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in generated code.
 HIP_FLAGS = [

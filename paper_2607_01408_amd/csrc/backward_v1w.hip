@@ -1,0 +1,268 @@
+// Gradients of the per-channel path-weighted product with the edge input shared by
+// the channels (spingtp_backward_v1_weighted; the forward is spingtp_forward_v1_weighted).
+//
+// The forward is out[n,c,k3] = sum_p W[c,p] sum_{(k1,k2,k3) in p} T[k1,k2,k3] x1[n,c,k1] x2[n,k2]
+// (App. E.1 mode uvu with V = 1 and one weight per channel and path of eq. spin_gtp,
+// Sec. 3.4).  It is linear in each of x1, x2 and W, so for dL/dout = g
+//   gx1[n,c,k1] = sum over the entries with k1 of W[c,p] T x2[n,k2] g[n,c,k3],
+//   gx2[n,k2]   = sum_c sum over the entries with k2 of W[c,p] T x1[n,c,k1] g[n,c,k3],
+//   gW[c,p]     = sum_n sum over the entries of p of T x1[n,c,k1] x2[n,k2] g[n,c,k3],
+// three sums over the nonzeros of T in three orders (by k1, by k2, by path).
+//
+// One wave per workgroup, one channel per lane: the workgroup owns a 64-channel tile
+// and a contiguous range of edges.  The tile's weight rows stay in LDS for the whole
+// range; per edge the x1 and g rows of the tile and the x2 row are staged in LDS
+// (odd row strides, so the per-lane gathers are conflict-free, and a zero column
+// past each row that the lists' padding entries point at).  The entry lists are
+// wave-uniform and come in through scalar loads, eight entries per step.
+//   * gW: per path, each lane sums its channel's products in a register and adds
+//     them into the workspace row of its edge range ([range][path][channel], so the
+//     64 lanes of a path touch 256 contiguous bytes);
+//   * gx2: per k2, each lane sums its channel's terms into an LDS column, and the
+//     lanes then add the 64 columns in a fixed order into the workspace row of the
+//     channel tile ([tile][edge][k2]);
+//   * gx1: per k1, each lane's sum goes into its x1 row in LDS (no longer read), and
+//     the tile leaves in coalesced stores.
+// A second kernel adds the partial sums of gx2 over the channel tiles and those of
+// gW over the edge ranges, in a fixed order: the results do not depend on scheduling.
+//
+// Table (uint32 words, built by build_bwd_v1w_table):
+//   [0, 16)  NC1, NC2, NCO, NP (paths), NNZ, then the word offsets of SEG1, SEG2,
+//            SEGP (list boundaries, in entries: NC1 + 1, NC2 + 1, NP + 1 words) and of
+//            LIST1, LIST2, LISTP; zeros
+//   each list entry is two words: a | b << 10 | c << 20, fp32 value;
+//   LIST1 (per k1): a = path, b = k2, c = k3;  LIST2 (per k2): a = path, b = k1, c = k3;
+//   LISTP (per path): a = k1, b = k2, c = k3.  Every segment is padded to a multiple
+//   of eight entries with value 0 whose indices point at the zero columns.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdint>
+
+#include "device_common.h"
+#include "internal.h"
+
+namespace spingtp {
+namespace {
+
+constexpr int kBw1wLanes = 64;
+
+__device__ __forceinline__ float bw_load(const float* p) { return *p; }
+__device__ __forceinline__ float bw_load(const uint16_t* p) { return bf16_to_f32(*p); }
+__device__ __forceinline__ void bw_store(float* p, float v) { *p = v; }
+__device__ __forceinline__ void bw_store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+
+// rows [0, nrows) of a contiguous [nrows][nc] block into an LDS tile of stride st
+template <typename TIO>
+__device__ __forceinline__ void bw_load_rows(const TIO* __restrict__ src, int nrows, int nc, int st, float* dst,
+                                             int lane) {
+    const int n = nrows * nc;
+    for (int e = lane; e < n; e += kBw1wLanes) {
+        const int r = e / nc;
+        dst[r * st + (e - r * nc)] = bw_load(src + e);
+    }
+}
+
+// Sum over one segment of a list: the term of an entry is value * f(a, b, c).
+template <typename F>
+__device__ __forceinline__ float bw_segment(const uint32_t* __restrict__ list, int e0, int e1, F&& term) {
+    float acc0 = 0.f, acc1 = 0.f;
+    for (int e = e0; e < e1; e += 8) {
+        const uint32_t* w = list + 2 * e;
+#pragma unroll
+        for (int i = 0; i < 8; i += 2) {
+            const uint32_t i0 = w[2 * i], i1 = w[2 * i + 2];
+            acc0 = fmaf(__uint_as_float(w[2 * i + 1]), term(i0 & 0x3ffu, (i0 >> 10) & 0x3ffu, i0 >> 20), acc0);
+            acc1 = fmaf(__uint_as_float(w[2 * i + 3]), term(i1 & 0x3ffu, (i1 >> 10) & 0x3ffu, i1 >> 20), acc1);
+        }
+    }
+    return acc0 + acc1;
+}
+
+__host__ __device__ constexpr int bw_stride(int n) { return (n + 1) | 1; }  // odd, with a zero column
+
+template <typename TIO>
+__global__ __launch_bounds__(kBw1wLanes) void spingtp_bwd_v1w_kernel(
+    const TIO* __restrict__ x1, const TIO* __restrict__ x2, const float* __restrict__ wts, const TIO* __restrict__ g,
+    TIO* __restrict__ gx1, float* __restrict__ ws_x2, float* __restrict__ ws_w, int64_t N, int64_t C, int64_t epg,
+    const uint32_t* __restrict__ tab) {
+    extern __shared__ float lds[];
+    const int nc1 = static_cast<int>(tab[0]), nc2 = static_cast<int>(tab[1]), nco = static_cast<int>(tab[2]);
+    const int np = static_cast<int>(tab[3]);
+    const uint32_t* __restrict__ seg1 = tab + tab[5];
+    const uint32_t* __restrict__ seg2 = tab + tab[6];
+    const uint32_t* __restrict__ segp = tab + tab[7];
+    const uint32_t* __restrict__ list1 = tab + tab[8];
+    const uint32_t* __restrict__ list2 = tab + tab[9];
+    const uint32_t* __restrict__ listp = tab + tab[10];
+    const int stw = bw_stride(np), st1 = bw_stride(nc1), sto = bw_stride(nco), st2 = bw_stride(nc2);
+    float* Wt = lds;                       // [64][stw] weights of the tile's channels
+    float* X1 = Wt + kBw1wLanes * stw;     // [64][st1] x1 rows, then the gx1 rows
+    float* G = X1 + kBw1wLanes * st1;      // [64][sto] grad_out rows
+    float* T2 = G + kBw1wLanes * sto;      // [64][st2] per-lane gx2 terms
+    float* X2 = T2 + kBw1wLanes * st2;     // [st2] the edge's x2 row
+
+    const int lane = threadIdx.x;
+    const int64_t group = blockIdx.x, tile = blockIdx.y;
+    const int64_t c0 = tile * kBw1wLanes;
+    const int nch = static_cast<int>(C - c0 < kBw1wLanes ? C - c0 : kBw1wLanes);
+    const int64_t n_begin = group * epg;
+    const int64_t n_end = n_begin + epg < N ? n_begin + epg : N;
+    const bool cvalid = lane < nch;
+    const int64_t c = c0 + lane;
+
+    // zero everything once (zero columns and the rows past nch stay zero: the per-edge
+    // loads write only rows < nch and columns < nc), then the weight rows
+    const int total = kBw1wLanes * (stw + st1 + sto + st2) + st2;
+    for (int i = lane; i < total; i += kBw1wLanes) lds[i] = 0.f;
+    __syncthreads();
+    for (int e = lane; e < nch * np; e += kBw1wLanes) {
+        const int r = e / np;
+        Wt[r * stw + (e - r * np)] = wts[c0 * np + e];
+    }
+    const float* Wr = Wt + lane * stw;
+    float* X1r = X1 + lane * st1;
+    const float* Gr = G + lane * sto;
+    float* T2r = T2 + lane * st2;
+
+    for (int64_t n = n_begin; n < n_end; ++n) {
+        __syncthreads();
+        const int64_t row0 = n * C + c0;
+        bw_load_rows(x1 + row0 * nc1, nch, nc1, st1, X1, lane);
+        bw_load_rows(g + row0 * nco, nch, nco, sto, G, lane);
+        for (int k = lane; k < nc2; k += kBw1wLanes) X2[k] = bw_load(x2 + n * nc2 + k);
+        __syncthreads();
+
+        // gW: one partial sum per (edge range, path, channel)
+        for (int p = 0; p < np; ++p) {
+            const float acc = bw_segment(listp, static_cast<int>(segp[p]), static_cast<int>(segp[p + 1]),
+                                         [&](uint32_t a, uint32_t b, uint32_t cc) { return X2[b] * (X1r[a] * Gr[cc]); });
+            if (cvalid) {
+                float* dst = ws_w + (group * np + p) * C + c;
+                *dst = n == n_begin ? acc : *dst + acc;
+            }
+        }
+        // gx2: per-lane terms, then the column sums of the tile
+        for (int k2 = 0; k2 < nc2; ++k2)
+            T2r[k2] = bw_segment(list2, static_cast<int>(seg2[k2]), static_cast<int>(seg2[k2 + 1]),
+                                 [&](uint32_t a, uint32_t b, uint32_t cc) { return Wr[a] * (X1r[b] * Gr[cc]); });
+        __syncthreads();
+        for (int k2 = lane; k2 < nc2; k2 += kBw1wLanes) {
+            float s = 0.f;
+            for (int r = 0; r < kBw1wLanes; ++r) s += T2[r * st2 + k2];
+            ws_x2[(tile * N + n) * nc2 + k2] = s;
+        }
+        // gx1 into the x1 rows (the gW and gx2 sums above were their last readers)
+        for (int k1 = 0; k1 < nc1; ++k1)
+            X1r[k1] = bw_segment(list1, static_cast<int>(seg1[k1]), static_cast<int>(seg1[k1 + 1]),
+                                 [&](uint32_t a, uint32_t b, uint32_t cc) { return X2[b] * (Wr[a] * Gr[cc]); });
+        __syncthreads();
+        TIO* dst = gx1 + row0 * nc1;
+        for (int e = lane; e < nch * nc1; e += kBw1wLanes) {
+            const int r = e / nc1;
+            bw_store(dst + e, X1[r * st1 + (e - r * nc1)]);
+        }
+    }
+}
+
+// gx2[n,k2] = sum over the channel tiles; gW[c,p] = sum over the edge ranges (fixed order)
+template <typename TIO>
+__global__ __launch_bounds__(256) void spingtp_bwd_v1w_reduce_kernel(const float* __restrict__ ws_x2,
+                                                                     const float* __restrict__ ws_w,
+                                                                     TIO* __restrict__ gx2, float* __restrict__ gw,
+                                                                     int64_t N, int nc2, int64_t tiles, int64_t C,
+                                                                     int np, int64_t groups) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t nx2 = N * nc2;
+    if (i < nx2) {
+        float s = 0.f;
+        for (int64_t t = 0; t < tiles; ++t) s += ws_x2[t * nx2 + i];
+        bw_store(gx2 + i, s);
+    } else if (i < nx2 + C * np) {
+        const int64_t j = i - nx2;
+        const int64_t ch = j / np, p = j - ch * np;
+        float s = 0.f;
+        for (int64_t r = 0; r < groups; ++r) s += ws_w[(r * np + p) * C + ch];
+        gw[j] = s;
+    }
+}
+
+template <typename TIO>
+hipError_t launch_typed(const void* x1, const void* x2, const float* w, const void* g, void* gx1, void* gx2,
+                        float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab,
+                        hipStream_t stream) {
+    const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
+    int64_t groups = 0, epg = 0;
+    bw1w_groups(N, C, &groups, &epg);
+    float* ws_x2 = ws;
+    float* ws_w = ws + tiles * N * s.nc2;
+    if (groups > 0 && tiles > 0) {
+        if (groups > 0x7fffffff || tiles > 0xffff) return hipErrorInvalidValue;
+        const size_t bytes = static_cast<size_t>(s.lds_floats) * sizeof(float);
+        if (bytes > 65536) {  // raise the dynamic LDS limit once per device
+            constexpr int kMaxDevices = 64;
+            static std::atomic<bool> raised[kMaxDevices];
+            int dev = 0;
+            if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+            if (!raised[dev].load(std::memory_order_acquire)) {
+                const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&spingtp_bwd_v1w_kernel<TIO>),
+                                                         hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                         static_cast<int>(kBw1wMaxLdsFloats * sizeof(float)));
+                if (e != hipSuccess) return e;
+                raised[dev].store(true, std::memory_order_release);
+            }
+        }
+        hipLaunchKernelGGL(spingtp_bwd_v1w_kernel<TIO>, dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)),
+                           dim3(kBw1wLanes), bytes, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w,
+                           static_cast<const TIO*>(g), static_cast<TIO*>(gx1), ws_x2, ws_w, N, C, epg, tab);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const int64_t outs = N * s.nc2 + C * s.np;
+    if (outs > 0) {
+        const int64_t blocks = (outs + 255) / 256;
+        if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(spingtp_bwd_v1w_reduce_kernel<TIO>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                           stream, ws_x2, ws_w, static_cast<TIO*>(gx2), gw, N, s.nc2, groups > 0 ? tiles : 0, C, s.np,
+                           groups);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+}  // namespace
+
+void bw1w_groups(int64_t N, int64_t C, int64_t* groups, int64_t* epg) {
+    // about kBw1wTargetWaves workgroups of one wave over the channel tiles and edge ranges
+    const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
+    if (N <= 0 || tiles <= 0) {
+        *groups = 0;
+        *epg = 0;
+        return;
+    }
+    int64_t want = kBw1wTargetWaves / tiles;
+    if (want < 1) want = 1;
+    if (want > N) want = N;
+    *epg = (N + want - 1) / want;
+    *groups = (N + *epg - 1) / *epg;
+}
+
+size_t bw1w_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s) {
+    int64_t groups = 0, epg = 0;
+    bw1w_groups(N, C, &groups, &epg);
+    const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
+    return static_cast<size_t>(tiles * N * s.nc2 + groups * s.np * C);
+}
+
+hipError_t launch_bwd_v1w(int dtype, const void* x1, const void* x2, const float* w, const void* g, void* gx1,
+                          void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
+                          const uint32_t* tab, hipStream_t stream) {
+    if (s.lds_floats <= 0 || s.lds_floats > kBw1wMaxLdsFloats) return hipErrorInvalidValue;
+    if (s.lds_floats != kBw1wLanes * (bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nco) + bw_stride(s.nc2)) +
+                            bw_stride(s.nc2))
+        return hipErrorInvalidValue;  // the kernel carves its LDS from the table's sizes
+    return dtype == 0 ? launch_typed<float>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream)
+                      : launch_typed<uint16_t>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream);
+}
+
+}  // namespace spingtp

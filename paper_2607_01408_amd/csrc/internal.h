@@ -146,6 +146,29 @@ spingtp_status run_forward(spingtp_plan plan, const KernelEntry* k, const void* 
                            int64_t N, int64_t C, bool shared_x2, void* stream, const float* tab = nullptr,
                            bool backward = false, const uint32_t* aux = nullptr);
 
+// Gradients of the per-channel path-weighted product (backward_v1w.hip).
+// Sizes of its table; lds_floats: the LDS of one workgroup (weight, x1, grad_out and
+// gx2-term tiles of 64 rows and the x2 row).
+struct Bw1wShape {
+    int nc1, nc2, nco, np, lds_floats;
+};
+constexpr int kBw1wMaxLdsFloats = 40960;  // 160 KB
+constexpr int kBw1wMaxIndex = 1022;       // 10-bit entry fields; a row's zero column sits at index n
+constexpr int kBw1wTargetWaves = 1024;    // workgroups (one wave each) a launch aims for
+// Entry lists of the table (layout in backward_v1w.hip); false where an index or the
+// LDS tile does not fit.  `dense`: the tensor of build_dense_tensor if the caller has it.
+bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                         std::vector<uint32_t>& out, Bw1wShape* shape, const std::vector<double>* dense = nullptr);
+// Edge ranges of a launch: `groups` ranges of `epg` edges (0, 0 when N or C is 0).
+void bw1w_groups(int64_t N, int64_t C, int64_t* groups, int64_t* epg);
+// Workspace of a launch, in floats: gx2 partial sums per channel tile and edge, then
+// gW partial sums per edge range, path and channel.
+size_t bw1w_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s);
+// dtype 0: fp32 x1, x2, grad_out, gx1, gx2; 1: bf16.  Weights and gW are fp32.
+hipError_t launch_bwd_v1w(int dtype, const void* x1, const void* x2, const float* w, const void* g, void* gx1,
+                          void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
+                          const uint32_t* tab, hipStream_t stream);
+
 // Paths of the instruction-weighted product (spingtp_paths_host): the block triples
 // (i (L+1) + l of spin index i and degree l, per input and output) on which T has
 // a nonzero entry, in ascending lexicographic order.
@@ -176,6 +199,8 @@ struct spingtp_plan_s {
     uint32_t* d_pre_bwd;  // the same with J x2 (spingtp_backward_v1), nullptr if not used
     uint32_t* d_pre_w;    // the per-channel path-weighted table (SPINGTP_CHANNEL_WEIGHTS), nullptr if not built
     const spingtp::KernelEntry* kernel_v1w;  // its kernel (spingtp_forward_v1_weighted)
+    uint32_t* d_bw1w;  // entry lists of spingtp_backward_v1_weighted, nullptr if not built
+    spingtp::Bw1wShape bw1w;
     float* d_tab_bwd;  // tables of spingtp_backward (d_tab when equal), nullptr without a backward
     bool own_tab_bwd;  // d_tab_bwd is a separate allocation
     uint32_t* d_dir;     // direct-kernel entry table of the forward (family 6), nullptr if not used

@@ -604,6 +604,91 @@ bool build_pre_tables_channel_weighted(int L1, int L2, int LO, const int* spins,
                                static_cast<int>(paths.size()), out);
 }
 
+bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                         std::vector<uint32_t>& out, Bw1wShape* shape, const std::vector<double>* dense) {
+    std::vector<double> own;
+    if (dense == nullptr) build_dense_tensor(L1, L2, LO, spins, n_spins, flags, own);
+    const std::vector<double>& T = dense != nullptr ? *dense : own;
+    std::vector<std::array<int, 3>> paths;
+    tensor_paths(L1, L2, LO, spins, n_spins, T, paths);
+    const std::vector<int> b1 = slot_blocks(L1, spins, n_spins), b2 = slot_blocks(L2, spins, n_spins),
+                           b3 = slot_blocks(LO, spins, n_spins);
+    const int nc1 = static_cast<int>(b1.size()), nc2 = static_cast<int>(b2.size()), nco = static_cast<int>(b3.size());
+    const int np = static_cast<int>(paths.size());
+    if (std::max(std::max(nc1, nc2), std::max(nco, np)) > kBw1wMaxIndex) return false;
+    auto st = [](int n) { return (n + 1) | 1; };
+    const int lds = 64 * (st(np) + st(nc1) + st(nco) + st(nc2)) + st(nc2);
+    if (lds > kBw1wMaxLdsFloats) return false;
+    struct Ent {
+        int k1, k2, k3, p;
+        float v;
+    };
+    std::vector<Ent> ents;
+    std::map<std::array<int, 3>, int> index;
+    for (int p = 0; p < np; ++p) index[paths[p]] = p;
+    for (int k1 = 0; k1 < nc1; ++k1)
+        for (int k2 = 0; k2 < nc2; ++k2)
+            for (int k3 = 0; k3 < nco; ++k3) {
+                const double v = T[(static_cast<size_t>(k1) * nc2 + k2) * nco + k3];
+                if (std::fabs(v) <= 1e-12) continue;  // quadrature round-off of an exact zero
+                ents.push_back({k1, k2, k3, index.at({b1[k1], b2[k2], b3[k3]}), static_cast<float>(v)});
+            }
+    // one list: entries grouped by key (stable, so ascending (k1, k2, k3) inside a
+    // group), each group padded to a multiple of 8 with zero-column entries
+    struct List {
+        std::vector<uint32_t> seg, words;
+    };
+    auto make = [&](int nkeys, auto key, auto fields, std::array<int, 3> pad) {
+        List l;
+        std::vector<std::vector<const Ent*>> by(nkeys);
+        for (const Ent& e : ents) by[key(e)].push_back(&e);
+        auto put = [&](std::array<int, 3> f, float v) {
+            l.words.push_back(static_cast<uint32_t>(f[0]) | (static_cast<uint32_t>(f[1]) << 10) |
+                              (static_cast<uint32_t>(f[2]) << 20));
+            uint32_t bits = 0;
+            std::memcpy(&bits, &v, 4);
+            l.words.push_back(bits);
+        };
+        uint32_t at = 0;
+        for (int k = 0; k < nkeys; ++k) {
+            l.seg.push_back(at);
+            for (const Ent* e : by[k]) put(fields(*e), e->v);
+            size_t n = by[k].size();
+            for (; n % 8 != 0; ++n) put(pad, 0.f);
+            at += static_cast<uint32_t>(n);
+        }
+        l.seg.push_back(at);
+        return l;
+    };
+    const List l1 = make(
+        nc1, [](const Ent& e) { return e.k1; }, [](const Ent& e) { return std::array<int, 3>{e.p, e.k2, e.k3}; },
+        {np, nc2, nco});
+    const List l2 = make(
+        nc2, [](const Ent& e) { return e.k2; }, [](const Ent& e) { return std::array<int, 3>{e.p, e.k1, e.k3}; },
+        {np, nc1, nco});
+    const List lp = make(
+        np, [](const Ent& e) { return e.p; }, [](const Ent& e) { return std::array<int, 3>{e.k1, e.k2, e.k3}; },
+        {nc1, nc2, nco});
+    out.assign(16, 0u);
+    out[0] = static_cast<uint32_t>(nc1);
+    out[1] = static_cast<uint32_t>(nc2);
+    out[2] = static_cast<uint32_t>(nco);
+    out[3] = static_cast<uint32_t>(np);
+    out[4] = static_cast<uint32_t>(ents.size());
+    const List* lists[3] = {&l1, &l2, &lp};
+    for (int i = 0; i < 3; ++i) {
+        out[5 + i] = static_cast<uint32_t>(out.size());
+        out.insert(out.end(), lists[i]->seg.begin(), lists[i]->seg.end());
+    }
+    for (int i = 0; i < 3; ++i) {
+        out.resize((out.size() + 1) & ~size_t{1});  // 8-byte aligned entries
+        out[8 + i] = static_cast<uint32_t>(out.size());
+        out.insert(out.end(), lists[i]->words.begin(), lists[i]->words.end());
+    }
+    if (shape != nullptr) *shape = Bw1wShape{nc1, nc2, nco, np, lds};
+    return true;
+}
+
 // Dense real tensor T[k1][k2][k3] = Re sum conj(Q3) G Q1 Q2 (see spingtp.h).
 // G^{(l3,m3,s3)}_{(l1,m1,s1)(l2,m2,s2)} = 2 pi sum_j w_j Y1(theta_j) Y2(theta_j) Y3(theta_j) for
 // s3 = s1 + s2, m3 = m1 + m2 (the phi integral of the other combinations vanishes), on the
@@ -936,17 +1021,19 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
     if (count == nullptr || (capacity > 0 && words == nullptr)) return SPINGTP_ERR_INVALID_ARG;
     const bool backward = (flags & SPINGTP_TABLES_BACKWARD) != 0;
     flags &= ~SPINGTP_TABLES_BACKWARD;
-    if (backward && (L1 != L2 || L2 != Lout)) return SPINGTP_ERR_UNSUPPORTED;
+    if (backward && (flags & SPINGTP_CHANNEL_WEIGHTS) == 0 && (L1 != L2 || L2 != Lout)) return SPINGTP_ERR_UNSUPPORTED;
     int spin_mode = 0;
     const spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
     const bool channel_weights = (flags & SPINGTP_CHANNEL_WEIGHTS) != 0;
-    if (channel_weights && backward) return SPINGTP_ERR_INVALID_ARG;
     if (!channel_weights && spingtp::find_pre_kernel(L1, L2, Lout, n_spins, 0) == nullptr)
         return SPINGTP_ERR_UNSUPPORTED;
     try {
         std::vector<uint32_t> w;
-        if (channel_weights) {  // the table of spingtp_forward_v1_weighted, as a plan with the flag builds it
+        if (channel_weights && backward) {  // the entry lists of spingtp_backward_v1_weighted
+            if (!spingtp::build_bwd_v1w_table(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, w, nullptr))
+                return SPINGTP_ERR_UNSUPPORTED;
+        } else if (channel_weights) {  // the table of spingtp_forward_v1_weighted, as a plan with the flag builds it
             const int nc1 = n_spins * (L1 + 1) * (L1 + 1), nc2 = n_spins * (L2 + 1) * (L2 + 1);
             const int nco = n_spins * (Lout + 1) * (Lout + 1);
             int rows = 0, ks = 0, nt = 0;
@@ -1059,7 +1146,8 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
 
     std::vector<double> tab;
     std::vector<double> tab_bwd;
-    std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2, pre_w;
+    std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2, pre_w, bw1w;
+    spingtp::Bw1wShape bw1w_shape{};
     const spingtp::KernelEntry* kw = nullptr;
     bool has_backward = false, same_bwd = false;
     try {
@@ -1083,14 +1171,23 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
             const int nc2 = n_spins * (L2 + 1) * (L2 + 1), nco = n_spins * (Lout + 1) * (Lout + 1);
             const int nc1 = n_spins * (L1 + 1) * (L1 + 1);
             int rows = 0, ks = 0, nt = 0;
-            if (nc2 > spingtp::kPreMaxNC) return SPINGTP_ERR_UNSUPPORTED;
-            // with ks = 0 the builder only counts the path slots
-            (void)spingtp::build_pre_tables_channel_weighted(L1, L2, Lout, spins, n_spins, basis, 0, pre_w, &rows);
-            kw = spingtp::find_pre_weighted_kernel((std::max(rows, nc1) + 15) / 16, (nco + 15) / 16,
-                                                   static_cast<int>(dtype), &ks, &nt);
+            if (nc2 <= spingtp::kPreMaxNC) {
+                // with ks = 0 the builder only counts the path slots
+                (void)spingtp::build_pre_tables_channel_weighted(L1, L2, Lout, spins, n_spins, basis, 0, pre_w,
+                                                                 &rows);
+                kw = spingtp::find_pre_weighted_kernel((std::max(rows, nc1) + 15) / 16, (nco + 15) / 16,
+                                                       static_cast<int>(dtype), &ks, &nt);
+            }
             if (kw == nullptr ||
-                !spingtp::build_pre_tables_channel_weighted(L1, L2, Lout, spins, n_spins, basis, ks, pre_w, &rows))
-                return SPINGTP_ERR_UNSUPPORTED;
+                !spingtp::build_pre_tables_channel_weighted(L1, L2, Lout, spins, n_spins, basis, ks, pre_w, &rows)) {
+                kw = nullptr;
+                pre_w.clear();
+            }
+            // the gradients (spingtp_backward_v1_weighted) where their tiles fit; a plan
+            // needs the forward or the gradients
+            if (!spingtp::build_bwd_v1w_table(L1, L2, Lout, spins, n_spins, basis, bw1w, &bw1w_shape))
+                bw1w.clear();
+            if (pre_w.empty() && bw1w.empty()) return SPINGTP_ERR_UNSUPPORTED;
         }
         if (kd != nullptr && !fourier_bwd) {
             spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 1, dir_b1, &lds_floats, &dense);
@@ -1149,8 +1246,9 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     if (e == hipSuccess) e = upload(dir, &ddir);
     if (e == hipSuccess) e = upload(dir_b1, &ddir1);
     if (e == hipSuccess) e = upload(dir_b2, &ddir2);
-    uint32_t* dprew = nullptr;
+    uint32_t *dprew = nullptr, *dbw1w = nullptr;
     if (e == hipSuccess) e = upload(pre_w, &dprew);
+    if (e == hipSuccess) e = upload(bw1w, &dbw1w);
     if (e == hipSuccess && has_backward && !same_bwd) {
         std::vector<float> f(tab_bwd.size());
         for (size_t i = 0; i < tab_bwd.size(); ++i) f[i] = static_cast<float>(tab_bwd[i]);
@@ -1166,6 +1264,7 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
         if (ddir1 != nullptr) (void)hipFree(ddir1);
         if (ddir2 != nullptr) (void)hipFree(ddir2);
         if (dprew != nullptr) (void)hipFree(dprew);
+        if (dbw1w != nullptr) (void)hipFree(dbw1w);
         if (d != nullptr) (void)hipFree(d);
     };
     if (e != hipSuccess) {
@@ -1199,6 +1298,8 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     p->dir_lds_floats = dir_lds;
     p->d_pre_w = dprew;
     p->kernel_v1w = dprew != nullptr ? kw : nullptr;
+    p->d_bw1w = dbw1w;
+    p->bw1w = bw1w_shape;
     p->kernel = k;
     p->kernel_v1 = kv1;
     *out_plan = p;
@@ -1252,6 +1353,7 @@ spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
     if (e == hipSuccess && plan->d_dir_b1 != nullptr) e = hipFree(plan->d_dir_b1);
     if (e == hipSuccess && plan->d_dir_b2 != nullptr) e = hipFree(plan->d_dir_b2);
     if (e == hipSuccess && plan->d_pre_w != nullptr) e = hipFree(plan->d_pre_w);
+    if (e == hipSuccess && plan->d_bw1w != nullptr) e = hipFree(plan->d_bw1w);
     if (e == hipSuccess && plan->d_pre != nullptr) e = hipFree(plan->d_pre);
     if (e == hipSuccess && plan->d_pre_bwd != nullptr) e = hipFree(plan->d_pre_bwd);
     if (e == hipSuccess && plan->own_tab_bwd) e = hipFree(plan->d_tab_bwd);

@@ -68,7 +68,7 @@ def mfma_operands_host(L):
 def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, backward=False, channel_weights=False):
     """spingtp_pre_table_host: the tensor table of the precontracted kernel (uint32 words); with
     backward=True the table of spingtp_backward_v1, with channel_weights=True that of
-    spingtp_forward_v1_weighted."""
+    spingtp_forward_v1_weighted, with both the entry lists of spingtp_backward_v1_weighted."""
     arr, n = _spin_array(spins)
     basis = basis | (0x800 if backward else 0) | (CHANNEL_WEIGHTS if channel_weights else 0)
     count = ctypes.c_size_t(0)
@@ -287,6 +287,41 @@ class Plan:
                                                   n.value if ws is not None else 0, N, C,
                                                   ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_v1")
         return gx1, gx2
+
+    def backward_v1_weighted(self, x1, x2, weights, grad_out, stream=None):
+        """spingtp_backward_v1_weighted: (grad_x1 [N, C, ...], grad_x2 [N, 1, ...], grad_weights [C, n_paths]
+        fp32) through forward_v1_weighted; the workspace comes from torch's allocator."""
+        import torch
+
+        if x2.dim() == 3:
+            x2 = x2.unsqueeze(1)
+        N, C = x1.shape[0], x1.shape[1]
+        for t, shape in ((x1, (N, C) + tuple(self.shape_in(1))), (x2, (N, 1) + tuple(self.shape_in(2))),
+                         (grad_out, (N, C) + tuple(self.shape_out))):
+            if (tuple(t.shape) != shape or t.dtype != self.torch_dtype or not t.is_cuda
+                    or not t.is_contiguous()):
+                raise ValueError("x1 [N, C, ...], x2 [N, 1, ...], grad_out [N, C, ...] must be contiguous device "
+                                 "tensors of the plan's dtype")
+        if (weights.dtype != torch.float32 or not weights.is_contiguous() or tuple(weights.shape) != (C, self.n_paths)
+                or weights.device != x1.device):
+            raise ValueError(f"weights must be a contiguous fp32 [C, {self.n_paths}] tensor on the inputs' device "
+                             "(a plan created with channel_weights=True)")
+        gx1, gx2 = torch.empty_like(x1), torch.empty_like(x2)
+        gw = torch.empty((C, self.n_paths), dtype=torch.float32, device=x1.device)
+        n = ctypes.c_size_t(0)
+        _lib.check(_lib.lib().spingtp_backward_v1_weighted_workspace_size(self._handle, N, C, ctypes.byref(n)),
+                   "spingtp_backward_v1_weighted_workspace_size")
+        ws = torch.empty(max(1, n.value), dtype=torch.uint8, device=x1.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+
+        def ptr(t):
+            return t.data_ptr() if t.numel() else None
+
+        _lib.check(_lib.lib().spingtp_backward_v1_weighted(
+            self._handle, ptr(x1), ptr(x2), ptr(weights), ptr(grad_out), ptr(gx1), ptr(gx2), ptr(gw),
+            ws.data_ptr(), n.value, N, C, ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_v1_weighted")
+        return gx1, gx2, gw
 
     __call__ = forward
 

@@ -735,3 +735,69 @@ def test_channel_weighted_pre_table_reproduces_oracle(built_library, L1, L2, LO,
     for c in range(C):
         yo = oracle.PathWeightedTensor(L1, L2, LO, spins, basis, W[c]).apply(x1[c:c + 1], x2[None]).reshape(-1)
         assert np.linalg.norm(y[c] - yo) <= 1e-6 * np.linalg.norm(yo), c
+
+
+def emulate_bwd_v1w(words, x1, x2, W, g):
+    """The arithmetic of spingtp_backward_v1_weighted on its entry lists, for one edge: x1 and g
+    [C, n] rows of the edge's channels, x2 its shared row, W [C, n_paths].  Each list segment
+    is summed as the kernel sums it (value times the gathered product), the zero columns past
+    each row included.  Returns (gx1 [C, NC1], gx2 [NC2], gW [C, NP]) in float64."""
+    nc1, nc2, nco, npth = (int(v) for v in words[:4])
+    seg = [words[int(words[5 + i]):] for i in range(3)]
+    lst = [words[int(words[8 + i]):] for i in range(3)]
+
+    def entries(i, key):
+        e0, e1 = int(seg[i][key]), int(seg[i][key + 1])
+        assert e0 % 8 == 0 and e1 % 8 == 0
+        w = lst[i][2 * e0:2 * e1].reshape(-1, 2)
+        f = w[:, 0].astype(np.int64)
+        return f & 0x3ff, (f >> 10) & 0x3ff, f >> 20, w[:, 1].view(np.float32).astype(np.float64)
+
+    C = x1.shape[0]
+    pad = lambda a: np.concatenate([a, np.zeros(a.shape[:-1] + (1,))], axis=-1)  # the zero column
+    X1, X2, G, Wp = pad(x1), pad(x2), pad(g), pad(W)
+    gx1 = np.zeros((C, nc1))
+    gx2 = np.zeros(nc2)
+    gW = np.zeros((C, npth))
+    for k1 in range(nc1):
+        p, k2, k3, v = entries(0, k1)
+        gx1[:, k1] = (v * X2[k2] * Wp[:, p] * G[:, k3]).sum(axis=1)
+    for k2 in range(nc2):
+        p, a, k3, v = entries(1, k2)
+        gx2[k2] = (v * Wp[:, p] * X1[:, a] * G[:, k3]).sum()
+    for q in range(npth):
+        a, b, k3, v = entries(2, q)
+        gW[:, q] = (v * X2[b] * X1[:, a] * G[:, k3]).sum(axis=1)
+    return gx1, gx2, gW
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [(1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 2),
+                                                   (1, 3, 3, (-1, 0, 1), 0), (2, 1, 2, (-2, -1, 0, 1, 2), 1),
+                                                   (3, 2, 1, (0,), 0)])
+def test_weighted_backward_lists_reproduce_oracle(built_library, L1, L2, LO, spins, basis):
+    """spingtp_backward_v1_weighted's three entry lists, re-enacted on the CPU, give the oracle's
+    gradients of the per-channel path-weighted product; every nonzero of T is in each list once."""
+    from paper_2607_01408_amd.spingtp import paths_host
+
+    words = pre_table_host(L1, L2, LO, spins, basis, backward=True, channel_weights=True)
+    P = paths_host(L1, L2, LO, spins, basis)
+    n1, n2, n3 = (len(spins) * (L + 1) ** 2 for L in (L1, L2, LO))
+    assert [int(v) for v in words[:4]] == [n1, n2, n3, len(P)]
+    for i, n in enumerate((n1, n2, len(P))):  # real entries per list: the tensor's nonzeros
+        s = words[int(words[5 + i]):int(words[5 + i]) + n + 1].astype(np.int64)
+        ent = words[int(words[8 + i]):][:2 * int(s[-1])].reshape(-1, 2)
+        assert int((ent[:, 1] != 0).sum()) == int(words[4])
+    rng = np.random.default_rng(7 + L1 + 5 * L2 + 25 * LO)
+    N, C = 2, 3
+    W = rng.standard_normal((C, len(P)))
+    x1 = rng.standard_normal((N, C, n1)) * valid_mask(spins, L1).ravel()
+    x2 = rng.standard_normal((N, n2)) * valid_mask(spins, L2).ravel()
+    g = rng.standard_normal((N, C, n3)) * valid_mask(spins, LO).ravel()
+    r1, r2, rW = oracle.channel_weighted_v1_vjp(x1, x2, W, g, L1, L2, LO, spins, basis)
+    gW = np.zeros_like(W)
+    for n in range(N):
+        e1, e2, eW = emulate_bwd_v1w(words, x1[n], x2[n], W, g[n])
+        assert np.linalg.norm(e1 - r1[n]) <= 1e-6 * np.linalg.norm(r1[n])
+        assert np.linalg.norm(e2 - r2[n]) <= 1e-6 * np.linalg.norm(r2[n])
+        gW += eW
+    assert np.linalg.norm(gW - rW) <= 1e-6 * np.linalg.norm(rW)

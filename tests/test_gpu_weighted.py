@@ -178,5 +178,135 @@ def test_channel_weighted_rules():
     y = plan.forward_v1_weighted(x1, x2, torch.zeros((3, n), device="cuda"))
     torch.cuda.synchronize()
     assert not y.any()
-    with pytest.raises(SpinGTPError):  # path slots beyond the instantiations: degree 3 with spins {-1, 0, +1}
-        Plan(3, 3, 3, S3, "fp32", channel_weights=True)
+    # path slots beyond the forward's instantiations (degree 3 with spins {-1, 0, +1}): the plan
+    # holds only the gradients' table
+    plan3 = Plan(3, 3, 3, S3, "fp32", channel_weights=True)
+    x13 = torch.zeros((2, 3, 3, 16), device="cuda")
+    with pytest.raises(SpinGTPError):
+        plan3.forward_v1_weighted(x13, torch.zeros((2, 1, 3, 16), device="cuda"),
+                                  torch.zeros((3, plan3.n_paths), device="cuda"))
+    with pytest.raises(SpinGTPError):  # neither fits: 2002 paths at degree 6
+        Plan(6, 6, 6, S3, "fp32", channel_weights=True)
+
+
+# --- gradients of the per-channel path-weighted product (spingtp_backward_v1_weighted) ---
+
+def run_channel_weighted_backward(L1, L2, LO, spins, N, C, basis=0, dtype="fp32", seed=0):
+    P = paths_host(L1, L2, LO, spins, basis)
+    print(f"[v1-weighted-bwd] L=({L1},{L2},{LO}) spins={spins} basis={basis} N={N} C={C} {dtype} "
+          f"paths={len(P)}", flush=True)
+    rng = np.random.default_rng(100 + seed)
+    W = torch.as_tensor(rng.standard_normal((C, len(P))), dtype=torch.float32, device="cuda")
+    x1 = workloads.draw(L1, N, C, 60 + seed, dtype, spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, 1, 61 + seed, dtype, spins, "unit", "cuda")
+    g = workloads.draw(LO, N, C, 62 + seed, dtype, spins, "unit", "cuda")
+    plan = Plan(L1, L2, LO, spins, dtype, basis, channel_weights=True)
+    gx1, gx2, gW = plan.backward_v1_weighted(x1, x2, W, g)
+    torch.cuda.synchronize()
+    a, b, c = host(x1, N * C).reshape(N, C, -1), host(x2, N), host(g, N * C).reshape(N, C, -1)
+    r1, r2, rW = oracle.channel_weighted_v1_vjp(a, b, W.double().cpu().numpy(), c, L1, L2, LO, spins, basis)
+    e1 = rel_l2(host(gx1, N * C), r1.reshape(N * C, -1)) if N * C else 0.0
+    e2 = rel_l2(host(gx2, N), r2) if N else 0.0
+    eW = rel_l2(gW.double().cpu().numpy(), rW) if N * C else float(gW.abs().max()) if C else 0.0
+    print(f"[v1-weighted-bwd]   rel_l2 gx1={e1:.3e} gx2={e2:.3e} gW={eW:.3e}", flush=True)
+    tol = TOL[dtype]
+    assert e1 <= tol and e2 <= tol and eW <= tol, (e1, e2, eW)
+    return plan, (x1, x2, W, g), (gx1, gx2, gW)
+
+
+@pytest.mark.parametrize("shape,C", [((1, 1, 1), 16), ((2, 2, 2), 64), ((2, 2, 2), 17), ((1, 3, 3), 128),
+                                     ((1, 3, 3), 1)])
+@pytest.mark.parametrize("basis", [0, 2])
+def test_channel_weighted_backward_table_shapes(shape, C, basis):
+    # the depthwise V = 1 shapes of the paper's runtime table (App. E.2)
+    run_channel_weighted_backward(*shape, S3, 11, C, basis, seed=C + sum(shape))
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [(2, 1, 2, S3, 1), (2, 2, 2, (0,), 0), (3, 3, 3, S3, 2),
+                                                   (2, 1, 2, S5, 0)])
+def test_channel_weighted_backward_other_shapes(L1, L2, LO, spins, basis):
+    # shapes without a weighted forward kernel too (degree 3): the gradients have their own
+    # kernel, and plan creation keeps its table
+    run_channel_weighted_backward(L1, L2, LO, spins, 5, 70, basis, seed=L1 + 3 * L2)
+
+
+def test_channel_weighted_backward_many_edge_ranges():
+    # 1500 edges over 3 channel tiles (130 channels, the last tile ragged): several edges
+    # per workgroup, so the weight gradient adds partial sums over edge ranges
+    run_channel_weighted_backward(1, 1, 1, S3, 1500, 130, 0, seed=3)
+
+
+def test_channel_weighted_backward_bf16():
+    run_channel_weighted_backward(2, 2, 2, S3, 9, 48, 2, "bf16", seed=5)
+
+
+def test_channel_weighted_backward_empty():
+    # no edges: grad_weights is an empty sum (zeros); no channels: grad_x2 is zeros
+    plan = Plan(2, 2, 2, S3, "fp32", channel_weights=True)
+    n = plan.n_paths
+    x1, x2 = torch.zeros((0, 8, 3, 9), device="cuda"), torch.zeros((0, 1, 3, 9), device="cuda")
+    gx1, gx2, gW = plan.backward_v1_weighted(x1, x2, torch.ones((8, n), device="cuda"), x1)
+    torch.cuda.synchronize()
+    assert gx1.shape == (0, 8, 3, 9) and gx2.shape == (0, 1, 3, 9)
+    assert gW.shape == (8, n) and not gW.any()
+    x1 = torch.zeros((4, 0, 3, 9), device="cuda")
+    x2 = workloads.draw(2, 4, 1, 3, "fp32", S3, "unit", "cuda")
+    gx1, gx2, gW = plan.backward_v1_weighted(x1, x2, torch.zeros((0, n), device="cuda"), x1)
+    torch.cuda.synchronize()
+    assert gx2.shape == (4, 1, 3, 9) and not gx2.any() and gW.shape == (0, n)
+
+
+def test_channel_weighted_backward_matches_forward_identity():
+    # oracle-free: the product is linear in each argument, so <g, y> = <gx1, x1> = <gx2, x2> = <gW, W>
+    # with y from the forward kernel and the gradients from the backward kernel on the same device data
+    plan, (x1, x2, W, g), (gx1, gx2, gW) = run_channel_weighted_backward(2, 2, 2, S3, 40, 96, 2, seed=9)
+    y = plan.forward_v1_weighted(x1, x2, W)
+    torch.cuda.synchronize()
+    e = float((g.double() * y.double()).sum())
+    for grad, val in ((gx1, x1), (gx2, x2), (gW, W)):
+        d = float((grad.double() * val.double()).sum())
+        assert abs(d - e) <= 1e-5 * max(1.0, abs(e)), (d, e)
+
+
+def test_channel_weighted_backward_repeatable():
+    # the partial sums are added in a fixed order: two calls give identical bits
+    _, (x1, x2, W, g), (gx1, gx2, gW) = run_channel_weighted_backward(1, 3, 3, S3, 600, 64, 0, seed=4)
+    plan = Plan(1, 3, 3, S3, "fp32", 0, channel_weights=True)
+    hx1, hx2, hW = plan.backward_v1_weighted(x1, x2, W, g)
+    torch.cuda.synchronize()
+    assert torch.equal(gx1, hx1) and torch.equal(gx2, hx2) and torch.equal(gW, hW)
+
+
+def test_channel_weighted_backward_rules():
+    from paper_2607_01408_amd import _lib
+    x1 = torch.zeros((2, 3, 3, 9), device="cuda")
+    x2 = torch.zeros((2, 1, 3, 9), device="cuda")
+    n = len(paths_host(2, 2, 2))
+    W = torch.zeros((3, n), device="cuda")
+    with pytest.raises(ValueError):  # weights need a plan created with channel_weights=True
+        Plan(2, 2, 2, S3, "fp32").backward_v1_weighted(x1, x2, W, x1)
+    size = ctypes_size_t()
+    assert _lib.lib().spingtp_backward_v1_weighted_workspace_size(Plan(2, 2, 2, S3, "fp32").handle, 2, 3,
+                                                                  size) == 2
+    plan = Plan(2, 2, 2, S3, "fp32", channel_weights=True)
+    with pytest.raises(ValueError):
+        plan.backward_v1_weighted(x1, x2, W[:, :-1].contiguous(), x1)  # one weight per path
+    assert _lib.lib().spingtp_backward_v1_weighted_workspace_size(plan.handle, 2, 3, size) == 0
+    gx1, gx2 = torch.empty_like(x1), torch.empty_like(x2)
+    gW = torch.empty_like(W)
+    ws = torch.empty(max(1, size.value), dtype=torch.uint8, device="cuda")
+    args = [x1.data_ptr(), x2.data_ptr(), W.data_ptr(), x1.data_ptr(), gx1.data_ptr(), gx2.data_ptr(),
+            gW.data_ptr(), ws.data_ptr()]
+    if size.value > 0:  # too small a workspace
+        assert _lib.lib().spingtp_backward_v1_weighted(plan.handle, *args, size.value - 1, 2, 3, None) == 1
+    bad = list(args)
+    bad[6] = None  # grad_weights missing
+    assert _lib.lib().spingtp_backward_v1_weighted(plan.handle, *bad, size.value, 2, 3, None) == 1
+    assert _lib.lib().spingtp_backward_v1_weighted(plan.handle, *args, size.value, 2, 3, None) == 0
+    torch.cuda.synchronize()
+    assert not gx1.any() and not gx2.any() and not gW.any()
+
+
+def ctypes_size_t():
+    import ctypes
+    return ctypes.c_size_t(0)
