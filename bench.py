@@ -247,6 +247,63 @@ def run_v1(args):
         return {"ms": ms, "paths": n_paths, "basis": basis,
                 "parity_rel_l2": float(np.linalg.norm(got - ref) / np.linalg.norm(ref)), "tp_per_s": U / (ms / 1e3)}
 
+    def measure_weighted_backward(L1, L2, LO, C, B, basis, seed):
+        """spingtp_backward_v1_weighted (gradients of x1, the shared x2 and the per-channel weights),
+        preallocated buffers; parity of gx1 and gx2 on sampled edges against the oracle, and of gW
+        through the identity <gW, W> = <g, y> with y from the weighted forward."""
+        import oracle
+        from paper_2607_01408_amd import paths_host
+
+        try:
+            plan = Plan(L1, L2, LO, workloads.SPINS, "fp32", basis, channel_weights=True)
+        except Exception:
+            return None
+        n_paths = len(paths_host(L1, L2, LO, workloads.SPINS, basis))
+        x1 = workloads.draw(L1, B, C, 9600 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        x2 = workloads.draw(L2, B, 1, 9700 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        g = workloads.draw(LO, B, C, 9800 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        w = torch.randn((C, n_paths), generator=torch.Generator().manual_seed(seed)).to("cuda:0")
+        gx1, gx2 = torch.empty_like(x1), torch.empty_like(x2)
+        gw = torch.empty_like(w)
+        n = ctypes.c_size_t(0)
+        assert _lib.lib().spingtp_backward_v1_weighted_workspace_size(plan.handle, B, C, ctypes.byref(n)) == 0
+        ws = torch.empty(max(1, n.value), dtype=torch.uint8, device="cuda:0")
+        st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        call = (plan.handle, x1.data_ptr(), x2.data_ptr(), w.data_ptr(), g.data_ptr(), gx1.data_ptr(),
+                gx2.data_ptr(), gw.data_ptr(), ws.data_ptr(), n.value, B, C, st)
+        bfn = _lib.lib().spingtp_backward_v1_weighted
+        for _ in range(args.warmup):
+            assert bfn(*call) == 0
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(args.steps):
+            bfn(*call)
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / args.steps
+        edges = sorted({0, B // 2, B - 1})
+        sel = torch.as_tensor(edges, device="cuda:0")
+        a, b, c = (t[sel].double().cpu().numpy() for t in (x1, x2, g))
+        r1, r2, _ = oracle.channel_weighted_v1_vjp(a.reshape(len(edges), C, -1), b.reshape(len(edges), -1),
+                                                   w.double().cpu().numpy(), c.reshape(len(edges), C, -1),
+                                                   L1, L2, LO, workloads.SPINS, basis)
+        got1 = gx1[sel].double().cpu().numpy().reshape(r1.shape)
+        got2 = gx2[sel].double().cpu().numpy().reshape(r2.shape)
+        try:
+            y = plan.forward_v1_weighted(x1, x2, w)
+        except Exception:  # a plan with the gradients' table only
+            y = None
+        ident = None
+        if y is not None:
+            torch.cuda.synchronize()
+            dot = float((g.double() * y.double()).sum())
+            ident = abs(float((gw.double() * w.double()).sum()) - dot) / max(abs(dot), 1e-300)
+        return {"ms": ms, "paths": n_paths, "basis": basis,
+                "parity_rel_l2_gx1_sampled": float(np.linalg.norm(got1 - r1) / np.linalg.norm(r1)),
+                "parity_rel_l2_gx2_sampled": float(np.linalg.norm(got2 - r2) / np.linalg.norm(r2)),
+                "gw_identity_rel": ident, "units_per_s": B * C / (ms / 1e3)}
+
     def measure_backward(L, C, B, seed):
         """spingtp_backward_v1 (both gradients) on the default route, preallocated buffers."""
         x1 = workloads.draw(L, B, C, 9300 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
@@ -280,11 +337,14 @@ def run_v1(args):
             row[name] = measure(L1, L2, LO, C, B, fourier, L1 + 3 * L2 + C)
         for name, basis in (("channel_weighted_parity_basis", 2), ("channel_weighted_paper_basis", 0)):
             row[name] = measure_weighted(L1, L2, LO, C, B, basis, L1 + 3 * L2 + C)
+            row[name + "_backward"] = measure_weighted_backward(L1, L2, LO, C, B, basis, L1 + 3 * L2 + C)
         table.append(row)
         print(f"[v1] ({L1},{L2},{LO}) C={C} B={B}: pre {row['precontracted']['ms'] * 1e3:.1f} us, "
               f"fourier {row['fourier']['ms'] * 1e3:.1f} us, weighted (parity / paper basis) "
               f"{row['channel_weighted_parity_basis']['ms'] * 1e3:.1f} / "
-              f"{row['channel_weighted_paper_basis']['ms'] * 1e3:.1f} us", file=sys.stderr, flush=True)
+              f"{row['channel_weighted_paper_basis']['ms'] * 1e3:.1f} us, its gradients "
+              f"{row['channel_weighted_parity_basis_backward']['ms'] * 1e3:.1f} / "
+              f"{row['channel_weighted_paper_basis_backward']['ms'] * 1e3:.1f} us", file=sys.stderr, flush=True)
     sweep = []
     for L in args.v1_sweep_degrees:
         row = {"L": L, "C": args.v1_sweep_channels, "B": args.v1_sweep_edges}

@@ -407,7 +407,8 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  * and an fp32 value: LIST1 holds per k1 (path, k2, k3), LIST2 per k2 (path, k1, k3),
  * LISTP per path (k1, k2, k3); each segment is padded to a multiple of 8 entries
  * of value 0 whose fields are the row lengths (NP, NC1, NC2 or NCO: the zero
- * columns).  SPINGTP_ERR_UNSUPPORTED where the kernel does not take the shape.
+ * columns), and each list ends with 64 more such entries.
+ * SPINGTP_ERR_UNSUPPORTED where the kernel does not take the shape.
  * Writes min(capacity, total) words to `words` (may be NULL when capacity is 0)
  * and the total to *count.
  */

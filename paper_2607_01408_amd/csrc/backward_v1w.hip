@@ -9,20 +9,24 @@
 //   gW[c,p]     = sum_n sum over the entries of p of T x1[n,c,k1] x2[n,k2] g[n,c,k3],
 // three sums over the nonzeros of T in three orders (by k1, by k2, by path).
 //
-// One wave per workgroup, one channel per lane: the workgroup owns a 64-channel tile
-// and a contiguous range of edges.  The tile's weight rows stay in LDS for the whole
-// range; per edge the x1 and g rows of the tile and the x2 row are staged in LDS
-// (odd row strides, so the per-lane gathers are conflict-free, and a zero column
-// past each row that the lists' padding entries point at).  The entry lists are
-// wave-uniform and come in through scalar loads, eight entries per step.
-//   * gW: per path, each lane sums its channel's products in a register and adds
-//     them into the workspace row of its edge range ([range][path][channel], so the
-//     64 lanes of a path touch 256 contiguous bytes);
-//   * gx2: per k2, each lane sums its channel's terms into an LDS column, and the
-//     lanes then add the 64 columns in a fixed order into the workspace row of the
+// A workgroup owns a 64-channel tile (one channel per lane) and a contiguous range
+// of edges; its four waves work on the same edge and split each pass's keys into
+// four ranges of about equal entry counts.  The tile's weight rows and its running
+// gW sums stay in LDS for the whole range; per edge the x1 and g rows of the tile
+// and the x2 row are staged in LDS (odd row strides, so the per-lane gathers are
+// conflict-free, and a zero column past each row that the lists' padding entries
+// point at).  The entry lists are wave-uniform: they come in through vector loads,
+// 32 entries (one word per lane) a block with the next block loading meanwhile, and
+// reach scalar registers by readlane, eight entries per step.  (Scalar loads would
+// share their wait counter with the LDS gathers, so every gather would also wait
+// for the prefetch.)
+//   * gW: per path, each lane adds its channel's sum to its row of the LDS tile;
+//     at the end of the range the tile goes to the workspace ([range][path][channel]);
+//   * gx2: per k2, each lane sums its channel's terms in a register, and a
+//     fixed-order wave reduction writes the tile's sum into the workspace row of the
 //     channel tile ([tile][edge][k2]);
-//   * gx1: per k1, each lane's sum goes into its x1 row in LDS (no longer read), and
-//     the tile leaves in coalesced stores.
+//   * gx1: per k1, each lane's sum goes into its x1 row in LDS (after a barrier: the
+//     other passes read those rows), and the tile leaves in coalesced stores.
 // A second kernel adds the partial sums of gx2 over the channel tiles and those of
 // gW over the edge ranges, in a fixed order: the results do not depend on scheduling.
 //
@@ -30,10 +34,13 @@
 //   [0, 16)  NC1, NC2, NCO, NP (paths), NNZ, then the word offsets of SEG1, SEG2,
 //            SEGP (list boundaries, in entries: NC1 + 1, NC2 + 1, NP + 1 words) and of
 //            LIST1, LIST2, LISTP; zeros
+//   [16, 31) the key ranges of the four waves: five boundaries per list (LIST1,
+//            LIST2, LISTP), 0 ... number of keys
 //   each list entry is two words: a | b << 10 | c << 20, fp32 value;
 //   LIST1 (per k1): a = path, b = k2, c = k3;  LIST2 (per k2): a = path, b = k1, c = k3;
 //   LISTP (per path): a = k1, b = k2, c = k3.  Every segment is padded to a multiple
-//   of eight entries with value 0 whose indices point at the zero columns.
+//   of eight entries with value 0 whose indices point at the zero columns, and every
+//   list ends with 96 more of those (the prefetch of the last blocks reads them).
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -46,6 +53,7 @@ namespace spingtp {
 namespace {
 
 constexpr int kBw1wLanes = 64;
+constexpr int kBw1wThreads = 64 * kBw1wWaves;
 
 __device__ __forceinline__ float bw_load(const float* p) { return *p; }
 __device__ __forceinline__ float bw_load(const uint16_t* p) { return bf16_to_f32(*p); }
@@ -55,34 +63,75 @@ __device__ __forceinline__ void bw_store(uint16_t* p, float v) { *p = f32_to_bf1
 // rows [0, nrows) of a contiguous [nrows][nc] block into an LDS tile of stride st
 template <typename TIO>
 __device__ __forceinline__ void bw_load_rows(const TIO* __restrict__ src, int nrows, int nc, int st, float* dst,
-                                             int lane) {
+                                             int tid) {
     const int n = nrows * nc;
-    for (int e = lane; e < n; e += kBw1wLanes) {
+    for (int e = tid; e < n; e += kBw1wThreads) {
         const int r = e / nc;
         dst[r * st + (e - r * nc)] = bw_load(src + e);
     }
 }
 
-// Sum over one segment of a list: the term of an entry is value * f(a, b, c).
-template <typename F>
-__device__ __forceinline__ float bw_segment(const uint32_t* __restrict__ list, int e0, int e1, F&& term) {
-    float acc0 = 0.f, acc1 = 0.f;
-    for (int e = e0; e < e1; e += 8) {
-        const uint32_t* w = list + 2 * e;
-#pragma unroll
-        for (int i = 0; i < 8; i += 2) {
-            const uint32_t i0 = w[2 * i], i1 = w[2 * i + 2];
-            acc0 = fmaf(__uint_as_float(w[2 * i + 1]), term(i0 & 0x3ffu, (i0 >> 10) & 0x3ffu, i0 >> 20), acc0);
-            acc1 = fmaf(__uint_as_float(w[2 * i + 3]), term(i1 & 0x3ffu, (i1 >> 10) & 0x3ffu, i1 >> 20), acc1);
-        }
+// One pass over keys [k0, k1) of a list: for every key k the sum over its segment of
+// value * term(a, b, c), handed to emit(k, sum).  The entries are walked as one
+// stream of 32-entry blocks (lane l holds word l of the block, the next block loads
+// meanwhile), four 8-entry steps a block with static readlane positions; a key ends
+// where its segment does (segments are multiples of 8, so at a step boundary), and
+// keys with empty segments get 0.
+template <typename F, typename E>
+__device__ __forceinline__ void bw_pass(const uint32_t* __restrict__ seg, const uint32_t* __restrict__ list, int k0,
+                                        int k1, int lane, F&& term, E&& emit) {
+    int k = k0;
+    int kend = k < k1 ? static_cast<int>(seg[k + 1]) : 0;
+    const int e0 = static_cast<int>(seg[k0]), e1 = static_cast<int>(seg[k1]);
+    while (k < k1 && kend == e0) {  // empty keys before the first entry
+        emit(k, 0.f);
+        ++k;
+        kend = k < k1 ? static_cast<int>(seg[k + 1]) : 0;
     }
-    return acc0 + acc1;
+    const uint32_t* __restrict__ base = list + 2 * e0;
+    uint32_t vcur = base[lane], vnxt = base[64 + lane];
+    float acc0 = 0.f, acc1 = 0.f;
+    for (int blk = e0; blk < e1; blk += 32) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int e = blk + 8 * j;
+            if (e < e1) {
+                uint32_t w[16];
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    w[i] = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(vcur), 16 * j + i));
+#pragma unroll
+                for (int i = 0; i < 8; i += 2) {
+                    const uint32_t i0 = w[2 * i], i1 = w[2 * i + 2];
+                    acc0 = fmaf(__uint_as_float(w[2 * i + 1]), term(i0 & 0x3ffu, (i0 >> 10) & 0x3ffu, i0 >> 20),
+                                acc0);
+                    acc1 = fmaf(__uint_as_float(w[2 * i + 3]), term(i1 & 0x3ffu, (i1 >> 10) & 0x3ffu, i1 >> 20),
+                                acc1);
+                }
+                while (k < k1 && kend == e + 8) {  // keys ending here (then the empty ones after them)
+                    emit(k, acc0 + acc1);
+                    acc0 = acc1 = 0.f;
+                    ++k;
+                    kend = k < k1 ? static_cast<int>(seg[k + 1]) : 0;
+                }
+            }
+        }
+        vcur = vnxt;
+        vnxt = base[2 * (blk - e0) + 128 + lane];
+    }
+}
+
+// sum of v over the 64 lanes of the wave, in a fixed order (every lane gets it)
+__device__ __forceinline__ float bw_wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kBw1wLanes);
+    return v;
 }
 
 __host__ __device__ constexpr int bw_stride(int n) { return (n + 1) | 1; }  // odd, with a zero column
 
 template <typename TIO>
-__global__ __launch_bounds__(kBw1wLanes) void spingtp_bwd_v1w_kernel(
+__global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
     const TIO* __restrict__ x1, const TIO* __restrict__ x2, const float* __restrict__ wts, const TIO* __restrict__ g,
     TIO* __restrict__ gx1, float* __restrict__ ws_x2, float* __restrict__ ws_w, int64_t N, int64_t C, int64_t epg,
     const uint32_t* __restrict__ tab) {
@@ -97,72 +146,76 @@ __global__ __launch_bounds__(kBw1wLanes) void spingtp_bwd_v1w_kernel(
     const uint32_t* __restrict__ listp = tab + tab[10];
     const int stw = bw_stride(np), st1 = bw_stride(nc1), sto = bw_stride(nco), st2 = bw_stride(nc2);
     float* Wt = lds;                       // [64][stw] weights of the tile's channels
-    float* X1 = Wt + kBw1wLanes * stw;     // [64][st1] x1 rows, then the gx1 rows
+    float* GW = Wt + kBw1wLanes * stw;     // [64][stw] gW sums of the edge range
+    float* X1 = GW + kBw1wLanes * stw;     // [64][st1] x1 rows, then the gx1 rows
     float* G = X1 + kBw1wLanes * st1;      // [64][sto] grad_out rows
-    float* T2 = G + kBw1wLanes * sto;      // [64][st2] per-lane gx2 terms
-    float* X2 = T2 + kBw1wLanes * st2;     // [st2] the edge's x2 row
+    float* X2 = G + kBw1wLanes * sto;      // [st2] the edge's x2 row
 
-    const int lane = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t group = blockIdx.x, tile = blockIdx.y;
     const int64_t c0 = tile * kBw1wLanes;
     const int nch = static_cast<int>(C - c0 < kBw1wLanes ? C - c0 : kBw1wLanes);
     const int64_t n_begin = group * epg;
     const int64_t n_end = n_begin + epg < N ? n_begin + epg : N;
-    const bool cvalid = lane < nch;
-    const int64_t c = c0 + lane;
+    // this wave's keys in each pass
+    const uint32_t* __restrict__ kr = tab + 16;
+    const int k1b = static_cast<int>(kr[wave]), k1e = static_cast<int>(kr[wave + 1]);
+    const int k2b = static_cast<int>(kr[5 + wave]), k2e = static_cast<int>(kr[6 + wave]);
+    const int kpb = static_cast<int>(kr[10 + wave]), kpe = static_cast<int>(kr[11 + wave]);
 
     // zero everything once (zero columns and the rows past nch stay zero: the per-edge
     // loads write only rows < nch and columns < nc), then the weight rows
-    const int total = kBw1wLanes * (stw + st1 + sto + st2) + st2;
-    for (int i = lane; i < total; i += kBw1wLanes) lds[i] = 0.f;
+    const int total = kBw1wLanes * (2 * stw + st1 + sto) + st2;
+    for (int i = tid; i < total; i += kBw1wThreads) lds[i] = 0.f;
     __syncthreads();
-    for (int e = lane; e < nch * np; e += kBw1wLanes) {
+    for (int e = tid; e < nch * np; e += kBw1wThreads) {
         const int r = e / np;
         Wt[r * stw + (e - r * np)] = wts[c0 * np + e];
     }
     const float* Wr = Wt + lane * stw;
+    float* GWr = GW + lane * stw;
     float* X1r = X1 + lane * st1;
     const float* Gr = G + lane * sto;
-    float* T2r = T2 + lane * st2;
 
     for (int64_t n = n_begin; n < n_end; ++n) {
-        __syncthreads();
+        __syncthreads();  // the previous edge's gx1 rows have left
         const int64_t row0 = n * C + c0;
-        bw_load_rows(x1 + row0 * nc1, nch, nc1, st1, X1, lane);
-        bw_load_rows(g + row0 * nco, nch, nco, sto, G, lane);
-        for (int k = lane; k < nc2; k += kBw1wLanes) X2[k] = bw_load(x2 + n * nc2 + k);
+        bw_load_rows(x1 + row0 * nc1, nch, nc1, st1, X1, tid);
+        bw_load_rows(g + row0 * nco, nch, nco, sto, G, tid);
+        for (int k = tid; k < nc2; k += kBw1wThreads) X2[k] = bw_load(x2 + n * nc2 + k);
         __syncthreads();
 
-        // gW: one partial sum per (edge range, path, channel)
-        for (int p = 0; p < np; ++p) {
-            const float acc = bw_segment(listp, static_cast<int>(segp[p]), static_cast<int>(segp[p + 1]),
-                                         [&](uint32_t a, uint32_t b, uint32_t cc) { return X2[b] * (X1r[a] * Gr[cc]); });
-            if (cvalid) {
-                float* dst = ws_w + (group * np + p) * C + c;
-                *dst = n == n_begin ? acc : *dst + acc;
-            }
-        }
-        // gx2: per-lane terms, then the column sums of the tile
-        for (int k2 = 0; k2 < nc2; ++k2)
-            T2r[k2] = bw_segment(list2, static_cast<int>(seg2[k2]), static_cast<int>(seg2[k2 + 1]),
-                                 [&](uint32_t a, uint32_t b, uint32_t cc) { return Wr[a] * (X1r[b] * Gr[cc]); });
-        __syncthreads();
-        for (int k2 = lane; k2 < nc2; k2 += kBw1wLanes) {
-            float s = 0.f;
-            for (int r = 0; r < kBw1wLanes; ++r) s += T2[r * st2 + k2];
-            ws_x2[(tile * N + n) * nc2 + k2] = s;
-        }
-        // gx1 into the x1 rows (the gW and gx2 sums above were their last readers)
-        for (int k1 = 0; k1 < nc1; ++k1)
-            X1r[k1] = bw_segment(list1, static_cast<int>(seg1[k1]), static_cast<int>(seg1[k1 + 1]),
-                                 [&](uint32_t a, uint32_t b, uint32_t cc) { return X2[b] * (Wr[a] * Gr[cc]); });
+        // gW: every (channel, path) sum belongs to one wave
+        bw_pass(segp, listp, kpb, kpe, lane,
+                [&](uint32_t a, uint32_t b, uint32_t cc) { return X2[b] * (X1r[a] * Gr[cc]); },
+                [&](int p, float acc) { GWr[p] += acc; });
+        // gx2: per k2 the sum over the tile's channels (a fixed-order wave reduction)
+        bw_pass(seg2, list2, k2b, k2e, lane,
+                [&](uint32_t a, uint32_t b, uint32_t cc) { return Wr[a] * (X1r[b] * Gr[cc]); },
+                [&](int k2, float acc) {
+                    const float s = bw_wave_sum(acc);
+                    if (lane == 0) ws_x2[(tile * N + n) * nc2 + k2] = s;
+                });
+        __syncthreads();  // the x1 rows have been read by every wave
+        // gx1 into the x1 rows
+        bw_pass(seg1, list1, k1b, k1e, lane,
+                [&](uint32_t a, uint32_t b, uint32_t cc) { return X2[b] * (Wr[a] * Gr[cc]); },
+                [&](int k, float acc) { X1r[k] = acc; });
         __syncthreads();
         TIO* dst = gx1 + row0 * nc1;
-        for (int e = lane; e < nch * nc1; e += kBw1wLanes) {
+        for (int e = tid; e < nch * nc1; e += kBw1wThreads) {
             const int r = e / nc1;
             bw_store(dst + e, X1[r * st1 + (e - r * nc1)]);
         }
     }
+    __syncthreads();
+    // the range's gW sums: 64 consecutive channels of a path per wave store
+    if (n_end > n_begin)
+        for (int i = tid; i < np * kBw1wLanes; i += kBw1wThreads) {
+            const int p = i >> 6, r = i & 63;
+            if (r < nch) ws_w[(group * np + p) * C + c0 + r] = GW[r * stw + p];
+        }
 }
 
 // gx2[n,k2] = sum over the channel tiles; gW[c,p] = sum over the edge ranges (fixed order)
@@ -181,9 +234,19 @@ __global__ __launch_bounds__(256) void spingtp_bwd_v1w_reduce_kernel(const float
     } else if (i < nx2 + C * np) {
         const int64_t j = i - nx2;
         const int64_t ch = j / np, p = j - ch * np;
-        float s = 0.f;
-        for (int64_t r = 0; r < groups; ++r) s += ws_w[(r * np + p) * C + ch];
-        gw[j] = s;
+        // four interleaved partial sums (r mod 4), combined in a fixed order
+        float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+        const int64_t stride = static_cast<int64_t>(np) * C;
+        const float* src = ws_w + p * C + ch;
+        int64_t r = 0;
+        for (; r + 4 <= groups; r += 4) {
+            s0 += src[r * stride];
+            s1 += src[(r + 1) * stride];
+            s2 += src[(r + 2) * stride];
+            s3 += src[(r + 3) * stride];
+        }
+        for (; r < groups; ++r) s0 += src[r * stride];
+        gw[j] = (s0 + s1) + (s2 + s3);
     }
 }
 
@@ -213,7 +276,7 @@ hipError_t launch_typed(const void* x1, const void* x2, const float* w, const vo
             }
         }
         hipLaunchKernelGGL(spingtp_bwd_v1w_kernel<TIO>, dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)),
-                           dim3(kBw1wLanes), bytes, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w,
+                           dim3(kBw1wThreads), bytes, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w,
                            static_cast<const TIO*>(g), static_cast<TIO*>(gx1), ws_x2, ws_w, N, C, epg, tab);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -233,14 +296,14 @@ hipError_t launch_typed(const void* x1, const void* x2, const float* w, const vo
 }  // namespace
 
 void bw1w_groups(int64_t N, int64_t C, int64_t* groups, int64_t* epg) {
-    // about kBw1wTargetWaves workgroups of one wave over the channel tiles and edge ranges
+    // about kBw1wTargetGroups workgroups over the channel tiles and edge ranges
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     if (N <= 0 || tiles <= 0) {
         *groups = 0;
         *epg = 0;
         return;
     }
-    int64_t want = kBw1wTargetWaves / tiles;
+    int64_t want = kBw1wTargetGroups / tiles;
     if (want < 1) want = 1;
     if (want > N) want = N;
     *epg = (N + want - 1) / want;
@@ -258,8 +321,7 @@ hipError_t launch_bwd_v1w(int dtype, const void* x1, const void* x2, const float
                           void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
                           const uint32_t* tab, hipStream_t stream) {
     if (s.lds_floats <= 0 || s.lds_floats > kBw1wMaxLdsFloats) return hipErrorInvalidValue;
-    if (s.lds_floats != kBw1wLanes * (bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nco) + bw_stride(s.nc2)) +
-                            bw_stride(s.nc2))
+    if (s.lds_floats != kBw1wLanes * (2 * bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nco)) + bw_stride(s.nc2))
         return hipErrorInvalidValue;  // the kernel carves its LDS from the table's sizes
     return dtype == 0 ? launch_typed<float>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream)
                       : launch_typed<uint16_t>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream);

@@ -147,14 +147,15 @@ spingtp_status run_forward(spingtp_plan plan, const KernelEntry* k, const void* 
                            bool backward = false, const uint32_t* aux = nullptr);
 
 // Gradients of the per-channel path-weighted product (backward_v1w.hip).
-// Sizes of its table; lds_floats: the LDS of one workgroup (weight, x1, grad_out and
-// gx2-term tiles of 64 rows and the x2 row).
+// Sizes of its table; lds_floats: the LDS of one workgroup (weight, gW, x1 and
+// grad_out tiles of 64 rows and the x2 row).
 struct Bw1wShape {
     int nc1, nc2, nco, np, lds_floats;
 };
+constexpr int kBw1wWaves = 4;             // waves of a workgroup, splitting each pass's keys
 constexpr int kBw1wMaxLdsFloats = 40960;  // 160 KB
 constexpr int kBw1wMaxIndex = 1022;       // 10-bit entry fields; a row's zero column sits at index n
-constexpr int kBw1wTargetWaves = 1024;    // workgroups (one wave each) a launch aims for
+constexpr int kBw1wTargetGroups = 512;    // workgroups a launch aims for (two per CU)
 // Entry lists of the table (layout in backward_v1w.hip); false where an index or the
 // LDS tile does not fit.  `dense`: the tensor of build_dense_tensor if the caller has it.
 bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,

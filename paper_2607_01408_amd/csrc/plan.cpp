@@ -617,7 +617,7 @@ bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, 
     const int np = static_cast<int>(paths.size());
     if (std::max(std::max(nc1, nc2), std::max(nco, np)) > kBw1wMaxIndex) return false;
     auto st = [](int n) { return (n + 1) | 1; };
-    const int lds = 64 * (st(np) + st(nc1) + st(nco) + st(nc2)) + st(nc2);
+    const int lds = 64 * (2 * st(np) + st(nc1) + st(nco)) + st(nc2);
     if (lds > kBw1wMaxLdsFloats) return false;
     struct Ent {
         int k1, k2, k3, p;
@@ -658,6 +658,7 @@ bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, 
             at += static_cast<uint32_t>(n);
         }
         l.seg.push_back(at);
+        for (int i = 0; i < 96; ++i) put(pad, 0.f);  // read by the kernel's last prefetches
         return l;
     };
     const List l1 = make(
@@ -669,13 +670,26 @@ bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, 
     const List lp = make(
         np, [](const Ent& e) { return e.p; }, [](const Ent& e) { return std::array<int, 3>{e.k1, e.k2, e.k3}; },
         {nc1, nc2, nco});
-    out.assign(16, 0u);
+    out.assign(32, 0u);
     out[0] = static_cast<uint32_t>(nc1);
     out[1] = static_cast<uint32_t>(nc2);
     out[2] = static_cast<uint32_t>(nco);
     out[3] = static_cast<uint32_t>(np);
     out[4] = static_cast<uint32_t>(ents.size());
     const List* lists[3] = {&l1, &l2, &lp};
+    for (int i = 0; i < 3; ++i) {  // the waves' key ranges: about equal entry counts
+        const std::vector<uint32_t>& sg = lists[i]->seg;
+        const int nkeys = static_cast<int>(sg.size()) - 1;
+        uint32_t* kr = out.data() + 16 + 5 * i;
+        kr[0] = 0;
+        kr[kBw1wWaves] = static_cast<uint32_t>(nkeys);
+        for (int w = 1; w < kBw1wWaves; ++w) {
+            const uint64_t target = static_cast<uint64_t>(sg[nkeys]) * w / kBw1wWaves;
+            int k = static_cast<int>(kr[w - 1]);
+            while (k < nkeys && sg[k] < target) ++k;
+            kr[w] = static_cast<uint32_t>(k);
+        }
+    }
     for (int i = 0; i < 3; ++i) {
         out[5 + i] = static_cast<uint32_t>(out.size());
         out.insert(out.end(), lists[i]->seg.begin(), lists[i]->seg.end());

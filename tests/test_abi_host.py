@@ -787,6 +787,11 @@ def test_weighted_backward_lists_reproduce_oracle(built_library, L1, L2, LO, spi
         s = words[int(words[5 + i]):int(words[5 + i]) + n + 1].astype(np.int64)
         ent = words[int(words[8 + i]):][:2 * int(s[-1])].reshape(-1, 2)
         assert int((ent[:, 1] != 0).sum()) == int(words[4])
+        assert np.all(np.diff(s) % 8 == 0) and s[0] == 0
+        kr = words[16 + 5 * i:21 + 5 * i].astype(np.int64)  # the four waves' key ranges
+        assert kr[0] == 0 and kr[-1] == n and np.all(np.diff(kr) >= 0)
+        tail = words[int(words[8 + i]) + 2 * int(s[-1]):][:2 * 96].reshape(-1, 2)  # prefetch padding
+        assert tail.shape == (96, 2) and not tail[:, 1].any()
     rng = np.random.default_rng(7 + L1 + 5 * L2 + 25 * LO)
     N, C = 2, 3
     W = rng.standard_normal((C, len(P)))
