@@ -27,7 +27,7 @@
 //     channel tile ([tile][edge][k2]);
 //   * gx1: per k1, each lane's sum goes into its x1 row in LDS (after a barrier: the
 //     other passes read those rows), and the tile leaves in coalesced stores.
-// A second kernel adds the partial sums of gx2 over the channel tiles and those of
+// Two small kernels add the partial sums of gx2 over the channel tiles and those of
 // gW over the edge ranges, in a fixed order: the results do not depend on scheduling.
 //
 // Table (uint32 words, built by build_bwd_v1w_table):
@@ -218,35 +218,38 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
         }
 }
 
-// gx2[n,k2] = sum over the channel tiles; gW[c,p] = sum over the edge ranges (fixed order)
+// gx2[n,k2] = sum over the channel tiles (fixed order)
 template <typename TIO>
-__global__ __launch_bounds__(256) void spingtp_bwd_v1w_reduce_kernel(const float* __restrict__ ws_x2,
-                                                                     const float* __restrict__ ws_w,
-                                                                     TIO* __restrict__ gx2, float* __restrict__ gw,
-                                                                     int64_t N, int nc2, int64_t tiles, int64_t C,
-                                                                     int np, int64_t groups) {
+__global__ __launch_bounds__(256) void spingtp_bwd_v1w_reduce_x2_kernel(const float* __restrict__ ws_x2,
+                                                                        TIO* __restrict__ gx2, int64_t nx2,
+                                                                        int64_t tiles) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    const int64_t nx2 = N * nc2;
-    if (i < nx2) {
-        float s = 0.f;
-        for (int64_t t = 0; t < tiles; ++t) s += ws_x2[t * nx2 + i];
-        bw_store(gx2 + i, s);
-    } else if (i < nx2 + C * np) {
-        const int64_t j = i - nx2;
-        const int64_t ch = j / np, p = j - ch * np;
-        // four interleaved partial sums (r mod 4), combined in a fixed order
-        float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-        const int64_t stride = static_cast<int64_t>(np) * C;
-        const float* src = ws_w + p * C + ch;
-        int64_t r = 0;
-        for (; r + 4 <= groups; r += 4) {
-            s0 += src[r * stride];
-            s1 += src[(r + 1) * stride];
-            s2 += src[(r + 2) * stride];
-            s3 += src[(r + 3) * stride];
-        }
-        for (; r < groups; ++r) s0 += src[r * stride];
-        gw[j] = (s0 + s1) + (s2 + s3);
+    if (i >= nx2) return;
+    float s = 0.f;
+    for (int64_t t = 0; t < tiles; ++t) s += ws_x2[t * nx2 + i];
+    bw_store(gx2 + i, s);
+}
+
+// gW[c,p] = sum over the edge ranges: one workgroup per (path, 64 channels); wave w
+// adds the ranges r = w, w + 16, ... (64 consecutive channels per load), and the 16
+// wave sums are added in wave order.
+constexpr int kBw1wReduceWaves = 16;
+
+__global__ __launch_bounds__(64 * kBw1wReduceWaves) void spingtp_bwd_v1w_reduce_w_kernel(
+    const float* __restrict__ ws_w, float* __restrict__ gw, int64_t C, int np, int64_t groups) {
+    __shared__ float part[kBw1wReduceWaves][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t p = blockIdx.x, c = static_cast<int64_t>(blockIdx.y) * 64 + lane;
+    float s = 0.f;
+    if (c < C)
+        for (int64_t r = wave; r < groups; r += kBw1wReduceWaves) s += ws_w[(r * np + p) * C + c];
+    part[wave][lane] = s;
+    __syncthreads();
+    if (wave == 0 && c < C) {
+        float t = 0.f;
+#pragma unroll
+        for (int w = 0; w < kBw1wReduceWaves; ++w) t += part[w][lane];
+        gw[c * np + p] = t;
     }
 }
 
@@ -281,13 +284,19 @@ hipError_t launch_typed(const void* x1, const void* x2, const float* w, const vo
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    const int64_t outs = N * s.nc2 + C * s.np;
-    if (outs > 0) {
-        const int64_t blocks = (outs + 255) / 256;
+    const int64_t nx2 = N * s.nc2;
+    if (nx2 > 0) {
+        const int64_t blocks = (nx2 + 255) / 256;
         if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(spingtp_bwd_v1w_reduce_kernel<TIO>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
-                           stream, ws_x2, ws_w, static_cast<TIO*>(gx2), gw, N, s.nc2, groups > 0 ? tiles : 0, C, s.np,
-                           groups);
+        hipLaunchKernelGGL(spingtp_bwd_v1w_reduce_x2_kernel<TIO>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                           stream, ws_x2, static_cast<TIO*>(gx2), nx2, groups > 0 ? tiles : 0);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (C > 0 && s.np > 0) {  // zeros when there are no edges
+        if (tiles > 0xffff) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(spingtp_bwd_v1w_reduce_w_kernel, dim3(static_cast<unsigned>(s.np), static_cast<unsigned>(tiles)),
+                           dim3(64 * kBw1wReduceWaves), 0, stream, ws_w, gw, C, s.np, groups);
         return hipGetLastError();
     }
     return hipSuccess;
