@@ -250,7 +250,7 @@ def run_v1(args):
     def measure_weighted_backward(L1, L2, LO, C, B, basis, seed):
         """spingtp_backward_v1_weighted (gradients of x1, the shared x2 and the per-channel weights),
         preallocated buffers; parity of gx1 and gx2 on sampled edges against the oracle, and of gW
-        through the identity <gW, W> = <g, y> with y from the weighted forward."""
+        through the identity <gW, W> = <g, y> with y from the weighted forward (relative to |g| |y|)."""
         import oracle
         from paper_2607_01408_amd import paths_host
 
@@ -297,8 +297,10 @@ def run_v1(args):
         ident = None
         if y is not None:
             torch.cuda.synchronize()
+            # normalized by |g| |y| (the bound of <g, y>): the dot product itself cancels
             dot = float((g.double() * y.double()).sum())
-            ident = abs(float((gw.double() * w.double()).sum()) - dot) / max(abs(dot), 1e-300)
+            scale = float(g.double().norm() * y.double().norm())
+            ident = abs(float((gw.double() * w.double()).sum()) - dot) / max(scale, 1e-300)
         return {"ms": ms, "paths": n_paths, "basis": basis,
                 "parity_rel_l2_gx1_sampled": float(np.linalg.norm(got1 - r1) / np.linalg.norm(r1)),
                 "parity_rel_l2_gx2_sampled": float(np.linalg.norm(got2 - r2) / np.linalg.norm(r2)),
