@@ -312,3 +312,47 @@ def channel_weighted_v1_vjp(x1, x2, weights, g, L1, L2, Lout, spins=(-1, 0, 1), 
         per_entry = (X1[:, c, k1] * X2[:, k2] * G[:, c, k3]).sum(axis=0) * val
         gW[c] = np.bincount(path, weights=per_entry, minlength=n_paths)
     return gx1.reshape(x1.shape), gx2.reshape(x2.shape), gW
+
+
+def channel_weighted(x1, x2, weights, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Elementwise product with one weight per (channel, path) (App. E.1 mode uuu with
+    per-channel path weights, eq. spin_gtp): out[n, c] = T_{W[c]}(x1[n, c], x2[n, c]),
+    T_{W[c]} the PathWeightedTensor of channel c's weights.
+
+    x1 [N, C, ...] (n1 values per unit), x2 [N, C, ...] (n2 per unit), weights [C, P]."""
+    spins = tuple(spins)
+    x1 = np.asarray(x1, dtype=np.float64)
+    N, C = x1.shape[:2]
+    X1 = x1.reshape(N, C, -1)
+    X2 = np.asarray(x2, dtype=np.float64).reshape(N, C, -1)
+    W = np.asarray(weights, dtype=np.float64).reshape(C, -1)
+    out = np.zeros((N, C, len(spins) * (Lout + 1) ** 2))
+    for c in range(C):
+        out[:, c] = PathWeightedTensor(L1, L2, Lout, spins, basis, W[c]).apply(X1[:, c], X2[:, c]).reshape(N, -1)
+    return out.reshape((N, C, len(spins), (Lout + 1) ** 2))
+
+
+def channel_weighted_vjp(x1, x2, weights, g, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Reverse-mode derivative of channel_weighted for dL/dout = g (float64): per unit
+    the VJP of T_{W[c]}, and
+      gW[c,p] = sum_n sum_{(k1,k2,k3) in path p} T[k1,k2,k3] x1[n,c,k1] x2[n,c,k2] g[n,c,k3].
+    Returns (gx1 shaped like x1, gx2 shaped like x2, gW [C, P])."""
+    spins = tuple(spins)
+    x1 = np.asarray(x1, dtype=np.float64)
+    x2 = np.asarray(x2, dtype=np.float64)
+    N, C = x1.shape[:2]
+    X1 = x1.reshape(N, C, -1)
+    X2 = x2.reshape(N, C, -1)
+    G = np.asarray(g, dtype=np.float64).reshape(N, C, -1)
+    W = np.asarray(weights, dtype=np.float64).reshape(C, -1)
+    k1, k2, k3, val, path, n_paths = _path_entries(L1, L2, Lout, spins, basis)
+    gx1 = np.zeros_like(X1)
+    gx2 = np.zeros_like(X2)
+    gW = np.zeros((C, n_paths))
+    for c in range(C):
+        a, b = PathWeightedTensor(L1, L2, Lout, spins, basis, W[c]).vjp(X1[:, c], X2[:, c], G[:, c])
+        gx1[:, c] = a
+        gx2[:, c] = b
+        per_entry = (X1[:, c, k1] * X2[:, c, k2] * G[:, c, k3]).sum(axis=0) * val
+        gW[c] = np.bincount(path, weights=per_entry, minlength=n_paths)
+    return gx1.reshape(x1.shape), gx2.reshape(x2.shape), gW

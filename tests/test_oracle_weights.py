@@ -154,3 +154,55 @@ def test_channel_weighted_v1_gradients_central_differences(L1, L2, LO, spins, ba
         d[n, k] = 1.0
         fd = (f(x1, x2 + d, W) - f(x1, x2 - d, W)) / 2.0
         assert abs(fd - gx2[n, k]) <= 1e-11 * max(1.0, abs(fd))
+
+
+# --- per-channel path weights with a per-unit second input (mode uuu) ---
+
+def cu_inputs(L1, L2, LO, spins, basis, N, C, seed):
+    P = len(oracle.PathWeightedTensor(L1, L2, LO, spins, basis).paths)
+    rng = np.random.default_rng(seed)
+    x1 = draw(spins, L1, N * C, seed + 1).reshape(N, C, -1)
+    x2 = draw(spins, L2, N * C, seed + 2).reshape(N, C, -1)
+    g = draw(spins, LO, N * C, seed + 3).reshape(N, C, -1)
+    return x1, x2, rng.standard_normal((C, P)), g
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CW_CASES)
+def test_channel_weighted_reduces_to_the_shared_form(L1, L2, LO, spins, basis):
+    # with x2 equal over the channels of an edge, the per-unit form is the V = 1 form
+    x1, _, W, g = cu_inputs(L1, L2, LO, spins, basis, 3, 4, 41)
+    x2s = draw(spins, L2, 3, 45)
+    x2 = np.repeat(x2s[:, None, :], 4, axis=1)
+    y = oracle.channel_weighted(x1, x2, W, L1, L2, LO, spins, basis)
+    assert np.abs(y - oracle.channel_weighted_v1(x1, x2s, W, L1, L2, LO, spins, basis)).max() <= 1e-13
+    gx1, gx2, gW = oracle.channel_weighted_vjp(x1, x2, W, g, L1, L2, LO, spins, basis)
+    r1, r2, rW = oracle.channel_weighted_v1_vjp(x1, x2s, W, g, L1, L2, LO, spins, basis)
+    assert np.abs(gx1 - r1).max() <= 1e-12 and np.abs(gW - rW).max() <= 1e-12
+    assert np.abs(gx2.sum(axis=1) - r2).max() <= 1e-12  # the shared input's gradient sums the units'
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CW_CASES)
+def test_channel_weighted_gradients_central_differences(L1, L2, LO, spins, basis):
+    N, C = 3, 2
+    x1, x2, W, g = cu_inputs(L1, L2, LO, spins, basis, N, C, 51)
+    gx1, gx2, gW = oracle.channel_weighted_vjp(x1, x2, W, g, L1, L2, LO, spins, basis)
+
+    def f(a, b, w):
+        return float((g * oracle.channel_weighted(a, b, w, L1, L2, LO, spins, basis).reshape(N, C, -1)).sum())
+
+    e = f(x1, x2, W)
+    for grad, val in ((gx1, x1), (gx2, x2), (gW, W)):  # homogeneity in each argument
+        assert abs(float((grad * val).sum()) - e) <= 1e-11 * max(1.0, abs(e))
+    rng = np.random.default_rng(9)
+    for _ in range(5):
+        c, p = int(rng.integers(C)), int(rng.integers(W.shape[1]))
+        d = np.zeros_like(W)
+        d[c, p] = 1.0
+        assert abs((f(x1, x2, W + d) - f(x1, x2, W - d)) / 2.0 - gW[c, p]) <= 1e-11 * max(1.0, abs(gW[c, p]))
+    valid2 = np.flatnonzero(valid_mask(spins, L2).ravel())
+    for _ in range(4):
+        n, c, k = int(rng.integers(N)), int(rng.integers(C)), int(rng.choice(valid2))
+        d = np.zeros_like(x2)
+        d[n, c, k] = 1.0
+        fd = (f(x1, x2 + d, W) - f(x1, x2 - d, W)) / 2.0
+        assert abs(fd - gx2[n, c, k]) <= 1e-11 * max(1.0, abs(fd))
