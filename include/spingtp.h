@@ -244,6 +244,44 @@ spingtp_status spingtp_backward_v1_weighted(spingtp_plan plan, const void* x1, c
 spingtp_status spingtp_backward_v1_weighted_workspace_size(spingtp_plan plan, int64_t N, int64_t C, size_t* bytes);
 
 /*
+ * Elementwise product with one weight per (channel, path) and a per-unit second
+ * input (Sec. 3.4 eq. spin_gtp with per-channel path weights; App. E.1 mode uuu):
+ *   out[n][c][k3] = sum over paths p of weights[c][p] sum_{k1,k2 on p}
+ *                   T[k1][k2][k3] x1[n][c][k1] x2[n][c][k2],
+ * paths in the order of spingtp_paths_host.
+ *   x1, x2, out: as spingtp_forward (x2 [N][C][n_spins][(L2+1)^2], per unit);
+ *   weights: device fp32 [C][n_paths], 4-byte aligned, read only.
+ * Needs a plan created with SPINGTP_CHANNEL_WEIGHTS whose entry lists hold the
+ * shape (as spingtp_backward_v1_weighted; the tile here is the weight, x1, x2 and
+ * output rows of 64 channels, 64 (P + NC1 + NC2 + NCO + 4) floats <= 160 KB), else
+ * SPINGTP_ERR_UNSUPPORTED.  Kernel: four waves per 64-channel tile and range of
+ * edges walk the tensor's nonzeros ordered by output slot.  Asynchronous, no
+ * allocation.
+ */
+spingtp_status spingtp_forward_weighted(spingtp_plan plan, const void* x1, const void* x2, const float* weights,
+                                        void* out, int64_t N, int64_t C, void* stream);
+
+/*
+ * Gradients of spingtp_forward_weighted for dL/dout = grad_out:
+ *   grad_x1[n][c][k1]  = sum_p weights[c][p] sum_{k2,k3 on p} T x2[n][c][k2] grad_out[n][c][k3],
+ *   grad_x2[n][c][k2]  = sum_p weights[c][p] sum_{k1,k3 on p} T x1[n][c][k1] grad_out[n][c][k3],
+ *   grad_weights[c][p] = sum_n sum_{k1,k2,k3 on p} T x1[n][c][k1] x2[n][c][k2] grad_out[n][c][k3].
+ * Arguments and rules as spingtp_backward_v1_weighted, with x2 and grad_x2
+ * [N][C][n_spins][(L2+1)^2] per unit and the workspace of
+ * spingtp_backward_weighted_workspace_size (grad_weights partial sums per edge
+ * range, added in a fixed order).  SPINGTP_ERR_UNSUPPORTED where the plan's lists
+ * do not hold the shape or the tile (64 (2 P + NC1 + NCO + 2 NC2 + 6) floats)
+ * exceeds 160 KB.  Asynchronous, no allocation.
+ */
+spingtp_status spingtp_backward_weighted(spingtp_plan plan, const void* x1, const void* x2, const float* weights,
+                                         const void* grad_out, void* grad_x1, void* grad_x2, float* grad_weights,
+                                         void* workspace, size_t workspace_bytes, int64_t N, int64_t C, void* stream);
+
+/* Bytes of workspace spingtp_backward_weighted needs for N edges x C channels.
+ * SPINGTP_ERR_UNSUPPORTED as for it. */
+spingtp_status spingtp_backward_weighted_workspace_size(spingtp_plan plan, int64_t N, int64_t C, size_t* bytes);
+
+/*
  * Gradients of a scalar loss through out = SpinGTP(x1, x2) of spingtp_forward:
  * given grad_out = dLoss/dout, writes
  *   grad_x1[n][c][k1] = sum_{k2,k3} T[k1][k2][k3] x2[n][c][k2] grad_out[n][c][k3],
@@ -400,14 +438,18 @@ spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacit
  * the kernel's instantiations), word 13 the number of paths and word 14 the
  * offset of Q words after the items: path slot q = x1 slot | path << 16, listed
  * path by path; an item's kernel position is dst = k3 KST + q.
- * With both flags: the entry lists of spingtp_backward_v1_weighted (any degrees):
- * words [0, 16) NC1, NC2, NCO, NP (paths), NNZ (nonzeros of T), the word offsets of
+ * With both flags: the entry lists of the per-channel weighted kernels
+ * (spingtp_backward_v1_weighted, spingtp_forward_weighted, spingtp_backward_weighted):
+ * words [0, 11) NC1, NC2, NCO, NP (paths), NNZ (nonzeros of T), the word offsets of
  * SEG1, SEG2, SEGP (NC1 + 1, NC2 + 1, NP + 1 list boundaries, counted in entries)
- * and of LIST1, LIST2, LISTP, zeros.  An entry is two words, a | b << 10 | c << 20
+ * and of LIST1, LIST2, LISTP.  An entry is two words, a | b << 10 | c << 20
  * and an fp32 value: LIST1 holds per k1 (path, k2, k3), LIST2 per k2 (path, k1, k3),
- * LISTP per path (k1, k2, k3); each segment is padded to a multiple of 8 entries
+ * LISTP per path (k1, k2, k3); words 11, 12 the offsets of SEG3 (NCO + 1) and
+ * LIST3, per k3 (path, k1, k2), the list of spingtp_forward_weighted; words [16, 36)
+ * five key boundaries per list (LIST1, LIST2, LISTP, LIST3) splitting it among the
+ * kernel's four waves; each segment is padded to a multiple of 8 entries
  * of value 0 whose fields are the row lengths (NP, NC1, NC2 or NCO: the zero
- * columns), and each list ends with 64 more such entries.
+ * columns), and each list ends with 96 more such entries.
  * SPINGTP_ERR_UNSUPPORTED where the kernel does not take the shape.
  * Writes min(capacity, total) words to `words` (may be NULL when capacity is 0)
  * and the total to *count.

@@ -88,7 +88,61 @@ extern "C" spingtp_status spingtp_backward_v1_weighted(spingtp_plan plan, const 
     if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
     if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
     const hipError_t e = spingtp::launch_bwd_v1w(
-        plan->dtype == SPINGTP_FP32 ? 0 : 1, x1, x2, weights, grad_out, grad_x1, grad_x2, grad_weights,
+        plan->dtype == SPINGTP_FP32 ? 0 : 1, true, x1, x2, weights, grad_out, grad_x1, grad_x2, grad_weights,
+        static_cast<float*>(workspace), N, C, plan->bw1w, plan->d_bw1w, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
+}
+
+extern "C" spingtp_status spingtp_forward_weighted(spingtp_plan plan, const void* x1, const void* x2,
+                                                   const float* weights, void* out, int64_t N, int64_t C,
+                                                   void* stream) {
+    if (plan == nullptr || N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
+    if (plan->d_bw1w == nullptr || plan->bw1w.lds_unit_fwd == 0) return SPINGTP_ERR_UNSUPPORTED;
+    if (N == 0 || C == 0) return SPINGTP_OK;
+    if (N > (int64_t{1} << 40) / C) return SPINGTP_ERR_INVALID_ARG;
+    if (x1 == nullptr || x2 == nullptr || out == nullptr || weights == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    const auto misaligned = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; };
+    if (misaligned(x1, 16) || misaligned(x2, 16) || misaligned(out, 16) || misaligned(weights, 4))
+        return SPINGTP_ERR_INVALID_ARG;
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
+    if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
+    const hipError_t e = spingtp::launch_fwd_cw(plan->dtype == SPINGTP_FP32 ? 0 : 1, x1, x2, weights, out, N, C,
+                                                plan->bw1w, plan->d_bw1w, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
+}
+
+extern "C" spingtp_status spingtp_backward_weighted_workspace_size(spingtp_plan plan, int64_t N, int64_t C,
+                                                                   size_t* bytes) {
+    if (plan == nullptr || bytes == nullptr || N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
+    if (plan->d_bw1w == nullptr || plan->bw1w.lds_unit_bwd == 0) return SPINGTP_ERR_UNSUPPORTED;
+    if (N > 0 && C > 0 && N > (int64_t{1} << 40) / C) return SPINGTP_ERR_INVALID_ARG;
+    *bytes = spingtp::bwcw_workspace_floats(N, C, plan->bw1w) * sizeof(float);
+    return SPINGTP_OK;
+}
+
+extern "C" spingtp_status spingtp_backward_weighted(spingtp_plan plan, const void* x1, const void* x2,
+                                                    const float* weights, const void* grad_out, void* grad_x1,
+                                                    void* grad_x2, float* grad_weights, void* workspace,
+                                                    size_t workspace_bytes, int64_t N, int64_t C, void* stream) {
+    size_t need = 0;
+    const spingtp_status st = spingtp_backward_weighted_workspace_size(plan, N, C, &need);
+    if (st != SPINGTP_OK) return st;
+    if (C == 0) return SPINGTP_OK;  // every output is empty
+    const auto misaligned = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; };
+    if ((N > 0 && (x1 == nullptr || x2 == nullptr || grad_out == nullptr || grad_x1 == nullptr ||
+                   grad_x2 == nullptr)) ||
+        weights == nullptr || grad_weights == nullptr)
+        return SPINGTP_ERR_INVALID_ARG;
+    if (misaligned(x1, 16) || misaligned(x2, 16) || misaligned(grad_out, 16) || misaligned(grad_x1, 16) ||
+        misaligned(grad_x2, 16) || misaligned(weights, 4) || misaligned(grad_weights, 4) || misaligned(workspace, 4))
+        return SPINGTP_ERR_INVALID_ARG;
+    if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return SPINGTP_ERR_INVALID_ARG;
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
+    if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
+    const hipError_t e = spingtp::launch_bwd_v1w(
+        plan->dtype == SPINGTP_FP32 ? 0 : 1, false, x1, x2, weights, grad_out, grad_x1, grad_x2, grad_weights,
         static_cast<float*>(workspace), N, C, plan->bw1w, plan->d_bw1w, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
 }

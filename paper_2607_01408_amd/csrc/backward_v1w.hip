@@ -1,5 +1,8 @@
 // Gradients of the per-channel path-weighted product with the edge input shared by
-// the channels (spingtp_backward_v1_weighted; the forward is spingtp_forward_v1_weighted).
+// the channels (spingtp_backward_v1_weighted; the forward is spingtp_forward_v1_weighted),
+// and the same product with a per-unit second input, forward and gradients
+// (spingtp_forward_weighted, spingtp_backward_weighted: App. E.1 mode uuu with
+// per-channel path weights; there gx2 is per unit and x2 is staged as a tile).
 //
 // The forward is out[n,c,k3] = sum_p W[c,p] sum_{(k1,k2,k3) in p} T[k1,k2,k3] x1[n,c,k1] x2[n,k2]
 // (App. E.1 mode uvu with V = 1 and one weight per channel and path of eq. spin_gtp,
@@ -34,11 +37,13 @@
 //   [0, 16)  NC1, NC2, NCO, NP (paths), NNZ, then the word offsets of SEG1, SEG2,
 //            SEGP (list boundaries, in entries: NC1 + 1, NC2 + 1, NP + 1 words) and of
 //            LIST1, LIST2, LISTP; zeros
-//   [16, 31) the key ranges of the four waves: five boundaries per list (LIST1,
-//            LIST2, LISTP), 0 ... number of keys
+//   [11, 13) the word offsets of SEG3 (NCO + 1) and LIST3
+//   [16, 36) the key ranges of the four waves: five boundaries per list (LIST1,
+//            LIST2, LISTP, LIST3), 0 ... number of keys
 //   each list entry is two words: a | b << 10 | c << 20, fp32 value;
 //   LIST1 (per k1): a = path, b = k2, c = k3;  LIST2 (per k2): a = path, b = k1, c = k3;
-//   LISTP (per path): a = k1, b = k2, c = k3.  Every segment is padded to a multiple
+//   LISTP (per path): a = k1, b = k2, c = k3;  LIST3 (per k3, the forward): a = path,
+//   b = k1, c = k2.  Every segment is padded to a multiple
 //   of eight entries with value 0 whose indices point at the zero columns, and every
 //   list ends with 96 more of those (the prefetch of the last blocks reads them).
 #include <hip/hip_runtime.h>
@@ -130,11 +135,14 @@ __device__ __forceinline__ float bw_wave_sum(float v) {
 
 __host__ __device__ constexpr int bw_stride(int n) { return (n + 1) | 1; }  // odd, with a zero column
 
-template <typename TIO>
+// SHARED: x2 [N][NC2] shared by the channels of an edge (gx2 summed over the
+// channels into the workspace); else x2 [N][C][NC2] per unit (gx2 per unit, staged
+// in an LDS tile and stored with gx1).
+template <typename TIO, bool SHARED>
 __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
     const TIO* __restrict__ x1, const TIO* __restrict__ x2, const float* __restrict__ wts, const TIO* __restrict__ g,
-    TIO* __restrict__ gx1, float* __restrict__ ws_x2, float* __restrict__ ws_w, int64_t N, int64_t C, int64_t epg,
-    const uint32_t* __restrict__ tab) {
+    TIO* __restrict__ gx1, TIO* __restrict__ gx2, float* __restrict__ ws_x2, float* __restrict__ ws_w, int64_t N,
+    int64_t C, int64_t epg, const uint32_t* __restrict__ tab) {
     extern __shared__ float lds[];
     const int nc1 = static_cast<int>(tab[0]), nc2 = static_cast<int>(tab[1]), nco = static_cast<int>(tab[2]);
     const int np = static_cast<int>(tab[3]);
@@ -149,7 +157,8 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
     float* GW = Wt + kBw1wLanes * stw;     // [64][stw] gW sums of the edge range
     float* X1 = GW + kBw1wLanes * stw;     // [64][st1] x1 rows, then the gx1 rows
     float* G = X1 + kBw1wLanes * st1;      // [64][sto] grad_out rows
-    float* X2 = G + kBw1wLanes * sto;      // [st2] the edge's x2 row
+    float* X2 = G + kBw1wLanes * sto;      // SHARED: [st2] the edge's x2 row; else [64][st2] x2 rows
+    float* GX2 = X2 + kBw1wLanes * st2;    // [64][st2] gx2 rows (per-unit x2 only)
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -166,7 +175,7 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
 
     // zero everything once (zero columns and the rows past nch stay zero: the per-edge
     // loads write only rows < nch and columns < nc), then the weight rows
-    const int total = kBw1wLanes * (2 * stw + st1 + sto) + st2;
+    const int total = kBw1wLanes * (2 * stw + st1 + sto) + (SHARED ? st2 : 2 * kBw1wLanes * st2);
     for (int i = tid; i < total; i += kBw1wThreads) lds[i] = 0.f;
     __syncthreads();
     for (int e = tid; e < nch * np; e += kBw1wThreads) {
@@ -177,36 +186,54 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
     float* GWr = GW + lane * stw;
     float* X1r = X1 + lane * st1;
     const float* Gr = G + lane * sto;
+    const float* X2r = SHARED ? X2 : X2 + lane * st2;
+    float* GX2r = GX2 + lane * st2;
 
     for (int64_t n = n_begin; n < n_end; ++n) {
-        __syncthreads();  // the previous edge's gx1 rows have left
+        __syncthreads();  // the previous edge's gradient rows have left
         const int64_t row0 = n * C + c0;
         bw_load_rows(x1 + row0 * nc1, nch, nc1, st1, X1, tid);
         bw_load_rows(g + row0 * nco, nch, nco, sto, G, tid);
-        for (int k = tid; k < nc2; k += kBw1wThreads) X2[k] = bw_load(x2 + n * nc2 + k);
+        if constexpr (SHARED) {
+            for (int k = tid; k < nc2; k += kBw1wThreads) X2[k] = bw_load(x2 + n * nc2 + k);
+        } else {
+            bw_load_rows(x2 + row0 * nc2, nch, nc2, st2, X2, tid);
+        }
         __syncthreads();
 
         // gW: every (channel, path) sum belongs to one wave
         bw_pass(segp, listp, kpb, kpe, lane,
-                [&](uint32_t a, uint32_t b, uint32_t cc) { return X2[b] * (X1r[a] * Gr[cc]); },
+                [&](uint32_t a, uint32_t b, uint32_t cc) { return X2r[b] * (X1r[a] * Gr[cc]); },
                 [&](int p, float acc) { GWr[p] += acc; });
-        // gx2: per k2 the sum over the tile's channels (a fixed-order wave reduction)
+        // gx2: per k2 the sum over the tile's channels (a fixed-order wave reduction), or
+        // per unit into the gx2 rows
         bw_pass(seg2, list2, k2b, k2e, lane,
                 [&](uint32_t a, uint32_t b, uint32_t cc) { return Wr[a] * (X1r[b] * Gr[cc]); },
                 [&](int k2, float acc) {
-                    const float s = bw_wave_sum(acc);
-                    if (lane == 0) ws_x2[(tile * N + n) * nc2 + k2] = s;
+                    if constexpr (SHARED) {
+                        const float s = bw_wave_sum(acc);
+                        if (lane == 0) ws_x2[(tile * N + n) * nc2 + k2] = s;
+                    } else {
+                        GX2r[k2] = acc;
+                    }
                 });
         __syncthreads();  // the x1 rows have been read by every wave
         // gx1 into the x1 rows
         bw_pass(seg1, list1, k1b, k1e, lane,
-                [&](uint32_t a, uint32_t b, uint32_t cc) { return X2[b] * (Wr[a] * Gr[cc]); },
+                [&](uint32_t a, uint32_t b, uint32_t cc) { return X2r[b] * (Wr[a] * Gr[cc]); },
                 [&](int k, float acc) { X1r[k] = acc; });
         __syncthreads();
         TIO* dst = gx1 + row0 * nc1;
         for (int e = tid; e < nch * nc1; e += kBw1wThreads) {
             const int r = e / nc1;
             bw_store(dst + e, X1[r * st1 + (e - r * nc1)]);
+        }
+        if constexpr (!SHARED) {
+            TIO* dst2 = gx2 + row0 * nc2;
+            for (int e = tid; e < nch * nc2; e += kBw1wThreads) {
+                const int r = e / nc2;
+                bw_store(dst2 + e, GX2[r * st2 + (e - r * nc2)]);
+            }
         }
     }
     __syncthreads();
@@ -216,6 +243,65 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
             const int p = i >> 6, r = i & 63;
             if (r < nch) ws_w[(group * np + p) * C + c0 + r] = GW[r * stw + p];
         }
+}
+
+// Forward with per-unit x2: out[n,c,k3] = sum over the entries of k3 of
+// W[c,p] T x1[n,c,k1] x2[n,c,k2] (the k3-ordered list).  Same tiling as the
+// gradients: a 64-channel tile and a range of edges per workgroup, the weight rows
+// in LDS for the range, the four waves splitting the output slots.
+template <typename TIO>
+__global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
+    const TIO* __restrict__ x1, const TIO* __restrict__ x2, const float* __restrict__ wts, TIO* __restrict__ out,
+    int64_t N, int64_t C, int64_t epg, const uint32_t* __restrict__ tab) {
+    extern __shared__ float lds[];
+    const int nc1 = static_cast<int>(tab[0]), nc2 = static_cast<int>(tab[1]), nco = static_cast<int>(tab[2]);
+    const int np = static_cast<int>(tab[3]);
+    const uint32_t* __restrict__ seg3 = tab + tab[11];
+    const uint32_t* __restrict__ list3 = tab + tab[12];
+    const int stw = bw_stride(np), st1 = bw_stride(nc1), sto = bw_stride(nco), st2 = bw_stride(nc2);
+    float* Wt = lds;                       // [64][stw] weights of the tile's channels
+    float* X1 = Wt + kBw1wLanes * stw;     // [64][st1] x1 rows
+    float* X2 = X1 + kBw1wLanes * st1;     // [64][st2] x2 rows
+    float* O = X2 + kBw1wLanes * st2;      // [64][sto] output rows
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t group = blockIdx.x, tile = blockIdx.y;
+    const int64_t c0 = tile * kBw1wLanes;
+    const int nch = static_cast<int>(C - c0 < kBw1wLanes ? C - c0 : kBw1wLanes);
+    const int64_t n_begin = group * epg;
+    const int64_t n_end = n_begin + epg < N ? n_begin + epg : N;
+    const uint32_t* __restrict__ kr = tab + 31;
+    const int kb = static_cast<int>(kr[wave]), ke = static_cast<int>(kr[wave + 1]);
+
+    const int total = kBw1wLanes * (stw + st1 + st2 + sto);
+    for (int i = tid; i < total; i += kBw1wThreads) lds[i] = 0.f;
+    __syncthreads();
+    for (int e = tid; e < nch * np; e += kBw1wThreads) {
+        const int r = e / np;
+        Wt[r * stw + (e - r * np)] = wts[c0 * np + e];
+    }
+    const float* Wr = Wt + lane * stw;
+    const float* X1r = X1 + lane * st1;
+    const float* X2r = X2 + lane * st2;
+    float* Or = O + lane * sto;
+
+    for (int64_t n = n_begin; n < n_end; ++n) {
+        __syncthreads();  // the previous edge's output rows have left
+        const int64_t row0 = n * C + c0;
+        bw_load_rows(x1 + row0 * nc1, nch, nc1, st1, X1, tid);
+        bw_load_rows(x2 + row0 * nc2, nch, nc2, st2, X2, tid);
+        __syncthreads();
+        bw_pass(seg3, list3, kb, ke, lane,
+                [&](uint32_t a, uint32_t b, uint32_t cc) { return Wr[a] * (X1r[b] * X2r[cc]); },
+                [&](int k3, float acc) { Or[k3] = acc; });
+        __syncthreads();
+        TIO* dst = out + row0 * nco;
+        for (int e = tid; e < nch * nco; e += kBw1wThreads) {
+            const int r = e / nco;
+            bw_store(dst + e, O[r * sto + (e - r * nco)]);
+        }
+    }
 }
 
 // gx2[n,k2] = sum over the channel tiles (fixed order)
@@ -253,7 +339,24 @@ __global__ __launch_bounds__(64 * kBw1wReduceWaves) void spingtp_bwd_v1w_reduce_
     }
 }
 
-template <typename TIO>
+// raise a kernel's dynamic LDS limit once per device (to the family's maximum); one
+// flag set per (TIO, TAG), i.e. per kernel
+template <typename TIO, int TAG>
+hipError_t raise_lds_limit(const void* kernel) {
+    constexpr int kMaxDevices = 64;
+    static std::atomic<bool> raised[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    if (!raised[dev].load(std::memory_order_acquire)) {
+        const hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 static_cast<int>(kBw1wMaxLdsFloats * sizeof(float)));
+        if (e != hipSuccess) return e;
+        raised[dev].store(true, std::memory_order_release);
+    }
+    return hipSuccess;
+}
+
+template <typename TIO, bool SHARED>
 hipError_t launch_typed(const void* x1, const void* x2, const float* w, const void* g, void* gx1, void* gx2,
                         float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab,
                         hipStream_t stream) {
@@ -261,30 +364,25 @@ hipError_t launch_typed(const void* x1, const void* x2, const float* w, const vo
     int64_t groups = 0, epg = 0;
     bw1w_groups(N, C, &groups, &epg);
     float* ws_x2 = ws;
-    float* ws_w = ws + tiles * N * s.nc2;
+    float* ws_w = SHARED ? ws + tiles * N * s.nc2 : ws;
     if (groups > 0 && tiles > 0) {
         if (groups > 0x7fffffff || tiles > 0xffff) return hipErrorInvalidValue;
-        const size_t bytes = static_cast<size_t>(s.lds_floats) * sizeof(float);
-        if (bytes > 65536) {  // raise the dynamic LDS limit once per device
-            constexpr int kMaxDevices = 64;
-            static std::atomic<bool> raised[kMaxDevices];
-            int dev = 0;
-            if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-            if (!raised[dev].load(std::memory_order_acquire)) {
-                const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&spingtp_bwd_v1w_kernel<TIO>),
-                                                         hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                         static_cast<int>(kBw1wMaxLdsFloats * sizeof(float)));
-                if (e != hipSuccess) return e;
-                raised[dev].store(true, std::memory_order_release);
-            }
+        const int lds_floats = SHARED ? s.lds_floats : s.lds_unit_bwd;
+        const size_t bytes = static_cast<size_t>(lds_floats) * sizeof(float);
+        if (bytes > 65536) {
+            const hipError_t e = raise_lds_limit<TIO, SHARED ? 1 : 2>(
+                reinterpret_cast<const void*>(&spingtp_bwd_v1w_kernel<TIO, SHARED>));
+            if (e != hipSuccess) return e;
         }
-        hipLaunchKernelGGL(spingtp_bwd_v1w_kernel<TIO>, dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)),
-                           dim3(kBw1wThreads), bytes, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w,
-                           static_cast<const TIO*>(g), static_cast<TIO*>(gx1), ws_x2, ws_w, N, C, epg, tab);
+        hipLaunchKernelGGL((spingtp_bwd_v1w_kernel<TIO, SHARED>),
+                           dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)), dim3(kBw1wThreads), bytes,
+                           stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w,
+                           static_cast<const TIO*>(g), static_cast<TIO*>(gx1), static_cast<TIO*>(gx2), ws_x2, ws_w, N,
+                           C, epg, tab);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    const int64_t nx2 = N * s.nc2;
+    const int64_t nx2 = SHARED ? N * s.nc2 : 0;  // per-unit gx2 is written by the kernel
     if (nx2 > 0) {
         const int64_t blocks = (nx2 + 255) / 256;
         if (blocks > 0x7fffffff) return hipErrorInvalidValue;
@@ -326,14 +424,57 @@ size_t bw1w_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s) {
     return static_cast<size_t>(tiles * N * s.nc2 + groups * s.np * C);
 }
 
-hipError_t launch_bwd_v1w(int dtype, const void* x1, const void* x2, const float* w, const void* g, void* gx1,
-                          void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
+size_t bwcw_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s) {
+    int64_t groups = 0, epg = 0;
+    bw1w_groups(N, C, &groups, &epg);
+    return static_cast<size_t>(groups * s.np * C);
+}
+
+hipError_t launch_bwd_v1w(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, const void* g,
+                          void* gx1, void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
                           const uint32_t* tab, hipStream_t stream) {
-    if (s.lds_floats <= 0 || s.lds_floats > kBw1wMaxLdsFloats) return hipErrorInvalidValue;
-    if (s.lds_floats != kBw1wLanes * (2 * bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nco)) + bw_stride(s.nc2))
-        return hipErrorInvalidValue;  // the kernel carves its LDS from the table's sizes
-    return dtype == 0 ? launch_typed<float>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream)
-                      : launch_typed<uint16_t>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream);
+    // the kernel carves its LDS from the table's sizes
+    const int base = kBw1wLanes * (2 * bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nco));
+    if (shared_x2) {
+        if (s.lds_floats <= 0 || s.lds_floats > kBw1wMaxLdsFloats || s.lds_floats != base + bw_stride(s.nc2))
+            return hipErrorInvalidValue;
+        return dtype == 0 ? launch_typed<float, true>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream)
+                          : launch_typed<uint16_t, true>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream);
+    }
+    if (s.lds_unit_bwd <= 0 || s.lds_unit_bwd > kBw1wMaxLdsFloats ||
+        s.lds_unit_bwd != base + 2 * kBw1wLanes * bw_stride(s.nc2))
+        return hipErrorInvalidValue;
+    return dtype == 0 ? launch_typed<float, false>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream)
+                      : launch_typed<uint16_t, false>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream);
+}
+
+template <typename TIO>
+static hipError_t launch_fwd_typed(const void* x1, const void* x2, const float* w, void* out, int64_t N, int64_t C,
+                                   const Bw1wShape& s, const uint32_t* tab, hipStream_t stream) {
+    const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
+    int64_t groups = 0, epg = 0;
+    bw1w_groups(N, C, &groups, &epg);
+    if (groups == 0 || tiles == 0) return hipSuccess;
+    if (groups > 0x7fffffff || tiles > 0xffff) return hipErrorInvalidValue;
+    const size_t bytes = static_cast<size_t>(s.lds_unit_fwd) * sizeof(float);
+    if (bytes > 65536) {
+        const hipError_t e = raise_lds_limit<TIO, 3>(reinterpret_cast<const void*>(&spingtp_fwd_cw_kernel<TIO>));
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(spingtp_fwd_cw_kernel<TIO>, dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)),
+                       dim3(kBw1wThreads), bytes, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w,
+                       static_cast<TIO*>(out), N, C, epg, tab);
+    return hipGetLastError();
+}
+
+hipError_t launch_fwd_cw(int dtype, const void* x1, const void* x2, const float* w, void* out, int64_t N, int64_t C,
+                         const Bw1wShape& s, const uint32_t* tab, hipStream_t stream) {
+    if (s.lds_unit_fwd <= 0 || s.lds_unit_fwd > kBw1wMaxLdsFloats ||
+        s.lds_unit_fwd !=
+            kBw1wLanes * (bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nc2) + bw_stride(s.nco)))
+        return hipErrorInvalidValue;
+    return dtype == 0 ? launch_fwd_typed<float>(x1, x2, w, out, N, C, s, tab, stream)
+                      : launch_fwd_typed<uint16_t>(x1, x2, w, out, N, C, s, tab, stream);
 }
 
 }  // namespace spingtp

@@ -148,9 +148,11 @@ spingtp_status run_forward(spingtp_plan plan, const KernelEntry* k, const void* 
 
 // Gradients of the per-channel path-weighted product (backward_v1w.hip).
 // Sizes of its table; lds_floats: the LDS of one workgroup (weight, gW, x1 and
-// grad_out tiles of 64 rows and the x2 row).
+// grad_out tiles of 64 rows and the x2 row); lds_unit_bwd, lds_unit_fwd: those of
+// the per-unit x2 forms (spingtp_backward_weighted, spingtp_forward_weighted), 0
+// where they exceed 160 KB.
 struct Bw1wShape {
-    int nc1, nc2, nco, np, lds_floats;
+    int nc1, nc2, nco, np, lds_floats, lds_unit_bwd, lds_unit_fwd;
 };
 constexpr int kBw1wWaves = 4;             // waves of a workgroup, splitting each pass's keys
 constexpr int kBw1wMaxLdsFloats = 40960;  // 160 KB
@@ -165,10 +167,17 @@ void bw1w_groups(int64_t N, int64_t C, int64_t* groups, int64_t* epg);
 // Workspace of a launch, in floats: gx2 partial sums per channel tile and edge, then
 // gW partial sums per edge range, path and channel.
 size_t bw1w_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s);
+// Workspace of the per-unit x2 gradients, in floats: gW partial sums per edge range.
+size_t bwcw_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s);
 // dtype 0: fp32 x1, x2, grad_out, gx1, gx2; 1: bf16.  Weights and gW are fp32.
-hipError_t launch_bwd_v1w(int dtype, const void* x1, const void* x2, const float* w, const void* g, void* gx1,
-                          void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
+// shared_x2: x2 [N][NC2] shared by the channels (spingtp_backward_v1_weighted), else
+// x2 [N][C][NC2] per unit (spingtp_backward_weighted).
+hipError_t launch_bwd_v1w(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, const void* g,
+                          void* gx1, void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
                           const uint32_t* tab, hipStream_t stream);
+// out[n][c] = sum_p W[c][p] T_p(x1[n][c], x2[n][c]) (spingtp_forward_weighted).
+hipError_t launch_fwd_cw(int dtype, const void* x1, const void* x2, const float* w, void* out, int64_t N, int64_t C,
+                         const Bw1wShape& s, const uint32_t* tab, hipStream_t stream);
 
 // Paths of the instruction-weighted product (spingtp_paths_host): the block triples
 // (i (L+1) + l of spin index i and degree l, per input and output) on which T has

@@ -670,14 +670,17 @@ bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, 
     const List lp = make(
         np, [](const Ent& e) { return e.p; }, [](const Ent& e) { return std::array<int, 3>{e.k1, e.k2, e.k3}; },
         {nc1, nc2, nco});
-    out.assign(32, 0u);
+    const List l3 = make(
+        nco, [](const Ent& e) { return e.k3; }, [](const Ent& e) { return std::array<int, 3>{e.p, e.k1, e.k2}; },
+        {np, nc1, nc2});
+    out.assign(40, 0u);
     out[0] = static_cast<uint32_t>(nc1);
     out[1] = static_cast<uint32_t>(nc2);
     out[2] = static_cast<uint32_t>(nco);
     out[3] = static_cast<uint32_t>(np);
     out[4] = static_cast<uint32_t>(ents.size());
-    const List* lists[3] = {&l1, &l2, &lp};
-    for (int i = 0; i < 3; ++i) {  // the waves' key ranges: about equal entry counts
+    const List* lists[4] = {&l1, &l2, &lp, &l3};
+    for (int i = 0; i < 4; ++i) {  // the waves' key ranges: about equal entry counts
         const std::vector<uint32_t>& sg = lists[i]->seg;
         const int nkeys = static_cast<int>(sg.size()) - 1;
         uint32_t* kr = out.data() + 16 + 5 * i;
@@ -690,16 +693,23 @@ bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, 
             kr[w] = static_cast<uint32_t>(k);
         }
     }
-    for (int i = 0; i < 3; ++i) {
-        out[5 + i] = static_cast<uint32_t>(out.size());
+    const int seg_at[4] = {5, 6, 7, 11}, list_at[4] = {8, 9, 10, 12};
+    for (int i = 0; i < 4; ++i) {
+        out[seg_at[i]] = static_cast<uint32_t>(out.size());
         out.insert(out.end(), lists[i]->seg.begin(), lists[i]->seg.end());
     }
-    for (int i = 0; i < 3; ++i) {
+    for (int i = 0; i < 4; ++i) {
         out.resize((out.size() + 1) & ~size_t{1});  // 8-byte aligned entries
-        out[8 + i] = static_cast<uint32_t>(out.size());
+        out[list_at[i]] = static_cast<uint32_t>(out.size());
         out.insert(out.end(), lists[i]->words.begin(), lists[i]->words.end());
     }
-    if (shape != nullptr) *shape = Bw1wShape{nc1, nc2, nco, np, lds};
+    // the per-unit forms (x2 per unit): the gradients add x2 and gx2 tiles, the
+    // forward holds the weight, x1, x2 and output tiles; 0 where they do not fit
+    const int lds_unit_bwd = 64 * (2 * st(np) + st(nc1) + st(nco) + 2 * st(nc2));
+    const int lds_unit_fwd = 64 * (st(np) + st(nc1) + st(nc2) + st(nco));
+    if (shape != nullptr)
+        *shape = Bw1wShape{nc1, nc2, nco, np, lds, lds_unit_bwd <= kBw1wMaxLdsFloats ? lds_unit_bwd : 0,
+                           lds_unit_fwd <= kBw1wMaxLdsFloats ? lds_unit_fwd : 0};
     return true;
 }
 

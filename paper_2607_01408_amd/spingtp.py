@@ -323,6 +323,64 @@ class Plan:
             ws.data_ptr(), n.value, N, C, ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_v1_weighted")
         return gx1, gx2, gw
 
+    def _check_weighted(self, x1, x2, weights, grad_out=None):
+        import torch
+
+        N, C = x1.shape[0], x1.shape[1]
+        shapes = [(x1, (N, C) + tuple(self.shape_in(1))), (x2, (N, C) + tuple(self.shape_in(2)))]
+        if grad_out is not None:
+            shapes.append((grad_out, (N, C) + tuple(self.shape_out)))
+        for t, shape in shapes:
+            if (tuple(t.shape) != shape or t.dtype != self.torch_dtype or not t.is_cuda
+                    or not t.is_contiguous()):
+                raise ValueError("x1, x2 [N, C, ...] (and grad_out) must be contiguous device tensors of the "
+                                 "plan's dtype")
+        if (weights.dtype != torch.float32 or not weights.is_contiguous() or tuple(weights.shape) != (C, self.n_paths)
+                or weights.device != x1.device):
+            raise ValueError(f"weights must be a contiguous fp32 [C, {self.n_paths}] tensor on the inputs' device "
+                             "(a plan created with channel_weights=True)")
+        return N, C
+
+    def forward_weighted(self, x1, x2, weights, out=None, stream=None):
+        """spingtp_forward_weighted: per-channel path weights [C, n_paths] with x2 [N, C, ...] per unit."""
+        import torch
+
+        N, C = self._check_weighted(x1, x2, weights)
+        if out is None:
+            out = torch.empty((N, C) + self.shape_out, dtype=self.torch_dtype, device=x1.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+
+        def ptr(t):
+            return t.data_ptr() if t.numel() else None
+
+        _lib.check(_lib.lib().spingtp_forward_weighted(self._handle, ptr(x1), ptr(x2), ptr(weights), ptr(out), N, C,
+                                                       ctypes.c_void_p(stream.cuda_stream)), "spingtp_forward_weighted")
+        return out
+
+    def backward_weighted(self, x1, x2, weights, grad_out, stream=None):
+        """spingtp_backward_weighted: (grad_x1, grad_x2 [N, C, ...], grad_weights [C, n_paths] fp32) through
+        forward_weighted; the workspace comes from torch's allocator."""
+        import torch
+
+        N, C = self._check_weighted(x1, x2, weights, grad_out)
+        gx1, gx2 = torch.empty_like(x1), torch.empty_like(x2)
+        gw = torch.empty((C, self.n_paths), dtype=torch.float32, device=x1.device)
+        n = ctypes.c_size_t(0)
+        _lib.check(_lib.lib().spingtp_backward_weighted_workspace_size(self._handle, N, C, ctypes.byref(n)),
+                   "spingtp_backward_weighted_workspace_size")
+        ws = torch.empty(max(1, n.value), dtype=torch.uint8, device=x1.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+
+        def ptr(t):
+            return t.data_ptr() if t.numel() else None
+
+        _lib.check(_lib.lib().spingtp_backward_weighted(
+            self._handle, ptr(x1), ptr(x2), ptr(weights), ptr(grad_out), ptr(gx1), ptr(gx2), ptr(gw),
+            ws.data_ptr(), n.value, N, C, ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_weighted")
+        return gx1, gx2, gw
+
     __call__ = forward
 
     def close(self):

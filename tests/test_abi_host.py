@@ -806,3 +806,20 @@ def test_weighted_backward_lists_reproduce_oracle(built_library, L1, L2, LO, spi
         assert np.linalg.norm(e2 - r2[n]) <= 1e-6 * np.linalg.norm(r2[n])
         gW += eW
     assert np.linalg.norm(gW - rW) <= 1e-6 * np.linalg.norm(rW)
+    # the k3-ordered list (spingtp_forward_weighted, x2 per unit) and its key ranges
+    s3 = words[int(words[11]):int(words[11]) + n3 + 1].astype(np.int64)
+    l3 = words[int(words[12]):]
+    kr = words[31:36].astype(np.int64)
+    assert kr[0] == 0 and kr[-1] == n3 and np.all(np.diff(kr) >= 0) and np.all(np.diff(s3) % 8 == 0)
+    x2u = rng.standard_normal((N, C, n2)) * valid_mask(spins, L2).ravel()
+    ref = oracle.channel_weighted(x1, x2u, W, L1, L2, LO, spins, basis).reshape(N, C, -1)
+    pad = lambda a: np.concatenate([a, np.zeros(a.shape[:-1] + (1,))], axis=-1)
+    X1, X2, Wp = pad(x1), pad(x2u), pad(W)
+    y = np.zeros((N, C, n3))
+    for k3 in range(n3):
+        w = l3[2 * int(s3[k3]):2 * int(s3[k3 + 1])].reshape(-1, 2)
+        f = w[:, 0].astype(np.int64)
+        p, a, b = f & 0x3ff, (f >> 10) & 0x3ff, f >> 20
+        v = w[:, 1].view(np.float32).astype(np.float64)
+        y[:, :, k3] = (v * Wp[None, :, p] * X1[:, :, a] * X2[:, :, b]).sum(axis=-1)
+    assert np.linalg.norm(y - ref) <= 1e-6 * np.linalg.norm(ref)

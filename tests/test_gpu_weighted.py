@@ -178,9 +178,11 @@ def test_channel_weighted_rules():
     y = plan.forward_v1_weighted(x1, x2, torch.zeros((3, n), device="cuda"))
     torch.cuda.synchronize()
     assert not y.any()
-    # path slots beyond the forward's instantiations (degree 3 with spins {-1, 0, +1}): the plan
-    # holds only the gradients' table
-    plan3 = Plan(3, 3, 3, S3, "fp32", channel_weights=True)
+    # path slots beyond the forward's instantiations (degree 3 with spins {-1, 0, +1}, parity
+    # basis): the plan holds only the gradients' table; in the paper basis (335 paths) neither fits
+    plan3 = Plan(3, 3, 3, S3, "fp32", 2, channel_weights=True)
+    with pytest.raises(SpinGTPError):
+        Plan(3, 3, 3, S3, "fp32", 0, channel_weights=True)
     x13 = torch.zeros((2, 3, 3, 16), device="cuda")
     with pytest.raises(SpinGTPError):
         plan3.forward_v1_weighted(x13, torch.zeros((2, 1, 3, 16), device="cuda"),
@@ -310,3 +312,97 @@ def test_channel_weighted_backward_rules():
 def ctypes_size_t():
     import ctypes
     return ctypes.c_size_t(0)
+
+
+# --- per-channel path weights with a per-unit second input (spingtp_forward_weighted and
+# spingtp_backward_weighted, mode uuu) ---
+
+def run_channel_weighted_unit(L1, L2, LO, spins, N, C, basis=0, dtype="fp32", seed=0):
+    P = paths_host(L1, L2, LO, spins, basis)
+    print(f"[weighted-unit] L=({L1},{L2},{LO}) spins={spins} basis={basis} N={N} C={C} {dtype} paths={len(P)}",
+          flush=True)
+    rng = np.random.default_rng(200 + seed)
+    W = torch.as_tensor(rng.standard_normal((C, len(P))), dtype=torch.float32, device="cuda")
+    x1 = workloads.draw(L1, N, C, 70 + seed, dtype, spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, C, 71 + seed, dtype, spins, "unit", "cuda")
+    g = workloads.draw(LO, N, C, 72 + seed, dtype, spins, "unit", "cuda")
+    plan = Plan(L1, L2, LO, spins, dtype, basis, channel_weights=True)
+    y = plan.forward_weighted(x1, x2, W)
+    gx1, gx2, gW = plan.backward_weighted(x1, x2, W, g)
+    torch.cuda.synchronize()
+    a, b, c = (host(t, N * C).reshape(N, C, -1) for t in (x1, x2, g))
+    Wd = W.double().cpu().numpy()
+    ref = oracle.channel_weighted(a, b, Wd, L1, L2, LO, spins, basis).reshape(N * C, -1)
+    r1, r2, rW = oracle.channel_weighted_vjp(a, b, Wd, c, L1, L2, LO, spins, basis)
+    ey = rel_l2(host(y, N * C), ref)
+    e1 = rel_l2(host(gx1, N * C), r1.reshape(N * C, -1))
+    e2 = rel_l2(host(gx2, N * C), r2.reshape(N * C, -1))
+    eW = rel_l2(gW.double().cpu().numpy(), rW)
+    print(f"[weighted-unit]   rel_l2 y={ey:.3e} gx1={e1:.3e} gx2={e2:.3e} gW={eW:.3e}", flush=True)
+    tol = TOL[dtype]
+    assert max(ey, e1, e2, eW) <= tol, (ey, e1, e2, eW)
+    return plan, (x1, x2, W, g), (y, gx1, gx2, gW)
+
+
+@pytest.mark.parametrize("shape,C,basis", [((1, 1, 1), 16, 0), ((2, 2, 2), 64, 2), ((2, 2, 2), 70, 0),
+                                           ((1, 3, 3), 128, 0), ((1, 3, 3), 33, 2)])
+def test_channel_weighted_unit_shapes(shape, C, basis):
+    run_channel_weighted_unit(*shape, S3, 9, C, basis, seed=C + sum(shape))
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [(2, 1, 2, S5, 0), (3, 3, 3, S3, 2), (2, 2, 2, (0,), 0)])
+def test_channel_weighted_unit_other_shapes(L1, L2, LO, spins, basis):
+    run_channel_weighted_unit(L1, L2, LO, spins, 5, 40, basis, seed=L1 + 5 * L2)
+
+
+def test_channel_weighted_unit_many_edge_ranges():
+    # 1500 edges over 3 channel tiles (130 channels): several edges per workgroup
+    run_channel_weighted_unit(1, 1, 1, S3, 1500, 130, 0, seed=8)
+
+
+def test_channel_weighted_unit_bf16():
+    run_channel_weighted_unit(2, 2, 2, S3, 9, 48, 2, "bf16", seed=6)
+
+
+def test_channel_weighted_unit_matches_the_shared_form():
+    # x2 equal over the channels of an edge: the per-unit kernels agree with the V = 1 ones
+    N, C = 21, 70
+    n = len(paths_host(2, 2, 2))
+    plan = Plan(2, 2, 2, S3, "fp32", 0, channel_weights=True)
+    W = torch.randn((C, n), generator=torch.Generator().manual_seed(3)).to("cuda")
+    x1 = workloads.draw(2, N, C, 80, "fp32", S3, "unit", "cuda")
+    x2s = workloads.draw(2, N, 1, 81, "fp32", S3, "unit", "cuda")
+    g = workloads.draw(2, N, C, 82, "fp32", S3, "unit", "cuda")
+    x2 = x2s.expand(N, C, 3, 9).contiguous()
+    y = plan.forward_weighted(x1, x2, W)
+    y1 = plan.forward_v1_weighted(x1, x2s, W)
+    gx1, gx2, gW = plan.backward_weighted(x1, x2, W, g)
+    hx1, hx2, hW = plan.backward_v1_weighted(x1, x2s, W, g)
+    torch.cuda.synchronize()
+    assert rel_l2(host(y, N * C), host(y1, N * C)) <= 1e-6
+    assert rel_l2(host(gx1, N * C), host(hx1, N * C)) <= 1e-6
+    assert rel_l2(host(gx2.sum(dim=1, keepdim=True), N), host(hx2, N)) <= 1e-5
+    assert rel_l2(gW.double().cpu().numpy(), hW.double().cpu().numpy()) <= 1e-6
+
+
+def test_channel_weighted_unit_empty_and_rules():
+    plan = Plan(2, 2, 2, S3, "fp32", channel_weights=True)
+    n = plan.n_paths
+    x1, x2 = torch.zeros((0, 8, 3, 9), device="cuda"), torch.zeros((0, 8, 3, 9), device="cuda")
+    W = torch.ones((8, n), device="cuda")
+    y = plan.forward_weighted(x1, x2, W)
+    gx1, gx2, gW = plan.backward_weighted(x1, x2, W, x1)
+    torch.cuda.synchronize()
+    assert y.shape == (0, 8, 3, 9) and gW.shape == (8, n) and not gW.any()
+    x1 = torch.zeros((2, 3, 3, 9), device="cuda")
+    with pytest.raises(ValueError):  # a plan without channel weights has no path count
+        Plan(2, 2, 2, S3, "fp32").forward_weighted(x1, x1, torch.zeros((3, n), device="cuda"))
+    with pytest.raises(ValueError):  # x2 per unit
+        plan.forward_weighted(x1, x1[:, :1].contiguous(), torch.zeros((3, n), device="cuda"))
+    from paper_2607_01408_amd import _lib
+    w = torch.zeros((3, n), device="cuda")
+    y = torch.empty_like(x1)
+    assert _lib.lib().spingtp_forward_weighted(Plan(2, 2, 2, S3, "fp32").handle, x1.data_ptr(), x1.data_ptr(),
+                                               w.data_ptr(), y.data_ptr(), 2, 3, None) == 2
+    assert _lib.lib().spingtp_forward_weighted(plan.handle, x1.data_ptr(), x1.data_ptr(), None, y.data_ptr(), 2, 3,
+                                               None) == 1
