@@ -306,6 +306,58 @@ def run_v1(args):
                 "parity_rel_l2_gx2_sampled": float(np.linalg.norm(got2 - r2) / np.linalg.norm(r2)),
                 "gw_identity_rel": ident, "units_per_s": B * C / (ms / 1e3)}
 
+    def measure_weighted_unit(L1, L2, LO, C, B, basis, seed):
+        """spingtp_forward_weighted and spingtp_backward_weighted (per-channel path weights, x2 per
+        unit), preallocated buffers; parity of the forward and gx2 on sampled edges against the oracle."""
+        import oracle
+        from paper_2607_01408_amd import paths_host
+
+        try:
+            plan = Plan(L1, L2, LO, workloads.SPINS, "fp32", basis, channel_weights=True)
+        except Exception:
+            return None
+        n_paths = len(paths_host(L1, L2, LO, workloads.SPINS, basis))
+        x1 = workloads.draw(L1, B, C, 9610 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        x2 = workloads.draw(L2, B, C, 9710 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        g = workloads.draw(LO, B, C, 9810 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        w = torch.randn((C, n_paths), generator=torch.Generator().manual_seed(seed)).to("cuda:0")
+        out = torch.empty_like(g)
+        gx1, gx2 = torch.empty_like(x1), torch.empty_like(x2)
+        gw = torch.empty_like(w)
+        n = ctypes.c_size_t(0)
+        if _lib.lib().spingtp_backward_weighted_workspace_size(plan.handle, B, C, ctypes.byref(n)) != 0:
+            return None
+        ws = torch.empty(max(1, n.value), dtype=torch.uint8, device="cuda:0")
+        st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        calls = {"forward": (_lib.lib().spingtp_forward_weighted,
+                             (plan.handle, x1.data_ptr(), x2.data_ptr(), w.data_ptr(), out.data_ptr(), B, C, st)),
+                 "backward": (_lib.lib().spingtp_backward_weighted,
+                              (plan.handle, x1.data_ptr(), x2.data_ptr(), w.data_ptr(), g.data_ptr(), gx1.data_ptr(),
+                               gx2.data_ptr(), gw.data_ptr(), ws.data_ptr(), n.value, B, C, st))}
+        res = {"paths": n_paths, "basis": basis}
+        for name, (fn_, call) in calls.items():
+            for _ in range(args.warmup):
+                assert fn_(*call) == 0
+            torch.cuda.synchronize()
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            for _ in range(args.steps):
+                fn_(*call)
+            e.record()
+            torch.cuda.synchronize()
+            res[name + "_ms"] = s.elapsed_time(e) / args.steps
+        edges = sorted({0, B // 2, B - 1})
+        sel = torch.as_tensor(edges, device="cuda:0")
+        a, b, c = (t[sel].double().cpu().numpy().reshape(len(edges), C, -1) for t in (x1, x2, g))
+        W = w.double().cpu().numpy()
+        ref = oracle.channel_weighted(a, b, W, L1, L2, LO, workloads.SPINS, basis).reshape(a.shape[0], C, -1)
+        _, r2, _ = oracle.channel_weighted_vjp(a, b, W, c, L1, L2, LO, workloads.SPINS, basis)
+        got = out[sel].double().cpu().numpy().reshape(ref.shape)
+        got2 = gx2[sel].double().cpu().numpy().reshape(r2.shape)
+        res["parity_rel_l2_sampled"] = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+        res["parity_rel_l2_gx2_sampled"] = float(np.linalg.norm(got2 - r2) / np.linalg.norm(r2))
+        return res
+
     def measure_backward(L, C, B, seed):
         """spingtp_backward_v1 (both gradients) on the default route, preallocated buffers."""
         x1 = workloads.draw(L, B, C, 9300 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
@@ -340,13 +392,19 @@ def run_v1(args):
         for name, basis in (("channel_weighted_parity_basis", 2), ("channel_weighted_paper_basis", 0)):
             row[name] = measure_weighted(L1, L2, LO, C, B, basis, L1 + 3 * L2 + C)
             row[name + "_backward"] = measure_weighted_backward(L1, L2, LO, C, B, basis, L1 + 3 * L2 + C)
+        for name, basis in (("channel_weighted_unit_parity_basis", 2), ("channel_weighted_unit_paper_basis", 0)):
+            row[name] = measure_weighted_unit(L1, L2, LO, C, B, basis, L1 + 3 * L2 + C)
         table.append(row)
         print(f"[v1] ({L1},{L2},{LO}) C={C} B={B}: pre {row['precontracted']['ms'] * 1e3:.1f} us, "
               f"fourier {row['fourier']['ms'] * 1e3:.1f} us, weighted (parity / paper basis) "
               f"{row['channel_weighted_parity_basis']['ms'] * 1e3:.1f} / "
               f"{row['channel_weighted_paper_basis']['ms'] * 1e3:.1f} us, its gradients "
               f"{row['channel_weighted_parity_basis_backward']['ms'] * 1e3:.1f} / "
-              f"{row['channel_weighted_paper_basis_backward']['ms'] * 1e3:.1f} us", file=sys.stderr, flush=True)
+              f"{row['channel_weighted_paper_basis_backward']['ms'] * 1e3:.1f} us; x2 per unit: forward "
+              f"{row['channel_weighted_unit_parity_basis']['forward_ms'] * 1e3:.1f} / "
+              f"{row['channel_weighted_unit_paper_basis']['forward_ms'] * 1e3:.1f} us, gradients "
+              f"{row['channel_weighted_unit_parity_basis']['backward_ms'] * 1e3:.1f} / "
+              f"{row['channel_weighted_unit_paper_basis']['backward_ms'] * 1e3:.1f} us", file=sys.stderr, flush=True)
     sweep = []
     for L in args.v1_sweep_degrees:
         row = {"L": L, "C": args.v1_sweep_channels, "B": args.v1_sweep_edges}

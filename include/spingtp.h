@@ -200,14 +200,20 @@ spingtp_status spingtp_forward_v1(spingtp_plan plan, const void* x1, const void*
  *   weights: device fp32 [C][n_paths], 4-byte aligned, read only.
  *   x1, x2, out, N, C, stream: as spingtp_forward_v1.
  * Needs a plan created with SPINGTP_CHANNEL_WEIGHTS (else SPINGTP_ERR_UNSUPPORTED).
- * Route: the precontracted kernel over path slots q = (p, k1): per edge the kernel
+ * Route: the entry-list kernel of spingtp_forward_weighted with the x2 row shared
+ * by the tile's channels (four waves per 64-channel tile walk the tensor's nonzeros
+ * by output slot; measured faster on the depthwise runtime table's shapes), where
+ * the plan's lists hold the shape and the plan was not created with
+ * SPINGTP_V1_PRECONTRACT; otherwise the precontracted kernel over path slots
+ * q = (p, k1): per edge the kernel
  * K[q][k3] = sum_{k2 on p} T x2 is built once, and each channel's operand is
  * weights[c][p] x1[c][k1]; the contraction then runs over all path slots (at L = 2
  * with spins {-1, 0, +1}: 263 in the parity basis, 471 in the paper basis, whose
  * +-1 blocks split paths; 27 without weights).  Built for shapes whose
  * path slots fit 480 and output rows 48 (the depthwise runtime table's shapes,
- * degree <= 2 with spins {-1, 0, +1}, (1, 3, 3), degree <= 4 with spin {0});
- * plan creation with the flag fails with SPINGTP_ERR_UNSUPPORTED otherwise.
+ * degree <= 2 with spins {-1, 0, +1}, (1, 3, 3), degree <= 4 with spin {0}).
+ * Plan creation with SPINGTP_CHANNEL_WEIGHTS fails with SPINGTP_ERR_UNSUPPORTED
+ * when neither route nor the gradients' lists hold the shape.
  * Gradients: spingtp_backward_v1_weighted.  Asynchronous, no allocation.
  */
 spingtp_status spingtp_forward_v1_weighted(spingtp_plan plan, const void* x1, const void* x2,

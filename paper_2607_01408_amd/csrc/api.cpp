@@ -49,10 +49,27 @@ extern "C" spingtp_status spingtp_forward_v1_weighted(spingtp_plan plan, const v
                                                       const float* weights, void* out, int64_t N, int64_t C,
                                                       void* stream) {
     if (plan == nullptr) return SPINGTP_ERR_INVALID_ARG;
-    if (plan->kernel_v1w == nullptr) return SPINGTP_ERR_UNSUPPORTED;
+    // the entry-list kernel unless the plan asks for the precontracted route
+    const bool entry_lists = plan->d_bw1w != nullptr && plan->bw1w.lds_shared_fwd > 0 &&
+                             !((plan->flags & SPINGTP_V1_PRECONTRACT) && plan->kernel_v1w != nullptr);
+    if (plan->kernel_v1w == nullptr && !entry_lists) return SPINGTP_ERR_UNSUPPORTED;
     if (N > 0 && C > 0 && (weights == nullptr || (reinterpret_cast<uintptr_t>(weights) & 3u) != 0))
         return SPINGTP_ERR_INVALID_ARG;
-    // the weighted kernel takes the weights in place of the plan tables
+    if (entry_lists) {  // the entry-list kernel (measured faster on the depthwise runtime table's shapes)
+        if (N < 0 || C < 0) return SPINGTP_ERR_INVALID_ARG;
+        if (N == 0 || C == 0) return SPINGTP_OK;
+        if (N > (int64_t{1} << 40) / C) return SPINGTP_ERR_INVALID_ARG;
+        if (x1 == nullptr || x2 == nullptr || out == nullptr) return SPINGTP_ERR_INVALID_ARG;
+        const auto misaligned = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; };
+        if (misaligned(x1) || misaligned(x2) || misaligned(out)) return SPINGTP_ERR_INVALID_ARG;
+        int cur = -1;
+        if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
+        if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
+        const hipError_t e = spingtp::launch_fwd_cw(plan->dtype == SPINGTP_FP32 ? 0 : 1, true, x1, x2, weights, out,
+                                                    N, C, plan->bw1w, plan->d_bw1w, static_cast<hipStream_t>(stream));
+        return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
+    }
+    // the weighted precontracted kernel takes the weights in place of the plan tables
     return spingtp::run_forward(plan, plan->kernel_v1w, x1, x2, out, N, C, true, stream, weights, false,
                                 plan->d_pre_w);
 }
@@ -107,8 +124,8 @@ extern "C" spingtp_status spingtp_forward_weighted(spingtp_plan plan, const void
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
     if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
-    const hipError_t e = spingtp::launch_fwd_cw(plan->dtype == SPINGTP_FP32 ? 0 : 1, x1, x2, weights, out, N, C,
-                                                plan->bw1w, plan->d_bw1w, static_cast<hipStream_t>(stream));
+    const hipError_t e = spingtp::launch_fwd_cw(plan->dtype == SPINGTP_FP32 ? 0 : 1, false, x1, x2, weights, out, N,
+                                                C, plan->bw1w, plan->d_bw1w, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
 }
 

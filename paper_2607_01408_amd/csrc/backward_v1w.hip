@@ -245,11 +245,11 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
         }
 }
 
-// Forward with per-unit x2: out[n,c,k3] = sum over the entries of k3 of
-// W[c,p] T x1[n,c,k1] x2[n,c,k2] (the k3-ordered list).  Same tiling as the
-// gradients: a 64-channel tile and a range of edges per workgroup, the weight rows
-// in LDS for the range, the four waves splitting the output slots.
-template <typename TIO>
+// Forward: out[n,c,k3] = sum over the entries of k3 of W[c,p] T x1[n,c,k1] x2[.,k2]
+// (the k3-ordered list), x2 per unit or (SHARED) one row per edge.  Same tiling as
+// the gradients: a 64-channel tile and a range of edges per workgroup, the weight
+// rows in LDS for the range, the four waves splitting the output slots.
+template <typename TIO, bool SHARED>
 __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
     const TIO* __restrict__ x1, const TIO* __restrict__ x2, const float* __restrict__ wts, TIO* __restrict__ out,
     int64_t N, int64_t C, int64_t epg, const uint32_t* __restrict__ tab) {
@@ -261,8 +261,8 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
     const int stw = bw_stride(np), st1 = bw_stride(nc1), sto = bw_stride(nco), st2 = bw_stride(nc2);
     float* Wt = lds;                       // [64][stw] weights of the tile's channels
     float* X1 = Wt + kBw1wLanes * stw;     // [64][st1] x1 rows
-    float* X2 = X1 + kBw1wLanes * st1;     // [64][st2] x2 rows
-    float* O = X2 + kBw1wLanes * st2;      // [64][sto] output rows
+    float* O = X1 + kBw1wLanes * st1;      // [64][sto] output rows
+    float* X2 = O + kBw1wLanes * sto;      // [64][st2] x2 rows, or (SHARED) the edge's x2 row
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -274,7 +274,7 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
     const uint32_t* __restrict__ kr = tab + 31;
     const int kb = static_cast<int>(kr[wave]), ke = static_cast<int>(kr[wave + 1]);
 
-    const int total = kBw1wLanes * (stw + st1 + st2 + sto);
+    const int total = kBw1wLanes * (stw + st1 + sto) + (SHARED ? st2 : kBw1wLanes * st2);
     for (int i = tid; i < total; i += kBw1wThreads) lds[i] = 0.f;
     __syncthreads();
     for (int e = tid; e < nch * np; e += kBw1wThreads) {
@@ -283,14 +283,18 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
     }
     const float* Wr = Wt + lane * stw;
     const float* X1r = X1 + lane * st1;
-    const float* X2r = X2 + lane * st2;
+    const float* X2r = SHARED ? X2 : X2 + lane * st2;
     float* Or = O + lane * sto;
 
     for (int64_t n = n_begin; n < n_end; ++n) {
         __syncthreads();  // the previous edge's output rows have left
         const int64_t row0 = n * C + c0;
         bw_load_rows(x1 + row0 * nc1, nch, nc1, st1, X1, tid);
-        bw_load_rows(x2 + row0 * nc2, nch, nc2, st2, X2, tid);
+        if constexpr (SHARED) {
+            for (int k = tid; k < nc2; k += kBw1wThreads) X2[k] = bw_load(x2 + n * nc2 + k);
+        } else {
+            bw_load_rows(x2 + row0 * nc2, nch, nc2, st2, X2, tid);
+        }
         __syncthreads();
         bw_pass(seg3, list3, kb, ke, lane,
                 [&](uint32_t a, uint32_t b, uint32_t cc) { return Wr[a] * (X1r[b] * X2r[cc]); },
@@ -448,33 +452,40 @@ hipError_t launch_bwd_v1w(int dtype, bool shared_x2, const void* x1, const void*
                       : launch_typed<uint16_t, false>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream);
 }
 
-template <typename TIO>
+template <typename TIO, bool SHARED>
 static hipError_t launch_fwd_typed(const void* x1, const void* x2, const float* w, void* out, int64_t N, int64_t C,
-                                   const Bw1wShape& s, const uint32_t* tab, hipStream_t stream) {
+                                   int lds_floats, const uint32_t* tab, hipStream_t stream) {
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     int64_t groups = 0, epg = 0;
     bw1w_groups(N, C, &groups, &epg);
     if (groups == 0 || tiles == 0) return hipSuccess;
     if (groups > 0x7fffffff || tiles > 0xffff) return hipErrorInvalidValue;
-    const size_t bytes = static_cast<size_t>(s.lds_unit_fwd) * sizeof(float);
+    const size_t bytes = static_cast<size_t>(lds_floats) * sizeof(float);
     if (bytes > 65536) {
-        const hipError_t e = raise_lds_limit<TIO, 3>(reinterpret_cast<const void*>(&spingtp_fwd_cw_kernel<TIO>));
+        const hipError_t e = raise_lds_limit<TIO, SHARED ? 3 : 4>(
+            reinterpret_cast<const void*>(&spingtp_fwd_cw_kernel<TIO, SHARED>));
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(spingtp_fwd_cw_kernel<TIO>, dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)),
-                       dim3(kBw1wThreads), bytes, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w,
-                       static_cast<TIO*>(out), N, C, epg, tab);
+    hipLaunchKernelGGL((spingtp_fwd_cw_kernel<TIO, SHARED>),
+                       dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)), dim3(kBw1wThreads), bytes,
+                       stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w, static_cast<TIO*>(out), N,
+                       C, epg, tab);
     return hipGetLastError();
 }
 
-hipError_t launch_fwd_cw(int dtype, const void* x1, const void* x2, const float* w, void* out, int64_t N, int64_t C,
-                         const Bw1wShape& s, const uint32_t* tab, hipStream_t stream) {
-    if (s.lds_unit_fwd <= 0 || s.lds_unit_fwd > kBw1wMaxLdsFloats ||
-        s.lds_unit_fwd !=
-            kBw1wLanes * (bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nc2) + bw_stride(s.nco)))
+hipError_t launch_fwd_cw(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, void* out,
+                         int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab, hipStream_t stream) {
+    // the kernel carves its LDS from the table's sizes
+    const int base = kBw1wLanes * (bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nco));
+    const int lds = shared_x2 ? s.lds_shared_fwd : s.lds_unit_fwd;
+    if (lds <= 0 || lds > kBw1wMaxLdsFloats ||
+        lds != base + (shared_x2 ? bw_stride(s.nc2) : kBw1wLanes * bw_stride(s.nc2)))
         return hipErrorInvalidValue;
-    return dtype == 0 ? launch_fwd_typed<float>(x1, x2, w, out, N, C, s, tab, stream)
-                      : launch_fwd_typed<uint16_t>(x1, x2, w, out, N, C, s, tab, stream);
+    if (shared_x2)
+        return dtype == 0 ? launch_fwd_typed<float, true>(x1, x2, w, out, N, C, lds, tab, stream)
+                          : launch_fwd_typed<uint16_t, true>(x1, x2, w, out, N, C, lds, tab, stream);
+    return dtype == 0 ? launch_fwd_typed<float, false>(x1, x2, w, out, N, C, lds, tab, stream)
+                      : launch_fwd_typed<uint16_t, false>(x1, x2, w, out, N, C, lds, tab, stream);
 }
 
 }  // namespace spingtp

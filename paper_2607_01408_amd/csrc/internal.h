@@ -150,9 +150,10 @@ spingtp_status run_forward(spingtp_plan plan, const KernelEntry* k, const void* 
 // Sizes of its table; lds_floats: the LDS of one workgroup (weight, gW, x1 and
 // grad_out tiles of 64 rows and the x2 row); lds_unit_bwd, lds_unit_fwd: those of
 // the per-unit x2 forms (spingtp_backward_weighted, spingtp_forward_weighted), 0
-// where they exceed 160 KB.
+// where they exceed 160 KB; lds_shared_fwd: that of the entry-list forward with x2
+// shared by the channels (spingtp_forward_v1_weighted), 0 where it exceeds 160 KB.
 struct Bw1wShape {
-    int nc1, nc2, nco, np, lds_floats, lds_unit_bwd, lds_unit_fwd;
+    int nc1, nc2, nco, np, lds_floats, lds_unit_bwd, lds_unit_fwd, lds_shared_fwd;
 };
 constexpr int kBw1wWaves = 4;             // waves of a workgroup, splitting each pass's keys
 constexpr int kBw1wMaxLdsFloats = 40960;  // 160 KB
@@ -175,9 +176,10 @@ size_t bwcw_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s);
 hipError_t launch_bwd_v1w(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, const void* g,
                           void* gx1, void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
                           const uint32_t* tab, hipStream_t stream);
-// out[n][c] = sum_p W[c][p] T_p(x1[n][c], x2[n][c]) (spingtp_forward_weighted).
-hipError_t launch_fwd_cw(int dtype, const void* x1, const void* x2, const float* w, void* out, int64_t N, int64_t C,
-                         const Bw1wShape& s, const uint32_t* tab, hipStream_t stream);
+// out[n][c] = sum_p W[c][p] T_p(x1[n][c], x2[n][c]) (spingtp_forward_weighted), or with
+// x2[n] shared by the channels (shared_x2, spingtp_forward_v1_weighted).
+hipError_t launch_fwd_cw(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, void* out,
+                         int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab, hipStream_t stream);
 
 // Paths of the instruction-weighted product (spingtp_paths_host): the block triples
 // (i (L+1) + l of spin index i and degree l, per input and output) on which T has

@@ -707,9 +707,11 @@ bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, 
     // forward holds the weight, x1, x2 and output tiles; 0 where they do not fit
     const int lds_unit_bwd = 64 * (2 * st(np) + st(nc1) + st(nco) + 2 * st(nc2));
     const int lds_unit_fwd = 64 * (st(np) + st(nc1) + st(nc2) + st(nco));
+    const int lds_shared_fwd = 64 * (st(np) + st(nc1) + st(nco)) + st(nc2);
     if (shape != nullptr)
         *shape = Bw1wShape{nc1, nc2, nco, np, lds, lds_unit_bwd <= kBw1wMaxLdsFloats ? lds_unit_bwd : 0,
-                           lds_unit_fwd <= kBw1wMaxLdsFloats ? lds_unit_fwd : 0};
+                           lds_unit_fwd <= kBw1wMaxLdsFloats ? lds_unit_fwd : 0,
+                           lds_shared_fwd <= kBw1wMaxLdsFloats ? lds_shared_fwd : 0};
     return true;
 }
 

@@ -178,15 +178,18 @@ def test_channel_weighted_rules():
     y = plan.forward_v1_weighted(x1, x2, torch.zeros((3, n), device="cuda"))
     torch.cuda.synchronize()
     assert not y.any()
-    # path slots beyond the forward's instantiations (degree 3 with spins {-1, 0, +1}, parity
-    # basis): the plan holds only the gradients' table; in the paper basis (335 paths) neither fits
-    plan3 = Plan(3, 3, 3, S3, "fp32", 2, channel_weights=True)
+    # path slots beyond the precontracted kernel's instantiations (degree 3 with spins {-1, 0, +1},
+    # parity basis): the forward runs on the entry lists only; with SPINGTP_V1_PRECONTRACT too, as
+    # that route does not exist; in the paper basis (335 paths) nothing fits
     with pytest.raises(SpinGTPError):
         Plan(3, 3, 3, S3, "fp32", 0, channel_weights=True)
-    x13 = torch.zeros((2, 3, 3, 16), device="cuda")
-    with pytest.raises(SpinGTPError):
-        plan3.forward_v1_weighted(x13, torch.zeros((2, 1, 3, 16), device="cuda"),
-                                  torch.zeros((3, plan3.n_paths), device="cuda"))
+    for pre in (False, True):
+        plan3 = Plan(3, 3, 3, S3, "fp32", 2, channel_weights=True, v1_precontract=pre)
+        x13 = torch.ones((2, 3, 3, 16), device="cuda")
+        y3 = plan3.forward_v1_weighted(x13, torch.ones((2, 1, 3, 16), device="cuda"),
+                                       torch.zeros((3, plan3.n_paths), device="cuda"))
+        torch.cuda.synchronize()
+        assert not y3.any()
     with pytest.raises(SpinGTPError):  # neither fits: 2002 paths at degree 6
         Plan(6, 6, 6, S3, "fp32", channel_weights=True)
 
@@ -406,3 +409,18 @@ def test_channel_weighted_unit_empty_and_rules():
                                                w.data_ptr(), y.data_ptr(), 2, 3, None) == 2
     assert _lib.lib().spingtp_forward_weighted(plan.handle, x1.data_ptr(), x1.data_ptr(), None, y.data_ptr(), 2, 3,
                                                None) == 1
+
+
+@pytest.mark.parametrize("shape,basis", [((2, 2, 2), 2), ((1, 3, 3), 0), ((1, 1, 1), 0)])
+def test_channel_weighted_v1_routes_agree(shape, basis):
+    # the default entry-list route and the precontracted route (SPINGTP_V1_PRECONTRACT) of
+    # spingtp_forward_v1_weighted on the same data
+    N, C = 17, 70
+    n = len(paths_host(*shape, S3, basis))
+    W = torch.randn((C, n), generator=torch.Generator().manual_seed(11)).to("cuda")
+    x1 = workloads.draw(shape[0], N, C, 90, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(shape[1], N, 1, 91, "fp32", S3, "unit", "cuda")
+    y0 = Plan(*shape, S3, "fp32", basis, channel_weights=True).forward_v1_weighted(x1, x2, W)
+    y1 = Plan(*shape, S3, "fp32", basis, channel_weights=True, v1_precontract=True).forward_v1_weighted(x1, x2, W)
+    torch.cuda.synchronize()
+    assert rel_l2(host(y0, N * C), host(y1, N * C)) <= 1e-6
