@@ -31,7 +31,7 @@ from .swsh import swsh, theta_part, goldberg_prefactor
 from .realbasis import q_matrix, real_index, conjugation_map, parity_mix, BASIS_PAPER, BASIS_M0_PAIRED, BASIS_PARITY
 from .gaunt import gauss_legendre_grid, gaunt_block, gaunt_full_quadrature
 from .spingtp import (RealGauntTensor, PathWeightedTensor, slot_blocks, spingtp, spingtp_vjp, channel_weighted_v1,
-                      channel_weighted_v1_vjp, channel_weighted, channel_weighted_vjp)
+                      channel_weighted_v1_vjp, channel_weighted, channel_weighted_vjp, depthwise, depthwise_vjp)
 
 __all__ = [
     "swsh", "theta_part", "goldberg_prefactor",
@@ -39,4 +39,5 @@ __all__ = [
     "gauss_legendre_grid", "gaunt_block", "gaunt_full_quadrature",
     "RealGauntTensor", "PathWeightedTensor", "slot_blocks", "spingtp", "spingtp_vjp",
     "channel_weighted_v1", "channel_weighted_v1_vjp", "channel_weighted", "channel_weighted_vjp",
+    "depthwise", "depthwise_vjp",
 ]

@@ -356,3 +356,44 @@ def channel_weighted_vjp(x1, x2, weights, g, L1, L2, Lout, spins=(-1, 0, 1), bas
         per_entry = (X1[:, c, k1] * X2[:, c, k2] * G[:, c, k3]).sum(axis=0) * val
         gW[c] = np.bincount(path, weights=per_entry, minlength=n_paths)
     return gx1.reshape(x1.shape), gx2.reshape(x2.shape), gW
+
+
+def depthwise(x1, x2, weights, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Depthwise product (App. E.1 mode uvu) with V second-input channels per edge and one
+    weight per (path, u, v): out[n, u] = sum_v sum_p W[v, u, p] T_p(x1[n, u], x2[n, v]),
+    T_p the tensor restricted to path p (eq. spin_gtp).
+
+    x1 [N, U, ...], x2 [N, V, ...], weights [V, U, P] (v-major, so that V = 1 is the
+    layout of channel_weighted_v1)."""
+    spins = tuple(spins)
+    x1 = np.asarray(x1, dtype=np.float64)
+    N, U = x1.shape[:2]
+    X2 = np.asarray(x2, dtype=np.float64).reshape(N, -1, len(spins) * (L2 + 1) ** 2)
+    W = np.asarray(weights, dtype=np.float64).reshape(X2.shape[1], U, -1)
+    out = np.zeros((N, U, len(spins), (Lout + 1) ** 2))
+    for v in range(X2.shape[1]):
+        out += channel_weighted_v1(x1, X2[:, v], W[v], L1, L2, Lout, spins, basis)
+    return out
+
+
+def depthwise_vjp(x1, x2, weights, g, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Reverse-mode derivative of depthwise for dL/dout = g (float64): by linearity in
+    each argument, gx1 = sum_v of the V = 1 gradient for (x2[:, v], W[v]), and gx2[:, v]
+    and gW[v] are the V = 1 gradients of that term.  Returns (gx1, gx2, gW) shaped like
+    x1, x2 and weights."""
+    spins = tuple(spins)
+    x1 = np.asarray(x1, dtype=np.float64)
+    x2 = np.asarray(x2, dtype=np.float64)
+    N, U = x1.shape[:2]
+    X2 = x2.reshape(N, -1, len(spins) * (L2 + 1) ** 2)
+    V = X2.shape[1]
+    W = np.asarray(weights, dtype=np.float64).reshape(V, U, -1)
+    gx1 = np.zeros(x1.shape)
+    gx2 = np.zeros(X2.shape)
+    gW = np.zeros(W.shape)
+    for v in range(V):
+        a, b, c = channel_weighted_v1_vjp(x1, X2[:, v], W[v], g, L1, L2, Lout, spins, basis)
+        gx1 += a
+        gx2[:, v] = b.reshape(N, -1)
+        gW[v] = c
+    return gx1, gx2.reshape(x2.shape), gW.reshape(np.asarray(weights).shape)

@@ -206,3 +206,40 @@ def test_channel_weighted_gradients_central_differences(L1, L2, LO, spins, basis
         d[n, c, k] = 1.0
         fd = (f(x1, x2 + d, W) - f(x1, x2 - d, W)) / 2.0
         assert abs(fd - gx2[n, c, k]) <= 1e-11 * max(1.0, abs(fd))
+
+
+# --- depthwise mode with V second-input channels (uvu, W[v, u, p]) ---
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", CW_CASES[:3])
+def test_depthwise_definition_and_gradients(L1, L2, LO, spins, basis):
+    N, U, V = 2, 3, 2
+    P = len(oracle.PathWeightedTensor(L1, L2, LO, spins, basis).paths)
+    rng = np.random.default_rng(61)
+    x1 = draw(spins, L1, N * U, 62).reshape(N, U, -1)
+    x2 = draw(spins, L2, N * V, 63).reshape(N, V, -1)
+    g = draw(spins, LO, N * U, 64).reshape(N, U, -1)
+    W = rng.standard_normal((V, U, P))
+    y = oracle.depthwise(x1, x2, W, L1, L2, LO, spins, basis).reshape(N, U, -1)
+    # the definition per unit: sum over v and paths with the path-weighted tensor of W[v, u]
+    for n in range(N):
+        for u in range(U):
+            ref = sum(oracle.PathWeightedTensor(L1, L2, LO, spins, basis, W[v, u]).apply(x1[n, u][None], x2[n, v][None])
+                      .reshape(-1) for v in range(V))
+            assert np.abs(y[n, u] - ref).max() <= 1e-12
+    gx1, gx2, gW = oracle.depthwise_vjp(x1, x2, W, g, L1, L2, LO, spins, basis)
+
+    def f(a, b, w):
+        return float((g * oracle.depthwise(a, b, w, L1, L2, LO, spins, basis).reshape(N, U, -1)).sum())
+
+    e = f(x1, x2, W)
+    for grad, val in ((gx1, x1), (gx2, x2), (gW, W)):
+        assert grad.shape == val.shape
+        assert abs(float((grad * val).sum()) - e) <= 1e-11 * max(1.0, abs(e))
+    for idx in ((1, 2, P - 1), (0, 0, 0)):
+        d = np.zeros_like(W)
+        d[idx] = 1.0
+        assert abs((f(x1, x2, W + d) - f(x1, x2, W - d)) / 2.0 - gW[idx]) <= 1e-11 * max(1.0, abs(gW[idx]))
+    valid2 = np.flatnonzero(valid_mask(spins, L2).ravel())
+    d = np.zeros_like(x2)
+    d[1, 1, valid2[-1]] = 1.0
+    assert abs((f(x1, x2 + d, W) - f(x1, x2 - d, W)) / 2.0 - gx2[1, 1, valid2[-1]]) <= 1e-11
