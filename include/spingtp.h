@@ -288,6 +288,41 @@ spingtp_status spingtp_backward_weighted(spingtp_plan plan, const void* x1, cons
 spingtp_status spingtp_backward_weighted_workspace_size(spingtp_plan plan, int64_t N, int64_t C, size_t* bytes);
 
 /*
+ * The depthwise product with V second-input channels per edge (App. E.1, mode uvu,
+ * one weight per path and channel pair):
+ *   out[n][u][k3] = sum_{v < V} sum over paths p of weights[v][u][p] sum_{k1,k2 on p}
+ *                   T[k1][k2][k3] x1[n][u][k1] x2[n][v][k2].
+ *   x1, out: [N][C][...] as spingtp_forward_v1 (u < C); x2: device [N][V][n_spins]
+ *   [(L2+1)^2] of the plan's dtype, 16-byte aligned; weights: device fp32 [V][C][n_paths]
+ *   (the slice of channel v is the weight layout of spingtp_forward_v1_weighted);
+ *   V >= 1.
+ * Runs the entry-list kernel of spingtp_forward_v1_weighted once per v, reading the
+ * x2 rows V n_spins (L2+1)^2 elements apart and adding into out after the first
+ * (bf16 outputs round at every add).  Needs a plan created with
+ * SPINGTP_CHANNEL_WEIGHTS whose entry lists hold the shape, else
+ * SPINGTP_ERR_UNSUPPORTED.  Asynchronous on `stream`, no allocation.
+ */
+spingtp_status spingtp_forward_depthwise(spingtp_plan plan, const void* x1, const void* x2, const float* weights,
+                                         void* out, int64_t N, int64_t C, int64_t V, void* stream);
+
+/*
+ * Gradients of spingtp_forward_depthwise: grad_x1 [N][C][...] (the sum over v),
+ * grad_x2 [N][V][...] and grad_weights [V][C][n_paths] (fp32), each channel v's part
+ * computed as by spingtp_backward_v1_weighted (deterministic).  The workspace
+ * (spingtp_backward_depthwise_workspace_size, that of spingtp_backward_v1_weighted
+ * for N, C) is reused by every v, so calls on one stream are ordered.  Rules as
+ * spingtp_backward_v1_weighted.
+ */
+spingtp_status spingtp_backward_depthwise(spingtp_plan plan, const void* x1, const void* x2, const float* weights,
+                                          const void* grad_out, void* grad_x1, void* grad_x2, float* grad_weights,
+                                          void* workspace, size_t workspace_bytes, int64_t N, int64_t C, int64_t V,
+                                          void* stream);
+
+/* Bytes of workspace spingtp_backward_depthwise needs (independent of V >= 1). */
+spingtp_status spingtp_backward_depthwise_workspace_size(spingtp_plan plan, int64_t N, int64_t C, int64_t V,
+                                                         size_t* bytes);
+
+/*
  * Gradients of a scalar loss through out = SpinGTP(x1, x2) of spingtp_forward:
  * given grad_out = dLoss/dout, writes
  *   grad_x1[n][c][k1] = sum_{k2,k3} T[k1][k2][k3] x2[n][c][k2] grad_out[n][c][k3],

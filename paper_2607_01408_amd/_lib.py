@@ -15,7 +15,8 @@ EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "s
             "spingtp_backward_v1_workspace_size", "spingtp_direct_table_host", "spingtp_paths_host",
             "spingtp_plan_create_weighted", "spingtp_forward_v1_weighted", "spingtp_backward_v1_weighted",
             "spingtp_backward_v1_weighted_workspace_size", "spingtp_forward_weighted", "spingtp_backward_weighted",
-            "spingtp_backward_weighted_workspace_size")
+            "spingtp_backward_weighted_workspace_size", "spingtp_forward_depthwise", "spingtp_backward_depthwise",
+            "spingtp_backward_depthwise_workspace_size")
 
 _lib = None
 
@@ -59,6 +60,14 @@ def lib() -> ctypes.CDLL:
         L.spingtp_backward_weighted.restype = ctypes.c_int
         L.spingtp_backward_weighted_workspace_size.argtypes = L.spingtp_backward_v1_weighted_workspace_size.argtypes
         L.spingtp_backward_weighted_workspace_size.restype = ctypes.c_int
+        L.spingtp_forward_depthwise.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int64] * 3 + [ctypes.c_void_p]
+        L.spingtp_forward_depthwise.restype = ctypes.c_int
+        L.spingtp_backward_depthwise.argtypes = [ctypes.c_void_p] * 9 + [ctypes.c_size_t] + [ctypes.c_int64] * 3 + [
+            ctypes.c_void_p]
+        L.spingtp_backward_depthwise.restype = ctypes.c_int
+        L.spingtp_backward_depthwise_workspace_size.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                                                ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]
+        L.spingtp_backward_depthwise_workspace_size.restype = ctypes.c_int
         L.spingtp_forward.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
         L.spingtp_forward.restype = ctypes.c_int

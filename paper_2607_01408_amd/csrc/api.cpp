@@ -163,3 +163,70 @@ extern "C" spingtp_status spingtp_backward_weighted(spingtp_plan plan, const voi
         static_cast<float*>(workspace), N, C, plan->bw1w, plan->d_bw1w, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
 }
+
+extern "C" spingtp_status spingtp_forward_depthwise(spingtp_plan plan, const void* x1, const void* x2,
+                                                    const float* weights, void* out, int64_t N, int64_t C, int64_t V,
+                                                    void* stream) {
+    if (plan == nullptr || N < 0 || C < 0 || V < 1) return SPINGTP_ERR_INVALID_ARG;
+    if (plan->d_bw1w == nullptr || plan->bw1w.lds_shared_fwd == 0) return SPINGTP_ERR_UNSUPPORTED;
+    if (N == 0 || C == 0) return SPINGTP_OK;
+    if (N > (int64_t{1} << 40) / C || V > (int64_t{1} << 20)) return SPINGTP_ERR_INVALID_ARG;
+    if (x1 == nullptr || x2 == nullptr || out == nullptr || weights == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    const auto misaligned = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; };
+    if (misaligned(x1, 16) || misaligned(x2, 16) || misaligned(out, 16) || misaligned(weights, 4))
+        return SPINGTP_ERR_INVALID_ARG;
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
+    if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
+    const int64_t n2 = plan->bw1w.nc2, elem = plan->dtype == SPINGTP_FP32 ? 4 : 2;
+    const int64_t wslice = C * plan->bw1w.np;
+    for (int64_t v = 0; v < V; ++v) {  // out = sum over the second-input channels, in order
+        const hipError_t e = spingtp::launch_fwd_cw(
+            plan->dtype == SPINGTP_FP32 ? 0 : 1, true, x1, static_cast<const char*>(x2) + v * n2 * elem,
+            weights + v * wslice, out, N, C, plan->bw1w, plan->d_bw1w, static_cast<hipStream_t>(stream), V * n2,
+            v > 0);
+        if (e != hipSuccess) return SPINGTP_ERR_HIP;
+    }
+    return SPINGTP_OK;
+}
+
+extern "C" spingtp_status spingtp_backward_depthwise_workspace_size(spingtp_plan plan, int64_t N, int64_t C,
+                                                                    int64_t V, size_t* bytes) {
+    if (V < 1) return SPINGTP_ERR_INVALID_ARG;
+    return spingtp_backward_v1_weighted_workspace_size(plan, N, C, bytes);  // reused by every channel v
+}
+
+extern "C" spingtp_status spingtp_backward_depthwise(spingtp_plan plan, const void* x1, const void* x2,
+                                                     const float* weights, const void* grad_out, void* grad_x1,
+                                                     void* grad_x2, float* grad_weights, void* workspace,
+                                                     size_t workspace_bytes, int64_t N, int64_t C, int64_t V,
+                                                     void* stream) {
+    size_t need = 0;
+    if (V < 1 || V > (int64_t{1} << 20)) return SPINGTP_ERR_INVALID_ARG;
+    const spingtp_status st = spingtp_backward_v1_weighted_workspace_size(plan, N, C, &need);
+    if (st != SPINGTP_OK) return st;
+    if (N == 0 && C == 0) return SPINGTP_OK;
+    const auto misaligned = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; };
+    if ((N > 0 && (x2 == nullptr || grad_x2 == nullptr)) ||
+        (N > 0 && C > 0 && (x1 == nullptr || grad_out == nullptr || grad_x1 == nullptr)) ||
+        (C > 0 && (weights == nullptr || grad_weights == nullptr)))
+        return SPINGTP_ERR_INVALID_ARG;
+    if (misaligned(x1, 16) || misaligned(x2, 16) || misaligned(grad_out, 16) || misaligned(grad_x1, 16) ||
+        misaligned(grad_x2, 16) || misaligned(weights, 4) || misaligned(grad_weights, 4) || misaligned(workspace, 4))
+        return SPINGTP_ERR_INVALID_ARG;
+    if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return SPINGTP_ERR_INVALID_ARG;
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
+    if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
+    const int64_t n2 = plan->bw1w.nc2, elem = plan->dtype == SPINGTP_FP32 ? 4 : 2;
+    const int64_t wslice = C * plan->bw1w.np;
+    for (int64_t v = 0; v < V; ++v) {  // grad_x1 sums the channels' terms in order; the rest is per channel
+        const hipError_t e = spingtp::launch_bwd_v1w(
+            plan->dtype == SPINGTP_FP32 ? 0 : 1, true, x1, static_cast<const char*>(x2) + v * n2 * elem,
+            weights + v * wslice, grad_out, grad_x1, static_cast<char*>(grad_x2) + v * n2 * elem,
+            grad_weights + v * wslice, static_cast<float*>(workspace), N, C, plan->bw1w, plan->d_bw1w,
+            static_cast<hipStream_t>(stream), V * n2, v > 0);
+        if (e != hipSuccess) return SPINGTP_ERR_HIP;
+    }
+    return SPINGTP_OK;
+}

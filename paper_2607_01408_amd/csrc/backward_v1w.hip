@@ -142,7 +142,7 @@ template <typename TIO, bool SHARED>
 __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
     const TIO* __restrict__ x1, const TIO* __restrict__ x2, const float* __restrict__ wts, const TIO* __restrict__ g,
     TIO* __restrict__ gx1, TIO* __restrict__ gx2, float* __restrict__ ws_x2, float* __restrict__ ws_w, int64_t N,
-    int64_t C, int64_t epg, const uint32_t* __restrict__ tab) {
+    int64_t C, int64_t epg, const uint32_t* __restrict__ tab, int64_t x2s, bool acc_gx1) {
     extern __shared__ float lds[];
     const int nc1 = static_cast<int>(tab[0]), nc2 = static_cast<int>(tab[1]), nco = static_cast<int>(tab[2]);
     const int np = static_cast<int>(tab[3]);
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
         bw_load_rows(x1 + row0 * nc1, nch, nc1, st1, X1, tid);
         bw_load_rows(g + row0 * nco, nch, nco, sto, G, tid);
         if constexpr (SHARED) {
-            for (int k = tid; k < nc2; k += kBw1wThreads) X2[k] = bw_load(x2 + n * nc2 + k);
+            for (int k = tid; k < nc2; k += kBw1wThreads) X2[k] = bw_load(x2 + n * x2s + k);
         } else {
             bw_load_rows(x2 + row0 * nc2, nch, nc2, st2, X2, tid);
         }
@@ -226,7 +226,8 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
         TIO* dst = gx1 + row0 * nc1;
         for (int e = tid; e < nch * nc1; e += kBw1wThreads) {
             const int r = e / nc1;
-            bw_store(dst + e, X1[r * st1 + (e - r * nc1)]);
+            const float v = X1[r * st1 + (e - r * nc1)];
+            bw_store(dst + e, acc_gx1 ? bw_load(dst + e) + v : v);
         }
         if constexpr (!SHARED) {
             TIO* dst2 = gx2 + row0 * nc2;
@@ -252,7 +253,7 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
 template <typename TIO, bool SHARED>
 __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
     const TIO* __restrict__ x1, const TIO* __restrict__ x2, const float* __restrict__ wts, TIO* __restrict__ out,
-    int64_t N, int64_t C, int64_t epg, const uint32_t* __restrict__ tab) {
+    int64_t N, int64_t C, int64_t epg, const uint32_t* __restrict__ tab, int64_t x2s, bool acc_out) {
     extern __shared__ float lds[];
     const int nc1 = static_cast<int>(tab[0]), nc2 = static_cast<int>(tab[1]), nco = static_cast<int>(tab[2]);
     const int np = static_cast<int>(tab[3]);
@@ -291,7 +292,7 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
         const int64_t row0 = n * C + c0;
         bw_load_rows(x1 + row0 * nc1, nch, nc1, st1, X1, tid);
         if constexpr (SHARED) {
-            for (int k = tid; k < nc2; k += kBw1wThreads) X2[k] = bw_load(x2 + n * nc2 + k);
+            for (int k = tid; k < nc2; k += kBw1wThreads) X2[k] = bw_load(x2 + n * x2s + k);
         } else {
             bw_load_rows(x2 + row0 * nc2, nch, nc2, st2, X2, tid);
         }
@@ -303,7 +304,8 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
         TIO* dst = out + row0 * nco;
         for (int e = tid; e < nch * nco; e += kBw1wThreads) {
             const int r = e / nco;
-            bw_store(dst + e, O[r * sto + (e - r * nco)]);
+            const float v = O[r * sto + (e - r * nco)];
+            bw_store(dst + e, acc_out ? bw_load(dst + e) + v : v);
         }
     }
 }
@@ -312,12 +314,13 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
 template <typename TIO>
 __global__ __launch_bounds__(256) void spingtp_bwd_v1w_reduce_x2_kernel(const float* __restrict__ ws_x2,
                                                                         TIO* __restrict__ gx2, int64_t nx2,
-                                                                        int64_t tiles) {
+                                                                        int64_t tiles, int nc2, int64_t gx2s) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     if (i >= nx2) return;
     float s = 0.f;
     for (int64_t t = 0; t < tiles; ++t) s += ws_x2[t * nx2 + i];
-    bw_store(gx2 + i, s);
+    const int64_t n = i / nc2;
+    bw_store(gx2 + n * gx2s + (i - n * nc2), s);  // rows gx2s elements apart
 }
 
 // gW[c,p] = sum over the edge ranges: one workgroup per (path, 64 channels); wave w
@@ -363,7 +366,7 @@ hipError_t raise_lds_limit(const void* kernel) {
 template <typename TIO, bool SHARED>
 hipError_t launch_typed(const void* x1, const void* x2, const float* w, const void* g, void* gx1, void* gx2,
                         float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab,
-                        hipStream_t stream) {
+                        hipStream_t stream, int64_t x2s, bool acc_gx1) {
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     int64_t groups = 0, epg = 0;
     bw1w_groups(N, C, &groups, &epg);
@@ -382,7 +385,7 @@ hipError_t launch_typed(const void* x1, const void* x2, const float* w, const vo
                            dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)), dim3(kBw1wThreads), bytes,
                            stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w,
                            static_cast<const TIO*>(g), static_cast<TIO*>(gx1), static_cast<TIO*>(gx2), ws_x2, ws_w, N,
-                           C, epg, tab);
+                           C, epg, tab, x2s, acc_gx1);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -391,7 +394,7 @@ hipError_t launch_typed(const void* x1, const void* x2, const float* w, const vo
         const int64_t blocks = (nx2 + 255) / 256;
         if (blocks > 0x7fffffff) return hipErrorInvalidValue;
         hipLaunchKernelGGL(spingtp_bwd_v1w_reduce_x2_kernel<TIO>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
-                           stream, ws_x2, static_cast<TIO*>(gx2), nx2, groups > 0 ? tiles : 0);
+                           stream, ws_x2, static_cast<TIO*>(gx2), nx2, groups > 0 ? tiles : 0, s.nc2, x2s);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -436,25 +439,31 @@ size_t bwcw_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s) {
 
 hipError_t launch_bwd_v1w(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, const void* g,
                           void* gx1, void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
-                          const uint32_t* tab, hipStream_t stream) {
+                          const uint32_t* tab, hipStream_t stream, int64_t x2_stride, bool accumulate_gx1) {
+    const int64_t x2s = x2_stride > 0 ? x2_stride : s.nc2;
     // the kernel carves its LDS from the table's sizes
     const int base = kBw1wLanes * (2 * bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nco));
     if (shared_x2) {
         if (s.lds_floats <= 0 || s.lds_floats > kBw1wMaxLdsFloats || s.lds_floats != base + bw_stride(s.nc2))
             return hipErrorInvalidValue;
-        return dtype == 0 ? launch_typed<float, true>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream)
-                          : launch_typed<uint16_t, true>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream);
+        return dtype == 0
+                   ? launch_typed<float, true>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream, x2s, accumulate_gx1)
+                   : launch_typed<uint16_t, true>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream, x2s,
+                                                  accumulate_gx1);
     }
     if (s.lds_unit_bwd <= 0 || s.lds_unit_bwd > kBw1wMaxLdsFloats ||
         s.lds_unit_bwd != base + 2 * kBw1wLanes * bw_stride(s.nc2))
         return hipErrorInvalidValue;
-    return dtype == 0 ? launch_typed<float, false>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream)
-                      : launch_typed<uint16_t, false>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream);
+    return dtype == 0
+               ? launch_typed<float, false>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream, x2s, accumulate_gx1)
+               : launch_typed<uint16_t, false>(x1, x2, w, g, gx1, gx2, gw, ws, N, C, s, tab, stream, x2s,
+                                               accumulate_gx1);
 }
 
 template <typename TIO, bool SHARED>
 static hipError_t launch_fwd_typed(const void* x1, const void* x2, const float* w, void* out, int64_t N, int64_t C,
-                                   int lds_floats, const uint32_t* tab, hipStream_t stream) {
+                                   int lds_floats, const uint32_t* tab, hipStream_t stream, int64_t x2s,
+                                   bool acc_out) {
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     int64_t groups = 0, epg = 0;
     bw1w_groups(N, C, &groups, &epg);
@@ -469,12 +478,14 @@ static hipError_t launch_fwd_typed(const void* x1, const void* x2, const float* 
     hipLaunchKernelGGL((spingtp_fwd_cw_kernel<TIO, SHARED>),
                        dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)), dim3(kBw1wThreads), bytes,
                        stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w, static_cast<TIO*>(out), N,
-                       C, epg, tab);
+                       C, epg, tab, x2s, acc_out);
     return hipGetLastError();
 }
 
 hipError_t launch_fwd_cw(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, void* out,
-                         int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab, hipStream_t stream) {
+                         int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab, hipStream_t stream,
+                         int64_t x2_stride, bool accumulate) {
+    const int64_t x2s = x2_stride > 0 ? x2_stride : s.nc2;
     // the kernel carves its LDS from the table's sizes
     const int base = kBw1wLanes * (bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nco));
     const int lds = shared_x2 ? s.lds_shared_fwd : s.lds_unit_fwd;
@@ -482,10 +493,10 @@ hipError_t launch_fwd_cw(int dtype, bool shared_x2, const void* x1, const void* 
         lds != base + (shared_x2 ? bw_stride(s.nc2) : kBw1wLanes * bw_stride(s.nc2)))
         return hipErrorInvalidValue;
     if (shared_x2)
-        return dtype == 0 ? launch_fwd_typed<float, true>(x1, x2, w, out, N, C, lds, tab, stream)
-                          : launch_fwd_typed<uint16_t, true>(x1, x2, w, out, N, C, lds, tab, stream);
-    return dtype == 0 ? launch_fwd_typed<float, false>(x1, x2, w, out, N, C, lds, tab, stream)
-                      : launch_fwd_typed<uint16_t, false>(x1, x2, w, out, N, C, lds, tab, stream);
+        return dtype == 0 ? launch_fwd_typed<float, true>(x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate)
+                          : launch_fwd_typed<uint16_t, true>(x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate);
+    return dtype == 0 ? launch_fwd_typed<float, false>(x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate)
+                      : launch_fwd_typed<uint16_t, false>(x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate);
 }
 
 }  // namespace spingtp

@@ -173,13 +173,19 @@ size_t bwcw_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s);
 // dtype 0: fp32 x1, x2, grad_out, gx1, gx2; 1: bf16.  Weights and gW are fp32.
 // shared_x2: x2 [N][NC2] shared by the channels (spingtp_backward_v1_weighted), else
 // x2 [N][C][NC2] per unit (spingtp_backward_weighted).
+// x2_stride (shared x2): elements between the x2 (and gx2) rows of consecutive edges,
+// 0 for NC2; accumulate_gx1: add gx1 to what grad_x1 holds (the depthwise mode's sum
+// over its second-input channels).
 hipError_t launch_bwd_v1w(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, const void* g,
                           void* gx1, void* gx2, float* gw, float* ws, int64_t N, int64_t C, const Bw1wShape& s,
-                          const uint32_t* tab, hipStream_t stream);
+                          const uint32_t* tab, hipStream_t stream, int64_t x2_stride = 0,
+                          bool accumulate_gx1 = false);
 // out[n][c] = sum_p W[c][p] T_p(x1[n][c], x2[n][c]) (spingtp_forward_weighted), or with
 // x2[n] shared by the channels (shared_x2, spingtp_forward_v1_weighted).
+// x2_stride, accumulate: as for launch_bwd_v1w (accumulate adds to out).
 hipError_t launch_fwd_cw(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, void* out,
-                         int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab, hipStream_t stream);
+                         int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab, hipStream_t stream,
+                         int64_t x2_stride = 0, bool accumulate = false);
 
 // Paths of the instruction-weighted product (spingtp_paths_host): the block triples
 // (i (L+1) + l of spin index i and degree l, per input and output) on which T has

@@ -381,6 +381,64 @@ class Plan:
             ws.data_ptr(), n.value, N, C, ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_weighted")
         return gx1, gx2, gw
 
+    def _check_depthwise(self, x1, x2, weights, grad_out=None):
+        import torch
+
+        N, C, V = x1.shape[0], x1.shape[1], x2.shape[1]
+        shapes = [(x1, (N, C) + tuple(self.shape_in(1))), (x2, (N, V) + tuple(self.shape_in(2)))]
+        if grad_out is not None:
+            shapes.append((grad_out, (N, C) + tuple(self.shape_out)))
+        for t, shape in shapes:
+            if (tuple(t.shape) != shape or t.dtype != self.torch_dtype or not t.is_cuda
+                    or not t.is_contiguous()):
+                raise ValueError("x1 [N, C, ...], x2 [N, V, ...] (and grad_out [N, C, ...]) must be contiguous "
+                                 "device tensors of the plan's dtype")
+        if (weights.dtype != torch.float32 or not weights.is_contiguous()
+                or tuple(weights.shape) != (V, C, self.n_paths) or weights.device != x1.device):
+            raise ValueError(f"weights must be a contiguous fp32 [V, C, {self.n_paths}] tensor on the inputs' "
+                             "device (a plan created with channel_weights=True)")
+        return N, C, V
+
+    def forward_depthwise(self, x1, x2, weights, out=None, stream=None):
+        """spingtp_forward_depthwise: x2 [N, V, ...] with V >= 1 channels per edge, weights [V, C, n_paths]."""
+        import torch
+
+        N, C, V = self._check_depthwise(x1, x2, weights)
+        if out is None:
+            out = torch.empty((N, C) + self.shape_out, dtype=self.torch_dtype, device=x1.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+
+        def ptr(t):
+            return t.data_ptr() if t.numel() else None
+
+        _lib.check(_lib.lib().spingtp_forward_depthwise(self._handle, ptr(x1), ptr(x2), ptr(weights), ptr(out), N, C,
+                                                        V, ctypes.c_void_p(stream.cuda_stream)),
+                   "spingtp_forward_depthwise")
+        return out
+
+    def backward_depthwise(self, x1, x2, weights, grad_out, stream=None):
+        """spingtp_backward_depthwise: (grad_x1 [N, C, ...], grad_x2 [N, V, ...], grad_weights [V, C, n_paths])."""
+        import torch
+
+        N, C, V = self._check_depthwise(x1, x2, weights, grad_out)
+        gx1, gx2 = torch.empty_like(x1), torch.empty_like(x2)
+        gw = torch.empty_like(weights)
+        n = ctypes.c_size_t(0)
+        _lib.check(_lib.lib().spingtp_backward_depthwise_workspace_size(self._handle, N, C, V, ctypes.byref(n)),
+                   "spingtp_backward_depthwise_workspace_size")
+        ws = torch.empty(max(1, n.value), dtype=torch.uint8, device=x1.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+
+        def ptr(t):
+            return t.data_ptr() if t.numel() else None
+
+        _lib.check(_lib.lib().spingtp_backward_depthwise(
+            self._handle, ptr(x1), ptr(x2), ptr(weights), ptr(grad_out), ptr(gx1), ptr(gx2), ptr(gw),
+            ws.data_ptr(), n.value, N, C, V, ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_depthwise")
+        return gx1, gx2, gw
+
     __call__ = forward
 
     def close(self):

@@ -424,3 +424,57 @@ def test_channel_weighted_v1_routes_agree(shape, basis):
     y1 = Plan(*shape, S3, "fp32", basis, channel_weights=True, v1_precontract=True).forward_v1_weighted(x1, x2, W)
     torch.cuda.synchronize()
     assert rel_l2(host(y0, N * C), host(y1, N * C)) <= 1e-6
+
+
+# --- depthwise mode with V second-input channels (spingtp_forward_depthwise, uvu) ---
+
+def run_depthwise(L1, L2, LO, spins, N, C, V, basis=0, dtype="fp32", seed=0):
+    P = paths_host(L1, L2, LO, spins, basis)
+    print(f"[depthwise] L=({L1},{L2},{LO}) spins={spins} basis={basis} N={N} C={C} V={V} {dtype}", flush=True)
+    rng = np.random.default_rng(300 + seed)
+    W = torch.as_tensor(rng.standard_normal((V, C, len(P))), dtype=torch.float32, device="cuda")
+    x1 = workloads.draw(L1, N, C, 73 + seed, dtype, spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, V, 74 + seed, dtype, spins, "unit", "cuda")
+    g = workloads.draw(LO, N, C, 75 + seed, dtype, spins, "unit", "cuda")
+    plan = Plan(L1, L2, LO, spins, dtype, basis, channel_weights=True)
+    y = plan.forward_depthwise(x1, x2, W)
+    gx1, gx2, gW = plan.backward_depthwise(x1, x2, W, g)
+    torch.cuda.synchronize()
+    a, c = host(x1, N * C).reshape(N, C, -1), host(g, N * C).reshape(N, C, -1)
+    b = host(x2, N * V).reshape(N, V, -1)
+    Wd = W.double().cpu().numpy()
+    ref = oracle.depthwise(a, b, Wd, L1, L2, LO, spins, basis).reshape(N * C, -1)
+    r1, r2, rW = oracle.depthwise_vjp(a, b, Wd, c, L1, L2, LO, spins, basis)
+    errs = (rel_l2(host(y, N * C), ref), rel_l2(host(gx1, N * C), r1.reshape(N * C, -1)),
+            rel_l2(host(gx2, N * V), r2.reshape(N * V, -1)), rel_l2(gW.double().cpu().numpy(), rW))
+    print(f"[depthwise]   rel_l2 y={errs[0]:.3e} gx1={errs[1]:.3e} gx2={errs[2]:.3e} gW={errs[3]:.3e}", flush=True)
+    assert max(errs) <= TOL[dtype], errs
+    return plan, (x1, x2, W, g), (y, gx1, gx2, gW)
+
+
+@pytest.mark.parametrize("shape,C,V,basis", [((1, 1, 1), 16, 3, 0), ((2, 2, 2), 70, 2, 2), ((1, 3, 3), 33, 4, 0),
+                                             ((2, 1, 2), 64, 2, 1)])
+def test_depthwise_shapes(shape, C, V, basis):
+    run_depthwise(*shape, S3, 11, C, V, basis, seed=C + V)
+
+
+def test_depthwise_bf16():
+    run_depthwise(2, 2, 2, S3, 9, 48, 2, 2, "bf16", seed=4)
+
+
+def test_depthwise_one_channel_is_the_v1_form():
+    plan, (x1, x2, W, g), (y, gx1, gx2, gW) = run_depthwise(2, 2, 2, S3, 13, 40, 1, 0, seed=2)
+    y1 = plan.forward_v1_weighted(x1, x2, W[0].contiguous())
+    hx1, hx2, hW = plan.backward_v1_weighted(x1, x2, W[0].contiguous(), g)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y1) and torch.equal(gx1, hx1) and torch.equal(gx2, hx2) and torch.equal(gW[0], hW)
+
+
+def test_depthwise_rules():
+    plan = Plan(2, 2, 2, S3, "fp32", channel_weights=True)
+    n = plan.n_paths
+    x1 = torch.zeros((2, 3, 3, 9), device="cuda")
+    with pytest.raises(SpinGTPError):  # V = 0: no second-input channel
+        plan.forward_depthwise(x1, torch.zeros((2, 0, 3, 9), device="cuda"), torch.zeros((0, 3, n), device="cuda"))
+    with pytest.raises(ValueError):  # one weight slice per second-input channel
+        plan.forward_depthwise(x1, torch.zeros((2, 2, 3, 9), device="cuda"), torch.zeros((1, 3, n), device="cuda"))
