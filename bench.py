@@ -358,6 +358,48 @@ def run_v1(args):
         res["parity_rel_l2_gx2_sampled"] = float(np.linalg.norm(got2 - r2) / np.linalg.norm(r2))
         return res
 
+    def measure_depthwise(L1, L2, LO, C, B, V, seed):
+        """spingtp_forward_depthwise and spingtp_backward_depthwise with V second-input channels
+        (parity basis), preallocated buffers; sampled parity of the forward against the oracle."""
+        import oracle
+        from paper_2607_01408_amd import paths_host
+
+        plan = Plan(L1, L2, LO, workloads.SPINS, "fp32", 2, channel_weights=True)
+        n_paths = len(paths_host(L1, L2, LO, workloads.SPINS, 2))
+        x1 = workloads.draw(L1, B, C, 9620 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        x2 = workloads.draw(L2, B, V, 9720 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        g = workloads.draw(LO, B, C, 9820 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
+        w = torch.randn((V, C, n_paths), generator=torch.Generator().manual_seed(seed)).to("cuda:0")
+        out, gx1, gx2, gw = torch.empty_like(g), torch.empty_like(x1), torch.empty_like(x2), torch.empty_like(w)
+        n = ctypes.c_size_t(0)
+        assert _lib.lib().spingtp_backward_depthwise_workspace_size(plan.handle, B, C, V, ctypes.byref(n)) == 0
+        ws = torch.empty(max(1, n.value), dtype=torch.uint8, device="cuda:0")
+        st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        calls = {"forward": (_lib.lib().spingtp_forward_depthwise,
+                             (plan.handle, x1.data_ptr(), x2.data_ptr(), w.data_ptr(), out.data_ptr(), B, C, V, st)),
+                 "backward": (_lib.lib().spingtp_backward_depthwise,
+                              (plan.handle, x1.data_ptr(), x2.data_ptr(), w.data_ptr(), g.data_ptr(), gx1.data_ptr(),
+                               gx2.data_ptr(), gw.data_ptr(), ws.data_ptr(), n.value, B, C, V, st))}
+        res = {"V": V, "paths": n_paths, "basis": 2}
+        for name, (fn_, call) in calls.items():
+            for _ in range(args.warmup):
+                assert fn_(*call) == 0
+            torch.cuda.synchronize()
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            for _ in range(args.steps):
+                fn_(*call)
+            e.record()
+            torch.cuda.synchronize()
+            res[name + "_ms"] = s.elapsed_time(e) / args.steps
+        sel = torch.as_tensor(sorted({0, B - 1}), device="cuda:0")
+        a = x1[sel].double().cpu().numpy().reshape(len(sel), C, -1)
+        b = x2[sel].double().cpu().numpy().reshape(len(sel), V, -1)
+        ref = oracle.depthwise(a, b, w.double().cpu().numpy(), L1, L2, LO, workloads.SPINS, 2).reshape(len(sel), -1)
+        got = out[sel].double().cpu().numpy().reshape(len(sel), -1)
+        res["parity_rel_l2_sampled"] = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+        return res
+
     def measure_backward(L, C, B, seed):
         """spingtp_backward_v1 (both gradients) on the default route, preallocated buffers."""
         x1 = workloads.draw(L, B, C, 9300 + seed, "fp32", workloads.SPINS, "unit", "cuda:0")
@@ -394,6 +436,11 @@ def run_v1(args):
             row[name + "_backward"] = measure_weighted_backward(L1, L2, LO, C, B, basis, L1 + 3 * L2 + C)
         for name, basis in (("channel_weighted_unit_parity_basis", 2), ("channel_weighted_unit_paper_basis", 0)):
             row[name] = measure_weighted_unit(L1, L2, LO, C, B, basis, L1 + 3 * L2 + C)
+        if B == 1024:  # the depthwise mode with four second-input channels on the largest rows
+            row["depthwise_v4_parity_basis"] = measure_depthwise(L1, L2, LO, C, B, 4, L1 + 3 * L2 + C)
+            print(f"[v1] ({L1},{L2},{LO}) C={C} B={B}: depthwise V=4 (parity basis) forward "
+                  f"{row['depthwise_v4_parity_basis']['forward_ms'] * 1e3:.1f} us, gradients "
+                  f"{row['depthwise_v4_parity_basis']['backward_ms'] * 1e3:.1f} us", file=sys.stderr, flush=True)
         table.append(row)
         print(f"[v1] ({L1},{L2},{LO}) C={C} B={B}: pre {row['precontracted']['ms'] * 1e3:.1f} us, "
               f"fourier {row['fourier']['ms'] * 1e3:.1f} us, weighted (parity / paper basis) "
