@@ -34,7 +34,8 @@ def kernel_sources(kname):
     """The source files a forward kernel is compiled from (its counters go stale when they change)."""
     main = {"spingtp_fwd_mfma_kernel": "forward_mfma.hip",
             "spingtp_fwd_direct_kernel": "forward_direct.hip"}.get(kname, "forward.hip")
-    return tuple(_CSRC + f for f in (main, "device_common.h", "layout.h"))
+    extra = ("forward_pair.h",) if main == "forward.hip" else ()
+    return tuple(_CSRC + f for f in (main, "device_common.h", "layout.h") + extra)
 
 
 def route_flops(L1, L2, LO, spin=True):

@@ -9,7 +9,11 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libspingtp.so")
-SOURCES = ["plan.cpp", "api.cpp", "forward.hip", "forward_mfma.hip", "forward_pre.hip", "forward_pre_large.hip", "forward_pre_weighted.hip", "forward_direct.hip", "backward.hip", "backward_v1w.hip"]
+SOURCES = ["plan.cpp", "api.cpp", "forward.hip", "forward_big_parity.hip", "forward_mfma.hip", "forward_pre.hip",
+           "forward_pre_large.hip", "forward_pre_weighted.hip", "forward_direct.hip", "backward.hip", "backward_v1w.hip"]
+# per-source additions: the parity-basis large-degree kernels schedule for fewer registers
+# (they spill less and run 22-35 % faster that way; the other kernels run slower with it)
+EXTRA_FLAGS = {"forward_big_parity.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-minreg"]}
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in generated code.
 HIP_FLAGS = [
@@ -34,8 +38,8 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     for src in SOURCES:
         obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
-        cmd = [hipcc()] + HIP_FLAGS + ["-I", os.path.join(ROOT, "include"), "-c",
-                                        os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc()] + HIP_FLAGS + EXTRA_FLAGS.get(src, []) + ["-I", os.path.join(ROOT, "include"), "-c",
+                                                                  os.path.join(CSRC, src), "-o", obj]
         if src.endswith(".cpp"):
             cmd.insert(1, "-x")
             cmd.insert(2, "hip")

@@ -34,33 +34,12 @@
 #include <cstdint>
 
 #include "device_common.h"
+#include "forward_pair.h"
 #include "internal.h"
 
 namespace spingtp {
 namespace {
 
-template <int L>
-__device__ __forceinline__ void synth(const float (&pc)[L + 1], const float (&ps)[L + 1], const float* __restrict__ cs,
-                                      const float* __restrict__ sn, float& plus, float& minus) {
-    float ev = pc[0], od = 0.f;
-#pragma unroll
-    for (int t = 1; t <= L; ++t) {
-        ev = fmaf(pc[t], cs[t], ev);
-        od = fmaf(ps[t], sn[t], od);
-    }
-    plus = ev + od;
-    minus = ev - od;
-}
-
-// Per-node spectra exchanged between the theta-node waves before the final
-// projection (step E).  Slot order inside one unit's record:
-//   t = 0 : R0c[0], and with spins Z+ and Z- (the m3 = 0, |s3| = 1 sums);
-//   t >= 1: R0c[t], R0s[t], and with spins the four combinations
-//           P1c+P2s (s3=+1, m3=+t), P1c-P2s (s3=-1, m3=+t),
-//           P2c-P1s (s3=+1, m3=-t), -P2c-P1s (s3=-1, m3=-t).
-// A "group" is one slot: it feeds the output coefficients l = lmin..Lout of one
-// (spin block, m3).  Each group is owned by exactly one wave, which sums the
-// slot over all theta nodes in a fixed order, so the result is deterministic.
 template <int LO, bool SPIN>
 struct Spectra {
     static constexpr int PER_T = SPIN ? 6 : 2;
@@ -75,10 +54,6 @@ struct Spectra {
     __host__ __device__ static constexpr int size(int g) { return LO + 1 - lmin(g); }
 };
 
-template <int NG>
-struct Owners {
-    int owner[NG];
-};
 
 // Longest-processing-time assignment of the groups to NW waves.
 template <int LO, bool SPIN, int NW>
@@ -344,208 +319,6 @@ __global__ __launch_bounds__((Shape<L1, L2, LO, SPIN>::THREADS)) void spingtp_fw
     store_tile<S::NCO, S::STO>(out + u0 * S::NCO, nvalid, YT, tid, S::THREADS);
 }
 
-// ---------------------------------------------------------------------------
-// Lane-pair kernel for L1 = L2 = Lout = L with larger L (7, 8).
-//
-// Lanes 2u and 2u+1 share unit u: lane 2u keeps the three polynomials of input
-// 1, lane 2u+1 those of input 2 (halving the per-lane state), and each
-// synthesised value is handed to the partner lane with one DPP swap.  The
-// products are symmetric in the two inputs, so both lanes form them with the
-// same code.  The analysis is split by trigonometric type: the even lane
-// accumulates the cosine spectra of R0, P1, P2 and the odd lane the sine
-// spectra, reading its own row of a cos/sin table in LDS; every other table
-// value is still wave-uniform.  Step (E) pairs the output coefficient
-// m3 = +t (even lane) with m3 = -t (odd lane), which use the same table entry
-// (for R0 the sine table is the negated cosine table, folded into the sign of
-// the exchanged value).
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ float swap_pair(float v) {
-    // quad_perm [1,0,3,2]: exchange with the neighbouring lane
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
-}
-
-template <int L, bool SPIN>
-struct PairShape {
-    static constexpr Layout Y = make_layout(L, L, L);
-    static constexpr int NS = SPIN ? 3 : 1;
-    static constexpr int NC = NS * (L + 1) * (L + 1);
-    static constexpr int ST = NC | 1;
-    static constexpr int NT = Y.NT;
-    static constexpr int NP = Y.NP;
-    static constexpr int KP = (NP - 1) / 2;
-    static constexpr int UNITS = 32;
-    static constexpr int WAVES = NT;
-    static constexpr int THREADS = 64 * WAVES;
-    // exchanged slots per unit: t = 0: (R0, unused, Z+, Z-) | t >= 1: (R0 +/-, P +/-, M +/-)
-    static constexpr int T0 = SPIN ? 4 : 2;
-    static constexpr int PER_T = SPIN ? 6 : 2;
-    static constexpr int ND = T0 + PER_T * L;
-    static constexpr int DS = ND | 1;
-    static constexpr int XF = UNITS * 2 * ST;
-    static constexpr int DF = NT * UNITS * DS;
-    static constexpr int REGION = XF > DF ? XF : DF;
-    static constexpr int TRIG = 2 * NP * (L + 1);
-    static constexpr int LDS_FLOATS = REGION + UNITS * ST + TRIG;
-    // pair groups: t = 0 -> R0 (l >= 0), Z (l >= 1, spins); t >= 1 -> R0, P, M (spins) or R0
-    static constexpr int G0 = SPIN ? 2 : 1;
-    static constexpr int GT = SPIN ? 3 : 1;
-    static constexpr int NG = G0 + GT * L;
-    __host__ __device__ static constexpr int t_of(int g) { return g < G0 ? 0 : 1 + (g - G0) / GT; }
-    __host__ __device__ static constexpr int kind_of(int g) { return g < G0 ? (g == 0 ? 0 : 3) : (g - G0) % GT; }
-    __host__ __device__ static constexpr int lmin(int g) { return kind_of(g) == 3 ? 1 : t_of(g); }
-    __host__ __device__ static constexpr int size(int g) { return L + 1 - lmin(g); }
-    __host__ __device__ static constexpr int slot(int g) {
-        return t_of(g) == 0 ? (kind_of(g) == 0 ? 0 : 2) : T0 + PER_T * (t_of(g) - 1) + 2 * kind_of(g);
-    }
-};
-
-template <int L, bool SPIN, int NW>
-constexpr Owners<PairShape<L, SPIN>::NG> assign_pair_owners() {
-    using P = PairShape<L, SPIN>;
-    Owners<P::NG> o{};
-    int load[NW] = {};
-    bool done[P::NG] = {};
-    for (int n = 0; n < P::NG; ++n) {
-        int best = -1;
-        for (int g = 0; g < P::NG; ++g)
-            if (!done[g] && (best < 0 || P::size(g) > P::size(best))) best = g;
-        int w = 0;
-        for (int k = 1; k < NW; ++k)
-            if (load[k] < load[w]) w = k;
-        o.owner[best] = w;
-        load[w] += P::size(best);
-        done[best] = true;
-    }
-    return o;
-}
-
-// Steps (A)-(D) of one unit at one node for the lane pair (see above).  On
-// return Q0/Q1/Q2 hold the exchanged slot values of this lane:
-//   Q0[t]: R0c[t] (even lane) or -R0s[t] (odd lane), t >= 1; Q0[0] = R0c[0]
-//   Q1[t]: P1c+P2s (even) or P2c-P1s (odd);  Q2[t]: P1c-P2s (even) or -P2c-P1s (odd)
-//   zslot: Z+ (even lane) or Z- (odd lane), the m3 = 0, |s3| = 1 sums.
-template <int L, bool SPIN, bool BWD, bool PAR = false>
-__device__ __forceinline__ void pair_spectra(const float* xr, const float* __restrict__ tb,
-                                             const float* __restrict__ g, const float* trl, int sub,
-                                             float (&Q0)[L + 1], float (&Q1)[L + 1], float (&Q2)[L + 1],
-                                             float& zslot) {
-    constexpr Layout Y = make_layout(L, L, L);
-    constexpr int TM1 = Y.TM + 1;
-    constexpr int NP = Y.NP;
-    constexpr int KP = (NP - 1) / 2;
-    float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
-    coef_to_theta_fourier<L, L, SPIN, PAR>(xr, tb, g + Y.n0, BWD && sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
-    const float sg = sub ? -1.f : 1.f;
-
-    // accumulators: cosine spectra on the even lane, sine spectra on the odd lane
-#pragma unroll
-    for (int t = 0; t <= L; ++t) Q0[t] = Q1[t] = Q2[t] = 0.f;
-
-    auto accumulate = [&](float vr, float v1, float v2, const float* tr) {
-#pragma unroll
-        for (int t = 0; t <= L; ++t) {
-            const float w = tr[t];
-            Q0[t] = fmaf(vr, w, Q0[t]);
-            if constexpr (SPIN) {
-                Q1[t] = fmaf(v1, w, Q1[t]);
-                Q2[t] = fmaf(v2, w, Q2[t]);
-            }
-        }
-    };
-    // phi = 0 (and phi = pi when n_phi is even): a single point
-    auto single_point = [&](int k, float sgn_t_odd) {
-        float o0 = 0.f, o1 = 0.f, o2 = 0.f;
-#pragma unroll
-        for (int t = 0; t <= L; ++t) {
-            const float c = (t & 1) ? sgn_t_odd : 1.f;
-            o0 = fmaf(c, Pc0[t], o0);
-            if constexpr (SPIN) o1 = fmaf(c, Pc1[t], o1), o2 = fmaf(c, Pc2[t], o2);
-        }
-        const float p0 = swap_pair(o0);
-        float r0 = o0 * p0, q1 = 0.f, q2 = 0.f;
-        if constexpr (SPIN) {
-            const float p1 = swap_pair(o1), p2 = swap_pair(o2);
-            r0 = fmaf(o1, p1, fmaf(o2, p2, r0));
-            q1 = fmaf(o0, p1, p0 * o1);
-            q2 = fmaf(o0, p2, p0 * o2);
-        }
-        accumulate(r0, q1, q2, trl + k * (L + 1));
-    };
-    single_point(0, 1.f);
-#pragma unroll 1
-    for (int k = 1; k <= KP; ++k) {
-        const float* __restrict__ cs = g + Y.cosT + k * TM1;
-        const float* __restrict__ sn = g + Y.sinT + k * TM1;
-        float o0p, o0m, o1p = 0.f, o1m = 0.f, o2p = 0.f, o2m = 0.f;
-        synth<L>(Pc0, Ps0, cs, sn, o0p, o0m);
-        if constexpr (SPIN) {
-            synth<L>(Pc1, Ps1, cs, sn, o1p, o1m);
-            synth<L>(Pc2, Ps2, cs, sn, o2p, o2m);
-        }
-        const float p0p = swap_pair(o0p), p0m = swap_pair(o0m);
-        float r0p = o0p * p0p, r0m = o0m * p0m, q1p = 0.f, q1m = 0.f, q2p = 0.f, q2m = 0.f;
-        if constexpr (SPIN) {
-            const float p1p = swap_pair(o1p), p1m = swap_pair(o1m);
-            const float p2p = swap_pair(o2p), p2m = swap_pair(o2m);
-            r0p = fmaf(o1p, p1p, fmaf(o2p, p2p, r0p));
-            r0m = fmaf(o1m, p1m, fmaf(o2m, p2m, r0m));
-            q1p = fmaf(o0p, p1p, p0p * o1p);
-            q1m = fmaf(o0m, p1m, p0m * o1m);
-            q2p = fmaf(o0p, p2p, p0p * o2p);
-            q2m = fmaf(o0m, p2m, p0m * o2m);
-        }
-        // even lane: sums (cosine), odd lane: differences (sine)
-        accumulate(fmaf(sg, r0m, r0p), fmaf(sg, q1m, q1p), fmaf(sg, q2m, q2p), trl + k * (L + 1));
-    }
-    if constexpr (NP % 2 == 0) single_point(NP / 2, -1.f);
-
-    // t = 0 terms (valid on the even lane, which holds input 1 and every cosine spectrum)
-    zslot = 0.f;
-    if constexpr (SPIN) {
-        const float a0p = swap_pair(Pc0[0]);
-        const float dlp = swap_pair(dl), epp = swap_pair(ep);
-        Q0[0] = fmaf(-0.5f * NP, fmaf(dl, dlp, ep * epp), Q0[0]);
-        const float sP1 = 1.41421356237309505f * Q1[0];
-        const float sP2 = 1.41421356237309505f * Q2[0];
-        const float sP4 = -static_cast<float>(NP) * fmaf(dlp, Pc0[0], dl * a0p);
-        const float sP3 = static_cast<float>(NP) * fmaf(epp, Pc0[0], ep * a0p);
-        const float v0 = 0.5f * (sP1 + sP4), v1 = 0.5f * (sP3 + sP2);
-        const float v2 = 0.5f * (sP1 - sP4), v3 = 0.5f * (sP3 - sP2);
-        const float* m0 = g + Y.m0;
-        const float zp = fmaf(m0[0], v0, fmaf(m0[1], v1, fmaf(m0[2], v2, m0[3] * v3)));
-        const float zm = fmaf(m0[4], v0, fmaf(m0[5], v1, fmaf(m0[6], v2, m0[7] * v3)));
-        const float zm_even = swap_pair(zm);  // all lanes active: DPP reads the even lane
-        zslot = sub ? zm_even : zp;
-        // cross terms: the even lane needs P2s, the odd lane P2c
-#pragma unroll
-        for (int t = 1; t <= L; ++t) {
-            const float b = swap_pair(Q2[t]);
-            const float p1 = Q1[t];
-            Q1[t] = fmaf(sg, p1, b);
-            Q2[t] = fmaf(sg, p1, -b);
-        }
-    }
-#pragma unroll
-    for (int t = 1; t <= L; ++t) Q0[t] *= sg;
-}
-
-// Writes one unit's slot record (layout of PairShape) for this lane.
-template <int L, bool SPIN>
-__device__ __forceinline__ void pair_publish(float* D, int sub, const float (&Q0)[L + 1], const float (&Q1)[L + 1],
-                                             const float (&Q2)[L + 1], float zslot) {
-    constexpr int T0 = SPIN ? 4 : 2, PER_T = SPIN ? 6 : 2;
-    D[sub] = Q0[0];
-    if constexpr (SPIN) D[2 + sub] = zslot;
-#pragma unroll
-    for (int t = 1; t <= L; ++t) {
-        float* d = D + T0 + PER_T * (t - 1);
-        d[sub] = Q0[t];
-        if constexpr (SPIN) {
-            d[2 + sub] = Q1[t];
-            d[4 + sub] = Q2[t];
-        }
-    }
-}
 
 template <int L, bool SPIN, typename TIO, bool BWD>
 __global__ __launch_bounds__((PairShape<L, SPIN>::THREADS)) void spingtp_fwd_pair_kernel(
@@ -645,151 +418,6 @@ hipError_t launch_pair(const void* x1, const void* x2, void* out, int64_t units,
     return hipGetLastError();
 }
 
-// ---------------------------------------------------------------------------
-// Large-degree kernel (L = 9..16, fp32 I/O).  More nodes than a workgroup has
-// waves, and 32-unit input tiles that no longer fit in LDS: the nodes are
-// processed in rounds of W waves, each lane pair reads its unit's input rows
-// straight from global memory (cached in L1/L2), the spectra of one round are
-// exchanged in LDS, and every output group's owner lane accumulates the
-// round's contribution into the output row (written in round 0, then read,
-// added and written by the same lane in later rounds: ordered, deterministic).
-// Where LDS has room for it (L <= 12) the output rows of the tile live in LDS
-// across the rounds and leave in one coalesced store; above that they are
-// updated in global memory.
-// ---------------------------------------------------------------------------
-template <int L, bool SPIN, int W>
-struct BigShape {
-    using PS = PairShape<L, SPIN>;
-    static constexpr Layout Y = make_layout(L, L, L);
-    static constexpr int NC = PS::NC;
-    static constexpr int NT = Y.NT;
-    static constexpr int NP = Y.NP;
-    static constexpr int UNITS = 32;
-    static constexpr int WAVES = W;
-    static constexpr int THREADS = 64 * W;
-    static constexpr int ROUNDS = (NT + W - 1) / W;
-    static constexpr int DF = W * UNITS * PS::DS;
-    static constexpr int TRIG = 2 * NP * (L + 1);
-    static constexpr int STO = NC | 1;  // odd row stride of the output tile
-    static constexpr bool OUT_LDS = (DF + TRIG + UNITS * STO) * 4 <= 160 * 1024;
-    static constexpr int LDS_FLOATS = DF + TRIG + (OUT_LDS ? UNITS * STO : 0);
-};
-
-// PAR (spins only): the plan's basis is the parity-labelled one; a separate
-// instantiation, since a run-time switch between the two step-(A) forms costs the
-// paper-basis kernels registers.
-template <int L, bool SPIN, int W, bool BWD, bool PAR>
-__global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_big_kernel(
-    const float* __restrict__ x1, const float* __restrict__ x2, float* __restrict__ out, int64_t units, int64_t cpx2,
-    const float* __restrict__ tab) {
-    using B = BigShape<L, SPIN, W>;
-    using P = typename B::PS;
-    constexpr Layout Y = B::Y;
-    constexpr int TM1 = Y.TM + 1;
-    constexpr int BO = (L + 1) * (L + 1);
-    __shared__ float lds[B::LDS_FLOATS];
-    float* D = lds;
-    float* TR = lds + B::DF;
-    float* YT = TR + B::TRIG;  // output tile (OUT_LDS only)
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int u = lane >> 1;
-    const int sub = lane & 1;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t u0 = static_cast<int64_t>(blockIdx.x) * B::UNITS;
-    const int nvalid = static_cast<int>(units - u0 < B::UNITS ? units - u0 : B::UNITS);
-    const bool valid = u < nvalid;
-    const int64_t row = u0 + (valid ? u : 0);  // invalid lanes compute on a valid row, store nothing
-    const float* g = tab;
-    const float* xr = sub ? x2 + (row / cpx2) * B::NC : x1 + row * B::NC;
-    float* orow = out + row * B::NC;
-
-    for (int i = tid; i < B::TRIG; i += B::THREADS) {
-        const int sb = i / (B::NP * (L + 1));
-        const int r = i - sb * (B::NP * (L + 1));
-        const int k = r / (L + 1), t = r - k * (L + 1);
-        TR[i] = g[(sb ? Y.sinT : Y.cosT) + k * TM1 + t];
-    }
-    // parity basis: the |s| = 1 blocks of each input row are mixed by P as step (A)
-    // reads them, and the finished output rows by P^T before they are final
-    static_assert(SPIN || !PAR, "the parity basis only mixes |s| = 1 blocks");
-    if constexpr (SPIN) {  // l = 0 slots of the |s| = 1 blocks
-        if constexpr (B::OUT_LDS) {
-            if (wave == 0) YT[u * B::STO + (sub ? 2 * BO : 0)] = 0.f;
-        } else {
-            if (wave == 0 && valid) orow[sub ? 2 * BO : 0] = 0.f;
-        }
-    }
-    __syncthreads();
-
-    constexpr Owners<P::NG> own = assign_pair_owners<L, SPIN, W>();
-#pragma unroll 1
-    for (int r = 0; r < B::ROUNDS; ++r) {
-        const int node = r * W + wave;
-        const int nr = (B::NT - r * W) < W ? (B::NT - r * W) : W;
-        if (node < B::NT) {
-            float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
-            const float* tb = tab + Y.glob + node * Y.pb;
-            const float* trl = TR + sub * (B::NP * (L + 1));
-            pair_spectra<L, SPIN, BWD, PAR>(xr, tb, g, trl, sub, Q0, Q1, Q2, zslot);
-            pair_publish<L, SPIN>(D + (wave * B::UNITS + u) * P::DS, sub, Q0, Q1, Q2, zslot);
-        }
-        __syncthreads();
-#pragma unroll
-        for (int gi = 0; gi < P::NG; ++gi) {
-            if (own.owner[gi] != wave) continue;
-            const int t = P::t_of(gi), kind = P::kind_of(gi);
-            int tab_base = Y.e0c, blk = SPIN ? BO : 0;
-            if (kind == 1) tab_base = Y.e1p, blk = 2 * BO;
-            if (kind == 2) tab_base = Y.e1m, blk = 0;
-            if (kind == 3) tab_base = Y.e1z, blk = sub ? 0 : 2 * BO;
-            float acc[L + 1];
-#pragma unroll
-            for (int l = 0; l <= L; ++l) acc[l] = 0.f;
-#pragma unroll 1
-            for (int jj = 0; jj < nr; ++jj) {
-                const float d = D[(jj * B::UNITS + u) * P::DS + P::slot(gi) + sub];
-                const float* te = tab + Y.glob + (r * W + jj) * Y.pb;
-#pragma unroll
-                for (int l = P::lmin(gi); l <= L; ++l)
-                    acc[l] = fmaf(te[kind == 3 ? tab_base + l : tab_base + tri(L, t, l)], d, acc[l]);
-            }
-            if (valid && !(t == 0 && kind == 0 && sub)) {
-                float* yrow = B::OUT_LDS ? YT + u * B::STO : orow;
-#pragma unroll
-                for (int l = P::lmin(gi); l <= L; ++l) {
-                    float* o = yrow + blk + l * l + l + (sub ? -t : t);
-                    *o = (r == 0) ? acc[l] : *o + acc[l];
-                }
-            }
-        }
-        __syncthreads();
-    }
-    if constexpr (B::OUT_LDS) {
-        if constexpr (PAR) {
-            parity_mix_rows<L>(YT, B::STO, nvalid, true, tid, B::THREADS);
-            __syncthreads();
-        }
-        store_tile<B::NC, B::STO>(out + u0 * B::NC, nvalid, YT, tid, B::THREADS);
-    } else if constexpr (PAR) {
-        // the rows were accumulated in global memory by several waves; the barrier
-        // that ends the last round orders those stores before these reads
-        parity_mix_rows<L>(out + u0 * B::NC, B::NC, nvalid, true, tid, B::THREADS);
-    }
-}
-
-template <int L, bool SPIN, int W, bool BWD, bool PAR>
-hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
-                      const uint32_t*, hipStream_t stream) {
-    using B = BigShape<L, SPIN, W>;
-    const int64_t blocks = (units + B::UNITS - 1) / B::UNITS;
-    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W, BWD, PAR>), dim3(static_cast<unsigned>(blocks)), dim3(B::THREADS),
-                       0, stream, static_cast<const float*>(x1), static_cast<const float*>(x2),
-                       static_cast<float*>(out), units, cpx2, tab);
-    return hipGetLastError();
-}
 
 template <int L1, int L2, int LO, bool SPIN, typename TIO>
 hipError_t launch(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
@@ -838,24 +466,8 @@ constexpr Registered reg_big() {
                                   &launch_big<L, SPIN, W, false, PAR>, &launch_big<L, SPIN, W, true, PAR>},
                       SPIN ? (PAR ? 1 : 0) : -1};
 }
-// Nodes per round: eight (two waves per SIMD at up to 256 VGPRs) where the output tile
-// fits in LDS next to eight waves' spectra; for spins at L = 13, 14 the most waves (7, 6)
-// that still leave room for the tile, since a global read-modify-write of the outputs
-// per round costs more than the extra rounds' input re-reads. Below 6 waves (L = 15, 16)
-// the lost latency hiding costs more than the tile saves, so those keep 8 waves and
-// accumulate into global memory.
-template <int L, bool SPIN>
-constexpr int big_waves() {
-    for (int w = 8; w >= 6; --w) {
-        const int spectra = w * 32 * PairShape<L, SPIN>::DS, trig = 2 * (3 * L + 1) * (L + 1);
-        const int tile = 32 * (PairShape<L, SPIN>::NC | 1);
-        if ((spectra + trig + tile) * 4 <= 160 * 1024) return w;
-    }
-    return 8;
-}
-#define SPINGTP_REG_BIG(L)                                                                   \
-    reg_big<L, true, big_waves<L, true>()>(), reg_big<L, true, big_waves<L, true>(), true>(), \
-        reg_big<L, false, big_waves<L, false>()>()
+// (the parity-basis instantiations with spins are in forward_big_parity.hip)
+#define SPINGTP_REG_BIG(L) reg_big<L, true, big_waves<L, true>()>(), reg_big<L, false, big_waves<L, false>()>()
 
 const Registered kRegistry[] = {
     SPINGTP_REG(0, 0, 0, false), SPINGTP_REG(1, 1, 1, false), SPINGTP_REG(2, 2, 2, false),
@@ -876,6 +488,7 @@ const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype,
         if (r.L1 == L1 && r.L2 == L2 && r.LO == LO && r.spin == spin_mode && r.dtype == dtype &&
             (r.basis_par < 0 || r.basis_par == (parity ? 1 : 0)))
             return &r.entry;
+    if (parity && spin_mode == 1 && L1 == L2 && L2 == LO && dtype == 0) return find_big_parity_kernel(L1);
     return nullptr;
 }
 
