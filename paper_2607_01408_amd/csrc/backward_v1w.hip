@@ -409,15 +409,15 @@ hipError_t launch_typed(const void* x1, const void* x2, const float* w, const vo
 
 }  // namespace
 
-void bw1w_groups(int64_t N, int64_t C, int64_t* groups, int64_t* epg) {
-    // about kBw1wTargetGroups workgroups over the channel tiles and edge ranges
+void bw1w_groups(int64_t N, int64_t C, int64_t* groups, int64_t* epg, int target) {
+    // about `target` workgroups over the channel tiles and edge ranges
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     if (N <= 0 || tiles <= 0) {
         *groups = 0;
         *epg = 0;
         return;
     }
-    int64_t want = kBw1wTargetGroups / tiles;
+    int64_t want = target / tiles;
     if (want < 1) want = 1;
     if (want > N) want = N;
     *epg = (N + want - 1) / want;
@@ -466,7 +466,11 @@ static hipError_t launch_fwd_typed(const void* x1, const void* x2, const float* 
                                    bool acc_out) {
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     int64_t groups = 0, epg = 0;
-    bw1w_groups(N, C, &groups, &epg);
+    // as many workgroups as fit the chip at once (256 CUs, as many per CU as
+    // their LDS allows): more ranges where the tile is small, and the weight rows
+    // amortised over more edges where it is large
+    const int per_cu = kBw1wMaxLdsFloats / (lds_floats > 0 ? lds_floats : 1);
+    bw1w_groups(N, C, &groups, &epg, 256 * (per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu)));
     if (groups == 0 || tiles == 0) return hipSuccess;
     if (groups > 0x7fffffff || tiles > 0xffff) return hipErrorInvalidValue;
     const size_t bytes = static_cast<size_t>(lds_floats) * sizeof(float);

@@ -161,13 +161,14 @@ struct Bw1wShape {
 constexpr int kBw1wWaves = 4;             // waves of a workgroup, splitting each pass's keys
 constexpr int kBw1wMaxLdsFloats = 40960;  // 160 KB
 constexpr int kBw1wMaxIndex = 1022;       // 10-bit entry fields; a row's zero column sits at index n
-constexpr int kBw1wTargetGroups = 512;    // workgroups a launch aims for (two per CU)
+constexpr int kBw1wTargetGroups = 512;    // workgroups a gradient launch aims for (two per CU)
 // Entry lists of the table (layout in backward_v1w.hip); false where an index or the
 // LDS tile does not fit.  `dense`: the tensor of build_dense_tensor if the caller has it.
 bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
                          std::vector<uint32_t>& out, Bw1wShape* shape, const std::vector<double>* dense = nullptr);
-// Edge ranges of a launch: `groups` ranges of `epg` edges (0, 0 when N or C is 0).
-void bw1w_groups(int64_t N, int64_t C, int64_t* groups, int64_t* epg);
+// Edge ranges of a launch: `groups` ranges of `epg` edges (0, 0 when N or C is 0), for
+// about `target` workgroups.
+void bw1w_groups(int64_t N, int64_t C, int64_t* groups, int64_t* epg, int target = kBw1wTargetGroups);
 // Workspace of a launch, in floats: gx2 partial sums per channel tile and edge, then
 // gW partial sums per edge range, path and channel.
 size_t bw1w_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s);
