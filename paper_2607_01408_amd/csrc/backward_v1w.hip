@@ -135,6 +135,14 @@ __device__ __forceinline__ float bw_wave_sum(float v) {
 
 __host__ __device__ constexpr int bw_stride(int n) { return (n + 1) | 1; }  // odd, with a zero column
 
+// Workgroups a launch aims for: as many as fit the chip at once (256 CUs, as many
+// per CU as their LDS allows, at most 8): more edge ranges where the tile is small,
+// and the weight rows amortised over more edges where it is large.
+int bw_target_groups(int lds_floats) {
+    const int per_cu = kBw1wMaxLdsFloats / (lds_floats > 0 ? lds_floats : 1);
+    return 256 * (per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu));
+}
+
 // SHARED: x2 [N][NC2] shared by the channels of an edge (gx2 summed over the
 // channels into the workspace); else x2 [N][C][NC2] per unit (gx2 per unit, staged
 // in an LDS tile and stored with gx1).
@@ -369,7 +377,7 @@ hipError_t launch_typed(const void* x1, const void* x2, const float* w, const vo
                         hipStream_t stream, int64_t x2s, bool acc_gx1) {
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     int64_t groups = 0, epg = 0;
-    bw1w_groups(N, C, &groups, &epg);
+    bw1w_groups(N, C, &groups, &epg, bw_target_groups(SHARED ? s.lds_floats : s.lds_unit_bwd));
     float* ws_x2 = ws;
     float* ws_w = SHARED ? ws + tiles * N * s.nc2 : ws;
     if (groups > 0 && tiles > 0) {
@@ -426,14 +434,14 @@ void bw1w_groups(int64_t N, int64_t C, int64_t* groups, int64_t* epg, int target
 
 size_t bw1w_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s) {
     int64_t groups = 0, epg = 0;
-    bw1w_groups(N, C, &groups, &epg);
+    bw1w_groups(N, C, &groups, &epg, bw_target_groups(s.lds_floats));  // as the launch splits them
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     return static_cast<size_t>(tiles * N * s.nc2 + groups * s.np * C);
 }
 
 size_t bwcw_workspace_floats(int64_t N, int64_t C, const Bw1wShape& s) {
     int64_t groups = 0, epg = 0;
-    bw1w_groups(N, C, &groups, &epg);
+    bw1w_groups(N, C, &groups, &epg, bw_target_groups(s.lds_unit_bwd));  // as the launch splits them
     return static_cast<size_t>(groups * s.np * C);
 }
 
@@ -466,11 +474,7 @@ static hipError_t launch_fwd_typed(const void* x1, const void* x2, const float* 
                                    bool acc_out) {
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     int64_t groups = 0, epg = 0;
-    // as many workgroups as fit the chip at once (256 CUs, as many per CU as
-    // their LDS allows): more ranges where the tile is small, and the weight rows
-    // amortised over more edges where it is large
-    const int per_cu = kBw1wMaxLdsFloats / (lds_floats > 0 ? lds_floats : 1);
-    bw1w_groups(N, C, &groups, &epg, 256 * (per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu)));
+    bw1w_groups(N, C, &groups, &epg, bw_target_groups(lds_floats));
     if (groups == 0 || tiles == 0) return hipSuccess;
     if (groups > 0x7fffffff || tiles > 0xffff) return hipErrorInvalidValue;
     const size_t bytes = static_cast<size_t>(lds_floats) * sizeof(float);

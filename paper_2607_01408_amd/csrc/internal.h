@@ -161,7 +161,7 @@ struct Bw1wShape {
 constexpr int kBw1wWaves = 4;             // waves of a workgroup, splitting each pass's keys
 constexpr int kBw1wMaxLdsFloats = 40960;  // 160 KB
 constexpr int kBw1wMaxIndex = 1022;       // 10-bit entry fields; a row's zero column sits at index n
-constexpr int kBw1wTargetGroups = 512;    // workgroups a gradient launch aims for (two per CU)
+constexpr int kBw1wTargetGroups = 512;    // default workgroup target of bw1w_groups
 // Entry lists of the table (layout in backward_v1w.hip); false where an index or the
 // LDS tile does not fit.  `dense`: the tensor of build_dense_tensor if the caller has it.
 bool build_bwd_v1w_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
