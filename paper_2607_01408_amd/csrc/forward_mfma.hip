@@ -88,13 +88,24 @@ __device__ __forceinline__ float swap_adjacent(float v) {
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 
 // (a, b) split as fp16 hi + lo: hw = (fp16(a), fp16(b)) rounded to nearest,
-// lw = (fp16(a - hi_a), fp16(b - hi_b)), each residual formed in fp32 and
-// rounded once by v_fma_mix{lo,hi}_f16; |x - hi - lo| <= 2^-22 |x| for normal x.
+// lw = (fp16(a - hi_a), fp16(b - hi_b)).  Each residual is exact in fp32 (hi is a
+// rounding of the value, so the difference needs at most 13 significant bits) and
+// is rounded once; |x - hi - lo| <= 2^-22 |x| for normal x.
+//
+// hi and lo must both come from the same fp32 value.  Left to itself the compiler
+// folds the FMA that produced a value into the fp16 conversion of the high word
+// (v_fma_mix: one rounding of the exact result) while it forms the residual from
+// the fp32-rounded value; where the two roundings differ, hi + lo misses the value
+// by one fp16 unit.  The empty asm statements (no instruction is emitted) make a
+// and b opaque, so every conversion below starts from the same fp32 registers; all
+// instructions are the compiler's own, so its hazard model sees every write.
 __device__ __forceinline__ void split_pair(float a, float b, uint32_t& hw, uint32_t& lw) {
-    const h2 hp = {static_cast<_Float16>(a), static_cast<_Float16>(b)};
+    asm("" : "+v"(a), "+v"(b));
+    const _Float16 ha = static_cast<_Float16>(a), hb = static_cast<_Float16>(b);
+    const h2 hp = {ha, hb};
+    const h2 lp = {static_cast<_Float16>(a - static_cast<float>(ha)), static_cast<_Float16>(b - static_cast<float>(hb))};
     hw = __builtin_bit_cast(uint32_t, hp);
-    asm("v_fma_mixlo_f16 %0, %1, -1.0, %2 op_sel_hi:[1,0,0]" : "=v"(lw) : "v"(hw), "v"(a));
-    asm("v_fma_mixhi_f16 %0, %1, -1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "+v"(lw) : "v"(hw), "v"(b));
+    lw = __builtin_bit_cast(uint32_t, lp);
 }
 
 __device__ __forceinline__ uint32_t pack_hi(float a, float b) {
@@ -125,20 +136,9 @@ __device__ __forceinline__ void split8(const float (&v)[8], const bool (&live)[8
     lo = __builtin_bit_cast(v8h, l);
 }
 
-// v_permlane32_swap with two wait states on each side, kept in place by
-// scheduling barriers.  Without them the ROCm 7.2 compiler can emit the swap
-// next to the VALU writes of its operands (or the reads of its results); those
-// schedules gave silently wrong operand words on gfx950 (relative errors near
-// 5e-5 instead of 2e-7), and the wait states remove the error in every build
-// tried.
-__device__ __forceinline__ void permlane32_swap_guarded(uint32_t a, uint32_t b, uint32_t& r0, uint32_t& r1) {
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_nop 1" ::: "memory");
-    __builtin_amdgcn_sched_barrier(0);
+// v_permlane32_swap: exchanges the upper half-wave of a with the lower half-wave of b.
+__device__ __forceinline__ void permlane32_swap(uint32_t a, uint32_t b, uint32_t& r0, uint32_t& r1) {
     const auto r = __builtin_amdgcn_permlane32_swap(a, b, false, false);
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_nop 1" ::: "memory");
-    __builtin_amdgcn_sched_barrier(0);
     r0 = r[0];
     r1 = r[1];
 }
@@ -151,7 +151,7 @@ __device__ __forceinline__ void swap_halves(const v8h& a, const v8h& b, v8h& r0,
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
         uint32_t x, y;
-        permlane32_swap_guarded(ua[w], ub[w], x, y);
+        permlane32_swap(ua[w], ub[w], x, y);
         o0[w] = x;
         o1[w] = y;
     }
@@ -162,7 +162,7 @@ __device__ __forceinline__ void swap_halves(const v8h& a, const v8h& b, v8h& r0,
 // Value of lanes 0..31 (lo) and of lanes 32..63 (hi) of x, in every lane.
 __device__ __forceinline__ void bcast_halves(float x, float& lo, float& hi) {
     uint32_t a, b;
-    permlane32_swap_guarded(__float_as_uint(x), __float_as_uint(x), a, b);
+    permlane32_swap(__float_as_uint(x), __float_as_uint(x), a, b);
     lo = __uint_as_float(a);
     hi = __uint_as_float(b);
 }

@@ -1371,21 +1371,28 @@ spingtp_status spingtp_paths_host(int L1, int L2, int Lout, const int* spins, in
 spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
     if (plan == nullptr) return SPINGTP_OK;
     int cur = 0;
-    hipError_t e = hipGetDevice(&cur);
-    if (e == hipSuccess && cur != plan->device) e = hipSetDevice(plan->device);
-    if (e == hipSuccess && plan->d_tab != nullptr) e = hipFree(plan->d_tab);
-    if (e == hipSuccess && plan->d_aux != nullptr) e = hipFree(plan->d_aux);
-    if (e == hipSuccess && plan->d_dir != nullptr) e = hipFree(plan->d_dir);
-    if (e == hipSuccess && plan->d_dir_b1 != nullptr) e = hipFree(plan->d_dir_b1);
-    if (e == hipSuccess && plan->d_dir_b2 != nullptr) e = hipFree(plan->d_dir_b2);
-    if (e == hipSuccess && plan->d_pre_w != nullptr) e = hipFree(plan->d_pre_w);
-    if (e == hipSuccess && plan->d_bw1w != nullptr) e = hipFree(plan->d_bw1w);
-    if (e == hipSuccess && plan->d_pre != nullptr) e = hipFree(plan->d_pre);
-    if (e == hipSuccess && plan->d_pre_bwd != nullptr) e = hipFree(plan->d_pre_bwd);
-    if (e == hipSuccess && plan->own_tab_bwd) e = hipFree(plan->d_tab_bwd);
-    if (cur != plan->device) (void)hipSetDevice(cur);
+    hipError_t first = hipGetDevice(&cur);
+    const bool switched = first == hipSuccess && cur != plan->device;
+    if (switched) first = hipSetDevice(plan->device);
+    // every buffer is freed even after a failure; the first error is reported
+    auto release = [&first](void* p) {
+        if (p == nullptr) return;
+        const hipError_t e = hipFree(p);
+        if (first == hipSuccess) first = e;
+    };
+    release(plan->d_tab);
+    release(plan->d_aux);
+    release(plan->d_dir);
+    release(plan->d_dir_b1);
+    release(plan->d_dir_b2);
+    release(plan->d_pre_w);
+    release(plan->d_bw1w);
+    release(plan->d_pre);
+    release(plan->d_pre_bwd);
+    if (plan->own_tab_bwd) release(plan->d_tab_bwd);
+    if (switched) (void)hipSetDevice(cur);
     delete plan;
-    return e == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
+    return first == hipSuccess ? SPINGTP_OK : SPINGTP_ERR_HIP;
 }
 
 spingtp_status spingtp_plan_kernel_info(spingtp_plan plan, int* info) {

@@ -97,6 +97,44 @@ def test_matrix_core_sizes(L, N, C, dtype):
     run_and_compare(L, L, L, S3, N, C, dtype, 0, seed=50 + L + N % 7)
 
 
+def _ulp_bf16(y):
+    e = np.floor(np.log2(np.maximum(np.abs(y), 1e-300)))
+    return np.ldexp(1.0, (e - 7).astype(int))
+
+
+@pytest.mark.parametrize("L", [4, 5, 6])
+@pytest.mark.parametrize("N,C,basis", [(37, 3, 0), (4113, 1, 0), (125, 8, 2)])
+def test_matrix_core_bf16_against_reenactment(L, N, C, basis):
+    """The bf16 mode of the matrix-core kernel (fp16 high parts only) against the
+    CPU re-enactment of its own arithmetic from the library's operand words.
+
+    The oracle bar for bf16 (2e-2) leaves room for a corrupted operand word, so every
+    output element is also held to the re-enactment: within half a bf16 unit in the
+    last place (the output's own rounding) plus 2^-10 of the unit's largest output.
+    Two faithful evaluations drift apart by at most about 3e-4 of that scale (fp32
+    versus float64 step-(A) results move some fp16 roundings of step (B) by one
+    unit); a stale or wrong fp16 word in step (B) or (D) moves a field or spectrum
+    value by a sizable fraction of itself, which this bound catches."""
+    from tests.kernel_emulation import emulate_mfma_kernel
+    print(f"[reenact] L={L} N={N} C={C} bf16 basis={basis}", flush=True)
+    x1 = workloads.draw(L, N, C, 9100 + L, "bf16", S3, "unit", "cuda")
+    x2 = workloads.draw(L, N, C, 9200 + L, "bf16", S3, "unit", "cuda")
+    plan = Plan(L, L, L, S3, "bf16", basis)
+    assert plan.kernel_info()["family"] == 4
+    y = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    U = N * C
+    a = x1.view(U, -1).double().cpu().numpy()
+    b = x2.view(U, -1).double().cpu().numpy()
+    g = y.view(U, -1).double().cpu().numpy()
+    emu = emulate_mfma_kernel(a, b, L, basis, split=1)
+    scale = np.abs(emu).max(axis=1, keepdims=True)
+    excess = (np.abs(g - emu) - 0.5 * _ulp_bf16(emu)) / np.maximum(scale, 1e-300)
+    worst = float(excess.max())
+    print(f"[reenact]   worst excess over half an ulp = {worst:.3e} of the unit scale", flush=True)
+    assert worst <= 2.0 ** -10, worst
+
+
 @pytest.mark.parametrize("L,basis", [(9, 0), (9, 1), (12, 0), (16, 0)])
 def test_ragged_large_degree(L, basis):
     # 37 * 3 = 111 units: three full 32-unit tiles and a ragged tail of 15
@@ -144,10 +182,12 @@ def test_parity_basis_changes_the_map():
     assert float((y0 - y2).abs().max()) > 1e-2
 
 
-@pytest.mark.parametrize("L", [9, 12, 13, 16])
+@pytest.mark.parametrize("L", [9, 10, 11, 12, 13, 14, 15, 16])
 def test_parity_basis_large_degree(L):
     # the large-degree kernels mix the input rows as they read them; the output tile
-    # in LDS (L = 9, 12 with 8 waves, L = 13 with 7) or accumulated in global memory (L = 16)
+    # in LDS (L = 9..12 with 8 waves, L = 13 with 7, L = 14 with 6) or accumulated in
+    # global memory (L = 15, 16); every degree, since these instantiations are built
+    # with their own scheduling strategy
     run_and_compare(L, L, L, S3, 37, 3, "fp32", 2, seed=100 + L)
 
 
