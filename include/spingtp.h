@@ -60,7 +60,8 @@ typedef enum {
     SPINGTP_ERR_UNSUPPORTED = 2,   /* valid by the paper but not built in this library */
     SPINGTP_ERR_OUT_OF_MEMORY = 3, /* device allocation failed */
     SPINGTP_ERR_HIP = 4,           /* a HIP runtime call or kernel launch failed */
-    SPINGTP_ERR_INTERNAL = 5       /* plan self-check failed (a library bug) */
+    SPINGTP_ERR_INTERNAL = 5,      /* plan self-check failed (a library bug) */
+    SPINGTP_ERR_TOO_LARGE = 6      /* the request needs more than the library's fixed device scratch */
 } spingtp_status;
 
 typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
@@ -382,6 +383,27 @@ spingtp_status spingtp_backward(spingtp_plan plan, const void* x1, const void* x
 spingtp_status spingtp_backward_v1(spingtp_plan plan, const void* x1, const void* x2, const void* grad_out,
                                    void* grad_x1, void* grad_x2, void* workspace, size_t workspace_bytes,
                                    int64_t N, int64_t C, void* stream);
+
+/*
+ * spingtp_backward_v1 for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same gradients, computed by the same kernels in the same order (bit-identical
+ * results), with the per-unit products of grad_x2 staged in a fixed device array
+ * of SPINGTP_NOALLOC_SCRATCH_BYTES (64 MiB) that the library holds on each GPU
+ * it runs on until the process ends, instead of a caller workspace.
+ *   Arguments as for spingtp_backward_v1 without workspace/workspace_bytes.
+ *   grad_x2 != NULL with spingtp_backward_v1_workspace_size(plan, N, C) above
+ *   SPINGTP_NOALLOC_SCRATCH_BYTES: SPINGTP_ERR_TOO_LARGE, nothing launched
+ *   (grad_x1 alone has no limit).  The first call on a device looks up the
+ *   array's device address (hipGetSymbolAddress, the plan's device current);
+ *   failure: SPINGTP_ERR_HIP.  No hipMalloc or hipFree, no allocation.
+ *   Every call on one GPU shares that GPU's array (each call overwrites the rows
+ *   it reads, so nothing carries over): calls that overlap in time on one GPU,
+ *   on different streams or threads, race and give undefined gradients.
+ */
+#define SPINGTP_NOALLOC_SCRATCH_BYTES (64u << 20)
+spingtp_status spingtp_backward_v1_noalloc(spingtp_plan plan, const void* x1, const void* x2, const void* grad_out,
+                                           void* grad_x1, void* grad_x2, int64_t N, int64_t C, void* stream);
 
 /* Bytes of workspace spingtp_backward_v1 needs for grad_x2 with N x C units:
  * N C n_spins (L2+1)^2 elements of the plan's dtype.  SPINGTP_ERR_UNSUPPORTED as

@@ -7,7 +7,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspingtp.
 
 SPINGTP_OK = 0
 STATUS_NAMES = {0: "OK", 1: "ERR_INVALID_ARG", 2: "ERR_UNSUPPORTED", 3: "ERR_OUT_OF_MEMORY",
-                4: "ERR_HIP", 5: "ERR_INTERNAL"}
+                4: "ERR_HIP", 5: "ERR_INTERNAL", 6: "ERR_TOO_LARGE"}
 EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "spingtp_status_string",
             "spingtp_plan_tables_host", "spingtp_plan_kernel_info", "spingtp_dense_tensor_host",
             "spingtp_mfma_operands_host", "spingtp_forward_v1", "spingtp_plan_kernel_info_v1",
@@ -16,7 +16,7 @@ EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "s
             "spingtp_plan_create_weighted", "spingtp_forward_v1_weighted", "spingtp_backward_v1_weighted",
             "spingtp_backward_v1_weighted_workspace_size", "spingtp_forward_weighted", "spingtp_backward_weighted",
             "spingtp_backward_weighted_workspace_size", "spingtp_forward_depthwise", "spingtp_backward_depthwise",
-            "spingtp_backward_depthwise_workspace_size")
+            "spingtp_backward_depthwise_workspace_size", "spingtp_backward_v1_noalloc")
 
 _lib = None
 
@@ -104,6 +104,9 @@ def lib() -> ctypes.CDLL:
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                           ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
         L.spingtp_backward_v1.restype = ctypes.c_int
+        L.spingtp_backward_v1_noalloc.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_int64, ctypes.c_int64,
+                                                                         ctypes.c_void_p]
+        L.spingtp_backward_v1_noalloc.restype = ctypes.c_int
         L.spingtp_backward_v1_workspace_size.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                                          ctypes.POINTER(ctypes.c_size_t)]
         L.spingtp_backward_v1_workspace_size.restype = ctypes.c_int

@@ -18,6 +18,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 
 #include "internal.h"
 
@@ -193,4 +194,52 @@ extern "C" spingtp_status spingtp_backward_v1(spingtp_plan plan, const void* x1,
             return SPINGTP_ERR_HIP;
     }
     return SPINGTP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// spingtp_backward_v1 without a caller workspace: the grad_x2 staging rows live in
+// a fixed device array.  Host code never passes the array's name to a kernel (in
+// host code it names a host-side stand-in); it uses the device address looked up
+// once per device with that device current.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[SPINGTP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kScratchDevices] = {};
+
+// Device address of `scratch` on the current device (looked up on first use).
+spingtp_status scratch_address(int device, void** out) {
+    if (device < 0 || device >= kScratchDevices) return SPINGTP_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[device] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return SPINGTP_ERR_HIP;
+        g_scratch_ptr[device] = p;
+    }
+    *out = g_scratch_ptr[device];
+    return SPINGTP_OK;
+}
+
+}  // namespace
+
+extern "C" spingtp_status spingtp_backward_v1_noalloc(spingtp_plan plan, const void* x1, const void* x2,
+                                                      const void* grad_out, void* grad_x1, void* grad_x2, int64_t N,
+                                                      int64_t C, void* stream) {
+    size_t need = 0;
+    const spingtp_status st = spingtp_backward_v1_workspace_size(plan, N, C, &need);
+    if (st != SPINGTP_OK) return st;
+    if (grad_x2 != nullptr && need > SPINGTP_NOALLOC_SCRATCH_BYTES) return SPINGTP_ERR_TOO_LARGE;
+    void* ws = nullptr;
+    if (grad_x2 != nullptr && N > 0 && C > 0) {
+        int cur = -1;
+        if (hipGetDevice(&cur) != hipSuccess) return SPINGTP_ERR_HIP;
+        if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
+        const spingtp_status sa = scratch_address(cur, &ws);
+        if (sa != SPINGTP_OK) return sa;
+    }
+    return spingtp_backward_v1(plan, x1, x2, grad_out, grad_x1, grad_x2, ws, SPINGTP_NOALLOC_SCRATCH_BYTES, N, C,
+                               stream);
 }

@@ -973,6 +973,7 @@ const char* spingtp_status_string(spingtp_status s) {
         case SPINGTP_ERR_OUT_OF_MEMORY: return "out of device memory";
         case SPINGTP_ERR_HIP: return "HIP runtime error";
         case SPINGTP_ERR_INTERNAL: return "internal error (plan self-check failed)";
+        case SPINGTP_ERR_TOO_LARGE: return "request exceeds the fixed device scratch of the no-allocation entry point";
     }
     return "unknown status";
 }

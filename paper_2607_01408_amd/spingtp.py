@@ -288,6 +288,30 @@ class Plan:
                                                   ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_v1")
         return gx1, gx2
 
+    def backward_v1_noalloc(self, x1, x2, grad_out, grad_x1=None, grad_x2=None, stream=None):
+        """spingtp_backward_v1_noalloc: the gradients of backward_v1 written into the caller's
+        grad_x1 [N, C, ...] and/or grad_x2 [N, 1, ...] tensors; the library stages grad_x2 in its
+        fixed device scratch, so the call allocates nothing."""
+        import torch
+
+        if x2.dim() == 3:
+            x2 = x2.unsqueeze(1)
+        N, C = x1.shape[0], x1.shape[1]
+        for t, shape in ((x1, (N, C) + tuple(self.shape_in(1))), (x2, (N, 1) + tuple(self.shape_in(2))),
+                         (grad_out, (N, C) + tuple(self.shape_out)), (grad_x1, (N, C) + tuple(self.shape_in(1))),
+                         (grad_x2, (N, 1) + tuple(self.shape_in(2)))):
+            if t is not None and (tuple(t.shape) != shape or t.dtype != self.torch_dtype or not t.is_cuda
+                                  or not t.is_contiguous()):
+                raise ValueError("x1, grad_out, grad_x1 [N, C, ...], x2, grad_x2 [N, 1, ...] must be contiguous "
+                                 "device tensors of the plan's dtype")
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+        _lib.check(_lib.lib().spingtp_backward_v1_noalloc(
+            self._handle, x1.data_ptr(), x2.data_ptr(), grad_out.data_ptr(),
+            grad_x1.data_ptr() if grad_x1 is not None else None, grad_x2.data_ptr() if grad_x2 is not None else None,
+            N, C, ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_v1_noalloc")
+        return grad_x1, grad_x2
+
     def backward_v1_weighted(self, x1, x2, weights, grad_out, stream=None):
         """spingtp_backward_v1_weighted: (grad_x1 [N, C, ...], grad_x2 [N, 1, ...], grad_weights [C, n_paths]
         fp32) through forward_v1_weighted; the workspace comes from torch's allocator."""

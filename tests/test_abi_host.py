@@ -76,8 +76,9 @@ def test_table_entry_point_argument_checks(built_library, args, status):
 
 
 def test_status_strings(built_library):
-    for s in range(6):
+    for s in range(7):
         assert len(_lib.message(s)) >= 2
+    assert "scratch" in _lib.message(6)
 
 
 def emulate_kernel(x1, x2, L1, L2, LO, spin, basis, backward=False):
