@@ -22,8 +22,19 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-PEAK_FP32_VECTOR_TFLOPS = 157.3  # MI355X published fp32 vector peak
-PEAK_HBM_GBS = 8000.0
+PEAK_HBM_GBS = 8000.0             # MI355X HBM3E
+# vector ALU without packed fp32 (the build turns packed fp32 off): 256 CUs x 4 SIMDs x
+# 16 lanes x 2 flops (FMA) x 2.4 GHz
+PEAK_VALU_FP32_TFLOPS = 78.6
+PEAK_VALU_PACKED_FP32_TFLOPS = 157.3  # the published fp32 vector figure (packed FMA)
+PEAK_MFMA_F16_TFLOPS = 2500.0     # dense fp16 / bf16 matrix cores
+# The scope table's charged work per unit at spins (-1, 0, +1) (the survey's 2D (u,v) Fourier
+# route): coef->Fourier for both inputs, the spin-pair convolution done directly and by FFT,
+# and Fourier->coef.  Its floor charges the cheaper convolution on the vector ALU and the
+# transforms on the matrix cores (fp32 at 157.3 TF, bf16 at the fp16 peak).
+SCOPE_CHARGED = {2: (1152, 26600, 34168, 1800), 4: (5840, 276696, 160672, 9928),
+                 6: (16640, 1201928, 364544, 29000), 8: (35728, 3511928, 742048, 63624),
+                 12: (110672, 16415000, 1680896, 197960), 16: (251280, 49823928, 3377152, 449800)}
 METRIC = "edge·channel tensor products/sec at L=6 fp32; % HBM/MFMA roofline"
 # sources of the spingtp_forward kernels (families 1-4): a stored traffic record
 # is used only while their hash is unchanged
@@ -38,11 +49,11 @@ def kernel_sources(kname):
     return tuple(_CSRC + f for f in (main, "device_common.h", "layout.h") + extra)
 
 
-def route_flops(L1, L2, LO, spin=True):
-    """Algorithmic flops per unit of the exact-grid route (FMA = 2 flops).
+def route_steps(L1, L2, LO, spin=True):
+    """Algorithmic flops per unit of the exact-grid route, by step (FMA = 2 flops).
 
     Counts the structural work of the five steps on the n_theta x n_phi grid:
-    (A) one FMA per valid input coefficient plus the spin recombination,
+    (A) one FMA per valid input coefficient plus the spin recombination (both inputs),
     (B) even/odd synthesis of each real trigonometric polynomial,
     (C) the spin-pair products, (D) even/odd analysis of each product,
     (E) one FMA per valid output coefficient plus the spin recombination.
@@ -65,9 +76,70 @@ def route_flops(L1, L2, LO, spin=True):
     prod = 11 if spin else 1
     analysis = (LO + 1) + KP * (3 + 4 * LO) + (2 * (LO + 1) if even else 0)
     stage_e = 2 * coeffs(LO) + ((4 * LO + 23) if spin else 0)
-    per_node = (stage_a(L1) + stage_a(L2) + npoly * (synth(L1) + synth(L2)) + NP * prod
-                + npoly * analysis + stage_e)
-    return NT * per_node
+    return {"A": NT * (stage_a(L1) + stage_a(L2)), "B": NT * npoly * (synth(L1) + synth(L2)),
+            "C": NT * NP * prod, "D": NT * npoly * analysis, "E": NT * stage_e}
+
+
+def route_flops(L1, L2, LO, spin=True):
+    """All five steps of route_steps, per unit."""
+    return sum(route_steps(L1, L2, LO, spin).values())
+
+
+def mfma_flops_executed(family, L, dtype):
+    """fp16 matrix-core flops one unit costs on the matrix-core kernel, as executed: per wave
+    (32 units) and Gauss node, step (B) is six 32x32x16 products and step (D) three per
+    16-point K block, each repeated three times for the hi/lo split of fp32 I/O; all padding
+    (19 of 32 rows, 13 of 16 slots at L = 6) is counted."""
+    if family != 4:
+        return 0
+    NT = (3 * L + 2) // 2
+    NP = 3 * L + 1
+    NB = (NP + 15) // 16
+    split = 3 if dtype == "fp32" else 1
+    per_wave_node = (6 + 3 * NB) * split
+    return per_wave_node * (32 * 32 * 16 * 2) * NT // 32
+
+
+def roofline(family, L, dtype, units, avg_ms, bytes_unit, direct_flops=None, spin=True):
+    """Floors of the executed route on each resource and the one that binds.
+
+    hbm: algorithmic bytes (x1 + x2 + out) at 8 TB/s; valu: the route's vector-ALU flops (all
+    steps on the vector kernels, steps A, C, E on the matrix-core kernel) at the non-packed
+    78.6 TF this build can reach; mfma: the matrix-core work as executed (split products and
+    padding) at the dense fp16 peak.  bound = the largest floor; frac = floor / measured."""
+    t = avg_ms / 1e3
+    steps = route_steps(L, L, L, spin)
+    if direct_flops is not None:      # the direct kernel: a product and an FMA per tensor entry
+        valu = direct_flops
+    elif family == 4:
+        valu = steps["A"] + steps["C"] + steps["E"]
+    else:
+        valu = sum(steps.values())
+    mfma = mfma_flops_executed(family, L, dtype)
+    floors = {"hbm": bytes_unit * units / (PEAK_HBM_GBS * 1e9),
+              "alu": valu * units / (PEAK_VALU_FP32_TFLOPS * 1e12),
+              "mfma": mfma * units / (PEAK_MFMA_F16_TFLOPS * 1e12)}
+    bound = max(floors, key=floors.get)
+    if bound == "hbm":
+        achieved, peak, unit = bytes_unit * units / t / 1e9, PEAK_HBM_GBS, "GB/s"
+    elif bound == "alu":
+        achieved, peak, unit = valu * units / t / 1e12, PEAK_VALU_FP32_TFLOPS, "TFLOP/s"
+    else:
+        achieved, peak, unit = mfma * units / t / 1e12, PEAK_MFMA_F16_TFLOPS, "TFLOP/s"
+    out = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+           "floors_ms": {k: v * 1e3 for k, v in floors.items()},
+           "fracs": {k: v / t for k, v in floors.items()},
+           "valu_flops_per_unit": valu, "mfma_f16_flops_per_unit_executed": mfma,
+           "hbm_bytes_per_unit": bytes_unit,
+           "route_flops_per_unit": sum(steps.values()) if direct_flops is None else direct_flops}
+    if L in SCOPE_CHARGED and spin:
+        s2, s3d, s3f, s4 = SCOPE_CHARGED[L]
+        p_tr = (PEAK_VALU_PACKED_FP32_TFLOPS if dtype == "fp32" else PEAK_MFMA_F16_TFLOPS) * 1e12
+        t_scope = max(bytes_unit * units / (PEAK_HBM_GBS * 1e9),
+                      units * ((s2 + s4) / p_tr + min(s3d, s3f) / (PEAK_VALU_PACKED_FP32_TFLOPS * 1e12)))
+        out["scope_charged_flops_per_unit"] = s2 + min(s3d, s3f) + s4
+        out["scope_charged_frac"] = t_scope / t   # reported as-is; above 1 when the route does less work
+    return out
 
 
 def hbm_bytes_per_unit(L1, L2, LO, dtype, n_spins=3):
@@ -108,40 +180,132 @@ def measured_traffic(workload, dtype, units, L, kname, valu=False, basis="paper"
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(L, x1, x2, seconds, spins=(-1, 0, 1), basis=0):
-    """The CPU oracle on a bounded sample of the same inputs, on the host cores."""
+def cpu_workers_available():
+    """Host cores this process may use, capped at one GPU's share of the box (16)."""
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def _cpu_worker(conn):
+    """One CPU-oracle process: holds the oracle's tensor and its share of the sample.
+    Started with the spawn method before the parent touches the GPU; never uses it."""
+    for var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+        os.environ[var] = "1"
     import numpy as np
 
     import oracle
 
-    t0 = time.perf_counter()
-    T = oracle.RealGauntTensor(L, L, L, spins, basis)
-    build_s = time.perf_counter() - t0
+    T, X1, X2 = None, None, None
+    while True:
+        msg = conn.recv()
+        if msg[0] == "tensor":
+            t0 = time.perf_counter()
+            T = oracle.RealGauntTensor(msg[1], msg[1], msg[1], msg[2], msg[3])
+            conn.send(time.perf_counter() - t0)
+        elif msg[0] == "data":
+            X1, X2 = msg[1], msg[2]
+            conn.send(0 if X1 is None else len(X1))
+        elif msg[0] == "run":
+            t0 = time.perf_counter()
+            y = T.apply(X1, X2)
+            conn.send((time.perf_counter() - t0, float(np.abs(y[:1]).sum())))
+        elif msg[0] == "apply":
+            conn.send(T.apply(msg[1], msg[2]))
+        else:
+            break
+    conn.close()
+
+
+class CpuPool:
+    """n spawned oracle workers with one pipe each (no shared memory, no GPU)."""
+
+    def __init__(self, n):
+        import multiprocessing
+
+        ctx = multiprocessing.get_context("spawn")
+        self.conns, self.procs = [], []
+        for _ in range(n):
+            a, b = ctx.Pipe()
+            p = ctx.Process(target=_cpu_worker, args=(b,), daemon=True)
+            p.start()
+            self.conns.append(a)
+            self.procs.append(p)
+
+    def __len__(self):
+        return len(self.conns)
+
+    def all(self, msg):
+        for c in self.conns:
+            c.send(msg)
+        return [c.recv() for c in self.conns]
+
+    def scatter(self, kind, parts):
+        for c, part in zip(self.conns, parts):
+            c.send((kind,) + tuple(part))
+        return [c.recv() for c in self.conns[:len(parts)]]
+
+    def apply(self, a, b):
+        """The oracle on rows a, b (float64), split over the workers; rows in order."""
+        import numpy as np
+
+        k = max(1, min(len(self), len(a)))
+        cuts = np.linspace(0, len(a), k + 1).astype(int)
+        ys = self.scatter("apply", [(a[cuts[i]:cuts[i + 1]], b[cuts[i]:cuts[i + 1]]) for i in range(k)])
+        return np.concatenate([y.reshape(len(y), -1) for y in ys])
+
+    def close(self):
+        for c in self.conns:
+            try:
+                c.send(("exit",))
+            except OSError:
+                pass
+        for p in self.procs:
+            p.join(timeout=10)
+
+
+def cpu_baseline(pool, L, x1, x2, seconds, spins=(-1, 0, 1), basis=0):
+    """The unchanged CPU oracle on a bounded random sample of the same inputs, spread over
+    the worker processes (one core each); throughput = sampled units / wall time of the
+    parallel contraction.  The tensor build is timed apart and excluded."""
+    import numpy as np
+    import torch
+
+    n_w = len(pool)
+    build_s = max(pool.all(("tensor", L, tuple(spins), basis)))
     U = x1.shape[0] * x1.shape[1]
     a = x1.reshape(U, -1)
     b = x2.reshape(U, -1)
-    # calibrate on 256 units, then size the sample to ~`seconds`
-    probe = 256
-    t0 = time.perf_counter()
-    T.apply(a[:probe].double().cpu().numpy(), b[:probe].double().cpu().numpy())
-    per_unit = (time.perf_counter() - t0) / probe
-    n = int(max(probe, min(U, seconds / max(per_unit, 1e-9))))
     rng = np.random.default_rng(1234)
-    import torch
-    idx = torch.as_tensor(np.sort(rng.choice(U, size=n, replace=False)), device=a.device)
-    A = a[idx].double().cpu().numpy()
-    B = b[idx].double().cpu().numpy()
+
+    def load(idx):
+        ti = torch.as_tensor(idx, device=a.device)
+        return a[ti].float().cpu().numpy(), b[ti].float().cpu().numpy()
+
+    def split(A, B):
+        cuts = np.linspace(0, len(A), n_w + 1).astype(int)
+        return [(A[cuts[i]:cuts[i + 1]], B[cuts[i]:cuts[i + 1]]) for i in range(n_w)]
+
+    # calibrate: 256 units per worker
+    A, B = load(np.sort(rng.choice(U, size=min(U, 256 * n_w), replace=False)))
+    pool.scatter("data", split(A, B))
+    per_unit = float(np.median([r[0] for r in pool.all(("run",))])) / max(1, len(A) // n_w)
+    n = int(max(256 * n_w, min(U, seconds * n_w / max(per_unit, 1e-9))))
+    A, B = load(np.sort(rng.choice(U, size=n, replace=False)))
+    pool.scatter("data", split(A, B))
+    del A, B
     t0 = time.perf_counter()
-    T.apply(A, B)
-    dt = time.perf_counter() - t0
+    res = pool.all(("run",))
+    wall = time.perf_counter() - t0
+    pool.scatter("data", [(None, None)] * n_w)  # free the workers' copies
     return {
-        "value": n / dt,
+        "value": n / wall,
         "unit": "TP/s",
-        "cores": 1,
+        "cores": n_w,
         "kind": "oracle",
-        "sample": f"{n} seeded-random units of the same inputs ({dt:.1f} s of contraction, float64, "
-                  f"single-threaded numpy/scipy); sparse tensor build {build_s:.2f} s excluded",
-        "extrapolated_full_job_s": U / (n / dt),
+        "sample": f"{n} seeded-random units of the same inputs, split over {n_w} single-threaded "
+                  f"worker processes ({wall:.1f} s wall; float64 numpy/scipy); sparse tensor build "
+                  f"{build_s:.2f} s excluded",
+        "per_worker_s": [round(r[0], 3) for r in res],
+        "extrapolated_full_job_s": U / (n / wall),
         "host_cpus_visible": len(os.sched_getaffinity(0)),
     }
 
@@ -639,9 +803,11 @@ def main():
     ap.add_argument("--basis", default="paper", choices=sorted(BASES),
                     help="real basis of the coefficients (parity: the parity-labelled basis)")
     ap.add_argument("--L", type=int, default=None, help="degree (sweep workload only)")
-    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="CPU seconds per worker process of the oracle baseline (wall time about the same)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--parity-units", type=int, default=2048)
+    ap.add_argument("--parity-units", type=int, default=16384,
+                    help="seeded-random units checked against the oracle (plus the first and last 512)")
     ap.add_argument("--sweep", action="store_true", help="run the degree sweep against the dense CG comparator")
     ap.add_argument("--sweep-degrees", type=int, nargs="+", default=[2, 4, 8, 12, 16])
     ap.add_argument("--backward", action="store_true",
@@ -663,6 +829,18 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    # the CPU-oracle workers start before this process touches the GPU
+    pool = None
+    if not (args.sweep or args.v1 or args.backward) and not args.no_cpu_baseline:
+        pool = CpuPool(cpu_workers_available())
+    try:
+        run_main(args, pool)
+    finally:
+        if pool is not None:
+            pool.close()
+
+
+def run_main(args, pool):
     if args.sweep:
         run_sweep(args)
         return
@@ -722,7 +900,6 @@ def main():
         flops_unit = 3 * int((vals != 0).sum())
     else:
         flops_unit = route_flops(L, L, L, True)
-    achieved_tflops = flops_unit * U / (avg_launch_ms / 1e3) / 1e12
     # arithmetic of the path: the matrix-core kernel runs the two phi transforms as fp16
     # products with fp32 accumulation (three split products per term for fp32 I/O)
     if kinfo["family"] == 4:
@@ -741,17 +918,21 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # sampled parity against the oracle on the timed output
+    # sampled parity against the oracle on the timed output: the first and last 512 units
+    # (tile tails) and a seeded random sample
     import oracle
 
     rng = np.random.default_rng(77)
-    n_par = min(U, args.parity_units)
-    idx = np.unique(np.concatenate([np.arange(min(64, U)), np.arange(max(0, U - 64), U),
-                                    rng.choice(U, size=n_par, replace=False)]))
+    idx = np.unique(np.concatenate([np.arange(min(512, U)), np.arange(max(0, U - 512), U),
+                                    rng.choice(U, size=min(U, args.parity_units), replace=False)]))
     ti = torch.as_tensor(idx, device="cuda:0")
     ya = out.view(U, -1)[ti].double().cpu().numpy()
-    ref = oracle.spingtp(x1.view(U, -1)[ti].double().cpu().numpy(), x2.view(U, -1)[ti].double().cpu().numpy(),
-                         L, L, L, spins, BASES[args.basis]).reshape(len(idx), -1)
+    pa, pb = x1.view(U, -1)[ti].double().cpu().numpy(), x2.view(U, -1)[ti].double().cpu().numpy()
+    if pool is not None:
+        pool.all(("tensor", L, tuple(spins), BASES[args.basis]))
+        ref = pool.apply(pa, pb)
+    else:
+        ref = oracle.spingtp(pa, pb, L, L, L, spins, BASES[args.basis]).reshape(len(idx), -1)
     parity = float(np.linalg.norm(ya - ref) / np.linalg.norm(ref))
 
     result = {
@@ -775,37 +956,15 @@ def main():
             "L1": L, "L2": L, "Lout": L, "N": meta["N"], "C": meta["C"], "units": U, "basis": args.basis,
             "seeds": list(meta["seeds"]),
         },
-        "roofline": {
-            "bound": "alu",
-            "achieved": achieved_tflops,
-            "peak": PEAK_FP32_VECTOR_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,
-        } if kinfo["family"] != 6 else {
-            # the direct kernel moves more bytes per flop than the fp32 ridge point: HBM bound
-            "bound": "hbm",
-            "achieved": bytes_unit * U / (avg_launch_ms / 1e3) / 1e9,
-            "peak": PEAK_HBM_GBS,
-            "unit": "GB/s",
-            "frac": bytes_unit * U / (avg_launch_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
-            "alu_tflops": achieved_tflops,
-            "alu_frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,
-        },
+        "roofline": roofline(kinfo["family"], L, args.dtype, U, avg_launch_ms, bytes_unit,
+                             flops_unit if kinfo["family"] == 6 else None, len(spins) > 1),
     }
-    result["roofline"].update({
-            "traffic": traffic,
-            "kernel": kname,
-            "kernel_family": kinfo["family"],
-            "avg_launch_ms": avg_launch_ms,
-            "flops_per_unit": flops_unit,
-            "hbm_bytes_per_unit": bytes_unit,
-            "hbm_achieved_gbs": bytes_unit * U / (avg_launch_ms / 1e3) / 1e9,
-            "hbm_frac": bytes_unit * U / (avg_launch_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
-    })
+    result["roofline"].update({"traffic": traffic, "kernel": kname, "kernel_family": kinfo["family"],
+                               "avg_launch_ms": avg_launch_ms})
     result["parity_rel_l2"] = parity
     result["parity_units"] = int(len(idx))
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(L, x1, x2, args.cpu_seconds, spins, BASES[args.basis])
+    if pool is not None:
+        result["cpu_baseline"] = cpu_baseline(pool, L, x1, x2, args.cpu_seconds, spins, BASES[args.basis])
     print(json.dumps(result), flush=True)
 
 
