@@ -17,7 +17,7 @@
 //
 // Precision.  For fp32 I/O every operand is split into fp16 high and low parts
 // and each product is hi*hi + hi*lo + lo*hi (each exact in the fp32 accumulator),
-// which leaves a relative error near 2^-21 per term -- fp32-like.  bf16 I/O uses
+// which leaves a relative error near 2^-20 per term -- fp32-like.  bf16 I/O uses
 // the high parts only (2^-11).  fp16 has a narrow exponent range, so each input
 // row of every unit is first scaled by a power of two that puts its largest
 // magnitude in [1/2, 1); by Cauchy-Schwarz every field is then bounded by
@@ -87,24 +87,23 @@ __device__ __forceinline__ float swap_adjacent(float v) {
 
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 
-// (a, b) split as fp16 hi + lo: hw = (fp16(a), fp16(b)) rounded to nearest,
-// lw = (fp16(a - hi_a), fp16(b - hi_b)).  Each residual is exact in fp32 (hi is a
-// rounding of the value, so the difference needs at most 13 significant bits) and
-// is rounded once; |x - hi - lo| <= 2^-22 |x| for normal x.
+// (a, b) split as fp16 hi + lo: hw = (fp16(a), fp16(b)) rounded toward zero,
+// lw = (fp16(a - hi_a), fp16(b - hi_b)) rounded to nearest; each residual is exact
+// in fp32 and below one fp16 unit of the value, so |x - hi - lo| <= 2^-21 |x| for
+// normal x.
 //
-// hi and lo must both come from the same fp32 value.  Left to itself the compiler
-// folds the FMA that produced a value into the fp16 conversion of the high word
-// (v_fma_mix: one rounding of the exact result) while it forms the residual from
-// the fp32-rounded value; where the two roundings differ, hi + lo misses the value
-// by one fp16 unit.  The empty asm statements (no instruction is emitted) make a
-// and b opaque, so every conversion below starts from the same fp32 registers; all
-// instructions are the compiler's own, so its hazard model sees every write.
+// Six instructions a pair, all the compiler's own (its hazard model sees every
+// write; no inline asm, which its wait-state counting takes for one instruction
+// whatever it holds).  The high word comes from the v_cvt_pkrtz intrinsic and the
+// residuals from that word's own bits: a plain fp16 conversion would let the
+// compiler fold the FMA that produced a value into the conversion (one rounding
+// of the exact result) while forming the residual from the fp32-rounded value,
+// and where those two roundings differ hi + lo misses the value by one fp16 unit.
 __device__ __forceinline__ void split_pair(float a, float b, uint32_t& hw, uint32_t& lw) {
-    asm("" : "+v"(a), "+v"(b));
-    const _Float16 ha = static_cast<_Float16>(a), hb = static_cast<_Float16>(b);
-    const h2 hp = {ha, hb};
-    const h2 lp = {static_cast<_Float16>(a - static_cast<float>(ha)), static_cast<_Float16>(b - static_cast<float>(hb))};
-    hw = __builtin_bit_cast(uint32_t, hp);
+    const h2 hq = __builtin_bit_cast(h2, __builtin_amdgcn_cvt_pkrtz(a, b));
+    hw = __builtin_bit_cast(uint32_t, hq);
+    const h2 lp = {static_cast<_Float16>(a - static_cast<float>(hq.x)),
+                   static_cast<_Float16>(b - static_cast<float>(hq.y))};
     lw = __builtin_bit_cast(uint32_t, lp);
 }
 

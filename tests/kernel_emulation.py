@@ -48,17 +48,27 @@ def _operand_matrices(words):
     return hi, lo
 
 
+def _rtz16(x):
+    """fp16 rounding toward zero (the kernel's v_cvt_pkrtz for the data's high parts)."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.abs(x)
+    e = np.floor(np.log2(np.maximum(a, 2.0 ** -24)))
+    q = np.ldexp(1.0, (np.maximum(e, -14) - 10).astype(int))   # fp16 spacing at |x| (subnormal below 2^-14)
+    return np.sign(x) * np.floor(a / q) * q
+
+
 def _split16(x):
-    hi = x.astype(np.float16).astype(np.float64)
+    """Data split as the kernel does it: hi rounded toward zero, lo = fp16(x - hi) to nearest."""
+    hi = _rtz16(x)
     return hi, (x - hi).astype(np.float16).astype(np.float64)
 
 
 def _split_product(Mh, Ml, x, split=3):
     """(Mh + Ml) x with x split into fp16 hi + lo, summed as hi.hi + hi.lo + lo.hi
     (split = 3, the fp32 mode) or hi.hi alone (split = 1, the bf16 mode), in float64."""
-    xh, xl = _split16(x)
     if split == 1:
-        return xh @ Mh.T
+        return x.astype(np.float16).astype(np.float64) @ Mh.T
+    xh, xl = _split16(x)
     return xh @ Mh.T + xl @ Mh.T + xh @ Ml.T
 
 
