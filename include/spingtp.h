@@ -405,6 +405,20 @@ spingtp_status spingtp_backward_v1(spingtp_plan plan, const void* x1, const void
 spingtp_status spingtp_backward_v1_noalloc(spingtp_plan plan, const void* x1, const void* x2, const void* grad_out,
                                            void* grad_x1, void* grad_x2, int64_t N, int64_t C, void* stream);
 
+/*
+ * Host-only self-test of plan creation's device upload, for tests of its failure
+ * handling (no GPU needed).  Builds the host tables exactly as spingtp_plan_create
+ * (same arguments and rules), then runs the same upload routine with host memory
+ * standing in for device memory, failing allocation number fail_at (0-based; -1:
+ * none fails).  *n_allocs = allocations attempted, *n_live = allocations still held
+ * when the upload returned (0 after a failure: everything allocated so far was
+ * released; those of a successful upload are released afterwards by this call).
+ * Returns the upload's status: SPINGTP_ERR_OUT_OF_MEMORY for the injected failure.
+ */
+spingtp_status spingtp_plan_upload_selftest_host(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                                 spingtp_dtype dtype, unsigned flags, int fail_at, int* n_allocs,
+                                                 int* n_live);
+
 /* Bytes of workspace spingtp_backward_v1 needs for grad_x2 with N x C units:
  * N C n_spins (L2+1)^2 elements of the plan's dtype.  SPINGTP_ERR_UNSUPPORTED as
  * for spingtp_backward_v1. */

@@ -3,7 +3,10 @@
 import ctypes
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspingtp.so")
+# SPINGTP_LIBRARY names another build of the same library (the sanitizer-checked copy
+# the host tests use); by default the in-tree build.
+LIB_PATH = os.environ.get("SPINGTP_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                               "libspingtp.so")
 
 SPINGTP_OK = 0
 STATUS_NAMES = {0: "OK", 1: "ERR_INVALID_ARG", 2: "ERR_UNSUPPORTED", 3: "ERR_OUT_OF_MEMORY",
@@ -16,7 +19,8 @@ EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "s
             "spingtp_plan_create_weighted", "spingtp_forward_v1_weighted", "spingtp_backward_v1_weighted",
             "spingtp_backward_v1_weighted_workspace_size", "spingtp_forward_weighted", "spingtp_backward_weighted",
             "spingtp_backward_weighted_workspace_size", "spingtp_forward_depthwise", "spingtp_backward_depthwise",
-            "spingtp_backward_depthwise_workspace_size", "spingtp_backward_v1_noalloc")
+            "spingtp_backward_depthwise_workspace_size", "spingtp_backward_v1_noalloc",
+            "spingtp_plan_upload_selftest_host")
 
 _lib = None
 
@@ -107,6 +111,9 @@ def lib() -> ctypes.CDLL:
         L.spingtp_backward_v1_noalloc.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_int64, ctypes.c_int64,
                                                                          ctypes.c_void_p]
         L.spingtp_backward_v1_noalloc.restype = ctypes.c_int
+        L.spingtp_plan_upload_selftest_host.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, c_int_p, ctypes.c_int,
+                                                        ctypes.c_int, ctypes.c_uint, ctypes.c_int, c_int_p, c_int_p]
+        L.spingtp_plan_upload_selftest_host.restype = ctypes.c_int
         L.spingtp_backward_v1_workspace_size.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                                          ctypes.POINTER(ctypes.c_size_t)]
         L.spingtp_backward_v1_workspace_size.restype = ctypes.c_int

@@ -66,5 +66,51 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     return LIB
 
 
+# host code checked by AddressSanitizer and UndefinedBehaviorSanitizer (device code is
+# built as usual: -Xarch_host applies the flags to the host compilation only)
+SANITIZED_SOURCES = ("plan.cpp", "api.cpp")
+SANITIZE_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                  "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+                  "-Xarch_host", "-g"]
+
+
+def sanitizer_runtime() -> str:
+    """The shared AddressSanitizer runtime of this toolchain (LD_PRELOAD for a Python host)."""
+    out = subprocess.run([hipcc(), "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True,
+                         text=True).stdout.strip()
+    if not out or not os.path.exists(out):
+        import glob
+        hits = glob.glob("/opt/rocm/lib/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so")
+        out = hits[0] if hits else ""
+    if not out:
+        raise RuntimeError("AddressSanitizer runtime not found")
+    return out
+
+
+def build_sanitized() -> str:
+    """A copy of the library whose host table builders and entry points run under the
+    sanitizers, at _build/sanitized/libspingtp.so (the kernels' objects are the regular ones)."""
+    objdir = os.path.join(ROOT, "_build")
+    sdir = os.path.join(objdir, "sanitized")
+    os.makedirs(sdir, exist_ok=True)
+    objs = []
+    for src in SOURCES:
+        if src in SANITIZED_SOURCES:
+            obj = os.path.join(sdir, os.path.splitext(src)[0] + ".o")
+            cmd = [hipcc(), "-x", "hip"] + HIP_FLAGS + SANITIZE_FLAGS + ["-I", os.path.join(ROOT, "include"), "-c",
+                                                                        os.path.join(CSRC, src), "-o", obj]
+            r = subprocess.run(cmd, capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError("hipcc failed:\n" + r.stdout + r.stderr)
+        else:
+            obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
+            if not os.path.exists(obj):
+                build()
+        objs.append(obj)
+    lib = os.path.join(sdir, "libspingtp.so")
+    subprocess.run([hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", lib] + objs, check=True)
+    return lib
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

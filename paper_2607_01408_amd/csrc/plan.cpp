@@ -15,6 +15,7 @@
 #include <map>
 #include <set>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <utility>
@@ -1124,12 +1125,23 @@ spingtp_status spingtp_conj_map_host(int L, const int* spins, int n_spins, unsig
     return SPINGTP_OK;
 }
 
+namespace {
+
+// Everything a plan holds, built on the host: the chosen kernels and the float64 /
+// word tables that go to the device.
+struct PlanHost {
+    int spin_mode = 0, dir_lds = 0;
+    const spingtp::KernelEntry *k = nullptr, *kd = nullptr, *kv1 = nullptr, *kw = nullptr;
+    std::vector<double> tab, tab_bwd;
+    std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2, pre_w, bw1w;
+    spingtp::Bw1wShape bw1w_shape{};
+    bool has_backward = false, same_bwd = false;
+};
+
 // weights: one per path of spingtp_paths_host (n_weights of them), or nullptr for the
 // unweighted product.
-static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, int n_spins, spingtp_dtype dtype,
-                                  unsigned flags, const double* weights, size_t n_weights, spingtp_plan* out_plan) {
-    if (out_plan == nullptr) return SPINGTP_ERR_INVALID_ARG;
-    *out_plan = nullptr;
+spingtp_status build_plan_host(int L1, int L2, int Lout, const int* spins, int n_spins, spingtp_dtype dtype,
+                               unsigned flags, const double* weights, size_t n_weights, PlanHost& h) {
     int spin_mode = 0;
     spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
@@ -1171,12 +1183,18 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     if (kv1 == nullptr) return SPINGTP_ERR_UNSUPPORTED;
     const unsigned basis = flags & ~kRouteFlags;
 
-    std::vector<double> tab;
-    std::vector<double> tab_bwd;
-    std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2, pre_w, bw1w;
-    spingtp::Bw1wShape bw1w_shape{};
-    const spingtp::KernelEntry* kw = nullptr;
-    bool has_backward = false, same_bwd = false;
+    std::vector<double>& tab = h.tab;
+    std::vector<double>& tab_bwd = h.tab_bwd;
+    std::vector<uint32_t>&aux = h.aux, &pre = h.pre, &pre_bwd = h.pre_bwd, &dir = h.dir, &dir_b1 = h.dir_b1,
+                         &dir_b2 = h.dir_b2, &pre_w = h.pre_w, &bw1w = h.bw1w;
+    spingtp::Bw1wShape& bw1w_shape = h.bw1w_shape;
+    const spingtp::KernelEntry*& kw = h.kw;
+    bool &has_backward = h.has_backward, &same_bwd = h.same_bwd;
+    h.spin_mode = spin_mode;
+    h.dir_lds = dir_lds;
+    h.k = k;
+    h.kd = kd;
+    h.kv1 = kv1;
     try {
         if (spin_mode < 2 && !weighted && !spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab))
             return SPINGTP_ERR_INTERNAL;
@@ -1237,100 +1255,166 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     } catch (const std::bad_alloc&) {
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
-    std::vector<float> tabf(tab.size());
-    for (size_t i = 0; i < tab.size(); ++i) tabf[i] = static_cast<float>(tab[i]);  // round to nearest
+    return SPINGTP_OK;
+}
 
+// Device functions of the upload; plan creation passes HIP's, the host self-test its own.
+struct DeviceApi {
+    void* ctx;
+    int (*alloc)(void* ctx, void** p, size_t bytes);  // 0 ok, 1 out of memory, 2 other failure
+    int (*copy)(void* ctx, void* dst, const void* src, size_t bytes);
+    void (*release)(void* ctx, void* p);
+};
+
+// The device copies of a plan's tables; all null before a successful upload.
+struct PlanDevice {
+    float *tab = nullptr, *tab_bwd = nullptr;
+    uint32_t *aux = nullptr, *pre = nullptr, *pre_bwd = nullptr, *dir = nullptr, *dir_b1 = nullptr,
+             *dir_b2 = nullptr, *pre_w = nullptr, *bw1w = nullptr;
+};
+
+// Uploads every non-empty table (fp32 tables rounded to nearest).  On any failure every
+// buffer allocated so far is released and d is left all null: nothing leaks.
+spingtp_status upload_plan(const PlanHost& h, const DeviceApi& api, PlanDevice& d) {
+    d = PlanDevice{};
+    std::vector<void*> held;
+    int fail = 0;
+    auto put = [&](const void* src, size_t bytes, void** dst) {
+        if (fail != 0 || bytes == 0) return;
+        void* p = nullptr;
+        fail = api.alloc(api.ctx, &p, bytes);
+        if (fail != 0) return;
+        held.push_back(p);
+        if (api.copy(api.ctx, p, src, bytes) != 0) fail = 2;
+        *dst = p;
+    };
+    try {
+        std::vector<float> f(h.tab.size());
+        for (size_t i = 0; i < f.size(); ++i) f[i] = static_cast<float>(h.tab[i]);
+        put(f.data(), f.size() * sizeof(float), reinterpret_cast<void**>(&d.tab));
+        if (h.has_backward && !h.same_bwd) {
+            f.assign(h.tab_bwd.size(), 0.f);
+            for (size_t i = 0; i < f.size(); ++i) f[i] = static_cast<float>(h.tab_bwd[i]);
+            put(f.data(), f.size() * sizeof(float), reinterpret_cast<void**>(&d.tab_bwd));
+        }
+    } catch (const std::bad_alloc&) {
+        fail = 1;
+    }
+    const std::pair<const std::vector<uint32_t>*, uint32_t**> words[] = {
+        {&h.aux, &d.aux}, {&h.pre, &d.pre}, {&h.pre_bwd, &d.pre_bwd}, {&h.dir, &d.dir}, {&h.dir_b1, &d.dir_b1},
+        {&h.dir_b2, &d.dir_b2}, {&h.pre_w, &d.pre_w}, {&h.bw1w, &d.bw1w}};
+    for (const auto& w : words)
+        put(w.first->data(), w.first->size() * sizeof(uint32_t), reinterpret_cast<void**>(w.second));
+    if (fail == 0) return SPINGTP_OK;
+    for (void* p : held) api.release(api.ctx, p);
+    d = PlanDevice{};
+    return fail == 1 ? SPINGTP_ERR_OUT_OF_MEMORY : SPINGTP_ERR_HIP;
+}
+
+int hip_alloc(void*, void** p, size_t bytes) {
+    const hipError_t e = hipMalloc(p, bytes);
+    return e == hipSuccess ? 0 : (e == hipErrorOutOfMemory ? 1 : 2);
+}
+int hip_copy(void*, void* dst, const void* src, size_t bytes) {
+    return hipMemcpy(dst, src, bytes, hipMemcpyHostToDevice) == hipSuccess ? 0 : 2;
+}
+void hip_release(void*, void* p) {
+    (void)hipFree(p);
+}
+
+}  // namespace
+
+static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, int n_spins, spingtp_dtype dtype,
+                                  unsigned flags, const double* weights, size_t n_weights, spingtp_plan* out_plan) {
+    if (out_plan == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    *out_plan = nullptr;
+    PlanHost h;
+    const spingtp_status st = build_plan_host(L1, L2, Lout, spins, n_spins, dtype, flags, weights, n_weights, h);
+    if (st != SPINGTP_OK) return st;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return SPINGTP_ERR_HIP;
-    float* d = nullptr;
-    hipError_t e = hipSuccess;
-    if (!tabf.empty()) {
-        e = hipMalloc(&d, tabf.size() * sizeof(float));
-        if (e == hipErrorOutOfMemory) return SPINGTP_ERR_OUT_OF_MEMORY;
-        if (e != hipSuccess) return SPINGTP_ERR_HIP;
-        if (hipMemcpy(d, tabf.data(), tabf.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess) {
-            (void)hipFree(d);
-            return SPINGTP_ERR_HIP;
-        }
-    }
-    // device copy of a host word table; nullptr for an empty one
-    auto upload = [](const std::vector<uint32_t>& h, uint32_t** dp) -> hipError_t {
-        *dp = nullptr;
-        if (h.empty()) return hipSuccess;
-        hipError_t err = hipMalloc(dp, h.size() * sizeof(uint32_t));
-        if (err == hipSuccess) err = hipMemcpy(*dp, h.data(), h.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
-        if (err != hipSuccess && *dp != nullptr) {
-            (void)hipFree(*dp);
-            *dp = nullptr;
-        }
-        return err;
-    };
-    uint32_t *da = nullptr, *dpre = nullptr, *dpreb = nullptr, *ddir = nullptr, *ddir1 = nullptr, *ddir2 = nullptr;
-    float* dbwd = nullptr;
-    e = upload(aux, &da);
-    if (e == hipSuccess) e = upload(pre, &dpre);
-    if (e == hipSuccess) e = upload(pre_bwd, &dpreb);
-    if (e == hipSuccess) e = upload(dir, &ddir);
-    if (e == hipSuccess) e = upload(dir_b1, &ddir1);
-    if (e == hipSuccess) e = upload(dir_b2, &ddir2);
-    uint32_t *dprew = nullptr, *dbw1w = nullptr;
-    if (e == hipSuccess) e = upload(pre_w, &dprew);
-    if (e == hipSuccess) e = upload(bw1w, &dbw1w);
-    if (e == hipSuccess && has_backward && !same_bwd) {
-        std::vector<float> f(tab_bwd.size());
-        for (size_t i = 0; i < tab_bwd.size(); ++i) f[i] = static_cast<float>(tab_bwd[i]);
-        e = hipMalloc(&dbwd, f.size() * sizeof(float));
-        if (e == hipSuccess) e = hipMemcpy(dbwd, f.data(), f.size() * sizeof(float), hipMemcpyHostToDevice);
-    }
-    auto release = [&]() {
-        if (da != nullptr) (void)hipFree(da);
-        if (dpre != nullptr) (void)hipFree(dpre);
-        if (dpreb != nullptr) (void)hipFree(dpreb);
-        if (dbwd != nullptr) (void)hipFree(dbwd);
-        if (ddir != nullptr) (void)hipFree(ddir);
-        if (ddir1 != nullptr) (void)hipFree(ddir1);
-        if (ddir2 != nullptr) (void)hipFree(ddir2);
-        if (dprew != nullptr) (void)hipFree(dprew);
-        if (dbw1w != nullptr) (void)hipFree(dbw1w);
-        if (d != nullptr) (void)hipFree(d);
-    };
-    if (e != hipSuccess) {
-        release();
-        return e == hipErrorOutOfMemory ? SPINGTP_ERR_OUT_OF_MEMORY : SPINGTP_ERR_HIP;
-    }
+    PlanDevice d;
+    const DeviceApi api{nullptr, hip_alloc, hip_copy, hip_release};
+    const spingtp_status su = upload_plan(h, api, d);
+    if (su != SPINGTP_OK) return su;
     spingtp_plan p = new (std::nothrow) spingtp_plan_s;
     if (p == nullptr) {
-        release();
+        for (void* q : {static_cast<void*>(d.tab), static_cast<void*>(d.tab_bwd), static_cast<void*>(d.aux),
+                        static_cast<void*>(d.pre), static_cast<void*>(d.pre_bwd), static_cast<void*>(d.dir),
+                        static_cast<void*>(d.dir_b1), static_cast<void*>(d.dir_b2), static_cast<void*>(d.pre_w),
+                        static_cast<void*>(d.bw1w)})
+            if (q != nullptr) (void)hipFree(q);
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
     p->L1 = L1;
     p->L2 = L2;
     p->LO = Lout;
-    p->spin_mode = spin_mode;
+    p->spin_mode = h.spin_mode;
     p->n_spins = n_spins;
     p->dtype = dtype;
     p->flags = flags;
     p->device = dev;
-    p->d_tab = d;
-    p->n_tab = tabf.size();
-    p->d_aux = da;
-    p->d_pre = dpre;
-    p->d_pre_bwd = dpreb;
-    p->d_tab_bwd = has_backward ? (same_bwd ? d : dbwd) : nullptr;
-    p->own_tab_bwd = dbwd != nullptr;
-    p->d_dir = ddir;
-    p->d_dir_b1 = ddir1;
-    p->d_dir_b2 = ddir2;
-    p->kernel_dir = ddir1 != nullptr ? kd : nullptr;
-    p->dir_lds_floats = dir_lds;
-    p->d_pre_w = dprew;
-    p->kernel_v1w = dprew != nullptr ? kw : nullptr;
-    p->d_bw1w = dbw1w;
-    p->bw1w = bw1w_shape;
-    p->kernel = k;
-    p->kernel_v1 = kv1;
+    p->d_tab = d.tab;
+    p->n_tab = h.tab.size();
+    p->d_aux = d.aux;
+    p->d_pre = d.pre;
+    p->d_pre_bwd = d.pre_bwd;
+    p->d_tab_bwd = h.has_backward ? (h.same_bwd ? d.tab : d.tab_bwd) : nullptr;
+    p->own_tab_bwd = d.tab_bwd != nullptr;
+    p->d_dir = d.dir;
+    p->d_dir_b1 = d.dir_b1;
+    p->d_dir_b2 = d.dir_b2;
+    p->kernel_dir = d.dir_b1 != nullptr ? h.kd : nullptr;
+    p->dir_lds_floats = h.dir_lds;
+    p->d_pre_w = d.pre_w;
+    p->kernel_v1w = d.pre_w != nullptr ? h.kw : nullptr;
+    p->d_bw1w = d.bw1w;
+    p->bw1w = h.bw1w_shape;
+    p->kernel = h.k;
+    p->kernel_v1 = h.kv1;
     *out_plan = p;
     return SPINGTP_OK;
+}
+
+
+extern "C" spingtp_status spingtp_plan_upload_selftest_host(int L1, int L2, int Lout, const int* spins, int n_spins,
+                                                            spingtp_dtype dtype, unsigned flags, int fail_at,
+                                                            int* n_allocs, int* n_live) {
+    if (n_allocs == nullptr || n_live == nullptr) return SPINGTP_ERR_INVALID_ARG;
+    PlanHost h;
+    const spingtp_status st = build_plan_host(L1, L2, Lout, spins, n_spins, dtype, flags, nullptr, 0, h);
+    if (st != SPINGTP_OK) return st;
+    struct Counter {
+        int fail_at, allocs = 0, live = 0;
+    } c{fail_at};
+    const DeviceApi api{&c,
+                        [](void* ctx, void** p, size_t bytes) -> int {
+                            Counter& k = *static_cast<Counter*>(ctx);
+                            if (k.allocs++ == k.fail_at) return 1;
+                            *p = std::malloc(bytes);
+                            if (*p == nullptr) return 1;
+                            ++k.live;
+                            return 0;
+                        },
+                        [](void*, void* dst, const void* src, size_t bytes) -> int {
+                            std::memcpy(dst, src, bytes);
+                            return 0;
+                        },
+                        [](void* ctx, void* p) {
+                            --static_cast<Counter*>(ctx)->live;
+                            std::free(p);
+                        }};
+    PlanDevice d;
+    const spingtp_status su = upload_plan(h, api, d);
+    *n_allocs = c.allocs;
+    *n_live = c.live;
+    if (su == SPINGTP_OK)
+        for (void* q : {static_cast<void*>(d.tab), static_cast<void*>(d.tab_bwd), static_cast<void*>(d.aux),
+                        static_cast<void*>(d.pre), static_cast<void*>(d.pre_bwd), static_cast<void*>(d.dir),
+                        static_cast<void*>(d.dir_b1), static_cast<void*>(d.dir_b2), static_cast<void*>(d.pre_w),
+                        static_cast<void*>(d.bw1w)})
+            if (q != nullptr) api.release(api.ctx, q);
+    return su;
 }
 
 spingtp_status spingtp_plan_create(int L1, int L2, int Lout, const int* spins, int n_spins,

@@ -676,3 +676,32 @@ def test_weighted_backward_lists_reproduce_oracle(built_library, L1, L2, LO, spi
         v = w[:, 1].view(np.float32).astype(np.float64)
         y[:, :, k3] = (v * Wp[None, :, p] * X1[:, :, a] * X2[:, :, b]).sum(axis=-1)
     assert np.linalg.norm(y - ref) <= 1e-6 * np.linalg.norm(ref)
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,dtype,basis", [
+    (6, 6, 6, (-1, 0, 1), 0, 0),     # matrix-core plan: tables, backward tables, operand words
+    (2, 2, 2, (-1, 0, 1), 0, 2),     # precontracted v1 kernel and its conjugated table
+    (2, 2, 2, S5, 1, 1),             # direct kernel with its two gradient tables
+    (1, 3, 3, (-1, 0, 1), 0, 0),
+])
+def test_plan_upload_failure_releases_everything(built_library, L1, L2, LO, spins, dtype, basis):
+    """Plan creation's device upload, driven on the host with an allocator that fails at
+    each allocation in turn: the status is SPINGTP_ERR_OUT_OF_MEMORY and every buffer
+    allocated before the failure has been released."""
+    arr = (ctypes.c_int * len(spins))(*spins)
+    n_allocs, n_live = ctypes.c_int(-1), ctypes.c_int(-1)
+    st = built_library.spingtp_plan_upload_selftest_host(L1, L2, LO, arr, len(spins), dtype, basis, -1,
+                                                         ctypes.byref(n_allocs), ctypes.byref(n_live))
+    assert st == 0 and n_live.value == n_allocs.value   # a successful upload holds every buffer
+    total = n_allocs.value
+    assert total >= 2
+    for k in range(total):
+        st = built_library.spingtp_plan_upload_selftest_host(L1, L2, LO, arr, len(spins), dtype, basis, k,
+                                                             ctypes.byref(n_allocs), ctypes.byref(n_live))
+        assert st == 3, (k, st)              # SPINGTP_ERR_OUT_OF_MEMORY
+        assert n_allocs.value == k + 1       # nothing attempted after the failure
+        assert n_live.value == 0             # nothing leaked
+    # argument rules are those of spingtp_plan_create
+    bad = built_library.spingtp_plan_upload_selftest_host(17, 2, 2, arr, len(spins), dtype, basis, -1,
+                                                          ctypes.byref(n_allocs), ctypes.byref(n_live))
+    assert bad == 1
