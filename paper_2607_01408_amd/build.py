@@ -69,9 +69,9 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
 # host code checked by AddressSanitizer and UndefinedBehaviorSanitizer (device code is
 # built as usual: -Xarch_host applies the flags to the host compilation only)
 SANITIZED_SOURCES = ("plan.cpp", "api.cpp")
-SANITIZE_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
-                  "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
-                  "-Xarch_host", "-g"]
+SANITIZE_FLAGS = ("-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined "
+                  "-Xarch_host -fno-sanitize-recover=undefined -Xarch_host -fno-omit-frame-pointer "
+                  "-Xarch_host -g").split()
 
 
 def sanitizer_runtime() -> str:
@@ -97,7 +97,7 @@ def build_sanitized() -> str:
     for src in SOURCES:
         if src in SANITIZED_SOURCES:
             obj = os.path.join(sdir, os.path.splitext(src)[0] + ".o")
-            cmd = [hipcc(), "-x", "hip"] + HIP_FLAGS + SANITIZE_FLAGS + ["-I", os.path.join(ROOT, "include"), "-c",
+            cmd = [hipcc(), "-x", "hip"] + HIP_FLAGS + list(SANITIZE_FLAGS) + ["-I", os.path.join(ROOT, "include"), "-c",
                                                                         os.path.join(CSRC, src), "-o", obj]
             r = subprocess.run(cmd, capture_output=True, text=True)
             if r.returncode != 0:
