@@ -19,7 +19,9 @@ The oracle computes the plain definition of the operation and nothing else:
                    channel mode of App. E.1); ``vjp`` / ``spingtp_vjp`` give its
                    reverse-mode derivative by the chain rule on that definition;
                    ``PathWeightedTensor`` scales it by one weight per path
-                   (block triple) of eq. spin_gtp.
+                   (block triple) of eq. spin_gtp; ``channel_weighted*``,
+                   ``depthwise*`` and ``fully_connected*`` are the multiplicity
+                   modes uuu, uvu and uvw of App. E.1 and their derivatives.
 
 Readings of points where the paper is silent or ambiguous are listed in the
 docstrings of the functions that take them.  Every function here is pinned by
@@ -31,7 +33,8 @@ from .swsh import swsh, theta_part, goldberg_prefactor
 from .realbasis import q_matrix, real_index, conjugation_map, parity_mix, BASIS_PAPER, BASIS_M0_PAIRED, BASIS_PARITY
 from .gaunt import gauss_legendre_grid, gaunt_block, gaunt_full_quadrature
 from .spingtp import (RealGauntTensor, PathWeightedTensor, slot_blocks, spingtp, spingtp_vjp, channel_weighted_v1,
-                      channel_weighted_v1_vjp, channel_weighted, channel_weighted_vjp, depthwise, depthwise_vjp)
+                      channel_weighted_v1_vjp, channel_weighted, channel_weighted_vjp, depthwise, depthwise_vjp,
+                      fully_connected, fully_connected_vjp)
 
 __all__ = [
     "swsh", "theta_part", "goldberg_prefactor",
@@ -39,5 +42,5 @@ __all__ = [
     "gauss_legendre_grid", "gaunt_block", "gaunt_full_quadrature",
     "RealGauntTensor", "PathWeightedTensor", "slot_blocks", "spingtp", "spingtp_vjp",
     "channel_weighted_v1", "channel_weighted_v1_vjp", "channel_weighted", "channel_weighted_vjp",
-    "depthwise", "depthwise_vjp",
+    "depthwise", "depthwise_vjp", "fully_connected", "fully_connected_vjp",
 ]

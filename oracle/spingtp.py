@@ -397,3 +397,62 @@ def depthwise_vjp(x1, x2, weights, g, L1, L2, Lout, spins=(-1, 0, 1), basis=BASI
         gx2[:, v] = b.reshape(N, -1)
         gW[v] = c
     return gx1, gx2.reshape(x2.shape), gW.reshape(np.asarray(weights).shape)
+
+
+def fully_connected(x1, x2, weights, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Fully connected product (App. E.1 mode uvw, eq. spin_gtp): for every path p =
+    (rho1, rho2 -> rho3) first
+        R_p[n, u, v, k3] = sum_{(k1, k2, k3) in p} T[k1, k2, k3] x1[n, u, k1] x2[n, v, k2],
+    then the dense channel mixing
+        out[n, w, k3] = sum_p sum_{u, v} W[p, u, v, w] R_p[n, u, v, k3]   (k3 in rho3).
+    Paths and their order as in PathWeightedTensor.
+
+    x1 [N, U, ...] (n1 values per channel), x2 [N, V, ...] (n2), weights [P, U, V, W];
+    returns [N, W, n_spins, (Lout+1)^2]."""
+    spins = tuple(spins)
+    x1 = np.asarray(x1, dtype=np.float64)
+    N, U = x1.shape[:2]
+    X1 = x1.reshape(N, U, -1)
+    X2 = np.asarray(x2, dtype=np.float64).reshape(N, -1, len(spins) * (L2 + 1) ** 2)
+    V = X2.shape[1]
+    k1, k2, k3, val, path, n_paths = _path_entries(L1, L2, Lout, spins, basis)
+    Wt = np.asarray(weights, dtype=np.float64).reshape(n_paths, U, V, -1)
+    out = np.zeros((N, Wt.shape[3], len(spins) * (Lout + 1) ** 2))
+    for p in range(n_paths):
+        e = path == p
+        R = np.zeros((N, U, V, out.shape[2]))
+        for a, b, c, t in zip(k1[e], k2[e], k3[e], val[e]):
+            R[:, :, :, c] += t * X1[:, :, a, None] * X2[:, None, :, b]
+        out += np.einsum("nuvk,uvw->nwk", R, Wt[p])
+    return out.reshape((N, Wt.shape[3], len(spins), (Lout + 1) ** 2))
+
+
+def fully_connected_vjp(x1, x2, weights, g, L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """Reverse-mode derivative of fully_connected for dL/dout = g (float64), by the chain
+    rule through R_p and the mixing:
+      gR_p[n,u,v,k3] = sum_w W[p,u,v,w] g[n,w,k3],      gW[p,u,v,w] = sum_{n,k3 in p} R_p[n,u,v,k3] g[n,w,k3],
+      gx1[n,u,k1]    = sum_p sum_v sum_{(k1,k2,k3) in p} T x2[n,v,k2] gR_p[n,u,v,k3],
+      gx2[n,v,k2]    = sum_p sum_u sum_{(k1,k2,k3) in p} T x1[n,u,k1] gR_p[n,u,v,k3].
+    Returns (gx1, gx2, gW) shaped like x1, x2 and weights."""
+    spins = tuple(spins)
+    x1 = np.asarray(x1, dtype=np.float64)
+    x2 = np.asarray(x2, dtype=np.float64)
+    N, U = x1.shape[:2]
+    X1 = x1.reshape(N, U, -1)
+    X2 = x2.reshape(N, -1, len(spins) * (L2 + 1) ** 2)
+    V = X2.shape[1]
+    k1, k2, k3, val, path, n_paths = _path_entries(L1, L2, Lout, spins, basis)
+    Wt = np.asarray(weights, dtype=np.float64).reshape(n_paths, U, V, -1)
+    G = np.asarray(g, dtype=np.float64).reshape(N, Wt.shape[3], -1)
+    gx1, gx2, gW = np.zeros_like(X1), np.zeros_like(X2), np.zeros_like(Wt)
+    for p in range(n_paths):
+        e = path == p
+        R = np.zeros((N, U, V, G.shape[2]))
+        for a, b, c, t in zip(k1[e], k2[e], k3[e], val[e]):
+            R[:, :, :, c] += t * X1[:, :, a, None] * X2[:, None, :, b]
+        gW[p] = np.einsum("nuvk,nwk->uvw", R, G)
+        gR = np.einsum("uvw,nwk->nuvk", Wt[p], G)
+        for a, b, c, t in zip(k1[e], k2[e], k3[e], val[e]):
+            gx1[:, :, a] += t * (X2[:, None, :, b] * gR[:, :, :, c]).sum(axis=2)
+            gx2[:, :, b] += t * (X1[:, :, a, None] * gR[:, :, :, c]).sum(axis=1)
+    return gx1.reshape(x1.shape), gx2.reshape(x2.shape), gW.reshape(np.asarray(weights).shape)
