@@ -90,6 +90,8 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
 /* Also build the tables of spingtp_forward_v1_weighted (per-channel path weights),
  * OR-ed into the flags of spingtp_plan_create. */
 #define SPINGTP_CHANNEL_WEIGHTS 0x1000u
+/* plan also holds the entry table of spingtp_forward_fully_connected (mode uvw) */
+#define SPINGTP_FULLY_CONNECTED 0x2000u
 
 /* For spingtp_plan_tables_host only: return the tables spingtp_backward uses
  * (input 2's m = 0 mixing with the conjugation folded in). */
@@ -418,6 +420,24 @@ spingtp_status spingtp_backward_v1_noalloc(spingtp_plan plan, const void* x1, co
 spingtp_status spingtp_plan_upload_selftest_host(int L1, int L2, int Lout, const int* spins, int n_spins,
                                                  spingtp_dtype dtype, unsigned flags, int fail_at, int* n_allocs,
                                                  int* n_live);
+
+/*
+ * Fully connected product (mode uvw of App. E.1; Sec. 3.5 eq. spin_gtp), U channels of
+ * x1, V of x2, W of the output, one weight per (path, u, v, w):
+ *   R_p[n][u][v][m3] = sum over the nonzeros (k1, k2, m3) of path p of T x1[n][u][k1] x2[n][v][k2],
+ *   out[n][w][k3]    = sum_p sum_{u,v} weights[p][u][v][w] R_p[n][u][v][k3]  (k3 in p's output block),
+ * paths (block triples) numbered as by spingtp_paths_host.
+ *   x1 [N][U][n_spins][(L1+1)^2], x2 [N][V][n_spins][(L2+1)^2], fp32, 16-byte aligned;
+ *   weights [n_paths][U][V][W] fp32, 4-byte aligned; out [N][W][n_spins][(Lout+1)^2],
+ *   16-byte aligned, overwritten (0 in blocks no path reaches and in slots l < |s|).
+ *   N, U, V, W >= 0, U, V, W <= 65536, U V <= 2^24; N W = 0 is a no-op, U V = 0 writes 0.
+ * Needs an fp32 plan created with SPINGTP_FULLY_CONNECTED (else SPINGTP_ERR_UNSUPPORTED).
+ * Products and sums in fp32: the per-path products R on the vector ALU, the channel
+ * mixing on the matrix cores.  Asynchronous on `stream`, no allocation; deterministic.
+ */
+spingtp_status spingtp_forward_fully_connected(spingtp_plan plan, const void* x1, const void* x2,
+                                               const float* weights, void* out, int64_t N, int64_t U, int64_t V,
+                                               int64_t W, void* stream);
 
 /* Bytes of workspace spingtp_backward_v1 needs for grad_x2 with N x C units:
  * N C n_spins (L2+1)^2 elements of the plan's dtype.  SPINGTP_ERR_UNSUPPORTED as

@@ -201,6 +201,21 @@ void tensor_paths(int L1, int L2, int LO, const int* spins, int n_spins, const s
 void weight_paths(int L1, int L2, int LO, const int* spins, int n_spins, const std::vector<std::array<int, 3>>& paths,
                   const double* w, std::vector<double>& T);
 
+// Fully connected product (mode uvw): entry table of spingtp_forward_fully_connected.
+// Words: header [kUvwHeader]: n_paths, n_blocks (output blocks reached by a path), nc1,
+// nc2, nco, max_d3, first word of the path records, first word of the entries.
+// Then per block (4 words): slot offset o3 of the block in the output row, its width
+// d3, first path record, path count.  Per path record (4 words): path index (the
+// weights' leading index), d3, first word of its d3 + 1 entry offsets, 0.  The offsets
+// (absolute entry numbers) delimit its entries by output component m3; an entry is two
+// words: k1 | k2 << 16 and the fp32 value.
+constexpr int kUvwHeader = 8;
+constexpr int kUvwChunk = 8;  // output components per workgroup (the kernel's accumulators)
+bool build_uvw_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                     std::vector<uint32_t>& out, const std::vector<double>* dense = nullptr);
+hipError_t launch_fwd_uvw(const float* x1, const float* x2, const float* w, float* out, int64_t N, int U, int V,
+                          int W, const uint32_t* table, int n_blocks, int max_d3, int nco, hipStream_t stream);
+
 // Dense real tensor of the operation (see spingtp_dense_tensor_host), float64.
 void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
                         std::vector<double>& T);
@@ -230,6 +245,8 @@ struct spingtp_plan_s {
     uint32_t* d_dir_b2;  //   the gradients run on the direct kernel
     const spingtp::KernelEntry* kernel_dir;  // the direct kernel of d_dir_b1 and d_dir_b2
     int dir_lds_floats;  // LDS of the direct kernel's tiles (the same for its three tables)
+    uint32_t* d_uvw;  // entry table of spingtp_forward_fully_connected, nullptr unless SPINGTP_FULLY_CONNECTED
+    int uvw_blocks, uvw_max_d3;
     const spingtp::KernelEntry* kernel;     // spingtp_forward
     const spingtp::KernelEntry* kernel_v1;  // spingtp_forward_v1 (x2 shared by the channels of an edge)
 };

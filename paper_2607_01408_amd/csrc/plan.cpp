@@ -850,6 +850,93 @@ void weight_paths(int L1, int L2, int LO, const int* spins, int n_spins, const s
             }
 }
 
+bool build_uvw_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
+                     std::vector<uint32_t>& out, const std::vector<double>* dense) {
+    std::vector<double> own;
+    if (dense == nullptr) build_dense_tensor(L1, L2, LO, spins, n_spins, flags, own);
+    const std::vector<double>& T = dense != nullptr ? *dense : own;
+    std::vector<std::array<int, 3>> paths;
+    tensor_paths(L1, L2, LO, spins, n_spins, T, paths);
+    const std::vector<int> b1 = slot_blocks(L1, spins, n_spins), b2 = slot_blocks(L2, spins, n_spins),
+                           b3 = slot_blocks(LO, spins, n_spins);
+    const int nc1 = static_cast<int>(b1.size()), nc2 = static_cast<int>(b2.size()), nco = static_cast<int>(b3.size());
+    if (nc1 > 0xffff || nc2 > 0xffff) return false;
+    std::map<std::array<int, 3>, int> index;
+    for (size_t p = 0; p < paths.size(); ++p) index[paths[p]] = static_cast<int>(p);
+    // first slot and width of every output block
+    std::map<int, std::pair<int, int>> span;
+    for (int k = 0; k < nco; ++k)
+        if (b3[k] >= 0) {
+            auto it = span.find(b3[k]);
+            if (it == span.end()) span[b3[k]] = {k, 1};
+            else ++it->second.second;
+        }
+    // entries per path and output component
+    std::vector<std::vector<std::vector<std::pair<uint32_t, float>>>> ent(paths.size());
+    for (size_t p = 0; p < paths.size(); ++p) ent[p].resize(span.at(paths[p][2]).second);
+    for (int k1 = 0; k1 < nc1; ++k1)
+        for (int k2 = 0; k2 < nc2; ++k2)
+            for (int k3 = 0; k3 < nco; ++k3) {
+                const double v = T[(static_cast<size_t>(k1) * nc2 + k2) * nco + k3];
+                if (std::fabs(v) <= 1e-12) continue;
+                const int p = index.at({b1[k1], b2[k2], b3[k3]});
+                ent[p][k3 - span.at(b3[k3]).first].push_back(
+                    {static_cast<uint32_t>(k1) | (static_cast<uint32_t>(k2) << 16), static_cast<float>(v)});
+            }
+    // output blocks in slot order, each with its paths
+    std::vector<int> blocks;
+    for (const auto& kv : span) blocks.push_back(kv.first);
+    std::vector<std::vector<int>> by_block(blocks.size());
+    for (size_t p = 0; p < paths.size(); ++p)
+        by_block[std::lower_bound(blocks.begin(), blocks.end(), paths[p][2]) - blocks.begin()].push_back(
+            static_cast<int>(p));
+    std::vector<int> used;
+    for (size_t b = 0; b < blocks.size(); ++b)
+        if (!by_block[b].empty()) used.push_back(static_cast<int>(b));
+    int max_d3 = 0;
+    for (int b : used) max_d3 = std::max(max_d3, span.at(blocks[b]).second);
+    const size_t rec0 = kUvwHeader + 4 * used.size();
+    const size_t csr0 = rec0 + 4 * paths.size();
+    size_t n_csr = 0, n_ent = 0;
+    for (size_t p = 0; p < paths.size(); ++p) {
+        n_csr += ent[p].size() + 1;
+        for (const auto& e : ent[p]) n_ent += e.size();
+    }
+    const size_t ent0 = csr0 + n_csr;
+    out.assign(ent0 + 2 * n_ent, 0u);
+    const uint32_t hdr[kUvwHeader] = {static_cast<uint32_t>(paths.size()), static_cast<uint32_t>(used.size()),
+                                      static_cast<uint32_t>(nc1), static_cast<uint32_t>(nc2),
+                                      static_cast<uint32_t>(nco), static_cast<uint32_t>(max_d3),
+                                      static_cast<uint32_t>(rec0), static_cast<uint32_t>(ent0)};
+    std::copy(hdr, hdr + kUvwHeader, out.begin());
+    size_t rec = 0, csr = csr0, e_next = 0;
+    for (size_t i = 0; i < used.size(); ++i) {
+        const int b = used[i];
+        const auto sp = span.at(blocks[b]);
+        uint32_t* w = &out[kUvwHeader + 4 * i];
+        w[0] = static_cast<uint32_t>(sp.first);
+        w[1] = static_cast<uint32_t>(sp.second);
+        w[2] = static_cast<uint32_t>(rec);
+        w[3] = static_cast<uint32_t>(by_block[b].size());
+        for (int p : by_block[b]) {
+            uint32_t* r = &out[rec0 + 4 * rec++];
+            r[0] = static_cast<uint32_t>(p);
+            r[1] = static_cast<uint32_t>(sp.second);
+            r[2] = static_cast<uint32_t>(csr);
+            for (const auto& comp : ent[p]) {
+                out[csr++] = static_cast<uint32_t>(e_next);
+                for (const auto& e : comp) {
+                    out[ent0 + 2 * e_next] = e.first;
+                    std::memcpy(&out[ent0 + 2 * e_next + 1], &e.second, 4);
+                    ++e_next;
+                }
+            }
+            out[csr++] = static_cast<uint32_t>(e_next);
+        }
+    }
+    return true;
+}
+
 void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags, int role,
                         std::vector<uint32_t>& out, int* lds_floats, const std::vector<double>* dense) {
     std::vector<double> own;
@@ -930,8 +1017,8 @@ void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, u
 namespace {
 
 // flag bits that choose kernels, not the operation
-constexpr unsigned kRouteFlags =
-    SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER | SPINGTP_V1_PRECONTRACT | SPINGTP_CHANNEL_WEIGHTS;
+constexpr unsigned kRouteFlags = SPINGTP_KERNEL_VALU | SPINGTP_V1_FOURIER | SPINGTP_V1_PRECONTRACT |
+                                  SPINGTP_CHANNEL_WEIGHTS | SPINGTP_FULLY_CONNECTED;
 
 spingtp_status check_args(int L1, int L2, int Lout, const int* spins, int n_spins, unsigned flags,
                           int* spin_mode) {
@@ -1053,6 +1140,19 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
     int spin_mode = 0;
     const spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
+    if (flags & SPINGTP_FULLY_CONNECTED) {  // the entry table of spingtp_forward_fully_connected
+        try {
+            std::vector<uint32_t> w;
+            if (!spingtp::build_uvw_table(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, w))
+                return SPINGTP_ERR_UNSUPPORTED;
+            *count = w.size();
+            const size_t n = w.size() < capacity ? w.size() : capacity;
+            if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));
+        } catch (const std::bad_alloc&) {
+            return SPINGTP_ERR_OUT_OF_MEMORY;
+        }
+        return SPINGTP_OK;
+    }
     const bool channel_weights = (flags & SPINGTP_CHANNEL_WEIGHTS) != 0;
     if (!channel_weights && spingtp::find_pre_kernel(L1, L2, Lout, n_spins, 0) == nullptr)
         return SPINGTP_ERR_UNSUPPORTED;
@@ -1133,7 +1233,7 @@ struct PlanHost {
     int spin_mode = 0, dir_lds = 0;
     const spingtp::KernelEntry *k = nullptr, *kd = nullptr, *kv1 = nullptr, *kw = nullptr;
     std::vector<double> tab, tab_bwd;
-    std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2, pre_w, bw1w;
+    std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2, pre_w, bw1w, uvw;
     spingtp::Bw1wShape bw1w_shape{};
     bool has_backward = false, same_bwd = false;
 };
@@ -1239,6 +1339,9 @@ spingtp_status build_plan_host(int L1, int L2, int Lout, const int* spins, int n
             spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 2, dir_b2, &lds_floats, &dense);
         }
         if (k != nullptr && k->family == 4) spingtp::build_mfma_operands(L1, aux);
+        if ((flags & SPINGTP_FULLY_CONNECTED) &&
+            !spingtp::build_uvw_table(L1, L2, Lout, spins, n_spins, basis, h.uvw, dense.empty() ? nullptr : &dense))
+            return SPINGTP_ERR_UNSUPPORTED;
         if (kv1->family == 5 &&
             !spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre, false, weighted ? &dense : nullptr))
             return SPINGTP_ERR_INTERNAL;
@@ -1270,7 +1373,7 @@ struct DeviceApi {
 struct PlanDevice {
     float *tab = nullptr, *tab_bwd = nullptr;
     uint32_t *aux = nullptr, *pre = nullptr, *pre_bwd = nullptr, *dir = nullptr, *dir_b1 = nullptr,
-             *dir_b2 = nullptr, *pre_w = nullptr, *bw1w = nullptr;
+             *dir_b2 = nullptr, *pre_w = nullptr, *bw1w = nullptr, *uvw = nullptr;
 };
 
 // Uploads every non-empty table (fp32 tables rounded to nearest).  On any failure every
@@ -1302,7 +1405,7 @@ spingtp_status upload_plan(const PlanHost& h, const DeviceApi& api, PlanDevice& 
     }
     const std::pair<const std::vector<uint32_t>*, uint32_t**> words[] = {
         {&h.aux, &d.aux}, {&h.pre, &d.pre}, {&h.pre_bwd, &d.pre_bwd}, {&h.dir, &d.dir}, {&h.dir_b1, &d.dir_b1},
-        {&h.dir_b2, &d.dir_b2}, {&h.pre_w, &d.pre_w}, {&h.bw1w, &d.bw1w}};
+        {&h.dir_b2, &d.dir_b2}, {&h.pre_w, &d.pre_w}, {&h.bw1w, &d.bw1w}, {&h.uvw, &d.uvw}};
     for (const auto& w : words)
         put(w.first->data(), w.first->size() * sizeof(uint32_t), reinterpret_cast<void**>(w.second));
     if (fail == 0) return SPINGTP_OK;
@@ -1342,7 +1445,7 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
         for (void* q : {static_cast<void*>(d.tab), static_cast<void*>(d.tab_bwd), static_cast<void*>(d.aux),
                         static_cast<void*>(d.pre), static_cast<void*>(d.pre_bwd), static_cast<void*>(d.dir),
                         static_cast<void*>(d.dir_b1), static_cast<void*>(d.dir_b2), static_cast<void*>(d.pre_w),
-                        static_cast<void*>(d.bw1w)})
+                        static_cast<void*>(d.bw1w), static_cast<void*>(d.uvw)})
             if (q != nullptr) (void)hipFree(q);
         return SPINGTP_ERR_OUT_OF_MEMORY;
     }
@@ -1370,6 +1473,9 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     p->kernel_v1w = d.pre_w != nullptr ? h.kw : nullptr;
     p->d_bw1w = d.bw1w;
     p->bw1w = h.bw1w_shape;
+    p->d_uvw = d.uvw;
+    p->uvw_blocks = h.uvw.empty() ? 0 : static_cast<int>(h.uvw[1]);
+    p->uvw_max_d3 = h.uvw.empty() ? 0 : static_cast<int>(h.uvw[5]);
     p->kernel = h.k;
     p->kernel_v1 = h.kv1;
     *out_plan = p;
@@ -1412,7 +1518,7 @@ extern "C" spingtp_status spingtp_plan_upload_selftest_host(int L1, int L2, int 
         for (void* q : {static_cast<void*>(d.tab), static_cast<void*>(d.tab_bwd), static_cast<void*>(d.aux),
                         static_cast<void*>(d.pre), static_cast<void*>(d.pre_bwd), static_cast<void*>(d.dir),
                         static_cast<void*>(d.dir_b1), static_cast<void*>(d.dir_b2), static_cast<void*>(d.pre_w),
-                        static_cast<void*>(d.bw1w)})
+                        static_cast<void*>(d.bw1w), static_cast<void*>(d.uvw)})
             if (q != nullptr) api.release(api.ctx, q);
     return su;
 }
@@ -1474,6 +1580,7 @@ spingtp_status spingtp_plan_destroy(spingtp_plan plan) {
     release(plan->d_bw1w);
     release(plan->d_pre);
     release(plan->d_pre_bwd);
+    release(plan->d_uvw);
     if (plan->own_tab_bwd) release(plan->d_tab_bwd);
     if (switched) (void)hipSetDevice(cur);
     delete plan;

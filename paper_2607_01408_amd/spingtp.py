@@ -15,6 +15,7 @@ BASIS_M0_PAIRED = 1
 BASIS_PARITY = 2
 KERNEL_VALU = 0x100  # force the fp32 vector-ALU kernels (spingtp.h)
 CHANNEL_WEIGHTS = 0x1000  # also build the per-channel path-weighted table (spingtp.h)
+FULLY_CONNECTED = 0x2000  # also build the entry table of the fully connected product (spingtp.h)
 V1_FOURIER = 0x200  # spingtp_forward_v1 on the Fourier route (spingtp.h)
 V1_PRECONTRACT = 0x400  # spingtp_forward_v1 on the precontracted kernel wherever it is built
 FP32 = 0
@@ -62,6 +63,19 @@ def mfma_operands_host(L):
     out = np.zeros(count.value, dtype=np.uint32)
     _lib.check(_lib.lib().spingtp_mfma_operands_host(L, out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
                                                      out.size, ctypes.byref(count)), "spingtp_mfma_operands_host")
+    return out
+
+
+def uvw_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
+    """spingtp_pre_table_host with SPINGTP_FULLY_CONNECTED: the entry table of the fully connected product."""
+    arr, n = _spin_array(spins)
+    count = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, basis | FULLY_CONNECTED, None, 0,
+                                                 ctypes.byref(count)), "spingtp_pre_table_host")
+    out = np.zeros(count.value, dtype=np.uint32)
+    _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, basis | FULLY_CONNECTED,
+                                                 out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), out.size,
+                                                 ctypes.byref(count)), "spingtp_pre_table_host")
     return out
 
 
@@ -131,7 +145,8 @@ class Plan:
     """
 
     def __init__(self, L1, L2, Lout, spins=(-1, 0, 1), dtype="fp32", basis=BASIS_PAPER, valu_only=False,
-                 v1_fourier=False, v1_precontract=False, weights=None, channel_weights=False):
+                 v1_fourier=False, v1_precontract=False, weights=None, channel_weights=False,
+                 fully_connected=False):
         import torch  # device memory and streams only
 
         self.L1, self.L2, self.Lout = int(L1), int(L2), int(Lout)
@@ -146,7 +161,8 @@ class Plan:
         arr, n = _spin_array(self.spins)
         code = FP32 if self.dtype_name == "fp32" else BF16
         flags = (self.basis | (KERNEL_VALU if self.valu_only else 0) | (V1_FOURIER if self.v1_fourier else 0)
-                 | (V1_PRECONTRACT if self.v1_precontract else 0) | (CHANNEL_WEIGHTS if channel_weights else 0))
+                 | (V1_PRECONTRACT if self.v1_precontract else 0) | (CHANNEL_WEIGHTS if channel_weights else 0)
+                 | (FULLY_CONNECTED if fully_connected else 0))
         if weights is None:
             _lib.check(_lib.lib().spingtp_plan_create(self.L1, self.L2, self.Lout, arr, n, code, flags,
                                                       ctypes.byref(self._handle)), "spingtp_plan_create")
@@ -157,7 +173,8 @@ class Plan:
                 w.size, ctypes.byref(self._handle)), "spingtp_plan_create_weighted")
         self.device = torch.cuda.current_device()
         # paths of the per-channel weights (their count bounds the kernel's reads of a weight row)
-        self.n_paths = len(paths_host(self.L1, self.L2, self.Lout, self.spins, self.basis)) if channel_weights else 0
+        self.n_paths = (len(paths_host(self.L1, self.L2, self.Lout, self.spins, self.basis))
+                        if channel_weights or fully_connected else 0)
 
     @property
     def handle(self):
@@ -422,6 +439,33 @@ class Plan:
             raise ValueError(f"weights must be a contiguous fp32 [V, C, {self.n_paths}] tensor on the inputs' "
                              "device (a plan created with channel_weights=True)")
         return N, C, V
+
+    def forward_fully_connected(self, x1, x2, weights, out=None, stream=None):
+        """spingtp_forward_fully_connected (mode uvw): x1 [N, U, ...], x2 [N, V, ...], weights
+        [n_paths, U, V, W] fp32 -> out [N, W, ...]; plan created with fully_connected=True."""
+        import torch
+
+        if x1.dim() != 4 or x2.dim() != 4 or weights.dim() != 4:
+            raise ValueError("x1 [N, U, ...], x2 [N, V, ...], weights [n_paths, U, V, W]")
+        N, U, V, W = x1.shape[0], x1.shape[1], x2.shape[1], weights.shape[3]
+        for t, shape in ((x1, (N, U) + tuple(self.shape_in(1))), (x2, (N, V) + tuple(self.shape_in(2)))):
+            if tuple(t.shape) != shape or t.dtype != self.torch_dtype or not t.is_cuda or not t.is_contiguous():
+                raise ValueError("x1, x2 must be contiguous device tensors of the plan's dtype and shape")
+        if (tuple(weights.shape) != (self.n_paths, U, V, W) or weights.dtype != torch.float32 or not weights.is_cuda
+                or not weights.is_contiguous()):
+            raise ValueError(f"weights must be a contiguous fp32 device tensor [{self.n_paths}, U, V, W]")
+        if out is None:
+            out = torch.empty((N, W) + self.shape_out, dtype=self.torch_dtype, device=x1.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+
+        def ptr(t):
+            return t.data_ptr() if t.numel() else None
+
+        _lib.check(_lib.lib().spingtp_forward_fully_connected(self._handle, ptr(x1), ptr(x2), ptr(weights), ptr(out),
+                                                              N, U, V, W, ctypes.c_void_p(stream.cuda_stream)),
+                   "spingtp_forward_fully_connected")
+        return out
 
     def forward_depthwise(self, x1, x2, weights, out=None, stream=None):
         """spingtp_forward_depthwise: x2 [N, V, ...] with V >= 1 channels per edge, weights [V, C, n_paths]."""

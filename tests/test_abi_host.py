@@ -705,3 +705,52 @@ def test_plan_upload_failure_releases_everything(built_library, L1, L2, LO, spin
     bad = built_library.spingtp_plan_upload_selftest_host(17, 2, 2, arr, len(spins), dtype, basis, -1,
                                                           ctypes.byref(n_allocs), ctypes.byref(n_live))
     assert bad == 1
+
+
+def emulate_uvw_table(words, x1, x2, W, nco):
+    """float64 re-enactment of spingtp_forward_fully_connected from its entry table: per
+    output block and path, R from the entries (k1 | k2 << 16, value) of each component,
+    then the channel mixing with the path's weights."""
+    w = np.asarray(words, dtype=np.uint32)
+    n_paths, n_blocks, nc1, nc2, nco_t, max_d3, rec0, ent0 = (int(v) for v in w[:8])
+    assert nco_t == nco
+    vals = w.view(np.float32)
+    N, U, V = x1.shape[0], x1.shape[1], x2.shape[1]
+    out = np.zeros((N, W.shape[3], nco))
+    seen = set()
+    for b in range(n_blocks):
+        o3, d3, first, count = (int(v) for v in w[8 + 4 * b:12 + 4 * b])
+        assert d3 <= max_d3
+        for r in range(first, first + count):
+            pid, d3r, csr = (int(v) for v in w[rec0 + 4 * r:rec0 + 4 * r + 3])
+            assert d3r == d3 and pid not in seen
+            seen.add(pid)
+            for m3 in range(d3):
+                for k in range(int(w[csr + m3]), int(w[csr + m3 + 1])):
+                    ix = int(w[ent0 + 2 * k])
+                    t = float(vals[ent0 + 2 * k + 1])
+                    R = t * x1[:, :, ix & 0xFFFF, None] * x2[:, None, :, ix >> 16]      # [N, U, V]
+                    out[:, :, o3 + m3] += np.einsum("nuv,uvw->nw", R, W[pid])
+    assert seen == set(range(n_paths))
+    return out
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [
+    (1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 2), (1, 3, 3, (-1, 0, 1), 1),
+    (2, 1, 2, (0,), 0), (2, 2, 2, S5, 2),
+])
+def test_uvw_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
+    """The fully connected product's entry table, re-enacted in float64: every path
+    appears once under its output block, and the result matches the oracle's uvw mode."""
+    from paper_2607_01408_amd.spingtp import uvw_table_host
+    words = uvw_table_host(L1, L2, LO, spins, basis)
+    rng = np.random.default_rng(L1 + 10 * L2 + 100 * LO + basis)
+    N, U, V, Wc = 3, 3, 2, 4
+    x1 = rng.standard_normal((N, U, len(spins) * (L1 + 1) ** 2)) * valid_mask(spins, L1)
+    x2 = rng.standard_normal((N, V, len(spins) * (L2 + 1) ** 2)) * valid_mask(spins, L2)
+    P = len(oracle.PathWeightedTensor(L1, L2, LO, spins, basis).paths)
+    W = rng.standard_normal((P, U, V, Wc))
+    nco = len(spins) * (LO + 1) ** 2
+    y = emulate_uvw_table(words, x1, x2, W, nco)
+    yo = oracle.fully_connected(x1, x2, W, L1, L2, LO, spins, basis).reshape(N, Wc, -1)
+    assert np.abs(y - yo).max() <= 1e-6 * max(1.0, np.abs(yo).max())
