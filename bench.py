@@ -705,18 +705,22 @@ def run_backward(args):
 
 
 def run_sweep(args):
-    """The degree sweep: SpinGTP kernel vs the direct O(L^6) dense contraction.
+    """The degree sweep: SpinGTP kernel vs two direct O(L^6) Clebsch-Gordan contractions.
 
-    The comparator forms x1 (x) x2 per unit and contracts it with the explicit
-    dense real tensor T (spingtp_dense_tensor_host) as one fp32 GEMM on the GPU
-    (hipBLASLt through torch): the Clebsch-Gordan-style direct product on the same
-    inputs.  Its time is measured on up to 32,768 units and scaled to the job.
+    * dense-T GEMM: x1 (x) x2 per unit contracted with the explicit dense real tensor T
+      (spingtp_dense_tensor_host) as one fp32 GEMM (2 NC^3 + NC^2 flops per unit);
+    * per-path CG: for every path (block triple rho1, rho2 -> rho3 with a nonzero entry,
+      spingtp_paths_host) the dense block of T times the outer product of the two input
+      blocks (2 d1 d2 d3 + d1 d2 flops per unit and path, the scope table's O(L^6) count
+      within a few per cent); paths of equal block shape run as one batched fp32 GEMM.
+    Both run through torch (hipBLASLt / rocBLAS) on up to 32,768 units, scaled to the job,
+    and are checked against the kernel's output.
     """
     import numpy as np
     import torch
 
     import oracle
-    from paper_2607_01408_amd import Plan, dense_tensor_host, workloads
+    from paper_2607_01408_amd import Plan, dense_tensor_host, paths_host, workloads
 
     torch.cuda.set_device(0)
     torch.backends.cuda.matmul.allow_tf32 = False
@@ -759,6 +763,54 @@ def run_sweep(args):
         ms_cg = s.elapsed_time(e) * U / ucg
         ref = out.view(U, NC)[:ucg]
         cg_vs_kernel = float(torch.linalg.norm(ycg - ref) / torch.linalg.norm(ref))
+        del T
+        torch.cuda.empty_cache()
+
+        # per-path CG: group the paths by block shape (d1, d2, d3)
+        Td = dense_tensor_host(L, L, L)
+        paths = paths_host(L, L, L, workloads.SPINS, 0)
+        nb = L + 1
+
+        def slots(b):  # block id = spin index * (L + 1) + degree
+            si, l = divmod(int(b), nb)
+            o = si * nb * nb + l * l
+            return np.arange(o, o + 2 * l + 1)
+
+        groups = {}
+        for b1, b2, b3 in paths:
+            key = (2 * int(b1 % nb) + 1, 2 * int(b2 % nb) + 1, 2 * int(b3 % nb) + 1)
+            groups.setdefault(key, []).append((b1, b2, b3))
+        plan_g = []
+        path_flops = 0
+        for (d1, d2, d3), ps in groups.items():
+            i1 = torch.as_tensor(np.stack([slots(p[0]) for p in ps]), device="cuda:0")      # [n, d1]
+            i2 = torch.as_tensor(np.stack([slots(p[1]) for p in ps]), device="cuda:0")      # [n, d2]
+            i3 = torch.as_tensor(np.concatenate([slots(p[2]) for p in ps]), device="cuda:0")  # [n d3]
+            blk = np.stack([Td[np.ix_(slots(p[0]), slots(p[1]), slots(p[2]))].reshape(d1 * d2, d3) for p in ps])
+            plan_g.append((i1, i2, i3, torch.from_numpy(blk.astype(np.float32)).to("cuda:0")))
+            path_flops += int(len(ps) * (2 * d1 * d2 * d3 + d1 * d2))
+        upc = min(ucg, max(256, (1 << 28) // max(1, 4 * max(len(g[3]) * g[3].shape[1] for g in plan_g))))
+        ypc = torch.zeros((upc, NC), device="cuda:0")
+
+        def cg_paths():
+            ypc.zero_()
+            for i1, i2, i3, blk in plan_g:
+                n, dd, d3 = blk.shape
+                a = X1[:upc][:, i1]                                                   # [U, n, d1]
+                b = X2[:upc][:, i2]                                                   # [U, n, d2]
+                P = (a[:, :, :, None] * b[:, :, None, :]).reshape(upc, n, dd).transpose(0, 1).contiguous()
+                yb = torch.bmm(P, blk)                                                # [n, U, d3]
+                ypc.index_add_(1, i3, yb.transpose(0, 1).reshape(upc, n * d3))
+
+        cg_paths()
+        torch.cuda.synchronize()
+        s.record()
+        cg_paths()
+        e.record()
+        torch.cuda.synchronize()
+        ms_cgp = s.elapsed_time(e) * U / upc
+        cgp_vs_kernel = float(torch.linalg.norm(ypc - out.view(U, NC)[:upc]) / torch.linalg.norm(out.view(U, NC)[:upc]))
+        del plan_g
 
         n_or = 256 if L <= 8 else 64
         idx = torch.arange(n_or, device="cuda:0")
@@ -771,17 +823,23 @@ def run_sweep(args):
         to = (time.perf_counter() - t0) / n_or
         parity = float(np.linalg.norm(ref[:n_or].double().cpu().numpy() - yo) / np.linalg.norm(yo))
         fl = route_flops(L, L, L, True)
+        fam = plan.kernel_info()["family"]
+        rf = roofline(fam, L, "fp32", U, ms, hbm_bytes_per_unit(L, L, L, "fp32"))
         rows.append({
             "L": L, "units": U, "ms": ms, "tp_per_s": U / (ms / 1e3),
-            "kernel_family": plan.kernel_info()["family"],
+            "kernel_family": fam,
             "route_flops_per_unit": fl, "achieved_tflops": fl * U / (ms / 1e3) / 1e12,
+            "roofline": {k: rf[k] for k in ("bound", "frac", "fracs", "floors_ms")},
             "cg_dense_ms": ms_cg, "cg_dense_flops_per_unit": 2 * NC ** 3 + NC ** 2,
             "cg_dense_vs_kernel_rel_l2": cg_vs_kernel, "speedup_vs_cg_dense": ms_cg / ms,
+            "cg_path_ms": ms_cgp, "cg_path_flops_per_unit": path_flops, "cg_path_paths": int(len(paths)),
+            "cg_path_tflops": path_flops * U / (ms_cgp / 1e3) / 1e12,
+            "cg_path_vs_kernel_rel_l2": cgp_vs_kernel, "speedup_vs_cg_path": ms_cgp / ms,
             "oracle_cpu_s_per_unit": to, "oracle_tensor_build_s": tb, "parity_rel_l2": parity,
         })
-        print(f"[sweep] L={L} {ms:.3f} ms ({U / (ms / 1e3):.3e} TP/s), dense CG {ms_cg:.1f} ms, "
-              f"parity {parity:.2e}", file=sys.stderr, flush=True)
-        del T, x1, x2, out, ycg
+        print(f"[sweep] L={L} {ms:.3f} ms ({U / (ms / 1e3):.3e} TP/s), dense-T CG {ms_cg:.1f} ms, per-path CG "
+              f"{ms_cgp:.1f} ms, parity {parity:.2e}", file=sys.stderr, flush=True)
+        del x1, x2, out, ycg, ypc
         torch.cuda.empty_cache()
     last = rows[-1]
     print(json.dumps({
