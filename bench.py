@@ -87,16 +87,18 @@ def route_flops(L1, L2, LO, spin=True):
 
 def mfma_flops_executed(family, L, dtype):
     """fp16 matrix-core flops one unit costs on the matrix-core kernel, as executed: per wave
-    (32 units) and Gauss node, step (B) is six 32x32x16 products and step (D) three per
-    16-point K block, each repeated three times for the hi/lo split of fp32 I/O; all padding
-    (19 of 32 rows, 13 of 16 slots at L = 6) is counted."""
+    (32 units) and Gauss node, step (B) is six 32x32x16 products per 16-slot K block (two
+    blocks at L = 8, the second for cos 8 alone) and step (D) three per 16-point K block,
+    each repeated three times for the hi/lo split of fp32 I/O; all padding (19 of 32 rows,
+    13 of 16 slots at L = 6) is counted."""
     if family != 4:
         return 0
     NT = (3 * L + 2) // 2
     NP = 3 * L + 1
     NB = (NP + 15) // 16
+    KB = 2 if L >= 8 else 1
     split = 3 if dtype == "fp32" else 1
-    per_wave_node = (6 + 3 * NB) * split
+    per_wave_node = (6 * KB + 3 * NB) * split
     return per_wave_node * (32 * 32 * 16 * 2) * NT // 32
 
 

@@ -70,11 +70,15 @@ struct MShape {
     static constexpr int SCALE = REGION;        // 2 x UNITS power-of-two exponents
     static constexpr int LDS_FLOATS = REGION + 2 * UNITS;
     static constexpr int NB = (NP + 15) / 16;   // K blocks of step (D)
+    static constexpr int KB = L >= 8 ? 2 : 1;   // K blocks of step (B): cos 8 in the second
     static constexpr int NPW = (NT + 1) / 2;    // nodes per wave
     static constexpr int TB_WORDS = 64 * 8;     // one lane: 4 words hi, 4 words lo
-    static_assert(L >= 1 && L <= 7, "a polynomial's cos/sin slots must fit one 16-wide K block");
+    // waves per SIMD the register budget is sized for: two workgroups per CU while
+    // both tiles fit half the LDS, else one (L >= 7)
+    static constexpr int OCC = LDS_FLOATS * 4 <= 80 * 1024 ? 2 : 1;
+    static_assert(L >= 1 && L <= 8, "cos 0..7 and sin 1..8 share the first K block; only cos 8 takes a second");
     static_assert(NP <= 32, "the phi points must fit the 32 rows of one step-(B) tile");
-    static_assert(LDS_FLOATS * 4 <= 80 * 1024, "two workgroups per CU");
+    static_assert(LDS_FLOATS * 4 <= 160 * 1024, "the tiles must fit the LDS of a CU");
     // step-(B) accumulator position v holds point 8 (v/4) + 4h + v%4; it carries a
     // point (for h = 0, hence possibly for h = 1) when that row is < n_phi
     __host__ __device__ static constexpr bool holds_point(int v) { return 8 * (v / 4) + (v % 4) < NP; }
@@ -265,7 +269,7 @@ __device__ __forceinline__ void store_out(uint16_t* __restrict__ dst, int nvalid
 
 // SPLIT = 3: hi*hi + hi*lo + lo*hi (fp32 I/O); SPLIT = 1: hi*hi (bf16 I/O).
 template <int L, typename TIO, int SPLIT, bool BWD>
-__global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __restrict__ x1,
+__global__ __launch_bounds__(256, MShape<L>::OCC) void spingtp_fwd_mfma_kernel(const TIO* __restrict__ x1,
                                                                    const TIO* __restrict__ x2,
                                                                    TIO* __restrict__ out, int64_t units,
                                                                    int64_t cpx2, const float* __restrict__ tab,
@@ -356,6 +360,9 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
     const v4u* __restrict__ ops = reinterpret_cast<const v4u*>(aux);
     const v8h TBh = __builtin_bit_cast(v8h, ops[2 * lane]);
     const v8h TBl = __builtin_bit_cast(v8h, ops[2 * lane + 1]);
+    constexpr int TB2 = 2 * 64 * (1 + 2 * NB);  // the second step-(B) block (L = 8), in v4u
+    const v8h TB2h = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 2 * lane]) : v8h{};
+    const v8h TB2l = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 2 * lane + 1]) : v8h{};
     const v16f zero16 = {};
 
     // output accumulators of this lane: m3 >= 0 (h = 0) or m3 < 0 (h = 1)
@@ -378,8 +385,9 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
         coef_to_theta_fourier<L, L, true>(xr, tb, tab + Y.n0, BWD && h != 0, Pc[0], Ps[0], Pc[1], Ps[1], Pc[2],
                                           Ps[2], dl, ep);
 
-        // step-(B) operands of the three polynomials of both inputs
-        v8h oh[2][3], ol[2][3];
+        // step-(B) operands of the three polynomials of both inputs (L = 8: sin 8
+        // in the sin 0 slot, cos 8 alone in a second K block)
+        v8h oh[2][3], ol[2][3], oh2[2][3], ol2[2][3];
 #pragma unroll
         for (int p = 0; p < 3; ++p) {
             float cv[8], sv[8];
@@ -387,15 +395,26 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 cl_[e] = e <= L;
-                sl_[e] = e >= 1 && e <= L;
+                sl_[e] = (e >= 1 && e <= L) || (e == 0 && L >= 8);
                 cv[e] = cl_[e] ? Pc[p][e] : 0.f;
-                sv[e] = sl_[e] ? Ps[p][e] : 0.f;
+                sv[e] = sl_[e] ? Ps[p][e == 0 ? (L >= 8 ? 8 : 0) : e] : 0.f;
             }
             v8h ch, cl, sh, sl;
             split8<SPLIT>(cv, cl_, ch, cl);
             split8<SPLIT>(sv, sl_, sh, sl);
             swap_halves(ch, sh, oh[0][p], oh[1][p]);
             if constexpr (SPLIT == 3) swap_halves(cl, sl, ol[0][p], ol[1][p]);
+            if constexpr (S::KB == 2) {
+                // lanes 0..31 of input 1's operand: cos 8 of input 1 (own lane);
+                // of input 2's: cos 8 of input 2 (lane + 32); lanes 32..63: zero
+                float c8[8] = {Pc[p][L < 8 ? 0 : 8], 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                const bool l8[8] = {true, false, false, false, false, false, false, false};
+                v8h c8h, c8l;
+                split8<SPLIT>(c8, l8, c8h, c8l);
+                const v8h z = {};
+                swap_halves(c8h, z, oh2[0][p], oh2[1][p]);
+                if constexpr (SPLIT == 3) swap_halves(c8l, z, ol2[0][p], ol2[1][p]);
+            }
         }
 
         // (B) fields of the six polynomials at the n_phi points
@@ -408,6 +427,13 @@ __global__ __launch_bounds__(256, 2) void spingtp_fwd_mfma_kernel(const TIO* __r
                 if constexpr (SPLIT == 3) {
                     fb[in][p] = mfma(TBh, ol[in][p], fb[in][p]);
                     fb[in][p] = mfma(TBl, oh[in][p], fb[in][p]);
+                }
+                if constexpr (S::KB == 2) {
+                    fb[in][p] = mfma(TB2h, oh2[in][p], fb[in][p]);
+                    if constexpr (SPLIT == 3) {
+                        fb[in][p] = mfma(TB2h, ol2[in][p], fb[in][p]);
+                        fb[in][p] = mfma(TB2l, oh2[in][p], fb[in][p]);
+                    }
                 }
             }
 
@@ -570,7 +596,8 @@ constexpr MRegistered reg_mfma() {
 
 // L = 4 fp32 stays on the vector-ALU kernel, which is as fast there (0.37 ns/unit).
 const MRegistered kMfmaRegistry[] = {reg_mfma<4, uint16_t>(), reg_mfma<5, float>(), reg_mfma<5, uint16_t>(),
-                                     reg_mfma<6, float>(), reg_mfma<6, uint16_t>()};
+                                     reg_mfma<6, float>(),    reg_mfma<6, uint16_t>(), reg_mfma<7, float>(),
+                                     reg_mfma<7, uint16_t>(), reg_mfma<8, float>(),    reg_mfma<8, uint16_t>()};
 
 }  // namespace
 

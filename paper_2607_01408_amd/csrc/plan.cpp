@@ -403,7 +403,8 @@ bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::ve
 //   TB, 64 lanes x 8 words: lane l is row l % 32 of the step-(B) table (the phi
 //     point phi_k, k = row, zero for k >= n_phi) and its K elements
 //     8 (l / 32) + e, e = 0..7, are kappa = 8 (l / 32) + e: cos(kappa phi_k) for
-//     kappa <= L, sin((kappa - 8) phi_k) for 1 <= kappa - 8 <= L, else 0.
+//     kappa <= min(L, 7), sin((kappa - 8) phi_k) for 1 <= kappa - 8 <= L, and for
+//     L = 8 sin(8 phi_k) at kappa = 8 (the slot sin 0 leaves free), else 0.
 //     Words 0..3 hold hi, 4..7 lo.
 //   TD[type][block], 2 x NB blocks of 64 lanes x 8 words: lane l is row
 //     r' = l % 32 = 8i + 4h' + r of the step-(D) table, the spectrum t' = 4i + r
@@ -412,10 +413,13 @@ bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::ve
 //     k = 8 (v / 4) + 4 h'' + v % 4 (zero for k >= n_phi).  Type 0 (R0, P1) rows
 //     with h' = 0 are cos(t' phi_k) and with h' = 1 sin(t' phi_k); type 1 (P2)
 //     swaps the two; the t' = 0 rows are cos 0 = 1 in both halves.
+//   TB2 (L = 8 only), after the TD blocks: the second K block of step (B), whose
+//     only nonzero element is kappa = 16 (K element 0, lanes 0..31): cos(8 phi_k).
 void build_mfma_operands(int L, std::vector<uint32_t>& out) {
     const int NP = 3 * L + 1;
     const int NB = (NP + 15) / 16;
-    out.assign(512 + static_cast<size_t>(2 * NB) * 512, 0u);
+    const int KB = L >= 8 ? 2 : 1;  // K blocks of step (B)
+    out.assign(static_cast<size_t>(KB + 2 * NB) * 512, 0u);
     auto trig = [&](bool cosine, int t, int k) {
         const double ang = 2.0 * kPi * static_cast<double>((k * t) % NP) / NP;
         return cosine ? std::cos(ang) : std::sin(ang);
@@ -438,10 +442,14 @@ void build_mfma_operands(int L, std::vector<uint32_t>& out) {
             if (k < NP) {
                 if (kappa < 8 && kappa <= L) v = trig(true, kappa, k);
                 if (kappa >= 9 && kappa - 8 <= L) v = trig(false, kappa - 8, k);
+                if (kappa == 8 && L >= 8) v = trig(false, 8, k);
             }
             put(static_cast<size_t>(lane) * 8, e, v);
         }
     }
+    if (KB == 2)
+        for (int lane = 0; lane < 32; ++lane)
+            if (lane < NP) put(static_cast<size_t>(1 + 2 * NB) * 512 + static_cast<size_t>(lane) * 8, 0, trig(true, 8, lane));
     for (int type = 0; type < 2; ++type)
         for (int b = 0; b < NB; ++b)
             for (int lane = 0; lane < 64; ++lane) {
@@ -1118,7 +1126,7 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
 }
 
 spingtp_status spingtp_mfma_operands_host(int L, uint32_t* words, size_t capacity, size_t* count) {
-    if (L < 1 || L > 7 || count == nullptr || (capacity > 0 && words == nullptr)) return SPINGTP_ERR_INVALID_ARG;
+    if (L < 1 || L > 8 || count == nullptr || (capacity > 0 && words == nullptr)) return SPINGTP_ERR_INVALID_ARG;
     try {
         std::vector<uint32_t> w;
         spingtp::build_mfma_operands(L, w);

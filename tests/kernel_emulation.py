@@ -86,8 +86,12 @@ def emulate_mfma_kernel(x1, x2, L, basis, split=3, theta_dtype=np.float64):
     words = mfma_operands_host(L)
     NT, NP, PB, GLOB = dims["n_theta"], dims["n_phi"], dims["per_theta_block"], dims["global_block"]
     NB = (NP + 15) // 16
-    assert words.size == 512 * (1 + 2 * NB)
+    KB = 2 if L >= 8 else 1
+    assert words.size == 512 * (KB + 2 * NB)
     TB = _operand_matrices(words[:512])
+    if KB == 2:  # second K block (cos 8 at kappa 16) after the step-(D) blocks
+        TB2 = _operand_matrices(words[512 * (1 + 2 * NB):512 * (2 + 2 * NB)])
+        TB = (np.concatenate([TB[0], TB2[0]], axis=1), np.concatenate([TB[1], TB2[1]], axis=1))
     TD = [[_operand_matrices(words[512 * (1 + t * NB + b):512 * (2 + t * NB + b)]) for b in range(NB)]
           for t in range(2)]
     tri = lambda t, l: t * (L + 1) - t * (t - 1) // 2 + (l - t)  # noqa: E731
@@ -127,9 +131,13 @@ def emulate_mfma_kernel(x1, x2, L, basis, split=3, theta_dtype=np.float64):
         wpl = sum(xp[:, l * l + l] * tb[aw + l] for l in range(1, L + 1))
         wmi = sum(xm[:, l * l + l] * tb[aw + l] for l in range(1, L + 1))
         c[1, :, 0], c[2, :, 0], d, e = N0 @ np.stack([wpl, wmi])
-        kappa = np.zeros((3, U, 16))  # cos t at slot t, sin t at slot 8 + t
-        kappa[:, :, :L + 1] = c
-        kappa[:, :, 9:9 + L] = s[:, :, 1:]
+        # cos t at slot t, sin t at slot 8 + t; at L = 8 sin 8 at slot 8, cos 8 at 16
+        kappa = np.zeros((3, U, 16 * KB))
+        kappa[:, :, :min(L, 7) + 1] = c[:, :, :min(L, 7) + 1]
+        kappa[:, :, 9:9 + min(L, 7)] = s[:, :, 1:min(L, 7) + 1]
+        if L >= 8:
+            kappa[:, :, 8] = s[:, :, 8]
+            kappa[:, :, 16] = c[:, :, 8]
         return kappa.astype(theta_dtype).astype(np.float64), d, e, c[0, :, 0]
 
     holds = [8 * (v // 4) + v % 4 < NP for v in range(16)]

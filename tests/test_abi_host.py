@@ -17,8 +17,8 @@ import pytest
 
 import oracle
 from paper_2607_01408_amd import _lib
-from paper_2607_01408_amd.spingtp import dense_tensor_host, plan_tables_host, pre_table_host
-from tests.kernel_emulation import emulate_mfma_kernel, kernel_parity_mix
+from paper_2607_01408_amd.spingtp import dense_tensor_host, mfma_operands_host, plan_tables_host, pre_table_host
+from tests.kernel_emulation import _operand_matrices as _operand_matrices_abi, emulate_mfma_kernel, kernel_parity_mix
 from tests.oracle_helpers import valid_mask
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -213,7 +213,8 @@ def test_dense_tensor_matches_oracle(built_library, L1, L2, LO, spins, basis):
     assert np.abs(T - To).max() < 1e-13
 
 
-@pytest.mark.parametrize("L,basis", [(4, 0), (5, 0), (6, 0), (6, 1), (7, 0), (5, 2), (6, 2)])
+@pytest.mark.parametrize("L,basis", [(4, 0), (5, 0), (6, 0), (6, 1), (7, 0), (7, 2), (8, 0), (8, 1), (8, 2), (5, 2),
+                                     (6, 2)])
 def test_mfma_operand_tables_reproduce_oracle(built_library, L, basis):
     """The matrix-core kernel's data flow, re-enacted on the CPU with the exact fp16
     operand words the plan uploads, matches the oracle to fp32-like accuracy; a
@@ -231,10 +232,29 @@ def test_mfma_operand_tables_reproduce_oracle(built_library, L, basis):
 def test_mfma_operands_argument_checks(built_library):
     count = ctypes.c_size_t(0)
     assert built_library.spingtp_mfma_operands_host(0, None, 0, ctypes.byref(count)) == 1
-    assert built_library.spingtp_mfma_operands_host(8, None, 0, ctypes.byref(count)) == 1
+    assert built_library.spingtp_mfma_operands_host(9, None, 0, ctypes.byref(count)) == 1
     assert built_library.spingtp_mfma_operands_host(6, None, 0, None) == 1
     assert built_library.spingtp_mfma_operands_host(6, None, 0, ctypes.byref(count)) == 0
     assert count.value == 512 * (1 + 2 * 2)  # L = 6: n_phi = 19 points, two K blocks
+    assert built_library.spingtp_mfma_operands_host(8, None, 0, ctypes.byref(count)) == 0
+    assert count.value == 512 * (2 + 2 * 2)  # L = 8: two step-(B) and two step-(D) K blocks
+
+
+def test_mfma_operands_degree8_slots(built_library):
+    """At L = 8 the first step-(B) block carries sin(8 phi) at kappa 8 and the second
+    block only cos(8 phi) at kappa 16, row = phi point; checked against the trig values."""
+    L, NP = 8, 25
+    w = mfma_operands_host(L)
+    h1, l1 = _operand_matrices_abi(w[:512])
+    h2, l2 = _operand_matrices_abi(w[512 * 5:512 * 6])
+    phi = 2 * np.pi * np.arange(32) / NP
+    live = np.arange(32) < NP
+    assert np.abs((h1 + l1)[:, 8] - np.where(live, np.sin(8 * phi), 0.0)).max() < 1e-6
+    assert np.abs((h2 + l2)[:, 0] - np.where(live, np.cos(8 * phi), 0.0)).max() < 1e-6
+    assert not np.any(h2[:, 1:]) and not np.any(l2[:, 1:])
+    for k in range(1, 8):
+        assert np.abs((h1 + l1)[:, 8 + k] - np.where(live, np.sin(k * phi), 0.0)).max() < 1e-6
+        assert np.abs((h1 + l1)[:, k] - np.where(live, np.cos(k * phi), 0.0)).max() < 1e-6
 
 
 PRE_THREADS = 256
@@ -348,7 +368,7 @@ def test_plan_create_route_flags(built_library):
     # precontraction forced where no precontracted kernel is built (rows of 192)
     assert built_library.spingtp_plan_create(7, 7, 7, S, 3, 0, 0x400, ctypes.byref(plan)) == 2
     assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x800, ctypes.byref(plan)) == 1  # tables-only bit
-    assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x2000, ctypes.byref(plan)) == 1  # unknown bit
+    assert built_library.spingtp_plan_create(2, 2, 2, S, 3, 0, 0x4000, ctypes.byref(plan)) == 1  # unknown bit
 
 
 @pytest.mark.parametrize("L", [0, 1, 2, 4, 6, 16])

@@ -65,7 +65,7 @@ def test_backward_matches_oracle(L, basis):
 
 @pytest.mark.parametrize("L,N,C", [(8, 9, 3), (12, 5, 2)])
 def test_backward_large_degree(L, N, C):
-    # the lane-pair (L = 8) and large-L (L = 12) kernel families
+    # the matrix-core (L = 8, two step-(B) K blocks) and large-L (L = 12) kernel families
     run_backward(L, S3, N, C, "fp32", 0, seed=L)
 
 

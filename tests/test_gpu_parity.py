@@ -82,14 +82,14 @@ def test_ragged_spin_shapes(L, basis):
     run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=L)
 
 
-@pytest.mark.parametrize("L", [5, 6])
+@pytest.mark.parametrize("L", [5, 6, 7, 8])
 @pytest.mark.parametrize("basis", [0, 1, 2])
 def test_ragged_valu_kernels(L, basis):
     # the fp32 vector-ALU kernels of the degrees that default to the matrix-core kernel
     run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=40 + L, valu_only=True)
 
 
-@pytest.mark.parametrize("L", [4, 5, 6])
+@pytest.mark.parametrize("L", [4, 5, 6, 7, 8])
 @pytest.mark.parametrize("N,C", [(64, 1), (65, 1), (125, 8), (4113, 1)])
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_matrix_core_sizes(L, N, C, dtype):
@@ -102,7 +102,7 @@ def _ulp_bf16(y):
     return np.ldexp(1.0, (e - 7).astype(int))
 
 
-@pytest.mark.parametrize("L", [4, 5, 6])
+@pytest.mark.parametrize("L", [4, 5, 6, 7, 8])
 @pytest.mark.parametrize("N,C,basis", [(37, 3, 0), (4113, 1, 0), (125, 8, 2)])
 def test_matrix_core_bf16_against_reenactment(L, N, C, basis):
     """The bf16 mode of the matrix-core kernel (fp16 high parts only) against the
