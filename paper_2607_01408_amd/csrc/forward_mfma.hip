@@ -24,10 +24,13 @@
 // sqrt(sum_lm |Y_lm|^2 * n_coef) < 64 and every product combination by < 2^14,
 // well inside fp16, and the output is scaled back exactly.
 //
-// Work mapping.  A workgroup owns 64 units and has four waves (one per SIMD, two
-// workgroups per CU).  Wave w takes units 32 (w & 1) .. +31 and the Gauss nodes
-// j = (w >> 1) + 2k.  In a wave, lane u (< 32) works on input 1 and lane u + 32
-// on input 2 of unit u in step (A); a half-wave swap (v_permlane32_swap) then
+// Work mapping.  A workgroup owns 64 units.  Up to L = 6 it has four waves (one
+// per SIMD, two workgroups per CU); at L = 7, 8 the two fp32 tiles need more than
+// half the LDS, so one workgroup of eight waves fills the CU instead -- two waves
+// per SIMD either way.  Wave w takes units 32 (w & 1) .. +31 and the Gauss nodes
+// j = (w >> 1) + NG k, NG = waves / 2 node groups.  In a wave, lane u (< 32)
+// works on input 1 and lane u + 32 on input 2 of unit u in step (A); a
+// half-wave swap (v_permlane32_swap) then
 // turns the two halves into the (B) operands, whose K layout puts kappa 0..7 in
 // lanes 0..31 and 8..15 in lanes 32..63.  The (B) accumulator of lane u + 32h
 // holds rows (points) 8i + 4h + r, so the products are lane-local, and the same
@@ -37,11 +40,16 @@
 // output slots from its own registers: the h = 0 half accumulates the m3 >= 0
 // outputs and the h = 1 half the m3 < 0 outputs (plus the m3 = 0, s3 = -1 ones),
 // over its nodes, with table values that are the same for all 64 lanes (scalar
-// loads).  The two waves of a unit tile add their partial outputs in LDS at the
-// end, in a fixed order.
+// loads).  The waves of a unit tile add their partial outputs in LDS at the end,
+// in a fixed order (with four node groups, groups 2 and 3 write two tiles and
+// groups 0 and 1 then add into them).
+//
+// L = 8 needs 17 coefficient slots per polynomial: sin 8 takes the slot sin 0
+// leaves free and cos 8 goes alone into a second step-(B) K block.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "device_common.h"
 #include "internal.h"
@@ -61,8 +69,6 @@ struct MShape {
     static constexpr int NC = 3 * BLK;
     static constexpr int ST = NC | 1;           // odd row stride: conflict-free per-lane row reads
     static constexpr int UNITS = 64;
-    static constexpr int WAVES = 4;
-    static constexpr int THREADS = 64 * WAVES;
     static constexpr int X2 = UNITS * ST + 32;  // input-2 tile: lane u + 32 reads 32 banks away from lane u
     static constexpr int XF = X2 + UNITS * ST;
     static constexpr int YB = UNITS * ST;       // second partial-output tile (the first is at 0)
@@ -71,11 +77,15 @@ struct MShape {
     static constexpr int LDS_FLOATS = REGION + 2 * UNITS;
     static constexpr int NB = (NP + 15) / 16;   // K blocks of step (D)
     static constexpr int KB = L >= 8 ? 2 : 1;   // K blocks of step (B): cos 8 in the second
-    static constexpr int NPW = (NT + 1) / 2;    // nodes per wave
+    // Two waves per SIMD either way: two workgroups of four waves per CU while the
+    // tiles fit half the LDS, else (L >= 7) one workgroup of eight waves, each unit
+    // tile then shared by four node groups instead of two.
+    static constexpr bool WIDE = LDS_FLOATS * 4 > 80 * 1024;
+    static constexpr int WAVES = WIDE ? 8 : 4;
+    static constexpr int THREADS = 64 * WAVES;
+    static constexpr int NG = WAVES / 2;          // node groups: wave w takes nodes w/2, w/2 + NG, ...
+    static constexpr int NPW = (NT + NG - 1) / NG;  // nodes per wave (at most)
     static constexpr int TB_WORDS = 64 * 8;     // one lane: 4 words hi, 4 words lo
-    // waves per SIMD the register budget is sized for: two workgroups per CU while
-    // both tiles fit half the LDS, else one (L >= 7)
-    static constexpr int OCC = LDS_FLOATS * 4 <= 80 * 1024 ? 2 : 1;
     static_assert(L >= 1 && L <= 8, "cos 0..7 and sin 1..8 share the first K block; only cos 8 takes a second");
     static_assert(NP <= 32, "the phi points must fit the 32 rows of one step-(B) tile");
     static_assert(LDS_FLOATS * 4 <= 160 * 1024, "the tiles must fit the LDS of a CU");
@@ -96,18 +106,22 @@ typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 // in fp32 and below one fp16 unit of the value, so |x - hi - lo| <= 2^-21 |x| for
 // normal x.
 //
-// Six instructions a pair, all the compiler's own (its hazard model sees every
+// Four instructions a pair, all the compiler's own (its hazard model sees every
 // write; no inline asm, which its wait-state counting takes for one instruction
 // whatever it holds).  The high word comes from the v_cvt_pkrtz intrinsic and the
 // residuals from that word's own bits: a plain fp16 conversion would let the
 // compiler fold the FMA that produced a value into the conversion (one rounding
 // of the exact result) while forming the residual from the fp32-rounded value,
 // and where those two roundings differ hi + lo misses the value by one fp16 unit.
-__device__ __forceinline__ void split_pair(float a, float b, uint32_t& hw, uint32_t& lw) {
+// Each residual is fma(hi, m, a) with m = -1 passed in at run time: the compiler
+// cannot fold the product away, so it reads the fp16 half straight from the packed
+// word (v_fma_mix_f32, op_sel) instead of converting it first.  a - hi is exact in
+// fp32, so the residual equals a - hi bit for bit.
+__device__ __forceinline__ void split_pair(float a, float b, float m, uint32_t& hw, uint32_t& lw) {
     const h2 hq = __builtin_bit_cast(h2, __builtin_amdgcn_cvt_pkrtz(a, b));
     hw = __builtin_bit_cast(uint32_t, hq);
-    const h2 lp = {static_cast<_Float16>(a - static_cast<float>(hq.x)),
-                   static_cast<_Float16>(b - static_cast<float>(hq.y))};
+    const h2 lp = {static_cast<_Float16>(__builtin_fmaf(static_cast<float>(hq.x), m, a)),
+                   static_cast<_Float16>(__builtin_fmaf(static_cast<float>(hq.y), m, b))};
     lw = __builtin_bit_cast(uint32_t, lp);
 }
 
@@ -116,9 +130,10 @@ __device__ __forceinline__ uint32_t pack_hi(float a, float b) {
     return __builtin_bit_cast(uint32_t, hp);
 }
 
-// Eight values (v[0..7]; zero where !live) -> hi and (SPLIT == 3) lo operands.
+// Eight values (v[0..7]; zero where !live) -> hi and (SPLIT == 3) lo operands;
+// m = -1 (see split_pair).
 template <int SPLIT>
-__device__ __forceinline__ void split8(const float (&v)[8], const bool (&live)[8], v8h& hi, v8h& lo) {
+__device__ __forceinline__ void split8(const float (&v)[8], const bool (&live)[8], float m, v8h& hi, v8h& lo) {
     v4u h, l;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
@@ -127,7 +142,7 @@ __device__ __forceinline__ void split8(const float (&v)[8], const bool (&live)[8
             l[w] = 0u;
         } else if constexpr (SPLIT == 3) {
             uint32_t hw, lw;
-            split_pair(v[2 * w], v[2 * w + 1], hw, lw);
+            split_pair(v[2 * w], v[2 * w + 1], m, hw, lw);
             h[w] = hw;
             l[w] = lw;
         } else {
@@ -269,11 +284,12 @@ __device__ __forceinline__ void store_out(uint16_t* __restrict__ dst, int nvalid
 
 // SPLIT = 3: hi*hi + hi*lo + lo*hi (fp32 I/O); SPLIT = 1: hi*hi (bf16 I/O).
 template <int L, typename TIO, int SPLIT, bool BWD>
-__global__ __launch_bounds__(256, MShape<L>::OCC) void spingtp_fwd_mfma_kernel(const TIO* __restrict__ x1,
+__global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel(const TIO* __restrict__ x1,
                                                                    const TIO* __restrict__ x2,
                                                                    TIO* __restrict__ out, int64_t units,
                                                                    int64_t cpx2, const float* __restrict__ tab,
-                                                                   const uint32_t* __restrict__ aux) {
+                                                                   const uint32_t* __restrict__ aux,
+                                                                   float neg_one) {
     using S = MShape<L>;
     constexpr Layout Y = S::Y;
     constexpr int NC = S::NC, ST = S::ST, BLK = S::BLK, NB = S::NB;
@@ -303,7 +319,7 @@ __global__ __launch_bounds__(256, MShape<L>::OCC) void spingtp_fwd_mfma_kernel(c
     // (2) per unit and input: scale the row by 2^-e so that its largest valid
     //     magnitude is in [1/2, 1).  Two threads per row; the l = 0 slots of the
     //     |s| = 1 sectors are not data and are skipped.
-    {
+    if (tid < 256) {  // (the first four waves)
         constexpr int HALF = (NC + 1) / 2;
         const int row = tid >> 1;  // 0..127: input row >> 6, unit row & 63
         const bool odd = (tid & 1) != 0;
@@ -376,7 +392,7 @@ __global__ __launch_bounds__(256, MShape<L>::OCC) void spingtp_fwd_mfma_kernel(c
 
 #pragma unroll 1
     for (int k = 0; k < S::NPW; ++k) {
-        const int j = (wave >> 1) + 2 * k;
+        const int j = (wave >> 1) + S::NG * k;
         if (j >= S::NT) break;
         const float* __restrict__ tb = tab + Y.glob + j * Y.pb;
 
@@ -400,8 +416,8 @@ __global__ __launch_bounds__(256, MShape<L>::OCC) void spingtp_fwd_mfma_kernel(c
                 sv[e] = sl_[e] ? Ps[p][e == 0 ? (L >= 8 ? 8 : 0) : e] : 0.f;
             }
             v8h ch, cl, sh, sl;
-            split8<SPLIT>(cv, cl_, ch, cl);
-            split8<SPLIT>(sv, sl_, sh, sl);
+            split8<SPLIT>(cv, cl_, neg_one, ch, cl);
+            split8<SPLIT>(sv, sl_, neg_one, sh, sl);
             swap_halves(ch, sh, oh[0][p], oh[1][p]);
             if constexpr (SPLIT == 3) swap_halves(cl, sl, ol[0][p], ol[1][p]);
             if constexpr (S::KB == 2) {
@@ -410,7 +426,7 @@ __global__ __launch_bounds__(256, MShape<L>::OCC) void spingtp_fwd_mfma_kernel(c
                 float c8[8] = {Pc[p][L < 8 ? 0 : 8], 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
                 const bool l8[8] = {true, false, false, false, false, false, false, false};
                 v8h c8h, c8l;
-                split8<SPLIT>(c8, l8, c8h, c8l);
+                split8<SPLIT>(c8, l8, neg_one, c8h, c8l);
                 const v8h z = {};
                 swap_halves(c8h, z, oh2[0][p], oh2[1][p]);
                 if constexpr (SPLIT == 3) swap_halves(c8l, z, ol2[0][p], ol2[1][p]);
@@ -468,7 +484,7 @@ __global__ __launch_bounds__(256, MShape<L>::OCC) void spingtp_fwd_mfma_kernel(c
                     hv[e] = live[e] ? H[q][8 * b + e] : 0.f;
                 }
                 v8h hh, hl;
-                split8<SPLIT>(hv, live, hh, hl);
+                split8<SPLIT>(hv, live, neg_one, hh, hl);
                 const v4u* td = ops + 2 * (64 + (qt * NB + b) * 64 + lane);
                 const v8h tdh = __builtin_bit_cast(v8h, td[0]);
                 sp[q] = mfma(tdh, hh, sp[q]);
@@ -517,12 +533,14 @@ __global__ __launch_bounds__(256, MShape<L>::OCC) void spingtp_fwd_mfma_kernel(c
         }
     }
 
-    // partial outputs -> LDS (tile of waves 0, 1 at 0, of waves 2, 3 at YB)
+    // partial outputs -> LDS: node group g = wave / 2 writes the tile at (g % 2) YB;
+    // with four node groups, groups 2 and 3 write first and groups 0 and 1 add theirs
     __syncthreads();  // every wave is done with the input tiles
     // undo the input scaling: the output of a unit scales with 2^(e1 + e2)
     const int unit = 32 * T + (lane & 31);
     const int es = ex[unit] + ex[64 + unit];
-    float* yr = lds + (wave >> 1) * S::YB + unit * ST;
+    const int ngrp = wave >> 1;
+    float* yr = lds + (ngrp & 1) * S::YB + unit * ST;
     if (parity) {
         // back to the parity-labelled basis (P^T, linear, so on the partial tiles):
         // (a, b) of the s = -1, +1 blocks become ((a + (-1)^l b)/sqrt2, (a - (-1)^l b)/sqrt2).
@@ -544,26 +562,43 @@ __global__ __launch_bounds__(256, MShape<L>::OCC) void spingtp_fwd_mfma_kernel(c
             oZ[l] = (h ? (a + b) : (a - b)) * hs;
         }
     }
-    if (h == 0) {
-        yr[0] = 0.f;        // l = 0 of s = -1
-        yr[2 * BLK] = 0.f;  // l = 0 of s = +1
+    // put (ADD = false) or add (ADD = true) this lane's outputs into its row of the tile
+    auto emit = [&](auto add_tag) {
+        constexpr bool ADD = decltype(add_tag)::value;
+        auto put = [&](int q, float v) {
+            const float w = ldexpf(v, es);
+            yr[q] = ADD ? yr[q] + w : w;
+        };
+        if (h == 0) {
+            if constexpr (!ADD) {
+                yr[0] = 0.f;        // l = 0 of s = -1
+                yr[2 * BLK] = 0.f;  // l = 0 of s = +1
+            }
 #pragma unroll
-        for (int l = 0; l <= L; ++l) yr[BLK + l * l + l] = ldexpf(oA[l], es);
+            for (int l = 0; l <= L; ++l) put(BLK + l * l + l, oA[l]);
 #pragma unroll
-        for (int l = 1; l <= L; ++l) yr[2 * BLK + l * l + l] = ldexpf(oZ[l], es);
-    } else {
+            for (int l = 1; l <= L; ++l) put(2 * BLK + l * l + l, oZ[l]);
+        } else {
 #pragma unroll
-        for (int l = 1; l <= L; ++l) yr[l * l + l] = ldexpf(oZ[l], es);
-    }
-    const int sm = h ? -1 : 1;
-#pragma unroll
-    for (int t = 1; t <= L; ++t)
-#pragma unroll
-        for (int l = t; l <= L; ++l) {
-            yr[BLK + l * l + l + sm * t] = ldexpf(oR[t][l], es);
-            yr[2 * BLK + l * l + l + sm * t] = ldexpf(oP[t][l], es);
-            yr[l * l + l + sm * t] = ldexpf(oM[t][l], es);
+            for (int l = 1; l <= L; ++l) put(l * l + l, oZ[l]);
         }
+        const int sm = h ? -1 : 1;
+#pragma unroll
+        for (int t = 1; t <= L; ++t)
+#pragma unroll
+            for (int l = t; l <= L; ++l) {
+                put(BLK + l * l + l + sm * t, oR[t][l]);
+                put(2 * BLK + l * l + l + sm * t, oP[t][l]);
+                put(l * l + l + sm * t, oM[t][l]);
+            }
+    };
+    if constexpr (S::NG == 2) {
+        emit(std::false_type{});
+    } else {
+        if (ngrp >= 2) emit(std::false_type{});
+        __syncthreads();
+        if (ngrp < 2) emit(std::true_type{});
+    }
     __syncthreads();
     store_out<NC, ST, S::UNITS, S::THREADS>(out + u0 * NC, nvalid, lds, S::YB, tid);
 }
@@ -576,7 +611,7 @@ hipError_t launch_mfma(const void* x1, const void* x2, void* out, int64_t units,
     if (blocks > 0x7fffffff || aux == nullptr) return hipErrorInvalidValue;
     hipLaunchKernelGGL((spingtp_fwd_mfma_kernel<L, TIO, SPLIT, BWD>), dim3(static_cast<unsigned>(blocks)),
                        dim3(S::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
-                       static_cast<TIO*>(out), units, cpx2, tab, aux);
+                       static_cast<TIO*>(out), units, cpx2, tab, aux, -1.0f);
     return hipGetLastError();
 }
 
