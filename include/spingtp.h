@@ -501,8 +501,9 @@ spingtp_status spingtp_dense_tensor_host(int L1, int L2, int Lout, const int* sp
  *                            (phi point), K elements 8 (l / 32) + e;
  *   [512 + 512 (type NB + b), ...)  the step-(D) operand of table type 0 (R0, P1)
  *                            or 1 (P2) and K block b, NB = ceil((3L + 1) / 16);
- *   [512 (1 + 2 NB), + 512)  (L = 8 only) the second K block of step (B), whose
- *                            one nonzero K element (kappa 16) is cos(8 phi).
+ *   [512 (1 + 2 NB), + 1024) (L = 8 only) the second K block of step (B), once
+ *                            for input 1 (cos(8 phi) at kappa 16 only) and once
+ *                            for input 2 (cos(8 phi) at kappa 24 only).
  * At L = 8 the first block holds sin(8 phi) at kappa 8, which sin 0 leaves free.
  * 1 <= L <= 8, else SPINGTP_ERR_INVALID_ARG.  Writes min(capacity, total) words
  * to `words` (may be NULL when capacity is 0) and the total to *count.

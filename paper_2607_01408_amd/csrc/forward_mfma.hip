@@ -45,7 +45,9 @@
 // groups 0 and 1 then add into them).
 //
 // L = 8 needs 17 coefficient slots per polynomial: sin 8 takes the slot sin 0
-// leaves free and cos 8 goes alone into a second step-(B) K block.
+// leaves free and cos 8 goes into a second step-(B) K block, whose operand holds
+// each lane's own cos 8 (input 1 at kappa 16, input 2 at kappa 24 -- no swap) and
+// whose two tables each keep one of the two.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -376,9 +378,11 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
     const v4u* __restrict__ ops = reinterpret_cast<const v4u*>(aux);
     const v8h TBh = __builtin_bit_cast(v8h, ops[2 * lane]);
     const v8h TBl = __builtin_bit_cast(v8h, ops[2 * lane + 1]);
-    constexpr int TB2 = 2 * 64 * (1 + 2 * NB);  // the second step-(B) block (L = 8), in v4u
-    const v8h TB2h = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 2 * lane]) : v8h{};
-    const v8h TB2l = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 2 * lane + 1]) : v8h{};
+    constexpr int TB2 = 2 * 64 * (1 + 2 * NB);  // the second step-(B) blocks (L = 8), in v4u
+    const v8h TB2ah = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 2 * lane]) : v8h{};
+    const v8h TB2al = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 2 * lane + 1]) : v8h{};
+    const v8h TB2bh = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 128 + 2 * lane]) : v8h{};
+    const v8h TB2bl = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 128 + 2 * lane + 1]) : v8h{};
     const v16f zero16 = {};
 
     // output accumulators of this lane: m3 >= 0 (h = 0) or m3 < 0 (h = 1)
@@ -403,7 +407,7 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
 
         // step-(B) operands of the three polynomials of both inputs (L = 8: sin 8
         // in the sin 0 slot, cos 8 alone in a second K block)
-        v8h oh[2][3], ol[2][3], oh2[2][3], ol2[2][3];
+        v8h oh[2][3], ol[2][3], oh2[3], ol2[3];
 #pragma unroll
         for (int p = 0; p < 3; ++p) {
             float cv[8], sv[8];
@@ -421,15 +425,12 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
             swap_halves(ch, sh, oh[0][p], oh[1][p]);
             if constexpr (SPLIT == 3) swap_halves(cl, sl, ol[0][p], ol[1][p]);
             if constexpr (S::KB == 2) {
-                // lanes 0..31 of input 1's operand: cos 8 of input 1 (own lane);
-                // of input 2's: cos 8 of input 2 (lane + 32); lanes 32..63: zero
+                // cos 8 of the lane's own input in K element 0: kappa 16 of input 1
+                // (lanes 0..31) and kappa 24 of input 2 (lanes 32..63) in one
+                // operand; the tables TB2a / TB2b pick one input each
                 float c8[8] = {Pc[p][L < 8 ? 0 : 8], 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
                 const bool l8[8] = {true, false, false, false, false, false, false, false};
-                v8h c8h, c8l;
-                split8<SPLIT>(c8, l8, neg_one, c8h, c8l);
-                const v8h z = {};
-                swap_halves(c8h, z, oh2[0][p], oh2[1][p]);
-                if constexpr (SPLIT == 3) swap_halves(c8l, z, ol2[0][p], ol2[1][p]);
+                split8<SPLIT>(c8, l8, neg_one, oh2[p], ol2[p]);
             }
         }
 
@@ -445,10 +446,11 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
                     fb[in][p] = mfma(TBl, oh[in][p], fb[in][p]);
                 }
                 if constexpr (S::KB == 2) {
-                    fb[in][p] = mfma(TB2h, oh2[in][p], fb[in][p]);
+                    const v8h& t2h = in ? TB2bh : TB2ah;
+                    fb[in][p] = mfma(t2h, oh2[p], fb[in][p]);
                     if constexpr (SPLIT == 3) {
-                        fb[in][p] = mfma(TB2h, ol2[in][p], fb[in][p]);
-                        fb[in][p] = mfma(TB2l, oh2[in][p], fb[in][p]);
+                        fb[in][p] = mfma(t2h, ol2[p], fb[in][p]);
+                        fb[in][p] = mfma(in ? TB2bl : TB2al, oh2[p], fb[in][p]);
                     }
                 }
             }

@@ -413,13 +413,16 @@ bool build_tables(int L1, int L2, int LO, int spin_mode, unsigned flags, std::ve
 //     k = 8 (v / 4) + 4 h'' + v % 4 (zero for k >= n_phi).  Type 0 (R0, P1) rows
 //     with h' = 0 are cos(t' phi_k) and with h' = 1 sin(t' phi_k); type 1 (P2)
 //     swaps the two; the t' = 0 rows are cos 0 = 1 in both halves.
-//   TB2 (L = 8 only), after the TD blocks: the second K block of step (B), whose
-//     only nonzero element is kappa = 16 (K element 0, lanes 0..31): cos(8 phi_k).
+//   TB2a, TB2b (L = 8 only), after the TD blocks: the second K block of step (B)
+//     for input 1 and input 2.  Its operand carries cos 8 of each lane's own input
+//     in K element 0, i.e. input 1's at kappa 16 (lanes 0..31) and input 2's at
+//     kappa 24 (lanes 32..63); TB2a has cos(8 phi_k) at kappa 16 only, TB2b at
+//     kappa 24 only, so one operand serves both inputs.
 void build_mfma_operands(int L, std::vector<uint32_t>& out) {
     const int NP = 3 * L + 1;
     const int NB = (NP + 15) / 16;
-    const int KB = L >= 8 ? 2 : 1;  // K blocks of step (B)
-    out.assign(static_cast<size_t>(KB + 2 * NB) * 512, 0u);
+    const int KB2 = L >= 8 ? 2 : 0;  // second-K-block tables of step (B)
+    out.assign(static_cast<size_t>(1 + 2 * NB + KB2) * 512, 0u);
     auto trig = [&](bool cosine, int t, int k) {
         const double ang = 2.0 * kPi * static_cast<double>((k * t) % NP) / NP;
         return cosine ? std::cos(ang) : std::sin(ang);
@@ -447,9 +450,10 @@ void build_mfma_operands(int L, std::vector<uint32_t>& out) {
             put(static_cast<size_t>(lane) * 8, e, v);
         }
     }
-    if (KB == 2)
-        for (int lane = 0; lane < 32; ++lane)
-            if (lane < NP) put(static_cast<size_t>(1 + 2 * NB) * 512 + static_cast<size_t>(lane) * 8, 0, trig(true, 8, lane));
+    for (int b = 0; b < KB2; ++b)  // b = 0: input 1 (lanes 0..31), b = 1: input 2 (lanes 32..63)
+        for (int row = 0; row < NP; ++row)
+            put(static_cast<size_t>(1 + 2 * NB + b) * 512 + static_cast<size_t>(32 * b + row) * 8, 0,
+                trig(true, 8, row));
     for (int type = 0; type < 2; ++type)
         for (int b = 0; b < NB; ++b)
             for (int lane = 0; lane < 64; ++lane) {

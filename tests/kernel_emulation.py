@@ -87,11 +87,13 @@ def emulate_mfma_kernel(x1, x2, L, basis, split=3, theta_dtype=np.float64):
     NT, NP, PB, GLOB = dims["n_theta"], dims["n_phi"], dims["per_theta_block"], dims["global_block"]
     NB = (NP + 15) // 16
     KB = 2 if L >= 8 else 1
-    assert words.size == 512 * (KB + 2 * NB)
-    TB = _operand_matrices(words[:512])
-    if KB == 2:  # second K block (cos 8 at kappa 16) after the step-(D) blocks
-        TB2 = _operand_matrices(words[512 * (1 + 2 * NB):512 * (2 + 2 * NB)])
-        TB = (np.concatenate([TB[0], TB2[0]], axis=1), np.concatenate([TB[1], TB2[1]], axis=1))
+    assert words.size == 512 * (1 + 2 * NB + (2 if KB == 2 else 0))
+    TB1 = _operand_matrices(words[:512])
+    TBin = [TB1, TB1]
+    if KB == 2:  # second K block after the step-(D) blocks: one table per input
+        for i in range(2):
+            T2 = _operand_matrices(words[512 * (1 + 2 * NB + i):512 * (2 + 2 * NB + i)])
+            TBin[i] = (np.concatenate([TB1[0], T2[0]], axis=1), np.concatenate([TB1[1], T2[1]], axis=1))
     TD = [[_operand_matrices(words[512 * (1 + t * NB + b):512 * (2 + t * NB + b)]) for b in range(NB)]
           for t in range(2)]
     tri = lambda t, l: t * (L + 1) - t * (t - 1) // 2 + (l - t)  # noqa: E731
@@ -113,7 +115,7 @@ def emulate_mfma_kernel(x1, x2, L, basis, split=3, theta_dtype=np.float64):
         _, e = np.frexp(m)
         return x * np.ldexp(1.0, -e)[:, None], e
 
-    def theta_fourier(x, tb):
+    def theta_fourier(x, tb, inp):
         xm, x0, xp = x[:, :BO], x[:, BO:2 * BO], x[:, 2 * BO:]
         c, s = np.zeros((3, U, L + 1)), np.zeros((3, U, L + 1))
         for t in range(L + 1):
@@ -135,9 +137,9 @@ def emulate_mfma_kernel(x1, x2, L, basis, split=3, theta_dtype=np.float64):
         kappa = np.zeros((3, U, 16 * KB))
         kappa[:, :, :min(L, 7) + 1] = c[:, :, :min(L, 7) + 1]
         kappa[:, :, 9:9 + min(L, 7)] = s[:, :, 1:min(L, 7) + 1]
-        if L >= 8:
+        if L >= 8:  # cos 8 at kappa 16 (input 1, lanes 0..31) or 24 (input 2, lanes 32..63)
             kappa[:, :, 8] = s[:, :, 8]
-            kappa[:, :, 16] = c[:, :, 8]
+            kappa[:, :, 16 + 8 * inp] = c[:, :, 8]
         return kappa.astype(theta_dtype).astype(np.float64), d, e, c[0, :, 0]
 
     holds = [8 * (v // 4) + v % 4 < NP for v in range(16)]
@@ -146,10 +148,10 @@ def emulate_mfma_kernel(x1, x2, L, basis, split=3, theta_dtype=np.float64):
     y = np.zeros((U, 3 * BO))
     for j in range(NT):
         tb = tab[GLOB + j * PB:GLOB + (j + 1) * PB]
-        K1, d1, e1, a1 = theta_fourier(x1s, tb)
-        K2, d2, e2, a2 = theta_fourier(x2s, tb)
-        f1 = [_split_product(*TB, K1[p], split) for p in range(3)]  # (U, 32): row = phi point
-        f2 = [_split_product(*TB, K2[p], split) for p in range(3)]
+        K1, d1, e1, a1 = theta_fourier(x1s, tb, 0)
+        K2, d2, e2, a2 = theta_fourier(x2s, tb, 1)
+        f1 = [_split_product(*TBin[0], K1[p], split) for p in range(3)]  # (U, 32): row = phi point
+        f2 = [_split_product(*TBin[1], K2[p], split) for p in range(3)]
         A, B, C = f1
         a, b, c = f2
         H = [A * a + B * b + C * c, A * b + a * B, A * c + a * C]

@@ -237,21 +237,25 @@ def test_mfma_operands_argument_checks(built_library):
     assert built_library.spingtp_mfma_operands_host(6, None, 0, ctypes.byref(count)) == 0
     assert count.value == 512 * (1 + 2 * 2)  # L = 6: n_phi = 19 points, two K blocks
     assert built_library.spingtp_mfma_operands_host(8, None, 0, ctypes.byref(count)) == 0
-    assert count.value == 512 * (2 + 2 * 2)  # L = 8: two step-(B) and two step-(D) K blocks
+    assert count.value == 512 * (3 + 2 * 2)  # L = 8: step (B) K blocks 1, 2a, 2b; two step-(D) K blocks
 
 
 def test_mfma_operands_degree8_slots(built_library):
-    """At L = 8 the first step-(B) block carries sin(8 phi) at kappa 8 and the second
-    block only cos(8 phi) at kappa 16, row = phi point; checked against the trig values."""
+    """At L = 8 the first step-(B) block carries sin(8 phi) at kappa 8; the second K
+    block comes once per input, with cos(8 phi) only at kappa 16 (input 1) or only at
+    kappa 24 (input 2), row = phi point; checked against the trig values."""
     L, NP = 8, 25
     w = mfma_operands_host(L)
     h1, l1 = _operand_matrices_abi(w[:512])
-    h2, l2 = _operand_matrices_abi(w[512 * 5:512 * 6])
     phi = 2 * np.pi * np.arange(32) / NP
     live = np.arange(32) < NP
     assert np.abs((h1 + l1)[:, 8] - np.where(live, np.sin(8 * phi), 0.0)).max() < 1e-6
-    assert np.abs((h2 + l2)[:, 0] - np.where(live, np.cos(8 * phi), 0.0)).max() < 1e-6
-    assert not np.any(h2[:, 1:]) and not np.any(l2[:, 1:])
+    for i in range(2):
+        h2, l2 = _operand_matrices_abi(w[512 * (5 + i):512 * (6 + i)])
+        k = 8 * i  # K element within the block: kappa 16 + k
+        assert np.abs((h2 + l2)[:, k] - np.where(live, np.cos(8 * phi), 0.0)).max() < 1e-6
+        rest = np.delete(h2, k, axis=1), np.delete(l2, k, axis=1)
+        assert not np.any(rest[0]) and not np.any(rest[1])
     for k in range(1, 8):
         assert np.abs((h1 + l1)[:, 8 + k] - np.where(live, np.sin(k * phi), 0.0)).max() < 1e-6
         assert np.abs((h1 + l1)[:, k] - np.where(live, np.cos(k * phi), 0.0)).max() < 1e-6
