@@ -319,9 +319,32 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
     const bool parity = tab[Y.par] != 0.f;  // uniform
 
     // (2) per unit and input: scale the row by 2^-e so that its largest valid
-    //     magnitude is in [1/2, 1).  Two threads per row; the l = 0 slots of the
-    //     |s| = 1 sectors are not data and are skipped.
-    if (tid < 256) {  // (the first four waves)
+    //     magnitude is in [1/2, 1).  Two threads per row (four in the eight-wave
+    //     layout, outside the parity basis); the l = 0 slots of the |s| = 1 sectors
+    //     are not data and are skipped.
+    if (S::WIDE && !parity) {
+        constexpr int Q = (NC + 3) / 4;
+        const int row = tid >> 2;  // 0..127, the four threads of a row in one quad
+        const int part = tid & 3;
+        float* xr = lds + ((row >> 6) ? S::X2 : 0) + (row & 63) * ST + part * Q;
+        float v[Q];
+        float m = 0.f;
+#pragma unroll
+        for (int i = 0; i < Q; ++i) {
+            const int q = part * Q + i;
+            v[i] = q < NC ? xr[i] : 0.f;
+            m = fmaxf(m, (q == 0 || q == 2 * BLK) ? 0.f : fabsf(v[i]));
+        }
+        m = fmaxf(m, swap_adjacent(m));
+        m = fmaxf(m, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(m), 0x4E, 0xF, 0xF, false)));
+        int e = 0;
+        if (m > 0.f && m <= 3.0e38f) (void)frexpf(m, &e);
+        e = e < -100 ? -100 : (e > 100 ? 100 : e);
+#pragma unroll
+        for (int i = 0; i < Q; ++i)
+            if (part * Q + i < NC) xr[i] = ldexpf(v[i], -e);
+        if (part == 0) ex[row] = e;
+    } else if (tid < 256) {  // (the first four waves)
         constexpr int HALF = (NC + 1) / 2;
         const int row = tid >> 1;  // 0..127: input row >> 6, unit row & 63
         const bool odd = (tid & 1) != 0;
@@ -564,12 +587,14 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
             oZ[l] = (h ? (a + b) : (a - b)) * hs;
         }
     }
-    // put (ADD = false) or add (ADD = true) this lane's outputs into its row of the tile
-    auto emit = [&](auto add_tag) {
+    // put (ADD = false) or add (ADD = true) this lane's outputs into its row of the
+    // tile; SCALED: times 2^es (with four node groups only the sum is scaled)
+    auto emit = [&](auto add_tag, auto scaled_tag) {
         constexpr bool ADD = decltype(add_tag)::value;
+        constexpr bool SCALED = decltype(scaled_tag)::value;
         auto put = [&](int q, float v) {
-            const float w = ldexpf(v, es);
-            yr[q] = ADD ? yr[q] + w : w;
+            const float w = ADD ? yr[q] + v : v;
+            yr[q] = SCALED ? ldexpf(w, es) : w;
         };
         if (h == 0) {
             if constexpr (!ADD) {
@@ -595,11 +620,11 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
             }
     };
     if constexpr (S::NG == 2) {
-        emit(std::false_type{});
+        emit(std::false_type{}, std::true_type{});
     } else {
-        if (ngrp >= 2) emit(std::false_type{});
+        if (ngrp >= 2) emit(std::false_type{}, std::false_type{});
         __syncthreads();
-        if (ngrp < 2) emit(std::true_type{});
+        if (ngrp < 2) emit(std::true_type{}, std::true_type{});
     }
     __syncthreads();
     store_out<NC, ST, S::UNITS, S::THREADS>(out + u0 * NC, nvalid, lds, S::YB, tid);
