@@ -239,7 +239,10 @@ __device__ void parity_mix_rows(float* tile, int st, int rows, bool inverse, int
 //   PAR : the row holds parity-basis coefficients; the |s| = 1 blocks are mixed by
 //         P as they are read (the kernels that stage tiles in LDS mix them there
 //         instead and pass false).
-template <int L, int LA, bool SPIN, bool PAR = false>
+//   FENCE: a scheduling barrier after each order t of the |s| = 1 sums and after
+//         the s = 0 sums, so that the compiler keeps only one order's row values
+//         in flight (for callers that hold other live state across this step).
+template <int L, int LA, bool SPIN, bool PAR = false, bool FENCE = false>
 __device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const float* __restrict__ tb,
                                                       const float* __restrict__ n0, bool second, float (&Ac)[L + 1],
                                                       float (&As)[L + 1], float (&Bc)[L + 1], float (&Bs)[L + 1],
@@ -258,6 +261,7 @@ __device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const flo
         Ac[t] = sc;
         As[t] = ss;
     }
+    if constexpr (FENCE) __builtin_amdgcn_sched_barrier(0);
     if constexpr (SPIN) {
         const float* xm = xr;
         const float* xp = xr + 2 * B;
@@ -284,6 +288,7 @@ __device__ __forceinline__ void coef_to_theta_fourier(const float* xr, const flo
             Bs[t] = -(vp + vm);
             Cc[t] = vp - vm;
             Cs[t] = up - um;
+            if constexpr (FENCE) __builtin_amdgcn_sched_barrier(0);
         }
         float wpl = 0.f, wmi = 0.f;
 #pragma unroll

@@ -90,6 +90,7 @@ struct MShape {
     static constexpr int TB_WORDS = 64 * 8;     // one lane: 4 words hi, 4 words lo
     static_assert(L >= 1 && L <= 8, "cos 0..7 and sin 1..8 share the first K block; only cos 8 takes a second");
     static_assert(NP <= 32, "the phi points must fit the 32 rows of one step-(B) tile");
+    static_assert(NT >= NG, "every wave takes at least one node");
     static_assert(LDS_FLOATS * 4 <= 160 * 1024, "the tiles must fit the LDS of a CU");
     // step-(B) accumulator position v holds point 8 (v/4) + 4h + v%4; it carries a
     // point (for h = 0, hence possibly for h = 1) when that row is < n_phi
@@ -417,17 +418,31 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
         for (int b = 0; b <= L; ++b) oR[a][b] = oP[a][b] = oM[a][b] = 0.f;
     }
 
-#pragma unroll 1
-    for (int k = 0; k < S::NPW; ++k) {
-        const int j = (wave >> 1) + S::NG * k;
-        if (j >= S::NT) break;
-        const float* __restrict__ tb = tab + Y.glob + j * Y.pb;
-
-        // (A) this lane's input at node j
+    // The node loop is software-pipelined by one stage: node k's step (A) runs
+    // while node k-1's step-(D) products (issued at the end of the previous pass)
+    // are still in the matrix cores; then node k-1's step (E), then node k's steps
+    // (B) to (D).
+    struct Front {  // node k after step (A)
         float Pc[3][L + 1], Ps[3][L + 1], dl, ep;
-        coef_to_theta_fourier<L, L, true>(xr, tb, tab + Y.n0, BWD && h != 0, Pc[0], Ps[0], Pc[1], Ps[1], Pc[2],
-                                          Ps[2], dl, ep);
-
+        const float* tb;
+    };
+    struct Back {  // node k between the issue of step (D) and step (E)
+        v16f sp[3];
+        float d_1, d_2, e_1, e_2, a_1, a_2;
+        const float* tb;
+    };
+    auto front1 = [&](int j) {
+        Front F;
+        F.tb = tab + Y.glob + j * Y.pb;
+        // (A) this lane's input at node j
+        coef_to_theta_fourier<L, L, true, false, true>(xr, F.tb, tab + Y.n0, BWD && h != 0, F.Pc[0], F.Ps[0], F.Pc[1], F.Ps[1],
+                                          F.Pc[2], F.Ps[2], F.dl, F.ep);
+        return F;
+    };
+    auto front2 = [&](const Front& F) {
+        Back Bk;
+        const float (&Pc)[3][L + 1] = F.Pc;
+        const float (&Ps)[3][L + 1] = F.Ps;
         // step-(B) operands of the three polynomials of both inputs (L = 8: sin 8
         // in the sin 0 slot, cos 8 alone in a second K block)
         v8h oh[2][3], ol[2][3], oh2[3], ol2[3];
@@ -494,7 +509,7 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
         }
 
         // (D) spectra: R0 and P1 with table type 0, P2 with type 1
-        v16f sp[3];
+        v16f (&sp)[3] = Bk.sp;
 #pragma unroll
         for (int q = 0; q < 3; ++q) {
             sp[q] = zero16;
@@ -521,11 +536,17 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
             }
         }
 
+        bcast_halves(F.dl, Bk.d_1, Bk.d_2);
+        bcast_halves(F.ep, Bk.e_1, Bk.e_2);
+        bcast_halves(F.Pc[0][0], Bk.a_1, Bk.a_2);
+        Bk.tb = F.tb;
+        return Bk;
+    };
+    auto back = [&](const Back& Bk) {
+        const v16f (&sp)[3] = Bk.sp;
+        const float* __restrict__ tb = Bk.tb;
+        const float d_1 = Bk.d_1, d_2 = Bk.d_2, e_1 = Bk.e_1, e_2 = Bk.e_2, a_1 = Bk.a_1, a_2 = Bk.a_2;
         // m3 = 0 closed forms (both halves hold the t' = 0 cosine sums)
-        float d_1, d_2, e_1, e_2, a_1, a_2;
-        bcast_halves(dl, d_1, d_2);
-        bcast_halves(ep, e_1, e_2);
-        bcast_halves(Pc[0][0], a_1, a_2);
         constexpr float NPf = static_cast<float>(S::NP);
         const float r0c0 = fmaf(-0.5f * NPf, fmaf(d_1, d_2, e_1 * e_2), sp[0][0]);
         const float sP1 = 1.41421356237309505f * sp[1][0];
@@ -556,7 +577,19 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
                 oM[t][l] = fmaf(tb[Y.e1m + tri(L, t, l)], smm, oM[t][l]);
             }
         }
+    };
+
+    // nodes j = wave / 2 + NG k; every wave has at least one (n_theta >= NG)
+    Back prev = front2(front1(wave >> 1));
+#pragma unroll 1
+    for (int k = 1; k < S::NPW; ++k) {
+        const int j = (wave >> 1) + S::NG * k;
+        if (j >= S::NT) break;
+        const Front F = front1(j);  // (A) of node k while (D) of node k-1 finishes
+        back(prev);                 // (E) of node k-1
+        prev = front2(F);           // (B) to (D) of node k
     }
+    back(prev);
 
     // partial outputs -> LDS: node group g = wave / 2 writes the tile at (g % 2) YB;
     // with four node groups, groups 2 and 3 write first and groups 0 and 1 add theirs
