@@ -28,6 +28,7 @@ PEAK_HBM_GBS = 8000.0             # MI355X HBM3E
 PEAK_VALU_FP32_TFLOPS = 78.6
 PEAK_VALU_PACKED_FP32_TFLOPS = 157.3  # the published fp32 vector figure (packed FMA)
 PEAK_MFMA_F16_TFLOPS = 2500.0     # dense fp16 / bf16 matrix cores
+PEAK_MFMA_FP32_TFLOPS = 157.3     # dense fp32 matrix cores
 # The scope table's charged work per unit at spins (-1, 0, +1) (the survey's 2D (u,v) Fourier
 # route): coef->Fourier for both inputs, the spin-pair convolution done directly and by FFT,
 # and Fourier->coef.  Its floor charges the cheaper convolution on the vector ALU and the
@@ -872,6 +873,8 @@ def main():
     ap.add_argument("--sweep-degrees", type=int, nargs="+", default=[2, 4, 8, 12, 16])
     ap.add_argument("--backward", action="store_true",
                     help="time spingtp_backward (both gradients) on the chosen workload")
+    ap.add_argument("--uvw", action="store_true",
+                    help="spingtp_forward_fully_connected (mode uvw) on the App. E.2 shapes")
     ap.add_argument("--v1", action="store_true",
                     help="spingtp_forward_v1: the paper's V = 1 shapes and a degree sweep, both routes")
     ap.add_argument("--v1-sweep-degrees", type=int, nargs="+", default=[1, 2, 3, 4, 5, 6])
@@ -891,7 +894,7 @@ def main():
 
     # the CPU-oracle workers start before this process touches the GPU
     pool = None
-    if not (args.sweep or args.v1 or args.backward) and not args.no_cpu_baseline:
+    if not (args.sweep or args.v1 or args.backward or args.uvw) and not args.no_cpu_baseline:
         pool = CpuPool(cpu_workers_available())
     try:
         run_main(args, pool)
@@ -900,9 +903,77 @@ def main():
             pool.close()
 
 
+# the depthwise runtime table's shapes (App. E.2): (L1, L2, Lout, channels C, edges B)
+UVW_SHAPES = [(1, 1, 1, 16, 128), (1, 1, 1, 64, 128), (1, 1, 1, 128, 128),
+              (2, 2, 2, 16, 32), (2, 2, 2, 64, 32), (2, 2, 2, 128, 32),
+              (2, 2, 2, 16, 128), (2, 2, 2, 64, 128), (2, 2, 2, 128, 128),
+              (1, 3, 3, 16, 128), (1, 3, 3, 64, 128), (1, 3, 3, 128, 128),
+              (2, 2, 2, 64, 1024), (1, 3, 3, 64, 1024), (1, 3, 3, 128, 1024)]
+
+
+def run_uvw(args):
+    """spingtp_forward_fully_connected (mode uvw, App. E.1) on the App. E.2 shapes: U = W = C
+    channels, one edge channel (V = 1), B edges, spins (-1, 0, +1), fp32.  Time per call
+    (HIP events on the launch stream, fill kernel included), the channel mixing's flops
+    (2 U V W d3 per edge and path, run on the fp32 matrix cores) against the fp32 matrix-core
+    peak, and the relative L2 error on sampled edges against the oracle."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2607_01408_amd import Plan, paths_host, workloads
+
+    torch.cuda.set_device(0)
+    rows = []
+    for L1, L2, LO, C, B in UVW_SHAPES:
+        U, V, W = C, 1, C
+        plan = Plan(L1, L2, LO, workloads.SPINS, "fp32", fully_connected=True)
+        x1 = workloads.draw(L1, B, U, 7300 + C, "fp32", workloads.SPINS, "unit", "cuda:0")
+        x2 = workloads.draw(L2, B, V, 7400 + C, "fp32", workloads.SPINS, "unit", "cuda:0")
+        g = torch.Generator(device="cuda:0")
+        g.manual_seed(7500 + B)
+        w = torch.randn((plan.n_paths, U, V, W), generator=g, device="cuda:0") / np.sqrt(U * V)
+        out = plan.forward_fully_connected(x1, x2, w)
+        for _ in range(args.warmup):
+            plan.forward_fully_connected(x1, x2, w, out)
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(args.steps):
+            plan.forward_fully_connected(x1, x2, w, out)
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / args.steps
+        d3 = [2 * (int(b3) % (LO + 1)) + 1 for _, _, b3 in paths_host(L1, L2, LO, workloads.SPINS, 0)]
+        mix_flops = 2.0 * U * V * W * sum(d3) * B
+        sel = np.unique(np.concatenate([np.arange(min(B, 8)), np.arange(max(0, B - 8), B), [B // 2]]))
+        ti = torch.as_tensor(sel, device="cuda:0")
+        a = x1[ti].double().cpu().numpy().reshape(len(sel), U, -1)
+        b = x2[ti].double().cpu().numpy().reshape(len(sel), V, -1)
+        ref = oracle.fully_connected(a, b, w.double().cpu().numpy(), L1, L2, LO, workloads.SPINS, 0)
+        got = out[ti].double().cpu().numpy().reshape(ref.shape)
+        rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+        row = {"L1": L1, "L2": L2, "Lout": LO, "C": C, "B": B, "U": U, "V": V, "W": W, "n_paths": plan.n_paths,
+               "ms": ms, "mix_flops": mix_flops, "mix_tflops": mix_flops / (ms * 1e-3) / 1e12,
+               "mix_frac_of_fp32_mfma_peak": mix_flops / (ms * 1e-3) / (PEAK_MFMA_FP32_TFLOPS * 1e12),
+               "parity_rel_l2_sampled": rel, "parity_edges": int(len(sel))}
+        rows.append(row)
+        print(f"[uvw] ({L1},{L2},{LO}) C={C} B={B}: {ms * 1e3:.1f} us, mixing {row['mix_tflops']:.2f} TF/s, "
+              f"parity {rel:.2e}", file=sys.stderr, flush=True)
+    print(json.dumps({"metric": "fully connected SpinGTP (mode uvw) forward time on the App. E.2 shapes",
+                      "unit": "ms", "higher_is_better": False, "n_gpus": 1, "steps": args.steps,
+                      "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
+                      "config": {"workload": "App. E.2 shapes, U = W = C, V = 1, spins (-1,0,1), N(0,1) inputs, "
+                                             "N(0,1)/sqrt(U V) weights"},
+                      "rows": rows}), flush=True)
+
+
 def run_main(args, pool):
     if args.sweep:
         run_sweep(args)
+        return
+    if args.uvw:
+        run_uvw(args)
         return
     if args.v1:
         run_v1(args)
