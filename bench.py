@@ -1054,8 +1054,11 @@ def run_main(args, pool):
     import oracle
 
     rng = np.random.default_rng(77)
-    idx = np.unique(np.concatenate([np.arange(min(512, U)), np.arange(max(0, U - 512), U),
-                                    rng.choice(U, size=min(U, args.parity_units), replace=False)]))
+    # the random units are drawn from between the head and the tail, so the sample holds
+    # 1,024 + parity_units distinct units whenever the job has that many
+    lo, hi = min(512, U), max(min(512, U), U - 512)
+    inner = rng.choice(hi - lo, size=min(hi - lo, args.parity_units), replace=False) + lo
+    idx = np.unique(np.concatenate([np.arange(lo), np.arange(hi, U), inner]))
     ti = torch.as_tensor(idx, device="cuda:0")
     ya = out.view(U, -1)[ti].double().cpu().numpy()
     pa, pb = x1.view(U, -1)[ti].double().cpu().numpy(), x2.view(U, -1)[ti].double().cpu().numpy()
