@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "device_common.h"
 #include "internal.h"
@@ -269,12 +270,82 @@ struct BigShape {
     static constexpr int WAVES = W;
     static constexpr int THREADS = 64 * W;
     static constexpr int ROUNDS = (NT + W - 1) / W;
-    static constexpr int DF = W * UNITS * PS::DS;
     static constexpr int TRIG = 2 * NP * (L + 1);
     static constexpr int STO = NC | 1;  // odd row stride of the output tile
-    static constexpr bool OUT_LDS = (DF + TRIG + UNITS * STO) * 4 <= 160 * 1024;
+    // A round's spectra go through LDS in K parts, part k holding the slots of the
+    // orders t in [tlo(k), tlo(k + 1)); K is the fewest parts (up to 4) with which
+    // the output tile stays in LDS next to one part of W waves' spectra.
+    __host__ __device__ static constexpr int tlo(int k, int K) { return k * (L + 1) / K; }
+    __host__ __device__ static constexpr int sbase(int t) { return t == 0 ? 0 : PS::T0 + PS::PER_T * (t - 1); }
+    __host__ __device__ static constexpr int pwidth(int K) {
+        int w = 0;
+        for (int k = 0; k < K; ++k) {
+            const int a = sbase(tlo(k, K)), b = tlo(k + 1, K) > L ? PS::ND : sbase(tlo(k + 1, K));
+            w = b - a > w ? b - a : w;
+        }
+        return w | 1;
+    }
+    __host__ __device__ static constexpr bool fits(int K) {
+        return (W * UNITS * pwidth(K) + TRIG + UNITS * STO) * 4 <= 160 * 1024;
+    }
+    static constexpr int K = fits(1) ? 1 : fits(2) ? 2 : fits(3) ? 3 : fits(4) ? 4 : 1;
+    static constexpr bool OUT_LDS = fits(K);
+    static constexpr int DSP = pwidth(K);  // record stride of one part
+    static constexpr int DF = W * UNITS * DSP;
     static constexpr int LDS_FLOATS = DF + TRIG + (OUT_LDS ? UNITS * STO : 0);
+    __host__ __device__ static constexpr int part_of_t(int t) {
+        int k = 0;
+        while (k + 1 < K && t >= tlo(k + 1, K)) ++k;
+        return k;
+    }
 };
+
+// Owners of the output groups with several spectrum parts: each part's groups are
+// spread over the waves by size (largest first, least-loaded wave).
+template <int L, bool SPIN, int NW, int K>
+constexpr Owners<PairShape<L, SPIN>::NG> assign_part_owners() {
+    using P = PairShape<L, SPIN>;
+    using B = BigShape<L, SPIN, NW>;
+    Owners<P::NG> o{};
+    for (int k = 0; k < K; ++k) {
+        int load[NW] = {};
+        bool done[P::NG] = {};
+        for (;;) {
+            int best = -1;
+            for (int g = 0; g < P::NG; ++g)
+                if (!done[g] && B::part_of_t(P::t_of(g)) == k && (best < 0 || P::size(g) > P::size(best))) best = g;
+            if (best < 0) break;
+            int w = 0;
+            for (int q = 1; q < NW; ++q)
+                if (load[q] < load[w]) w = q;
+            o.owner[best] = w;
+            load[w] += P::size(best);
+            done[best] = true;
+        }
+    }
+    return o;
+}
+
+// pair_publish restricted to the orders t in [T_LO, T_HI), slot s stored at s - sbase(T_LO).
+template <int L, bool SPIN, int T_LO, int T_HI>
+__device__ __forceinline__ void pair_publish_part(float* D, int sub, const float (&Q0)[L + 1],
+                                                  const float (&Q1)[L + 1], const float (&Q2)[L + 1], float zslot) {
+    constexpr int T0 = SPIN ? 4 : 2, PER_T = SPIN ? 6 : 2;
+    constexpr int base = T_LO == 0 ? 0 : T0 + PER_T * (T_LO - 1);
+    if constexpr (T_LO == 0) {
+        D[sub] = Q0[0];
+        if constexpr (SPIN) D[2 + sub] = zslot;
+    }
+#pragma unroll
+    for (int t = (T_LO > 1 ? T_LO : 1); t < T_HI; ++t) {
+        float* d = D + T0 + PER_T * (t - 1) - base;
+        d[sub] = Q0[t];
+        if constexpr (SPIN) {
+            d[2 + sub] = Q1[t];
+            d[4 + sub] = Q2[t];
+        }
+    }
+}
 
 // PAR (spins only): the plan's basis is the parity-labelled one; a separate
 // instantiation, since a run-time switch between the two step-(A) forms costs the
@@ -324,48 +395,60 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     }
     __syncthreads();
 
-    constexpr Owners<P::NG> own = assign_pair_owners<L, SPIN, W>();
+    constexpr int K = B::K;
+    constexpr Owners<P::NG> own = K == 1 ? assign_pair_owners<L, SPIN, W>() : assign_part_owners<L, SPIN, W, K>();
 #pragma unroll 1
     for (int r = 0; r < B::ROUNDS; ++r) {
         const int node = r * W + wave;
         const int nr = (B::NT - r * W) < W ? (B::NT - r * W) : W;
+        float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
         if (node < B::NT) {
-            float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
             const float* tb = tab + Y.glob + node * Y.pb;
             const float* trl = TR + sub * (B::NP * (L + 1));
             pair_spectra<L, SPIN, BWD, PAR>(xr, tb, g, trl, sub, Q0, Q1, Q2, zslot);
-            pair_publish<L, SPIN>(D + (wave * B::UNITS + u) * P::DS, sub, Q0, Q1, Q2, zslot);
         }
-        __syncthreads();
+        // the round's spectra in K parts (orders t in [tlo(k), tlo(k + 1))): publish
+        // part k, then every owner of a group of part k adds the round's nodes
+        auto part = [&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            constexpr int T_LO = B::tlo(k, K), T_HI = B::tlo(k + 1, K);
+            if (node < B::NT)
+                pair_publish_part<L, SPIN, T_LO, T_HI>(D + (wave * B::UNITS + u) * B::DSP, sub, Q0, Q1, Q2, zslot);
+            __syncthreads();
 #pragma unroll
-        for (int gi = 0; gi < P::NG; ++gi) {
-            if (own.owner[gi] != wave) continue;
-            const int t = P::t_of(gi), kind = P::kind_of(gi);
-            int tab_base = Y.e0c, blk = SPIN ? BO : 0;
-            if (kind == 1) tab_base = Y.e1p, blk = 2 * BO;
-            if (kind == 2) tab_base = Y.e1m, blk = 0;
-            if (kind == 3) tab_base = Y.e1z, blk = sub ? 0 : 2 * BO;
-            float acc[L + 1];
+            for (int gi = 0; gi < P::NG; ++gi) {
+                if (B::part_of_t(P::t_of(gi)) != k || own.owner[gi] != wave) continue;
+                const int t = P::t_of(gi), kind = P::kind_of(gi);
+                int tab_base = Y.e0c, blk = SPIN ? BO : 0;
+                if (kind == 1) tab_base = Y.e1p, blk = 2 * BO;
+                if (kind == 2) tab_base = Y.e1m, blk = 0;
+                if (kind == 3) tab_base = Y.e1z, blk = sub ? 0 : 2 * BO;
+                float acc[L + 1];
 #pragma unroll
-            for (int l = 0; l <= L; ++l) acc[l] = 0.f;
+                for (int l = 0; l <= L; ++l) acc[l] = 0.f;
 #pragma unroll 1
-            for (int jj = 0; jj < nr; ++jj) {
-                const float d = D[(jj * B::UNITS + u) * P::DS + P::slot(gi) + sub];
-                const float* te = tab + Y.glob + (r * W + jj) * Y.pb;
+                for (int jj = 0; jj < nr; ++jj) {
+                    const float d = D[(jj * B::UNITS + u) * B::DSP + P::slot(gi) - B::sbase(T_LO) + sub];
+                    const float* te = tab + Y.glob + (r * W + jj) * Y.pb;
 #pragma unroll
-                for (int l = P::lmin(gi); l <= L; ++l)
-                    acc[l] = fmaf(te[kind == 3 ? tab_base + l : tab_base + tri(L, t, l)], d, acc[l]);
-            }
-            if (valid && !(t == 0 && kind == 0 && sub)) {
-                float* yrow = B::OUT_LDS ? YT + u * B::STO : orow;
+                    for (int l = P::lmin(gi); l <= L; ++l)
+                        acc[l] = fmaf(te[kind == 3 ? tab_base + l : tab_base + tri(L, t, l)], d, acc[l]);
+                }
+                if (valid && !(t == 0 && kind == 0 && sub)) {
+                    float* yrow = B::OUT_LDS ? YT + u * B::STO : orow;
 #pragma unroll
-                for (int l = P::lmin(gi); l <= L; ++l) {
-                    float* o = yrow + blk + l * l + l + (sub ? -t : t);
-                    *o = (r == 0) ? acc[l] : *o + acc[l];
+                    for (int l = P::lmin(gi); l <= L; ++l) {
+                        float* o = yrow + blk + l * l + l + (sub ? -t : t);
+                        *o = (r == 0) ? acc[l] : *o + acc[l];
+                    }
                 }
             }
-        }
-        __syncthreads();
+            __syncthreads();
+        };
+        part(std::integral_constant<int, 0>{});
+        if constexpr (K > 1) part(std::integral_constant<int, 1>{});
+        if constexpr (K > 2) part(std::integral_constant<int, 2>{});
+        if constexpr (K > 3) part(std::integral_constant<int, 3>{});
     }
     if constexpr (B::OUT_LDS) {
         if constexpr (PAR) {
@@ -392,19 +475,10 @@ hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, 
     return hipGetLastError();
 }
 
-// Nodes per round: eight (two waves per SIMD at up to 256 VGPRs) where the output tile
-// fits in LDS next to eight waves' spectra; for spins at L = 13, 14 the most waves (7, 6)
-// that still leave room for the tile, since a global read-modify-write of the outputs
-// per round costs more than the extra rounds' input re-reads. Below 6 waves (L = 15, 16)
-// the lost latency hiding costs more than the tile saves, so those keep 8 waves and
-// accumulate into global memory.
+// Nodes per round: eight waves (two per SIMD at up to 256 VGPRs); the spectra go
+// through LDS in as many parts as the output tile needs to stay there (BigShape::K).
 template <int L, bool SPIN>
 constexpr int big_waves() {
-    for (int w = 8; w >= 6; --w) {
-        const int spectra = w * 32 * PairShape<L, SPIN>::DS, trig = 2 * (3 * L + 1) * (L + 1);
-        const int tile = 32 * (PairShape<L, SPIN>::NC | 1);
-        if ((spectra + trig + tile) * 4 <= 160 * 1024) return w;
-    }
     return 8;
 }
 
