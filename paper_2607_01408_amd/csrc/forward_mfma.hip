@@ -24,11 +24,11 @@
 // sqrt(sum_lm |Y_lm|^2 * n_coef) < 64 and every product combination by < 2^14,
 // well inside fp16, and the output is scaled back exactly.
 //
-// Work mapping.  A workgroup owns 64 units.  Up to L = 6 it has four waves (one
-// per SIMD, two workgroups per CU); at L = 7, 8 the two fp32 tiles need more than
-// half the LDS, so one workgroup of eight waves fills the CU instead -- two waves
-// per SIMD either way.  Wave w takes units 32 (w & 1) .. +31 and the Gauss nodes
-// j = (w >> 1) + NG k, NG = waves / 2 node groups.  In a wave, lane u (< 32)
+// Work mapping.  A workgroup has four waves (one per SIMD, two workgroups per
+// CU).  Up to L = 6 it owns 64 units: wave w takes units 32 (w & 1) .. +31 and the
+// Gauss nodes j = (w >> 1) + 2k.  At L = 7, 8 two fp32 64-unit tiles would need
+// more than half the LDS, so a workgroup owns 32 units and wave w takes the nodes
+// j = w + 4k (NG = 4 node groups).  In a wave, lane u (< 32)
 // works on input 1 and lane u + 32 on input 2 of unit u in step (A); a
 // half-wave swap (v_permlane32_swap) then
 // turns the two halves into the (B) operands, whose K layout puts kappa 0..7 in
@@ -70,7 +70,12 @@ struct MShape {
     static constexpr int BLK = (L + 1) * (L + 1);
     static constexpr int NC = 3 * BLK;
     static constexpr int ST = NC | 1;           // odd row stride: conflict-free per-lane row reads
-    static constexpr int UNITS = 64;
+    // Two workgroups of four waves per CU (two waves per SIMD): 64-unit tiles (two
+    // unit tiles of 32, two node groups) while two fp32 64-unit tiles fit half the
+    // LDS, else (L >= 7) 32-unit tiles (one unit tile, four node groups).
+    static constexpr bool WIDE = (2 * 64 * ST + 32 + 2 * 64) * 4 > 80 * 1024;
+    static constexpr int UNITS = WIDE ? 32 : 64;
+    static constexpr int UT = UNITS / 32;         // unit tiles of a workgroup
     static constexpr int X2 = UNITS * ST + 32;  // input-2 tile: lane u + 32 reads 32 banks away from lane u
     static constexpr int XF = X2 + UNITS * ST;
     static constexpr int YB = UNITS * ST;       // second partial-output tile (the first is at 0)
@@ -79,19 +84,15 @@ struct MShape {
     static constexpr int LDS_FLOATS = REGION + 2 * UNITS;
     static constexpr int NB = (NP + 15) / 16;   // K blocks of step (D)
     static constexpr int KB = L >= 8 ? 2 : 1;   // K blocks of step (B): cos 8 in the second
-    // Two waves per SIMD either way: two workgroups of four waves per CU while the
-    // tiles fit half the LDS, else (L >= 7) one workgroup of eight waves, each unit
-    // tile then shared by four node groups instead of two.
-    static constexpr bool WIDE = LDS_FLOATS * 4 > 80 * 1024;
-    static constexpr int WAVES = WIDE ? 8 : 4;
+    static constexpr int WAVES = 4;
     static constexpr int THREADS = 64 * WAVES;
-    static constexpr int NG = WAVES / 2;          // node groups: wave w takes nodes w/2, w/2 + NG, ...
+    static constexpr int NG = WAVES / UT;         // node groups: wave w takes nodes w/UT, w/UT + NG, ...
     static constexpr int NPW = (NT + NG - 1) / NG;  // nodes per wave (at most)
     static constexpr int TB_WORDS = 64 * 8;     // one lane: 4 words hi, 4 words lo
     static_assert(L >= 1 && L <= 8, "cos 0..7 and sin 1..8 share the first K block; only cos 8 takes a second");
     static_assert(NP <= 32, "the phi points must fit the 32 rows of one step-(B) tile");
     static_assert(NT >= NG, "every wave takes at least one node");
-    static_assert(LDS_FLOATS * 4 <= 160 * 1024, "the tiles must fit the LDS of a CU");
+    static_assert(LDS_FLOATS * 4 <= 80 * 1024, "two workgroups per CU");
     // step-(B) accumulator position v holds point 8 (v/4) + 4h + v%4; it carries a
     // point (for h = 0, hence possibly for h = 1) when that row is < n_phi
     __host__ __device__ static constexpr bool holds_point(int v) { return 8 * (v / 4) + (v % 4) < NP; }
@@ -320,14 +321,14 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
     const bool parity = tab[Y.par] != 0.f;  // uniform
 
     // (2) per unit and input: scale the row by 2^-e so that its largest valid
-    //     magnitude is in [1/2, 1).  Two threads per row (four in the eight-wave
-    //     layout, outside the parity basis); the l = 0 slots of the |s| = 1 sectors
-    //     are not data and are skipped.
+    //     magnitude is in [1/2, 1).  Two threads per row (four with 32-unit tiles,
+    //     outside the parity basis); the l = 0 slots of the |s| = 1 sectors are not
+    //     data and are skipped.
     if (S::WIDE && !parity) {
         constexpr int Q = (NC + 3) / 4;
-        const int row = tid >> 2;  // 0..127, the four threads of a row in one quad
+        const int row = tid >> 2;  // 0..2 UNITS - 1, the four threads of a row in one quad
         const int part = tid & 3;
-        float* xr = lds + ((row >> 6) ? S::X2 : 0) + (row & 63) * ST + part * Q;
+        float* xr = lds + (row >= S::UNITS ? S::X2 : 0) + (row % S::UNITS) * ST + part * Q;
         float v[Q];
         float m = 0.f;
 #pragma unroll
@@ -345,11 +346,11 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
         for (int i = 0; i < Q; ++i)
             if (part * Q + i < NC) xr[i] = ldexpf(v[i], -e);
         if (part == 0) ex[row] = e;
-    } else if (tid < 256) {  // (the first four waves)
+    } else if (tid < 4 * S::UNITS) {  // two threads per row
         constexpr int HALF = (NC + 1) / 2;
-        const int row = tid >> 1;  // 0..127: input row >> 6, unit row & 63
+        const int row = tid >> 1;  // 0..2 UNITS - 1: input row / UNITS, unit row % UNITS
         const bool odd = (tid & 1) != 0;
-        float* xr = lds + ((row >> 6) ? S::X2 : 0) + (row & 63) * ST + (odd ? HALF : 0);
+        float* xr = lds + (row >= S::UNITS ? S::X2 : 0) + (row % S::UNITS) * ST + (odd ? HALF : 0);
         float v[HALF];
         float m = 0.f;
 #pragma unroll
@@ -396,7 +397,8 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
     __syncthreads();
 
     const int h = lane >> 5;  // (A): input h + 1; (D)-(E): accumulator type
-    const int T = wave & 1;   // unit tile of this wave
+    const int T = S::UT == 2 ? (wave & 1) : 0;       // unit tile of this wave
+    const int ngrp = S::UT == 2 ? (wave >> 1) : wave;  // node group of this wave
     const float* xr = lds + (h ? S::X2 : 0) + (32 * T + (lane & 31)) * ST;
     const float sg = h ? -1.f : 1.f;
     const v4u* __restrict__ ops = reinterpret_cast<const v4u*>(aux);
@@ -579,11 +581,11 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
         }
     };
 
-    // nodes j = wave / 2 + NG k; every wave has at least one (n_theta >= NG)
-    Back prev = front2(front1(wave >> 1));
+    // nodes j = ngrp + NG k; every wave has at least one (n_theta >= NG)
+    Back prev = front2(front1(ngrp));
 #pragma unroll 1
     for (int k = 1; k < S::NPW; ++k) {
-        const int j = (wave >> 1) + S::NG * k;
+        const int j = ngrp + S::NG * k;
         if (j >= S::NT) break;
         const Front F = front1(j);  // (A) of node k while (D) of node k-1 finishes
         back(prev);                 // (E) of node k-1
@@ -591,13 +593,12 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
     }
     back(prev);
 
-    // partial outputs -> LDS: node group g = wave / 2 writes the tile at (g % 2) YB;
+    // partial outputs -> LDS: node group g writes the tile at (g % 2) YB;
     // with four node groups, groups 2 and 3 write first and groups 0 and 1 add theirs
     __syncthreads();  // every wave is done with the input tiles
     // undo the input scaling: the output of a unit scales with 2^(e1 + e2)
     const int unit = 32 * T + (lane & 31);
-    const int es = ex[unit] + ex[64 + unit];
-    const int ngrp = wave >> 1;
+    const int es = ex[unit] + ex[S::UNITS + unit];
     float* yr = lds + (ngrp & 1) * S::YB + unit * ST;
     if (parity) {
         // back to the parity-labelled basis (P^T, linear, so on the partial tiles):
