@@ -9,6 +9,7 @@
 
 #include <cstdint>
 #include <type_traits>
+#include <utility>
 
 #include "device_common.h"
 #include "internal.h"
@@ -124,17 +125,23 @@ constexpr Owners<PairShape<L, SPIN>::NG> assign_pair_owners() {
 //   Q0[t]: R0c[t] (even lane) or -R0s[t] (odd lane), t >= 1; Q0[0] = R0c[0]
 //   Q1[t]: P1c+P2s (even) or P2c-P1s (odd);  Q2[t]: P1c-P2s (even) or -P2c-P1s (odd)
 //   zslot: Z+ (even lane) or Z- (odd lane), the m3 = 0, |s3| = 1 sums.
-template <int L, bool SPIN, bool BWD, bool PAR = false>
-__device__ __forceinline__ void pair_spectra(const float* xr, const float* __restrict__ tb,
-                                             const float* __restrict__ g, const float* trl, int sub,
-                                             float (&Q0)[L + 1], float (&Q1)[L + 1], float (&Q2)[L + 1],
-                                             float& zslot) {
+// Steps (B)-(D) from the lane's step-(A) output (theta-Fourier coefficients of its
+// input at the node), over the phi-point pairs k in [k_lo, k_hi).  The spectra are
+// linear in the point sums, so a node's points can be split over several waves
+// whose partial spectra add up: `lead` (wave-uniform) marks the part that also
+// takes the single points (phi = 0, pi) and the closed-form t = 0 terms.
+template <int L, bool SPIN>
+__device__ __forceinline__ void pair_spectra_from_fourier(const float (&Pc0)[L + 1], const float (&Ps0)[L + 1],
+                                                          const float (&Pc1)[L + 1], const float (&Ps1)[L + 1],
+                                                          const float (&Pc2)[L + 1], const float (&Ps2)[L + 1],
+                                                          float dl, float ep, const float* __restrict__ g,
+                                                          const float* trl, int sub, float (&Q0)[L + 1],
+                                                          float (&Q1)[L + 1], float (&Q2)[L + 1], float& zslot,
+                                                          int k_lo = 1, int k_hi = (make_layout(L, L, L).NP - 1) / 2 + 1,
+                                                          bool lead = true) {
     constexpr Layout Y = make_layout(L, L, L);
     constexpr int TM1 = Y.TM + 1;
     constexpr int NP = Y.NP;
-    constexpr int KP = (NP - 1) / 2;
-    float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
-    coef_to_theta_fourier<L, L, SPIN, PAR>(xr, tb, g + Y.n0, BWD && sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
     const float sg = sub ? -1.f : 1.f;
 
     // accumulators: cosine spectra on the even lane, sine spectra on the odd lane
@@ -171,9 +178,9 @@ __device__ __forceinline__ void pair_spectra(const float* xr, const float* __res
         }
         accumulate(r0, q1, q2, trl + k * (L + 1));
     };
-    single_point(0, 1.f);
+    if (lead) single_point(0, 1.f);
 #pragma unroll 1
-    for (int k = 1; k <= KP; ++k) {
+    for (int k = k_lo; k < k_hi; ++k) {
         const float* __restrict__ cs = g + Y.cosT + k * TM1;
         const float* __restrict__ sn = g + Y.sinT + k * TM1;
         float o0p, o0m, o1p = 0.f, o1m = 0.f, o2p = 0.f, o2m = 0.f;
@@ -197,18 +204,20 @@ __device__ __forceinline__ void pair_spectra(const float* xr, const float* __res
         // even lane: sums (cosine), odd lane: differences (sine)
         accumulate(fmaf(sg, r0m, r0p), fmaf(sg, q1m, q1p), fmaf(sg, q2m, q2p), trl + k * (L + 1));
     }
-    if constexpr (NP % 2 == 0) single_point(NP / 2, -1.f);
+    if constexpr (NP % 2 == 0) {
+        if (lead) single_point(NP / 2, -1.f);
+    }
 
     // t = 0 terms (valid on the even lane, which holds input 1 and every cosine spectrum)
     zslot = 0.f;
     if constexpr (SPIN) {
         const float a0p = swap_pair(Pc0[0]);
         const float dlp = swap_pair(dl), epp = swap_pair(ep);
-        Q0[0] = fmaf(-0.5f * NP, fmaf(dl, dlp, ep * epp), Q0[0]);
+        if (lead) Q0[0] = fmaf(-0.5f * NP, fmaf(dl, dlp, ep * epp), Q0[0]);
         const float sP1 = 1.41421356237309505f * Q1[0];
         const float sP2 = 1.41421356237309505f * Q2[0];
-        const float sP4 = -static_cast<float>(NP) * fmaf(dlp, Pc0[0], dl * a0p);
-        const float sP3 = static_cast<float>(NP) * fmaf(epp, Pc0[0], ep * a0p);
+        const float sP4 = lead ? -static_cast<float>(NP) * fmaf(dlp, Pc0[0], dl * a0p) : 0.f;
+        const float sP3 = lead ? static_cast<float>(NP) * fmaf(epp, Pc0[0], ep * a0p) : 0.f;
         const float v0 = 0.5f * (sP1 + sP4), v1 = 0.5f * (sP3 + sP2);
         const float v2 = 0.5f * (sP1 - sP4), v3 = 0.5f * (sP3 - sP2);
         const float* m0 = g + Y.m0;
@@ -227,6 +236,122 @@ __device__ __forceinline__ void pair_spectra(const float* xr, const float* __res
     }
 #pragma unroll
     for (int t = 1; t <= L; ++t) Q0[t] *= sg;
+}
+
+template <int L, bool SPIN, bool BWD, bool PAR = false>
+__device__ __forceinline__ void pair_spectra(const float* xr, const float* __restrict__ tb,
+                                             const float* __restrict__ g, const float* trl, int sub,
+                                             float (&Q0)[L + 1], float (&Q1)[L + 1], float (&Q2)[L + 1],
+                                             float& zslot) {
+    constexpr Layout Y = make_layout(L, L, L);
+    float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
+    coef_to_theta_fourier<L, L, SPIN, PAR>(xr, tb, g + Y.n0, BWD && sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
+    pair_spectra_from_fourier<L, SPIN>(Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep, g, trl, sub, Q0, Q1, Q2, zslot);
+}
+
+// Step (A) a few degrees at a time.  The large-degree kernel stages slots
+// LA^2 .. LB^2 - 1 of every spin block of its input rows in LDS (one chunk of
+// degrees l in [LA, LB)) and adds each chunk's terms to sums that persist across
+// the chunks.  Every sum still runs over l in increasing order, so the results
+// are those of coef_to_theta_fourier.
+template <int L, bool SPIN>
+struct ThetaSums {
+    float sc[L + 1], ss[L + 1];                        // spin 0: cosine, sine (t >= 1)
+    float up[L + 1], vp[L + 1], um[L + 1], vm[L + 1];  // |s| = 1, t >= 1
+    float wpl, wmi;                                    // |s| = 1, t = 0
+};
+
+template <int L, bool SPIN>
+__device__ __forceinline__ void theta_sums_zero(ThetaSums<L, SPIN>& a) {
+#pragma unroll
+    for (int t = 0; t <= L; ++t) a.sc[t] = a.ss[t] = a.up[t] = a.vp[t] = a.um[t] = a.vm[t] = 0.f;
+    a.wpl = a.wmi = 0.f;
+}
+
+// s: the lane's staged row, block b (spins -1, 0, +1, or 0 alone) at s + b CW with
+// CW = LB^2 - LA^2 slots, slot q of a block at offset q - LA^2.
+template <int L, bool SPIN, bool PAR, int LA, int LB>
+__device__ __forceinline__ void theta_sums_add(const float* s, const float* __restrict__ tb, ThetaSums<L, SPIN>& a) {
+    constexpr Layout Y = make_layout(L, 0, 0);
+    constexpr int CW = LB * LB - LA * LA, O = LA * LA;
+    const float* x0 = s + (SPIN ? CW : 0);
+    // (scheduling fences per order t keep one order's row values in flight at a time)
+#pragma unroll
+    for (int t = 0; t < LB; ++t) {
+#pragma unroll
+        for (int l = (t > LA ? t : LA); l < LB; ++l) {
+            a.sc[t] = fmaf(x0[l * l + l + t - O], tb[Y.a0c + tri(L, t, l)], a.sc[t]);
+            if (t > 0) a.ss[t] = fmaf(x0[l * l + l - t - O], tb[Y.a0s + tri(L, t, l)], a.ss[t]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (SPIN) {
+        const float* xm = s;
+        const float* xp = s + 2 * CW;
+        // paper-basis -1 and +1 values of slot q from the parity-labelled ones (up to
+        // the factor 1/sqrt2 applied to the finished sums)
+        auto vm_of = [&](int q) { return PAR ? xm[q - O] + xp[q - O] : xm[q - O]; };
+        auto vp_of = [&](int q, int l) {
+            return PAR ? ((l & 1) ? xp[q - O] - xm[q - O] : xm[q - O] - xp[q - O]) : xp[q - O];
+        };
+#pragma unroll
+        for (int t = 1; t < LB; ++t) {
+#pragma unroll
+            for (int l = (t > LA ? t : LA); l < LB; ++l) {
+                const float wp = tb[Y.aup + tri(L, t, l)];
+                const float wm = tb[Y.aum + tri(L, t, l)];
+                a.up[t] = fmaf(vp_of(l * l + l + t, l), wp, a.up[t]);
+                a.vp[t] = fmaf(vp_of(l * l + l - t, l), wp, a.vp[t]);
+                a.um[t] = fmaf(vm_of(l * l + l + t), wm, a.um[t]);
+                a.vm[t] = fmaf(vm_of(l * l + l - t), wm, a.vm[t]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int l = (LA > 1 ? LA : 1); l < LB; ++l) {
+            const float w = tb[Y.aw + l];
+            a.wpl = fmaf(vp_of(l * l + l, l), w, a.wpl);
+            a.wmi = fmaf(vm_of(l * l + l), w, a.wmi);
+        }
+    }
+}
+
+// The step-(A) outputs from the finished sums (the closing steps of coef_to_theta_fourier).
+template <int L, bool SPIN, bool PAR>
+__device__ __forceinline__ void theta_sums_finish(const ThetaSums<L, SPIN>& a, const float* __restrict__ n0,
+                                                  bool second, float (&Ac)[L + 1], float (&As)[L + 1],
+                                                  float (&Bc)[L + 1], float (&Bs)[L + 1], float (&Cc)[L + 1],
+                                                  float (&Cs)[L + 1], float& dl, float& ep) {
+#pragma unroll
+    for (int t = 0; t <= L; ++t) {
+        Ac[t] = a.sc[t];
+        As[t] = t > 0 ? a.ss[t] : 0.f;
+    }
+    if constexpr (SPIN) {
+        const float hs = PAR ? 0.70710678118654752440f : 1.f;
+#pragma unroll
+        for (int t = 1; t <= L; ++t) {
+            float up = a.up[t], vp = a.vp[t], um = a.um[t], vm = a.vm[t];
+            if constexpr (PAR) up *= hs, vp *= hs, um *= hs, vm *= hs;
+            Bc[t] = up + um;
+            Bs[t] = -(vp + vm);
+            Cc[t] = vp - vm;
+            Cs[t] = up - um;
+        }
+        float wpl = a.wpl, wmi = a.wmi;
+        if constexpr (PAR) wpl *= hs, wmi *= hs;
+        float c[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = second ? n0[8 + i] : n0[i];
+        Bc[0] = fmaf(c[0], wpl, c[1] * wmi);
+        Cc[0] = fmaf(c[2], wpl, c[3] * wmi);
+        dl = fmaf(c[4], wpl, c[5] * wmi);
+        ep = fmaf(c[6], wpl, c[7] * wmi);
+        Bs[0] = 0.f;
+        Cs[0] = 0.f;
+    } else {
+        dl = ep = 0.f;
+    }
 }
 
 // Writes one unit's slot record (layout of PairShape) for this lane.
@@ -250,14 +375,15 @@ __device__ __forceinline__ void pair_publish(float* D, int sub, const float (&Q0
 // ---------------------------------------------------------------------------
 // Large-degree kernel (L = 9..16, fp32 I/O).  More nodes than a workgroup has
 // waves, and 32-unit input tiles that no longer fit in LDS: the nodes are
-// processed in rounds of W waves, each lane pair reads its unit's input rows
-// straight from global memory (cached in L1/L2), the spectra of one round are
-// exchanged in LDS, and every output group's owner lane accumulates the
-// round's contribution into the output row (written in round 0, then read,
-// added and written by the same lane in later rounds: ordered, deterministic).
-// Where LDS has room for it (L <= 12) the output rows of the tile live in LDS
-// across the rounds and leave in one coalesced store; above that they are
-// updated in global memory.
+// processed in rounds of W waves.  In each round the workgroup stages the tile's
+// input rows in LDS a chunk of degrees at a time (coalesced loads, the next
+// chunk's loads in flight while the waves work on the current one) and every
+// lane pair runs step (A) for its wave's node from there; the spectra of the
+// round are then exchanged in LDS (the same region), and every output group's
+// owner lane accumulates the round's contribution into the output row (written
+// in round 0, then read, added and written by the same lane in later rounds:
+// ordered, deterministic).  The output rows of the tile live in LDS across the
+// rounds and leave in one coalesced store.
 // ---------------------------------------------------------------------------
 template <int L, bool SPIN, int W>
 struct BigShape {
@@ -298,7 +424,38 @@ struct BigShape {
         while (k + 1 < K && t >= tlo(k + 1, K)) ++k;
         return k;
     }
+    // Step (A) reads the tile's 64 input rows (two per unit: lane 2u + i holds input
+    // i + 1 of unit u) from LDS.  They are staged in the spectra region, which is
+    // free until the round's spectra are published, one chunk of degrees
+    // [chunk_lo(c), chunk_lo(c + 1)) at a time: NS blocks of at most SCAP slots per
+    // row, odd row stride.
+    static constexpr int NS = SPIN ? 3 : 1;
+    static constexpr int BB = (L + 1) * (L + 1);
+    static constexpr int SROW = (DF / 64) % 2 ? DF / 64 : DF / 64 - 1;
+    static constexpr int SCAP = SROW / NS;
+    static_assert(2 * L + 1 <= SCAP, "a chunk holds at least one degree");
+    __host__ __device__ static constexpr int chunk_end(int la) {  // as many degrees as fit
+        int lb = la + 1;
+        while (lb <= L && (lb + 1) * (lb + 1) - la * la <= SCAP) ++lb;
+        return lb;
+    }
+    __host__ __device__ static constexpr int chunk_lo(int c) {
+        int la = 0;
+        for (int i = 0; i < c; ++i) la = chunk_end(la);
+        return la;
+    }
+    __host__ __device__ static constexpr int n_chunks() {
+        int n = 0;
+        for (int la = 0; la <= L; la = chunk_end(la)) ++n;
+        return n;
+    }
+    static constexpr int NCH = n_chunks();
 };
+
+template <typename F, int... I>
+__device__ __forceinline__ void for_each_index(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
 
 // Owners of the output groups with several spectrum parts: each part's groups are
 // spread over the waves by size (largest first, least-loaded wave).
@@ -374,8 +531,13 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     const bool valid = u < nvalid;
     const int64_t row = u0 + (valid ? u : 0);  // invalid lanes compute on a valid row, store nothing
     const float* g = tab;
-    const float* xr = sub ? x2 + (row / cpx2) * B::NC : x1 + row * B::NC;
     float* orow = out + row * B::NC;
+    // staging: TPR threads per input row (row r = lane r of every wave)
+    constexpr int TPR = B::THREADS / 64;
+    static_assert(B::THREADS % 64 == 0, "whole waves");
+    const int sr = tid / TPR, sk = tid % TPR;
+    const int64_t srow = u0 + ((sr >> 1) < nvalid ? (sr >> 1) : 0);
+    const float* ssrc = (sr & 1) ? x2 + (srow / cpx2) * B::NC : x1 + srow * B::NC;
 
     for (int i = tid; i < B::TRIG; i += B::THREADS) {
         const int sb = i / (B::NP * (L + 1));
@@ -402,10 +564,51 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
         const int node = r * W + wave;
         const int nr = (B::NT - r * W) < W ? (B::NT - r * W) : W;
         float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
+        // (A) chunk by chunk: stage the 64 rows' slots of the chunk's degrees, then
+        // every wave adds them to its node's sums
+        const float* tb = tab + Y.glob + (node < B::NT ? node : 0) * Y.pb;
+        ThetaSums<L, SPIN> acc;
+        theta_sums_zero(acc);
+        // software pipeline: chunk c + 1's global loads are in flight while the
+        // waves work on chunk c
+        constexpr int IT = (B::SCAP + TPR - 1) / TPR;  // staged values per block and thread
+        float pre[B::NS][IT];
+        auto fetch = [&](auto cc) {
+            constexpr int c = decltype(cc)::value;
+            constexpr int LA = B::chunk_lo(c), LB = B::chunk_lo(c + 1);
+            constexpr int CW = LB * LB - LA * LA;
+#pragma unroll
+            for (int b = 0; b < B::NS; ++b)
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int q = sk + it * TPR;
+                    if (it * TPR < CW) pre[b][it] = q < CW ? ssrc[b * B::BB + LA * LA + q] : 0.f;
+                }
+        };
+        auto chunk = [&](auto cc) {
+            constexpr int c = decltype(cc)::value;
+            constexpr int LA = B::chunk_lo(c), LB = B::chunk_lo(c + 1);
+            constexpr int CW = LB * LB - LA * LA, STR = (B::NS * CW) | 1;
+            if constexpr (c > 0) __syncthreads();  // every wave is done with the previous chunk
+#pragma unroll
+            for (int b = 0; b < B::NS; ++b)
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int q = sk + it * TPR;
+                    if (it * TPR < CW && q < CW) D[sr * STR + b * CW + q] = pre[b][it];
+                }
+            __syncthreads();
+            if constexpr (c + 1 < B::NCH) fetch(std::integral_constant<int, c + 1>{});
+            if (node < B::NT) theta_sums_add<L, SPIN, PAR, LA, LB>(D + lane * STR, tb, acc);
+        };
+        fetch(std::integral_constant<int, 0>{});
+        for_each_index(chunk, std::make_integer_sequence<int, B::NCH>{});
+        __syncthreads();  // the staged rows are read before the spectra take the region
         if (node < B::NT) {
-            const float* tb = tab + Y.glob + node * Y.pb;
+            float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
+            theta_sums_finish<L, SPIN, PAR>(acc, g + Y.n0, BWD && sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
             const float* trl = TR + sub * (B::NP * (L + 1));
-            pair_spectra<L, SPIN, BWD, PAR>(xr, tb, g, trl, sub, Q0, Q1, Q2, zslot);
+            pair_spectra_from_fourier<L, SPIN>(Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep, g, trl, sub, Q0, Q1, Q2, zslot);
         }
         // the round's spectra in K parts (orders t in [tlo(k), tlo(k + 1))): publish
         // part k, then every owner of a group of part k adds the round's nodes

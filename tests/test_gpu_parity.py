@@ -82,7 +82,7 @@ def test_ragged_spin_shapes(L, basis):
     run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=L)
 
 
-@pytest.mark.parametrize("L", [5, 6, 7, 8])
+@pytest.mark.parametrize("L", [4, 5, 6, 7, 8])
 @pytest.mark.parametrize("basis", [0, 1, 2])
 def test_ragged_valu_kernels(L, basis):
     # the fp32 vector-ALU kernels of the degrees that default to the matrix-core kernel
@@ -135,13 +135,23 @@ def test_matrix_core_bf16_against_reenactment(L, N, C, basis):
     assert worst <= 2.0 ** -10, worst
 
 
-@pytest.mark.parametrize("L,basis", [(9, 0), (9, 1), (12, 0), (16, 0)])
+@pytest.mark.parametrize("L,basis", [(9, 0), (9, 1), (10, 0), (11, 0), (12, 0), (13, 0), (13, 1), (14, 0), (15, 0),
+                                     (16, 0), (16, 1)])
 def test_ragged_large_degree(L, basis):
-    # 37 * 3 = 111 units: three full 32-unit tiles and a ragged tail of 15
+    # 37 * 3 = 111 units: three full 32-unit tiles and a ragged tail of 15; every
+    # degree, since each stages its input rows in its own chunks of degrees
     run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=L)
 
 
-@pytest.mark.parametrize("L", [0, 1, 2, 3, 4, 6, 8, 12])
+@pytest.mark.parametrize("L", [9, 16])
+def test_large_degree_many_tiles(L):
+    # 41 tiles of 32 units (more than one workgroup per XCD) and a ragged tail of 7;
+    # the oracle on the first, a middle and the last tiles
+    units = np.r_[0:40, 600:640, 1279:1319]
+    run_and_compare(L, L, L, S3, 1319, 1, "fp32", 0, seed=200 + L, units=units)
+
+
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 4, 6, 8, 12, 16])
 def test_ragged_scalar_shapes(L):
     run_and_compare(L, L, L, (0,), 29, 5, "fp32", 0, seed=10 + L)
 
@@ -184,10 +194,9 @@ def test_parity_basis_changes_the_map():
 
 @pytest.mark.parametrize("L", [9, 10, 11, 12, 13, 14, 15, 16])
 def test_parity_basis_large_degree(L):
-    # the large-degree kernels mix the input rows as they read them; the output tile
-    # in LDS (L = 9..12 with 8 waves, L = 13 with 7, L = 14 with 6) or accumulated in
-    # global memory (L = 15, 16); every degree, since these instantiations are built
-    # with their own scheduling strategy
+    # the large-degree kernels mix the input rows as step (A) reads them from the staged
+    # chunks; every degree, since these instantiations are built with their own
+    # scheduling strategy
     run_and_compare(L, L, L, S3, 37, 3, "fp32", 2, seed=100 + L)
 
 
