@@ -504,16 +504,43 @@ __device__ __forceinline__ void pair_publish_part(float* D, int sub, const float
     }
 }
 
+// Whether the last round splits its nodes' phi points over the idle waves.  Measured
+// on 262,144 units: it pays wherever the last round leaves waves idle, except where
+// the extra per-round state costs spills (paper basis L = 9: 0.89 -> 0.96 ms;
+// parity basis L = 12: 2.67 -> 2.93 ms; the scalar-spin kernels up to L = 13).
+template <int L, bool SPIN, bool PAR>
+constexpr bool big_split_last() {
+    if (!SPIN) return L == 16;
+    if (PAR) return L == 11 || L == 13 || L == 14 || L == 16;
+    return L >= 11;
+}
+
+// Whether the staging loads may stay hoisted out of the round loop: the compiler then
+// loads every chunk's rows once per tile and keeps them in registers, which pays
+// where they fit without spilling (L = 9 0.88 against 1.01 ms, L = 12 2.61 against
+// 2.80 on 262,144 units; from L = 13 on they spill 22-61 VGPRs, and the scalar-spin
+// kernels gain nothing).
+template <int L, bool SPIN, bool PAR>
+constexpr bool big_hoist_rows() {
+    return SPIN && L <= 12;
+}
+
 // PAR (spins only): the plan's basis is the parity-labelled one; a separate
 // instantiation, since a run-time switch between the two step-(A) forms costs the
 // paper-basis kernels registers.
 template <int L, bool SPIN, int W, bool BWD, bool PAR>
+// zero: 0 from the launcher.  The input rows are the same in every round, so the
+// compiler hoists the staging loads of all chunks out of the round loop; where they
+// do not fit in registers it holds them in scratch (106 spilled VGPRs at L = 16).
+// Offsetting them by round * zero keeps them in the loop, in flight one chunk ahead
+// (big_hoist_rows picks the degrees where the hoisted form fits).
 __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_big_kernel(
     const float* __restrict__ x1, const float* __restrict__ x2, float* __restrict__ out, int64_t units, int64_t cpx2,
-    const float* __restrict__ tab) {
+    const float* __restrict__ tab, int zero) {
     using B = BigShape<L, SPIN, W>;
     using P = typename B::PS;
     constexpr Layout Y = B::Y;
+    constexpr bool SPLIT = big_split_last<L, SPIN, PAR>();
     constexpr int TM1 = Y.TM + 1;
     constexpr int BO = (L + 1) * (L + 1);
     __shared__ float lds[B::LDS_FLOATS];
@@ -561,18 +588,26 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     constexpr Owners<P::NG> own = K == 1 ? assign_pair_owners<L, SPIN, W>() : assign_part_owners<L, SPIN, W, K>();
 #pragma unroll 1
     for (int r = 0; r < B::ROUNDS; ++r) {
-        const int node = r * W + wave;
+        // A round takes nr nodes.  With SPLIT, a round with fewer nodes than waves (the
+        // last one) splits each node's phi points over nsplit = W / nr waves: wave w
+        // takes node r W + w % nr, part w / nr, and publishes a partial record; the
+        // owners' sum over the nw = nr nsplit records below adds the parts up.
         const int nr = (B::NT - r * W) < W ? (B::NT - r * W) : W;
+        const int nsplit = SPLIT ? W / nr : 1, nw = SPLIT ? nr * nsplit : nr;
+        const int node = SPLIT ? r * W + wave % nr : r * W + wave;
+        const int ppart = SPLIT ? wave / nr : 0;
+        const bool active = SPLIT ? wave < nw : node < B::NT;
         float Q0[L + 1], Q1[L + 1], Q2[L + 1], zslot;
         // (A) chunk by chunk: stage the 64 rows' slots of the chunk's degrees, then
         // every wave adds them to its node's sums
-        const float* tb = tab + Y.glob + (node < B::NT ? node : 0) * Y.pb;
+        const float* tb = tab + Y.glob + (active ? node : 0) * Y.pb;
         ThetaSums<L, SPIN> acc;
         theta_sums_zero(acc);
         // software pipeline: chunk c + 1's global loads are in flight while the
         // waves work on chunk c
         constexpr int IT = (B::SCAP + TPR - 1) / TPR;  // staged values per block and thread
         float pre[B::NS][IT];
+        const float* rsrc = big_hoist_rows<L, SPIN, PAR>() ? ssrc : ssrc + r * zero;
         auto fetch = [&](auto cc) {
             constexpr int c = decltype(cc)::value;
             constexpr int LA = B::chunk_lo(c), LB = B::chunk_lo(c + 1);
@@ -582,7 +617,7 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
 #pragma unroll
                 for (int it = 0; it < IT; ++it) {
                     const int q = sk + it * TPR;
-                    if (it * TPR < CW) pre[b][it] = q < CW ? ssrc[b * B::BB + LA * LA + q] : 0.f;
+                    if (it * TPR < CW) pre[b][it] = q < CW ? rsrc[b * B::BB + LA * LA + q] : 0.f;
                 }
         };
         auto chunk = [&](auto cc) {
@@ -599,23 +634,31 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
                 }
             __syncthreads();
             if constexpr (c + 1 < B::NCH) fetch(std::integral_constant<int, c + 1>{});
-            if (node < B::NT) theta_sums_add<L, SPIN, PAR, LA, LB>(D + lane * STR, tb, acc);
+            if (active) theta_sums_add<L, SPIN, PAR, LA, LB>(D + lane * STR, tb, acc);
         };
         fetch(std::integral_constant<int, 0>{});
         for_each_index(chunk, std::make_integer_sequence<int, B::NCH>{});
         __syncthreads();  // the staged rows are read before the spectra take the region
-        if (node < B::NT) {
+        if (active) {
             float Pc0[L + 1], Ps0[L + 1], Pc1[L + 1], Ps1[L + 1], Pc2[L + 1], Ps2[L + 1], dl, ep;
             theta_sums_finish<L, SPIN, PAR>(acc, g + Y.n0, BWD && sub != 0, Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep);
             const float* trl = TR + sub * (B::NP * (L + 1));
-            pair_spectra_from_fourier<L, SPIN>(Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep, g, trl, sub, Q0, Q1, Q2, zslot);
+            if constexpr (SPLIT) {
+                constexpr int KP = (B::NP - 1) / 2;  // phi-point pairs k = 1..KP
+                const int k_lo = 1 + ppart * KP / nsplit, k_hi = 1 + (ppart + 1) * KP / nsplit;
+                pair_spectra_from_fourier<L, SPIN>(Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep, g, trl, sub, Q0, Q1, Q2,
+                                                   zslot, k_lo, k_hi, ppart == 0);
+            } else {
+                pair_spectra_from_fourier<L, SPIN>(Pc0, Ps0, Pc1, Ps1, Pc2, Ps2, dl, ep, g, trl, sub, Q0, Q1, Q2,
+                                                   zslot);
+            }
         }
         // the round's spectra in K parts (orders t in [tlo(k), tlo(k + 1))): publish
         // part k, then every owner of a group of part k adds the round's nodes
         auto part = [&](auto kc) {
             constexpr int k = decltype(kc)::value;
             constexpr int T_LO = B::tlo(k, K), T_HI = B::tlo(k + 1, K);
-            if (node < B::NT)
+            if (active)
                 pair_publish_part<L, SPIN, T_LO, T_HI>(D + (wave * B::UNITS + u) * B::DSP, sub, Q0, Q1, Q2, zslot);
             __syncthreads();
 #pragma unroll
@@ -630,9 +673,9 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
 #pragma unroll
                 for (int l = 0; l <= L; ++l) acc[l] = 0.f;
 #pragma unroll 1
-                for (int jj = 0; jj < nr; ++jj) {
+                for (int jj = 0; jj < nw; ++jj) {
                     const float d = D[(jj * B::UNITS + u) * B::DSP + P::slot(gi) - B::sbase(T_LO) + sub];
-                    const float* te = tab + Y.glob + (r * W + jj) * Y.pb;
+                    const float* te = tab + Y.glob + (r * W + (SPLIT ? jj % nr : jj)) * Y.pb;
 #pragma unroll
                     for (int l = P::lmin(gi); l <= L; ++l)
                         acc[l] = fmaf(te[kind == 3 ? tab_base + l : tab_base + tri(L, t, l)], d, acc[l]);
@@ -674,7 +717,7 @@ hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, 
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W, BWD, PAR>), dim3(static_cast<unsigned>(blocks)), dim3(B::THREADS),
                        0, stream, static_cast<const float*>(x1), static_cast<const float*>(x2),
-                       static_cast<float*>(out), units, cpx2, tab);
+                       static_cast<float*>(out), units, cpx2, tab, 0);
     return hipGetLastError();
 }
 
