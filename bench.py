@@ -916,7 +916,9 @@ def run_uvw(args):
     channels, one edge channel (V = 1), B edges, spins (-1, 0, +1), fp32.  Time per call
     (HIP events on the launch stream, fill kernel included), the channel mixing's flops
     (2 U V W d3 per edge and path, run on the fp32 matrix cores) against the fp32 matrix-core
-    peak, and the relative L2 error on sampled edges against the oracle."""
+    peak, and the relative L2 error on sampled edges against the oracle.  Then the same for
+    spingtp_backward_fully_connected (all three gradients per call: three mixings of that
+    size), against the oracle's reverse mode."""
     import numpy as np
     import torch
 
@@ -960,11 +962,50 @@ def run_uvw(args):
         rows.append(row)
         print(f"[uvw] ({L1},{L2},{LO}) C={C} B={B}: {ms * 1e3:.1f} us, mixing {row['mix_tflops']:.2f} TF/s, "
               f"parity {rel:.2e}", file=sys.stderr, flush=True)
-    print(json.dumps({"metric": "fully connected SpinGTP (mode uvw) forward time on the App. E.2 shapes",
+    # the gradients (spingtp_backward_fully_connected), after every forward so that a kernel
+    # trace splits into the two phases by dispatch order
+    for row in rows:
+        L1, L2, LO, C, B = row["L1"], row["L2"], row["Lout"], row["C"], row["B"]
+        U, V, W = C, 1, C
+        plan = Plan(L1, L2, LO, workloads.SPINS, "fp32", fully_connected=True)
+        x1 = workloads.draw(L1, B, U, 7300 + C, "fp32", workloads.SPINS, "unit", "cuda:0")
+        x2 = workloads.draw(L2, B, V, 7400 + C, "fp32", workloads.SPINS, "unit", "cuda:0")
+        g = torch.Generator(device="cuda:0")
+        g.manual_seed(7500 + B)
+        w = torch.randn((plan.n_paths, U, V, W), generator=g, device="cuda:0") / np.sqrt(U * V)
+        gy = torch.randn((B, W) + tuple(plan.shape_out), generator=g, device="cuda:0")
+        grads = plan.backward_fully_connected(x1, x2, w, gy)
+        for _ in range(args.warmup):
+            plan.backward_fully_connected(x1, x2, w, gy)
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(args.steps):
+            plan.backward_fully_connected(x1, x2, w, gy)
+        e.record()
+        torch.cuda.synchronize()
+        bms = s.elapsed_time(e) / args.steps
+        sel = np.unique(np.concatenate([np.arange(min(B, 8)), np.arange(max(0, B - 8), B), [B // 2]]))
+        ti = torch.as_tensor(sel, device="cuda:0")
+        ref = oracle.fully_connected_vjp(x1[ti].double().cpu().numpy().reshape(len(sel), U, -1),
+                                         x2[ti].double().cpu().numpy().reshape(len(sel), V, -1),
+                                         w.double().cpu().numpy(), gy[ti].double().cpu().numpy().reshape(len(sel), W, -1),
+                                         L1, L2, LO, workloads.SPINS, 0)
+        # grad_weights sums over the edges: compared on a call given the sampled edges' rows alone
+        gw_sel = plan.backward_fully_connected(x1[ti].contiguous(), x2[ti].contiguous(), w, gy[ti].contiguous(),
+                                               need=(False, False, True))[2]
+        got = (grads[0][ti], grads[1][ti], gw_sel)
+        rels = [float(np.linalg.norm(a.double().cpu().numpy().reshape(r.shape) - r) / np.linalg.norm(r))
+                for a, r in zip(got, ref)]
+        row.update({"bwd_ms": bms, "bwd_mix_flops": 3 * row["mix_flops"],
+                    "bwd_parity_rel_l2_sampled": {"grad_x1": rels[0], "grad_x2": rels[1], "grad_w": rels[2]}})
+        print(f"[uvw-bwd] ({L1},{L2},{LO}) C={C} B={B}: {bms * 1e3:.1f} us, parity "
+              f"{max(rels):.2e}", file=sys.stderr, flush=True)
+    print(json.dumps({"metric": "fully connected SpinGTP (mode uvw) forward and backward time on the App. E.2 shapes",
                       "unit": "ms", "higher_is_better": False, "n_gpus": 1, "steps": args.steps,
                       "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
                       "config": {"workload": "App. E.2 shapes, U = W = C, V = 1, spins (-1,0,1), N(0,1) inputs, "
-                                             "N(0,1)/sqrt(U V) weights"},
+                                             "N(0,1)/sqrt(U V) weights, N(0,1) output gradients"},
                       "rows": rows}), flush=True)
 
 

@@ -439,6 +439,28 @@ spingtp_status spingtp_forward_fully_connected(spingtp_plan plan, const void* x1
                                                const float* weights, void* out, int64_t N, int64_t U, int64_t V,
                                                int64_t W, void* stream);
 
+/*
+ * Gradients of spingtp_forward_fully_connected (reverse mode; App. E.1 mode uvw, Sec. 3.5
+ * eq. spin_gtp, chain rule through R_p and the channel mixing) for g = grad_out = dL/dout:
+ *   grad_x1[n][u][k1]       = sum_p sum_{v,w} weights[p][u][v][w] sum_{(k1,k2,k3) in p} T x2[n][v][k2] g[n][w][k3],
+ *   grad_x2[n][v][k2]       = sum_p sum_{u,w} weights[p][u][v][w] sum_{(k1,k2,k3) in p} T x1[n][u][k1] g[n][w][k3],
+ *   grad_weights[p][u][v][w] = sum_n sum_{k3 in p's output block} R_p[n][u][v][k3] g[n][w][k3].
+ *   x1, x2, weights: as for the forward; grad_out [N][W][n_spins][(Lout+1)^2] fp32,
+ *   16-byte aligned; grad_x1, grad_x2 shaped like x1 and x2 (16-byte aligned) and
+ *   grad_weights like weights (4-byte aligned), each overwritten, or nullptr to skip
+ *   that gradient.  Slots with l < |s| and blocks no path reaches get 0; with N = 0,
+ *   grad_weights is 0.  U, V, W <= 65536 and U V, V W, U W <= 2^24.
+ * Needs an fp32 plan created with SPINGTP_FULLY_CONNECTED (else SPINGTP_ERR_UNSUPPORTED).
+ * fp32 products and sums (grad_x1 and grad_x2 on the forward's kernel with the tensor's
+ * axes exchanged, grad_weights on the matrix cores with the edges as the reduction);
+ * asynchronous on `stream`, no allocation; deterministic (every element has one owner
+ * that sums in a fixed order).
+ */
+spingtp_status spingtp_backward_fully_connected(spingtp_plan plan, const void* x1, const void* x2,
+                                                const float* weights, const void* grad_out, void* grad_x1,
+                                                void* grad_x2, float* grad_weights, int64_t N, int64_t U, int64_t V,
+                                                int64_t W, void* stream);
+
 /* Bytes of workspace spingtp_backward_v1 needs for grad_x2 with N x C units:
  * N C n_spins (L2+1)^2 elements of the plan's dtype.  SPINGTP_ERR_UNSUPPORTED as
  * for spingtp_backward_v1. */

@@ -20,7 +20,8 @@ EXPORTED = ("spingtp_plan_create", "spingtp_forward", "spingtp_plan_destroy", "s
             "spingtp_backward_v1_weighted_workspace_size", "spingtp_forward_weighted", "spingtp_backward_weighted",
             "spingtp_backward_weighted_workspace_size", "spingtp_forward_depthwise", "spingtp_backward_depthwise",
             "spingtp_backward_depthwise_workspace_size", "spingtp_backward_v1_noalloc",
-            "spingtp_plan_upload_selftest_host", "spingtp_forward_fully_connected")
+            "spingtp_plan_upload_selftest_host", "spingtp_forward_fully_connected",
+            "spingtp_backward_fully_connected")
 
 _lib = None
 
@@ -116,6 +117,8 @@ def lib() -> ctypes.CDLL:
         L.spingtp_plan_upload_selftest_host.restype = ctypes.c_int
         L.spingtp_forward_fully_connected.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int64] * 4 + [ctypes.c_void_p]
         L.spingtp_forward_fully_connected.restype = ctypes.c_int
+        L.spingtp_backward_fully_connected.argtypes = [ctypes.c_void_p] * 8 + [ctypes.c_int64] * 4 + [ctypes.c_void_p]
+        L.spingtp_backward_fully_connected.restype = ctypes.c_int
         L.spingtp_backward_v1_workspace_size.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                                          ctypes.POINTER(ctypes.c_size_t)]
         L.spingtp_backward_v1_workspace_size.restype = ctypes.c_int

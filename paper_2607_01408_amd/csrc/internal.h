@@ -201,20 +201,40 @@ void tensor_paths(int L1, int L2, int LO, const int* spins, int n_spins, const s
 void weight_paths(int L1, int L2, int LO, const int* spins, int n_spins, const std::vector<std::array<int, 3>>& paths,
                   const double* w, std::vector<double>& T);
 
-// Fully connected product (mode uvw): entry table of spingtp_forward_fully_connected.
-// Words: header [kUvwHeader]: n_paths, n_blocks (output blocks reached by a path), nc1,
-// nc2, nco, max_d3, first word of the path records, first word of the entries.
-// Then per block (4 words): slot offset o3 of the block in the output row, its width
-// d3, first path record, path count.  Per path record (4 words): path index (the
-// weights' leading index), d3, first word of its d3 + 1 entry offsets, 0.  The offsets
+// Fully connected product (mode uvw): entry tables of spingtp_forward_fully_connected
+// (role 0: inputs x1, x2, output out) and of the gradients w.r.t. x1 (role 1: inputs x2
+// and grad_out, output grad_x1) and x2 (role 2: inputs x1 and grad_out, output grad_x2);
+// "a", "b" and "o" below are the role's first input, second input and output.
+// Words: header [kUvwHeader]: n_paths, n_blocks (output blocks reached by a path), the
+// row widths of a, b and o, max_d3, first word of the path records, first word of the
+// entries.  Then per block (4 words): slot offset o3 of the block in the output row, its
+// width d3, first path record, path count.  Per path record (kUvwRec words): path index
+// (the weights' leading index), d3, first word of its d3 + 1 entry offsets, then the
+// path's block of x1, of x2 and of the forward's output as first slot | width << 16
+// each.  The offsets
 // (absolute entry numbers) delimit its entries by output component m3; an entry is two
-// words: k1 | k2 << 16 and the fp32 value.
+// words: ka | kb << 16 and the fp32 value T (at (k1, k2, k3) = (ka, kb, o3 + m3) for
+// role 0, (o3 + m3, ka, kb) for role 1, (ka, o3 + m3, kb) for role 2).
 constexpr int kUvwHeader = 8;
+constexpr int kUvwRec = 6;
 constexpr int kUvwChunk = 8;  // output components per workgroup (the kernel's accumulators)
 bool build_uvw_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
-                     std::vector<uint32_t>& out, const std::vector<double>* dense = nullptr);
-hipError_t launch_fwd_uvw(const float* x1, const float* x2, const float* w, float* out, int64_t N, int U, int V,
-                          int W, const uint32_t* table, int n_blocks, int max_d3, int nco, hipStream_t stream);
+                     std::vector<uint32_t>& out, const std::vector<double>* dense = nullptr, int role = 0);
+// One role's product and channel mixing: out[n][o][k] = sum_p sum_(a, b) weights[p-th block
+// + a sa + b sb + o so] R_p[n][(a, b)][k], R_p from xa [N][A][.] and xb [N][B][.]; the
+// output (N x O rows of nco floats) is written 0 first.
+hipError_t launch_uvw_mix(const float* xa, const float* xb, const float* w, float* out, int64_t N, int A, int B, int O,
+                          int64_t sa, int64_t sb, int64_t so, int64_t ps, const uint32_t* table, int n_blocks,
+                          int max_d3, int nco, hipStream_t stream);
+// grad_w[p][u][v][w] = sum_n sum_(k3 in p) R_p[n][(u, v)][k3] g[n][w][k3] (role-0 table).
+hipError_t launch_uvw_grad_w(const float* x1, const float* x2, const float* g, float* gw, int64_t N, int U, int V,
+                             int W, const uint32_t* table, int n_paths, int nco, hipStream_t stream);
+// grad_x2 through gR_p = W_p g (role-0 table; the blocks of x2 from the role-2 table); LDS
+// bytes it needs for blocks of x1 and x2 up to d1max and d2max wide (0 if more than a CU has).
+size_t uvw_grad_x2_lds(int d1max, int d2max);
+hipError_t launch_uvw_grad_x2(const float* x1, const float* g, const float* w, float* gx2, int64_t N, int U, int V,
+                              int W, const uint32_t* table, const uint32_t* table2, int n_blocks2, int n_paths,
+                              int nc1, int nc2, int nco, int d1max, int d2max, hipStream_t stream);
 
 // Dense real tensor of the operation (see spingtp_dense_tensor_host), float64.
 void build_dense_tensor(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
@@ -245,8 +265,11 @@ struct spingtp_plan_s {
     uint32_t* d_dir_b2;  //   the gradients run on the direct kernel
     const spingtp::KernelEntry* kernel_dir;  // the direct kernel of d_dir_b1 and d_dir_b2
     int dir_lds_floats;  // LDS of the direct kernel's tiles (the same for its three tables)
-    uint32_t* d_uvw;  // entry table of spingtp_forward_fully_connected, nullptr unless SPINGTP_FULLY_CONNECTED
-    int uvw_blocks, uvw_max_d3;
+    // entry tables of the fully connected product (SPINGTP_FULLY_CONNECTED, else nullptr):
+    // roles 0 (forward), 1 and 2 (gradients w.r.t. x1 and x2), each from word uvw_off[role]
+    uint32_t* d_uvw;
+    size_t uvw_off[3];
+    int uvw_blocks[3], uvw_max_d3[3], uvw_paths;
     const spingtp::KernelEntry* kernel;     // spingtp_forward
     const spingtp::KernelEntry* kernel_v1;  // spingtp_forward_v1 (x2 shared by the channels of an edge)
 };

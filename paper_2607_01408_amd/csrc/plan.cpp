@@ -863,7 +863,7 @@ void weight_paths(int L1, int L2, int LO, const int* spins, int n_spins, const s
 }
 
 bool build_uvw_table(int L1, int L2, int LO, const int* spins, int n_spins, unsigned flags,
-                     std::vector<uint32_t>& out, const std::vector<double>* dense) {
+                     std::vector<uint32_t>& out, const std::vector<double>* dense, int role) {
     std::vector<double> own;
     if (dense == nullptr) build_dense_tensor(L1, L2, LO, spins, n_spins, flags, own);
     const std::vector<double>& T = dense != nullptr ? *dense : own;
@@ -872,35 +872,44 @@ bool build_uvw_table(int L1, int L2, int LO, const int* spins, int n_spins, unsi
     const std::vector<int> b1 = slot_blocks(L1, spins, n_spins), b2 = slot_blocks(L2, spins, n_spins),
                            b3 = slot_blocks(LO, spins, n_spins);
     const int nc1 = static_cast<int>(b1.size()), nc2 = static_cast<int>(b2.size()), nco = static_cast<int>(b3.size());
-    if (nc1 > 0xffff || nc2 > 0xffff) return false;
+    // tensor axes (0: x1, 1: x2, 2: out) of the role's first input, second input and output
+    const int ax_a = role == 1 ? 1 : 0, ax_b = role == 0 ? 1 : 2, ax_o = role == 0 ? 2 : (role == 1 ? 0 : 1);
+    const int widths[3] = {nc1, nc2, nco};
+    const std::vector<int>* blk_of[3] = {&b1, &b2, &b3};
+    const std::vector<int>& bo = *blk_of[ax_o];
+    if (widths[ax_a] > 0xffff || widths[ax_b] > 0xffff) return false;
     std::map<std::array<int, 3>, int> index;
     for (size_t p = 0; p < paths.size(); ++p) index[paths[p]] = static_cast<int>(p);
-    // first slot and width of every output block
-    std::map<int, std::pair<int, int>> span;
-    for (int k = 0; k < nco; ++k)
-        if (b3[k] >= 0) {
-            auto it = span.find(b3[k]);
-            if (it == span.end()) span[b3[k]] = {k, 1};
+    // first slot and width of every block of each axis; span: the role's output axis
+    std::map<int, std::pair<int, int>> spans[3];
+    for (int ax = 0; ax < 3; ++ax)
+        for (int k = 0; k < widths[ax]; ++k) {
+            const int b = (*blk_of[ax])[k];
+            if (b < 0) continue;
+            auto it = spans[ax].find(b);
+            if (it == spans[ax].end()) spans[ax][b] = {k, 1};
             else ++it->second.second;
         }
+    const std::map<int, std::pair<int, int>>& span = spans[ax_o];
     // entries per path and output component
     std::vector<std::vector<std::vector<std::pair<uint32_t, float>>>> ent(paths.size());
-    for (size_t p = 0; p < paths.size(); ++p) ent[p].resize(span.at(paths[p][2]).second);
+    for (size_t p = 0; p < paths.size(); ++p) ent[p].resize(span.at(paths[p][ax_o]).second);
     for (int k1 = 0; k1 < nc1; ++k1)
         for (int k2 = 0; k2 < nc2; ++k2)
             for (int k3 = 0; k3 < nco; ++k3) {
                 const double v = T[(static_cast<size_t>(k1) * nc2 + k2) * nco + k3];
                 if (std::fabs(v) <= 1e-12) continue;
                 const int p = index.at({b1[k1], b2[k2], b3[k3]});
-                ent[p][k3 - span.at(b3[k3]).first].push_back(
-                    {static_cast<uint32_t>(k1) | (static_cast<uint32_t>(k2) << 16), static_cast<float>(v)});
+                const int k[3] = {k1, k2, k3};
+                ent[p][k[ax_o] - span.at(bo[k[ax_o]]).first].push_back(
+                    {static_cast<uint32_t>(k[ax_a]) | (static_cast<uint32_t>(k[ax_b]) << 16), static_cast<float>(v)});
             }
     // output blocks in slot order, each with its paths
     std::vector<int> blocks;
     for (const auto& kv : span) blocks.push_back(kv.first);
     std::vector<std::vector<int>> by_block(blocks.size());
     for (size_t p = 0; p < paths.size(); ++p)
-        by_block[std::lower_bound(blocks.begin(), blocks.end(), paths[p][2]) - blocks.begin()].push_back(
+        by_block[std::lower_bound(blocks.begin(), blocks.end(), paths[p][ax_o]) - blocks.begin()].push_back(
             static_cast<int>(p));
     std::vector<int> used;
     for (size_t b = 0; b < blocks.size(); ++b)
@@ -908,7 +917,7 @@ bool build_uvw_table(int L1, int L2, int LO, const int* spins, int n_spins, unsi
     int max_d3 = 0;
     for (int b : used) max_d3 = std::max(max_d3, span.at(blocks[b]).second);
     const size_t rec0 = kUvwHeader + 4 * used.size();
-    const size_t csr0 = rec0 + 4 * paths.size();
+    const size_t csr0 = rec0 + kUvwRec * paths.size();
     size_t n_csr = 0, n_ent = 0;
     for (size_t p = 0; p < paths.size(); ++p) {
         n_csr += ent[p].size() + 1;
@@ -917,8 +926,8 @@ bool build_uvw_table(int L1, int L2, int LO, const int* spins, int n_spins, unsi
     const size_t ent0 = csr0 + n_csr;
     out.assign(ent0 + 2 * n_ent, 0u);
     const uint32_t hdr[kUvwHeader] = {static_cast<uint32_t>(paths.size()), static_cast<uint32_t>(used.size()),
-                                      static_cast<uint32_t>(nc1), static_cast<uint32_t>(nc2),
-                                      static_cast<uint32_t>(nco), static_cast<uint32_t>(max_d3),
+                                      static_cast<uint32_t>(widths[ax_a]), static_cast<uint32_t>(widths[ax_b]),
+                                      static_cast<uint32_t>(widths[ax_o]), static_cast<uint32_t>(max_d3),
                                       static_cast<uint32_t>(rec0), static_cast<uint32_t>(ent0)};
     std::copy(hdr, hdr + kUvwHeader, out.begin());
     size_t rec = 0, csr = csr0, e_next = 0;
@@ -931,10 +940,14 @@ bool build_uvw_table(int L1, int L2, int LO, const int* spins, int n_spins, unsi
         w[2] = static_cast<uint32_t>(rec);
         w[3] = static_cast<uint32_t>(by_block[b].size());
         for (int p : by_block[b]) {
-            uint32_t* r = &out[rec0 + 4 * rec++];
+            uint32_t* r = &out[rec0 + kUvwRec * rec++];
             r[0] = static_cast<uint32_t>(p);
             r[1] = static_cast<uint32_t>(sp.second);
             r[2] = static_cast<uint32_t>(csr);
+            for (int ax = 0; ax < 3; ++ax) {  // the path's block of x1, x2 and the output
+                const auto& bs = spans[ax].at(paths[p][ax]);
+                r[3 + ax] = static_cast<uint32_t>(bs.first) | (static_cast<uint32_t>(bs.second) << 16);
+            }
             for (const auto& comp : ent[p]) {
                 out[csr++] = static_cast<uint32_t>(e_next);
                 for (const auto& e : comp) {
@@ -1246,6 +1259,7 @@ struct PlanHost {
     const spingtp::KernelEntry *k = nullptr, *kd = nullptr, *kv1 = nullptr, *kw = nullptr;
     std::vector<double> tab, tab_bwd;
     std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2, pre_w, bw1w, uvw;
+    size_t uvw_off[3] = {0, 0, 0};  // first word of each role's table in uvw
     spingtp::Bw1wShape bw1w_shape{};
     bool has_backward = false, same_bwd = false;
 };
@@ -1351,9 +1365,17 @@ spingtp_status build_plan_host(int L1, int L2, int Lout, const int* spins, int n
             spingtp::build_direct_table(L1, L2, Lout, spins, n_spins, basis, 2, dir_b2, &lds_floats, &dense);
         }
         if (k != nullptr && k->family == 4) spingtp::build_mfma_operands(L1, aux);
-        if ((flags & SPINGTP_FULLY_CONNECTED) &&
-            !spingtp::build_uvw_table(L1, L2, Lout, spins, n_spins, basis, h.uvw, dense.empty() ? nullptr : &dense))
-            return SPINGTP_ERR_UNSUPPORTED;
+        if (flags & SPINGTP_FULLY_CONNECTED) {
+            // the forward's table, then those of the gradients w.r.t. x1 and x2, in one buffer
+            for (int role = 0; role < 3; ++role) {
+                std::vector<uint32_t> t;
+                if (!spingtp::build_uvw_table(L1, L2, Lout, spins, n_spins, basis, t, dense.empty() ? nullptr : &dense,
+                                              role))
+                    return SPINGTP_ERR_UNSUPPORTED;
+                h.uvw_off[role] = h.uvw.size();
+                h.uvw.insert(h.uvw.end(), t.begin(), t.end());
+            }
+        }
         if (kv1->family == 5 &&
             !spingtp::build_pre_tables(L1, L2, Lout, spins, n_spins, basis, pre, false, weighted ? &dense : nullptr))
             return SPINGTP_ERR_INTERNAL;
@@ -1486,8 +1508,13 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     p->d_bw1w = d.bw1w;
     p->bw1w = h.bw1w_shape;
     p->d_uvw = d.uvw;
-    p->uvw_blocks = h.uvw.empty() ? 0 : static_cast<int>(h.uvw[1]);
-    p->uvw_max_d3 = h.uvw.empty() ? 0 : static_cast<int>(h.uvw[5]);
+    for (int role = 0; role < 3; ++role) {
+        const size_t o = h.uvw_off[role];
+        p->uvw_off[role] = o;
+        p->uvw_blocks[role] = h.uvw.empty() ? 0 : static_cast<int>(h.uvw[o + 1]);
+        p->uvw_max_d3[role] = h.uvw.empty() ? 0 : static_cast<int>(h.uvw[o + 5]);
+    }
+    p->uvw_paths = h.uvw.empty() ? 0 : static_cast<int>(h.uvw[0]);
     p->kernel = h.k;
     p->kernel_v1 = h.kv1;
     *out_plan = p;

@@ -467,6 +467,36 @@ class Plan:
                    "spingtp_forward_fully_connected")
         return out
 
+    def backward_fully_connected(self, x1, x2, weights, grad_out, need=(True, True, True), stream=None):
+        """spingtp_backward_fully_connected: the gradients (grad_x1, grad_x2, grad_weights) of
+        forward_fully_connected for grad_out [N, W, ...]; `need` picks which are computed
+        (the others are returned as None)."""
+        import torch
+
+        if x1.dim() != 4 or x2.dim() != 4 or weights.dim() != 4 or grad_out.dim() != 4:
+            raise ValueError("x1 [N, U, ...], x2 [N, V, ...], weights [n_paths, U, V, W], grad_out [N, W, ...]")
+        N, U, V, W = x1.shape[0], x1.shape[1], x2.shape[1], weights.shape[3]
+        for t, shape in ((x1, (N, U) + tuple(self.shape_in(1))), (x2, (N, V) + tuple(self.shape_in(2))),
+                         (grad_out, (N, W) + tuple(self.shape_out))):
+            if tuple(t.shape) != shape or t.dtype != self.torch_dtype or not t.is_cuda or not t.is_contiguous():
+                raise ValueError("x1, x2, grad_out must be contiguous device tensors of the plan's dtype and shape")
+        if (tuple(weights.shape) != (self.n_paths, U, V, W) or weights.dtype != torch.float32 or not weights.is_cuda
+                or not weights.is_contiguous()):
+            raise ValueError(f"weights must be a contiguous fp32 device tensor [{self.n_paths}, U, V, W]")
+        g1 = torch.empty_like(x1) if need[0] else None
+        g2 = torch.empty_like(x2) if need[1] else None
+        gw = torch.empty_like(weights) if need[2] else None
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+
+        def ptr(t):
+            return t.data_ptr() if t is not None and t.numel() else None
+
+        _lib.check(_lib.lib().spingtp_backward_fully_connected(
+            self._handle, ptr(x1), ptr(x2), ptr(weights), ptr(grad_out), ptr(g1), ptr(g2), ptr(gw), N, U, V, W,
+            ctypes.c_void_p(stream.cuda_stream)), "spingtp_backward_fully_connected")
+        return g1, g2, gw
+
     def forward_depthwise(self, x1, x2, weights, out=None, stream=None):
         """spingtp_forward_depthwise: x2 [N, V, ...] with V >= 1 channels per edge, weights [V, C, n_paths]."""
         import torch

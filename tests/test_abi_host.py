@@ -746,13 +746,16 @@ def emulate_uvw_table(words, x1, x2, W, nco):
         o3, d3, first, count = (int(v) for v in w[8 + 4 * b:12 + 4 * b])
         assert d3 <= max_d3
         for r in range(first, first + count):
-            pid, d3r, csr = (int(v) for v in w[rec0 + 4 * r:rec0 + 4 * r + 3])
+            pid, d3r, csr, b1, b2, b3 = (int(v) for v in w[rec0 + 6 * r:rec0 + 6 * r + 6])
             assert d3r == d3 and pid not in seen
+            assert (b3 & 0xFFFF, b3 >> 16) == (o3, d3)      # the path's output block
             seen.add(pid)
             for m3 in range(d3):
                 for k in range(int(w[csr + m3]), int(w[csr + m3 + 1])):
                     ix = int(w[ent0 + 2 * k])
                     t = float(vals[ent0 + 2 * k + 1])
+                    # the entry lies in the path's blocks of x1 and x2
+                    assert 0 <= (ix & 0xFFFF) - (b1 & 0xFFFF) < b1 >> 16 and 0 <= (ix >> 16) - (b2 & 0xFFFF) < b2 >> 16
                     R = t * x1[:, :, ix & 0xFFFF, None] * x2[:, None, :, ix >> 16]      # [N, U, V]
                     out[:, :, o3 + m3] += np.einsum("nuv,uvw->nw", R, W[pid])
     assert seen == set(range(n_paths))

@@ -122,3 +122,126 @@ def test_uvw_bitwise_deterministic():
     y2 = plan.forward_fully_connected(x1, x2, w)
     torch.cuda.synchronize()
     assert torch.equal(y, y2)
+
+
+# --- gradients (spingtp_backward_fully_connected) against the oracle's reverse mode ---
+
+def run_uvw_backward(L1, L2, LO, spins, N, U, V, W, basis=0, seed=0, edges=None):
+    """All three gradients on the device against oracle.fully_connected_vjp.  grad_x1 and
+    grad_x2 are compared on the sampled edges; grad_weights sums over every edge, so with
+    `edges` it is compared on a second call given only the sampled edges' rows.  Returns
+    the gradients of the call over all N edges."""
+    print(f"[uvw-bwd] L=({L1},{L2},{LO}) spins={spins} N={N} U={U} V={V} W={W} basis={basis}", flush=True)
+    plan = Plan(L1, L2, LO, spins, "fp32", basis, fully_connected=True)
+    x1 = workloads.draw(L1, N, U, 5600 + seed, "fp32", spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, V, 5700 + seed, "fp32", spins, "unit", "cuda")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5800 + seed)
+    w = torch.randn((plan.n_paths, U, V, W), generator=gen, device="cuda") / np.sqrt(max(1, U * V))
+    gy = torch.randn((N, W) + tuple(plan.shape_out), generator=gen, device="cuda")
+    gy.view(N, W, -1)[:, :, torch.as_tensor(~valid_mask(spins, LO), device="cuda")] = 0.0
+    g1, g2, gw = plan.backward_fully_connected(x1, x2, w, gy)
+    torch.cuda.synchronize()
+    sel = np.arange(N) if edges is None else np.unique(np.asarray(edges))
+    ti = torch.as_tensor(sel, device="cuda")
+    a = x1[ti].double().cpu().numpy().reshape(len(sel), U, -1)
+    b = x2[ti].double().cpu().numpy().reshape(len(sel), V, -1)
+    g = gy[ti].double().cpu().numpy().reshape(len(sel), W, -1)
+    r1, r2, rw = oracle.fully_connected_vjp(a, b, w.double().cpu().numpy(), g, L1, L2, LO, spins, basis)
+    gw_all = gw
+    if edges is not None:
+        # grad_weights of the sampled edges alone: the same entry point on their rows
+        _, _, gw = plan.backward_fully_connected(x1[ti].contiguous(), x2[ti].contiguous(), w, gy[ti].contiguous(),
+                                                 need=(False, False, True))
+        torch.cuda.synchronize()
+    errs = []
+    for got, ref, name in ((g1[ti], r1, "grad_x1"), (g2[ti], r2, "grad_x2"), (gw, rw, "grad_w")):
+        got = got.double().cpu().numpy().reshape(ref.shape)
+        err = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300))
+        errs.append(err)
+        print(f"[uvw-bwd]   {name} rel_l2={err:.3e}", flush=True)
+        assert err <= TOL, (name, err)
+    # slots with l < |s| of the input gradients are 0
+    assert np.all(g1[ti].cpu().numpy().reshape(len(sel), U, -1)[:, :, ~valid_mask(spins, L1)] == 0.0)
+    assert np.all(g2[ti].cpu().numpy().reshape(len(sel), V, -1)[:, :, ~valid_mask(spins, L2)] == 0.0)
+    return plan, (x1, x2, w, gy), (g1, g2, gw_all)
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [
+    (1, 1, 1, S3, 0), (2, 2, 2, S3, 0), (2, 2, 2, S3, 2), (1, 3, 3, S3, 1), (2, 1, 2, (0,), 0), (2, 2, 2, S5, 2),
+    (3, 3, 3, S3, 0), (2, 2, 4, S3, 0), (3, 1, 2, S3, 0),
+])
+def test_uvw_backward_small_ragged(L1, L2, LO, spins, basis):
+    # 37 edges (a full 32-edge tile and a ragged tail), 6 (u, v) pairs, 5 output channels;
+    # mixed degrees give the three roles different block widths
+    run_uvw_backward(L1, L2, LO, spins, 37, 3, 2, 5, basis, seed=L1 + 10 * LO + basis)
+
+
+@pytest.mark.parametrize("N,U,V,W", [(65, 7, 5, 130), (33, 1, 1, 1), (40, 33, 1, 64), (9, 2, 3, 257),
+                                     (70, 130, 1, 3)])
+def test_uvw_backward_channel_counts(N, U, V, W):
+    # pair counts (v w, u w, u v) across 32-pair blocks, channel counts across 128-channel groups
+    run_uvw_backward(2, 2, 2, S3, N, U, V, W, 0, seed=N + U + V + W)
+
+
+@pytest.mark.parametrize("shape,C,B", [((1, 3, 3), 64, 128), ((2, 2, 2), 128, 1024)])
+def test_uvw_backward_runtime_table_shapes(shape, C, B):
+    # App. E.2 shapes: U = W = C, V = 1; sampled edges
+    edges = np.concatenate([np.arange(min(B, 5)), np.arange(max(0, B - 5), B), [B // 2]])
+    run_uvw_backward(*shape, S3, B, C, 1, C, 0, seed=B + C, edges=edges)
+
+
+def test_uvw_backward_subsets_and_empty():
+    plan, (x1, x2, w, gy), (g1, g2, gw) = run_uvw_backward(2, 2, 2, S3, 20, 4, 2, 6, 0, seed=3)
+    # each gradient alone equals the one from the joint call
+    for need, ref in (((True, False, False), g1), ((False, True, False), g2), ((False, False, True), gw)):
+        got = plan.backward_fully_connected(x1, x2, w, gy, need=need)
+        torch.cuda.synchronize()
+        i = need.index(True)
+        assert torch.equal(got[i], ref) and all(got[k] is None for k in range(3) if k != i)
+    # N = 0: grad_weights is 0
+    x1e = torch.zeros((0, 4, 3, 9), device="cuda")
+    x2e = torch.zeros((0, 2, 3, 9), device="cuda")
+    gye = torch.zeros((0, 6, 3, 9), device="cuda")
+    _, _, gwe = plan.backward_fully_connected(x1e, x2e, w, gye)
+    torch.cuda.synchronize()
+    assert gwe.shape == w.shape and float(gwe.abs().max()) == 0.0
+    # V = 0: the products are empty sums, grad_x1 is 0
+    x2z = torch.zeros((20, 0, 3, 9), device="cuda")
+    wz = torch.zeros((plan.n_paths, 4, 0, 6), device="cuda")
+    g1z, _, _ = plan.backward_fully_connected(x1, x2z, wz, gy)
+    torch.cuda.synchronize()
+    assert float(g1z.abs().max()) == 0.0
+
+
+def test_uvw_backward_argument_checks():
+    L = _lib.lib()
+    plan = Plan(2, 2, 2, S3, "fp32", 0, fully_connected=True)
+    plain = Plan(2, 2, 2, S3, "fp32", 0)
+    x = torch.zeros((4, 2, 3, 9), device="cuda")
+    w = torch.zeros((plan.n_paths, 2, 2, 2), device="cuda")
+    gy = torch.zeros((4, 2, 3, 9), device="cuda")
+    g1 = torch.zeros_like(x)
+    g2 = torch.zeros_like(x)
+    gw = torch.zeros_like(w)
+    args = [x.data_ptr(), x.data_ptr(), w.data_ptr(), gy.data_ptr(), g1.data_ptr(), g2.data_ptr(), gw.data_ptr(),
+            4, 2, 2, 2, None]
+    assert L.spingtp_backward_fully_connected(plan.handle, *args) == 0
+    assert L.spingtp_backward_fully_connected(plain.handle, *args) == 2  # no entry tables: unsupported
+    assert L.spingtp_backward_fully_connected(None, *args) == 1
+    for i, bad in ((4, g1.data_ptr() + 4), (3, gy.data_ptr() + 8), (3, None), (8, -1)):
+        a = list(args)
+        a[i] = bad
+        assert L.spingtp_backward_fully_connected(plan.handle, *a) == 1, i
+    a = list(args)
+    a[4] = a[5] = a[6] = None                                            # nothing requested: no-op
+    assert L.spingtp_backward_fully_connected(plan.handle, *a) == 0
+    torch.cuda.synchronize()
+
+
+def test_uvw_backward_bitwise_deterministic():
+    plan, (x1, x2, w, gy), (g1, g2, gw) = run_uvw_backward(2, 2, 2, S3, 100, 8, 2, 40, 0, seed=7,
+                                                           edges=[0, 50, 99])
+    h1, h2, hw = plan.backward_fully_connected(x1, x2, w, gy)
+    torch.cuda.synchronize()
+    assert torch.equal(g1, h1) and torch.equal(g2, h2) and torch.equal(gw, hw)
