@@ -22,9 +22,9 @@
 // is the product [UV x (edges x d3)] . [(edges x d3) x W] per path: its own kernel.
 //
 // Mapping of the mixing kernel.  A workgroup owns 32 edges, one output block, 128 output
-// channels and up to 8 of the block's components; wave i owns channels 32 i .. 32 i + 31
-// of the 128.  For every path into the block and every 32 pairs:
-//   (1) the 256 threads form R for 32 pairs x 32 edges x 8 components into LDS, laid out
+// channels and CH of the block's components (1 or 8, chosen per launch); wave i owns
+// channels 32 i .. 32 i + 31 of the 128.  For every path into the block and every 32 pairs:
+//   (1) the 256 threads form R for 32 pairs x 32 edges x CH components into LDS, laid out
 //       [pair][component][edge] (a lane's B operand is one conflict-free LDS read), and the
 //       pairs' weight offsets;
 //   (2) each wave multiplies: A = W[p, pair, o] from global memory, B = R from LDS, 16 K
@@ -55,6 +55,8 @@ constexpr int kEdges = 32;    // N of the matrix-core product: edges of a tile
 constexpr int kPairs = 32;    // (a, b) pairs staged per round (16 K steps of two)
 constexpr int kGroupW = 128;  // output channels of a workgroup (4 waves x 32)
 constexpr int kThreads = 256;
+constexpr int kSmallGrid = 512;  // see launch_uvw_mix
+constexpr int kSmallChunk = 1;
 
 __global__ __launch_bounds__(kThreads) void spingtp_fill_zero_kernel(float* __restrict__ out, int64_t n) {
     const int64_t n4 = n >> 2;
@@ -69,14 +71,15 @@ __global__ __launch_bounds__(kThreads) void spingtp_fill_zero_kernel(float* __re
 
 // R of pair pr (< A B) at edge n (< N) for the components j < mc of one path record:
 // r[j] = sum over the record's entries of component m0 + j of T a[ka] b[kb].
+template <int CH>
 __device__ __forceinline__ void form_r(const float* __restrict__ xa, const float* __restrict__ xb, int64_t n, int pr,
                                        int A, int B, int nca, int ncb, const uint32_t* __restrict__ csr,
-                                       const uint32_t* __restrict__ ent, int mc, float (&r)[kUvwChunk]) {
+                                       const uint32_t* __restrict__ ent, int mc, float (&r)[CH]) {
     const int a = pr / B, b = pr - a * B;
     const float* __restrict__ ra = xa + (n * A + a) * nca;
     const float* __restrict__ rb = xb + (n * B + b) * ncb;
 #pragma unroll
-    for (int j = 0; j < kUvwChunk; ++j) {
+    for (int j = 0; j < CH; ++j) {
         if (j < mc) {
             float s = 0.f;
             for (uint32_t k = csr[j]; k < csr[j + 1]; ++k) {
@@ -88,6 +91,8 @@ __device__ __forceinline__ void form_r(const float* __restrict__ xa, const float
     }
 }
 
+// CH: output components per workgroup (the accumulators of a wave)
+template <int CH>
 __global__ __launch_bounds__(kThreads) void spingtp_uvw_mix_kernel(const float* __restrict__ xa,
                                                                    const float* __restrict__ xb,
                                                                    const float* __restrict__ wt,
@@ -95,7 +100,7 @@ __global__ __launch_bounds__(kThreads) void spingtp_uvw_mix_kernel(const float* 
                                                                    int O, int64_t sa, int64_t sb, int64_t so,
                                                                    int64_t ps, const uint32_t* __restrict__ tab,
                                                                    int n_chunks, int nco) {
-    __shared__ float R[kPairs * kUvwChunk * kEdges];
+    __shared__ float R[kPairs * CH * kEdges];
     __shared__ int64_t woff[kPairs];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -105,9 +110,9 @@ __global__ __launch_bounds__(kThreads) void spingtp_uvw_mix_kernel(const float* 
     const int o3 = static_cast<int>(blk[0]), d3 = static_cast<int>(blk[1]);
     const int rec_first = static_cast<int>(blk[2]), n_rec = static_cast<int>(blk[3]);
     const int og = static_cast<int>(blockIdx.z) / n_chunks;
-    const int m0 = (static_cast<int>(blockIdx.z) - og * n_chunks) * kUvwChunk;
+    const int m0 = (static_cast<int>(blockIdx.z) - og * n_chunks) * CH;
     if (m0 >= d3) return;  // the whole workgroup: this block has fewer components
-    const int mc = d3 - m0 < kUvwChunk ? d3 - m0 : kUvwChunk;
+    const int mc = d3 - m0 < CH ? d3 - m0 : CH;
     const int nca = static_cast<int>(tab[2]), ncb = static_cast<int>(tab[3]);
     const uint32_t* recs = tab + tab[6];
     const uint32_t* ent = tab + tab[7];
@@ -118,9 +123,9 @@ __global__ __launch_bounds__(kThreads) void spingtp_uvw_mix_kernel(const float* 
     const int64_t o_off = static_cast<int64_t>(o_lane) * so;
     const int half = lane >> 5;
 
-    v16f acc[kUvwChunk];
+    v16f acc[CH];
 #pragma unroll
-    for (int j = 0; j < kUvwChunk; ++j) acc[j] = v16f{};
+    for (int j = 0; j < CH; ++j) acc[j] = v16f{};
 
     for (int q = 0; q < n_rec; ++q) {
         const uint32_t* rec = recs + kUvwRec * (rec_first + q);
@@ -132,12 +137,12 @@ __global__ __launch_bounds__(kThreads) void spingtp_uvw_mix_kernel(const float* 
                 const int pl = it >> 5, e = it & 31;
                 const int pr = c0 + pl;
                 const int64_t n = e0 + e;
-                float r[kUvwChunk];
+                float r[CH];
 #pragma unroll
-                for (int j = 0; j < kUvwChunk; ++j) r[j] = 0.f;
+                for (int j = 0; j < CH; ++j) r[j] = 0.f;
                 if (pr < AB && n < N) form_r(xa, xb, n, pr, A, B, nca, ncb, csr, ent, mc, r);
 #pragma unroll
-                for (int j = 0; j < kUvwChunk; ++j) R[(pl * kUvwChunk + j) * kEdges + e] = r[j];
+                for (int j = 0; j < CH; ++j) R[(pl * CH + j) * kEdges + e] = r[j];
             }
             if (tid < kPairs) {
                 const int pr = c0 + tid;
@@ -151,9 +156,9 @@ __global__ __launch_bounds__(kThreads) void spingtp_uvw_mix_kernel(const float* 
                 for (int kk = 0; kk < kPairs; kk += 2) {
                     const int pr = c0 + kk + half;
                     const float av = (pr < AB && o_lane < O) ? wp[woff[kk + half] + o_off] : 0.f;
-                    const float* rb = R + ((kk + half) * kUvwChunk) * kEdges + (lane & 31);
+                    const float* rb = R + ((kk + half) * CH) * kEdges + (lane & 31);
 #pragma unroll
-                    for (int j = 0; j < kUvwChunk; ++j)
+                    for (int j = 0; j < CH; ++j)
                         if (j < mc) acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, rb[j * kEdges], acc[j], 0, 0, 0);
                 }
             }
@@ -167,7 +172,7 @@ __global__ __launch_bounds__(kThreads) void spingtp_uvw_mix_kernel(const float* 
     const int64_t n = e0 + (lane & 31);
     if (n >= N) return;
 #pragma unroll
-    for (int j = 0; j < kUvwChunk; ++j) {
+    for (int j = 0; j < CH; ++j) {
         if (j >= mc) break;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
@@ -379,12 +384,25 @@ hipError_t launch_uvw_mix(const float* xa, const float* xb, const float* w, floa
     if (e != hipSuccess) return e;
     if (N == 0 || A == 0 || B == 0 || O == 0 || n_blocks == 0) return hipSuccess;
     const int64_t gx = (N + kEdges - 1) / kEdges;
-    const int n_chunks = (max_d3 + kUvwChunk - 1) / kUvwChunk;
-    const int64_t gz = static_cast<int64_t>((O + kGroupW - 1) / kGroupW) * n_chunks;
+    const int64_t groups = (O + kGroupW - 1) / kGroupW;
+    // One output component per workgroup: each forms R of its own component only, so only
+    // the weight reads repeat.  That pays wherever the weights of consecutive output
+    // channels are adjacent (so = 1, the forward: 1.6-2.2x faster on the App. E.2 shapes and
+    // still 1.6x at 16,384 edges), and for the strided weight reads of the gradient roles
+    // only in launches of fewer than kSmallGrid workgroups (measured: B = 1024 1.45x faster,
+    // B = 4096 1.24x slower).
+    const bool small = so == 1 || gx * n_blocks * groups * ((max_d3 + kUvwChunk - 1) / kUvwChunk) < kSmallGrid;
+    const int ch = small ? kSmallChunk : kUvwChunk;
+    const int n_chunks = (max_d3 + ch - 1) / ch;
+    const int64_t gz = groups * n_chunks;
     if (gx > 0x7fffffff || n_blocks > 65535 || gz > 65535) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(spingtp_uvw_mix_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(n_blocks),
-                                                     static_cast<unsigned>(gz)),
-                       dim3(kThreads), 0, stream, xa, xb, w, out, N, A, B, O, sa, sb, so, ps, table, n_chunks, nco);
+    const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(n_blocks), static_cast<unsigned>(gz));
+    if (small)
+        hipLaunchKernelGGL(spingtp_uvw_mix_kernel<kSmallChunk>, grid, dim3(kThreads), 0, stream, xa, xb, w, out, N, A,
+                           B, O, sa, sb, so, ps, table, n_chunks, nco);
+    else
+        hipLaunchKernelGGL(spingtp_uvw_mix_kernel<kUvwChunk>, grid, dim3(kThreads), 0, stream, xa, xb, w, out, N, A,
+                           B, O, sa, sb, so, ps, table, n_chunks, nco);
     return hipGetLastError();
 }
 
