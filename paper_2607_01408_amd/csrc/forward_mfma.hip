@@ -402,13 +402,25 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
     const float* xr = lds + (h ? S::X2 : 0) + (32 * T + (lane & 31)) * ST;
     const float sg = h ? -1.f : 1.f;
     const v4u* __restrict__ ops = reinterpret_cast<const v4u*>(aux);
-    const v8h TBh = __builtin_bit_cast(v8h, ops[2 * lane]);
-    const v8h TBl = __builtin_bit_cast(v8h, ops[2 * lane + 1]);
+    // The step-(B) operand tables of this lane: held in registers across the node loop,
+    // except in the fp32 instantiations at L = 7, 8, whose registers run short: there
+    // each node reads them again (L1-resident; offset by node x a zero the compiler
+    // cannot see, so that the reads are not hoisted back out of the loop).  Measured on
+    // 262,144 units: L = 8 0.565 -> 0.515 ms (63 -> 44 spilled VGPRs), L = 7 -2 %
+    // (15 -> 0); at L = 6 fp32 and in bf16 the reads cost 1-2 %.
+    constexpr bool RELOAD = SPLIT == 3 && L >= 7;
     constexpr int TB2 = 2 * 64 * (1 + 2 * NB);  // the second step-(B) blocks (L = 8), in v4u
-    const v8h TB2ah = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 2 * lane]) : v8h{};
-    const v8h TB2al = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 2 * lane + 1]) : v8h{};
-    const v8h TB2bh = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 128 + 2 * lane]) : v8h{};
-    const v8h TB2bl = S::KB == 2 ? __builtin_bit_cast(v8h, ops[TB2 + 128 + 2 * lane + 1]) : v8h{};
+    const int zero_i = static_cast<int>(neg_one + 1.0f);
+    auto tables = [&](const v4u* __restrict__ o, v8h& h, v8h& l, v8h& ah, v8h& al, v8h& bh, v8h& bl) {
+        h = __builtin_bit_cast(v8h, o[2 * lane]);
+        l = __builtin_bit_cast(v8h, o[2 * lane + 1]);
+        ah = S::KB == 2 ? __builtin_bit_cast(v8h, o[TB2 + 2 * lane]) : v8h{};
+        al = S::KB == 2 ? __builtin_bit_cast(v8h, o[TB2 + 2 * lane + 1]) : v8h{};
+        bh = S::KB == 2 ? __builtin_bit_cast(v8h, o[TB2 + 128 + 2 * lane]) : v8h{};
+        bl = S::KB == 2 ? __builtin_bit_cast(v8h, o[TB2 + 128 + 2 * lane + 1]) : v8h{};
+    };
+    v8h rTBh{}, rTBl{}, rTB2ah{}, rTB2al{}, rTB2bh{}, rTB2bl{};
+    if constexpr (!RELOAD) tables(ops, rTBh, rTBl, rTB2ah, rTB2al, rTB2bh, rTB2bl);
     const v16f zero16 = {};
 
     // output accumulators of this lane: m3 >= 0 (h = 0) or m3 < 0 (h = 1)
@@ -427,6 +439,7 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
     struct Front {  // node k after step (A)
         float Pc[3][L + 1], Ps[3][L + 1], dl, ep;
         const float* tb;
+        int j;
     };
     struct Back {  // node k between the issue of step (D) and step (E)
         v16f sp[3];
@@ -435,6 +448,7 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
     };
     auto front1 = [&](int j) {
         Front F;
+        F.j = j;
         F.tb = tab + Y.glob + j * Y.pb;
         // (A) this lane's input at node j
         coef_to_theta_fourier<L, L, true, false, true>(xr, F.tb, tab + Y.n0, BWD && h != 0, F.Pc[0], F.Ps[0], F.Pc[1], F.Ps[1],
@@ -475,6 +489,8 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
         }
 
         // (B) fields of the six polynomials at the n_phi points
+        v8h TBh = rTBh, TBl = rTBl, TB2ah = rTB2ah, TB2al = rTB2al, TB2bh = rTB2bh, TB2bl = rTB2bl;
+        if constexpr (RELOAD) tables(ops + F.j * zero_i, TBh, TBl, TB2ah, TB2al, TB2bh, TB2bl);
         v16f fb[2][3];
 #pragma unroll
         for (int in = 0; in < 2; ++in)
