@@ -63,9 +63,11 @@ def test_backward_matches_oracle(L, basis):
     run_backward(L, S3, 37, 3, "fp32", basis, seed=L + 10 * basis)
 
 
-@pytest.mark.parametrize("L,N,C", [(8, 9, 3), (12, 5, 2)])
+@pytest.mark.parametrize("L,N,C", [(8, 9, 3), (9, 7, 5), (12, 5, 2), (14, 3, 13), (16, 4, 9)])
 def test_backward_large_degree(L, N, C):
-    # the matrix-core (L = 8, two step-(B) K blocks) and large-L (L = 12) kernel families
+    # the matrix-core kernel (L = 8, two step-(B) K blocks) and the large-degree kernel
+    # (L = 9: rows held in registers, two rounds; L = 12: a split last round; L = 14, 16:
+    # staging loads per round, L = 16 with a one-node last round split over the waves)
     run_backward(L, S3, N, C, "fp32", 0, seed=L)
 
 
