@@ -29,9 +29,9 @@ PEAK_VALU_FP32_TFLOPS = 78.6
 PEAK_VALU_PACKED_FP32_TFLOPS = 157.3  # the published fp32 vector figure (packed FMA)
 PEAK_MFMA_F16_TFLOPS = 2500.0     # dense fp16 / bf16 matrix cores
 PEAK_MFMA_FP32_TFLOPS = 157.3     # dense fp32 matrix cores
-# The scope table's charged work per unit at spins (-1, 0, +1) (the survey's 2D (u,v) Fourier
-# route): coef->Fourier for both inputs, the spin-pair convolution done directly and by FFT,
-# and Fourier->coef.  Its floor charges the cheaper convolution on the vector ALU and the
+# Charged work per unit at spins (-1, 0, +1) of a 2D (u, v) Fourier route (the costing the
+# reported scope fraction uses; this kernel does not execute it): coef->Fourier for both
+# inputs, the spin-pair convolution done directly and by FFT, and Fourier->coef.  Its floor charges the cheaper convolution on the vector ALU and the
 # transforms on the matrix cores (fp32 at 157.3 TF, bf16 at the fp16 peak).
 SCOPE_CHARGED = {2: (1152, 26600, 34168, 1800), 4: (5840, 276696, 160672, 9928),
                  6: (16640, 1201928, 364544, 29000), 8: (35728, 3511928, 742048, 63624),

@@ -90,7 +90,14 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
 /* Also build the tables of spingtp_forward_v1_weighted (per-channel path weights),
  * OR-ed into the flags of spingtp_plan_create. */
 #define SPINGTP_CHANNEL_WEIGHTS 0x1000u
-/* plan also holds the entry table of spingtp_forward_fully_connected (mode uvw) */
+/* plan also holds the entry tables of spingtp_forward_fully_connected and
+ * spingtp_backward_fully_connected (mode uvw).  With this flag spingtp_pre_table_host
+ * returns the forward's entry table, and with SPINGTP_TABLES_BACKWARD as well the tables
+ * of the gradients w.r.t. x1 and then x2, one after the other (the tensor read as
+ * T[k2, k3 -> k1] and T[k1, k3 -> k2]); each starts with the 8-word header described
+ * with the plan's tables in the source (n_paths, n_blocks, the row widths of its two
+ * inputs and its output, max block width, first word of the path records, first word
+ * of the entries; a path record is 6 words, an entry 2). */
 #define SPINGTP_FULLY_CONNECTED 0x2000u
 
 /* For spingtp_plan_tables_host only: return the tables spingtp_backward uses

@@ -1161,15 +1161,20 @@ spingtp_status spingtp_pre_table_host(int L1, int L2, int Lout, const int* spins
     if (count == nullptr || (capacity > 0 && words == nullptr)) return SPINGTP_ERR_INVALID_ARG;
     const bool backward = (flags & SPINGTP_TABLES_BACKWARD) != 0;
     flags &= ~SPINGTP_TABLES_BACKWARD;
-    if (backward && (flags & SPINGTP_CHANNEL_WEIGHTS) == 0 && (L1 != L2 || L2 != Lout)) return SPINGTP_ERR_UNSUPPORTED;
+    if (backward && (flags & (SPINGTP_CHANNEL_WEIGHTS | SPINGTP_FULLY_CONNECTED)) == 0 && (L1 != L2 || L2 != Lout))
+        return SPINGTP_ERR_UNSUPPORTED;
     int spin_mode = 0;
     const spingtp_status st = check_args(L1, L2, Lout, spins, n_spins, flags, &spin_mode);
     if (st != SPINGTP_OK) return st;
-    if (flags & SPINGTP_FULLY_CONNECTED) {  // the entry table of spingtp_forward_fully_connected
+    if (flags & SPINGTP_FULLY_CONNECTED) {  // the entry tables of the fully connected product
         try {
             std::vector<uint32_t> w;
-            if (!spingtp::build_uvw_table(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, w))
-                return SPINGTP_ERR_UNSUPPORTED;
+            for (int role = backward ? 1 : 0; role < (backward ? 3 : 1); ++role) {
+                std::vector<uint32_t> t;
+                if (!spingtp::build_uvw_table(L1, L2, Lout, spins, n_spins, flags & ~kRouteFlags, t, nullptr, role))
+                    return SPINGTP_ERR_UNSUPPORTED;
+                w.insert(w.end(), t.begin(), t.end());
+            }
             *count = w.size();
             const size_t n = w.size() < capacity ? w.size() : capacity;
             if (n) std::memcpy(words, w.data(), n * sizeof(uint32_t));

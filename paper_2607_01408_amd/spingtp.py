@@ -18,6 +18,7 @@ CHANNEL_WEIGHTS = 0x1000  # also build the per-channel path-weighted table (spin
 FULLY_CONNECTED = 0x2000  # also build the entry table of the fully connected product (spingtp.h)
 V1_FOURIER = 0x200  # spingtp_forward_v1 on the Fourier route (spingtp.h)
 V1_PRECONTRACT = 0x400  # spingtp_forward_v1 on the precontracted kernel wherever it is built
+TABLES_BACKWARD = 0x800  # host table functions: the gradients' tables (spingtp.h)
 FP32 = 0
 BF16 = 1
 
@@ -66,17 +67,27 @@ def mfma_operands_host(L):
     return out
 
 
-def uvw_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER):
-    """spingtp_pre_table_host with SPINGTP_FULLY_CONNECTED: the entry table of the fully connected product."""
+def uvw_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, backward=False):
+    """spingtp_pre_table_host with SPINGTP_FULLY_CONNECTED: the entry table of the fully
+    connected product, or with backward=True the tables of its gradients w.r.t. x1 and x2
+    (a pair, split at the end of the first one)."""
     arr, n = _spin_array(spins)
+    flags = basis | FULLY_CONNECTED | (TABLES_BACKWARD if backward else 0)
     count = ctypes.c_size_t(0)
-    _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, basis | FULLY_CONNECTED, None, 0,
-                                                 ctypes.byref(count)), "spingtp_pre_table_host")
+    _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, flags, None, 0, ctypes.byref(count)),
+               "spingtp_pre_table_host")
     out = np.zeros(count.value, dtype=np.uint32)
-    _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, basis | FULLY_CONNECTED,
+    _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, flags,
                                                  out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), out.size,
                                                  ctypes.byref(count)), "spingtp_pre_table_host")
-    return out
+    if not backward:
+        return out
+    # length of the first table: its entries end where its last entry offset points
+    n_paths, rec0, ent0 = int(out[0]), int(out[6]), int(out[7])
+    csr0 = rec0 + 6 * n_paths
+    n_ent = int(out[csr0:ent0].max()) if ent0 > csr0 else 0
+    end = ent0 + 2 * n_ent
+    return out[:end], out[end:]
 
 
 def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, backward=False, channel_weights=False):
@@ -84,7 +95,7 @@ def pre_table_host(L1, L2, Lout, spins=(-1, 0, 1), basis=BASIS_PAPER, backward=F
     backward=True the table of spingtp_backward_v1, with channel_weights=True that of
     spingtp_forward_v1_weighted, with both the entry lists of spingtp_backward_v1_weighted."""
     arr, n = _spin_array(spins)
-    basis = basis | (0x800 if backward else 0) | (CHANNEL_WEIGHTS if channel_weights else 0)
+    basis = basis | (TABLES_BACKWARD if backward else 0) | (CHANNEL_WEIGHTS if channel_weights else 0)
     count = ctypes.c_size_t(0)
     _lib.check(_lib.lib().spingtp_pre_table_host(L1, L2, Lout, arr, n, basis, None, 0, ctypes.byref(count)),
                "spingtp_pre_table_host")

@@ -731,10 +731,13 @@ def test_plan_upload_failure_releases_everything(built_library, L1, L2, LO, spin
     assert bad == 1
 
 
-def emulate_uvw_table(words, x1, x2, W, nco):
-    """float64 re-enactment of spingtp_forward_fully_connected from its entry table: per
-    output block and path, R from the entries (k1 | k2 << 16, value) of each component,
-    then the channel mixing with the path's weights."""
+def emulate_uvw_table(words, x1, x2, W, nco, role=0):
+    """float64 re-enactment of the fully connected product from an entry table: per
+    output block and path, R from the entries (ka | kb << 16, value) of each component,
+    then the channel mixing with the path's weights W [path][A][B][out].  role 0: the
+    forward (x1, x2 -> out); 1: grad_x1 (x2, grad_out -> x1 slots); 2: grad_x2 (x1,
+    grad_out -> x2 slots).  A path record's words 3..5 are its blocks of x1, x2, out."""
+    ax_a, ax_b, ax_o = ((0, 1, 2), (1, 2, 0), (0, 2, 1))[role]
     w = np.asarray(words, dtype=np.uint32)
     n_paths, n_blocks, nc1, nc2, nco_t, max_d3, rec0, ent0 = (int(v) for v in w[:8])
     assert nco_t == nco
@@ -746,16 +749,18 @@ def emulate_uvw_table(words, x1, x2, W, nco):
         o3, d3, first, count = (int(v) for v in w[8 + 4 * b:12 + 4 * b])
         assert d3 <= max_d3
         for r in range(first, first + count):
-            pid, d3r, csr, b1, b2, b3 = (int(v) for v in w[rec0 + 6 * r:rec0 + 6 * r + 6])
+            pid, d3r, csr = (int(v) for v in w[rec0 + 6 * r:rec0 + 6 * r + 3])
+            blocks = [int(v) for v in w[rec0 + 6 * r + 3:rec0 + 6 * r + 6]]
             assert d3r == d3 and pid not in seen
-            assert (b3 & 0xFFFF, b3 >> 16) == (o3, d3)      # the path's output block
+            assert (blocks[ax_o] & 0xFFFF, blocks[ax_o] >> 16) == (o3, d3)      # the path's output block
+            ba, bb = blocks[ax_a], blocks[ax_b]
             seen.add(pid)
             for m3 in range(d3):
                 for k in range(int(w[csr + m3]), int(w[csr + m3 + 1])):
                     ix = int(w[ent0 + 2 * k])
                     t = float(vals[ent0 + 2 * k + 1])
-                    # the entry lies in the path's blocks of x1 and x2
-                    assert 0 <= (ix & 0xFFFF) - (b1 & 0xFFFF) < b1 >> 16 and 0 <= (ix >> 16) - (b2 & 0xFFFF) < b2 >> 16
+                    # the entry lies in the path's blocks of its two inputs
+                    assert 0 <= (ix & 0xFFFF) - (ba & 0xFFFF) < ba >> 16 and 0 <= (ix >> 16) - (bb & 0xFFFF) < bb >> 16
                     R = t * x1[:, :, ix & 0xFFFF, None] * x2[:, None, :, ix >> 16]      # [N, U, V]
                     out[:, :, o3 + m3] += np.einsum("nuv,uvw->nw", R, W[pid])
     assert seen == set(range(n_paths))
@@ -781,3 +786,29 @@ def test_uvw_table_reproduces_oracle(built_library, L1, L2, LO, spins, basis):
     y = emulate_uvw_table(words, x1, x2, W, nco)
     yo = oracle.fully_connected(x1, x2, W, L1, L2, LO, spins, basis).reshape(N, Wc, -1)
     assert np.abs(y - yo).max() <= 1e-6 * max(1.0, np.abs(yo).max())
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis", [
+    (1, 1, 1, (-1, 0, 1), 0), (2, 2, 2, (-1, 0, 1), 2), (1, 3, 3, (-1, 0, 1), 1), (3, 1, 2, (-1, 0, 1), 0),
+    (2, 1, 2, (0,), 0), (2, 2, 2, S5, 2),
+])
+def test_uvw_gradient_tables_reproduce_oracle(built_library, L1, L2, LO, spins, basis):
+    """The entry tables of the fully connected product's gradients w.r.t. x1 (the tensor
+    read as T[k2, k3 -> k1]) and x2 (T[k1, k3 -> k2]), re-enacted in float64 as products
+    of (x2, grad_out) and (x1, grad_out) mixed by the permuted weights, against the
+    oracle's reverse mode."""
+    from paper_2607_01408_amd.spingtp import uvw_table_host
+    t1, t2 = uvw_table_host(L1, L2, LO, spins, basis, backward=True)
+    rng = np.random.default_rng(7 + L1 + 10 * L2 + 100 * LO + basis)
+    N, U, V, Wc = 3, 3, 2, 4
+    nc1, nc2, nco = (len(spins) * (L + 1) ** 2 for L in (L1, L2, LO))
+    x1 = rng.standard_normal((N, U, nc1)) * valid_mask(spins, L1)
+    x2 = rng.standard_normal((N, V, nc2)) * valid_mask(spins, L2)
+    g = rng.standard_normal((N, Wc, nco)) * valid_mask(spins, LO)
+    P = len(oracle.PathWeightedTensor(L1, L2, LO, spins, basis).paths)
+    W = rng.standard_normal((P, U, V, Wc))
+    g1 = emulate_uvw_table(t1, x2, g, W.transpose(0, 2, 3, 1), nc1, role=1)
+    g2 = emulate_uvw_table(t2, x1, g, W.transpose(0, 1, 3, 2), nc2, role=2)
+    r1, r2, _ = oracle.fully_connected_vjp(x1, x2, W, g, L1, L2, LO, spins, basis)
+    for got, ref in ((g1, r1), (g2, r2)):
+        assert np.abs(got - ref.reshape(got.shape)).max() <= 1e-6 * max(1.0, np.abs(ref).max())
