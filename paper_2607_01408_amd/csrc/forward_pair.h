@@ -528,12 +528,12 @@ constexpr bool big_hoist_rows() {
 // PAR (spins only): the plan's basis is the parity-labelled one; a separate
 // instantiation, since a run-time switch between the two step-(A) forms costs the
 // paper-basis kernels registers.
-template <int L, bool SPIN, int W, bool BWD, bool PAR>
 // zero: 0 from the launcher.  The input rows are the same in every round, so the
 // compiler hoists the staging loads of all chunks out of the round loop; where they
 // do not fit in registers it holds them in scratch (106 spilled VGPRs at L = 16).
 // Offsetting them by round * zero keeps them in the loop, in flight one chunk ahead
 // (big_hoist_rows picks the degrees where the hoisted form fits).
+template <int L, bool SPIN, int W, bool BWD, bool PAR>
 __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_big_kernel(
     const float* __restrict__ x1, const float* __restrict__ x2, float* __restrict__ out, int64_t units, int64_t cpx2,
     const float* __restrict__ tab, int zero) {
