@@ -376,7 +376,7 @@ def test_v1_bf16(shape, fourier):
     run_v1(*shape, S3, 23, 48, "bf16", fourier, seed=7)
 
 
-@pytest.mark.parametrize("L,C", [(7, 5), (8, 5), (12, 3)])
+@pytest.mark.parametrize("L,C", [(7, 5), (8, 5), (9, 4), (12, 3), (16, 3)])
 def test_v1_fourier_route_large_degree(L, C):
     # beyond the precontracted kernel's size the v1 entry runs the forward kernel with x2 per edge
     fam, _ = run_v1(L, L, L, S3, 19, C, "fp32", False, seed=L)
