@@ -458,16 +458,18 @@ constexpr Registered reg_pair() {
 }
 #define SPINGTP_REG_PAIR(L, SPIN) reg_pair<L, SPIN, float>(), reg_pair<L, SPIN, uint16_t>()
 
-template <int L, bool SPIN, int W, bool PAR = false>
+template <int L, bool SPIN, int W, typename TIO, bool PAR = false>
 constexpr Registered reg_big() {
     using B = BigShape<L, SPIN, W>;
-    return Registered{L, L, L, SPIN ? 1 : 0, 0,
+    return Registered{L, L, L, SPIN ? 1 : 0, sizeof(TIO) == 4 ? 0 : 1,
                       KernelEntry{B::WAVES, B::UNITS, static_cast<int>(B::LDS_FLOATS * sizeof(float)), 3,
-                                  &launch_big<L, SPIN, W, false, PAR>, &launch_big<L, SPIN, W, true, PAR>},
+                                  &launch_big<L, SPIN, W, false, PAR, TIO>, &launch_big<L, SPIN, W, true, PAR, TIO>},
                       SPIN ? (PAR ? 1 : 0) : -1};
 }
 // (the parity-basis instantiations with spins are in forward_big_parity.hip)
-#define SPINGTP_REG_BIG(L) reg_big<L, true, big_waves<L, true>()>(), reg_big<L, false, big_waves<L, false>()>()
+#define SPINGTP_REG_BIG(L)                                                                                        \
+    reg_big<L, true, big_waves<L, true>(), float>(), reg_big<L, false, big_waves<L, false>(), float>(),          \
+        reg_big<L, true, big_waves<L, true>(), uint16_t>(), reg_big<L, false, big_waves<L, false>(), uint16_t>()
 
 const Registered kRegistry[] = {
     SPINGTP_REG(0, 0, 0, false), SPINGTP_REG(1, 1, 1, false), SPINGTP_REG(2, 2, 2, false),
@@ -488,7 +490,7 @@ const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype,
         if (r.L1 == L1 && r.L2 == L2 && r.LO == LO && r.spin == spin_mode && r.dtype == dtype &&
             (r.basis_par < 0 || r.basis_par == (parity ? 1 : 0)))
             return &r.entry;
-    if (parity && spin_mode == 1 && L1 == L2 && L2 == LO && dtype == 0) return find_big_parity_kernel(L1);
+    if (parity && spin_mode == 1 && L1 == L2 && L2 == LO) return find_big_parity_kernel(L1, dtype);
     return nullptr;
 }
 

@@ -373,7 +373,7 @@ __device__ __forceinline__ void pair_publish(float* D, int sub, const float (&Q0
 }
 
 // ---------------------------------------------------------------------------
-// Large-degree kernel (L = 9..16, fp32 I/O).  More nodes than a workgroup has
+// Large-degree kernel (L = 9..16, fp32 or bf16 I/O, fp32 arithmetic).  More nodes than a workgroup has
 // waves, and 32-unit input tiles that no longer fit in LDS: the nodes are
 // processed in rounds of W waves.  In each round the workgroup stages the tile's
 // input rows in LDS a chunk of degrees at a time (coalesced loads, the next
@@ -533,11 +533,15 @@ constexpr bool big_hoist_rows() {
 // do not fit in registers it holds them in scratch (106 spilled VGPRs at L = 16).
 // Offsetting them by round * zero keeps them in the loop, in flight one chunk ahead
 // (big_hoist_rows picks the degrees where the hoisted form fits).
-template <int L, bool SPIN, int W, bool BWD, bool PAR>
+// TIO: float (fp32 I/O) or uint16_t (bf16 I/O: rows widened to fp32 as they are staged,
+// the output tile rounded to nearest even as it is stored; all arithmetic in fp32).
+template <int L, bool SPIN, int W, bool BWD, bool PAR, typename TIO>
 __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_big_kernel(
-    const float* __restrict__ x1, const float* __restrict__ x2, float* __restrict__ out, int64_t units, int64_t cpx2,
+    const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units, int64_t cpx2,
     const float* __restrict__ tab, int zero) {
     using B = BigShape<L, SPIN, W>;
+    constexpr bool F32 = std::is_same<TIO, float>::value;
+    static_assert(F32 || B::OUT_LDS, "bf16 I/O needs the output tile in LDS");
     using P = typename B::PS;
     constexpr Layout Y = B::Y;
     constexpr bool SPLIT = big_split_last<L, SPIN, PAR>();
@@ -558,13 +562,14 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     const bool valid = u < nvalid;
     const int64_t row = u0 + (valid ? u : 0);  // invalid lanes compute on a valid row, store nothing
     const float* g = tab;
-    float* orow = out + row * B::NC;
+    float* orow = nullptr;  // the output row in global memory (fp32 without the LDS tile)
+    if constexpr (F32) orow = out + row * B::NC;
     // staging: TPR threads per input row (row r = lane r of every wave)
     constexpr int TPR = B::THREADS / 64;
     static_assert(B::THREADS % 64 == 0, "whole waves");
     const int sr = tid / TPR, sk = tid % TPR;
     const int64_t srow = u0 + ((sr >> 1) < nvalid ? (sr >> 1) : 0);
-    const float* ssrc = (sr & 1) ? x2 + (srow / cpx2) * B::NC : x1 + srow * B::NC;
+    const TIO* ssrc = (sr & 1) ? x2 + (srow / cpx2) * B::NC : x1 + srow * B::NC;
 
     for (int i = tid; i < B::TRIG; i += B::THREADS) {
         const int sb = i / (B::NP * (L + 1));
@@ -607,7 +612,11 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
         // waves work on chunk c
         constexpr int IT = (B::SCAP + TPR - 1) / TPR;  // staged values per block and thread
         float pre[B::NS][IT];
-        const float* rsrc = big_hoist_rows<L, SPIN, PAR>() ? ssrc : ssrc + r * zero;
+        const TIO* rsrc = big_hoist_rows<L, SPIN, PAR>() ? ssrc : ssrc + r * zero;
+        auto widen = [](TIO v) {
+            if constexpr (F32) return v;
+            else return __uint_as_float(static_cast<uint32_t>(v) << 16);
+        };
         auto fetch = [&](auto cc) {
             constexpr int c = decltype(cc)::value;
             constexpr int LA = B::chunk_lo(c), LB = B::chunk_lo(c + 1);
@@ -617,7 +626,7 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
 #pragma unroll
                 for (int it = 0; it < IT; ++it) {
                     const int q = sk + it * TPR;
-                    if (it * TPR < CW) pre[b][it] = q < CW ? rsrc[b * B::BB + LA * LA + q] : 0.f;
+                    if (it * TPR < CW) pre[b][it] = q < CW ? widen(rsrc[b * B::BB + LA * LA + q]) : 0.f;
                 }
         };
         auto chunk = [&](auto cc) {
@@ -702,22 +711,22 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
             __syncthreads();
         }
         store_tile<B::NC, B::STO>(out + u0 * B::NC, nvalid, YT, tid, B::THREADS);
-    } else if constexpr (PAR) {
+    } else if constexpr (PAR && F32) {
         // the rows were accumulated in global memory by several waves; the barrier
         // that ends the last round orders those stores before these reads
         parity_mix_rows<L>(out + u0 * B::NC, B::NC, nvalid, true, tid, B::THREADS);
     }
 }
 
-template <int L, bool SPIN, int W, bool BWD, bool PAR>
+template <int L, bool SPIN, int W, bool BWD, bool PAR, typename TIO = float>
 hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                       const uint32_t*, hipStream_t stream) {
     using B = BigShape<L, SPIN, W>;
     const int64_t blocks = (units + B::UNITS - 1) / B::UNITS;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W, BWD, PAR>), dim3(static_cast<unsigned>(blocks)), dim3(B::THREADS),
-                       0, stream, static_cast<const float*>(x1), static_cast<const float*>(x2),
-                       static_cast<float*>(out), units, cpx2, tab, 0);
+    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W, BWD, PAR, TIO>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(B::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
+                       static_cast<TIO*>(out), units, cpx2, tab, 0);
     return hipGetLastError();
 }
 

@@ -75,8 +75,8 @@ void build_direct_table(int L1, int L2, int LO, const int* spins, int n_spins, u
 // with an |s| = 1 sector (the large-degree family has a separate instantiation).
 const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype, bool parity);
 // The parity-basis large-degree kernel of L1 = L2 = Lout = L (9..16, spins {-1, 0, +1},
-// fp32; forward_big_parity.hip), nullptr otherwise.
-const KernelEntry* find_big_parity_kernel(int L);
+// dtype 0 fp32, 1 bf16 I/O; forward_big_parity.hip), nullptr otherwise.
+const KernelEntry* find_big_parity_kernel(int L, int dtype);
 const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
 // The precontracted kernel of spingtp_forward_v1 (x2 shared by the channels of an edge).
 const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int n_spins, int dtype);

@@ -82,7 +82,7 @@ def test_backward_scalar_spin(L):
     run_backward(L, (0,), 29, 5, "fp32", 0, seed=3 + L)
 
 
-@pytest.mark.parametrize("L", [4, 6])
+@pytest.mark.parametrize("L", [4, 6, 12, 16])
 def test_backward_bf16(L):
     run_backward(L, S3, 41, 4, "bf16", 0, seed=20 + L)
 

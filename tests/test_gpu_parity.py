@@ -143,6 +143,14 @@ def test_ragged_large_degree(L, basis):
     run_and_compare(L, L, L, S3, 37, 3, "fp32", basis, seed=L)
 
 
+@pytest.mark.parametrize("L,basis,spins", [(9, 0, S3), (12, 0, S3), (13, 1, S3), (16, 0, S3), (12, 2, S3),
+                                           (16, 2, S3), (12, 0, (0,)), (16, 0, (0,))])
+def test_bf16_large_degree(L, basis, spins):
+    # bf16 I/O on the large-degree kernels (rows widened as they are staged, the tile
+    # rounded to nearest even as it is stored): every staging form, both bases, spin {0}
+    run_and_compare(L, L, L, spins, 37, 3, "bf16", basis, seed=300 + L + basis)
+
+
 @pytest.mark.parametrize("L", [9, 16])
 def test_large_degree_many_tiles(L):
     # 41 tiles of 32 units (more than one workgroup per XCD) and a ragged tail of 7;
