@@ -113,8 +113,8 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  *   sets give SPINGTP_ERR_UNSUPPORTED.  Spins {-2..2} run on the direct kernel
  *   (family 6) and, for spingtp_forward_v1, on the precontracted kernel.
  *   dtype: element type of x1, x2 and out.  Arithmetic: the vector-ALU kernels
- *   compute in fp32.  The matrix-core kernel (L1 = L2 = Lout = 5 or 6, and
- *   4 for bf16; spins {-1, 0, +1}) runs the two phi transforms as fp16 matrix products with fp32
+ *   compute in fp32.  The matrix-core kernel (L1 = L2 = Lout = 4..8, spins
+ *   {-1, 0, +1}) runs the two phi transforms as fp16 matrix products with fp32
  *   accumulation: for fp32 plans every operand is split into fp16 high and low
  *   parts (three products per term, relative error near 2^-21 per term, like
  *   fp32), for bf16 plans only the high parts are used (near 2^-11).  Every
@@ -123,9 +123,15 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  *   SPINGTP_V1_FOURIER, SPINGTP_V1_PRECONTRACT.
  * A shape with no Fourier kernel (families 1-4) runs spingtp_forward on the
  * direct kernel (family 6) where its LDS tile fits (64 n_spins ((L1+1)^2 +
- * (L2+1)^2 + (Lout+1)^2) floats plus padding within 160 KB); a shape that only
- * the precontracted kernel of spingtp_forward_v1 covers gives a plan for that
- * entry point, and spingtp_forward and spingtp_plan_kernel_info then return
+ * (L2+1)^2 + (Lout+1)^2) floats plus padding within 160 KB, rows of at most 254
+ * slots); beyond that, with spins {0} or {-1, 0, +1}, on the large-degree kernel
+ * (family 3) of L = max(L1, L2, Lout): x1 and x2 are padded with zeros to degree
+ * L as the kernel stages them and the degree-L product is stored up to Lout,
+ * which is exact since that kernel's grid integrates degree 3 L >= L1 + L2 + Lout
+ * (forward and spingtp_forward_v1; spingtp_backward of such a plan gives
+ * SPINGTP_ERR_UNSUPPORTED).  A shape that only the precontracted kernel of
+ * spingtp_forward_v1 covers gives a plan for that entry point, and
+ * spingtp_forward and spingtp_plan_kernel_info then return
  * SPINGTP_ERR_UNSUPPORTED.
  * The plan tables (Gauss-Legendre weights and SWSH values on the quadrature
  * nodes, trigonometric tables, real-basis mixing constants) are computed in

@@ -1301,6 +1301,21 @@ spingtp_status build_plan_host(int L1, int L2, int Lout, const int* spins, int n
     const spingtp::KernelEntry* kd = dir_idx_ok ? spingtp::find_direct_kernel(dir_lds, static_cast<int>(dtype)) : nullptr;
     const bool fourier_bwd = k != nullptr && L1 == L2 && L2 == Lout;
     if (k == nullptr) k = kd;
+    // mixed degrees whose rows exceed the direct kernel's: the large-degree kernel of the
+    // largest degree, with x1 and x2 padded by zeros as it stages them and the product
+    // truncated to Lout as it stores it (exact: its grid integrates degree 3 max(L1, L2,
+    // Lout) >= L1 + L2 + Lout); the three degrees reach it through the plan's aux words.
+    // Forward and V = 1 only.
+    int L_pad = -1;
+    if (k == nullptr && !weighted && spin_mode < 2) {
+        const int Lm = std::max(L1, std::max(L2, Lout));
+        const spingtp::KernelEntry* kb =
+            spingtp::find_kernel(Lm, Lm, Lm, spin_mode, static_cast<int>(dtype), parity_tiles);
+        if (kb != nullptr && kb->family == 3) {
+            k = kb;
+            L_pad = Lm;
+        }
+    }
     const spingtp::KernelEntry* kv1 = nullptr;
     if ((flags & SPINGTP_V1_FOURIER) == 0) {
         kv1 = spingtp::find_pre_kernel(L1, L2, Lout, n_spins, static_cast<int>(dtype));
@@ -1327,8 +1342,12 @@ spingtp_status build_plan_host(int L1, int L2, int Lout, const int* spins, int n
     h.kd = kd;
     h.kv1 = kv1;
     try {
-        if (spin_mode < 2 && !weighted && !spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab))
+        if (L_pad >= 0) {  // the tables of the padded degree, and the true degrees
+            if (!spingtp::build_tables(L_pad, L_pad, L_pad, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
+            aux = {static_cast<uint32_t>(L1), static_cast<uint32_t>(L2), static_cast<uint32_t>(Lout)};
+        } else if (spin_mode < 2 && !weighted && !spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) {
             return SPINGTP_ERR_INTERNAL;
+        }
         int lds_floats = 0;
         std::vector<double> dense;  // built once for the direct kernel's tables (and weighted plans)
         if ((k != nullptr && k->family == 6) || (kd != nullptr && !fourier_bwd) || weighted)

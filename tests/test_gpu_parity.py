@@ -474,3 +474,28 @@ def test_v1_argument_checks():
     y = mixed.forward(a, b)
     torch.cuda.synchronize()
     assert y.shape == (2, 3, 3, 9) and not y.any()
+
+
+# --- mixed degrees beyond the direct kernel's rows: the large-degree kernel of the
+# largest degree, inputs padded with zeros as it stages them, the product truncated ---
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis,dtype", [
+    (9, 3, 10, S3, 0, "fp32"), (12, 12, 6, S3, 0, "fp32"), (16, 2, 16, S3, 0, "fp32"), (4, 12, 16, S3, 2, "fp32"),
+    (16, 15, 14, (0,), 0, "fp32"), (12, 5, 9, S3, 0, "bf16"), (3, 10, 12, S3, 1, "fp32"),
+])
+def test_mixed_large_degrees(L1, L2, LO, spins, basis, dtype):
+    run_and_compare(L1, L2, LO, spins, 37, 3, dtype, basis, seed=400 + L1 + L2 + LO)
+    assert Plan(L1, L2, LO, spins, dtype, basis).kernel_info()["family"] == 3
+
+
+def test_mixed_large_degrees_v1_and_no_backward():
+    # the shared-x2 entry on the padded route; gradients of such shapes are not built
+    fam, _ = run_v1(9, 3, 10, S3, 13, 5, "fp32", seed=11)
+    assert fam == 3
+    plan = Plan(9, 3, 10, S3, "fp32")
+    x1 = workloads.draw(9, 4, 2, 1, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(3, 4, 2, 2, "fp32", S3, "unit", "cuda")
+    g = workloads.draw(10, 4, 2, 3, "fp32", S3, "unit", "cuda")
+    with pytest.raises(SpinGTPError) as e:
+        plan.backward(x1, x2, g)
+    assert e.value.status == 2  # SPINGTP_ERR_UNSUPPORTED
