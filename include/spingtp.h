@@ -128,8 +128,9 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  * (family 3) of L = max(L1, L2, Lout): x1 and x2 are padded with zeros to degree
  * L as the kernel stages them and the degree-L product is stored up to Lout,
  * which is exact since that kernel's grid integrates degree 3 L >= L1 + L2 + Lout
- * (forward and spingtp_forward_v1; spingtp_backward of such a plan gives
- * SPINGTP_ERR_UNSUPPORTED).  A shape that only the precontracted kernel of
+ * (forward, spingtp_forward_v1 and the gradients of spingtp_backward and
+ * spingtp_backward_v1, the degree-L ones of the padded functions, truncated).
+ * A shape that only the precontracted kernel of
  * spingtp_forward_v1 covers gives a plan for that entry point, and
  * spingtp_forward and spingtp_plan_kernel_info then return
  * SPINGTP_ERR_UNSUPPORTED.

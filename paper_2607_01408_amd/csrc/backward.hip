@@ -51,13 +51,13 @@ extern "C" spingtp_status spingtp_backward(spingtp_plan plan, const void* x1, co
     if (grad_x1 != nullptr) {
         const spingtp_status r =
             spingtp::run_forward(plan, plan->kernel, grad_out, x2, grad_x1, N, C, false, stream, plan->d_tab_bwd,
-                                 true);
+                                 true, plan->deg_bwd(1));
         if (r != SPINGTP_OK) return r;
     }
     if (grad_x2 != nullptr) {
         const spingtp_status r =
             spingtp::run_forward(plan, plan->kernel, grad_out, x1, grad_x2, N, C, false, stream, plan->d_tab_bwd,
-                                 true);
+                                 true, plan->deg_bwd(2));
         if (r != SPINGTP_OK) return r;
     }
     return SPINGTP_OK;
@@ -171,7 +171,8 @@ extern "C" spingtp_status spingtp_backward_v1(spingtp_plan plan, const void* x1,
                                      plan->d_pre_bwd);
         } else if (plan->d_tab_bwd != nullptr) {  // the Fourier kernel, x2 read once per edge
             const spingtp::KernelEntry* kf = (k != nullptr && k->family != 5) ? k : plan->kernel;
-            r = spingtp::run_forward(plan, kf, grad_out, x2, grad_x1, N, C, true, stream, plan->d_tab_bwd, true);
+            r = spingtp::run_forward(plan, kf, grad_out, x2, grad_x1, N, C, true, stream, plan->d_tab_bwd, true,
+                                     plan->deg_bwd(1));
         } else if (plan->d_dir_b1 != nullptr) {  // the direct kernel, x2 shared by the channels
             r = spingtp::run_forward(plan, plan->kernel_dir, grad_out, x2, grad_x1, N, C, true, stream, nullptr,
                                      false, plan->d_dir_b1);
@@ -185,7 +186,7 @@ extern "C" spingtp_status spingtp_backward_v1(spingtp_plan plan, const void* x1,
         const spingtp_status r =
             plan->d_tab_bwd != nullptr
                 ? spingtp::run_forward(plan, plan->kernel, grad_out, x1, workspace, N, C, false, stream,
-                                       plan->d_tab_bwd, true)
+                                       plan->d_tab_bwd, true, plan->deg_bwd(2))
                 : spingtp::run_forward(plan, plan->kernel_dir, grad_out, x1, workspace, N, C, false, stream,
                                        nullptr, false, plan->d_dir_b2);
         if (r != SPINGTP_OK) return r;

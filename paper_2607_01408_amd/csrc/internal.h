@@ -270,6 +270,10 @@ struct spingtp_plan_s {
     uint32_t* d_uvw;
     size_t uvw_off[3];
     int uvw_blocks[3], uvw_max_d3[3], uvw_paths;
+    // mixed degrees on the large-degree kernel of the largest degree: d_aux holds the
+    // degree triples of the forward, the grad_x1 and the grad_x2 launches
+    bool padded;
+    const uint32_t* deg_bwd(int which) const { return padded ? d_aux + 3 * which : nullptr; }
     const spingtp::KernelEntry* kernel;     // spingtp_forward
     const spingtp::KernelEntry* kernel_v1;  // spingtp_forward_v1 (x2 shared by the channels of an edge)
 };

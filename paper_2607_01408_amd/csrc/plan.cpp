@@ -1265,6 +1265,7 @@ struct PlanHost {
     std::vector<double> tab, tab_bwd;
     std::vector<uint32_t> aux, pre, pre_bwd, dir, dir_b1, dir_b2, pre_w, bw1w, uvw;
     size_t uvw_off[3] = {0, 0, 0};  // first word of each role's table in uvw
+    bool padded = false;            // mixed degrees on the large-degree kernel (aux: 3 degree triples)
     spingtp::Bw1wShape bw1w_shape{};
     bool has_backward = false, same_bwd = false;
 };
@@ -1316,6 +1317,7 @@ spingtp_status build_plan_host(int L1, int L2, int Lout, const int* spins, int n
             L_pad = Lm;
         }
     }
+    h.padded = L_pad >= 0;
     const spingtp::KernelEntry* kv1 = nullptr;
     if ((flags & SPINGTP_V1_FOURIER) == 0) {
         kv1 = spingtp::find_pre_kernel(L1, L2, Lout, n_spins, static_cast<int>(dtype));
@@ -1344,7 +1346,16 @@ spingtp_status build_plan_host(int L1, int L2, int Lout, const int* spins, int n
     try {
         if (L_pad >= 0) {  // the tables of the padded degree, and the true degrees
             if (!spingtp::build_tables(L_pad, L_pad, L_pad, spin_mode, basis, tab)) return SPINGTP_ERR_INTERNAL;
-            aux = {static_cast<uint32_t>(L1), static_cast<uint32_t>(L2), static_cast<uint32_t>(Lout)};
+            // (x1, x2 -> out) of the forward, then the gradient launches' (grad_out, x2 -> grad_x1)
+            // and (grad_out, x1 -> grad_x2)
+            const uint32_t a = static_cast<uint32_t>(L1), b = static_cast<uint32_t>(L2),
+                           c = static_cast<uint32_t>(Lout);
+            aux = {a, b, c, c, b, a, c, a, b};
+            // the gradients: the degree-L ones of the padded functions, truncated
+            if (spingtp::build_tables(L_pad, L_pad, L_pad, spin_mode, basis, tab_bwd, true)) {
+                has_backward = true;
+                same_bwd = tab_bwd == tab;
+            }
         } else if (spin_mode < 2 && !weighted && !spingtp::build_tables(L1, L2, Lout, spin_mode, basis, tab)) {
             return SPINGTP_ERR_INTERNAL;
         }
@@ -1541,6 +1552,7 @@ static spingtp_status create_plan(int L1, int L2, int Lout, const int* spins, in
     p->uvw_paths = h.uvw.empty() ? 0 : static_cast<int>(h.uvw[0]);
     p->kernel = h.k;
     p->kernel_v1 = h.kv1;
+    p->padded = h.padded;
     *out_plan = p;
     return SPINGTP_OK;
 }

@@ -488,14 +488,52 @@ def test_mixed_large_degrees(L1, L2, LO, spins, basis, dtype):
     assert Plan(L1, L2, LO, spins, dtype, basis).kernel_info()["family"] == 3
 
 
-def test_mixed_large_degrees_v1_and_no_backward():
-    # the shared-x2 entry on the padded route; gradients of such shapes are not built
+def test_mixed_large_degrees_v1():
+    # the shared-x2 entry on the padded route
     fam, _ = run_v1(9, 3, 10, S3, 13, 5, "fp32", seed=11)
     assert fam == 3
-    plan = Plan(9, 3, 10, S3, "fp32")
-    x1 = workloads.draw(9, 4, 2, 1, "fp32", S3, "unit", "cuda")
-    x2 = workloads.draw(3, 4, 2, 2, "fp32", S3, "unit", "cuda")
-    g = workloads.draw(10, 4, 2, 3, "fp32", S3, "unit", "cuda")
-    with pytest.raises(SpinGTPError) as e:
-        plan.backward(x1, x2, g)
-    assert e.value.status == 2  # SPINGTP_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("L1,L2,LO,spins,basis,dtype", [
+    (9, 3, 10, S3, 0, "fp32"), (4, 12, 16, S3, 2, "fp32"), (12, 12, 6, S3, 1, "fp32"),
+    (16, 15, 14, (0,), 0, "fp32"), (12, 5, 9, S3, 0, "bf16"),
+])
+def test_mixed_large_degrees_backward(L1, L2, LO, spins, basis, dtype):
+    # the gradients: the degree-L ones of the padded functions (grad_out, x2 -> grad_x1
+    # and grad_out, x1 -> grad_x2 on the padded kernel), truncated
+    print(f"[mixed-bwd] L=({L1},{L2},{LO}) spins={spins} basis={basis} {dtype}", flush=True)
+    N, C = 11, 3
+    x1 = workloads.draw(L1, N, C, 500 + L1, dtype, spins, "unit", "cuda")
+    x2 = workloads.draw(L2, N, C, 510 + L2, dtype, spins, "unit", "cuda")
+    g = workloads.draw(LO, N, C, 520 + LO, dtype, spins, "unit", "cuda")
+    plan = Plan(L1, L2, LO, spins, dtype, basis)
+    gx1, gx2 = plan.backward(x1, x2, g)
+    torch.cuda.synchronize()
+    U = N * C
+    a, b, c = (t.view(U, -1).double().cpu().numpy() for t in (x1, x2, g))
+    r1, r2 = oracle.RealGauntTensor(L1, L2, LO, spins, basis).vjp(a, b, c)
+    e1 = rel_l2(gx1.view(U, -1).double().cpu().numpy(), r1)
+    e2 = rel_l2(gx2.view(U, -1).double().cpu().numpy(), r2)
+    print(f"[mixed-bwd]   rel_l2 {e1:.3e} {e2:.3e}", flush=True)
+    assert e1 <= TOL[dtype] and e2 <= TOL[dtype], (e1, e2)
+
+
+def test_mixed_large_degrees_backward_v1():
+    # x2 shared by the channels of an edge: grad_x2 summed over them
+    L1, L2, LO, N, C = 10, 4, 12, 7, 6
+    x1 = workloads.draw(L1, N, C, 530, "fp32", S3, "unit", "cuda")
+    x2 = workloads.draw(L2, N, 1, 531, "fp32", S3, "unit", "cuda")
+    g = workloads.draw(LO, N, C, 532, "fp32", S3, "unit", "cuda")
+    plan = Plan(L1, L2, LO, S3, "fp32")
+    gx1, gx2 = plan.backward_v1(x1, x2, g)
+    torch.cuda.synchronize()
+    U = N * C
+    a = x1.view(U, -1).double().cpu().numpy()
+    b = np.repeat(x2.view(N, -1).double().cpu().numpy(), C, axis=0)
+    c = g.view(U, -1).double().cpu().numpy()
+    r1, r2 = oracle.RealGauntTensor(L1, L2, LO, S3, 0).vjp(a, b, c)
+    r2 = r2.reshape(N, C, -1).sum(axis=1)
+    e1 = rel_l2(gx1.view(U, -1).double().cpu().numpy(), r1)
+    e2 = rel_l2(gx2.view(N, -1).double().cpu().numpy(), r2)
+    print(f"[mixed-bwd-v1]   rel_l2 {e1:.3e} {e2:.3e}", flush=True)
+    assert e1 <= TOL["fp32"] and e2 <= TOL["fp32"], (e1, e2)
