@@ -9,11 +9,13 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libspingtp.so")
-SOURCES = ["plan.cpp", "api.cpp", "forward.hip", "forward_big_parity.hip", "forward_mfma.hip", "forward_pre.hip",
+SOURCES = ["plan.cpp", "api.cpp", "forward.hip", "forward_big_parity.hip", "forward_big_padded.hip",
+           "forward_big_parity_padded.hip", "forward_mfma.hip", "forward_pre.hip",
            "forward_pre_large.hip", "forward_pre_weighted.hip", "forward_direct.hip", "backward.hip", "backward_v1w.hip", "forward_uvw.hip"]
 # per-source additions: the parity-basis large-degree kernels schedule for fewer registers
 # (they spill less and run 22-35 % faster that way; the other kernels run slower with it)
-EXTRA_FLAGS = {"forward_big_parity.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-minreg"]}
+_MINREG = ["-mllvm", "-amdgpu-sched-strategy=iterative-minreg"]
+EXTRA_FLAGS = {"forward_big_parity.hip": _MINREG, "forward_big_parity_padded.hip": _MINREG}
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in generated code.
 HIP_FLAGS = [

@@ -535,18 +535,21 @@ constexpr bool big_hoist_rows() {
 // (big_hoist_rows picks the degrees where the hoisted form fits).
 // TIO: float (fp32 I/O) or uint16_t (bf16 I/O: rows widened to fp32 as they are staged,
 // the output tile rounded to nearest even as it is stored; all arithmetic in fp32).
-// deg: nullptr, or the degrees (L1, L2, Lout) of a plan with mixed degrees, all <= L.
-// Such a product equals the degree-L one of the same functions (x1, x2 padded with
-// zeros above their degrees) truncated to Lout, since the degree-L grid is exact for
-// the products of degree <= 3 L >= L1 + L2 + Lout: the rows are staged with zeros above
-// L1 and L2 and the output tile is stored up to Lout.
-template <int L, bool SPIN, int W, bool BWD, bool PAR, typename TIO>
+// PAD: a plan with mixed degrees (L1, L2, Lout), all <= L, read from deg (ignored
+// otherwise).  Such a product equals the degree-L one of the same functions (x1, x2
+// padded with zeros above their degrees) truncated to Lout, since the degree-L grid is
+// exact for the products of degree <= 3 L >= L1 + L2 + Lout: the rows are staged with
+// zeros above L1 and L2 and the output tile is stored up to Lout.  A separate
+// instantiation: the run-time row strides and bounds cost the equal-degree kernels
+// registers (L = 16: 2 -> 147 spilled VGPRs).
+template <int L, bool SPIN, int W, bool BWD, bool PAR, typename TIO, bool PAD>
 __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_big_kernel(
     const TIO* __restrict__ x1, const TIO* __restrict__ x2, TIO* __restrict__ out, int64_t units, int64_t cpx2,
     const float* __restrict__ tab, const uint32_t* __restrict__ deg, int zero) {
     using B = BigShape<L, SPIN, W>;
     constexpr bool F32 = std::is_same<TIO, float>::value;
     static_assert(F32 || B::OUT_LDS, "bf16 I/O needs the output tile in LDS");
+    static_assert(!PAD || B::OUT_LDS, "mixed degrees need the output tile in LDS");
     using P = typename B::PS;
     constexpr Layout Y = B::Y;
     constexpr bool SPLIT = big_split_last<L, SPIN, PAR>();
@@ -568,9 +571,9 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     const int64_t row = u0 + (valid ? u : 0);  // invalid lanes compute on a valid row, store nothing
     const float* g = tab;
     // slots per spin block of the x1, x2 and output rows (their degrees' (l + 1)^2)
-    const int bb1 = deg ? static_cast<int>((deg[0] + 1) * (deg[0] + 1)) : B::BB;
-    const int bb2 = deg ? static_cast<int>((deg[1] + 1) * (deg[1] + 1)) : B::BB;
-    const int bbo = deg ? static_cast<int>((deg[2] + 1) * (deg[2] + 1)) : B::BB;
+    const int bb1 = PAD ? static_cast<int>((deg[0] + 1) * (deg[0] + 1)) : B::BB;
+    const int bb2 = PAD ? static_cast<int>((deg[1] + 1) * (deg[1] + 1)) : B::BB;
+    const int bbo = PAD ? static_cast<int>((deg[2] + 1) * (deg[2] + 1)) : B::BB;
     float* orow = nullptr;  // the output row in global memory (fp32 without the LDS tile)
     if constexpr (F32) orow = out + row * B::NC;
     // staging: TPR threads per input row (row r = lane r of every wave)
@@ -579,7 +582,9 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     const int sr = tid / TPR, sk = tid % TPR;
     const int64_t srow = u0 + ((sr >> 1) < nvalid ? (sr >> 1) : 0);
     const int sbb = (sr & 1) ? bb2 : bb1;  // this thread's row: slots per spin block
-    const TIO* ssrc = (sr & 1) ? x2 + (srow / cpx2) * (B::NS * bb2) : x1 + srow * (B::NS * bb1);
+    const TIO* ssrc;
+    if constexpr (PAD) ssrc = (sr & 1) ? x2 + (srow / cpx2) * (B::NS * bb2) : x1 + srow * (B::NS * bb1);
+    else ssrc = (sr & 1) ? x2 + (srow / cpx2) * B::NC : x1 + srow * B::NC;
 
     for (int i = tid; i < B::TRIG; i += B::THREADS) {
         const int sb = i / (B::NP * (L + 1));
@@ -636,8 +641,11 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
 #pragma unroll
                 for (int it = 0; it < IT; ++it) {
                     const int q = sk + it * TPR;
-                    if (it * TPR < CW)
+                    if (it * TPR >= CW) continue;
+                    if constexpr (PAD)
                         pre[b][it] = (q < CW && LA * LA + q < sbb) ? widen(rsrc[b * sbb + LA * LA + q]) : 0.f;
+                    else
+                        pre[b][it] = q < CW ? widen(rsrc[b * B::BB + LA * LA + q]) : 0.f;
                 }
         };
         auto chunk = [&](auto cc) {
@@ -721,7 +729,7 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
             parity_mix_rows<L>(YT, B::STO, nvalid, true, tid, B::THREADS);
             __syncthreads();
         }
-        if (deg == nullptr) {
+        if constexpr (!PAD) {
             store_tile<B::NC, B::STO>(out + u0 * B::NC, nvalid, YT, tid, B::THREADS);
         } else {  // slots of degree <= Lout of each spin block
             const int nco = B::NS * bbo;
@@ -739,15 +747,17 @@ __global__ __launch_bounds__((BigShape<L, SPIN, W>::THREADS)) void spingtp_fwd_b
     }
 }
 
-template <int L, bool SPIN, int W, bool BWD, bool PAR, typename TIO = float>
+// deg: the three degrees for PAD (launches of the mixed-degree plans), else unused.
+template <int L, bool SPIN, int W, bool BWD, bool PAR, typename TIO = float, bool PAD = false>
 hipError_t launch_big(const void* x1, const void* x2, void* out, int64_t units, int64_t cpx2, const float* tab,
                       const uint32_t* deg, hipStream_t stream) {
     using B = BigShape<L, SPIN, W>;
     const int64_t blocks = (units + B::UNITS - 1) / B::UNITS;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W, BWD, PAR, TIO>), dim3(static_cast<unsigned>(blocks)),
+    if (PAD && deg == nullptr) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((spingtp_fwd_big_kernel<L, SPIN, W, BWD, PAR, TIO, PAD>), dim3(static_cast<unsigned>(blocks)),
                        dim3(B::THREADS), 0, stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2),
-                       static_cast<TIO*>(out), units, cpx2, tab, deg, 0);
+                       static_cast<TIO*>(out), units, cpx2, tab, PAD ? deg : nullptr, 0);
     return hipGetLastError();
 }
 

@@ -77,6 +77,11 @@ const KernelEntry* find_kernel(int L1, int L2, int LO, int spin_mode, int dtype,
 // The parity-basis large-degree kernel of L1 = L2 = Lout = L (9..16, spins {-1, 0, +1},
 // dtype 0 fp32, 1 bf16 I/O; forward_big_parity.hip), nullptr otherwise.
 const KernelEntry* find_big_parity_kernel(int L, int dtype);
+// The mixed-degree (zero-padded) large-degree kernel of L = max(L1, L2, Lout), 9..16, for
+// spin mode 0 or 1 and dtype 0 / 1; its launches take the degree triple as `aux`
+// (forward_big_padded.hip, forward_big_parity_padded.hip).  nullptr otherwise.
+const KernelEntry* find_big_padded_kernel(int L, int spin_mode, int dtype, bool parity);
+const KernelEntry* find_big_parity_padded_kernel(int L, int dtype);
 const KernelEntry* find_mfma_kernel(int L1, int L2, int LO, int spin_mode, int dtype);
 // The precontracted kernel of spingtp_forward_v1 (x2 shared by the channels of an edge).
 const KernelEntry* find_pre_kernel(int L1, int L2, int LO, int n_spins, int dtype);

@@ -1312,6 +1312,8 @@ spingtp_status build_plan_host(int L1, int L2, int Lout, const int* spins, int n
         const int Lm = std::max(L1, std::max(L2, Lout));
         const spingtp::KernelEntry* kb =
             spingtp::find_kernel(Lm, Lm, Lm, spin_mode, static_cast<int>(dtype), parity_tiles);
+        if (kb != nullptr && kb->family == 3)
+            kb = spingtp::find_big_padded_kernel(Lm, spin_mode, static_cast<int>(dtype), parity_tiles);
         if (kb != nullptr && kb->family == 3) {
             k = kb;
             L_pad = Lm;
