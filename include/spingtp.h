@@ -313,9 +313,12 @@ spingtp_status spingtp_backward_weighted_workspace_size(spingtp_plan plan, int64
  *   [(L2+1)^2] of the plan's dtype, 16-byte aligned; weights: device fp32 [V][C][n_paths]
  *   (the slice of channel v is the weight layout of spingtp_forward_v1_weighted);
  *   V >= 1.
- * Runs the entry-list kernel of spingtp_forward_v1_weighted once per v, reading the
- * x2 rows V n_spins (L2+1)^2 elements apart and adding into out after the first
- * (bf16 outputs round at every add).  Needs a plan created with
+ * Runs the entry-list kernel of spingtp_forward_v1_weighted on groups of up to four
+ * channels v per launch (each tensor entry takes x1[k1] sum_v W_v[p] x2_v[k2]; as many
+ * channels as its LDS holds while two workgroups still fit a compute unit), reading
+ * the x2 rows of an edge V n_spins (L2+1)^2 elements apart and adding into out after
+ * the first launch (bf16 outputs round at every add).  V = 1 gives the results of
+ * spingtp_forward_v1_weighted bit for bit.  Needs a plan created with
  * SPINGTP_CHANNEL_WEIGHTS whose entry lists hold the shape, else
  * SPINGTP_ERR_UNSUPPORTED.  Asynchronous on `stream`, no allocation.
  */

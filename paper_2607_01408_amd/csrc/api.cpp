@@ -3,6 +3,7 @@
 // forward_mfma.hip and forward_pre*.hip.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "internal.h"
@@ -180,12 +181,23 @@ extern "C" spingtp_status spingtp_forward_depthwise(spingtp_plan plan, const voi
     if (cur != plan->device) return SPINGTP_ERR_INVALID_ARG;
     const int64_t n2 = plan->bw1w.nc2, elem = plan->dtype == SPINGTP_FP32 ? 4 : 2;
     const int64_t wslice = C * plan->bw1w.np;
-    for (int64_t v = 0; v < V; ++v) {  // out = sum over the second-input channels, in order
+    // up to kFwdCwMaxNv channels per launch, as many as the LDS holds without fewer
+    // workgroups per CU than one channel gets (at least two); later launches add
+    // into out, in channel order
+    const int lds1 = spingtp::fwd_cw_lds_floats(plan->bw1w, 1);
+    const int per_cu1 = std::min(2, spingtp::kBw1wMaxLdsFloats / std::max(lds1, 1));
+    int nv_max = 1;
+    while (nv_max < spingtp::kFwdCwMaxNv &&
+           spingtp::kBw1wMaxLdsFloats / spingtp::fwd_cw_lds_floats(plan->bw1w, nv_max + 1) >= per_cu1)
+        ++nv_max;
+    for (int64_t v = 0; v < V;) {
+        const int nv = static_cast<int>(std::min<int64_t>(nv_max, V - v));
         const hipError_t e = spingtp::launch_fwd_cw(
             plan->dtype == SPINGTP_FP32 ? 0 : 1, true, x1, static_cast<const char*>(x2) + v * n2 * elem,
             weights + v * wslice, out, N, C, plan->bw1w, plan->d_bw1w, static_cast<hipStream_t>(stream), V * n2,
-            v > 0);
+            v > 0, nv, n2, wslice);
         if (e != hipSuccess) return SPINGTP_ERR_HIP;
+        v += nv;
     }
     return SPINGTP_OK;
 }

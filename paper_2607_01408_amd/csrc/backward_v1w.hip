@@ -258,20 +258,27 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_bwd_v1w_kernel(
 // (the k3-ordered list), x2 per unit or (SHARED) one row per edge.  Same tiling as
 // the gradients: a 64-channel tile and a range of edges per workgroup, the weight
 // rows in LDS for the range, the four waves splitting the output slots.
-template <typename TIO, bool SHARED>
+// NV > 1 (SHARED only; the depthwise mode): NV second-input channels v of the edge
+// at once, out[n,c,k3] = sum_v sum over the entries of W_v[c,p] T x1[n,c,k1] x2_v[n,k2]
+// with the rows x2_v at x2 + n x2s + v x2v and the weight slices at wts + v wslice:
+// each entry takes x1[k1] * sum_v W_v[p] x2_v[k2], so x1 and the list are read once
+// for the NV channels and the output rows are stored once.
+template <typename TIO, bool SHARED, int NV>
 __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
     const TIO* __restrict__ x1, const TIO* __restrict__ x2, const float* __restrict__ wts, TIO* __restrict__ out,
-    int64_t N, int64_t C, int64_t epg, const uint32_t* __restrict__ tab, int64_t x2s, bool acc_out) {
+    int64_t N, int64_t C, int64_t epg, const uint32_t* __restrict__ tab, int64_t x2s, bool acc_out, int64_t x2v,
+    int64_t wslice) {
+    static_assert(NV >= 1 && (SHARED || NV == 1), "several second-input channels need the shared x2 form");
     extern __shared__ float lds[];
     const int nc1 = static_cast<int>(tab[0]), nc2 = static_cast<int>(tab[1]), nco = static_cast<int>(tab[2]);
     const int np = static_cast<int>(tab[3]);
     const uint32_t* __restrict__ seg3 = tab + tab[11];
     const uint32_t* __restrict__ list3 = tab + tab[12];
     const int stw = bw_stride(np), st1 = bw_stride(nc1), sto = bw_stride(nco), st2 = bw_stride(nc2);
-    float* Wt = lds;                       // [64][stw] weights of the tile's channels
-    float* X1 = Wt + kBw1wLanes * stw;     // [64][st1] x1 rows
-    float* O = X1 + kBw1wLanes * st1;      // [64][sto] output rows
-    float* X2 = O + kBw1wLanes * sto;      // [64][st2] x2 rows, or (SHARED) the edge's x2 row
+    float* Wt = lds;                          // [NV][64][stw] weights of the tile's channels
+    float* X1 = Wt + NV * kBw1wLanes * stw;   // [64][st1] x1 rows
+    float* O = X1 + kBw1wLanes * st1;         // [64][sto] output rows
+    float* X2 = O + kBw1wLanes * sto;         // [64][st2] x2 rows, or (SHARED) [NV][st2] the edge's x2 rows
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -283,13 +290,15 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
     const uint32_t* __restrict__ kr = tab + 31;
     const int kb = static_cast<int>(kr[wave]), ke = static_cast<int>(kr[wave + 1]);
 
-    const int total = kBw1wLanes * (stw + st1 + sto) + (SHARED ? st2 : kBw1wLanes * st2);
+    const int total = kBw1wLanes * (NV * stw + st1 + sto) + (SHARED ? NV * st2 : kBw1wLanes * st2);
     for (int i = tid; i < total; i += kBw1wThreads) lds[i] = 0.f;
     __syncthreads();
-    for (int e = tid; e < nch * np; e += kBw1wThreads) {
-        const int r = e / np;
-        Wt[r * stw + (e - r * np)] = wts[c0 * np + e];
-    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+        for (int e = tid; e < nch * np; e += kBw1wThreads) {
+            const int r = e / np;
+            Wt[(v * kBw1wLanes + r) * stw + (e - r * np)] = wts[v * wslice + c0 * np + e];
+        }
     const float* Wr = Wt + lane * stw;
     const float* X1r = X1 + lane * st1;
     const float* X2r = SHARED ? X2 : X2 + lane * st2;
@@ -300,14 +309,26 @@ __global__ __launch_bounds__(kBw1wThreads) void spingtp_fwd_cw_kernel(
         const int64_t row0 = n * C + c0;
         bw_load_rows(x1 + row0 * nc1, nch, nc1, st1, X1, tid);
         if constexpr (SHARED) {
-            for (int k = tid; k < nc2; k += kBw1wThreads) X2[k] = bw_load(x2 + n * x2s + k);
+#pragma unroll
+            for (int v = 0; v < NV; ++v)
+                for (int k = tid; k < nc2; k += kBw1wThreads) X2[v * st2 + k] = bw_load(x2 + n * x2s + v * x2v + k);
         } else {
             bw_load_rows(x2 + row0 * nc2, nch, nc2, st2, X2, tid);
         }
         __syncthreads();
-        bw_pass(seg3, list3, kb, ke, lane,
-                [&](uint32_t a, uint32_t b, uint32_t cc) { return Wr[a] * (X1r[b] * X2r[cc]); },
-                [&](int k3, float acc) { Or[k3] = acc; });
+        bw_pass(
+            seg3, list3, kb, ke, lane,
+            [&](uint32_t a, uint32_t b, uint32_t cc) {
+                if constexpr (NV == 1) {
+                    return Wr[a] * (X1r[b] * X2r[cc]);
+                } else {
+                    float w2 = Wr[a] * X2r[cc];
+#pragma unroll
+                    for (int v = 1; v < NV; ++v) w2 = fmaf(Wr[v * kBw1wLanes * stw + a], X2r[v * st2 + cc], w2);
+                    return X1r[b] * w2;
+                }
+            },
+            [&](int k3, float acc) { Or[k3] = acc; });
         __syncthreads();
         TIO* dst = out + row0 * nco;
         for (int e = tid; e < nch * nco; e += kBw1wThreads) {
@@ -468,10 +489,10 @@ hipError_t launch_bwd_v1w(int dtype, bool shared_x2, const void* x1, const void*
                                                accumulate_gx1);
 }
 
-template <typename TIO, bool SHARED>
+template <typename TIO, bool SHARED, int NV>
 static hipError_t launch_fwd_typed(const void* x1, const void* x2, const float* w, void* out, int64_t N, int64_t C,
                                    int lds_floats, const uint32_t* tab, hipStream_t stream, int64_t x2s,
-                                   bool acc_out) {
+                                   bool acc_out, int64_t x2v, int64_t wslice) {
     const int64_t tiles = (C + kBw1wLanes - 1) / kBw1wLanes;
     int64_t groups = 0, epg = 0;
     bw1w_groups(N, C, &groups, &epg, bw_target_groups(lds_floats));
@@ -479,32 +500,56 @@ static hipError_t launch_fwd_typed(const void* x1, const void* x2, const float* 
     if (groups > 0x7fffffff || tiles > 0xffff) return hipErrorInvalidValue;
     const size_t bytes = static_cast<size_t>(lds_floats) * sizeof(float);
     if (bytes > 65536) {
-        const hipError_t e = raise_lds_limit<TIO, SHARED ? 3 : 4>(
-            reinterpret_cast<const void*>(&spingtp_fwd_cw_kernel<TIO, SHARED>));
+        const hipError_t e = raise_lds_limit<TIO, SHARED ? 3 + 2 * (NV - 1) : 4>(
+            reinterpret_cast<const void*>(&spingtp_fwd_cw_kernel<TIO, SHARED, NV>));
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((spingtp_fwd_cw_kernel<TIO, SHARED>),
+    hipLaunchKernelGGL((spingtp_fwd_cw_kernel<TIO, SHARED, NV>),
                        dim3(static_cast<unsigned>(groups), static_cast<unsigned>(tiles)), dim3(kBw1wThreads), bytes,
                        stream, static_cast<const TIO*>(x1), static_cast<const TIO*>(x2), w, static_cast<TIO*>(out), N,
-                       C, epg, tab, x2s, acc_out);
+                       C, epg, tab, x2s, acc_out, x2v, wslice);
     return hipGetLastError();
+}
+
+template <typename TIO>
+static hipError_t launch_fwd_shared_nv(int nv, const void* x1, const void* x2, const float* w, void* out, int64_t N,
+                                       int64_t C, int lds, const uint32_t* tab, hipStream_t stream, int64_t x2s,
+                                       bool acc, int64_t x2v, int64_t wslice) {
+    switch (nv) {
+        case 1: return launch_fwd_typed<TIO, true, 1>(x1, x2, w, out, N, C, lds, tab, stream, x2s, acc, x2v, wslice);
+        case 2: return launch_fwd_typed<TIO, true, 2>(x1, x2, w, out, N, C, lds, tab, stream, x2s, acc, x2v, wslice);
+        case 3: return launch_fwd_typed<TIO, true, 3>(x1, x2, w, out, N, C, lds, tab, stream, x2s, acc, x2v, wslice);
+        case 4: return launch_fwd_typed<TIO, true, 4>(x1, x2, w, out, N, C, lds, tab, stream, x2s, acc, x2v, wslice);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+int fwd_cw_lds_floats(const Bw1wShape& s, int nv) {
+    return s.lds_shared_fwd + (nv - 1) * (kBw1wLanes * bw_stride(s.np) + bw_stride(s.nc2));
 }
 
 hipError_t launch_fwd_cw(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, void* out,
                          int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab, hipStream_t stream,
-                         int64_t x2_stride, bool accumulate) {
+                         int64_t x2_stride, bool accumulate, int nv, int64_t x2v, int64_t wslice) {
     const int64_t x2s = x2_stride > 0 ? x2_stride : s.nc2;
     // the kernel carves its LDS from the table's sizes
     const int base = kBw1wLanes * (bw_stride(s.np) + bw_stride(s.nc1) + bw_stride(s.nco));
-    const int lds = shared_x2 ? s.lds_shared_fwd : s.lds_unit_fwd;
-    if (lds <= 0 || lds > kBw1wMaxLdsFloats ||
-        lds != base + (shared_x2 ? bw_stride(s.nc2) : kBw1wLanes * bw_stride(s.nc2)))
+    const int lds1 = shared_x2 ? s.lds_shared_fwd : s.lds_unit_fwd;
+    if (lds1 <= 0 || lds1 > kBw1wMaxLdsFloats ||
+        lds1 != base + (shared_x2 ? bw_stride(s.nc2) : kBw1wLanes * bw_stride(s.nc2)))
         return hipErrorInvalidValue;
-    if (shared_x2)
-        return dtype == 0 ? launch_fwd_typed<float, true>(x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate)
-                          : launch_fwd_typed<uint16_t, true>(x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate);
-    return dtype == 0 ? launch_fwd_typed<float, false>(x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate)
-                      : launch_fwd_typed<uint16_t, false>(x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate);
+    if (nv < 1 || nv > kFwdCwMaxNv || (nv > 1 && !shared_x2)) return hipErrorInvalidValue;
+    if (shared_x2) {
+        const int lds = fwd_cw_lds_floats(s, nv);
+        if (lds > kBw1wMaxLdsFloats) return hipErrorInvalidValue;
+        return dtype == 0
+                   ? launch_fwd_shared_nv<float>(nv, x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate, x2v, wslice)
+                   : launch_fwd_shared_nv<uint16_t>(nv, x1, x2, w, out, N, C, lds, tab, stream, x2s, accumulate, x2v,
+                                                    wslice);
+    }
+    return dtype == 0
+               ? launch_fwd_typed<float, false, 1>(x1, x2, w, out, N, C, lds1, tab, stream, x2s, accumulate, 0, 0)
+               : launch_fwd_typed<uint16_t, false, 1>(x1, x2, w, out, N, C, lds1, tab, stream, x2s, accumulate, 0, 0);
 }
 
 }  // namespace spingtp

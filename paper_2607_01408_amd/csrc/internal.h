@@ -192,9 +192,15 @@ hipError_t launch_bwd_v1w(int dtype, bool shared_x2, const void* x1, const void*
 // out[n][c] = sum_p W[c][p] T_p(x1[n][c], x2[n][c]) (spingtp_forward_weighted), or with
 // x2[n] shared by the channels (shared_x2, spingtp_forward_v1_weighted).
 // x2_stride, accumulate: as for launch_bwd_v1w (accumulate adds to out).
+// nv > 1 (shared_x2 only): nv second-input channels in one launch (the depthwise mode),
+// their x2 rows x2v elements apart within an edge's row and their weight slices
+// wslice floats apart; the LDS that takes is fwd_cw_lds_floats(s, nv).
+constexpr int kFwdCwMaxNv = 4;
 hipError_t launch_fwd_cw(int dtype, bool shared_x2, const void* x1, const void* x2, const float* w, void* out,
                          int64_t N, int64_t C, const Bw1wShape& s, const uint32_t* tab, hipStream_t stream,
-                         int64_t x2_stride = 0, bool accumulate = false);
+                         int64_t x2_stride = 0, bool accumulate = false, int nv = 1, int64_t x2v = 0,
+                         int64_t wslice = 0);
+int fwd_cw_lds_floats(const Bw1wShape& s, int nv);
 
 // Paths of the instruction-weighted product (spingtp_paths_host): the block triples
 // (i (L+1) + l of spin index i and degree l, per input and output) on which T has

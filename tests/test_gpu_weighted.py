@@ -452,8 +452,9 @@ def run_depthwise(L1, L2, LO, spins, N, C, V, basis=0, dtype="fp32", seed=0):
     return plan, (x1, x2, W, g), (y, gx1, gx2, gW)
 
 
+# V = 2..4 run as one launch of the fused kernel, V = 5, 6 as four channels and then the rest
 @pytest.mark.parametrize("shape,C,V,basis", [((1, 1, 1), 16, 3, 0), ((2, 2, 2), 70, 2, 2), ((1, 3, 3), 33, 4, 0),
-                                             ((2, 1, 2), 64, 2, 1)])
+                                             ((2, 1, 2), 64, 2, 1), ((2, 2, 2), 40, 6, 0), ((1, 2, 2), 24, 5, 2)])
 def test_depthwise_shapes(shape, C, V, basis):
     run_depthwise(*shape, S3, 11, C, V, basis, seed=C + V)
 
