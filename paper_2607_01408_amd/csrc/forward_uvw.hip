@@ -72,12 +72,8 @@ __global__ __launch_bounds__(kThreads) void spingtp_fill_zero_kernel(float* __re
 // R of pair pr (< A B) at edge n (< N) for the components j < mc of one path record:
 // r[j] = sum over the record's entries of component m0 + j of T a[ka] b[kb].
 template <int CH>
-__device__ __forceinline__ void form_r(const float* __restrict__ xa, const float* __restrict__ xb, int64_t n, int pr,
-                                       int A, int B, int nca, int ncb, const uint32_t* __restrict__ csr,
-                                       const uint32_t* __restrict__ ent, int mc, float (&r)[CH]) {
-    const int a = pr / B, b = pr - a * B;
-    const float* __restrict__ ra = xa + (n * A + a) * nca;
-    const float* __restrict__ rb = xb + (n * B + b) * ncb;
+__device__ __forceinline__ void form_r_rows(const float* ra, const float* rb, const uint32_t* __restrict__ csr,
+                                            const uint32_t* __restrict__ ent, int mc, float (&r)[CH]) {
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
         if (j < mc) {
@@ -88,6 +84,59 @@ __device__ __forceinline__ void form_r(const float* __restrict__ xa, const float
             }
             r[j] = s;
         }
+    }
+}
+
+template <int CH>
+__device__ __forceinline__ void form_r(const float* __restrict__ xa, const float* __restrict__ xb, int64_t n, int pr,
+                                       int A, int B, int nca, int ncb, const uint32_t* __restrict__ csr,
+                                       const uint32_t* __restrict__ ent, int mc, float (&r)[CH]) {
+    const int a = pr / B, b = pr - a * B;
+    form_r_rows(xa + (n * A + a) * nca, xb + (n * B + b) * ncb, csr, ent, mc, r);
+}
+
+// Staging of a path's input blocks in LDS for R.  The pairs c0 .. c0 + 31 take the a rows
+// a_lo .. a_lo + n_a - 1 (a_lo = c0 / B) and the b rows (b0 + i) mod B, i < n_b (b0 = c0 mod
+// B, n_b = min(B, 32)); n_a + n_b <= 34 for every B.  Blocks up to kStageD wide (degree 3)
+// are staged: XS[e][row][k] with rows 0 .. n_a - 1 the a rows and n_a .. the b rows, an odd
+// edge stride (the lanes of a wave take consecutive edges).  Each value then comes from
+// HBM once per tile instead of once per tensor entry that reads it.
+constexpr int kStageD = 7;
+constexpr int kStageRows = 34;
+constexpr int kStageEdge = kStageRows * kStageD + 1;
+constexpr int kStageFloats = kEdges * kStageEdge;
+
+struct StageRows {
+    int a_lo, n_a, b0, n_b;
+};
+
+__device__ __forceinline__ StageRows stage_rows(int c0, int AB, int B) {
+    const int last = (c0 + kPairs < AB ? c0 + kPairs : AB) - 1;
+    StageRows s;
+    s.a_lo = c0 / B;
+    s.n_a = last / B - s.a_lo + 1;
+    s.b0 = c0 - s.a_lo * B;
+    s.n_b = B < kPairs ? B : kPairs;
+    return s;
+}
+
+// rows of the tile's edges e0 .. e0 + 31 (zeros past N): a block [oa, oa + da) of xa,
+// b block [ob, ob + db) of xb
+__device__ __forceinline__ void stage_blocks(const float* __restrict__ xa, const float* __restrict__ xb, int64_t e0,
+                                             int64_t N, int A, int B, int nca, int ncb, int oa, int da, int ob,
+                                             int db, const StageRows& sr, float* XS, int tid) {
+    const int pa = sr.n_a * da, pb = sr.n_b * db;
+    for (int it = tid; it < kEdges * pa; it += kThreads) {
+        const int e = it / pa, rem = it - e * pa, row = rem / da, k = rem - row * da;
+        const int64_t n = e0 + e;
+        XS[e * kStageEdge + row * kStageD + k] = n < N ? xa[(n * A + sr.a_lo + row) * nca + oa + k] : 0.f;
+    }
+    for (int it = tid; it < kEdges * pb; it += kThreads) {
+        const int e = it / pb, rem = it - e * pb, row = rem / db, k = rem - row * db;
+        const int64_t n = e0 + e;
+        int b = sr.b0 + row;
+        if (b >= B) b -= B;
+        XS[e * kStageEdge + (sr.n_a + row) * kStageD + k] = n < N ? xb[(n * B + b) * ncb + ob + k] : 0.f;
     }
 }
 
@@ -192,6 +241,7 @@ __global__ __launch_bounds__(kThreads) void spingtp_uvw_grad_w_kernel(const floa
                                                                       int W, const uint32_t* __restrict__ tab,
                                                                       int nco) {
     __shared__ float R[kUvwChunk * kEdges * kPairsPad];
+    __shared__ float XS[kStageFloats];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -205,35 +255,63 @@ __global__ __launch_bounds__(kThreads) void spingtp_uvw_grad_w_kernel(const floa
     const int wbase = static_cast<int>(blockIdx.z) * kGroupW + 32 * wave;
     const int w_lane = wbase + (lane & 31);
 
+    // the path's x1 and x2 blocks; staged in LDS per edge tile when both fit and one has
+    // degree 2 or more (with blocks of three slots or fewer the direct reads measured faster)
+    const int oa = static_cast<int>(rec[3] & 0xffffu), da = static_cast<int>(rec[3] >> 16);
+    const int ob = static_cast<int>(rec[4] & 0xffffu), db = static_cast<int>(rec[4] >> 16);
+    const bool staged = da <= kStageD && db <= kStageD && (da > 3 || db > 3);
+    const StageRows sr = stage_rows(c0, UV, V);
+
     v16f acc = v16f{};
     for (int64_t e0 = 0; e0 < N; e0 += kEdges) {
+        if (staged) {
+            stage_blocks(x1, x2, e0, N, U, V, nc1, nc2, oa, da, ob, db, sr, XS, tid);
+            __syncthreads();
+        }
         for (int m0 = 0; m0 < d3; m0 += kUvwChunk) {
             const int mc = d3 - m0 < kUvwChunk ? d3 - m0 : kUvwChunk;
             const uint32_t* csr = tab + rec[2] + m0;
             // (1) R[component][edge][pair] of the tile
             for (int it = tid; it < kPairs * kEdges; it += kThreads) {
-                const int pl = it & 31, e = it >> 5;
+                const int pl = it >> 5, e = it & 31;
                 const int pr = c0 + pl;
                 const int64_t n = e0 + e;
                 float r[kUvwChunk];
 #pragma unroll
                 for (int j = 0; j < kUvwChunk; ++j) r[j] = 0.f;
-                if (pr < UV && n < N) form_r(x1, x2, n, pr, U, V, nc1, nc2, csr, ent, mc, r);
+                if (pr < UV && n < N) {
+                    if (staged) {
+                        const int a = pr / V, b = pr - a * V;
+                        const int ai = a - sr.a_lo, bi = b >= sr.b0 ? b - sr.b0 : b - sr.b0 + V;
+                        const float* xs = XS + e * kStageEdge;
+                        form_r_rows(xs + ai * kStageD - oa, xs + (sr.n_a + bi) * kStageD - ob, csr, ent, mc, r);
+                    } else {
+                        form_r(x1, x2, n, pr, U, V, nc1, nc2, csr, ent, mc, r);
+                    }
+                }
 #pragma unroll
                 for (int j = 0; j < kUvwChunk; ++j) R[(j * kEdges + e) * kPairsPad + pl] = r[j];
             }
             __syncthreads();
-            // (2) grad_W[pair, w] += R[pair, (edge, m3)] g[edge, w, o3 + m3], edges 2 s + half
+            // (2) grad_W[pair, w] += R[pair, (edge, m3)] g[edge, w, o3 + m3], edges 2 s + half.
+            //     Per edge a lane loads the chunk's components of its (edge, w) row of g
+            //     together (adjacent words: the later ones hit the cache the first one
+            //     filled), then runs the chunk's products with them.
             if (wbase < W) {
-                for (int j = 0; j < mc; ++j) {
-#pragma unroll 4
-                    for (int s2 = 0; s2 < kEdges; s2 += 2) {
-                        const int e = s2 + half;
-                        const int64_t n = e0 + e;
-                        const float av = R[(j * kEdges + e) * kPairsPad + (lane & 31)];
-                        const float bv = (n < N && w_lane < W) ? g[(n * W + w_lane) * nco + o3 + m0 + j] : 0.f;
-                        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
-                    }
+#pragma unroll 2
+                for (int s2 = 0; s2 < kEdges; s2 += 2) {
+                    const int e = s2 + half;
+                    const int64_t n = e0 + e;
+                    const bool ok = n < N && w_lane < W;
+                    const float* __restrict__ gr = g + (ok ? (n * W + w_lane) * nco + o3 + m0 : 0);
+                    float bv[kUvwChunk];
+#pragma unroll
+                    for (int j = 0; j < kUvwChunk; ++j) bv[j] = (ok && j < mc) ? gr[j] : 0.f;
+#pragma unroll
+                    for (int j = 0; j < kUvwChunk; ++j)
+                        if (j < mc)
+                            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(R[(j * kEdges + e) * kPairsPad + (lane & 31)],
+                                                                       bv[j], acc, 0, 0, 0);
                 }
             }
             __syncthreads();
