@@ -479,9 +479,12 @@ def test_v1_argument_checks():
 # --- mixed degrees beyond the direct kernel's rows: the large-degree kernel of the
 # largest degree, inputs padded with zeros as it stages them, the product truncated ---
 
+# the padded instantiations of every degree 9..16 (each its own kernel), both bases, spin {0}, bf16
 @pytest.mark.parametrize("L1,L2,LO,spins,basis,dtype", [
     (9, 3, 10, S3, 0, "fp32"), (12, 12, 6, S3, 0, "fp32"), (16, 2, 16, S3, 0, "fp32"), (4, 12, 16, S3, 2, "fp32"),
     (16, 15, 14, (0,), 0, "fp32"), (12, 5, 9, S3, 0, "bf16"), (3, 10, 12, S3, 1, "fp32"),
+    (9, 9, 4, S3, 2, "bf16"), (11, 4, 9, S3, 0, "fp32"), (5, 13, 13, S3, 2, "fp32"), (14, 3, 12, S3, 1, "bf16"),
+    (15, 6, 15, (0,), 0, "fp32"), (13, 2, 15, S3, 0, "fp32"),
 ])
 def test_mixed_large_degrees(L1, L2, LO, spins, basis, dtype):
     run_and_compare(L1, L2, LO, spins, 37, 3, dtype, basis, seed=400 + L1 + L2 + LO)
@@ -497,6 +500,7 @@ def test_mixed_large_degrees_v1():
 @pytest.mark.parametrize("L1,L2,LO,spins,basis,dtype", [
     (9, 3, 10, S3, 0, "fp32"), (4, 12, 16, S3, 2, "fp32"), (12, 12, 6, S3, 1, "fp32"),
     (16, 15, 14, (0,), 0, "fp32"), (12, 5, 9, S3, 0, "bf16"),
+    (9, 4, 9, S3, 1, "fp32"), (11, 11, 5, S3, 0, "fp32"), (13, 8, 14, S3, 2, "bf16"), (15, 6, 15, (0,), 0, "fp32"),
 ])
 def test_mixed_large_degrees_backward(L1, L2, LO, spins, basis, dtype):
     # the gradients: the degree-L ones of the padded functions (grad_out, x2 -> grad_x1
