@@ -108,7 +108,7 @@ def roofline(family, L, dtype, units, avg_ms, bytes_unit, direct_flops=None, spi
 
     hbm: algorithmic bytes (x1 + x2 + out) at 8 TB/s; valu: the route's vector-ALU flops (all
     steps on the vector kernels, steps A, C, E on the matrix-core kernel) at the non-packed
-    78.6 TF this build can reach; mfma: the matrix-core work as executed (split products and
+    78.6 TF (the library is compiled without packed fp32 instructions); mfma: the matrix-core work as executed (split products and
     padding) at the dense fp16 peak.  bound = the largest floor; frac = floor / measured."""
     t = avg_ms / 1e3
     steps = route_steps(L, L, L, spin)
@@ -184,7 +184,7 @@ def measured_traffic(workload, dtype, units, L, kname, valu=False, basis="paper"
 
 
 def cpu_workers_available():
-    """Host cores this process may use, capped at one GPU's share of the box (16)."""
+    """Host cores this process may use, capped at one GPU's share of a shared host (16)."""
     return max(1, min(16, len(os.sched_getaffinity(0))))
 
 
