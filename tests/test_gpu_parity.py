@@ -247,6 +247,33 @@ def test_full_size_sampled(name, dtype, L):
     check_matrix_core(plan, dtype, err)
 
 
+# Tensors of more than 2^31 fp32 elements (element offsets past the int32 range) on the
+# matrix-core kernel (L = 6) and the large-degree kernel (L = 12); the last 512 units sit
+# past that offset.  About 27 and 26 GB of device memory.
+@pytest.mark.parametrize("L,N,C", [(6, 115_000, 128), (12, 33_600, 128)])
+def test_beyond_2g_elements(L, N, C):
+    U = N * C
+    assert U * 3 * (L + 1) ** 2 > 2 ** 31
+    print(f"[parity] beyond 2^31 elements L={L} units={U}", flush=True)
+    x1, x2, m = workloads.make_pair("sweep", dtype="fp32", L=L, device="cuda", N=N, C=C)
+    plan = Plan(L, L, L, S3, "fp32")
+    y = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    idx = sample_units(U, 2048, 7)
+    ti = torch.as_tensor(idx, device="cuda")
+    a = x1.view(U, -1)[ti].double().cpu().numpy()
+    b = x2.view(U, -1)[ti].double().cpu().numpy()
+    g = y.view(U, -1)[ti].double().cpu().numpy()
+    del x1, x2, y
+    torch.cuda.empty_cache()
+    ref = oracle.spingtp(a, b, L, L, L, S3).reshape(len(idx), -1)
+    err = rel_l2(g, ref)
+    tail = rel_l2(g[-512:], ref[-512:])
+    print(f"[parity]   rel_l2={err:.3e} (last 512 units {tail:.3e}) family={plan.kernel_info()['family']}",
+          flush=True)
+    assert err <= TOL["fp32"] and tail <= TOL["fp32"]
+
+
 def test_empty_is_noop():
     plan = Plan(2, 2, 2, S3, "fp32")
     x = torch.zeros((0, 4, 3, 9), device="cuda")
