@@ -518,9 +518,12 @@ def test_mixed_large_degrees(L1, L2, LO, spins, basis, dtype):
     assert Plan(L1, L2, LO, spins, dtype, basis).kernel_info()["family"] == 3
 
 
-def test_mixed_large_degrees_v1():
+@pytest.mark.parametrize("L1,L2,LO,spins,basis,dtype", [
+    (9, 3, 10, S3, 0, "fp32"), (13, 5, 11, S3, 2, "bf16"), (6, 15, 15, (0,), 0, "fp32"), (14, 4, 10, S3, 1, "fp32"),
+])
+def test_mixed_large_degrees_v1(L1, L2, LO, spins, basis, dtype):
     # the shared-x2 entry on the padded route
-    fam, _ = run_v1(9, 3, 10, S3, 13, 5, "fp32", seed=11)
+    fam, _ = run_v1(L1, L2, LO, spins, 13, 5, dtype, seed=11 + L1, basis=basis)
     assert fam == 3
 
 
