@@ -518,6 +518,29 @@ def test_mixed_large_degrees(L1, L2, LO, spins, basis, dtype):
     assert Plan(L1, L2, LO, spins, dtype, basis).kernel_info()["family"] == 3
 
 
+@pytest.mark.parametrize("L1,L2,LO,dtype", [(13, 5, 11, "fp32"), (4, 16, 9, "bf16")])
+def test_mixed_large_degrees_many_tiles(L1, L2, LO, dtype):
+    # 20,000 units (625 tiles of 32), x1 and x2 rows of different lengths; sampled
+    N, C = 2000, 10
+    U = N * C
+    print(f"[parity] mixed many tiles L=({L1},{L2},{LO}) {dtype} units={U}", flush=True)
+    x1 = workloads.draw(L1, N, C, 610 + L1, dtype, S3, "unit", "cuda")
+    x2 = workloads.draw(L2, N, C, 620 + L2, dtype, S3, "unit", "cuda")
+    plan = Plan(L1, L2, LO, S3, dtype)
+    assert plan.kernel_info()["family"] == 3
+    y = plan.forward(x1, x2)
+    torch.cuda.synchronize()
+    idx = sample_units(U, 1024, 5)
+    ti = torch.as_tensor(idx, device="cuda")
+    a = x1.view(U, -1)[ti].double().cpu().numpy()
+    b = x2.view(U, -1)[ti].double().cpu().numpy()
+    g = y.view(U, -1)[ti].double().cpu().numpy()
+    ref = oracle.spingtp(a, b, L1, L2, LO, S3).reshape(len(idx), -1)
+    err = rel_l2(g, ref)
+    print(f"[parity]   rel_l2={err:.3e} over {len(idx)} units", flush=True)
+    assert err <= TOL[dtype]
+
+
 @pytest.mark.parametrize("L1,L2,LO,spins,basis,dtype", [
     (9, 3, 10, S3, 0, "fp32"), (13, 5, 11, S3, 2, "bf16"), (6, 15, 15, (0,), 0, "fp32"), (14, 4, 10, S3, 1, "fp32"),
 ])
