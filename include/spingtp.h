@@ -81,7 +81,7 @@ typedef enum { SPINGTP_FP32 = 0, SPINGTP_BF16 = 1 } spingtp_dtype;
  * precontracted kernel (family 5 below) is the default; SPINGTP_V1_PRECONTRACT
  * takes the precontracted kernel wherever it is built (SPINGTP_ERR_UNSUPPORTED
  * where it is not).  Without either, the precontracted kernel is used for row
- * lengths n_spins (L+1)^2 <= 112 in L1 and Lout (degree <= 5 with spins
+ * lengths n_spins (L+1)^2 <= 75 in L1 and Lout (degree <= 4 with spins
  * {-1, 0, +1}, where it is the faster route) and for shapes with no
  * Fourier-route kernel. */
 #define SPINGTP_V1_FOURIER 0x200u

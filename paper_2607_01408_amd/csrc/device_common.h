@@ -134,17 +134,97 @@ __device__ __forceinline__ void load_two_full_tiles(const uint16_t* __restrict__
     }
 }
 
+// One full tile (UNITS rows), every 16-byte load of the thread issued before the first
+// LDS write (load_two_full_tiles for a single input).
+template <int NC, int ST, int UNITS, int NTHR>
+__device__ __forceinline__ void load_full_tile(const float* __restrict__ a, float* da, int tid) {
+    static_assert((UNITS * NC) % 4 == 0, "whole 16-byte chunks");
+    constexpr int N4 = UNITS * NC / 4;
+    constexpr int IT = (N4 + NTHR - 1) / NTHR;
+    const v4f* a4 = reinterpret_cast<const v4f*>(a);
+    v4f ra[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        const int i = tid + it * NTHR;
+        if (it < IT - 1 || i < N4) ra[it] = __builtin_nontemporal_load(a4 + i);
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        const int i = tid + it * NTHR;
+        if (it < IT - 1 || i < N4) {
+            const int e = 4 * i;
+            put<NC, ST>(da, e, ra[it].x);
+            put<NC, ST>(da, e + 1, ra[it].y);
+            put<NC, ST>(da, e + 2, ra[it].z);
+            put<NC, ST>(da, e + 3, ra[it].w);
+        }
+    }
+}
+
+template <int NC, int ST, int UNITS, int NTHR>
+__device__ __forceinline__ void load_full_tile(const uint16_t* __restrict__ a, float* da, int tid) {
+    static_assert((UNITS * NC) % 8 == 0, "whole 16-byte chunks");
+    constexpr int N8 = UNITS * NC / 8;
+    constexpr int IT = (N8 + NTHR - 1) / NTHR;
+    const v4u* a8 = reinterpret_cast<const v4u*>(a);
+    v4u ra[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        const int i = tid + it * NTHR;
+        if (it < IT - 1 || i < N8) ra[it] = __builtin_nontemporal_load(a8 + i);
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        const int i = tid + it * NTHR;
+        if (it < IT - 1 || i < N8) {
+            const int e = 8 * i;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                put<NC, ST>(da, e + 2 * q, __uint_as_float(ra[it][q] << 16));
+                put<NC, ST>(da, e + 2 * q + 1, __uint_as_float(ra[it][q] & 0xffff0000u));
+            }
+        }
+    }
+}
+
 // Tile of an input shared by groups of cpx consecutive units (edge multiplicity
-// one: unit u reads row u / cpx of src).  One wave per row, coalesced along the row.
+// one: unit u reads row u / cpx of src).  One wave per row, coalesced along the row;
+// a wave issues the loads of four rows before their LDS writes (rows past nvalid
+// repeat the last valid one and are not written), and the tile's first edge comes
+// from one division.
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
 
 template <int NC, int ST, typename TIO>
 __device__ __forceinline__ void load_tile_shared(const TIO* __restrict__ src, int64_t u0, int nvalid, int64_t cpx,
                                                  float* dst, int tid, int nthr) {
-    for (int r = tid >> 6; r < nvalid; r += nthr >> 6) {
-        const TIO* __restrict__ s = src + ((u0 + r) / cpx) * NC;
-        for (int c = tid & 63; c < NC; c += 64) dst[r * ST + c] = to_f32(s[c]);
+    constexpr int CI = (NC + 63) / 64;  // loads per row and lane
+    constexpr int RB = 4;               // rows in flight per wave
+    const int64_t n0 = u0 / cpx, r0 = u0 - n0 * cpx;  // the tile's first edge, its first channel
+    const int waves = nthr >> 6, lane = tid & 63;
+    for (int rb = tid >> 6; rb < nvalid; rb += RB * waves) {
+        float v[RB][CI];
+#pragma unroll
+        for (int i = 0; i < RB; ++i) {
+            const int r = rb + i * waves < nvalid ? rb + i * waves : nvalid - 1;
+            const TIO* __restrict__ s = src + (n0 + (r0 + r) / cpx) * NC;
+#pragma unroll
+            for (int j = 0; j < CI; ++j) {
+                const int c = lane + 64 * j;
+                v[i][j] = c < NC ? to_f32(s[c]) : 0.f;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < RB; ++i) {
+            const int r = rb + i * waves;
+            if (r < nvalid) {
+#pragma unroll
+                for (int j = 0; j < CI; ++j) {
+                    const int c = lane + 64 * j;
+                    if (c < NC) dst[r * ST + c] = v[i][j];
+                }
+            }
+        }
     }
 }
 

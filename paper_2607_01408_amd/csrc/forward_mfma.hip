@@ -310,7 +310,8 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
     if (cpx2 == 1) {
         load_two_tiles<NC, ST, S::UNITS, S::THREADS>(x1 + u0 * NC, x2 + u0 * NC, nvalid, lds, lds + S::X2, tid);
     } else {  // x2 shared by the cpx2 channels of an edge
-        load_tile<NC, ST>(x1 + u0 * NC, nvalid, lds, tid, S::THREADS);
+        if (nvalid == S::UNITS) load_full_tile<NC, ST, S::UNITS, S::THREADS>(x1 + u0 * NC, lds, tid);
+        else load_tile<NC, ST>(x1 + u0 * NC, nvalid, lds, tid, S::THREADS);
         load_tile_shared<NC, ST>(x2, u0, nvalid, cpx2, lds + S::X2, tid, S::THREADS);
     }
     for (int i = tid; i < (S::UNITS - nvalid) * ST; i += S::THREADS) {

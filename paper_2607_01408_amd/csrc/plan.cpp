@@ -1323,9 +1323,10 @@ spingtp_status build_plan_host(int L1, int L2, int Lout, const int* spins, int n
     const spingtp::KernelEntry* kv1 = nullptr;
     if ((flags & SPINGTP_V1_FOURIER) == 0) {
         kv1 = spingtp::find_pre_kernel(L1, L2, Lout, n_spins, static_cast<int>(dtype));
-        // measured crossover: with larger rows the Fourier route is faster
+        // measured crossover: with rows longer than 75 slots (degree 5 with spins {-1, 0, 1}:
+        // 0.54 against 0.66 ms at 8192 edges x 128 channels) the Fourier route is faster
         const int rows = n_spins * (std::max(L1, Lout) + 1) * (std::max(L1, Lout) + 1);
-        if (kv1 != nullptr && k != nullptr && k->family != 6 && rows > 112 && (flags & SPINGTP_V1_PRECONTRACT) == 0)
+        if (kv1 != nullptr && k != nullptr && k->family != 6 && rows > 75 && (flags & SPINGTP_V1_PRECONTRACT) == 0)
             kv1 = nullptr;
         if (kv1 == nullptr && (flags & SPINGTP_V1_PRECONTRACT)) return SPINGTP_ERR_UNSUPPORTED;
     }

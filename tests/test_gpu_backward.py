@@ -205,9 +205,9 @@ def run_backward_v1(L, spins, N, C, dtype="fp32", basis=0, seed=0, fourier=False
 @pytest.mark.parametrize("L", [1, 2, 3, 4, 5, 6])
 @pytest.mark.parametrize("basis", [0, 1, 2])
 def test_backward_v1_matches_oracle(L, basis):
-    # default route: precontracted up to L = 5, Fourier at L = 6
+    # default route: precontracted up to L = 4, Fourier at L = 5, 6
     fam, _ = run_backward_v1(L, S3, 13, 17, "fp32", basis, seed=L + 10 * basis)
-    assert (fam == 5) == (L <= 5)
+    assert (fam == 5) == (L <= 4)
 
 
 @pytest.mark.parametrize("L,C,fourier,precontract", [(3, 40, True, False), (4, 1, True, False),

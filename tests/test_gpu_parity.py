@@ -429,10 +429,10 @@ def test_v1_degree_5_and_6(shape, C, fourier):
     assert (fam == 5) == (not fourier)
 
 
-@pytest.mark.parametrize("shape,family", [((4, 4, 4), 5), ((1, 3, 3), 5), ((5, 5, 5), 5), ((6, 6, 6), 4),
+@pytest.mark.parametrize("shape,family", [((4, 4, 4), 5), ((1, 3, 3), 5), ((5, 5, 5), 4), ((6, 6, 6), 4),
                                           ((6, 2, 5), 5)])
 def test_v1_default_route(shape, family):
-    # precontracted for rows <= 112 and where no Fourier kernel exists, the Fourier route beyond
+    # precontracted for rows <= 75 and where no Fourier kernel exists, the Fourier route beyond
     assert Plan(*shape, S3, "fp32").kernel_info_v1()["family"] == family
 
 
