@@ -399,7 +399,15 @@ __global__ __launch_bounds__(MShape<L>::THREADS, 2) void spingtp_fwd_mfma_kernel
 
     const int h = lane >> 5;  // (A): input h + 1; (D)-(E): accumulator type
     const int T = S::UT == 2 ? (wave & 1) : 0;       // unit tile of this wave
-    const int ngrp = S::UT == 2 ? (wave >> 1) : wave;  // node group of this wave
+    // node group of this wave.  Where the nodes split evenly over the groups (L = 5, 6)
+    // the assignment rotates from one workgroup to the next (by blockIdx / 256), which
+    // measured 2-3 % faster (organic L = 6: fp32 8.41-8.53 against 8.68-8.78 ms, bf16
+    // 6.45 against 6.59, alternated on one GPU); where they do not (L = 4, 7, 8) it
+    // measured slower (catalyst +5 %, molecule +2 %) and is not applied.  Each group's
+    // nodes and the fixed order in which the groups' partial outputs are summed do not
+    // depend on the rotation, so the results are the same bit for bit.
+    constexpr int ROT = S::NT % S::NG == 0 ? 1 : 0;
+    const int ngrp = ((S::UT == 2 ? (wave >> 1) : wave) + ROT * static_cast<int>((blockIdx.x >> 8) % S::NG)) % S::NG;
     const float* xr = lds + (h ? S::X2 : 0) + (32 * T + (lane & 31)) * ST;
     const float sg = h ? -1.f : 1.f;
     const v4u* __restrict__ ops = reinterpret_cast<const v4u*>(aux);
